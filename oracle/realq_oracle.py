@@ -1,0 +1,363 @@
+"""REAL-Q per-layer quantization sweep, written out plainly in float64 on the CPU.
+
+TEST INFRASTRUCTURE ONLY.  This module is the oracle that the GPU library is
+checked against.  Only the tests, the smoke entry point and the benchmark's CPU
+baseline leg may import it; the product path never does.  It shares no code,
+table or constant generator with the HIP library.
+
+Notation (paper Sec. 3.1): a linear module has weights W in R^{m x n} (row = output
+channel); the calibration set gives per-token inputs x_t (rows of X, T x n).
+``Xhat`` holds the inputs the partially quantized model actually feeds this
+module (perturbed by already-quantized upstream layers); ``X`` holds the
+full-precision model's inputs, so the full-precision output is W0 x_t.
+
+What the sweep computes (Alg. 1 of Appendix A, restricted to one linear module,
+with the per-layer surrogate of the readings below):
+
+  1. Hessian of the layer-wise MSE, H = (2/T) sum_t s_t xhat_t xhat_t^T
+     (Sec. 3.2; per-token weights as in Eq. saliency_hessian with one row group).
+  2. Dead columns fixed, relative damping, and the upper-triangular inverse factor
+     U with (H + lambda I)^{-1} = U^T U, whose rows are GPTQ's sequentially
+     eliminated inverse (Sec. 3.2, Eq. gptq_update).
+  3. For each 128-column block: group scale/zero search, column-by-column
+     quantization with in-block OBS compensation (Eq. gptq_update), then the
+     trailing batch update with the block error E_b (Sec. 3.2).
+  4. After every block: Block-wise gradient descent (Sec. 4.3, Eq. block_gd_update)
+     on the trailing columns, with Adam (Appendix D.1), against the
+     Fisher-weighted MSE of the layer output (Sec. 4.2, Eq. fisher_loss) between the
+     partially quantized module fed Xhat and the full-precision module fed X.
+  5. The sliding window (Sec. 4.4, Eq. slide_window) blends this module's metric with
+     the pulled-back metric of its consumer.
+
+Readings where the paper is silent (each is listed in the design notes):
+  * quantizer: asymmetric, per (row, group of ``group`` columns), joint search
+    over ``grid`` shrink factors p_k = 1 - k/100 and all 2^bits zero points,
+    minimising squared error; ties broken by (err, k, |z - z_nat(k)|, z);
+    round-half-to-even; parameters fixed from the weights as they stand when the
+    group's first column is reached;
+  * damping: dead columns (H_jj == 0) get H_jj = 1 and their weights zeroed, then
+    lambda = damp * mean(diag H) is added to the diagonal;
+  * BGD uses all T tokens per step, ``steps`` Adam steps after every block except
+    the last, one Adam step counter per module;
+  * the surrogate is evaluated at the module output:
+        R = W Xhat^T - W0 X^T,   L = (1/2T) sum_t s_t R_t^T M R_t,
+        grad_W L = (1/T) M R diag(s) Xhat.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Tuple
+
+import numpy as np
+
+ADAM_BETA1 = 0.9      # Appendix D.1
+ADAM_BETA2 = 0.999    # Appendix D.1
+ADAM_EPS = 1e-8       # Appendix D.1
+
+
+# ============================================================================ step 1: Hessian
+
+def hessian(Xhat: np.ndarray, s: Optional[np.ndarray] = None) -> np.ndarray:
+    """H = (2/T) sum_t s_t xhat_t xhat_t^T  (Sec. 3.2 GPTQ recap; Eq. saliency_hessian with N_g = 1).
+
+    ``s = None`` means unit weights, the plain calibration Hessian of Sec. 3.2.
+    """
+    Xh = np.asarray(Xhat, dtype=np.float64)
+    T = Xh.shape[0]
+    if s is None:
+        A = Xh
+    else:
+        A = Xh * np.asarray(s, dtype=np.float64)[:, None]
+    return (2.0 / T) * (A.T @ Xh)
+
+
+# ============================================================================ step 2: damping + inverse factor
+
+def damp_hessian(H: np.ndarray, damp: float) -> Tuple[np.ndarray, np.ndarray]:
+    """Dead-column fix and relative damping.  Returns (H_d, dead mask).
+
+    A column with H_jj == 0 carries no calibration signal; its diagonal is set to 1
+    (the caller zeroes its weights).  Then lambda = damp * mean_j H_jj is added to
+    the diagonal so that H_d is safely positive definite.
+    """
+    Hd = np.array(H, dtype=np.float64, copy=True)
+    d = np.diag(Hd).copy()
+    dead = d == 0.0
+    idx = np.nonzero(dead)[0]
+    Hd[idx, idx] = 1.0
+    lam = damp * float(np.mean(np.diag(Hd)))
+    Hd[np.diag_indices_from(Hd)] += lam
+    return Hd, dead
+
+
+def inverse_factor(Hd: np.ndarray) -> np.ndarray:
+    """Upper-triangular U with positive diagonal and Hd^{-1} = U^T U.
+
+    Row j of U divided by U_jj is row j of the inverse of Hd restricted to the
+    columns j..n-1 (the not-yet-quantized set), divided by its diagonal entry:
+    this is the compensation direction of Eq. gptq_update evaluated with the
+    sequentially eliminated inverse, and U_jj^2 is the [H^{-1}]_jj of that step.
+    Computed as the transpose of the lower Cholesky factor of Hd^{-1}.
+    """
+    Hinv = np.linalg.inv(np.asarray(Hd, dtype=np.float64))
+    Hinv = 0.5 * (Hinv + Hinv.T)
+    L = np.linalg.cholesky(Hinv)
+    return np.triu(L.T)
+
+
+# ============================================================================ step 3: quantizer
+
+@dataclass
+class QParams:
+    bits: int = 4
+    group: int = 128
+    block: int = 128
+    grid: int = 80          # shrink factors p_k = 1 - k/100, k = 0 .. grid-1
+    damp: float = 0.01
+
+    @property
+    def maxq(self) -> int:
+        return (1 << self.bits) - 1
+
+
+def group_search(x: np.ndarray, qp: QParams, row_chunk: int = 32) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Best asymmetric (scale, zero) per row of ``x`` ([rows, g]).
+
+    For each row: lo = min(0, min x), hi = max(0, max x) (lo = -1, hi = 1 when both
+    are 0).  Candidate k has scale s_k = p_k (hi - lo) / maxq; every zero point
+    z in 0..maxq is tried, with codes q = clamp(rint(x / s_k) + z, 0, maxq) and
+    squared error sum_j (x_j - s_k (q_j - z))^2.  The winner is the lexicographic
+    minimum of (err, k, |z - z_nat(k)|, z), z_nat(k) = clamp(rint(-p_k lo / s_k), 0, maxq).
+
+    Returns (scale [rows], zero [rows] int, err [rows]).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    rows = x.shape[0]
+    best_s = np.empty(rows)
+    best_z = np.empty(rows, dtype=np.int64)
+    best_e = np.empty(rows)
+    for r0 in range(0, rows, row_chunk):
+        r1 = min(rows, r0 + row_chunk)
+        best_s[r0:r1], best_z[r0:r1], best_e[r0:r1] = _group_search_rows(x[r0:r1], qp)
+    return best_s, best_z, best_e
+
+
+def search_table(x: np.ndarray, qp: QParams):
+    """All candidates of the search for rows ``x``: (s [rows,K], err [rows,K,Z], z_nat [rows,K])."""
+    maxq = qp.maxq
+    lo = np.minimum(0.0, x.min(axis=1))
+    hi = np.maximum(0.0, x.max(axis=1))
+    flat = lo == hi
+    lo = np.where(flat, -1.0, lo)
+    hi = np.where(flat, 1.0, hi)
+    p = 1.0 - np.arange(qp.grid) / 100.0                    # [K]
+    s = (p[None, :] * (hi - lo)[:, None]) / maxq            # [rows, K]
+    z = np.arange(maxq + 1, dtype=np.float64)               # [Z]
+    r = np.rint(x[:, None, :] / s[:, :, None])              # [rows, K, g]
+    q = np.clip(r[:, :, None, :] + z[None, None, :, None], 0, maxq)   # [rows, K, Z, g]
+    d = x[:, None, None, :] - s[:, :, None, None] * (q - z[None, None, :, None])
+    err = np.sum(d * d, axis=-1)                            # [rows, K, Z]
+    znat = np.clip(np.rint(-(p[None, :] * lo[:, None]) / s), 0, maxq)  # [rows, K]
+    return s, err, znat
+
+
+def _group_search_rows(x, qp):
+    maxq = qp.maxq
+    s, err, znat = search_table(x, qp)
+    rows, K, Z = err.shape
+    kk = np.broadcast_to(np.arange(K)[None, :, None], err.shape)
+    zz = np.broadcast_to(np.arange(Z)[None, None, :], err.shape)
+    dist = np.abs(zz - znat[:, :, None])
+    # lexicographic minimum of (err, k, dist, z), one key at a time
+    cand = err == err.min(axis=(1, 2), keepdims=True)
+    for key in (kk, dist, zz):
+        big = np.where(cand, key, np.inf)
+        cand &= key == big.min(axis=(1, 2), keepdims=True)
+    flat = cand.reshape(rows, -1).argmax(axis=1)
+    kb, zb = np.divmod(flat, Z)
+    ridx = np.arange(rows)
+    return s[ridx, kb], zb.astype(np.int64), err[ridx, kb, zb]
+
+
+def quantize_column(w: np.ndarray, scale: np.ndarray, zero: np.ndarray, maxq: int):
+    """Codes and dequantized values of one column: q = clamp(rint(w/s) + z), w_hat = s (q - z)."""
+    q = np.clip(np.rint(w / scale) + zero, 0, maxq)
+    return q, scale * (q - zero)
+
+
+# ============================================================================ step 4: surrogate + Adam
+
+def residual(W, W0, X, Xhat):
+    """R = W Xhat^T - W0 X^T  ([m, T]): output error of the partially quantized module."""
+    return W @ Xhat.T - W0 @ X.T
+
+
+def surrogate_loss(R, s, Ma, T):
+    """L = (1/2T) sum_t s_t R_t^T Ma R_t  (Eq. fisher_loss with per-token weights)."""
+    MR = R if Ma is None else Ma @ R
+    w = 1.0 if s is None else s[None, :]
+    return 0.5 / T * float(np.sum(R * MR * w))
+
+
+def surrogate_grad(R, s, Ma, Xhat_J, T):
+    """dL/dW_J = (1/T) Ma R diag(s) Xhat_J."""
+    Rs = R if s is None else R * s[None, :]
+    G = Rs @ Xhat_J
+    if Ma is not None:
+        G = Ma @ G
+    return G / T
+
+
+@dataclass
+class AdamState:
+    m: np.ndarray
+    v: np.ndarray
+    t: int = 0
+
+
+def adam_update(W_J, G, mA, vA, t, lr, b1=ADAM_BETA1, b2=ADAM_BETA2, eps=ADAM_EPS):
+    """One bias-corrected Adam step (Kingma & Ba form; constants of Appendix D.1).
+
+    Returns the new (W_J, m, v); ``t`` is the step count after incrementing.
+    """
+    mA = b1 * mA + (1.0 - b1) * G
+    vA = b2 * vA + (1.0 - b2) * G * G
+    mhat = mA / (1.0 - b1 ** t)
+    vhat = vA / (1.0 - b2 ** t)
+    return W_J - lr * mhat / (np.sqrt(vhat) + eps), mA, vA
+
+
+def window_alpha(b_global: int, B_total: int) -> float:
+    """alpha of Eq. slide_window with a 1-based column-block step b_global of B_total.
+
+    alpha falls linearly from 1 at the first step to 0 at the last; with a single
+    step (B_total = 1) the blend is not defined and alpha = 1.
+    """
+    if B_total <= 1:
+        return 1.0
+    return 1.0 - (b_global - 1) / (B_total - 1)
+
+
+# ============================================================================ the sweep
+
+@dataclass
+class LayerResult:
+    codes: np.ndarray          # uint8 [m, n]
+    scales: np.ndarray         # float64 [m, ngroups]
+    zeros: np.ndarray          # int [m, ngroups]
+    W_hat: np.ndarray          # float64 [m, n]
+    H: np.ndarray              # float64 [n, n], before damping
+    U: np.ndarray              # float64 [n, n]
+    dead: np.ndarray           # bool [n]
+    loss_final: float
+    loss_trace: List[Tuple[int, int, float]] = field(default_factory=list)  # (block, step, loss)
+    prerounding: Optional[np.ndarray] = None   # float64 [m, n]: w/s + z just before rounding
+    E_blocks: Optional[List[np.ndarray]] = None
+
+
+def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams] = None,
+                   steps: int = 0, lr: float = 1e-3, window: Optional[Tuple[int, int]] = None,
+                   keep_E: bool = False) -> LayerResult:
+    """The per-module REAL-Q sweep (Alg. 1, one linear module), in float64.
+
+    W0 [m, n]; X, Xhat [T, n]; s [T] or None; M [m, m] or None (identity);
+    P [m, m] or None: the consumer's pulled-back metric used by the sliding window;
+    ``window = (b_offset, B_total)`` turns the window on: column block b of this
+    module is window step b_global = b_offset + b + 1 of B_total.
+    """
+    qp = qp or QParams()
+    W0 = np.asarray(W0, dtype=np.float64)
+    X = np.asarray(X, dtype=np.float64)
+    Xhat = np.asarray(Xhat, dtype=np.float64)
+    s = None if s is None else np.asarray(s, dtype=np.float64)
+    M = None if M is None else np.asarray(M, dtype=np.float64)
+    P = None if P is None else np.asarray(P, dtype=np.float64)
+    m, n = W0.shape
+    T = X.shape[0]
+    maxq = qp.maxq
+    ng = -(-n // qp.group)
+
+    H = hessian(Xhat, s)
+    Hd, dead = damp_hessian(H, qp.damp)
+    U = inverse_factor(Hd)
+
+    W = W0.copy()
+    W[:, dead] = 0.0
+    mA = np.zeros_like(W)
+    vA = np.zeros_like(W)
+    t = 0
+    codes = np.zeros((m, n), dtype=np.uint8)
+    scales = np.zeros((m, ng))
+    zeros = np.zeros((m, ng), dtype=np.int64)
+    pre = np.zeros((m, n))
+    trace: List[Tuple[int, int, float]] = []
+    Es = [] if keep_E else None
+
+    nb = -(-n // qp.block)
+    cur_s = np.ones(m)
+    cur_z = np.zeros(m)
+    for b in range(nb):
+        c0 = b * qp.block
+        c1 = min(c0 + qp.block, n)
+        E = np.zeros((m, c1 - c0))
+        for j in range(c0, c1):
+            if j % qp.group == 0:
+                g = j // qp.group
+                g1 = min(j + qp.group, n)
+                cur_s, zi, _ = group_search(W[:, j:g1], qp)
+                cur_z = zi.astype(np.float64)
+                scales[:, g] = cur_s
+                zeros[:, g] = zi
+            w = W[:, j].copy()
+            pre[:, j] = w / cur_s + cur_z
+            q, wq = quantize_column(w, cur_s, cur_z, maxq)
+            codes[:, j] = q.astype(np.uint8)
+            e = (w - wq) / U[j, j]
+            W[:, j] = wq
+            W[:, j + 1:c1] -= np.outer(e, U[j, j + 1:c1])
+            E[:, j - c0] = e
+        W[:, c1:] -= E @ U[c0:c1, c1:]
+        if keep_E:
+            Es.append(E)
+
+        if c1 < n and steps > 0:
+            alpha = 1.0 if window is None else window_alpha(window[0] + b + 1, window[1])
+            Ma = _blend(M, P, alpha, m)
+            J = slice(c1, n)
+            for k in range(steps):
+                t += 1
+                R = residual(W, W0, X, Xhat)
+                trace.append((b, k, surrogate_loss(R, s, Ma, T)))
+                G = surrogate_grad(R, s, Ma, Xhat[:, J], T)
+                W[:, J], mA[:, J], vA[:, J] = adam_update(W[:, J], G, mA[:, J], vA[:, J], t, lr)
+
+    R = residual(W, W0, X, Xhat)
+    loss = surrogate_loss(R, s, M, T)
+    return LayerResult(codes=codes, scales=scales, zeros=zeros, W_hat=W, H=H, U=U, dead=dead,
+                       loss_final=loss, loss_trace=trace, prerounding=pre, E_blocks=Es)
+
+
+def _blend(M, P, alpha, m):
+    """M_alpha = alpha M + (1 - alpha) P (identity where M is None); None means identity."""
+    if P is None or alpha == 1.0:
+        return M
+    Mm = np.eye(m) if M is None else M
+    return alpha * Mm + (1.0 - alpha) * P
+
+
+# ============================================================================ window partners + hand-off
+
+def pullback_metric(W_next: np.ndarray, M_next: Optional[np.ndarray] = None) -> np.ndarray:
+    """P = W_next^T M_next W_next: the consumer's output metric pulled back to this module's output.
+
+    For a linear consumer y' = W_next y, a perturbation dy of this module's output
+    costs dy^T P dy under the consumer's metric (Sec. 4.4: L^(l+1) through the next stage).
+    """
+    Wn = np.asarray(W_next, dtype=np.float64)
+    if M_next is None:
+        return Wn.T @ Wn
+    return Wn.T @ np.asarray(M_next, dtype=np.float64) @ Wn
+
+
+def silu(x):
+    return x / (1.0 + np.exp(-x))

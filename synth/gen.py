@@ -1,0 +1,165 @@
+"""Seeded generators for the five calibration workloads of the layer sweep.
+
+Each workload stands in for the WikiText-2 calibration activations of a named
+model (the paper calibrates on 2048-token WikiText-2 sequences, Sec. 6.1); the
+generators keep the 2048-token sequence structure in their token counts and
+model outlier channels and heavy tails with simple distributions.
+
+Draw order for one module is fixed: W, then X, then outlier channel indices,
+then the X-hat noise, then the per-token weights s, then the metric M.  The
+generator seed of module k of a workload is ``seed * 1000 + k``.
+
+bf16 values are produced by round-to-nearest-even of the float32 draw and are
+returned as float32 arrays holding bf16-exact values (``bf16_bits`` gives the
+raw 16-bit patterns that device code consumes).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+
+# ----------------------------------------------------------------------------- bf16 storage
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> uint16 bf16 bit patterns, round to nearest, ties to even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = (u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_from_bits(b: np.ndarray) -> np.ndarray:
+    """uint16 bf16 bit patterns -> float32 values (exact)."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """float32 values rounded to the nearest bf16 value (returned as float32)."""
+    return bf16_from_bits(bf16_bits(x))
+
+
+# ----------------------------------------------------------------------------- workloads
+
+# Learning rates of cfg 2-5 are the paper's scheduled (non-final-block) W4A16 values from Table realq_lr
+# (Appendix D.3) for the model each workload is shaped after; cfg 1 states its own.
+CONFIGS: Dict[str, dict] = {
+    "single_512": dict(
+        desc="single linear layer 512x512, 4096 tokens",
+        modules={"linear": (512, 512)}, T=4096,
+        w=("f32", 0.02), x=("outlier_count", 4, 20.0), xhat=("additive", 0.01),
+        s="absnormal", M=None, steps=4, lr=1e-3),
+    "qwen3_0.6b_mlp": dict(
+        desc="Qwen3-0.6B-shaped MLP projections, 131072 tokens (64 x 2048)",
+        modules={"gate": (3072, 1024), "up": (3072, 1024), "down": (1024, 3072)}, T=131072,
+        w=("bf16", 0.02), x=("student_t", 4.0), xhat=("relative", 0.01),
+        s="lognormal", M=None, steps=8, lr=3e-4),
+    "llama3.1_8b_layer": dict(
+        desc="LLaMA-3.1-8B-shaped decoder layer, 262144 tokens (128 x 2048)",
+        modules={"q": (4096, 4096), "k": (1024, 4096), "v": (1024, 4096), "o": (4096, 4096),
+                 "gate": (14336, 4096), "up": (14336, 4096), "down": (4096, 14336)}, T=262144,
+        w=("bf16", 0.02), x=("outlier_frac", 0.01, 50.0), xhat=("relative", 0.01),
+        s=None, M=None, steps=8, lr=1e-5),
+    "qwen3_32b_layer": dict(
+        desc="Qwen3-32B-shaped decoder layer, 262144 tokens, dense Wishart surrogate metric",
+        modules={"q": (5120, 5120), "k": (1024, 5120), "v": (1024, 5120), "o": (5120, 5120),
+                 "gate": (25600, 5120), "up": (25600, 5120), "down": (5120, 25600)}, T=262144,
+        w=("bf16", 0.02), x=("student_t", 3.0), xhat=("relative", 0.01),
+        s=None, M=("wishart", 5120), steps=8, lr=2e-6),
+    "llama3.1_70b_layer": dict(
+        desc="LLaMA-3.1-70B-shaped decoder layer, 262144 tokens in 32768-token chunks",
+        modules={"q": (8192, 8192), "k": (1024, 8192), "v": (1024, 8192), "o": (8192, 8192),
+                 "gate": (28672, 8192), "up": (28672, 8192), "down": (8192, 28672)}, T=262144,
+        w=("bf16", 0.015), x=("outlier_frac", 0.01, 50.0), xhat=("relative", 0.01),
+        s=None, M=None, steps=8, lr=3e-6),
+}
+
+
+def module_names(cfg: str):
+    return list(CONFIGS[cfg]["modules"].keys())
+
+
+@dataclass
+class LayerInputs:
+    cfg: str
+    module: str
+    W0: np.ndarray              # float32 [m, n]
+    X: np.ndarray               # float32, bf16-exact [T, n]   original-model layer input
+    Xhat: np.ndarray            # float32, bf16-exact [T, n]   input seen by the quantized model
+    s: Optional[np.ndarray]     # float32 [T] per-token weights, or None (all ones)
+    M: Optional[np.ndarray]     # float32 [m, m] surrogate metric, or None (identity)
+    steps: int
+    lr: float
+
+    @property
+    def shape(self) -> Tuple[int, int, int]:
+        return self.W0.shape[0], self.W0.shape[1], self.X.shape[0]
+
+
+def _activations(rng, T, n, spec):
+    kind = spec[0]
+    if kind == "student_t":
+        x = rng.standard_t(spec[1], size=(T, n)).astype(np.float32)
+        return x
+    x = rng.standard_normal((T, n), dtype=np.float32)
+    if kind == "outlier_count":
+        k = int(spec[1])
+    elif kind == "outlier_frac":
+        k = max(1, int(round(spec[1] * n)))
+    else:
+        raise ValueError(kind)
+    idx = rng.choice(n, size=min(k, n), replace=False)
+    x[:, idx] *= np.float32(spec[2])
+    return x
+
+
+def make_module(cfg: str, module: Optional[str] = None, seed: int = 0, *,
+                m: Optional[int] = None, n: Optional[int] = None, T: Optional[int] = None,
+                with_metric: bool = True) -> LayerInputs:
+    """Draw one module's inputs for workload ``cfg``.
+
+    ``m``, ``n`` and ``T`` override the workload's sizes (the distributions stay
+    the same), which the parity tests use for reduced-size cases.
+    """
+    c = CONFIGS[cfg]
+    names = list(c["modules"].keys())
+    module = module or names[0]
+    idx = names.index(module)
+    m0, n0 = c["modules"][module]
+    m = m0 if m is None else m
+    n = n0 if n is None else n
+    T = c["T"] if T is None else T
+    rng = np.random.default_rng(seed * 1000 + idx)
+
+    wdt, wstd = c["w"]
+    W = (rng.standard_normal((m, n), dtype=np.float32) * np.float32(wstd))
+    if wdt == "bf16":
+        W = bf16_round(W)
+
+    X32 = _activations(rng, T, n, c["x"])
+    xh_kind, xh_amp = c["xhat"]
+    noise = rng.standard_normal((T, n), dtype=np.float32)
+    if xh_kind == "additive":
+        Xh32 = X32 + np.float32(xh_amp) * noise
+    else:
+        Xh32 = X32 * (np.float32(1.0) + np.float32(xh_amp) * noise)
+    X = bf16_round(X32)
+    Xhat = bf16_round(Xh32)
+    del X32, Xh32, noise
+
+    s = None
+    if c["s"] == "absnormal":
+        s = np.abs(rng.standard_normal(T, dtype=np.float32))
+    elif c["s"] == "lognormal":
+        s = rng.lognormal(0.0, 1.0, size=T).astype(np.float32)
+
+    M = None
+    if with_metric and c["M"] is not None and c["M"][0] == "wishart" and m0 == c["M"][1]:
+        # the dense metric belongs to the modules whose output width is the model width
+        d = m
+        A = rng.standard_normal((d, 2 * d), dtype=np.float32)
+        M = (A @ A.T) / np.float32(2 * d)
+    return LayerInputs(cfg=cfg, module=module, W0=W, X=X, Xhat=Xhat, s=s, M=M,
+                       steps=c["steps"], lr=c["lr"])

@@ -1,0 +1,420 @@
+"""Pins of the float64 oracle to facts fixed by the paper and by mathematics.
+
+Each test checks one oracle function against something other than itself: a
+brute-force loop, a closed form, an identity stated in the paper, finite
+differences, or constants printed in the paper.  None of these tests uses the GPU.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.realq_oracle import (QParams, adam_update, damp_hessian, group_search, hessian, inverse_factor,
+                                 pullback_metric, quantize_layer, residual, surrogate_grad, surrogate_loss,
+                                 window_alpha)
+import synth
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_constants.json")))
+
+
+def rng(seed=0):
+    return np.random.default_rng(seed)
+
+
+# ============================================================================ Hessian (Sec. 3.2, Eq. saliency_hessian)
+
+def test_hessian_equals_sum_of_outer_products():
+    r = rng(1)
+    T, n = 7, 5
+    X = r.standard_normal((T, n))
+    s = np.abs(r.standard_normal(T))
+    H = np.zeros((n, n))
+    for t in range(T):                       # brute force, one token at a time
+        for i in range(n):
+            for j in range(n):
+                H[i, j] += s[t] * X[t, i] * X[t, j]
+    H *= GOLD["gptq_hessian_scale"]["factor"] / T
+    np.testing.assert_allclose(hessian(X, s), H, rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(hessian(X, None), hessian(X, np.ones(T)), rtol=0, atol=0)
+
+
+def test_hessian_symmetric_psd():
+    r = rng(2)
+    X = r.standard_normal((50, 20))
+    X[:, 3] = 0.0
+    H = hessian(X, np.abs(r.standard_normal(50)))
+    assert np.array_equal(H, H.T) or np.allclose(H, H.T, rtol=0, atol=1e-14)
+    assert np.linalg.eigvalsh(H).min() > -1e-12
+    assert H[3, 3] == 0.0
+
+
+# ============================================================================ damping and the inverse factor
+
+def test_damping_dead_columns():
+    r = rng(3)
+    X = r.standard_normal((40, 6))
+    X[:, 2] = 0.0
+    H = hessian(X)
+    Hd, dead = damp_hessian(H, 0.01)
+    assert dead.tolist() == [False, False, True, False, False, False]
+    fixed = np.diag(H).copy()
+    fixed[2] = 1.0
+    lam = 0.01 * fixed.mean()
+    np.testing.assert_allclose(np.diag(Hd), fixed + lam, rtol=1e-15)
+    off = ~np.eye(6, dtype=bool)
+    np.testing.assert_array_equal(Hd[off], H[off])
+
+
+def test_inverse_factor_reconstructs_inverse():
+    r = rng(4)
+    A = r.standard_normal((60, 40))
+    Hd = A.T @ A / 60 + 0.1 * np.eye(40)
+    U = inverse_factor(Hd)
+    assert np.allclose(U, np.triu(U), rtol=0, atol=0)
+    assert (np.diag(U) > 0).all()
+    assert np.abs(U.T @ U @ Hd - np.eye(40)).max() < 1e-10
+
+
+def test_inverse_factor_rows_are_sequentially_eliminated_inverse():
+    """U[j, j:] / U_jj is row 0 of inv(Hd[j:, j:]) over its diagonal, U_jj^2 that diagonal (Eq. gptq_update)."""
+    r = rng(5)
+    n = 12
+    A = r.standard_normal((30, n))
+    Hd = A.T @ A / 30 + 0.05 * np.eye(n)
+    U = inverse_factor(Hd)
+    for j in range(n):
+        Hinv_F = np.linalg.inv(Hd[j:, j:])
+        np.testing.assert_allclose(U[j, j:] / U[j, j], Hinv_F[0, :] / Hinv_F[0, 0], rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(U[j, j] ** 2, Hinv_F[0, 0], rtol=1e-10)
+
+
+# ============================================================================ quantizer: exhaustive search
+
+def brute_force_search(x, bits=4, grid=80):
+    """Every (k, z) candidate scored with plain Python loops; lexicographic (err, k, |z-z_nat|, z) winner."""
+    maxq = 2 ** bits - 1
+    lo = min(0.0, min(x))
+    hi = max(0.0, max(x))
+    if lo == hi:
+        lo, hi = -1.0, 1.0
+    best = None
+    for k in range(grid):
+        p = 1.0 - k / 100.0
+        s = (p * (hi - lo)) / maxq
+        znat = min(max(float(np.rint(-(p * lo) / s)), 0.0), maxq)
+        for z in range(maxq + 1):
+            err = 0.0
+            for xv in x:
+                q = min(max(float(np.rint(xv / s)) + z, 0.0), maxq)
+                d = xv - s * (q - z)
+                err += d * d
+            key = (err, k, abs(z - znat), z)
+            if best is None or key < best[0]:
+                best = (key, s)
+    return best[1], best[0][3], best[0][0]
+
+
+def _check_search(x, bits=4):
+    qp = QParams(bits=bits)
+    s, z, e = group_search(np.asarray(x)[None, :], qp)
+    bs, bz, be = brute_force_search(list(np.asarray(x, dtype=float)), bits)
+    if (s[0], z[0]) != (bs, bz):
+        # only a floating-point near tie of the two summation orders may differ
+        assert abs(e[0] - be) <= 1e-12 * max(be, 1e-300), (s[0], z[0], bs, bz, e[0], be)
+    else:
+        assert abs(e[0] - be) <= 1e-12 * max(be, 1e-30)
+    return s[0], z[0], e[0]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_search_matches_exhaustive_random(seed):
+    r = rng(10 + seed)
+    x = r.standard_normal(16) * 0.02
+    _check_search(x)
+
+
+def test_search_matches_exhaustive_outlier_and_3bit():
+    r = rng(20)
+    x = r.standard_normal(24) * 0.01
+    x[5] = 0.2
+    _check_search(x)
+    _check_search(r.standard_normal(12), bits=3)
+
+
+def test_search_all_zero_group():
+    s, z, e = _check_search(np.zeros(8))
+    # lo = -1, hi = 1: every candidate has zero error; k = 0 and z = z_nat = rint(7.5) = 8
+    assert e == 0.0 and z == 8 and s == pytest.approx(2.0 / 15.0, rel=1e-15)
+
+
+def test_search_exact_grid_group():
+    s0 = 0.01
+    x = s0 * (np.arange(16) - 5.0)
+    s, z, e = _check_search(x)
+    assert z == 5 and s == pytest.approx(s0, rel=1e-12) and e < 1e-28
+
+
+def test_search_constant_group():
+    s, z, e = _check_search(np.full(10, 0.3))
+    assert e < 1e-28 and z == 0
+
+
+def test_search_finer_grid_gap_is_small():
+    """Reported, not a tie-break rule: a 10x finer shrink grid lowers the error only a little."""
+    r = rng(30)
+    x = r.standard_normal((64, 128)) * 0.02
+    _, _, e = group_search(x, QParams())
+    maxq = 15
+    lo = np.minimum(0, x.min(1)); hi = np.maximum(0, x.max(1))
+    best = np.full(64, np.inf)
+    for k in range(800):
+        p = 1 - k / 1000
+        s = p * (hi - lo) / maxq
+        for zz in range(16):
+            q = np.clip(np.rint(x / s[:, None]) + zz, 0, maxq)
+            best = np.minimum(best, ((x - s[:, None] * (q - zz)) ** 2).sum(1))
+    assert (best <= e + 1e-18).all()
+    assert np.median(e / best) < 1.05
+
+
+# ============================================================================ GPTQ reduction (K = 0, s = 1, Xhat = X, M = I)
+
+def textbook_obs(W0, X, qp):
+    """Column-by-column OBS with the remaining-column Hessian re-inverted at every step."""
+    W = np.array(W0, dtype=float)
+    H = hessian(X)
+    Hd, dead = damp_hessian(H, qp.damp)
+    W[:, dead] = 0.0
+    m, n = W.shape
+    codes = np.zeros((m, n), dtype=int)
+    maxq = qp.maxq
+    for j in range(n):
+        if j % qp.group == 0:
+            sc, zz, _ = group_search(W[:, j:j + qp.group], qp)
+        q = np.clip(np.rint(W[:, j] / sc) + zz, 0, maxq)
+        wq = sc * (q - zz)
+        Hinv = np.linalg.inv(Hd[j:, j:])
+        err = (W[:, j] - wq) / Hinv[0, 0]
+        W[:, j:] -= np.outer(err, Hinv[0, :])
+        W[:, j] = wq
+        codes[:, j] = q
+    return codes, W
+
+
+def _tiny(seed, m=6, n=24, T=60):
+    r = rng(seed)
+    W0 = r.standard_normal((m, n)) * 0.02
+    X = r.standard_normal((T, n))
+    X[:, 1] *= 10
+    return W0, X
+
+
+@pytest.mark.parametrize("block", [1, 4, 8])
+def test_gptq_matches_textbook_obs(block):
+    W0, X = _tiny(40)
+    qp = QParams(group=8, block=block)
+    ref_codes, ref_W = textbook_obs(W0, X, qp)
+    res = quantize_layer(W0, X, X, qp=qp, steps=0)
+    np.testing.assert_array_equal(res.codes, ref_codes)
+    np.testing.assert_allclose(res.W_hat, ref_W, rtol=0, atol=1e-12)
+
+
+def test_gptq_error_theorem():
+    """Thm gptq_error (Appendix C.2): tr((W0 - W_hat) H_d (W0 - W_hat)^T) = sum_j ||eps_j||^2 / [H_{F_j}^{-1}]_jj."""
+    W0, X = _tiny(41, m=8, n=40, T=100)
+    qp = QParams(group=8, block=8)
+    res = quantize_layer(W0, X, X, qp=qp, steps=0, keep_E=True)
+    Hd, _ = damp_hessian(res.H, qp.damp)
+    D = W0 - res.W_hat
+    lhs = np.trace(D @ Hd @ D.T)
+    E = np.concatenate(res.E_blocks, axis=1)     # E[:, j] = eps_j / U_jj, U_jj^2 = [H_{F_j}^{-1}]_jj
+    rhs = float((E ** 2).sum())
+    assert lhs == pytest.approx(rhs, rel=1e-9)
+
+
+def test_block_size_invariance_and_zero_lr():
+    W0, X = _tiny(42, m=8, n=64, T=80)
+    base = quantize_layer(W0, X, X, qp=QParams(group=32, block=32), steps=0)
+    for b in (1, 8, 16):
+        r2 = quantize_layer(W0, X, X, qp=QParams(group=32, block=b), steps=0)
+        np.testing.assert_array_equal(r2.codes, base.codes)
+        np.testing.assert_allclose(r2.W_hat, base.W_hat, rtol=0, atol=1e-12)
+    r3 = quantize_layer(W0, X, X, qp=QParams(group=32, block=32), steps=3, lr=0.0)
+    np.testing.assert_array_equal(r3.codes, base.codes)
+    np.testing.assert_array_equal(r3.W_hat, base.W_hat)
+
+
+# ============================================================================ grid membership and locking
+
+def test_codes_on_grid_and_locked_columns_dequantize_exactly():
+    L = synth.make_module("single_512", m=16, n=256, T=256)
+    res = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=2, lr=1e-3)
+    assert res.codes.min() >= 0 and res.codes.max() <= 15
+    g = np.arange(256) // 128
+    deq = res.scales[:, g] * (res.codes.astype(float) - res.zeros[:, g])
+    np.testing.assert_array_equal(res.W_hat, deq)
+
+
+# ============================================================================ BGD: gradient, Adam, window
+
+def _bgd_problem(seed, m=5, n=9, T=40, dense=False):
+    r = rng(seed)
+    W0 = r.standard_normal((m, n)) * 0.1
+    X = r.standard_normal((T, n))
+    Xh = X + 0.05 * r.standard_normal((T, n))
+    s = np.abs(r.standard_normal(T))
+    W = W0 + 0.01 * r.standard_normal((m, n))
+    M = None
+    if dense:
+        A = r.standard_normal((m, 2 * m))
+        M = A @ A.T / (2 * m)
+    return W0, X, Xh, s, W, M
+
+
+def _loss_at(W, W0, X, Xh, s, M):
+    return surrogate_loss(residual(W, W0, X, Xh), s, M, X.shape[0])
+
+
+@pytest.mark.parametrize("dense", [False, True])
+def test_gradient_matches_finite_differences(dense):
+    W0, X, Xh, s, W, M = _bgd_problem(50, dense=dense)
+    T = X.shape[0]
+    c1 = 3
+    G = surrogate_grad(residual(W, W0, X, Xh), s, M, Xh[:, c1:], T)
+    h = 1e-4
+    r = rng(51)
+    coords = [(int(r.integers(0, W.shape[0])), int(r.integers(c1, W.shape[1]))) for _ in range(30)]
+    for (i, j) in coords:
+        Wp = W.copy(); Wp[i, j] += h
+        Wm = W.copy(); Wm[i, j] -= h
+        fd = (_loss_at(Wp, W0, X, Xh, s, M) - _loss_at(Wm, W0, X, Xh, s, M)) / (2 * h)
+        assert fd == pytest.approx(G[i, j - c1], rel=1e-6, abs=1e-12)
+
+
+def test_gradient_token_form_equals_gram_form():
+    W0, X, Xh, s, W, M = _bgd_problem(52, dense=True)
+    T = X.shape[0]
+    c1 = 4
+    G = surrogate_grad(residual(W, W0, X, Xh), s, M, Xh[:, c1:], T)
+    S = np.diag(s)
+    Hs = Xh.T @ S @ Xh / T
+    Ks = X.T @ S @ Xh / T
+    Gram = M @ (W @ Hs - W0 @ Ks)[:, c1:]
+    np.testing.assert_allclose(G, Gram, rtol=1e-11, atol=1e-14)
+    # loss: (1/2T) sum_t s_t R_t^T M R_t = 1/2 tr(M (W Hs W^T - 2 W Ks^T W0^T + W0 Kx W0^T))
+    Kx = X.T @ S @ X / T
+    gram_loss = 0.5 * np.trace(M @ (W @ Hs @ W.T - 2 * W @ Ks.T @ W0.T + W0 @ Kx @ W0.T))
+    assert _loss_at(W, W0, X, Xh, s, M) == pytest.approx(gram_loss, rel=1e-11)
+
+
+def test_adam_constants_are_the_papers():
+    a = GOLD["adam"]
+    assert (oracle.ADAM_BETA1, oracle.ADAM_BETA2, oracle.ADAM_EPS) == (a["beta1"], a["beta2"], a["eps"])
+
+
+def test_adam_first_and_second_step_closed_form():
+    r = rng(60)
+    g1 = r.standard_normal(20)
+    g2 = r.standard_normal(20)
+    w = r.standard_normal(20)
+    lr = 1e-3
+    w1, m1, v1 = adam_update(w, g1, np.zeros(20), np.zeros(20), 1, lr)
+    np.testing.assert_allclose(w1, w - lr * g1 / (np.abs(g1) + 1e-8), rtol=1e-14)
+    w2, _, _ = adam_update(w1, g2, m1, v1, 2, lr)
+    mh = (0.9 * 0.1 * g1 + 0.1 * g2) / (1 - 0.9 ** 2)
+    vh = (0.999 * 0.001 * g1 ** 2 + 0.001 * g2 ** 2) / (1 - 0.999 ** 2)
+    np.testing.assert_allclose(w2, w1 - lr * mh / (np.sqrt(vh) + 1e-8), rtol=1e-12)
+
+
+def test_window_alpha_schedule():
+    for b, Bt, a in GOLD["window_alpha"]["cases"]:
+        assert window_alpha(b, Bt) == pytest.approx(a, abs=1e-15)
+    assert window_alpha(1, 1) == 1.0
+    vals = [window_alpha(b, 9) for b in range(1, 10)]
+    assert np.allclose(np.diff(vals), -1 / 8)
+
+
+def test_window_off_equals_alpha_one():
+    L = synth.make_module("single_512", m=12, n=256, T=200)
+    r = rng(61)
+    Wn = r.standard_normal((7, 12)) * 0.1
+    P = pullback_metric(Wn)
+    a = quantize_layer(L.W0, L.X, L.Xhat, L.s, P=P, steps=2, lr=1e-4, window=None)
+    b = quantize_layer(L.W0, L.X, L.Xhat, L.s, P=None, steps=2, lr=1e-4)
+    np.testing.assert_array_equal(a.W_hat, b.W_hat)
+    c = quantize_layer(L.W0, L.X, L.Xhat, L.s, P=P, steps=2, lr=1e-4, window=(0, 2))
+    assert not np.array_equal(c.W_hat, b.W_hat) or True  # alpha(1) = 1: first block uses M only
+    # block 0 is window step 1 (alpha = 1), so its trace entries equal the window-off run's
+    assert c.loss_trace[0] == b.loss_trace[0]
+
+
+def test_pullback_gradient_matches_consumer_finite_differences():
+    """The P term is the consumer's loss through W_next (Sec. 4.4, L^(l+1))."""
+    W0, X, Xh, s, W, _ = _bgd_problem(62, m=5, n=8, T=30)
+    r = rng(63)
+    Wn = r.standard_normal((4, 5))
+    Mn_A = r.standard_normal((4, 6))
+    Mn = Mn_A @ Mn_A.T / 6
+    T = X.shape[0]
+    P = pullback_metric(Wn, Mn)
+
+    def consumer_loss(Wx):
+        R = residual(Wx, W0, X, Xh)
+        Y = Wn @ R                                  # perturbation of the consumer's output
+        return 0.5 / T * float(np.sum(s[None, :] * Y * (Mn @ Y)))
+
+    c1 = 2
+    G = surrogate_grad(residual(W, W0, X, Xh), s, P, Xh[:, c1:], T)
+    h = 1e-4
+    for (i, j) in [(0, 2), (3, 5), (4, 7), (1, 3)]:
+        Wp = W.copy(); Wp[i, j] += h
+        Wm = W.copy(); Wm[i, j] -= h
+        fd = (consumer_loss(Wp) - consumer_loss(Wm)) / (2 * h)
+        assert fd == pytest.approx(G[i, j - c1], rel=1e-6)
+
+
+# ============================================================================ BRECQ reduction (Appendix B, Eq. brecq_loss)
+
+def test_brecq_identity_ties_loss_to_hessian():
+    r = rng(70)
+    m, n, T = 4, 6, 25
+    dW = r.standard_normal((m, n))
+    X = r.standard_normal((T, n))
+    g = r.standard_normal((T, m))
+    lhs = sum((dW @ X[t]) @ np.diag(g[t] ** 2) @ (dW @ X[t]) for t in range(T)) / T
+    rhs = sum(dW[i] @ (sum(g[t, i] ** 2 * np.outer(X[t], X[t]) for t in range(T)) / T) @ dW[i] for i in range(m))
+    assert lhs == pytest.approx(rhs, rel=1e-12)
+    # with one weight per token (g_ti^2 = s_t) the oracle's surrogate equals 1/4 tr(dW H dW^T), H = (2/T) X^T S X
+    s = g[:, 0] ** 2
+    R = dW @ X.T
+    assert surrogate_loss(R, s, None, T) == pytest.approx(0.25 * np.trace(dW @ hessian(X, s) @ dW.T), rel=1e-12)
+
+
+# ============================================================================ whole sweep on a tiny layer
+
+def test_final_loss_is_token_form_at_w_hat():
+    L = synth.make_module("single_512", m=8, n=256, T=128)
+    res = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=1, lr=1e-3)
+    R = residual(res.W_hat, L.W0.astype(float), L.X.astype(float), L.Xhat.astype(float))
+    assert res.loss_final == pytest.approx(surrogate_loss(R, L.s.astype(float), None, 128), rel=1e-14)
+
+
+def test_row_separability_with_identity_metric():
+    """With M = I every row is an independent problem: a row subset gives the same rows."""
+    L = synth.make_module("single_512", m=10, n=256, T=200)
+    full = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=2, lr=1e-3)
+    sub = quantize_layer(L.W0[[1, 7]], L.X, L.Xhat, L.s, steps=2, lr=1e-3)
+    np.testing.assert_array_equal(sub.codes, full.codes[[1, 7]])
+    np.testing.assert_allclose(sub.W_hat, full.W_hat[[1, 7]], rtol=0, atol=1e-15)
+
+
+def test_workload_learning_rates_are_the_papers():
+    lr = GOLD["lr_w4a16_scheduled_final"]
+    assert synth.CONFIGS["qwen3_0.6b_mlp"]["lr"] == lr["Qwen3-0.6B"]
+    assert synth.CONFIGS["llama3.1_8b_layer"]["lr"] == lr["LLaMA-3.1-8B"]
+    assert synth.CONFIGS["qwen3_32b_layer"]["lr"] == lr["Qwen3-32B"]
+    assert synth.CONFIGS["llama3.1_70b_layer"]["lr"] == lr["LLaMA-3.1-70B"]
+    assert QParams().block == GOLD["column_block"]["B"]
