@@ -1,0 +1,206 @@
+/*
+ * realq.h - C ABI of the REAL-Q per-layer quantization sweep on MI355X (gfx950).
+ *
+ * The library quantizes one linear module W (m x n, row = output channel) to
+ * asymmetric group-wise integers with GPTQ-style compensation, and after every
+ * column block runs Block-wise Gradient Descent on the not-yet-quantized columns
+ * (REAL-Q, Sec. 3-4 and Alg. 1 of Appendix A).
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller, row-major and
+ *     contiguous unless a leading dimension says otherwise.  bf16 arrays are passed
+ *     as uint16_t bit patterns.  The library never frees caller memory.
+ *   - Work is enqueued on the HIP stream given to realq_ctx_create and is
+ *     asynchronous unless stated; caller buffers must stay alive until the stream
+ *     has passed the work.
+ *   - Return value: REALQ_OK (0) or a negative REALQ_ERR_* code.  Arguments are
+ *     validated before anything is launched, so an error return from validation
+ *     leaves all outputs untouched.  An error detected after launch (a HIP error,
+ *     a non-positive-definite Hessian) leaves outputs undefined.
+ *     realq_last_error(ctx) returns a message for the last failure on that context.
+ *   - A context is not thread-safe; use one context per host thread / stream.
+ *
+ * Shapes: m output channels, n input channels (columns), T calibration tokens.
+ * Calibration inputs are token-major: X[t*n + j].
+ */
+#ifndef REALQ_H
+#define REALQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define REALQ_OK               0
+#define REALQ_ERR_INVALID_ARG (-1) /* NULL where not allowed, bad parameter value           */
+#define REALQ_ERR_SHAPE       (-2) /* inconsistent or unsupported sizes                     */
+#define REALQ_ERR_NOT_SPD     (-3) /* damped Hessian not positive definite                  */
+#define REALQ_ERR_HIP         (-4) /* HIP runtime error (launch, copy, event)               */
+#define REALQ_ERR_OOM         (-5) /* device allocation failed                              */
+#define REALQ_ERR_NONFINITE   (-6) /* non-finite value found in an input checked on device  */
+
+typedef struct realq_ctx realq_ctx;             /* stream (borrowed), workspaces, last error */
+typedef struct realq_bgd_state realq_bgd_state; /* per-module BGD state, see realq_bgd_state_create */
+
+/* Quantizer and GPTQ parameters.
+ *   bits  : code width, 2..8 (codes are 0 .. 2^bits-1)                     [4]
+ *   group : columns sharing one (scale, zero) per row, >= 1               [128]
+ *   block : GPTQ column block B (Sec. 3.2), 1..128; BGD runs after each    [128]
+ *   grid  : number of shrink factors p_k = 1 - k/100, k = 0..grid-1, 1..100 [80]
+ *   damp  : relative damping, lambda = damp * mean(diag H), > 0            [0.01]
+ * Either block % group == 0 or group % block == 0 must hold. */
+typedef struct realq_qparams {
+    int32_t bits, group, block, grid;
+    float damp;
+} realq_qparams;
+
+/* Block-GD parameters (Sec. 4.3, Eq. block_gd_update; Adam constants of Appendix D.1).
+ *   steps     : Adam steps after every column block (0 = plain GPTQ)
+ *   lr        : learning rate eta
+ *   beta1, beta2, eps : Adam constants [0.9, 0.999, 1e-8]
+ *   tok_chunk : tokens per streamed chunk of the residual/gradient GEMMs (0 = all T) */
+typedef struct realq_bgd_params {
+    int32_t steps;
+    float lr, beta1, beta2, eps;
+    int64_t tok_chunk;
+} realq_bgd_params;
+
+/* Fill *q / *b with the defaults given above. */
+void realq_qparams_default(realq_qparams* q);
+void realq_bgd_params_default(realq_bgd_params* b);
+
+/* ------------------------------------------------------------------ context */
+
+/* Create a context bound to hip_stream (a hipStream_t; NULL = the null stream) on
+ * the current device.  The stream is borrowed, not owned. */
+int realq_ctx_create(realq_ctx** out, void* hip_stream);
+void realq_ctx_destroy(realq_ctx* ctx);
+const char* realq_last_error(const realq_ctx* ctx);
+
+/* Kernel timing: when enabled, the library brackets the launches of its main
+ * kernels with HIP events on its stream and accumulates their durations, read with
+ * realq_ctx_kernel_time after the stream has drained.  Names: "hessian",
+ * "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init".
+ * Returns REALQ_ERR_INVALID_ARG for an unknown name. */
+int realq_ctx_set_timing(realq_ctx* ctx, int enable);
+int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms);
+int realq_ctx_reset_timing(realq_ctx* ctx);
+
+/* ------------------------------------------------------------------ a1: Hessian
+ * Sec. 3.2 (H = (2/T) sum_t x_t x_t^T) and Eq. saliency_hessian (per-token weights).
+ * H_acc[n*n] (float64, caller-initialised, typically zeroed) += sum_t s_t xhat_t xhat_t^T
+ * over the T tokens given.  Call once per token chunk; the 2/T scale is applied by
+ * realq_chol_inverse with the total token count.  s may be NULL (all ones).
+ * T == 0 is a no-op.  The full symmetric matrix is written. */
+int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat /*[T,n]*/, const float* s /*[T]|NULL*/,
+                        int64_t T, int64_t n, double* H_acc /*[n,n]*/);
+
+/* ------------------------------------------------------------------ a2: inverse factor
+ * H = (2/T_total) H_acc is written to H_out (float32) when H_out != NULL.  Dead
+ * columns (H_jj == 0) get H_jj = 1 and are flagged in dead[j] (when non-NULL);
+ * then H_d = H + damp*mean(diag H) I, and U (upper triangular, positive diagonal,
+ * float32, lower triangle zero) with H_d^{-1} = U^T U is written.  Row j of U
+ * over U_jj is the compensation direction of Eq. gptq_update (Sec. 3.2) with the
+ * sequentially eliminated inverse.  Computed in float64.  Synchronises the stream
+ * once to read the positive-definiteness flag: REALQ_ERR_NOT_SPD if it fails
+ * (retry with a larger damp). */
+int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T_total, float damp,
+                       float* H_out /*[n,n]|NULL*/, float* U /*[n,n]*/, uint8_t* dead /*[n]|NULL*/);
+
+/* ------------------------------------------------------------------ BGD state
+ * Per-module state of Block-GD (Sec. 4.3): the residual base
+ *   B = W0 (Xhat - X)^T + (W_locked - W0_locked) Xhat_locked^T      ([m,T] float32),
+ * the Adam moments (m, v, [m,n] float32), the step counter, a transposed copy of
+ * Xhat and the split of W - W0 the GEMMs consume.  W0, X, Xhat, s, M and P are
+ * borrowed and must stay valid for the state's lifetime.
+ *   X    : inputs of the full-precision model ([T,n] bf16); Xhat: inputs the
+ *          partially quantized model feeds this module ([T,n] bf16); X == Xhat
+ *          (same pointer) is allowed.
+ *   s    : per-token weights [T] or NULL (all ones).
+ *   M    : surrogate output metric [m,m] float32 (symmetric) or NULL (identity):
+ *          the aggregated Fisher of Eq. fisher_full / fisher_loss.
+ *   P    : consumer's pulled-back metric [m,m] float32 or NULL, blended with M by
+ *          the sliding window (Eq. slide_window).
+ * The state assumes the caller's working weights start equal to W0 and are only
+ * changed through realq_quantize_block / realq_bgd_step afterwards. */
+int realq_bgd_state_create(realq_ctx* ctx, realq_bgd_state** out, const float* W0 /*[m,n]*/,
+                           const uint16_t* X /*[T,n]*/, const uint16_t* Xhat /*[T,n]*/,
+                           const float* s /*[T]|NULL*/, const float* M /*[m,m]|NULL*/,
+                           const float* P /*[m,m]|NULL*/, int64_t m, int64_t n, int64_t T,
+                           const realq_bgd_params* params);
+void realq_bgd_state_destroy(realq_bgd_state* st);
+
+/* ------------------------------------------------------------------ a3-a6: one column block
+ * Quantize columns [c0, c0+bs) of W (in place; the block is written back
+ * dequantized) following Alg. 1's inner loop: dead columns of the block are zeroed,
+ * group (scale, zero) parameters are searched when a group starts, each column is
+ * quantized and its error compensated on the block's remaining columns
+ * (Eq. gptq_update), then all columns >= c0+bs get the batch update W -= E_b U_{b,:}
+ * (Sec. 3.2).  Writes codes (uint8, 0..2^bits-1), scales ([m, ceil(n/group)] float32)
+ * and zeros ([m, ceil(n/group)] uint8) for the groups touched.  Group parameters of a
+ * group that started in an earlier block are read back from scales/zeros.
+ * U and dead come from realq_chol_inverse.  When st != NULL the residual base of
+ * the state is also advanced by the locked block (Sec. 4.3: quantized weights stay
+ * locked).  Requirements: c0 % block-boundaries as produced by walking the columns
+ * in order, bs <= 128. */
+int realq_quantize_block(realq_ctx* ctx, float* W /*[m,n]*/, int64_t m, int64_t n, int64_t c0, int64_t bs,
+                         const float* U /*[n,n]*/, const uint8_t* dead /*[n]|NULL*/, const realq_qparams* qp,
+                         uint8_t* codes /*[m,n]*/, float* scales, uint8_t* zeros, realq_bgd_state* st);
+
+/* ------------------------------------------------------------------ a7-a9: one BGD step
+ * One Adam step (Eq. block_gd_update) on the trailing columns W[:, c1:n] against
+ *   L = (1/2T) sum_t s_t R_t^T M_a R_t,  R = W Xhat^T - W0 X^T,  M_a = alpha M + (1-alpha) P
+ * (Eq. fisher_loss at the module output; Eq. slide_window for alpha).  The gradient
+ * (1/T) M_a R diag(s) Xhat[:, c1:] is formed with token-streamed GEMMs.
+ * loss_out (device float64 scalar, may be NULL) receives L before the update; it
+ * is computed for M_a = identity only and set to NaN otherwise.  c1 == n is a no-op. */
+int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, float* W /*[m,n]*/, int64_t c1, float alpha,
+                   double* loss_out);
+
+/* Final surrogate loss with the module's own metric (alpha = 1) at the current W,
+ * written to *loss_out (device float64).  M = identity only (else REALQ_ERR_SHAPE). */
+int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const float* W, double* loss_out);
+
+/* ------------------------------------------------------------------ a1-a11: whole module
+ * The whole sweep for one module: Hessian over all tokens, inverse factor, then for
+ * every column block realq_quantize_block followed (when steps > 0 and columns
+ * remain) by `steps` realq_bgd_step calls, and the final loss.
+ * Window: when window_total > 0, column block b of this module is step
+ * b_global = window_offset + b + 1 of window_total and alpha follows Eq. slide_window;
+ * otherwise alpha = 1. */
+typedef struct realq_layer_desc {
+    int64_t m, n, T;
+    const float* W0;          /* [m,n] float32                                 */
+    const uint16_t* X;        /* [T,n] bf16                                     */
+    const uint16_t* Xhat;     /* [T,n] bf16                                     */
+    const float* s;           /* [T] | NULL                                     */
+    const float* M;           /* [m,m] | NULL (identity)                        */
+    const float* P;           /* [m,m] | NULL                                   */
+    int32_t window_offset, window_total;
+    realq_qparams q;
+    realq_bgd_params bgd;
+} realq_layer_desc;
+
+typedef struct realq_layer_out {
+    uint8_t* codes;           /* [m,n]                     required             */
+    float* scales;            /* [m,ceil(n/group)]         required             */
+    uint8_t* zeros;           /* [m,ceil(n/group)]         required             */
+    float* W_hat;             /* [m,n] final dequantized weights, required; also the working buffer */
+    float* H;                 /* [n,n] float32 Hessian before damping | NULL    */
+    float* U;                 /* [n,n] inverse factor | NULL (workspace used)   */
+    uint8_t* dead;            /* [n] | NULL                                     */
+    double* loss_trace;       /* [nblocks*steps] device float64 | NULL          */
+    double loss_final;        /* host: final loss (M = identity), NaN otherwise */
+    double ms_total;          /* host: wall time of the call between events on the stream */
+} realq_layer_out;
+
+/* Synchronises the stream (after the inverse factor, and at the end to read the
+ * final loss).  Returns the first error of any stage. */
+int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* desc, realq_layer_out* out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* REALQ_H */

@@ -1,0 +1,778 @@
+// C ABI of the REAL-Q layer sweep (declared in include/realq.h): argument checks,
+// workspace management, and the launch sequences of the five public calls.
+// Everything runs on the context's stream; the only host synchronisations are the
+// positive-definiteness check of realq_chol_inverse and the end of
+// realq_quantize_layer.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "kernels.h"
+#include "../../include/realq.h"
+
+// ============================================================================ context
+
+struct realq_ctx {
+    hipStream_t stream = nullptr;
+    int device = 0;
+    std::string err;
+    // grow-only workspaces, by slot name
+    struct Buf {
+        void* p = nullptr;
+        size_t bytes = 0;
+    };
+    std::map<std::string, Buf> ws;
+    // kernel timing
+    bool timing = false;
+    struct Stat {
+        int64_t launches = 0;
+        double ms = 0.0;
+    };
+    std::map<std::string, Stat> stats;
+    struct Pending {
+        std::string name;
+        hipEvent_t a, b;
+    };
+    std::vector<Pending> pending;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> free_events;
+};
+
+namespace realq {
+
+int set_error(realq_ctx* ctx, int code, const std::string& msg) {
+    if (ctx) ctx->err = msg;
+    return code;
+}
+
+static int get_ws(realq_ctx* ctx, const char* slot, size_t bytes, void** out) {
+    auto& b = ctx->ws[slot];
+    if (bytes == 0) bytes = 16;
+    if (b.bytes < bytes) {
+        if (b.p) {
+            hipError_t e = hipStreamSynchronize(ctx->stream);
+            if (e != hipSuccess) return set_error(ctx, REALQ_ERR_HIP, std::string("sync: ") + hipGetErrorString(e));
+            (void)hipFree(b.p);
+            b.p = nullptr;
+            b.bytes = 0;
+        }
+        void* p = nullptr;
+        if (hipMalloc(&p, bytes) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return set_error(ctx, REALQ_ERR_OOM,
+                             std::string("device allocation of ") + std::to_string(bytes) + " bytes for " + slot);
+        }
+        b.p = p;
+        b.bytes = bytes;
+    }
+    *out = b.p;
+    return REALQ_OK;
+}
+
+// RAII-free timing helper: begin/end bracket a launch on the context stream.
+struct Timed {
+    realq_ctx* ctx;
+    const char* name;
+    hipEvent_t a = nullptr, b = nullptr;
+    Timed(realq_ctx* c, const char* n) : ctx(c), name(n) {
+        if (!ctx->timing) return;
+        if (!ctx->free_events.empty()) {
+            a = ctx->free_events.back().first;
+            b = ctx->free_events.back().second;
+            ctx->free_events.pop_back();
+        } else {
+            if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+                a = b = nullptr;
+                return;
+            }
+        }
+        (void)hipEventRecord(a, ctx->stream);
+    }
+    ~Timed() {
+        if (!a) return;
+        (void)hipEventRecord(b, ctx->stream);
+        ctx->pending.push_back({name, a, b});
+    }
+};
+
+static int harvest(realq_ctx* ctx) {
+    if (ctx->pending.empty()) return REALQ_OK;
+    RQ_HIP(ctx, hipEventSynchronize(ctx->pending.back().b));
+    for (auto& p : ctx->pending) {
+        float ms = 0.f;
+        RQ_HIP(ctx, hipEventElapsedTime(&ms, p.a, p.b));
+        auto& s = ctx->stats[p.name];
+        s.launches += 1;
+        s.ms += ms;
+        ctx->free_events.push_back({p.a, p.b});
+    }
+    ctx->pending.clear();
+    return REALQ_OK;
+}
+
+}  // namespace realq
+
+using realq::get_ws;
+using realq::set_error;
+using realq::Timed;
+
+// ============================================================================ BGD state
+
+struct realq_bgd_state {
+    realq_ctx* ctx = nullptr;
+    int64_t m = 0, n = 0, T = 0, Tc = 0;
+    const float* W0 = nullptr;
+    const uint16_t* X = nullptr;
+    const uint16_t* Xhat = nullptr;
+    const float* s = nullptr;
+    const float* M = nullptr;
+    const float* P = nullptr;
+    realq_bgd_params prm{};
+    int64_t t = 0;  // Adam step counter (one per module)
+    int64_t locked = 0;  // columns [0, locked) are folded into the residual base
+    bool owns = true;
+    float* B = nullptr;  // [m,T] residual base
+    float* mA = nullptr;
+    float* vA = nullptr;  // [m,n]
+    uint16_t* Dhi = nullptr;
+    uint16_t* Dlo = nullptr;  // [m,n] split(W - W0)
+    uint16_t* XhT = nullptr;  // [n,T]
+    uint16_t* Rhi = nullptr;
+    uint16_t* Rlo = nullptr;  // [m,Tc]
+    std::vector<void*> allocations;
+};
+
+extern "C" {
+
+void realq_qparams_default(realq_qparams* q) {
+    if (!q) return;
+    q->bits = 4;
+    q->group = 128;
+    q->block = 128;
+    q->grid = 80;
+    q->damp = 0.01f;
+}
+
+void realq_bgd_params_default(realq_bgd_params* b) {
+    if (!b) return;
+    b->steps = 0;
+    b->lr = 1e-3f;
+    b->beta1 = 0.9f;
+    b->beta2 = 0.999f;
+    b->eps = 1e-8f;
+    b->tok_chunk = 0;
+}
+
+int realq_ctx_create(realq_ctx** out, void* hip_stream) {
+    if (!out) return REALQ_ERR_INVALID_ARG;
+    *out = nullptr;
+    realq_ctx* c = new (std::nothrow) realq_ctx();
+    if (!c) return REALQ_ERR_OOM;
+    c->stream = (hipStream_t)hip_stream;
+    if (hipGetDevice(&c->device) != hipSuccess) {
+        (void)hipGetLastError();
+        delete c;
+        return REALQ_ERR_HIP;
+    }
+    *out = c;
+    return REALQ_OK;
+}
+
+void realq_ctx_destroy(realq_ctx* ctx) {
+    if (!ctx) return;
+    (void)hipStreamSynchronize(ctx->stream);
+    for (auto& kv : ctx->ws)
+        if (kv.second.p) (void)hipFree(kv.second.p);
+    for (auto& p : ctx->pending) {
+        (void)hipEventDestroy(p.a);
+        (void)hipEventDestroy(p.b);
+    }
+    for (auto& p : ctx->free_events) {
+        (void)hipEventDestroy(p.first);
+        (void)hipEventDestroy(p.second);
+    }
+    delete ctx;
+}
+
+const char* realq_last_error(const realq_ctx* ctx) { return ctx ? ctx->err.c_str() : "null context"; }
+
+int realq_ctx_set_timing(realq_ctx* ctx, int enable) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    ctx->timing = enable != 0;
+    return REALQ_OK;
+}
+
+static const char* kTimedNames[] = {"hessian", "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init"};
+
+int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms) {
+    if (!ctx || !name) return REALQ_ERR_INVALID_ARG;
+    bool known = false;
+    for (const char* k : kTimedNames) known |= std::strcmp(k, name) == 0;
+    if (!known) return set_error(ctx, REALQ_ERR_INVALID_ARG, std::string("unknown kernel name ") + name);
+    int rc = realq::harvest(ctx);
+    if (rc) return rc;
+    auto it = ctx->stats.find(name);
+    if (launches) *launches = it == ctx->stats.end() ? 0 : it->second.launches;
+    if (total_ms) *total_ms = it == ctx->stats.end() ? 0.0 : it->second.ms;
+    return REALQ_OK;
+}
+
+int realq_ctx_reset_timing(realq_ctx* ctx) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    int rc = realq::harvest(ctx);
+    ctx->stats.clear();
+    return rc;
+}
+
+// ============================================================================ a1: Hessian
+
+int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat, const float* s, int64_t T, int64_t n, double* H_acc) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (T < 0 || n <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "hessian_accum: need T >= 0, n > 0");
+    if (T == 0) return REALQ_OK;
+    if (!Xhat || !H_acc) return set_error(ctx, REALQ_ERR_INVALID_ARG, "hessian_accum: NULL Xhat or H_acc");
+    // token chunk bounded so the transposed workspace stays near 256 MiB per operand
+    int64_t tc = (int64_t)(128ll << 20) / n;
+    tc = tc < 256 ? 256 : (tc / 256) * 256;
+    if (tc > T) tc = ((T + 7) / 8) * 8;
+    void *xt = nullptr, *hi = nullptr, *lo = nullptr;
+    int rc = get_ws(ctx, "h_xt", (size_t)n * tc * 2, &xt);
+    if (rc) return rc;
+    if (s) {
+        if ((rc = get_ws(ctx, "h_hi", (size_t)n * tc * 2, &hi))) return rc;
+        if ((rc = get_ws(ctx, "h_lo", (size_t)n * tc * 2, &lo))) return rc;
+    }
+    Timed tm(ctx, "hessian");
+    for (int64_t t0 = 0; t0 < T; t0 += tc) {
+        const int64_t cur = std::min(tc, T - t0);
+        RQ_HIP(ctx, realq::transpose_u16(Xhat + t0 * n, n, (uint16_t*)xt, tc, cur, n, ctx->stream));
+        realq::GemmArgs g{};
+        g.B = (const uint16_t*)xt;
+        g.ldb = tc;
+        g.M = n;
+        g.N = n;
+        g.K = cur;
+        g.lda = tc;
+        g.splits = 1;
+        if (s) {
+            RQ_HIP(ctx, realq::transpose_scale_split(Xhat + t0 * n, n, s + t0, (uint16_t*)hi, (uint16_t*)lo, tc, cur,
+                                                     n, ctx->stream));
+            g.Ahi = (const uint16_t*)hi;
+            g.Alo = (const uint16_t*)lo;
+        } else {
+            g.Ahi = (const uint16_t*)xt;
+            g.Alo = nullptr;
+        }
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, H_acc, n, ctx->stream));
+    }
+    return REALQ_OK;
+}
+
+// ============================================================================ a2: inverse factor
+
+int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T_total, float damp, float* H_out,
+                       float* U, uint8_t* dead) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (n <= 0 || T_total <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "chol_inverse: need n > 0 and T_total > 0");
+    if (!H_acc || !U) return set_error(ctx, REALQ_ERR_INVALID_ARG, "chol_inverse: NULL H_acc or U");
+    if (!(damp > 0.f) || !std::isfinite(damp))
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "chol_inverse: damp must be finite and > 0");
+    const int64_t np = ((n + 63) / 64) * 64;
+    void *A, *L, *D, *F, *S;
+    int rc;
+    if ((rc = get_ws(ctx, "c_A", (size_t)np * np * 8, &A))) return rc;
+    if ((rc = get_ws(ctx, "c_L", (size_t)np * np * 8, &L))) return rc;
+    if ((rc = get_ws(ctx, "c_D", (size_t)np * 64 * 8, &D))) return rc;
+    if ((rc = get_ws(ctx, "c_F", 64, &F))) return rc;
+    if ((rc = get_ws(ctx, "c_S", 64, &S))) return rc;
+    RQ_HIP(ctx, realq::fill_f64((double*)F, 0.0, 1, ctx->stream));  // flag word (int) cleared via a double fill
+    realq::CholArgs c{};
+    c.Hacc = H_acc;
+    c.n = n;
+    c.np = np;
+    c.scale = 2.0 / (double)T_total;
+    c.damp = damp;
+    c.Hout = H_out;
+    c.dead = dead;
+    c.A = (double*)A;
+    c.Linv = (double*)L;
+    c.diaginv = (double*)D;
+    c.flag = (int*)F;
+    c.scratch = (double*)S;
+    c.U = U;
+    {
+        Timed tm(ctx, "chol");
+        RQ_HIP(ctx, realq::chol_inverse(c, ctx->stream));
+    }
+    int flag = 0;
+    RQ_HIP(ctx, hipMemcpyAsync(&flag, F, sizeof(int), hipMemcpyDeviceToHost, ctx->stream));
+    RQ_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    if (flag) return set_error(ctx, REALQ_ERR_NOT_SPD, "chol_inverse: damped Hessian is not positive definite");
+    return REALQ_OK;
+}
+
+// ============================================================================ BGD state
+
+static int state_alloc(realq_bgd_state* st, void** p, size_t bytes, const char* slot) {
+    realq_ctx* ctx = st->ctx;
+    if (!st->owns) return get_ws(ctx, slot, bytes, p);
+    *p = nullptr;
+    if (hipMalloc(p, bytes ? bytes : 16) != hipSuccess || !*p) {
+        (void)hipGetLastError();
+        return set_error(ctx, REALQ_ERR_OOM, std::string("device allocation of ") + std::to_string(bytes) + " bytes");
+    }
+    st->allocations.push_back(*p);
+    return REALQ_OK;
+}
+
+static void state_free(realq_bgd_state* st) {
+    if (!st) return;
+    if (st->ctx) (void)hipStreamSynchronize(st->ctx->stream);
+    for (void* p : st->allocations) (void)hipFree(p);
+    st->allocations.clear();
+}
+
+static int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
+    if (!p) return set_error(ctx, REALQ_ERR_INVALID_ARG, "NULL bgd params");
+    if (p->steps < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd steps must be >= 0");
+    if (!std::isfinite(p->lr) || p->lr < 0.f) return set_error(ctx, REALQ_ERR_INVALID_ARG, "lr must be finite, >= 0");
+    if (!(p->beta1 >= 0.f && p->beta1 < 1.f) || !(p->beta2 >= 0.f && p->beta2 < 1.f))
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "Adam betas must lie in [0, 1)");
+    if (!(p->eps > 0.f)) return set_error(ctx, REALQ_ERR_INVALID_ARG, "Adam eps must be > 0");
+    if (p->tok_chunk < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "tok_chunk must be >= 0");
+    return REALQ_OK;
+}
+
+static int state_init(realq_bgd_state* st) {
+    realq_ctx* ctx = st->ctx;
+    const int64_t m = st->m, n = st->n, T = st->T;
+    hipStream_t s = ctx->stream;
+    int64_t Tc = st->prm.tok_chunk > 0 ? std::min<int64_t>(st->prm.tok_chunk, T) : T;
+    st->Tc = Tc;
+    int rc;
+    void* p;
+    if ((rc = state_alloc(st, &p, (size_t)m * T * 4, "s_B"))) return rc;
+    st->B = (float*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 4, "s_m"))) return rc;
+    st->mA = (float*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 4, "s_v"))) return rc;
+    st->vA = (float*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 2, "s_Dh"))) return rc;
+    st->Dhi = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 2, "s_Dl"))) return rc;
+    st->Dlo = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)n * T * 2, "s_XT"))) return rc;
+    st->XhT = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * Tc * 2, "s_Rh"))) return rc;
+    st->Rhi = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * Tc * 2, "s_Rl"))) return rc;
+    st->Rlo = (uint16_t*)p;
+
+    Timed tm(ctx, "init");
+    RQ_HIP(ctx, realq::fill_f32(st->mA, 0.f, m * n, s));
+    RQ_HIP(ctx, realq::fill_f32(st->vA, 0.f, m * n, s));
+    RQ_HIP(ctx, realq::transpose_u16(st->Xhat, n, st->XhT, T, T, n, s));
+    // Residual base before any block is locked: B = W0 (Xhat - X)^T.
+    if (st->X == st->Xhat) {
+        RQ_HIP(ctx, realq::fill_f32(st->B, 0.f, m * T, s));
+    } else {
+        // W0 = W0hi + W0lo (in the D buffers for now), Xhat - X = Dxh + Dxl (bf16 pairs, exact
+        // difference in float32 first): B = W0 Dxh^T (both halves of W0) + W0hi Dxl^T.
+        RQ_HIP(ctx, realq::split_diff_f32(st->W0, n, nullptr, 0, st->Dhi, st->Dlo, n, m, n, s));
+        const int64_t tcx = std::max<int64_t>(8, std::min<int64_t>(T, ((int64_t)(256ll << 20) / (2 * n) / 8) * 8));
+        void *xh, *xl;
+        if ((rc = get_ws(ctx, "i_xh", (size_t)tcx * n * 2, &xh))) return rc;
+        if ((rc = get_ws(ctx, "i_xl", (size_t)tcx * n * 2, &xl))) return rc;
+        for (int64_t t0 = 0; t0 < T; t0 += tcx) {
+            const int64_t cur = std::min(tcx, T - t0);
+            RQ_HIP(ctx, realq::split_diff_bf16(st->Xhat + t0 * n, st->X + t0 * n, (uint16_t*)xh, (uint16_t*)xl,
+                                               cur * n, s));
+            realq::GemmArgs g{st->Dhi, st->Dlo, n, (const uint16_t*)xh, n, m, cur, n, 1};
+            RQ_HIP(ctx, realq::gemm_store_f32(g, st->B + t0, T, 0, 1.f, s));
+            realq::GemmArgs g2{st->Dhi, nullptr, n, (const uint16_t*)xl, n, m, cur, n, 1};
+            RQ_HIP(ctx, realq::gemm_acc_f32(g2, st->B + t0, T, 1.f, s));
+        }
+    }
+    RQ_HIP(ctx, realq::fill_u16(st->Dhi, 0, m * n, s));
+    RQ_HIP(ctx, realq::fill_u16(st->Dlo, 0, m * n, s));
+    st->t = 0;
+    st->locked = 0;
+    return REALQ_OK;
+}
+
+static int check_state_args(realq_ctx* ctx, const float* W0, const uint16_t* X, const uint16_t* Xhat, int64_t m,
+                            int64_t n, int64_t T, const realq_bgd_params* params) {
+    if (m <= 0 || n <= 0 || T <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "bgd state: need m, n, T > 0");
+    if (!W0 || !X || !Xhat) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd state: NULL W0, X or Xhat");
+    return validate_bgd(ctx, params);
+}
+
+int realq_bgd_state_create(realq_ctx* ctx, realq_bgd_state** out, const float* W0, const uint16_t* X,
+                           const uint16_t* Xhat, const float* s, const float* M, const float* P, int64_t m, int64_t n,
+                           int64_t T, const realq_bgd_params* params) {
+    if (!ctx || !out) return REALQ_ERR_INVALID_ARG;
+    *out = nullptr;
+    int rc = check_state_args(ctx, W0, X, Xhat, m, n, T, params);
+    if (rc) return rc;
+    realq_bgd_state* st = new (std::nothrow) realq_bgd_state();
+    if (!st) return set_error(ctx, REALQ_ERR_OOM, "host allocation");
+    st->ctx = ctx;
+    st->m = m;
+    st->n = n;
+    st->T = T;
+    st->W0 = W0;
+    st->X = X;
+    st->Xhat = Xhat;
+    st->s = s;
+    st->M = M;
+    st->P = P;
+    st->prm = *params;
+    st->owns = true;
+    rc = state_init(st);
+    if (rc) {
+        state_free(st);
+        delete st;
+        return rc;
+    }
+    *out = st;
+    return REALQ_OK;
+}
+
+void realq_bgd_state_destroy(realq_bgd_state* st) {
+    if (!st) return;
+    state_free(st);
+    delete st;
+}
+
+// ============================================================================ a3-a6: one column block
+
+static int validate_q(realq_ctx* ctx, const realq_qparams* qp) {
+    if (!qp) return set_error(ctx, REALQ_ERR_INVALID_ARG, "NULL qparams");
+    if (qp->bits < 2 || qp->bits > 4) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bits must be 2, 3 or 4");
+    if (qp->group < 1) return set_error(ctx, REALQ_ERR_INVALID_ARG, "group must be >= 1");
+    if (qp->block < 1 || qp->block > 128) return set_error(ctx, REALQ_ERR_INVALID_ARG, "block must be in 1..128");
+    if (qp->grid < 1 || qp->grid > 100) return set_error(ctx, REALQ_ERR_INVALID_ARG, "grid must be in 1..100");
+    if (qp->block % qp->group != 0 && qp->group % qp->block != 0)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "block and group must divide one another");
+    if (!(qp->damp > 0.f) || !std::isfinite(qp->damp))
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "damp must be finite and > 0");
+    return REALQ_OK;
+}
+
+int realq_quantize_block(realq_ctx* ctx, float* W, int64_t m, int64_t n, int64_t c0, int64_t bs, const float* U,
+                         const uint8_t* dead, const realq_qparams* qp, uint8_t* codes, float* scales, uint8_t* zeros,
+                         realq_bgd_state* st) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    int rc = validate_q(ctx, qp);
+    if (rc) return rc;
+    if (m <= 0 || n <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: need m, n > 0");
+    if (c0 < 0 || bs < 1 || bs > 128 || c0 + bs > n)
+        return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: need 0 <= c0, 1 <= bs <= 128, c0 + bs <= n");
+    if (c0 % qp->block != 0 || (bs != qp->block && c0 + bs != n))
+        return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: the block must be a whole column block of the sweep");
+    if (!W || !U || !codes || !scales || !zeros)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_block: NULL W, U, codes, scales or zeros");
+    if (st && (st->m != m || st->n != n))
+        return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: state shape differs from W");
+    void* E;
+    if ((rc = get_ws(ctx, "q_E", (size_t)m * bs * 4, &E))) return rc;
+    hipStream_t s = ctx->stream;
+    realq::QuantArgs q{};
+    q.W = W;
+    q.m = m;
+    q.n = n;
+    q.c0 = c0;
+    q.bs = bs;
+    q.U = U;
+    q.dead = dead;
+    q.bits = qp->bits;
+    q.group = qp->group;
+    q.grid = qp->grid;
+    q.codes = codes;
+    q.scales = scales;
+    q.zeros = zeros;
+    q.ngroups = (n + qp->group - 1) / qp->group;
+    q.E = (float*)E;
+    q.W0 = st ? st->W0 : nullptr;
+    q.Dhi = st ? st->Dhi : nullptr;
+    q.Dlo = st ? st->Dlo : nullptr;
+    {
+        Timed tm(ctx, "quantize");
+        RQ_HIP(ctx, realq::quantize_block(q, s));
+    }
+    const int64_t c1 = c0 + bs;
+    if (c1 < n) {
+        realq::SgemmArgs a{};
+        a.A = (const float*)E;
+        a.lda = bs;
+        a.B = U + c0 * n + c1;
+        a.ldb = n;
+        a.C = W + c1;
+        a.ldc = n;
+        a.M = m;
+        a.N = n - c1;
+        a.K = bs;
+        a.alpha = -1.f;
+        a.beta = 1.f;
+        if (st) {
+            a.W0 = st->W0 + c1;
+            a.ldw = n;
+            a.Dhi = st->Dhi + c1;
+            a.Dlo = st->Dlo + c1;
+            a.ldd = n;
+        }
+        Timed tm(ctx, "obs");
+        RQ_HIP(ctx, realq::sgemm(a, s));
+    }
+    if (st) {
+        // lock: B += (W_hat - W0)[:, block] Xhat[:, block]^T
+        realq::GemmArgs g{st->Dhi + c0, st->Dlo + c0, n, st->Xhat + c0, n, m, st->T, bs, 1};
+        Timed tm(ctx, "lock");
+        RQ_HIP(ctx, realq::gemm_acc_f32(g, st->B, st->T, 1.f, s));
+        st->locked = c1;
+    }
+    return REALQ_OK;
+}
+
+// ============================================================================ a7-a9: one BGD step
+
+static int64_t choose_splits(int64_t M, int64_t N, int64_t K) {
+    const int64_t blocks = realq::gemm_num_blocks(M, N);
+    int64_t s = (1024 + blocks - 1) / blocks;
+    int64_t kmax = K / 256;  // keep at least 256 tokens per split
+    if (s > kmax) s = kmax;
+    if (s > 64) s = 64;
+    return s < 1 ? 1 : s;
+}
+
+int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, float* W, int64_t c1, float alpha, double* loss_out) {
+    if (!ctx || !st) return REALQ_ERR_INVALID_ARG;
+    if (!W) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_step: NULL W");
+    if (c1 < 0 || c1 > st->n) return set_error(ctx, REALQ_ERR_SHAPE, "bgd_step: need 0 <= c1 <= n");
+    if (!std::isfinite(alpha) || alpha < 0.f || alpha > 1.f)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_step: alpha must lie in [0, 1]");
+    const int64_t m = st->m, n = st->n, T = st->T, Tc = st->Tc, nJ = n - c1;
+    hipStream_t s = ctx->stream;
+    if (nJ == 0) {
+        if (loss_out) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
+        return REALQ_OK;
+    }
+    const bool dense = st->M || (st->P && alpha < 1.f);
+    const int64_t nchunks = (T + Tc - 1) / Tc;
+    const int64_t S = choose_splits(m, nJ, Tc);
+    const int64_t Seff = realq::gemm_effective_splits(Tc, S);
+    int rc;
+    void *Gp, *Gacc = nullptr, *parts;
+    if ((rc = get_ws(ctx, "b_Gp", (size_t)Seff * m * nJ * 4, &Gp))) return rc;
+    if (nchunks > 1 || dense)
+        if ((rc = get_ws(ctx, "b_G", (size_t)m * nJ * 4, &Gacc))) return rc;
+    const int64_t kblocks = realq::gemm_num_blocks(m, Tc);
+    if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
+    RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, s));  // shorter last chunk writes fewer
+
+    int64_t splits_used = Seff;
+    for (int64_t ch = 0; ch < nchunks; ++ch) {
+        const int64_t t0 = ch * Tc, cur = std::min(Tc, T - t0);
+        {
+            realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
+            Timed tm(ctx, "resid");
+            RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, st->Rlo, cur,
+                                          (double*)parts + ch * kblocks, s));
+        }
+        {
+            realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, S};
+            splits_used = realq::gemm_effective_splits(cur, S);
+            Timed tm(ctx, "grad");
+            RQ_HIP(ctx, realq::gemm_store_f32(g, (float*)Gp, nJ, m * nJ, 1.f, s));
+        }
+        if (nchunks > 1 || dense) {
+            // Gacc (+)= sum of this chunk's split slices, chunks in order
+            RQ_HIP(ctx, realq::reduce_splits((const float*)Gp, splits_used, m, nJ, 1.f, (float*)Gacc, ch > 0, s));
+        }
+    }
+    if (loss_out) {
+        if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
+        else RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)T, loss_out, s));
+    }
+    st->t += 1;
+    realq::AdamArgs a{};
+    a.W = W;
+    a.W0 = st->W0;
+    a.mA = st->mA;
+    a.vA = st->vA;
+    a.Dhi = st->Dhi;
+    a.Dlo = st->Dlo;
+    a.m = m;
+    a.n = n;
+    a.c1 = c1;
+    a.Gp = (const float*)Gp;
+    a.splits = splits_used;
+    a.gscale = (float)(1.0 / (double)T);
+    a.lr = st->prm.lr;
+    a.beta1 = st->prm.beta1;
+    a.beta2 = st->prm.beta2;
+    a.eps = st->prm.eps;
+    a.bc1 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta1, (double)st->t)));
+    a.bc2 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta2, (double)st->t)));
+    Timed tm(ctx, "adam");
+    if (!dense && nchunks == 1) {
+        RQ_HIP(ctx, realq::adam_update(a, s));
+    } else if (!dense) {
+        a.Gp = (const float*)Gacc;
+        a.splits = 1;
+        RQ_HIP(ctx, realq::adam_update(a, s));
+    } else {
+        // G = (1/T) (alpha M + (1 - alpha) P) Gacc
+        void* Gm;
+        if ((rc = get_ws(ctx, "b_Gm", (size_t)m * nJ * 4, &Gm))) return rc;
+        realq::SgemmArgs sg{};
+        sg.B = (const float*)Gacc;
+        sg.ldb = nJ;
+        sg.C = (float*)Gm;
+        sg.ldc = nJ;
+        sg.M = m;
+        sg.N = nJ;
+        sg.K = m;
+        const float invT = (float)(1.0 / (double)T);
+        bool first = true;
+        if (alpha > 0.f) {
+            if (st->M) {
+                sg.A = st->M;
+                sg.lda = m;
+                sg.alpha = alpha * invT;
+                sg.beta = 0.f;
+                RQ_HIP(ctx, realq::sgemm(sg, s));
+            } else {
+                // identity metric: Gm = alpha/T * Gacc
+                RQ_HIP(ctx, realq::reduce_splits((const float*)Gacc, 1, m, nJ, alpha * invT, (float*)Gm, false, s));
+            }
+            first = false;
+        }
+        if (st->P && alpha < 1.f) {
+            sg.A = st->P;
+            sg.lda = m;
+            sg.alpha = (1.f - alpha) * invT;
+            sg.beta = first ? 0.f : 1.f;
+            RQ_HIP(ctx, realq::sgemm(sg, s));
+        }
+        RQ_HIP(ctx, realq::adam_update_dense(a, (const float*)Gm, s));
+    }
+    return REALQ_OK;
+}
+
+int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const float* W, double* loss_out) {
+    if (!ctx || !st) return REALQ_ERR_INVALID_ARG;
+    if (!W || !loss_out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_loss: NULL W or loss_out");
+    if (st->M) return set_error(ctx, REALQ_ERR_SHAPE, "bgd_loss: only the identity metric is supported");
+    // R = B + (W - W0)[:, J] Xhat[:, J]^T with J the columns not yet folded into B.
+    const int64_t m = st->m, T = st->T, Tc = st->Tc, n = st->n, c1 = st->locked, nJ = n - c1;
+    const int64_t nchunks = (T + Tc - 1) / Tc;
+    const int64_t kblocks = realq::gemm_num_blocks(m, Tc);
+    void* parts;
+    int rc;
+    if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
+    RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, ctx->stream));
+    if (nJ > 0) RQ_HIP(ctx, realq::split_diff_f32(W + c1, n, st->W0 + c1, n, st->Dhi + c1, st->Dlo + c1, n, m, nJ,
+                                                  ctx->stream));
+    for (int64_t ch = 0; ch < nchunks; ++ch) {
+        const int64_t t0 = ch * Tc, cur = std::min(Tc, T - t0);
+        realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
+        RQ_HIP(ctx, realq::gemm_loss(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, (double*)parts + ch * kblocks,
+                                     ctx->stream));
+    }
+    RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)T, loss_out, ctx->stream));
+    return REALQ_OK;
+}
+
+// ============================================================================ a1-a11: whole module
+
+int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_out* out) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (!d || !out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_layer: NULL desc or out");
+    int rc = validate_q(ctx, &d->q);
+    if (rc) return rc;
+    if ((rc = check_state_args(ctx, d->W0, d->X, d->Xhat, d->m, d->n, d->T, &d->bgd))) return rc;
+    if (!out->codes || !out->scales || !out->zeros || !out->W_hat)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_layer: NULL codes, scales, zeros or W_hat");
+    const int64_t m = d->m, n = d->n, T = d->T;
+    hipStream_t s = ctx->stream;
+    hipEvent_t ev0, ev1;
+    RQ_HIP(ctx, hipEventCreate(&ev0));
+    RQ_HIP(ctx, hipEventCreate(&ev1));
+    RQ_HIP(ctx, hipEventRecord(ev0, s));
+
+    // a1: Hessian
+    void *Hacc, *Uw = out->U, *deadw = out->dead;
+    if ((rc = get_ws(ctx, "l_H", (size_t)n * n * 8, &Hacc))) return rc;
+    if (!Uw && (rc = get_ws(ctx, "l_U", (size_t)n * n * 4, &Uw))) return rc;
+    if (!deadw && (rc = get_ws(ctx, "l_dead", (size_t)n, &deadw))) return rc;
+    RQ_HIP(ctx, realq::fill_f64((double*)Hacc, 0.0, n * n, s));
+    if ((rc = realq_hessian_accum(ctx, d->Xhat, d->s, T, n, (double*)Hacc))) return rc;
+    // a2: inverse factor (synchronises once)
+    if ((rc = realq_chol_inverse(ctx, (const double*)Hacc, n, T, d->q.damp, out->H, (float*)Uw, (uint8_t*)deadw)))
+        return rc;
+
+    // state on context workspaces (reused across calls of the same size)
+    realq_bgd_state st;
+    st.ctx = ctx;
+    st.m = m;
+    st.n = n;
+    st.T = T;
+    st.W0 = d->W0;
+    st.X = d->X;
+    st.Xhat = d->Xhat;
+    st.s = d->s;
+    st.M = d->M;
+    st.P = d->P;
+    st.prm = d->bgd;
+    st.owns = false;
+    const bool bgd = d->bgd.steps > 0;
+    if (bgd && (rc = state_init(&st))) return rc;
+
+    RQ_HIP(ctx, hipMemcpyAsync(out->W_hat, d->W0, (size_t)m * n * 4, hipMemcpyDeviceToDevice, s));
+    const int64_t nb = (n + d->q.block - 1) / d->q.block;
+    if (out->loss_trace && bgd) RQ_HIP(ctx, realq::fill_f64(out->loss_trace, NAN, nb * d->bgd.steps, s));
+    for (int64_t b = 0; b < nb; ++b) {
+        const int64_t c0 = b * d->q.block, bs = std::min<int64_t>(d->q.block, n - c0), c1 = c0 + bs;
+        if ((rc = realq_quantize_block(ctx, out->W_hat, m, n, c0, bs, (const float*)Uw, (const uint8_t*)deadw, &d->q,
+                                       out->codes, out->scales, out->zeros, bgd ? &st : nullptr)))
+            return rc;
+        if (!bgd || c1 >= n) continue;
+        float alpha = 1.f;
+        if (d->window_total > 1) {
+            const double bg = (double)(d->window_offset + b + 1);
+            alpha = (float)(1.0 - (bg - 1.0) / (double)(d->window_total - 1));
+            alpha = std::min(1.f, std::max(0.f, alpha));
+        }
+        for (int k = 0; k < d->bgd.steps; ++k) {
+            double* lo = out->loss_trace ? out->loss_trace + b * d->bgd.steps + k : nullptr;
+            if ((rc = realq_bgd_step(ctx, &st, out->W_hat, c1, alpha, lo))) return rc;
+        }
+    }
+    // a11: final loss (own metric) at the quantized weights
+    out->loss_final = NAN;
+    void* lf;
+    if ((rc = get_ws(ctx, "l_loss", 8, &lf))) return rc;
+    if (!d->M) {
+        if (!bgd) {
+            // no state yet: build the residual base once for the loss
+            st.prm.tok_chunk = d->bgd.tok_chunk;
+            if ((rc = state_init(&st))) return rc;
+        }
+        if ((rc = realq_bgd_loss(ctx, &st, out->W_hat, (double*)lf))) return rc;
+    }
+    RQ_HIP(ctx, hipEventRecord(ev1, s));
+    if (!d->M) RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lf, 8, hipMemcpyDeviceToHost, s));
+    RQ_HIP(ctx, hipStreamSynchronize(s));
+    float ms = 0.f;
+    RQ_HIP(ctx, hipEventElapsedTime(&ms, ev0, ev1));
+    out->ms_total = ms;
+    (void)hipEventDestroy(ev0);
+    (void)hipEventDestroy(ev1);
+    return realq::harvest(ctx);
+}
+
+}  // extern "C"

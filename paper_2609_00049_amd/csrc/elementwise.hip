@@ -1,0 +1,233 @@
+// Memory-bound helper kernels: fills, bf16 transposes and splits, deterministic
+// reductions and the fused split-K reduction + Adam update (Appendix D.1 constants
+// arrive as arguments).  Every kernel here is HBM-bound; loops are grid-strided
+// with coalesced rows.
+#include "common.h"
+#include "kernels.h"
+
+namespace realq {
+
+namespace {
+constexpr int TB = 256;
+inline unsigned grid_for(int64_t count, int per_thread = 1) {
+    int64_t b = (count + (int64_t)TB * per_thread - 1) / ((int64_t)TB * per_thread);
+    if (b < 1) b = 1;
+    if (b > 65536) b = 65536;
+    return (unsigned)b;
+}
+}  // namespace
+
+template <class T>
+__global__ void fill_kernel(T* p, T v, int64_t count) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+hipError_t fill_f32(float* p, float v, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_kernel<float>, dim3(grid_for(count, 4)), dim3(TB), 0, st, p, v, count);
+    return hipGetLastError();
+}
+hipError_t fill_f64(double* p, double v, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_kernel<double>, dim3(grid_for(count, 4)), dim3(TB), 0, st, p, v, count);
+    return hipGetLastError();
+}
+hipError_t fill_u16(uint16_t* p, uint16_t v, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_kernel<uint16_t>, dim3(grid_for(count, 4)), dim3(TB), 0, st, p, v, count);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- tiled transposes (64 x 64 tiles via LDS)
+// MODE 0: plain copy of bit patterns; MODE 1: value s[r] * x, written as a hi/lo bf16 pair.
+template <int MODE>
+__global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restrict__ in, int64_t ldi,
+                                                        const float* __restrict__ s, uint16_t* __restrict__ o1,
+                                                        uint16_t* __restrict__ o2, int64_t ldo, int64_t rows,
+                                                        int64_t cols, int64_t tiles_c) {
+    __shared__ float tile[64][65];
+    const int64_t tr = blockIdx.x / tiles_c, tc = blockIdx.x % tiles_c;
+    const int64_t r0 = tr * 64, c0 = tc * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 4 rows of 64 threads
+    for (int rr = ty; rr < 64; rr += 4) {
+        int64_t r = r0 + rr, c = c0 + tx;
+        float v = 0.f;
+        if (r < rows && c < cols) {
+            v = bf2f(in[r * ldi + c]);
+            if (MODE == 1 && s) v *= s[r];
+        }
+        tile[rr][tx] = v;
+    }
+    __syncthreads();
+    for (int cc = ty; cc < 64; cc += 4) {
+        int64_t c = c0 + cc, r = r0 + tx;
+        if (r < rows && c < cols) {
+            float v = tile[tx][cc];
+            if (MODE == 0) {
+                o1[c * ldo + r] = f2bf(v);  // exact: v is a bf16 value
+            } else {
+                uint16_t hi, lo;
+                split_bf16(v, hi, lo);
+                o1[c * ldo + r] = hi;
+                o2[c * ldo + r] = lo;
+            }
+        }
+    }
+}
+
+hipError_t transpose_u16(const uint16_t* in, int64_t ldi, uint16_t* out, int64_t ldo, int64_t rows, int64_t cols,
+                         hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    int64_t tr = (rows + 63) / 64, tc = (cols + 63) / 64;
+    hipLaunchKernelGGL(transpose_kernel<0>, dim3((unsigned)(tr * tc)), dim3(256), 0, st, in, ldi, nullptr, out,
+                       nullptr, ldo, rows, cols, tc);
+    return hipGetLastError();
+}
+
+hipError_t transpose_scale_split(const uint16_t* in, int64_t ldi, const float* s, uint16_t* hi, uint16_t* lo,
+                                 int64_t ldo, int64_t rows, int64_t cols, hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    int64_t tr = (rows + 63) / 64, tc = (cols + 63) / 64;
+    hipLaunchKernelGGL(transpose_kernel<1>, dim3((unsigned)(tr * tc)), dim3(256), 0, st, in, ldi, s, hi, lo, ldo,
+                       rows, cols, tc);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- splits
+__global__ void split_diff_f32_kernel(const float* __restrict__ A, int64_t lda, const float* __restrict__ Bm,
+                                      int64_t ldb, uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, int64_t ld,
+                                      int64_t rows, int64_t cols) {
+    const int64_t total = rows * cols;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int64_t i = e / cols, j = e % cols;
+        float v = A[i * lda + j];
+        if (Bm) v -= Bm[i * ldb + j];
+        uint16_t h, l;
+        split_bf16(v, h, l);
+        hi[i * ld + j] = h;
+        lo[i * ld + j] = l;
+    }
+}
+
+hipError_t split_diff_f32(const float* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
+                          int64_t ld, int64_t rows, int64_t cols, hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    hipLaunchKernelGGL(split_diff_f32_kernel, dim3(grid_for(rows * cols, 4)), dim3(TB), 0, st, A, lda, Bm, ldb, hi, lo,
+                       ld, rows, cols);
+    return hipGetLastError();
+}
+
+__global__ void split_diff_bf16_kernel(const uint16_t* __restrict__ a, const uint16_t* __restrict__ b,
+                                       uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, int64_t count) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x) {
+        float v = bf2f(a[e]) - bf2f(b[e]);  // exact in float32 for bf16 inputs of similar magnitude
+        uint16_t h, l;
+        split_bf16(v, h, l);
+        hi[e] = h;
+        lo[e] = l;
+    }
+}
+
+hipError_t split_diff_bf16(const uint16_t* a, const uint16_t* b, uint16_t* hi, uint16_t* lo, int64_t count,
+                           hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(split_diff_bf16_kernel, dim3(grid_for(count, 4)), dim3(TB), 0, st, a, b, hi, lo, count);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- deterministic reduction
+__global__ __launch_bounds__(256) void reduce_partials_kernel(const double* __restrict__ p, int64_t count,
+                                                              double scale, double* out) {
+    __shared__ double red[256];
+    double acc = 0.0;
+    for (int64_t i = threadIdx.x; i < count; i += 256) acc += p[i];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *out = red[0] * scale;
+}
+
+hipError_t reduce_partials(const double* partials, int64_t count, double scale, double* out, hipStream_t st) {
+    hipLaunchKernelGGL(reduce_partials_kernel, dim3(1), dim3(256), 0, st, partials, count, scale, out);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- split-K reduction + Adam
+// Bias-corrected Adam in the Kingma-Ba form: m = b1 m + (1-b1) g, v = b2 v + (1-b2) g^2,
+// w -= lr * (m * bc1) / (sqrt(v * bc2) + eps).
+__device__ __forceinline__ void adam_elem(const AdamArgs& a, int64_t i, int64_t j, float g) {
+    const int64_t idx = i * a.n + j;
+    float mv = a.beta1 * a.mA[idx] + (1.f - a.beta1) * g;
+    float vv = a.beta2 * a.vA[idx] + (1.f - a.beta2) * g * g;
+    a.mA[idx] = mv;
+    a.vA[idx] = vv;
+    float mh = mv * a.bc1;
+    float vh = vv * a.bc2;
+    float w = a.W[idx] - a.lr * mh / (sqrtf(vh) + a.eps);
+    a.W[idx] = w;
+    uint16_t h, l;
+    split_bf16(w - a.W0[idx], h, l);
+    a.Dhi[idx] = h;
+    a.Dlo[idx] = l;
+}
+
+__global__ void adam_kernel(AdamArgs a) {
+    const int64_t w = a.n - a.c1;
+    const int64_t total = a.m * w;
+    const int64_t zstride = a.m * w;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        float g = 0.f;
+        for (int64_t z = 0; z < a.splits; ++z) g += a.Gp[z * zstride + e];
+        g *= a.gscale;
+        int64_t i = e / w, j = a.c1 + e % w;
+        adam_elem(a, i, j, g);
+    }
+}
+
+hipError_t adam_update(const AdamArgs& a, hipStream_t st) {
+    const int64_t total = a.m * (a.n - a.c1);
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(adam_kernel, dim3(grid_for(total, 4)), dim3(TB), 0, st, a);
+    return hipGetLastError();
+}
+
+__global__ void adam_dense_kernel(AdamArgs a, const float* __restrict__ G) {
+    const int64_t w = a.n - a.c1;
+    const int64_t total = a.m * w;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int64_t i = e / w, j = a.c1 + e % w;
+        adam_elem(a, i, j, G[e]);
+    }
+}
+
+hipError_t adam_update_dense(const AdamArgs& a, const float* G, hipStream_t st) {
+    const int64_t total = a.m * (a.n - a.c1);
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(adam_dense_kernel, dim3(grid_for(total, 4)), dim3(TB), 0, st, a, G);
+    return hipGetLastError();
+}
+
+__global__ void reduce_splits_kernel(const float* __restrict__ Gp, int64_t splits, int64_t total, float gscale,
+                                     float* __restrict__ G, int accumulate) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        float g = 0.f;
+        for (int64_t z = 0; z < splits; ++z) g += Gp[z * total + e];
+        g *= gscale;
+        G[e] = accumulate ? G[e] + g : g;
+    }
+}
+
+hipError_t reduce_splits(const float* Gp, int64_t splits, int64_t m, int64_t w, float gscale, float* G,
+                         bool accumulate, hipStream_t st) {
+    const int64_t total = m * w;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(total, 4)), dim3(TB), 0, st, Gp, splits, total, gscale, G,
+                       (int)accumulate);
+    return hipGetLastError();
+}
+
+}  // namespace realq

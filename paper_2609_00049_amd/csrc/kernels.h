@@ -1,0 +1,127 @@
+// Internal launchers of the REAL-Q gfx950 library (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace realq {
+
+// ---------------------------------------------------------------- bf16 MFMA NT GEMM
+// acc[i][j] = sum_k (Ahi[i*lda+k] + Alo[i*lda+k]) * B[j*ldb+k], i < M, j < N, k < K;
+// Alo may be NULL.  splits > 1 partitions K into equal BK-aligned ranges (gridDim.z).
+struct GemmArgs {
+    const uint16_t* Ahi;
+    const uint16_t* Alo;
+    int64_t lda;
+    const uint16_t* B;
+    int64_t ldb;
+    int64_t M, N, K;
+    int64_t splits;
+};
+int64_t gemm_effective_splits(int64_t K, int64_t splits);
+int64_t gemm_num_blocks(int64_t M, int64_t N);
+hipError_t gemm_store_f32(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, float alpha, hipStream_t st);
+hipError_t gemm_acc_f32(const GemmArgs& g, float* C, int64_t ldc, float alpha, hipStream_t st);
+hipError_t gemm_acc_f64(const GemmArgs& g, double* C, int64_t ldc, hipStream_t st);
+hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
+                      int64_t ldr, double* partials, hipStream_t st);
+hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
+                     hipStream_t st);
+hipError_t gemm_store_bf16_t(const GemmArgs& g, uint16_t* out, int64_t ld, hipStream_t st);
+
+// ---------------------------------------------------------------- elementwise / layout
+hipError_t fill_f32(float* p, float v, int64_t count, hipStream_t st);
+hipError_t fill_f64(double* p, double v, int64_t count, hipStream_t st);
+hipError_t fill_u16(uint16_t* p, uint16_t v, int64_t count, hipStream_t st);
+// out[c*ldo + r] = in[r*ldi + c] for r < rows, c < cols (bf16 bit patterns)
+hipError_t transpose_u16(const uint16_t* in, int64_t ldi, uint16_t* out, int64_t ldo, int64_t rows, int64_t cols,
+                         hipStream_t st);
+// Transposed, weighted split: hi/lo[c*ldo + r] = split(s[r] * bf16(in[r*ldi + c]))   (s may be NULL)
+hipError_t transpose_scale_split(const uint16_t* in, int64_t ldi, const float* s, uint16_t* hi, uint16_t* lo,
+                                 int64_t ldo, int64_t rows, int64_t cols, hipStream_t st);
+// hi/lo[i*ld + j] = split(A[i*lda + j] - (Bm ? Bm[i*ldb + j] : 0)) for j < cols (float32 inputs)
+hipError_t split_diff_f32(const float* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
+                          int64_t ld, int64_t rows, int64_t cols, hipStream_t st);
+// hi/lo[i] = split(bf16(a[i]) - bf16(b[i]))
+hipError_t split_diff_bf16(const uint16_t* a, const uint16_t* b, uint16_t* hi, uint16_t* lo, int64_t count,
+                           hipStream_t st);
+// out = sum of partials (fixed order) * scale, written to *out (device)
+hipError_t reduce_partials(const double* partials, int64_t count, double scale, double* out, hipStream_t st);
+// Adam on W[:, c1:n] with G = gscale * sum_z Gp[z][i][j - c1]; refreshes Dhi/Dlo = split(W - W0) there.
+struct AdamArgs {
+    float* W;
+    const float* W0;
+    float* mA;
+    float* vA;
+    uint16_t* Dhi;
+    uint16_t* Dlo;
+    int64_t m, n, c1;
+    const float* Gp;  // [splits][m][n - c1]
+    int64_t splits;
+    float gscale, lr, beta1, beta2, eps, bc1, bc2;  // bc1 = 1/(1-beta1^t), bc2 = 1/(1-beta2^t)
+};
+hipError_t adam_update(const AdamArgs& a, hipStream_t st);
+// G[i][j] = (accumulate ? G[i][j] : 0) + gscale * sum_z Gp[z][i][j]  (m x w), z in order
+hipError_t reduce_splits(const float* Gp, int64_t splits, int64_t m, int64_t w, float gscale, float* G,
+                         bool accumulate, hipStream_t st);
+// Adam with a ready gradient G (m x (n-c1)).
+hipError_t adam_update_dense(const AdamArgs& a, const float* G, hipStream_t st);
+
+// ---------------------------------------------------------------- fp32 GEMM (VALU): C = beta*C + alpha*A*B
+// A [M,K] lda, B [K,N] ldb, C [M,N] ldc, all float32 row-major.  Optional split of the
+// result: when Dhi != NULL, also Dhi/Dlo[i*ldd + j] = split(C[i][j] - W0[i*ldw + j]).
+struct SgemmArgs {
+    const float* A;
+    int64_t lda;
+    const float* B;
+    int64_t ldb;
+    float* C;
+    int64_t ldc;
+    int64_t M, N, K;
+    float alpha, beta;
+    const float* W0;
+    int64_t ldw;
+    uint16_t* Dhi;
+    uint16_t* Dlo;
+    int64_t ldd;
+};
+hipError_t sgemm(const SgemmArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- quantize one column block
+struct QuantArgs {
+    float* W;
+    int64_t m, n, c0, bs;
+    const float* U;
+    const uint8_t* dead;
+    int bits, group, grid;
+    uint8_t* codes;
+    float* scales;
+    uint8_t* zeros;
+    int64_t ngroups;
+    float* E;  // [m][bs]
+    const float* W0;  // may be NULL (no split written)
+    uint16_t* Dhi;
+    uint16_t* Dlo;
+};
+hipError_t quantize_block(const QuantArgs& q, hipStream_t st);
+
+// ---------------------------------------------------------------- float64 factorisation
+// Prepares A = J (H + lambda I) J (index-reversed, padded to np with identity) from H_acc,
+// writes H_out and dead; lambda computed on device.  Then Cholesky + triangular inverse.
+struct CholArgs {
+    const double* Hacc;
+    int64_t n, np;
+    double scale;  // 2 / T_total
+    double damp;
+    float* Hout;
+    uint8_t* dead;
+    double* A;     // [np][np] work (becomes L, lower)
+    double* Linv;  // [np][np] work
+    double* diaginv;  // [np/64][64][64]
+    double* tmp;   // [64][np]
+    int* flag;     // device int: 0 ok, 1 not SPD
+    double* scratch;  // small: >= 8 doubles
+    float* U;      // [n][n] output
+};
+hipError_t chol_inverse(const CholArgs& c, hipStream_t st);
+
+}  // namespace realq

@@ -1,0 +1,278 @@
+"""Python binding of librealq.so (include/realq.h): argument marshalling only.
+
+Every function takes torch tensors that live on the GPU, passes their device
+pointers and sizes to the C ABI, and enqueues the work on torch's current stream.
+All arithmetic of the sweep runs in the HIP kernels of the library; if the library
+is not built this module raises on import.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from dataclasses import dataclass
+from pathlib import Path
+from typing import Optional
+
+import torch
+
+_LIB_PATH = Path(__file__).resolve().parent / "librealq.so"
+
+OK = 0
+ERRORS = {
+    -1: "REALQ_ERR_INVALID_ARG",
+    -2: "REALQ_ERR_SHAPE",
+    -3: "REALQ_ERR_NOT_SPD",
+    -4: "REALQ_ERR_HIP",
+    -5: "REALQ_ERR_OOM",
+    -6: "REALQ_ERR_NONFINITE",
+}
+
+EXPORTS = [
+    "realq_qparams_default", "realq_bgd_params_default",
+    "realq_ctx_create", "realq_ctx_destroy", "realq_last_error",
+    "realq_ctx_set_timing", "realq_ctx_kernel_time", "realq_ctx_reset_timing",
+    "realq_hessian_accum", "realq_chol_inverse",
+    "realq_bgd_state_create", "realq_bgd_state_destroy",
+    "realq_quantize_block", "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
+]
+
+
+class RealqError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+# ----------------------------------------------------------------------------- C structs
+
+class QParams(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32), ("group", ctypes.c_int32), ("block", ctypes.c_int32),
+                ("grid", ctypes.c_int32), ("damp", ctypes.c_float)]
+
+
+class BgdParams(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int32), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("tok_chunk", ctypes.c_int64)]
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int64), ("n", ctypes.c_int64), ("T", ctypes.c_int64),
+                ("W0", ctypes.c_void_p), ("X", ctypes.c_void_p), ("Xhat", ctypes.c_void_p),
+                ("s", ctypes.c_void_p), ("M", ctypes.c_void_p), ("P", ctypes.c_void_p),
+                ("window_offset", ctypes.c_int32), ("window_total", ctypes.c_int32),
+                ("q", QParams), ("bgd", BgdParams)]
+
+
+class LayerOut(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("zeros", ctypes.c_void_p),
+                ("W_hat", ctypes.c_void_p), ("H", ctypes.c_void_p), ("U", ctypes.c_void_p),
+                ("dead", ctypes.c_void_p), ("loss_trace", ctypes.c_void_p),
+                ("loss_final", ctypes.c_double), ("ms_total", ctypes.c_double)]
+
+
+def _load():
+    if not _LIB_PATH.exists():
+        raise ImportError(f"{_LIB_PATH} is not built; run paper_2609_00049_amd.build.build() first")
+    lib = ctypes.CDLL(str(_LIB_PATH))
+    vp, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+    sig = {
+        "realq_qparams_default": (None, [ctypes.POINTER(QParams)]),
+        "realq_bgd_params_default": (None, [ctypes.POINTER(BgdParams)]),
+        "realq_ctx_create": (ctypes.c_int, [ctypes.POINTER(vp), vp]),
+        "realq_ctx_destroy": (None, [vp]),
+        "realq_last_error": (ctypes.c_char_p, [vp]),
+        "realq_ctx_set_timing": (ctypes.c_int, [vp, ctypes.c_int]),
+        "realq_ctx_kernel_time": (ctypes.c_int, [vp, ctypes.c_char_p, ctypes.POINTER(i64),
+                                                 ctypes.POINTER(ctypes.c_double)]),
+        "realq_ctx_reset_timing": (ctypes.c_int, [vp]),
+        "realq_hessian_accum": (ctypes.c_int, [vp, vp, vp, i64, i64, vp]),
+        "realq_chol_inverse": (ctypes.c_int, [vp, vp, i64, i64, f32, vp, vp, vp]),
+        "realq_bgd_state_create": (ctypes.c_int, [vp, ctypes.POINTER(vp), vp, vp, vp, vp, vp, vp, i64, i64, i64,
+                                                  ctypes.POINTER(BgdParams)]),
+        "realq_bgd_state_destroy": (None, [vp]),
+        "realq_quantize_block": (ctypes.c_int, [vp, vp, i64, i64, i64, i64, vp, vp, ctypes.POINTER(QParams),
+                                                vp, vp, vp, vp]),
+        "realq_bgd_step": (ctypes.c_int, [vp, vp, vp, i64, f32, vp]),
+        "realq_bgd_loss": (ctypes.c_int, [vp, vp, vp, vp]),
+        "realq_quantize_layer": (ctypes.c_int, [vp, ctypes.POINTER(LayerDesc), ctypes.POINTER(LayerOut)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def lib():
+    return _lib
+
+
+# ----------------------------------------------------------------------------- helpers
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("realq expects device tensors")
+    if not t.is_contiguous():
+        raise ValueError("realq expects contiguous tensors")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _bits(t: torch.Tensor) -> torch.Tensor:
+    """bf16 tensor -> same storage viewed as int16 bit patterns."""
+    if t.dtype != torch.bfloat16:
+        raise ValueError("calibration inputs must be bfloat16")
+    return t
+
+
+def qparams(bits=4, group=128, block=128, grid=80, damp=0.01) -> QParams:
+    return QParams(bits, group, block, grid, damp)
+
+
+def bgd_params(steps=0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, tok_chunk=0) -> BgdParams:
+    return BgdParams(steps, lr, beta1, beta2, eps, tok_chunk)
+
+
+class Context:
+    """A realq_ctx bound to a torch stream (default: the current stream)."""
+
+    def __init__(self, stream: Optional[torch.cuda.Stream] = None):
+        stream = stream or torch.cuda.current_stream()
+        self.stream = stream
+        h = ctypes.c_void_p()
+        rc = _lib.realq_ctx_create(ctypes.byref(h), ctypes.c_void_p(stream.cuda_stream))
+        if rc != OK:
+            raise RealqError(rc, "realq_ctx_create failed")
+        self.h = h
+
+    def check(self, rc: int):
+        if rc != OK:
+            raise RealqError(rc, _lib.realq_last_error(self.h).decode())
+
+    def close(self):
+        if getattr(self, "h", None):
+            _lib.realq_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_timing(self, on: bool):
+        self.check(_lib.realq_ctx_set_timing(self.h, int(on)))
+
+    def reset_timing(self):
+        self.check(_lib.realq_ctx_reset_timing(self.h))
+
+    def kernel_time(self, name: str):
+        n = ctypes.c_int64()
+        ms = ctypes.c_double()
+        self.check(_lib.realq_ctx_kernel_time(self.h, name.encode(), ctypes.byref(n), ctypes.byref(ms)))
+        return n.value, ms.value
+
+
+# ----------------------------------------------------------------------------- the five calls
+
+def hessian_accum(ctx: Context, Xhat: torch.Tensor, s: Optional[torch.Tensor], H_acc: torch.Tensor):
+    """H_acc += sum_t s_t xhat_t xhat_t^T (float64 [n,n])."""
+    T, n = Xhat.shape
+    ctx.check(_lib.realq_hessian_accum(ctx.h, _ptr(_bits(Xhat)), _ptr(s), T, n, _ptr(H_acc)))
+
+
+def chol_inverse(ctx: Context, H_acc: torch.Tensor, T_total: int, damp: float, U: torch.Tensor,
+                 H_out: Optional[torch.Tensor] = None, dead: Optional[torch.Tensor] = None):
+    n = H_acc.shape[0]
+    ctx.check(_lib.realq_chol_inverse(ctx.h, _ptr(H_acc), n, T_total, damp, _ptr(H_out), _ptr(U), _ptr(dead)))
+
+
+class BgdState:
+    def __init__(self, ctx: Context, W0, X, Xhat, s=None, M=None, P=None, params: Optional[BgdParams] = None):
+        self.ctx = ctx
+        self._keep = (W0, X, Xhat, s, M, P)
+        m, n = W0.shape
+        T = X.shape[0]
+        params = params or bgd_params()
+        h = ctypes.c_void_p()
+        ctx.check(_lib.realq_bgd_state_create(ctx.h, ctypes.byref(h), _ptr(W0), _ptr(_bits(X)), _ptr(_bits(Xhat)),
+                                              _ptr(s), _ptr(M), _ptr(P), m, n, T, ctypes.byref(params)))
+        self.h = h
+
+    def close(self):
+        if getattr(self, "h", None):
+            _lib.realq_bgd_state_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def quantize_block(ctx: Context, W, c0: int, bs: int, U, dead, qp: QParams, codes, scales, zeros,
+                   state: Optional[BgdState] = None):
+    m, n = W.shape
+    ctx.check(_lib.realq_quantize_block(ctx.h, _ptr(W), m, n, c0, bs, _ptr(U), _ptr(dead), ctypes.byref(qp),
+                                        _ptr(codes), _ptr(scales), _ptr(zeros), state.h if state else None))
+
+
+def bgd_step(ctx: Context, state: BgdState, W, c1: int, alpha: float = 1.0, loss_out=None):
+    ctx.check(_lib.realq_bgd_step(ctx.h, state.h, _ptr(W), c1, alpha, _ptr(loss_out)))
+
+
+def bgd_loss(ctx: Context, state: BgdState, W, loss_out):
+    ctx.check(_lib.realq_bgd_loss(ctx.h, state.h, _ptr(W), _ptr(loss_out)))
+
+
+@dataclass
+class LayerResult:
+    codes: torch.Tensor
+    scales: torch.Tensor
+    zeros: torch.Tensor
+    W_hat: torch.Tensor
+    H: Optional[torch.Tensor]
+    U: Optional[torch.Tensor]
+    dead: Optional[torch.Tensor]
+    loss_trace: Optional[torch.Tensor]
+    loss_final: float
+    ms_total: float
+
+
+def quantize_layer(ctx: Context, W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams] = None,
+                   bgd: Optional[BgdParams] = None, window=None, want_H=False, want_U=False,
+                   want_trace=True, out: Optional[LayerResult] = None) -> LayerResult:
+    """Whole-module sweep; allocates the outputs unless ``out`` supplies them."""
+    qp = qp or qparams()
+    bgd = bgd or bgd_params()
+    m, n = W0.shape
+    T = X.shape[0]
+    dev = W0.device
+    if out is None:
+        ng = -(-n // qp.group)
+        nb = -(-n // qp.block)
+        out = LayerResult(
+            codes=torch.empty((m, n), dtype=torch.uint8, device=dev),
+            scales=torch.empty((m, ng), dtype=torch.float32, device=dev),
+            zeros=torch.empty((m, ng), dtype=torch.uint8, device=dev),
+            W_hat=torch.empty((m, n), dtype=torch.float32, device=dev),
+            H=torch.empty((n, n), dtype=torch.float32, device=dev) if want_H else None,
+            U=torch.empty((n, n), dtype=torch.float32, device=dev) if want_U else None,
+            dead=torch.empty((n,), dtype=torch.uint8, device=dev),
+            loss_trace=torch.empty((max(1, nb * bgd.steps),), dtype=torch.float64, device=dev)
+            if want_trace else None,
+            loss_final=math.nan, ms_total=math.nan)
+    woff, wtot = (0, 0) if window is None else window
+    desc = LayerDesc(m, n, T, _ptr(W0), _ptr(_bits(X)), _ptr(_bits(Xhat)), _ptr(s), _ptr(M), _ptr(P),
+                     woff, wtot, qp, bgd)
+    lo = LayerOut(_ptr(out.codes), _ptr(out.scales), _ptr(out.zeros), _ptr(out.W_hat), _ptr(out.H), _ptr(out.U),
+                  _ptr(out.dead), _ptr(out.loss_trace), math.nan, math.nan)
+    ctx.check(_lib.realq_quantize_layer(ctx.h, ctypes.byref(desc), ctypes.byref(lo)))
+    out.loss_final = lo.loss_final
+    out.ms_total = lo.ms_total
+    return out

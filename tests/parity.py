@@ -1,0 +1,50 @@
+"""Helpers shared by the GPU parity tests: moving seeded inputs to the device and
+comparing GPU results with the oracle under the acceptance bars of the sweep."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# acceptance bars
+CODE_IDENTITY = 0.999      # fraction of identical int4 codes
+SCALE_RTOL = 1e-4          # scales and zeros
+LOSS_RTOL = 1e-3           # final surrogate loss
+HESS_RTOL = 1e-3           # relative Frobenius error of H
+GROUP_AGREEMENT_AFTER_BGD = 0.99  # groups searched after Block-GD steps (see the test module)
+
+
+def to_device(L, torch):
+    dev = "cuda"
+    W0 = torch.from_numpy(np.ascontiguousarray(L.W0, dtype=np.float32)).to(dev)
+    X = torch.from_numpy(np.ascontiguousarray(L.X, dtype=np.float32)).to(torch.bfloat16).to(dev)
+    Xh = torch.from_numpy(np.ascontiguousarray(L.Xhat, dtype=np.float32)).to(torch.bfloat16).to(dev)
+    s = None if L.s is None else torch.from_numpy(np.ascontiguousarray(L.s, dtype=np.float32)).to(dev)
+    M = None if L.M is None else torch.from_numpy(np.ascontiguousarray(L.M, dtype=np.float32)).to(dev)
+    return W0, X, Xh, s, M
+
+
+def compare(gpu, ora, rows=None, group=128):
+    """Metrics of a GPU LayerResult against an oracle LayerResult (optionally on a row subset)."""
+    codes = gpu.codes.cpu().numpy()
+    scales = gpu.scales.cpu().numpy()
+    zeros = gpu.zeros.cpu().numpy()
+    What = gpu.W_hat.cpu().numpy()
+    if rows is not None:
+        codes, scales, zeros, What = codes[rows], scales[rows], zeros[rows], What[rows]
+    code_id = float((codes == ora.codes).mean())
+    srel = np.abs(scales - ora.scales) / np.maximum(np.abs(ora.scales), 1e-30)
+    grp_ok = (srel <= SCALE_RTOL) & (zeros == ora.zeros)
+    return dict(
+        code_identity=code_id,
+        code_mismatches=int((codes != ora.codes).sum()),
+        group_param_agreement=float(grp_ok.mean()),
+        # groups searched before any Block-GD step (the first group of every row)
+        first_group_agreement=float(grp_ok[:, 0].mean()),
+        scale_rel_max_agreeing=float(srel[grp_ok].max()) if grp_ok.any() else math.nan,
+        what_max_abs=float(np.abs(What - ora.W_hat).max()),
+    )
+
+
+def rel_fro(a, b):
+    return float(np.linalg.norm(a - b) / np.linalg.norm(b))

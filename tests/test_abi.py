@@ -1,0 +1,65 @@
+"""The C ABI: the built library loads and exports every entry point the header declares.
+
+No compute call is made here (this runs without a GPU).
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "realq.h")
+LIB = os.path.join(ROOT, "paper_2609_00049_amd", "librealq.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(realq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_five_sweep_calls():
+    names = declared_functions()
+    for f in ["realq_hessian_accum", "realq_chol_inverse", "realq_quantize_block", "realq_bgd_step",
+              "realq_quantize_layer"]:
+        assert f in names
+
+
+def test_header_compiles_as_c_and_cxx(tmp_path):
+    for compiler, ext in (("gcc", "c"), ("g++", "cpp")):
+        src = tmp_path / f"t.{ext}"
+        src.write_text('#include "realq.h"\nint main(void){ realq_qparams q; realq_qparams_default(&q); return 0; }\n')
+        r = subprocess.run([compiler, "-fsyntax-only", "-Wall", "-Werror", f"-I{os.path.dirname(HEADER)}", str(src)],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(LIB)
+    missing = [f for f in declared_functions() if not hasattr(lib, f)]
+    assert not missing, missing
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_binding_signatures_cover_the_header():
+    from paper_2609_00049_amd import realq
+    assert sorted(realq.EXPORTS) == declared_functions()
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_defaults_and_host_side_errors_without_gpu():
+    """Calls that touch no device memory: defaults, NULL-argument validation."""
+    from paper_2609_00049_amd import realq
+    lib = realq.lib()
+    q = realq.QParams()
+    lib.realq_qparams_default(ctypes.byref(q))
+    assert (q.bits, q.group, q.block, q.grid) == (4, 128, 128, 80) and abs(q.damp - 0.01) < 1e-9
+    b = realq.BgdParams()
+    lib.realq_bgd_params_default(ctypes.byref(b))
+    assert (b.beta1, b.beta2) == (pytest.approx(0.9), pytest.approx(0.999)) and b.eps == pytest.approx(1e-8)
+    assert lib.realq_ctx_create(None, None) == -1
+    assert lib.realq_hessian_accum(None, None, None, 0, 0, None) == -1
+    assert lib.realq_quantize_layer(None, None, None) == -1
