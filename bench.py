@@ -81,7 +81,7 @@ def make_inputs(torch, wl, seed=0):
     return W0.contiguous(), X.contiguous(), Xh.contiguous(), s
 
 
-def cpu_baseline(wl, rows=16, tokens=8192):
+def cpu_baseline(wl, rows=32, tokens=16384):
     """Oracle timed on a bounded sample of the same workload, scaled by algorithmic FLOPs."""
     import numpy as np
     import synth

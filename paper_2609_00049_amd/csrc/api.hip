@@ -539,9 +539,10 @@ int realq_quantize_block(realq_ctx* ctx, float* W, int64_t m, int64_t n, int64_t
 
 // ============================================================================ a7-a9: one BGD step
 
+// Split-K factor of the gradient GEMM: enough blocks for two rounds over the 256 CUs.
 static int64_t choose_splits(int64_t M, int64_t N, int64_t K) {
-    const int64_t blocks = realq::gemm_num_blocks(M, N);
-    int64_t s = (1024 + blocks - 1) / blocks;
+    const int64_t blocks = realq::gemm_grad_blocks(M, N);
+    int64_t s = (512 + blocks - 1) / blocks;
     int64_t kmax = K / 256;  // keep at least 256 tokens per split
     if (s > kmax) s = kmax;
     if (s > 64) s = 64;
@@ -586,7 +587,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, float* W, int64_t c1, fl
             realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, S};
             splits_used = realq::gemm_effective_splits(cur, S);
             Timed tm(ctx, "grad");
-            RQ_HIP(ctx, realq::gemm_store_f32(g, (float*)Gp, nJ, m * nJ, 1.f, s));
+            RQ_HIP(ctx, realq::gemm_grad(g, (float*)Gp, nJ, m * nJ, s));
         }
         if (nchunks > 1 || dense) {
             // Gacc (+)= sum of this chunk's split slices, chunks in order

@@ -8,13 +8,18 @@
 //   gradient   G  = (R o s) Xhat_J         A = split(R o s),        B = Xhat^T[J, :] (K = tokens)
 //   Hessian    H += (s o Xhat)^T Xhat      A = split(s o Xhat^T),   B = Xhat^T       (K = tokens)
 //   lock / init of the residual base       A = split(W - W0)[:, blk], B = Xhat[:, blk]
-// The fp32 operand is carried as a bf16 hi/lo pair and the bf16-exact operand
+// The float32 operand is carried as a bf16 hi/lo pair and the bf16-exact operand
 // (calibration activations) once; both passes reuse the same B fragments, so the
 // product is accurate to about 2^-16 relative at twice the MFMA work.
 //
-// Tiling: 256 threads = 4 wave64s in a 2x2 grid, each wave owning a 64x64 output
-// piece computed with 2x2 v_mfma_f32_32x32x16_bf16 tiles.  A and B tiles are
-// staged through LDS with a register prefetch of the next K slice.  Split-K over
+// Tiling (two shapes, picked by problem size):
+//   large: 256 x 256 block tile, 8 wave64s as 4 (M) x 2 (N), 64 x 128 per wave
+//   small: 128 x 128 block tile, 4 wave64s as 2 x 2,        64 x 64 per wave
+// with v_mfma_f32_32x32x16_bf16 (accumulators live in AGPRs).  K advances in
+// slices of 32 through a double-buffered LDS stage, one barrier per slice, with
+// the next slice's global loads in flight during the MFMAs.  Blocks are renumbered
+// so that each XCD (blocks are dealt round-robin over the 8 XCDs) owns a contiguous
+// run of tiles, walked in groups of `group_m` row tiles for L2 reuse.  Split-K over
 // gridDim.z with a fixed K range per split (deterministic).
 #include "common.h"
 #include "kernels.h"
@@ -23,143 +28,197 @@ namespace realq {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32;
-constexpr int LDS_STRIDE = BK + 8;  // bf16 elements per LDS row (16-byte pad against bank conflicts)
-constexpr int NTHREADS = 256;
+constexpr int BK = 32;
+constexpr int LDS_STRIDE = BK + 8;  // bf16 per LDS row: 16-byte pad against bank conflicts
+constexpr int EPI_STRIDE = 36;      // floats per row of the epilogue restaging tile (16-byte aligned)
 
-struct TileLoad {
-    u16x8 v[2];
+template <int BM_, int BN_, int WAVES_M_, int WAVES_N_>
+struct Cfg {
+    static constexpr int BM = BM_, BN = BN_, WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
+    static constexpr int NT = WAVES_M * WAVES_N * 64;
+    static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;  // wave tile
+    static constexpr int SM = WTM / 32, SN = WTN / 32;             // 32x32 MFMA tiles per wave
+    static constexpr int A_CH = BM * BK / 8 / NT;                  // 16-byte chunks per thread
+    static constexpr int B_CH = BN * BK / 8 / NT;
 };
+using CfgLarge = Cfg<256, 256, 4, 2>;
+using CfgSmall = Cfg<128, 128, 2, 2>;
 
-// Load a [128 x 32] bf16 tile (rows r0.., k k0..) into registers: 512 chunks of 8, 2 per thread.
-__device__ __forceinline__ void load_tile(TileLoad& t, const uint16_t* __restrict__ P, int64_t ld, int64_t rows,
-                                          int64_t r0, int64_t k0, int64_t kend, bool vec_ok) {
+template <int CH, int NT>
+__device__ __forceinline__ void load_rows(u16x8 (&v)[CH], const uint16_t* __restrict__ P, int64_t ld, int64_t rows,
+                                          int64_t r0, int64_t k0, int64_t kend, bool vec) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-        int chunk = threadIdx.x + c * NTHREADS;
-        int r = chunk >> 2;
-        int kc = (chunk & 3) * 8;
-        int64_t gr = r0 + r;
-        int64_t gk = k0 + kc;
-        u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int c = 0; c < CH; ++c) {
+        const int chunk = threadIdx.x + c * NT;
+        const int r = chunk >> 2;
+        const int kc = (chunk & 3) * 8;
+        const int64_t gr = r0 + r;
+        const int64_t gk = k0 + kc;
+        u16x8 x = {0, 0, 0, 0, 0, 0, 0, 0};
         if (gr < rows) {
             const uint16_t* p = P + gr * ld + gk;
-            if (vec_ok && gk + 8 <= kend) {
-                v = *reinterpret_cast<const u16x8*>(p);
+            if (vec && gk + 8 <= kend) {
+                x = *reinterpret_cast<const u16x8*>(p);
             } else {
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    if (gk + e < kend) v[e] = p[e];
+                    if (gk + e < kend) x[e] = p[e];
             }
         }
-        t.v[c] = v;
+        v[c] = x;
     }
 }
 
-__device__ __forceinline__ void store_tile(const TileLoad& t, uint16_t* lds) {
+template <int CH, int NT>
+__device__ __forceinline__ void store_rows(const u16x8 (&v)[CH], uint16_t* lds) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-        int chunk = threadIdx.x + c * NTHREADS;
-        int r = chunk >> 2;
-        int kc = (chunk & 3) * 8;
-        *reinterpret_cast<u16x8*>(lds + r * LDS_STRIDE + kc) = t.v[c];
+    for (int c = 0; c < CH; ++c) {
+        const int chunk = threadIdx.x + c * NT;
+        *reinterpret_cast<u16x8*>(lds + (chunk >> 2) * LDS_STRIDE + (chunk & 3) * 8) = v[c];
     }
 }
 
 __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int row, int k) {
-    u16x8 v = *reinterpret_cast<const u16x8*>(lds + row * LDS_STRIDE + k);
-    return __builtin_bit_cast(bf16x8, v);
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + row * LDS_STRIDE + k));
+}
+
+// Tile coordinates of this block: XCD-contiguous renumbering, then grouped row-tile order.
+__device__ __forceinline__ void tile_of(int64_t tiles_m, int64_t tiles_n, int64_t group_m, int64_t& tm, int64_t& tn) {
+    const int64_t nblk = tiles_m * tiles_n;
+    const int64_t b = blockIdx.x;
+    int64_t L = b;
+    if ((nblk & 7) == 0) L = (b & 7) * (nblk >> 3) + (b >> 3);
+    const int64_t per_group = group_m * tiles_n;
+    const int64_t g = L / per_group;
+    const int64_t first = g * group_m;
+    const int64_t gs = min(group_m, tiles_m - first);
+    const int64_t r = L - g * per_group;
+    tm = first + r % gs;
+    tn = r / gs;
 }
 
 }  // namespace
 
-template <class Epi, bool HAS_LO>
-__global__ __launch_bounds__(NTHREADS) void gemm_nt_kernel(const uint16_t* __restrict__ Ahi,
-                                                           const uint16_t* __restrict__ Alo, int64_t lda,
-                                                           const uint16_t* __restrict__ B, int64_t ldb, int64_t M,
-                                                           int64_t N, int64_t K, int64_t k_per_split, int vec_ok,
-                                                           int64_t tiles_n, Epi epi) {
-    __shared__ __attribute__((aligned(16))) uint16_t sA[BM * LDS_STRIDE];
-    __shared__ __attribute__((aligned(16))) uint16_t sAlo[HAS_LO ? BM * LDS_STRIDE : 8];
-    __shared__ __attribute__((aligned(16))) uint16_t sB[BN * LDS_STRIDE];
+template <class C, class Epi, bool HAS_LO>
+__global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restrict__ Ahi,
+                                                        const uint16_t* __restrict__ Alo, int64_t lda,
+                                                        const uint16_t* __restrict__ B, int64_t ldb, int64_t M,
+                                                        int64_t N, int64_t K, int64_t k_per_split, int vec_ok,
+                                                        int64_t tiles_m, int64_t tiles_n, int64_t group_m, Epi epi) {
+    constexpr int A_ROWS = C::BM * (HAS_LO ? 2 : 1);
+    constexpr int STAGE = (A_ROWS + C::BN) * LDS_STRIDE;  // bf16 elements per stage
+    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * STAGE];
 
-    const int64_t tile = blockIdx.x;
-    const int64_t tm = tile / tiles_n, tn = tile % tiles_n;
-    const int64_t m0 = tm * BM, n0 = tn * BN;
+    int64_t tm, tn;
+    tile_of(tiles_m, tiles_n, group_m, tm, tn);
+    const int64_t m0 = tm * C::BM, n0 = tn * C::BN;
     const int64_t kbeg = (int64_t)blockIdx.z * k_per_split;
     const int64_t kend = min(K, kbeg + k_per_split);
+    const int64_t nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+    const bool vec = vec_ok != 0;
 
-    f32x16 acc[2][2];
+    f32x16 acc[C::SM][C::SN];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < C::SM; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < C::SN; ++b)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
 
-    TileLoad ra, ralo, rb;
-    const bool vec = vec_ok != 0;
-    if (kbeg < kend) {
-        load_tile(ra, Ahi, lda, M, m0, kbeg, kend, vec);
-        if (HAS_LO) load_tile(ralo, Alo, lda, M, m0, kbeg, kend, vec);
-        load_tile(rb, B, ldb, N, n0, kbeg, kend, vec);
+    u16x8 ra[C::A_CH], ral[HAS_LO ? C::A_CH : 1], rb[C::B_CH];
+    auto gload = [&](int64_t k0) {
+        load_rows<C::A_CH, C::NT>(ra, Ahi, lda, M, m0, k0, kend, vec);
+        if constexpr (HAS_LO) load_rows<C::A_CH, C::NT>(ral, Alo, lda, M, m0, k0, kend, vec);
+        load_rows<C::B_CH, C::NT>(rb, B, ldb, N, n0, k0, kend, vec);
+    };
+    auto lstore = [&](int s) {
+        uint16_t* base = smem + s * STAGE;
+        store_rows<C::A_CH, C::NT>(ra, base);
+        if constexpr (HAS_LO) store_rows<C::A_CH, C::NT>(ral, base + C::BM * LDS_STRIDE);
+        store_rows<C::B_CH, C::NT>(rb, base + A_ROWS * LDS_STRIDE);
+    };
+
+    if (nk > 0) {
+        gload(kbeg);
+        lstore(0);
     }
-    for (int64_t k0 = kbeg; k0 < kend; k0 += BK) {
-        __syncthreads();
-        store_tile(ra, sA);
-        if (HAS_LO) store_tile(ralo, sAlo);
-        store_tile(rb, sB);
-        __syncthreads();
-        if (k0 + BK < kend) {
-            load_tile(ra, Ahi, lda, M, m0, k0 + BK, kend, vec);
-            if (HAS_LO) load_tile(ralo, Alo, lda, M, m0, k0 + BK, kend, vec);
-            load_tile(rb, B, ldb, N, n0, k0 + BK, kend, vec);
-        }
+    __syncthreads();
+    for (int64_t it = 0; it < nk; ++it) {
+        const int cur = (int)(it & 1);
+        const bool more = it + 1 < nk;
+        if (more) gload(kbeg + (it + 1) * BK);
+        const uint16_t* sA = smem + cur * STAGE;
+        const uint16_t* sAl = sA + C::BM * LDS_STRIDE;
+        const uint16_t* sB = sA + A_ROWS * LDS_STRIDE;
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 16) {
             const int kofs = kk + 8 * (lane >> 5);
-            bf16x8 a[2], alo[2], b[2];
+            bf16x8 a[C::SM], al[HAS_LO ? C::SM : 1], b[C::SN];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                a[i] = frag(sA, wm * 64 + i * 32 + (lane & 31), kofs);
-                if (HAS_LO) alo[i] = frag(sAlo, wm * 64 + i * 32 + (lane & 31), kofs);
-                b[i] = frag(sB, wn * 64 + i * 32 + (lane & 31), kofs);
+            for (int i = 0; i < C::SM; ++i) {
+                a[i] = frag(sA, wm * C::WTM + i * 32 + (lane & 31), kofs);
+                if constexpr (HAS_LO) al[i] = frag(sAl, wm * C::WTM + i * 32 + (lane & 31), kofs);
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int j = 0; j < C::SN; ++j) b[j] = frag(sB, wn * C::WTN + j * 32 + (lane & 31), kofs);
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
+            for (int i = 0; i < C::SM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::SN; ++j) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-                    if (HAS_LO)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo[i], b[j], acc[i][j], 0, 0, 0);
+                    if constexpr (HAS_LO)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], b[j], acc[i][j], 0, 0, 0);
                 }
         }
+        if (more) lstore(cur ^ 1);
+        __syncthreads();
     }
 
-    // Epilogue: element (row, col) of a 32x32 tile held by this lane in acc[e]:
-    // row = 8*(e/4) + 4*(lane/32) + e%4, col = lane%32.
+    // Epilogue.  Element (row, col) of a 32x32 tile held by this lane in acc[e] is
+    // row = 8*(e/4) + 4*(lane/32) + e%4, col = lane%32.  Each tile is restaged through
+    // LDS so that a lane then owns 4 consecutive columns of a row (16-byte accesses).
     float aux = 0.f;
+    float* scr = reinterpret_cast<float*>(smem) + wave * (32 * EPI_STRIDE);
+    const int64_t z = blockIdx.z;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < C::SM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
+        for (int j = 0; j < C::SN; ++j) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int64_t row = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                if (row < M && col < N) epi(row, col, acc[i][j][e], (int64_t)blockIdx.z, aux);
+            for (int e = 0; e < 16; ++e)
+                scr[(8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)) * EPI_STRIDE + (lane & 31)] = acc[i][j][e];
+            __syncthreads();
+            const int64_t r0 = m0 + wm * C::WTM + i * 32;
+            const int64_t c0 = n0 + wn * C::WTN + j * 32;
+            const int cc = (lane & 7) * 4;
+            const int64_t col = c0 + cc;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int rr = q * 8 + (lane >> 3);
+                const int64_t row = r0 + rr;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(scr + rr * EPI_STRIDE + cc);
+                if (row < M) {
+                    if (col + 3 < N) {
+                        epi.vec4(row, col, v, z, aux);
+                    } else {
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            if (col + u < N) epi(row, col + u, v[u], z, aux);
+                    }
+                }
             }
+            __syncthreads();
         }
-    if (Epi::kReduce) {
-        // deterministic block reduction of the per-thread partial sums
-        __shared__ double red[NTHREADS];
+    if constexpr (Epi::kReduce) {
+        // deterministic block reduction of the per-thread partial sums (reuses the LDS stage)
+        double* red = reinterpret_cast<double*>(smem);
         red[threadIdx.x] = (double)aux;
         __syncthreads();
-        for (int s = NTHREADS / 2; s > 0; s >>= 1) {
+        for (int s = C::NT / 2; s > 0; s >>= 1) {
             if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
             __syncthreads();
         }
@@ -168,6 +227,12 @@ __global__ __launch_bounds__(NTHREADS) void gemm_nt_kernel(const uint16_t* __res
 }
 
 // ---------------------------------------------------------------- epilogues
+// operator() handles one element; vec4() handles columns j..j+3 of row i (all < N) and
+// falls back to operator() when an address is not suitably aligned.
+
+__device__ __forceinline__ bool al16(const void* p) { return (((uintptr_t)p) & 15u) == 0; }
+__device__ __forceinline__ bool al8(const void* p) { return (((uintptr_t)p) & 7u) == 0; }
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 
 struct EpiStoreF32 {  // C[z][i][j] = alpha * acc
     static constexpr bool kReduce = false;
@@ -177,8 +242,20 @@ struct EpiStoreF32 {  // C[z][i][j] = alpha * acc
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t z, float&) const {
         C[z * split_stride + i * ldc + j] = alpha * v;
     }
+    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
+        float* p = C + z * split_stride + i * ldc + j;
+        if (al16(p)) {
+            *reinterpret_cast<f32x4*>(p) = v * alpha;
+        } else {
+            for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
+        }
+    }
     __device__ void partial(int64_t, double) const {}
 };
+
+// Gradient slices of the split-K token reduction: G[z][i][j] = acc (same as EpiStoreF32,
+// kept as its own type so the gradient GEMM is a kernel of its own in traces).
+struct EpiGrad : EpiStoreF32 {};
 
 struct EpiAccF32 {  // C[i][j] += alpha * acc
     static constexpr bool kReduce = false;
@@ -186,6 +263,15 @@ struct EpiAccF32 {  // C[i][j] += alpha * acc
     int64_t ldc;
     float alpha;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { C[i * ldc + j] += alpha * v; }
+    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
+        float* p = C + i * ldc + j;
+        if (al16(p)) {
+            f32x4 c = *reinterpret_cast<const f32x4*>(p);
+            *reinterpret_cast<f32x4*>(p) = c + v * alpha;
+        } else {
+            for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
+        }
+    }
     __device__ void partial(int64_t, double) const {}
 };
 
@@ -194,6 +280,9 @@ struct EpiAccF64 {  // C[i][j] += acc   (float64 accumulator across chunks)
     double* C;
     int64_t ldc;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { C[i * ldc + j] += (double)v; }
+    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
+        for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
+    }
     __device__ void partial(int64_t, double) const {}
 };
 
@@ -217,6 +306,30 @@ struct EpiResid {
         Rlo[i * ldr + t] = lo;
         aux += rs * r;
     }
+    __device__ void vec4(int64_t i, int64_t t, f32x4 v, int64_t z, float& aux) const {
+        const float* b = B0 + i * ldb0 + t;
+        uint16_t* ph = Rhi + i * ldr + t;
+        uint16_t* pl = Rlo + i * ldr + t;
+        if (!al16(b) || !al8(ph) || !al8(pl) || (s && !al16(s + t))) {
+            for (int u = 0; u < 4; ++u) (*this)(i, t + u, v[u], z, aux);
+            return;
+        }
+        const f32x4 r = *reinterpret_cast<const f32x4*>(b) + v;
+        f32x4 w = {1.f, 1.f, 1.f, 1.f};
+        if (s) w = *reinterpret_cast<const f32x4*>(s + t);
+        u16x4 h, l;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const float rs = r[u] * w[u];
+            uint16_t hh, ll;
+            split_bf16(rs, hh, ll);
+            h[u] = hh;
+            l[u] = ll;
+            aux += rs * r[u];
+        }
+        *reinterpret_cast<u16x4*>(ph) = h;
+        *reinterpret_cast<u16x4*>(pl) = l;
+    }
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
 
@@ -232,6 +345,9 @@ struct EpiLoss {
         float w = s ? s[t] : 1.f;
         aux += w * r * r;
     }
+    __device__ void vec4(int64_t i, int64_t t, f32x4 v, int64_t z, float& aux) const {
+        for (int u = 0; u < 4; ++u) (*this)(i, t + u, v[u], z, aux);
+    }
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
 
@@ -241,6 +357,9 @@ struct EpiStoreBf16T {
     uint16_t* out;
     int64_t ld;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { out[j * ld + i] = f2bf(v); }
+    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
+        for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
+    }
     __device__ void partial(int64_t, double) const {}
 };
 
@@ -248,26 +367,18 @@ struct EpiStoreBf16T {
 
 static inline bool aligned16(const void* p) { return (((uintptr_t)p) & 15u) == 0; }
 
-template <class Epi>
-static hipError_t launch(const GemmArgs& g, const Epi& epi, hipStream_t stream) {
-    if (g.M <= 0 || g.N <= 0) return hipSuccess;
-    const int64_t tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
-    int64_t splits = g.splits < 1 ? 1 : g.splits;
-    int64_t kps = (g.K + splits - 1) / splits;
-    kps = ((kps + BK - 1) / BK) * BK;
-    if (kps <= 0) kps = BK;
-    splits = (g.K + kps - 1) / kps;
-    if (splits < 1) splits = 1;
-    const bool vec = aligned16(g.Ahi) && (!g.Alo || aligned16(g.Alo)) && aligned16(g.B) && (g.lda % 8 == 0) &&
-                     (g.ldb % 8 == 0);
-    dim3 grid((unsigned)(tiles_m * tiles_n), 1, (unsigned)splits);
-    if (g.Alo)
-        hipLaunchKernelGGL((gemm_nt_kernel<Epi, true>), grid, dim3(NTHREADS), 0, stream, g.Ahi, g.Alo, g.lda, g.B,
-                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_n, epi);
-    else
-        hipLaunchKernelGGL((gemm_nt_kernel<Epi, false>), grid, dim3(NTHREADS), 0, stream, g.Ahi, g.Alo, g.lda, g.B,
-                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_n, epi);
-    return hipGetLastError();
+// The large tile is used once the problem has at least this many large tiles.
+static constexpr int64_t kLargeMinTiles = 256;
+
+template <class C>
+static int64_t tiles_of(int64_t M, int64_t N) {
+    return ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+}
+
+static bool use_large(int64_t M, int64_t N) { return tiles_of<CfgLarge>(M, N) >= kLargeMinTiles; }
+
+int64_t gemm_num_blocks(int64_t M, int64_t N) {
+    return use_large(M, N) ? tiles_of<CfgLarge>(M, N) : tiles_of<CfgSmall>(M, N);
 }
 
 int64_t gemm_effective_splits(int64_t K, int64_t splits) {
@@ -279,11 +390,50 @@ int64_t gemm_effective_splits(int64_t K, int64_t splits) {
     return s < 1 ? 1 : s;
 }
 
-int64_t gemm_num_blocks(int64_t M, int64_t N) { return ((M + BM - 1) / BM) * ((N + BN - 1) / BN); }
+template <class C, class Epi>
+static hipError_t launch_cfg(const GemmArgs& g, const Epi& epi, hipStream_t stream) {
+    const int64_t tiles_m = (g.M + C::BM - 1) / C::BM, tiles_n = (g.N + C::BN - 1) / C::BN;
+    int64_t splits = g.splits < 1 ? 1 : g.splits;
+    int64_t kps = (g.K + splits - 1) / splits;
+    kps = ((kps + BK - 1) / BK) * BK;
+    if (kps <= 0) kps = BK;
+    splits = (g.K + kps - 1) / kps;
+    if (splits < 1) splits = 1;
+    const bool vec = aligned16(g.Ahi) && (!g.Alo || aligned16(g.Alo)) && aligned16(g.B) && (g.lda % 8 == 0) &&
+                     (g.ldb % 8 == 0);
+    // row-tile group: enough row tiles per group that ~32 concurrent blocks of an XCD share operands
+    int64_t group_m = tiles_n >= 32 ? 8 : (tiles_n >= 8 ? 2 : 1);
+    if (g.group_m > 0) group_m = g.group_m;
+    dim3 grid((unsigned)(tiles_m * tiles_n), 1, (unsigned)splits);
+    if (g.Alo)
+        hipLaunchKernelGGL((gemm_nt_kernel<C, Epi, true>), grid, dim3(C::NT), 0, stream, g.Ahi, g.Alo, g.lda, g.B,
+                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_m, tiles_n, group_m, epi);
+    else
+        hipLaunchKernelGGL((gemm_nt_kernel<C, Epi, false>), grid, dim3(C::NT), 0, stream, g.Ahi, g.Alo, g.lda, g.B,
+                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_m, tiles_n, group_m, epi);
+    return hipGetLastError();
+}
+
+template <class Epi>
+static hipError_t launch(const GemmArgs& g, const Epi& epi, hipStream_t stream) {
+    if (g.M <= 0 || g.N <= 0) return hipSuccess;
+    if (use_large(g.M, g.N)) return launch_cfg<CfgLarge>(g, epi, stream);
+    return launch_cfg<CfgSmall>(g, epi, stream);
+}
 
 hipError_t gemm_store_f32(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, float alpha,
                           hipStream_t st) {
     return launch(g, EpiStoreF32{C, ldc, split_stride, alpha}, st);
+}
+int64_t gemm_grad_blocks(int64_t M, int64_t N) { return tiles_of<CfgLarge>(M, N); }
+hipError_t gemm_grad(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, hipStream_t st) {
+    if (g.M <= 0 || g.N <= 0) return hipSuccess;
+    EpiGrad e;
+    e.C = C;
+    e.ldc = ldc;
+    e.split_stride = split_stride;
+    e.alpha = 1.f;
+    return launch_cfg<CfgLarge>(g, e, st);  // always the large tile (split-K fills the chip)
 }
 hipError_t gemm_acc_f32(const GemmArgs& g, float* C, int64_t ldc, float alpha, hipStream_t st) {
     return launch(g, EpiAccF32{C, ldc, alpha}, st);

@@ -16,10 +16,14 @@ struct GemmArgs {
     int64_t ldb;
     int64_t M, N, K;
     int64_t splits;
+    int64_t group_m = 0;  // row tiles walked together per XCD (0 = chosen from the shape)
 };
 int64_t gemm_effective_splits(int64_t K, int64_t splits);
 int64_t gemm_num_blocks(int64_t M, int64_t N);
 hipError_t gemm_store_f32(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, float alpha, hipStream_t st);
+// Split-K gradient slices C[z][i][j] = acc, always on the 256x256 tile; gemm_grad_blocks gives its tile count.
+int64_t gemm_grad_blocks(int64_t M, int64_t N);
+hipError_t gemm_grad(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, hipStream_t st);
 hipError_t gemm_acc_f32(const GemmArgs& g, float* C, int64_t ldc, float alpha, hipStream_t st);
 hipError_t gemm_acc_f64(const GemmArgs& g, double* C, int64_t ldc, hipStream_t st);
 hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
