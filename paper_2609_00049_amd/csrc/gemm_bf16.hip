@@ -29,7 +29,12 @@ namespace realq {
 namespace {
 
 constexpr int BK = 32;
-constexpr int LDS_STRIDE = BK + 8;  // bf16 per LDS row: 16-byte pad against bank conflicts
+constexpr int LDS_STRIDE = BK;      // bf16 per LDS row (64 bytes, unpadded; 16-byte chunks XOR-swizzled)
+
+// Chunk position of 16-byte chunk c of LDS row r.  Fragment reads touch 8 (or 16)
+// consecutive rows at one chunk; the swizzle gives them distinct bank groups on both a
+// 32- and a 64-bank LDS, and keeps each thread's stage writes conflict-free as well.
+__device__ __forceinline__ int swz(int r, int c) { return (c ^ ((r >> 1) ^ (r >> 3))) & 3; }
 constexpr int EPI_STRIDE = 36;      // floats per row of the epilogue restaging tile (16-byte aligned)
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_>
@@ -69,17 +74,41 @@ __device__ __forceinline__ void load_rows(u16x8 (&v)[CH], const uint16_t* __rest
     }
 }
 
+// Per-thread row pointers of one operand tile: chunk c of this thread covers row
+// min(r0 + r, rows - 1) (rows past the end are clamped; their products only reach
+// accumulators the epilogue masks) at k offset kc.
+template <int CH, int NT>
+struct RowPtrs {
+    const uint16_t* p[CH];
+    __device__ __forceinline__ void init(const uint16_t* __restrict__ P, int64_t ld, int64_t rows, int64_t r0,
+                                         int64_t k0) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int chunk = threadIdx.x + c * NT;
+            const int64_t gr = min(r0 + (chunk >> 2), rows - 1);
+            p[c] = P + gr * ld + k0 + (chunk & 3) * 8;
+        }
+    }
+    // full 32-wide slice at k offset `off` from the start, 16-byte loads, no checks
+    __device__ __forceinline__ void load(u16x8 (&v)[CH], int64_t off) const {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) v[c] = *reinterpret_cast<const u16x8*>(p[c] + off);
+    }
+};
+
 template <int CH, int NT>
 __device__ __forceinline__ void store_rows(const u16x8 (&v)[CH], uint16_t* lds) {
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         const int chunk = threadIdx.x + c * NT;
-        *reinterpret_cast<u16x8*>(lds + (chunk >> 2) * LDS_STRIDE + (chunk & 3) * 8) = v[c];
+        const int r = chunk >> 2;
+        *reinterpret_cast<u16x8*>(lds + r * LDS_STRIDE + swz(r, chunk & 3) * 8) = v[c];
     }
 }
 
 __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int row, int k) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(lds + row * LDS_STRIDE + k));
+    return __builtin_bit_cast(bf16x8,
+                              *reinterpret_cast<const u16x8*>(lds + row * LDS_STRIDE + swz(row, k >> 3) * 8));
 }
 
 // Tile coordinates of this block: XCD-contiguous renumbering, then grouped row-tile order.
@@ -129,29 +158,33 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
 
-    u16x8 ra[C::A_CH], ral[HAS_LO ? C::A_CH : 1], rb[C::B_CH];
-    auto gload = [&](int64_t k0) {
-        load_rows<C::A_CH, C::NT>(ra, Ahi, lda, M, m0, k0, kend, vec);
-        if constexpr (HAS_LO) load_rows<C::A_CH, C::NT>(ral, Alo, lda, M, m0, k0, kend, vec);
-        load_rows<C::B_CH, C::NT>(rb, B, ldb, N, n0, k0, kend, vec);
-    };
-    auto lstore = [&](int s) {
-        uint16_t* base = smem + s * STAGE;
-        store_rows<C::A_CH, C::NT>(ra, base);
-        if constexpr (HAS_LO) store_rows<C::A_CH, C::NT>(ral, base + C::BM * LDS_STRIDE);
-        store_rows<C::B_CH, C::NT>(rb, base + A_ROWS * LDS_STRIDE);
-    };
-
-    if (nk > 0) {
-        gload(kbeg);
-        lstore(0);
-    }
-    __syncthreads();
-    for (int64_t it = 0; it < nk; ++it) {
-        const int cur = (int)(it & 1);
-        const bool more = it + 1 < nk;
-        if (more) gload(kbeg + (it + 1) * BK);
-        const uint16_t* sA = smem + cur * STAGE;
+    // Two register sets hold K slices in flight: slice s+2 is requested while slice s is
+    // multiplied out of LDS and slice s+1 waits in registers for its LDS stage.
+    u16x8 a0[C::A_CH], al0[HAS_LO ? C::A_CH : 1], b0[C::B_CH];
+    u16x8 a1[C::A_CH], al1[HAS_LO ? C::A_CH : 1], b1[C::B_CH];
+    RowPtrs<C::A_CH, C::NT> pa, pal;
+    RowPtrs<C::B_CH, C::NT> pb;
+    pa.init(Ahi, lda, M, m0, kbeg);
+    if constexpr (HAS_LO) pal.init(Alo, lda, M, m0, kbeg);
+    pb.init(B, ldb, N, n0, kbeg);
+    // Full, aligned slices run through the pipelined loop with unchecked 16-byte loads; a
+    // partial last slice (or every slice of unaligned operands) goes through the checked tail.
+    const int64_t nfull = vec ? (kend - kbeg) / BK : 0;
+#define RQ_GLOAD(RA, RAL, RB, S)                                                                \
+    do {                                                                                        \
+        pa.load(RA, (S) * BK);                                                                  \
+        if constexpr (HAS_LO) pal.load(RAL, (S) * BK);                                          \
+        pb.load(RB, (S) * BK);                                                                  \
+    } while (0)
+#define RQ_LSTORE(RA, RAL, RB, ST)                                                              \
+    do {                                                                                        \
+        uint16_t* base_ = smem + (ST) * STAGE;                                                  \
+        store_rows<C::A_CH, C::NT>(RA, base_);                                                  \
+        if constexpr (HAS_LO) store_rows<C::A_CH, C::NT>(RAL, base_ + C::BM * LDS_STRIDE);      \
+        store_rows<C::B_CH, C::NT>(RB, base_ + A_ROWS * LDS_STRIDE);                            \
+    } while (0)
+    auto compute = [&](int st) {
+        const uint16_t* sA = smem + st * STAGE;
         const uint16_t* sAl = sA + C::BM * LDS_STRIDE;
         const uint16_t* sB = sA + A_ROWS * LDS_STRIDE;
 #pragma unroll
@@ -174,9 +207,37 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], b[j], acc[i][j], 0, 0, 0);
                 }
         }
-        if (more) lstore(cur ^ 1);
+    };
+
+    if (nfull > 0) RQ_GLOAD(a0, al0, b0, 0);
+    if (nfull > 1) RQ_GLOAD(a1, al1, b1, 1);
+    if (nfull > 0) RQ_LSTORE(a0, al0, b0, 0);
+    __syncthreads();
+    for (int64_t it = 0; it < nfull; it += 2) {
+        // even slice `it` in stage 0; set 1 holds slice it+1; set 0 is free for slice it+2
+        if (it + 2 < nfull) RQ_GLOAD(a0, al0, b0, it + 2);
+        compute(0);
+        if (it + 1 < nfull) RQ_LSTORE(a1, al1, b1, 1);
+        __syncthreads();
+        if (it + 1 >= nfull) break;
+        // odd slice it+1 in stage 1; set 0 holds slice it+2; set 1 is free for slice it+3
+        if (it + 3 < nfull) RQ_GLOAD(a1, al1, b1, it + 3);
+        compute(1);
+        if (it + 2 < nfull) RQ_LSTORE(a0, al0, b0, 0);
         __syncthreads();
     }
+    for (int64_t s = nfull; s < nk; ++s) {  // checked tail, single-buffered
+        const int64_t k0 = kbeg + s * BK;
+        load_rows<C::A_CH, C::NT>(a0, Ahi, lda, M, m0, k0, kend, vec);
+        if constexpr (HAS_LO) load_rows<C::A_CH, C::NT>(al0, Alo, lda, M, m0, k0, kend, vec);
+        load_rows<C::B_CH, C::NT>(b0, B, ldb, N, n0, k0, kend, vec);
+        RQ_LSTORE(a0, al0, b0, 0);
+        __syncthreads();
+        compute(0);
+        __syncthreads();
+    }
+#undef RQ_GLOAD
+#undef RQ_LSTORE
 
     // Epilogue.  Element (row, col) of a 32x32 tile held by this lane in acc[e] is
     // row = 8*(e/4) + 4*(lane/32) + e%4, col = lane%32.  Each tile is restaged through
