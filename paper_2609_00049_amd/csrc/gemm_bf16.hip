@@ -111,6 +111,21 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int row, int k) {
                               *reinterpret_cast<const u16x8*>(lds + row * LDS_STRIDE + swz(row, k >> 3) * 8));
 }
 
+// 16-byte direct-to-LDS load of this lane's global chunk into LDS byte address
+// lds_base + 16 * lane (lds_base is wave-uniform).  Issued as inline assembly so the
+// compiler does not insert conservative waits for it; every consumer is ordered by the
+// explicit vmcnt waits and barriers of the K loop.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
 // Tile coordinates of this block: XCD-contiguous renumbering, then grouped row-tile order.
 __device__ __forceinline__ void tile_of(int64_t tiles_m, int64_t tiles_n, int64_t group_m, int64_t& tm, int64_t& tn) {
     const int64_t nblk = tiles_m * tiles_n;
@@ -136,7 +151,16 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
                                                         int64_t tiles_m, int64_t tiles_n, int64_t group_m, Epi epi) {
     constexpr int A_ROWS = C::BM * (HAS_LO ? 2 : 1);
     constexpr int STAGE = (A_ROWS + C::BN) * LDS_STRIDE;  // bf16 elements per stage
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * STAGE];
+    // Three LDS stages as separate arrays (the compiler can tell a stage being filled by the
+    // direct-to-LDS loads from the one being read), plus epilogue scratch when a stage is
+    // too small to hold it.
+    constexpr int EPI_FLOATS = (C::NT / 64) * 32 * EPI_STRIDE;
+    constexpr bool EPI_IN_STAGE = EPI_FLOATS * 4 <= STAGE * 2 && C::NT * 8 <= STAGE * 2;
+    __shared__ __attribute__((aligned(16))) uint16_t st0[STAGE];
+    __shared__ __attribute__((aligned(16))) uint16_t st1[STAGE];
+    __shared__ __attribute__((aligned(16))) uint16_t st2[STAGE];
+    __shared__ __attribute__((aligned(16))) float epi_extra[EPI_IN_STAGE ? 4 : EPI_FLOATS];
+    float* const scratch = EPI_IN_STAGE ? reinterpret_cast<float*>(st0) : epi_extra;
 
     int64_t tm, tn;
     tile_of(tiles_m, tiles_n, group_m, tm, tn);
@@ -158,33 +182,58 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
 
-    // Two register sets hold K slices in flight: slice s+2 is requested while slice s is
-    // multiplied out of LDS and slice s+1 waits in registers for its LDS stage.
-    u16x8 a0[C::A_CH], al0[HAS_LO ? C::A_CH : 1], b0[C::B_CH];
-    u16x8 a1[C::A_CH], al1[HAS_LO ? C::A_CH : 1], b1[C::B_CH];
-    RowPtrs<C::A_CH, C::NT> pa, pal;
-    RowPtrs<C::B_CH, C::NT> pb;
-    pa.init(Ahi, lda, M, m0, kbeg);
-    if constexpr (HAS_LO) pal.init(Alo, lda, M, m0, kbeg);
-    pb.init(B, ldb, N, n0, kbeg);
-    // Full, aligned slices run through the pipelined loop with unchecked 16-byte loads; a
-    // partial last slice (or every slice of unaligned operands) goes through the checked tail.
-    const int64_t nfull = vec ? (kend - kbeg) / BK : 0;
-#define RQ_GLOAD(RA, RAL, RB, S)                                                                \
-    do {                                                                                        \
-        pa.load(RA, (S) * BK);                                                                  \
-        if constexpr (HAS_LO) pal.load(RAL, (S) * BK);                                          \
-        pb.load(RB, (S) * BK);                                                                  \
-    } while (0)
-#define RQ_LSTORE(RA, RAL, RB, ST)                                                              \
-    do {                                                                                        \
-        uint16_t* base_ = smem + (ST) * STAGE;                                                  \
-        store_rows<C::A_CH, C::NT>(RA, base_);                                                  \
-        if constexpr (HAS_LO) store_rows<C::A_CH, C::NT>(RAL, base_ + C::BM * LDS_STRIDE);      \
-        store_rows<C::B_CH, C::NT>(RB, base_ + A_ROWS * LDS_STRIDE);                            \
-    } while (0)
-    auto compute = [&](int st) {
-        const uint16_t* sA = smem + st * STAGE;
+    // K pipeline.  Full, aligned 32-wide slices are fetched straight into LDS with
+    // global_load_lds_dwordx4 (lane i of a wave instruction fills bytes [16i, 16i+16) of a
+    // 1 KB run = 16 rows x 4 chunks); the lane picks the global chunk whose swizzled LDS
+    // position that is.  Three stages rotate: slice s+2 is in flight while slice s is
+    // multiplied and slice s+1 lands.  A partial last slice, or every slice of unaligned
+    // operands, goes through the checked register path.
+    constexpr int NW = C::NT / 64;
+    constexpr int A_RUNS = C::BM / 16 / NW, B_RUNS = C::BN / 16 / NW;  // 1 KB runs per wave per slice
+    constexpr int DMA_PER_SLICE = A_RUNS * (HAS_LO ? 2 : 1) + B_RUNS;
+    static_assert(C::BM % (16 * NW) == 0 && C::BN % (16 * NW) == 0, "tile rows must split into wave runs");
+    const uint16_t* pA[A_RUNS];
+    const uint16_t* pAl[HAS_LO ? A_RUNS : 1];
+    const uint16_t* pB[B_RUNS];
+    {
+        const int lr = lane >> 2, pc = lane & 3;
+#pragma unroll
+        for (int q = 0; q < A_RUNS; ++q) {
+            const int r = 16 * (wave + NW * q) + lr;
+            const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
+            const int64_t gr = min(m0 + r, M - 1);
+            pA[q] = Ahi + gr * lda + kbeg + c * 8;
+            if constexpr (HAS_LO) pAl[q] = Alo + gr * lda + kbeg + c * 8;
+        }
+#pragma unroll
+        for (int q = 0; q < B_RUNS; ++q) {
+            const int r = 16 * (wave + NW * q) + lr;
+            const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
+            const int64_t gr = min(n0 + r, N - 1);
+            pB[q] = B + gr * ldb + kbeg + c * 8;
+        }
+    }
+    auto issue = [&](int64_t s, uint16_t* stage) {
+        const int64_t off = s * BK;
+#pragma unroll
+        for (int q = 0; q < A_RUNS; ++q) {
+            const uint32_t d = __builtin_amdgcn_readfirstlane(lds_addr(stage + (wave + NW * q) * 16 * LDS_STRIDE));
+            dma16(pA[q] + off, d);
+            if constexpr (HAS_LO) dma16(pAl[q] + off, d + C::BM * LDS_STRIDE * 2);
+        }
+#pragma unroll
+        for (int q = 0; q < B_RUNS; ++q) {
+            const uint32_t d =
+                __builtin_amdgcn_readfirstlane(lds_addr(stage + (A_ROWS + (wave + NW * q) * 16) * LDS_STRIDE));
+            dma16(pB[q] + off, d);
+        }
+    };
+    // wait until at most n direct-to-LDS loads of this wave are outstanding
+    auto wait_vm = [](int n) {
+        if (n >= DMA_PER_SLICE) wait_vmcnt<DMA_PER_SLICE>();
+        else wait_vmcnt<0>();
+    };
+    auto compute = [&](const uint16_t* sA) {
         const uint16_t* sAl = sA + C::BM * LDS_STRIDE;
         const uint16_t* sB = sA + A_ROWS * LDS_STRIDE;
 #pragma unroll
@@ -208,42 +257,67 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
                 }
         }
     };
-
-    if (nfull > 0) RQ_GLOAD(a0, al0, b0, 0);
-    if (nfull > 1) RQ_GLOAD(a1, al1, b1, 1);
-    if (nfull > 0) RQ_LSTORE(a0, al0, b0, 0);
+    // Refill one stage and multiply out of another.  The two stage pointers are restrict
+    // parameters so that, once inlined, the compiler knows the direct-to-LDS writes cannot
+    // touch the stage being read and does not wait for them before the LDS reads.
+    auto step = [&](int64_t s, bool refill, uint16_t* fill, const uint16_t* read) {
+        if (refill) {
+            const int64_t off = s * BK;
+#pragma unroll
+            for (int q = 0; q < A_RUNS; ++q) {
+                const uint32_t d = __builtin_amdgcn_readfirstlane(lds_addr(fill + (wave + NW * q) * 16 * LDS_STRIDE));
+                dma16(pA[q] + off, d);
+                if constexpr (HAS_LO) dma16(pAl[q] + off, d + C::BM * LDS_STRIDE * 2);
+            }
+#pragma unroll
+            for (int q = 0; q < B_RUNS; ++q) {
+                const uint32_t d =
+                    __builtin_amdgcn_readfirstlane(lds_addr(fill + (A_ROWS + (wave + NW * q) * 16) * LDS_STRIDE));
+                dma16(pB[q] + off, d);
+            }
+        }
+        compute(read);
+    };
+    const int64_t nfull = vec ? (kend - kbeg) / BK : 0;
+    // one slice: wait until this slice has landed (the next may stay in flight), barrier (all
+    // waves' loads visible; the stage read two slices ago is free), refill it, multiply.
+#define RQ_STEP(S, CUR, NXT2)                                      \
+    do {                                                           \
+        wait_vm((S) + 1 < nfull ? DMA_PER_SLICE : 0);              \
+        __builtin_amdgcn_s_barrier();                              \
+        step((S) + 2, (S) + 2 < nfull, NXT2, CUR);                 \
+    } while (0)
+    if (nfull > 0) issue(0, st0);
+    if (nfull > 1) issue(1, st1);
+    for (int64_t s = 0; s < nfull; s += 3) {
+        RQ_STEP(s, st0, st2);
+        if (s + 1 >= nfull) break;
+        RQ_STEP(s + 1, st1, st0);
+        if (s + 2 >= nfull) break;
+        RQ_STEP(s + 2, st2, st1);
+    }
+#undef RQ_STEP
+    wait_vmcnt<0>();
     __syncthreads();
-    for (int64_t it = 0; it < nfull; it += 2) {
-        // even slice `it` in stage 0; set 1 holds slice it+1; set 0 is free for slice it+2
-        if (it + 2 < nfull) RQ_GLOAD(a0, al0, b0, it + 2);
-        compute(0);
-        if (it + 1 < nfull) RQ_LSTORE(a1, al1, b1, 1);
-        __syncthreads();
-        if (it + 1 >= nfull) break;
-        // odd slice it+1 in stage 1; set 0 holds slice it+2; set 1 is free for slice it+3
-        if (it + 3 < nfull) RQ_GLOAD(a1, al1, b1, it + 3);
-        compute(1);
-        if (it + 2 < nfull) RQ_LSTORE(a0, al0, b0, 0);
-        __syncthreads();
-    }
-    for (int64_t s = nfull; s < nk; ++s) {  // checked tail, single-buffered
+    for (int64_t s = nfull; s < nk; ++s) {  // checked tail, single-buffered in stage 0
         const int64_t k0 = kbeg + s * BK;
-        load_rows<C::A_CH, C::NT>(a0, Ahi, lda, M, m0, k0, kend, vec);
-        if constexpr (HAS_LO) load_rows<C::A_CH, C::NT>(al0, Alo, lda, M, m0, k0, kend, vec);
-        load_rows<C::B_CH, C::NT>(b0, B, ldb, N, n0, k0, kend, vec);
-        RQ_LSTORE(a0, al0, b0, 0);
+        u16x8 ra[C::A_CH], ral[HAS_LO ? C::A_CH : 1], rb[C::B_CH];
+        load_rows<C::A_CH, C::NT>(ra, Ahi, lda, M, m0, k0, kend, vec);
+        if constexpr (HAS_LO) load_rows<C::A_CH, C::NT>(ral, Alo, lda, M, m0, k0, kend, vec);
+        load_rows<C::B_CH, C::NT>(rb, B, ldb, N, n0, k0, kend, vec);
+        store_rows<C::A_CH, C::NT>(ra, st0);
+        if constexpr (HAS_LO) store_rows<C::A_CH, C::NT>(ral, st0 + C::BM * LDS_STRIDE);
+        store_rows<C::B_CH, C::NT>(rb, st0 + A_ROWS * LDS_STRIDE);
         __syncthreads();
-        compute(0);
+        compute(st0);
         __syncthreads();
     }
-#undef RQ_GLOAD
-#undef RQ_LSTORE
 
     // Epilogue.  Element (row, col) of a 32x32 tile held by this lane in acc[e] is
     // row = 8*(e/4) + 4*(lane/32) + e%4, col = lane%32.  Each tile is restaged through
     // LDS so that a lane then owns 4 consecutive columns of a row (16-byte accesses).
     float aux = 0.f;
-    float* scr = reinterpret_cast<float*>(smem) + wave * (32 * EPI_STRIDE);
+    float* scr = scratch + wave * (32 * EPI_STRIDE);
     const int64_t z = blockIdx.z;
 #pragma unroll
     for (int i = 0; i < C::SM; ++i)
@@ -276,7 +350,7 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
         }
     if constexpr (Epi::kReduce) {
         // deterministic block reduction of the per-thread partial sums (reuses the LDS stage)
-        double* red = reinterpret_cast<double*>(smem);
+        double* red = reinterpret_cast<double*>(st1);
         red[threadIdx.x] = (double)aux;
         __syncthreads();
         for (int s = C::NT / 2; s > 0; s >>= 1) {
@@ -438,8 +512,10 @@ static int64_t tiles_of(int64_t M, int64_t N) {
 
 static bool use_large(int64_t M, int64_t N) { return tiles_of<CfgLarge>(M, N) >= kLargeMinTiles; }
 
-int64_t gemm_num_blocks(int64_t M, int64_t N) {
-    return use_large(M, N) ? tiles_of<CfgLarge>(M, N) : tiles_of<CfgSmall>(M, N);
+static bool pick_large(int64_t M, int64_t N, int tile) { return tile == 1 || (tile == 0 && use_large(M, N)); }
+
+int64_t gemm_num_blocks(int64_t M, int64_t N, int tile) {
+    return pick_large(M, N, tile) ? tiles_of<CfgLarge>(M, N) : tiles_of<CfgSmall>(M, N);
 }
 
 int64_t gemm_effective_splits(int64_t K, int64_t splits) {
@@ -478,7 +554,7 @@ static hipError_t launch_cfg(const GemmArgs& g, const Epi& epi, hipStream_t stre
 template <class Epi>
 static hipError_t launch(const GemmArgs& g, const Epi& epi, hipStream_t stream) {
     if (g.M <= 0 || g.N <= 0) return hipSuccess;
-    if (use_large(g.M, g.N)) return launch_cfg<CfgLarge>(g, epi, stream);
+    if (pick_large(g.M, g.N, g.tile)) return launch_cfg<CfgLarge>(g, epi, stream);
     return launch_cfg<CfgSmall>(g, epi, stream);
 }
 

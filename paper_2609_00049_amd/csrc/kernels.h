@@ -17,9 +17,10 @@ struct GemmArgs {
     int64_t M, N, K;
     int64_t splits;
     int64_t group_m = 0;  // row tiles walked together per XCD (0 = chosen from the shape)
+    int tile = 0;         // 0: chosen from the shape, 1: 256x256 tile, 2: 128x128 tile
 };
 int64_t gemm_effective_splits(int64_t K, int64_t splits);
-int64_t gemm_num_blocks(int64_t M, int64_t N);
+int64_t gemm_num_blocks(int64_t M, int64_t N, int tile = 0);
 hipError_t gemm_store_f32(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, float alpha, hipStream_t st);
 // Split-K gradient slices C[z][i][j] = acc, always on the 256x256 tile; gemm_grad_blocks gives its tile count.
 int64_t gemm_grad_blocks(int64_t M, int64_t N);
