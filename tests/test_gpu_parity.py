@@ -202,3 +202,64 @@ def test_layer_qwen_mlp_full_size_sampled_rows(rq, ctx):
     R = oracle.residual(Wg, L.W0[rows].astype(np.float64), L.X.astype(np.float64), L.Xhat.astype(np.float64))
     lg = oracle.surrogate_loss(R, L.s.astype(np.float64), None, L.X.shape[0])
     assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+
+
+# ============================================================================ dense metric and sliding window
+
+def _wishart(m, seed):
+    r = np.random.default_rng(seed)
+    A = r.standard_normal((m, 2 * m))
+    return (A @ A.T / (2 * m)).astype(np.float32)
+
+
+def test_layer_dense_metric(rq, ctx):
+    """Dense surrogate metric M (Eq. fisher_loss with a full Fisher), rows coupled through M."""
+    torch = _torch()
+    L = synth.make_module("qwen3_32b_layer", "q", m=256, n=384, T=2048)
+    L.M = _wishart(256, 11)
+    _banner("layer dense metric m=256 n=384 T=2048")
+    W0, X, Xh, s, M = P.to_device(L, torch)
+    lr = 2e-4
+    g = rq.quantize_layer(ctx, W0, X, Xh, s, M, qp=rq.qparams(), bgd=rq.bgd_params(steps=4, lr=lr))
+    torch.cuda.synchronize()
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, M=L.M, steps=4, lr=lr)
+    met = P.compare(g, o)
+    _assert_parity(met)
+    # final loss with the dense metric, from the GPU weights and the oracle's formula
+    Wg = g.W_hat.cpu().numpy().astype(np.float64)
+    R = oracle.residual(Wg, L.W0.astype(np.float64), L.X.astype(np.float64), L.Xhat.astype(np.float64))
+    lg = oracle.surrogate_loss(R, None, L.M.astype(np.float64), L.X.shape[0])
+    assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+
+
+@pytest.mark.parametrize("window", [(0, 3), (2, 6)])
+def test_layer_sliding_window(rq, ctx, window):
+    """Window partner P = W_next^T W_next blended with alpha of Eq. slide_window."""
+    torch = _torch()
+    L = synth.make_module("llama3.1_8b_layer", "q", m=256, n=384, T=2048)
+    r = np.random.default_rng(12)
+    Wn = (r.standard_normal((192, 256)) * 0.05).astype(np.float32)
+    Pm = oracle.pullback_metric(Wn).astype(np.float32)
+    _banner(f"layer window {window}")
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    Pd = torch.from_numpy(Pm).cuda()
+    lr = L.lr
+    g = rq.quantize_layer(ctx, W0, X, Xh, s, None, Pd, qp=rq.qparams(), bgd=rq.bgd_params(steps=3, lr=lr),
+                          window=window)
+    torch.cuda.synchronize()
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, P=Pm, steps=3, lr=lr, window=window)
+    _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
+
+
+def test_layer_llama_gate_shape_sampled_rows(rq, ctx):
+    """14336x4096 gate projection at 8192 tokens (full m and n), oracle on sampled rows."""
+    L = synth.make_module("llama3.1_8b_layer", "gate", T=8192)
+    _banner("layer llama3.1-8b gate 14336x4096 T=8192")
+    g = _run(rq, ctx, L, L.steps, L.lr)
+    rows = np.random.default_rng(8).choice(L.W0.shape[0], 6, replace=False)
+    o = _oracle(L, L.steps, L.lr, rows=rows)
+    _assert_parity(P.compare(g, o, rows=rows))
+    Wg = g.W_hat.cpu().numpy().astype(np.float64)[rows]
+    R = oracle.residual(Wg, L.W0[rows].astype(np.float64), L.X.astype(np.float64), L.Xhat.astype(np.float64))
+    lg = oracle.surrogate_loss(R, None, None, L.X.shape[0])
+    assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
