@@ -133,6 +133,10 @@ int realq_bgd_state_create(realq_ctx* ctx, realq_bgd_state** out, const float* W
 void realq_bgd_state_destroy(realq_bgd_state* st);
 
 /* ------------------------------------------------------------------ a3-a6: one column block
+ * W is the caller's float64 working copy of the weights [m, n] (device, row-major),
+ * started from W0 and changed only by these calls: every column takes many small
+ * updates before it is quantized, and float64 keeps its rounding decisions those of
+ * exact arithmetic.
  * Quantize columns [c0, c0+bs) of W (in place; the block is written back
  * dequantized) following Alg. 1's inner loop: dead columns of the block are zeroed,
  * group (scale, zero) parameters are searched when a group starts, each column is
@@ -143,9 +147,10 @@ void realq_bgd_state_destroy(realq_bgd_state* st);
  * group that started in an earlier block are read back from scales/zeros.
  * U and dead come from realq_chol_inverse.  When st != NULL the residual base of
  * the state is also advanced by the locked block (Sec. 4.3: quantized weights stay
- * locked).  Requirements: c0 % block-boundaries as produced by walking the columns
- * in order, bs <= 128. */
-int realq_quantize_block(realq_ctx* ctx, float* W /*[m,n]*/, int64_t m, int64_t n, int64_t c0, int64_t bs,
+ * locked).  Requirements: c0 is a multiple of qp->block, bs == qp->block except for
+ * the last block (c0 + bs == n), bs <= 128, and blocks are quantized in column order;
+ * otherwise REALQ_ERR_SHAPE. */
+int realq_quantize_block(realq_ctx* ctx, double* W /*[m,n]*/, int64_t m, int64_t n, int64_t c0, int64_t bs,
                          const float* U /*[n,n]*/, const uint8_t* dead /*[n]|NULL*/, const realq_qparams* qp,
                          uint8_t* codes /*[m,n]*/, float* scales, uint8_t* zeros, realq_bgd_state* st);
 
@@ -156,12 +161,32 @@ int realq_quantize_block(realq_ctx* ctx, float* W /*[m,n]*/, int64_t m, int64_t 
  * (1/T) M_a R diag(s) Xhat[:, c1:] is formed with token-streamed GEMMs.
  * loss_out (device float64 scalar, may be NULL) receives L before the update; it
  * is computed for M_a = identity only and set to NaN otherwise.  c1 == n is a no-op. */
-int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, float* W /*[m,n]*/, int64_t c1, float alpha,
+int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W /*[m,n]*/, int64_t c1, float alpha,
                    double* loss_out);
 
 /* Final surrogate loss with the module's own metric (alpha = 1) at the current W,
  * written to *loss_out (device float64).  M = identity only (else REALQ_ERR_SHAPE). */
-int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const float* W, double* loss_out);
+int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const double* W /*[m,n]*/, double* loss_out);
+
+/* ------------------------------------------------------------------ a10: window partner and hand-off
+ * Sec. 4.4 (Eq. slide_window) blends this module's objective with the next stage's.  For a
+ * linear consumer y' = W_next y of this module's output, a perturbation dy costs
+ * dy^T P dy with P = W_next^T M_next W_next (M_next = NULL: identity).
+ *   W_next : [m_next, m] float32;  M_next : [m_next, m_next] float32 | NULL;
+ *   P      : [m, m] float32 output; accumulate != 0 adds to P (several consumers, e.g. gate and up).
+ * Computed in float32. */
+int realq_pullback_metric(realq_ctx* ctx, const float* W_next, const float* M_next, int64_t m_next, int64_t m,
+                          int accumulate, float* P);
+
+/* Hand-off to the next module of a layer: the inputs the next module sees.
+ *   Wb == NULL : Y[t, i] = bf16( sum_j Wa[i, j] X[t, j] )                  (q -> o, o -> gate/up)
+ *   Wb != NULL : Y[t, i] = bf16( silu(sum_j Wa[i,j] X[t,j]) * sum_j Wb[i,j] X[t,j] ),
+ *                silu(g) = g / (1 + e^-g)                                     (gate, up -> down)
+ * Wa, Wb: [m, n] float32 (quantized or original weights); X: [T, n] bf16; Y: [T, m] bf16,
+ * rounded to nearest even.  Products are accumulated in float32 (weights carried as bf16
+ * hi/lo pairs against the bf16 activations).  T == 0 is a no-op. */
+int realq_handoff(realq_ctx* ctx, const float* Wa, const float* Wb, const uint16_t* X, int64_t T, int64_t n,
+                  int64_t m, uint16_t* Y);
 
 /* ------------------------------------------------------------------ a1-a11: whole module
  * The whole sweep for one module: Hessian over all tokens, inverse factor, then for

@@ -32,7 +32,11 @@ with the per-layer surrogate of the readings below):
 Readings where the paper is silent (each is listed in the design notes):
   * quantizer: asymmetric, per (row, group of ``group`` columns), joint search
     over ``grid`` shrink factors p_k = 1 - k/100 and all 2^bits zero points,
-    minimising squared error; ties broken by (err, k, |z - z_nat(k)|, z);
+    minimising squared error; errors within 2^-40 (relative) of the minimum, plus
+    2^-60 of the group's sum of squares, count as equal (an exact tie can come out either
+    way in floating point, depending on the order of the sum), and among those the least
+    (k, |z - z_nat|, z) wins, with the
+    natural zero z_nat = rint(-lo maxq / (hi - lo)) of the unshrunk range;
     round-half-to-even; parameters fixed from the weights as they stand when the
     group's first column is reached;
   * damping: dead columns (H_jj == 0) get H_jj = 1 and their weights zeroed, then
@@ -120,14 +124,23 @@ class QParams:
         return (1 << self.bits) - 1
 
 
+TIE_RTOL = 2.0 ** -40   # search errors within TIE_RTOL * least + TIE_ATOL * sum x^2 are one tie
+TIE_ATOL = 2.0 ** -60
+
+
 def group_search(x: np.ndarray, qp: QParams, row_chunk: int = 32) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """Best asymmetric (scale, zero) per row of ``x`` ([rows, g]).
 
     For each row: lo = min(0, min x), hi = max(0, max x) (lo = -1, hi = 1 when both
     are 0).  Candidate k has scale s_k = p_k (hi - lo) / maxq; every zero point
     z in 0..maxq is tried, with codes q = clamp(rint(x / s_k) + z, 0, maxq) and
-    squared error sum_j (x_j - s_k (q_j - z))^2.  The winner is the lexicographic
-    minimum of (err, k, |z - z_nat(k)|, z), z_nat(k) = clamp(rint(-p_k lo / s_k), 0, maxq).
+    squared error sum_j (x_j - s_k (q_j - z))^2.  Candidates whose error is at most
+    least * (1 + TIE_RTOL) + TIE_ATOL * sum_j x_j^2 are equal (the absolute part makes
+    errors at rounding level, as in a group lying exactly on a grid, one tie); among them
+    the winner is
+    the lexicographic minimum of (k, |z - z_nat|, z), with
+    z_nat = clamp(rint(-lo maxq / (hi - lo)), 0, maxq) (the shrink factor cancels from
+    -p_k lo / s_k, so one natural zero serves every k, and an exact half stays exact).
 
     Returns (scale [rows], zero [rows] int, err [rows]).
     """
@@ -143,7 +156,7 @@ def group_search(x: np.ndarray, qp: QParams, row_chunk: int = 32) -> Tuple[np.nd
 
 
 def search_table(x: np.ndarray, qp: QParams):
-    """All candidates of the search for rows ``x``: (s [rows,K], err [rows,K,Z], z_nat [rows,K])."""
+    """All candidates of the search for rows ``x``: (s [rows,K], err [rows,K,Z], z_nat [rows])."""
     maxq = qp.maxq
     lo = np.minimum(0.0, x.min(axis=1))
     hi = np.maximum(0.0, x.max(axis=1))
@@ -157,7 +170,7 @@ def search_table(x: np.ndarray, qp: QParams):
     q = np.clip(r[:, :, None, :] + z[None, None, :, None], 0, maxq)   # [rows, K, Z, g]
     d = x[:, None, None, :] - s[:, :, None, None] * (q - z[None, None, :, None])
     err = np.sum(d * d, axis=-1)                            # [rows, K, Z]
-    znat = np.clip(np.rint(-(p[None, :] * lo[:, None]) / s), 0, maxq)  # [rows, K]
+    znat = np.clip(np.rint(-lo * maxq / (hi - lo)), 0, maxq)  # [rows]
     return s, err, znat
 
 
@@ -167,9 +180,10 @@ def _group_search_rows(x, qp):
     rows, K, Z = err.shape
     kk = np.broadcast_to(np.arange(K)[None, :, None], err.shape)
     zz = np.broadcast_to(np.arange(Z)[None, None, :], err.shape)
-    dist = np.abs(zz - znat[:, :, None])
-    # lexicographic minimum of (err, k, dist, z), one key at a time
-    cand = err == err.min(axis=(1, 2), keepdims=True)
+    dist = np.abs(zz - znat[:, None, None])
+    # near-least error first, then the lexicographic minimum of (k, dist, z), one key at a time
+    ss = np.sum(x * x, axis=1)[:, None, None]
+    cand = err <= err.min(axis=(1, 2), keepdims=True) * (1.0 + TIE_RTOL) + TIE_ATOL * ss
     for key in (kk, dist, zz):
         big = np.where(cand, key, np.inf)
         cand &= key == big.min(axis=(1, 2), keepdims=True)
@@ -361,3 +375,64 @@ def pullback_metric(W_next: np.ndarray, M_next: Optional[np.ndarray] = None) -> 
 
 def silu(x):
     return x / (1.0 + np.exp(-x))
+
+
+def bf16(x):
+    """Nearest bfloat16 value of each entry (ties to even), returned as float64.
+
+    The value is first rounded to float32, then to bfloat16 by adding half a bfloat16
+    ulp (minus one when the kept last bit is even) to the float32 bit pattern and
+    truncating; the two roundings agree with a direct rounding except on the rare
+    float32 values that land exactly on a bfloat16 midpoint.
+    """
+    u = np.ascontiguousarray(np.asarray(x, dtype=np.float64).astype(np.float32)).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def handoff(Wa, X, Wb=None):
+    """Inputs the next module of the layer sees (token-major, rounded to bf16).
+
+    Wb is None: Y = X Wa^T (output of a linear module feeding the next one);
+    otherwise Y = silu(X Wa^T) * (X Wb^T) (the SwiGLU input of a down projection).
+    """
+    Y = np.asarray(X, dtype=np.float64) @ np.asarray(Wa, dtype=np.float64).T
+    if Wb is not None:
+        Y = silu(Y) * (np.asarray(X, dtype=np.float64) @ np.asarray(Wb, dtype=np.float64).T)
+    return bf16(Y)
+
+
+def layer_chain(W0s, X0, Xhat0, *, qp: Optional[QParams] = None, steps=0, lr=1e-3, window=True,
+                modules=("q", "k", "v", "o", "gate", "up", "down"), return_inputs=False):
+    """Sweep every module of a synthetic decoder layer in order, handing inputs on.
+
+    q, k, v read the layer input; o reads q's output (a linear stand-in for attention);
+    gate and up read o's output; down reads silu(gate) * up.  The quantized chain feeds
+    quantized outputs forward (Xhat), the full-precision chain the original ones (X).
+    Window partners (Sec. 4.4, per-module reading): q's consumer is o, o's consumers are
+    gate and up, each through P = sum W0_next^T W0_next; B_total is the module's own block
+    count.  Returns {module: LayerResult}, and with return_inputs also {module: (X, Xhat)}.
+    """
+    qp = qp or QParams()
+    res = {}
+    X_in = {"q": (X0, Xhat0), "k": (X0, Xhat0), "v": (X0, Xhat0)}
+    partners = {"q": ["o"], "o": ["gate", "up"]}
+    for name in modules:
+        X, Xh = X_in[name]
+        W0 = W0s[name]
+        P = None
+        win = None
+        if window and name in partners:
+            P = sum(pullback_metric(W0s[p]) for p in partners[name])
+            win = (0, -(-W0.shape[1] // qp.block))
+        r = quantize_layer(W0, X, Xh, P=P, qp=qp, steps=steps, lr=lr, window=win)
+        res[name] = r
+        if name == "q":
+            X_in["o"] = (handoff(W0, X), handoff(r.W_hat, Xh))
+        elif name == "o":
+            X_in["gate"] = X_in["up"] = (handoff(W0, X), handoff(r.W_hat, Xh))
+        elif name == "up":
+            Xg, Xhg = X_in["gate"]
+            X_in["down"] = (handoff(W0s["gate"], Xg, W0),
+                            handoff(res["gate"].W_hat, Xhg, r.W_hat))
+    return (res, X_in) if return_inputs else res

@@ -462,7 +462,7 @@ static int validate_q(realq_ctx* ctx, const realq_qparams* qp) {
     return REALQ_OK;
 }
 
-int realq_quantize_block(realq_ctx* ctx, float* W, int64_t m, int64_t n, int64_t c0, int64_t bs, const float* U,
+int realq_quantize_block(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_t c0, int64_t bs, const float* U,
                          const uint8_t* dead, const realq_qparams* qp, uint8_t* codes, float* scales, uint8_t* zeros,
                          realq_bgd_state* st) {
     if (!ctx) return REALQ_ERR_INVALID_ARG;
@@ -478,7 +478,7 @@ int realq_quantize_block(realq_ctx* ctx, float* W, int64_t m, int64_t n, int64_t
     if (st && (st->m != m || st->n != n))
         return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: state shape differs from W");
     void* E;
-    if ((rc = get_ws(ctx, "q_E", (size_t)m * bs * 4, &E))) return rc;
+    if ((rc = get_ws(ctx, "q_E", (size_t)m * bs * 8, &E))) return rc;
     hipStream_t s = ctx->stream;
     realq::QuantArgs q{};
     q.W = W;
@@ -495,7 +495,7 @@ int realq_quantize_block(realq_ctx* ctx, float* W, int64_t m, int64_t n, int64_t
     q.scales = scales;
     q.zeros = zeros;
     q.ngroups = (n + qp->group - 1) / qp->group;
-    q.E = (float*)E;
+    q.E = (double*)E;
     q.W0 = st ? st->W0 : nullptr;
     q.Dhi = st ? st->Dhi : nullptr;
     q.Dlo = st ? st->Dlo : nullptr;
@@ -505,27 +505,25 @@ int realq_quantize_block(realq_ctx* ctx, float* W, int64_t m, int64_t n, int64_t
     }
     const int64_t c1 = c0 + bs;
     if (c1 < n) {
-        realq::SgemmArgs a{};
-        a.A = (const float*)E;
-        a.lda = bs;
-        a.B = U + c0 * n + c1;
-        a.ldb = n;
-        a.C = W + c1;
-        a.ldc = n;
+        realq::ObsArgs a{};
+        a.E = (const double*)E;
+        a.lde = bs;
+        a.U = U + c0 * n + c1;
+        a.ldu = n;
+        a.W = W + c1;
+        a.ldw = n;
         a.M = m;
         a.N = n - c1;
         a.K = bs;
-        a.alpha = -1.f;
-        a.beta = 1.f;
         if (st) {
             a.W0 = st->W0 + c1;
-            a.ldw = n;
+            a.ldw0 = n;
             a.Dhi = st->Dhi + c1;
             a.Dlo = st->Dlo + c1;
             a.ldd = n;
         }
         Timed tm(ctx, "obs");
-        RQ_HIP(ctx, realq::sgemm(a, s));
+        RQ_HIP(ctx, realq::obs_update(a, s));
     }
     if (st) {
         // lock: B += (W_hat - W0)[:, block] Xhat[:, block]^T
@@ -549,7 +547,7 @@ static int64_t choose_splits(int64_t M, int64_t N, int64_t K) {
     return s < 1 ? 1 : s;
 }
 
-int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, float* W, int64_t c1, float alpha, double* loss_out) {
+int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, float alpha, double* loss_out) {
     if (!ctx || !st) return REALQ_ERR_INVALID_ARG;
     if (!W) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_step: NULL W");
     if (c1 < 0 || c1 > st->n) return set_error(ctx, REALQ_ERR_SHAPE, "bgd_step: need 0 <= c1 <= n");
@@ -664,7 +662,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, float* W, int64_t c1, fl
     return REALQ_OK;
 }
 
-int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const float* W, double* loss_out) {
+int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const double* W, double* loss_out) {
     if (!ctx || !st) return REALQ_ERR_INVALID_ARG;
     if (!W || !loss_out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_loss: NULL W or loss_out");
     if (st->M) return set_error(ctx, REALQ_ERR_SHAPE, "bgd_loss: only the identity metric is supported");
@@ -676,7 +674,7 @@ int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const float* W, double* 
     int rc;
     if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
     RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, ctx->stream));
-    if (nJ > 0) RQ_HIP(ctx, realq::split_diff_f32(W + c1, n, st->W0 + c1, n, st->Dhi + c1, st->Dlo + c1, n, m, nJ,
+    if (nJ > 0) RQ_HIP(ctx, realq::split_diff_f64(W + c1, n, st->W0 + c1, n, st->Dhi + c1, st->Dlo + c1, n, m, nJ,
                                                   ctx->stream));
     for (int64_t ch = 0; ch < nchunks; ++ch) {
         const int64_t t0 = ch * Tc, cur = std::min(Tc, T - t0);
@@ -685,6 +683,79 @@ int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const float* W, double* 
                                      ctx->stream));
     }
     RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)T, loss_out, ctx->stream));
+    return REALQ_OK;
+}
+
+// ============================================================================ a10: window partner and hand-off
+
+int realq_pullback_metric(realq_ctx* ctx, const float* W_next, const float* M_next, int64_t m_next, int64_t m,
+                          int accumulate, float* P) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (m_next <= 0 || m <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "pullback_metric: need m_next, m > 0");
+    if (!W_next || !P) return set_error(ctx, REALQ_ERR_INVALID_ARG, "pullback_metric: NULL W_next or P");
+    hipStream_t s = ctx->stream;
+    void *WT, *T1 = nullptr;
+    int rc;
+    if ((rc = get_ws(ctx, "p_WT", (size_t)m * m_next * 4, &WT))) return rc;
+    RQ_HIP(ctx, realq::transpose_f32(W_next, m, (float*)WT, m_next, m_next, m, s));  // WT = W_next^T [m, m_next]
+    const float* right = W_next;
+    if (M_next) {  // T1 = M_next W_next  [m_next, m]
+        if ((rc = get_ws(ctx, "p_T1", (size_t)m_next * m * 4, &T1))) return rc;
+        realq::SgemmArgs a{};
+        a.A = M_next;
+        a.lda = m_next;
+        a.B = W_next;
+        a.ldb = m;
+        a.C = (float*)T1;
+        a.ldc = m;
+        a.M = m_next;
+        a.N = m;
+        a.K = m_next;
+        a.alpha = 1.f;
+        a.beta = 0.f;
+        RQ_HIP(ctx, realq::sgemm(a, s));
+        right = (const float*)T1;
+    }
+    realq::SgemmArgs a{};
+    a.A = (const float*)WT;
+    a.lda = m_next;
+    a.B = right;
+    a.ldb = m;
+    a.C = P;
+    a.ldc = m;
+    a.M = m;
+    a.N = m;
+    a.K = m_next;
+    a.alpha = 1.f;
+    a.beta = accumulate ? 1.f : 0.f;
+    RQ_HIP(ctx, realq::sgemm(a, s));
+    return REALQ_OK;
+}
+
+int realq_handoff(realq_ctx* ctx, const float* Wa, const float* Wb, const uint16_t* X, int64_t T, int64_t n,
+                  int64_t m, uint16_t* Y) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (T < 0 || n <= 0 || m <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "handoff: need T >= 0, n, m > 0");
+    if (T == 0) return REALQ_OK;
+    if (!Wa || !X || !Y) return set_error(ctx, REALQ_ERR_INVALID_ARG, "handoff: NULL Wa, X or Y");
+    hipStream_t s = ctx->stream;
+    void *hi, *lo;
+    int rc;
+    if ((rc = get_ws(ctx, "h_wh", (size_t)m * n * 2, &hi))) return rc;
+    if ((rc = get_ws(ctx, "h_wl", (size_t)m * n * 2, &lo))) return rc;
+    // acc[i][t] = sum_j W[i][j] X[t][j], stored token-major
+    realq::GemmArgs g{(const uint16_t*)hi, (const uint16_t*)lo, n, X, n, m, T, n, 1};
+    if (!Wb) {
+        RQ_HIP(ctx, realq::split_diff_f32(Wa, n, nullptr, 0, (uint16_t*)hi, (uint16_t*)lo, n, m, n, s));
+        RQ_HIP(ctx, realq::gemm_store_bf16_t(g, Y, m, s));
+        return REALQ_OK;
+    }
+    void* G;
+    if ((rc = get_ws(ctx, "h_gate", (size_t)T * m * 4, &G))) return rc;
+    RQ_HIP(ctx, realq::split_diff_f32(Wa, n, nullptr, 0, (uint16_t*)hi, (uint16_t*)lo, n, m, n, s));
+    RQ_HIP(ctx, realq::gemm_store_f32_t(g, (float*)G, m, s));  // gate pre-activation, token-major
+    RQ_HIP(ctx, realq::split_diff_f32(Wb, n, nullptr, 0, (uint16_t*)hi, (uint16_t*)lo, n, m, n, s));
+    RQ_HIP(ctx, realq::gemm_swiglu_t(g, (const float*)G, m, Y, m, s));
     return REALQ_OK;
 }
 
@@ -733,12 +804,16 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
     const bool bgd = d->bgd.steps > 0;
     if (bgd && (rc = state_init(&st))) return rc;
 
-    RQ_HIP(ctx, hipMemcpyAsync(out->W_hat, d->W0, (size_t)m * n * 4, hipMemcpyDeviceToDevice, s));
+    // float64 working weights; W_hat receives their float32 rounding at the end
+    void* Ww;
+    if ((rc = get_ws(ctx, "l_W", (size_t)m * n * 8, &Ww))) return rc;
+    double* W = (double*)Ww;
+    RQ_HIP(ctx, realq::widen_f32(d->W0, W, m * n, s));
     const int64_t nb = (n + d->q.block - 1) / d->q.block;
     if (out->loss_trace && bgd) RQ_HIP(ctx, realq::fill_f64(out->loss_trace, NAN, nb * d->bgd.steps, s));
     for (int64_t b = 0; b < nb; ++b) {
         const int64_t c0 = b * d->q.block, bs = std::min<int64_t>(d->q.block, n - c0), c1 = c0 + bs;
-        if ((rc = realq_quantize_block(ctx, out->W_hat, m, n, c0, bs, (const float*)Uw, (const uint8_t*)deadw, &d->q,
+        if ((rc = realq_quantize_block(ctx, W, m, n, c0, bs, (const float*)Uw, (const uint8_t*)deadw, &d->q,
                                        out->codes, out->scales, out->zeros, bgd ? &st : nullptr)))
             return rc;
         if (!bgd || c1 >= n) continue;
@@ -750,7 +825,7 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
         }
         for (int k = 0; k < d->bgd.steps; ++k) {
             double* lo = out->loss_trace ? out->loss_trace + b * d->bgd.steps + k : nullptr;
-            if ((rc = realq_bgd_step(ctx, &st, out->W_hat, c1, alpha, lo))) return rc;
+            if ((rc = realq_bgd_step(ctx, &st, W, c1, alpha, lo))) return rc;
         }
     }
     // a11: final loss (own metric) at the quantized weights
@@ -763,8 +838,9 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
             st.prm.tok_chunk = d->bgd.tok_chunk;
             if ((rc = state_init(&st))) return rc;
         }
-        if ((rc = realq_bgd_loss(ctx, &st, out->W_hat, (double*)lf))) return rc;
+        if ((rc = realq_bgd_loss(ctx, &st, W, (double*)lf))) return rc;
     }
+    RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat, m * n, s));
     RQ_HIP(ctx, hipEventRecord(ev1, s));
     if (!d->M) RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lf, 8, hipMemcpyDeviceToHost, s));
     RQ_HIP(ctx, hipStreamSynchronize(s));

@@ -94,6 +94,33 @@ hipError_t transpose_scale_split(const uint16_t* in, int64_t ldi, const float* s
     return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void transpose_f32_kernel(const float* __restrict__ in, int64_t ldi,
+                                                            float* __restrict__ out, int64_t ldo, int64_t rows,
+                                                            int64_t cols, int64_t tiles_c) {
+    __shared__ float tile[64][65];
+    const int64_t tr = blockIdx.x / tiles_c, tc = blockIdx.x % tiles_c;
+    const int64_t r0 = tr * 64, c0 = tc * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int rr = ty; rr < 64; rr += 4) {
+        const int64_t r = r0 + rr, c = c0 + tx;
+        tile[rr][tx] = (r < rows && c < cols) ? in[r * ldi + c] : 0.f;
+    }
+    __syncthreads();
+    for (int cc = ty; cc < 64; cc += 4) {
+        const int64_t c = c0 + cc, r = r0 + tx;
+        if (r < rows && c < cols) out[c * ldo + r] = tile[tx][cc];
+    }
+}
+
+hipError_t transpose_f32(const float* in, int64_t ldi, float* out, int64_t ldo, int64_t rows, int64_t cols,
+                         hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    const int64_t tr = (rows + 63) / 64, tc = (cols + 63) / 64;
+    hipLaunchKernelGGL(transpose_f32_kernel, dim3((unsigned)(tr * tc)), dim3(256), 0, st, in, ldi, out, ldo, rows,
+                       cols, tc);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- splits
 __global__ void split_diff_f32_kernel(const float* __restrict__ A, int64_t lda, const float* __restrict__ Bm,
                                       int64_t ldb, uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, int64_t ld,
@@ -108,6 +135,51 @@ __global__ void split_diff_f32_kernel(const float* __restrict__ A, int64_t lda, 
         hi[i * ld + j] = h;
         lo[i * ld + j] = l;
     }
+}
+
+__global__ void split_diff_f64_kernel(const double* __restrict__ A, int64_t lda, const float* __restrict__ Bm,
+                                      int64_t ldb, uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, int64_t ld,
+                                      int64_t rows, int64_t cols) {
+    const int64_t total = rows * cols;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / cols, j = e % cols;
+        const float v = (float)(A[i * lda + j] - (double)Bm[i * ldb + j]);
+        uint16_t h, l;
+        split_bf16(v, h, l);
+        hi[i * ld + j] = h;
+        lo[i * ld + j] = l;
+    }
+}
+
+hipError_t split_diff_f64(const double* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
+                          int64_t ld, int64_t rows, int64_t cols, hipStream_t st) {
+    const int64_t total = rows * cols;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(split_diff_f64_kernel, dim3(grid_for(total, 4)), dim3(TB), 0, st, A, lda, Bm, ldb, hi, lo, ld,
+                       rows, cols);
+    return hipGetLastError();
+}
+
+__global__ void widen_kernel(const float* __restrict__ in, double* __restrict__ out, int64_t count) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x)
+        out[e] = (double)in[e];
+}
+
+__global__ void narrow_kernel(const double* __restrict__ in, float* __restrict__ out, int64_t count) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x)
+        out[e] = (float)in[e];
+}
+
+hipError_t widen_f32(const float* in, double* out, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(widen_kernel, dim3(grid_for(count, 4)), dim3(TB), 0, st, in, out, count);
+    return hipGetLastError();
+}
+
+hipError_t narrow_f64(const double* in, float* out, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(narrow_kernel, dim3(grid_for(count, 4)), dim3(TB), 0, st, in, out, count);
+    return hipGetLastError();
 }
 
 hipError_t split_diff_f32(const float* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
@@ -158,7 +230,8 @@ hipError_t reduce_partials(const double* partials, int64_t count, double scale, 
 
 // ---------------------------------------------------------------- split-K reduction + Adam
 // Bias-corrected Adam in the Kingma-Ba form: m = b1 m + (1-b1) g, v = b2 v + (1-b2) g^2,
-// w -= lr * (m * bc1) / (sqrt(v * bc2) + eps).
+// w -= lr * (m * bc1) / (sqrt(v * bc2) + eps).  The moments and the step are float32; the
+// step is added to the float64 working weight.
 __device__ __forceinline__ void adam_elem(const AdamArgs& a, int64_t i, int64_t j, float g) {
     const int64_t idx = i * a.n + j;
     float mv = a.beta1 * a.mA[idx] + (1.f - a.beta1) * g;
@@ -167,10 +240,10 @@ __device__ __forceinline__ void adam_elem(const AdamArgs& a, int64_t i, int64_t 
     a.vA[idx] = vv;
     float mh = mv * a.bc1;
     float vh = vv * a.bc2;
-    float w = a.W[idx] - a.lr * mh / (sqrtf(vh) + a.eps);
+    const double w = a.W[idx] - (double)(a.lr * mh / (sqrtf(vh) + a.eps));
     a.W[idx] = w;
     uint16_t h, l;
-    split_bf16(w - a.W0[idx], h, l);
+    split_bf16((float)(w - (double)a.W0[idx]), h, l);
     a.Dhi[idx] = h;
     a.Dlo[idx] = l;
 }

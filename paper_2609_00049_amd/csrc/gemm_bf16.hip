@@ -16,8 +16,9 @@
 //   large: 256 x 256 block tile, 8 wave64s as 4 (M) x 2 (N), 64 x 128 per wave
 //   small: 128 x 128 block tile, 4 wave64s as 2 x 2,        64 x 64 per wave
 // with v_mfma_f32_32x32x16_bf16 (accumulators live in AGPRs).  K advances in
-// slices of 32 through a double-buffered LDS stage, one barrier per slice, with
-// the next slice's global loads in flight during the MFMAs.  Blocks are renumbered
+// slices of 32 through a ring of three LDS stages filled by direct-to-LDS 16-byte
+// loads, so two slices are in flight while the MFMAs consume the third; one barrier
+// per slice, with explicit vmcnt waits.  Blocks are renumbered
 // so that each XCD (blocks are dealt round-robin over the 8 XCDs) owns a contiguous
 // run of tiles, walked in groups of `group_m` row tiles for L2 reuse.  Split-K over
 // gridDim.z with a fixed K range per split (deterministic).
@@ -73,28 +74,6 @@ __device__ __forceinline__ void load_rows(u16x8 (&v)[CH], const uint16_t* __rest
         v[c] = x;
     }
 }
-
-// Per-thread row pointers of one operand tile: chunk c of this thread covers row
-// min(r0 + r, rows - 1) (rows past the end are clamped; their products only reach
-// accumulators the epilogue masks) at k offset kc.
-template <int CH, int NT>
-struct RowPtrs {
-    const uint16_t* p[CH];
-    __device__ __forceinline__ void init(const uint16_t* __restrict__ P, int64_t ld, int64_t rows, int64_t r0,
-                                         int64_t k0) {
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int chunk = threadIdx.x + c * NT;
-            const int64_t gr = min(r0 + (chunk >> 2), rows - 1);
-            p[c] = P + gr * ld + k0 + (chunk & 3) * 8;
-        }
-    }
-    // full 32-wide slice at k offset `off` from the start, 16-byte loads, no checks
-    __device__ __forceinline__ void load(u16x8 (&v)[CH], int64_t off) const {
-#pragma unroll
-        for (int c = 0; c < CH; ++c) v[c] = *reinterpret_cast<const u16x8*>(p[c] + off);
-    }
-};
 
 template <int CH, int NT>
 __device__ __forceinline__ void store_rows(const u16x8 (&v)[CH], uint16_t* lds) {
@@ -329,20 +308,44 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
             __syncthreads();
             const int64_t r0 = m0 + wm * C::WTM + i * 32;
             const int64_t c0 = n0 + wn * C::WTN + j * 32;
-            const int cc = (lane & 7) * 4;
-            const int64_t col = c0 + cc;
+            if constexpr (!Epi::kTransposed) {
+                // lane owns 4 consecutive columns of one row
+                const int cc = (lane & 7) * 4;
+                const int64_t col = c0 + cc;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int rr = q * 8 + (lane >> 3);
+                for (int q = 0; q < 4; ++q) {
+                    const int rr = q * 8 + (lane >> 3);
+                    const int64_t row = r0 + rr;
+                    const f32x4 v = *reinterpret_cast<const f32x4*>(scr + rr * EPI_STRIDE + cc);
+                    if (row < M) {
+                        if (col + 3 < N) {
+                            epi.vec4(row, col, v, z, aux);
+                        } else {
+#pragma unroll
+                            for (int u = 0; u < 4; ++u)
+                                if (col + u < N) epi(row, col + u, v[u], z, aux);
+                        }
+                    }
+                }
+            } else {
+                // lane owns 4 consecutive rows of one column (outputs stored column-major)
+                const int rr = (lane & 7) * 4;
                 const int64_t row = r0 + rr;
-                const f32x4 v = *reinterpret_cast<const f32x4*>(scr + rr * EPI_STRIDE + cc);
-                if (row < M) {
-                    if (col + 3 < N) {
-                        epi.vec4(row, col, v, z, aux);
-                    } else {
 #pragma unroll
-                        for (int u = 0; u < 4; ++u)
-                            if (col + u < N) epi(row, col + u, v[u], z, aux);
+                for (int q = 0; q < 4; ++q) {
+                    const int cc = q * 8 + (lane >> 3);
+                    const int64_t col = c0 + cc;
+                    f32x4 v;
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) v[u] = scr[(rr + u) * EPI_STRIDE + cc];
+                    if (col < N) {
+                        if (row + 3 < M) {
+                            epi.vec4t(row, col, v, z, aux);
+                        } else {
+#pragma unroll
+                            for (int u = 0; u < 4; ++u)
+                                if (row + u < M) epi(row + u, col, v[u], z, aux);
+                        }
                     }
                 }
             }
@@ -371,6 +374,7 @@ typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 
 struct EpiStoreF32 {  // C[z][i][j] = alpha * acc
     static constexpr bool kReduce = false;
+    static constexpr bool kTransposed = false;
     float* C;
     int64_t ldc, split_stride;
     float alpha;
@@ -394,6 +398,7 @@ struct EpiGrad : EpiStoreF32 {};
 
 struct EpiAccF32 {  // C[i][j] += alpha * acc
     static constexpr bool kReduce = false;
+    static constexpr bool kTransposed = false;
     float* C;
     int64_t ldc;
     float alpha;
@@ -412,6 +417,7 @@ struct EpiAccF32 {  // C[i][j] += alpha * acc
 
 struct EpiAccF64 {  // C[i][j] += acc   (float64 accumulator across chunks)
     static constexpr bool kReduce = false;
+    static constexpr bool kTransposed = false;
     double* C;
     int64_t ldc;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { C[i * ldc + j] += (double)v; }
@@ -424,6 +430,7 @@ struct EpiAccF64 {  // C[i][j] += acc   (float64 accumulator across chunks)
 // Residual: R = B0[i][t] + acc; writes split(R * s_t) and accumulates s_t R^2.
 struct EpiResid {
     static constexpr bool kReduce = true;
+    static constexpr bool kTransposed = false;
     const float* B0;
     int64_t ldb0;
     const float* s;
@@ -471,6 +478,7 @@ struct EpiResid {
 // Residual loss only (no outputs besides the partial sums): s_t (B0 + acc)^2.
 struct EpiLoss {
     static constexpr bool kReduce = true;
+    static constexpr bool kTransposed = false;
     const float* B0;
     int64_t ldb0;
     const float* s;
@@ -486,14 +494,67 @@ struct EpiLoss {
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
 
-// Transposed bf16 store: out[j][i] = bf16(acc) (hand-off of layer outputs, token-major).
+// Token-major outputs of the module hand-off (acc[i][j] is output channel i of token j):
+// a lane holds rows i..i+3 of one column j and stores them contiguously at out[j*ld + i].
+
+// out[j][i] = bf16(acc)
 struct EpiStoreBf16T {
     static constexpr bool kReduce = false;
+    static constexpr bool kTransposed = true;
     uint16_t* out;
     int64_t ld;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { out[j * ld + i] = f2bf(v); }
-    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
-        for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
+    __device__ void vec4t(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
+        uint16_t* p = out + j * ld + i;
+        if (al8(p)) {
+            u16x4 h = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+            *reinterpret_cast<u16x4*>(p) = h;
+        } else {
+            for (int u = 0; u < 4; ++u) (*this)(i + u, j, v[u], z, aux);
+        }
+    }
+    __device__ void partial(int64_t, double) const {}
+};
+
+// out[j][i] = acc (float32; the gate pre-activation of a SwiGLU hand-off)
+struct EpiStoreF32T {
+    static constexpr bool kReduce = false;
+    static constexpr bool kTransposed = true;
+    float* out;
+    int64_t ld;
+    __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { out[j * ld + i] = v; }
+    __device__ void vec4t(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
+        float* p = out + j * ld + i;
+        if (al16(p)) *reinterpret_cast<f32x4*>(p) = v;
+        else
+            for (int u = 0; u < 4; ++u) (*this)(i + u, j, v[u], z, aux);
+    }
+    __device__ void partial(int64_t, double) const {}
+};
+
+// SwiGLU hand-off: out[j][i] = bf16(silu(G[j][i]) * acc), silu(g) = g / (1 + e^-g).
+struct EpiSwiGLUT {
+    static constexpr bool kReduce = false;
+    static constexpr bool kTransposed = true;
+    const float* G;
+    int64_t ldg;
+    uint16_t* out;
+    int64_t ld;
+    __device__ static float silu(float g) { return g / (1.f + expf(-g)); }
+    __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const {
+        out[j * ld + i] = f2bf(silu(G[j * ldg + i]) * v);
+    }
+    __device__ void vec4t(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
+        const float* g = G + j * ldg + i;
+        uint16_t* p = out + j * ld + i;
+        if (al16(g) && al8(p)) {
+            const f32x4 gv = *reinterpret_cast<const f32x4*>(g);
+            u16x4 h;
+            for (int u = 0; u < 4; ++u) h[u] = f2bf(silu(gv[u]) * v[u]);
+            *reinterpret_cast<u16x4*>(p) = h;
+        } else {
+            for (int u = 0; u < 4; ++u) (*this)(i + u, j, v[u], z, aux);
+        }
     }
     __device__ void partial(int64_t, double) const {}
 };
@@ -588,6 +649,12 @@ hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const flo
 }
 hipError_t gemm_store_bf16_t(const GemmArgs& g, uint16_t* out, int64_t ld, hipStream_t st) {
     return launch(g, EpiStoreBf16T{out, ld}, st);
+}
+hipError_t gemm_store_f32_t(const GemmArgs& g, float* out, int64_t ld, hipStream_t st) {
+    return launch(g, EpiStoreF32T{out, ld}, st);
+}
+hipError_t gemm_swiglu_t(const GemmArgs& g, const float* G, int64_t ldg, uint16_t* out, int64_t ld, hipStream_t st) {
+    return launch(g, EpiSwiGLUT{G, ldg, out, ld}, st);
 }
 
 }  // namespace realq

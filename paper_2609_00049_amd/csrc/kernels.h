@@ -31,7 +31,14 @@ hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const fl
                       int64_t ldr, double* partials, hipStream_t st);
 hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
                      hipStream_t st);
+// Token-major stores for the module hand-off: out[j*ld + i] = bf16(acc[i][j]); float32 variant;
+// SwiGLU variant out[j*ld + i] = bf16(silu(G[j*ldg + i]) * acc[i][j]).
 hipError_t gemm_store_bf16_t(const GemmArgs& g, uint16_t* out, int64_t ld, hipStream_t st);
+hipError_t gemm_store_f32_t(const GemmArgs& g, float* out, int64_t ld, hipStream_t st);
+hipError_t gemm_swiglu_t(const GemmArgs& g, const float* G, int64_t ldg, uint16_t* out, int64_t ld, hipStream_t st);
+// out[c*ldo + r] = in[r*ldi + c] (float32)
+hipError_t transpose_f32(const float* in, int64_t ldi, float* out, int64_t ldo, int64_t rows, int64_t cols,
+                         hipStream_t st);
 
 // ---------------------------------------------------------------- elementwise / layout
 hipError_t fill_f32(float* p, float v, int64_t count, hipStream_t st);
@@ -46,6 +53,12 @@ hipError_t transpose_scale_split(const uint16_t* in, int64_t ldi, const float* s
 // hi/lo[i*ld + j] = split(A[i*lda + j] - (Bm ? Bm[i*ldb + j] : 0)) for j < cols (float32 inputs)
 hipError_t split_diff_f32(const float* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
                           int64_t ld, int64_t rows, int64_t cols, hipStream_t st);
+// hi/lo[i*ld + j] = split(float(A[i*lda + j] - Bm[i*ldb + j])) for j < cols (float64 A, float32 Bm)
+hipError_t split_diff_f64(const double* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
+                          int64_t ld, int64_t rows, int64_t cols, hipStream_t st);
+// out[i] = double(in[i]) / float(in[i])
+hipError_t widen_f32(const float* in, double* out, int64_t count, hipStream_t st);
+hipError_t narrow_f64(const double* in, float* out, int64_t count, hipStream_t st);
 // hi/lo[i] = split(bf16(a[i]) - bf16(b[i]))
 hipError_t split_diff_bf16(const uint16_t* a, const uint16_t* b, uint16_t* hi, uint16_t* lo, int64_t count,
                            hipStream_t st);
@@ -53,7 +66,7 @@ hipError_t split_diff_bf16(const uint16_t* a, const uint16_t* b, uint16_t* hi, u
 hipError_t reduce_partials(const double* partials, int64_t count, double scale, double* out, hipStream_t st);
 // Adam on W[:, c1:n] with G = gscale * sum_z Gp[z][i][j - c1]; refreshes Dhi/Dlo = split(W - W0) there.
 struct AdamArgs {
-    float* W;
+    double* W;
     const float* W0;
     float* mA;
     float* vA;
@@ -93,7 +106,7 @@ hipError_t sgemm(const SgemmArgs& a, hipStream_t st);
 
 // ---------------------------------------------------------------- quantize one column block
 struct QuantArgs {
-    float* W;
+    double* W;
     int64_t m, n, c0, bs;
     const float* U;
     const uint8_t* dead;
@@ -102,12 +115,29 @@ struct QuantArgs {
     float* scales;
     uint8_t* zeros;
     int64_t ngroups;
-    float* E;  // [m][bs]
+    double* E;  // [m][bs]
     const float* W0;  // may be NULL (no split written)
     uint16_t* Dhi;
     uint16_t* Dlo;
 };
 hipError_t quantize_block(const QuantArgs& q, hipStream_t st);
+// W[i][j] -= sum_k E[i][k] U[k][j] in float64 (M x N, K <= block width); when Dhi != NULL
+// also Dhi/Dlo[i*ldd + j] = split(W[i][j] - W0[i*ldw0 + j]).
+struct ObsArgs {
+    const double* E;
+    int64_t lde;
+    const float* U;
+    int64_t ldu;
+    double* W;
+    int64_t ldw;
+    int64_t M, N, K;
+    const float* W0;
+    int64_t ldw0;
+    uint16_t* Dhi;
+    uint16_t* Dlo;
+    int64_t ldd;
+};
+hipError_t obs_update(const ObsArgs& a, hipStream_t st);
 
 // ---------------------------------------------------------------- float64 factorisation
 // Prepares A = J (H + lambda I) J (index-reversed, padded to np with identity) from H_acc,

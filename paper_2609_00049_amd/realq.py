@@ -34,6 +34,7 @@ EXPORTS = [
     "realq_hessian_accum", "realq_chol_inverse",
     "realq_bgd_state_create", "realq_bgd_state_destroy",
     "realq_quantize_block", "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
+    "realq_pullback_metric", "realq_handoff",
 ]
 
 
@@ -95,6 +96,8 @@ def _load():
         "realq_bgd_step": (ctypes.c_int, [vp, vp, vp, i64, f32, vp]),
         "realq_bgd_loss": (ctypes.c_int, [vp, vp, vp, vp]),
         "realq_quantize_layer": (ctypes.c_int, [vp, ctypes.POINTER(LayerDesc), ctypes.POINTER(LayerOut)]),
+        "realq_pullback_metric": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int, vp]),
+        "realq_handoff": (ctypes.c_int, [vp, vp, vp, vp, i64, i64, i64, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -120,6 +123,13 @@ def _ptr(t: Optional[torch.Tensor]):
     if not t.is_contiguous():
         raise ValueError("realq expects contiguous tensors")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _f64(t: torch.Tensor) -> torch.Tensor:
+    """The sweep's working weights are float64."""
+    if t.dtype != torch.float64:
+        raise ValueError("working weights W must be float64")
+    return t
 
 
 def _bits(t: torch.Tensor) -> torch.Tensor:
@@ -218,16 +228,29 @@ class BgdState:
 def quantize_block(ctx: Context, W, c0: int, bs: int, U, dead, qp: QParams, codes, scales, zeros,
                    state: Optional[BgdState] = None):
     m, n = W.shape
-    ctx.check(_lib.realq_quantize_block(ctx.h, _ptr(W), m, n, c0, bs, _ptr(U), _ptr(dead), ctypes.byref(qp),
+    ctx.check(_lib.realq_quantize_block(ctx.h, _ptr(_f64(W)), m, n, c0, bs, _ptr(U), _ptr(dead), ctypes.byref(qp),
                                         _ptr(codes), _ptr(scales), _ptr(zeros), state.h if state else None))
 
 
 def bgd_step(ctx: Context, state: BgdState, W, c1: int, alpha: float = 1.0, loss_out=None):
-    ctx.check(_lib.realq_bgd_step(ctx.h, state.h, _ptr(W), c1, alpha, _ptr(loss_out)))
+    ctx.check(_lib.realq_bgd_step(ctx.h, state.h, _ptr(_f64(W)), c1, alpha, _ptr(loss_out)))
 
 
 def bgd_loss(ctx: Context, state: BgdState, W, loss_out):
-    ctx.check(_lib.realq_bgd_loss(ctx.h, state.h, _ptr(W), _ptr(loss_out)))
+    ctx.check(_lib.realq_bgd_loss(ctx.h, state.h, _ptr(_f64(W)), _ptr(loss_out)))
+
+
+def pullback_metric(ctx: Context, W_next, P, M_next=None, accumulate=False):
+    """P (+)= W_next^T M_next W_next."""
+    m_next, m = W_next.shape
+    ctx.check(_lib.realq_pullback_metric(ctx.h, _ptr(W_next), _ptr(M_next), m_next, m, int(accumulate), _ptr(P)))
+
+
+def handoff(ctx: Context, Wa, X, Y, Wb=None):
+    """Y = bf16(X Wa^T), or bf16(silu(X Wa^T) * (X Wb^T)) when Wb is given."""
+    T, n = X.shape
+    m = Wa.shape[0]
+    ctx.check(_lib.realq_handoff(ctx.h, _ptr(Wa), _ptr(Wb), _ptr(_bits(X)), T, n, m, _ptr(Y)))
 
 
 @dataclass

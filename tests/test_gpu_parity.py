@@ -129,6 +129,39 @@ def test_layer_single_512(rq, ctx, steps):
         np.testing.assert_allclose(tr[0], ref[0], rtol=1e-3)
 
 
+def _tie_rows(m, n, seed):
+    """bf16 weights whose first groups hold the search's exact ties: every other row with
+    extremes -max and +max (two zero points clamp opposite ends with equal error), plus an
+    all-zero, a constant and an exactly representable grid row."""
+    r = np.random.default_rng(seed)
+    W = synth.bf16_round((r.standard_normal((m, n)) * 0.02).astype(np.float32)).astype(np.float64)
+    g = W[:, :128]
+    half = np.arange(0, m, 2)
+    mx = np.abs(g[half]).max(1)
+    g[half, g[half].argmin(1)] = -mx
+    g[half, g[half].argmax(1)] = mx
+    g[1] = 0.0
+    g[3] = 0.03125
+    g[5] = 2.0 ** -8 * (np.arange(128) % 16 - 5)
+    return W.astype(np.float32)
+
+
+@pytest.mark.parametrize("bits", [4, 3])
+def test_search_ties_decided_like_the_oracle(rq, ctx, bits):
+    L = synth.make_module("single_512", m=256, n=256, T=512)
+    L.W0 = _tie_rows(256, 256, 7 + bits)
+    _banner(f"search ties bits={bits}")
+    qp = QParams(bits=bits)
+    g = _run(rq, ctx, L, 0, 0.0, qp=rq.qparams(bits=bits))
+    o = _oracle(L, 0, 0.0, qp=qp)
+    met = P.compare(g, o)
+    print(met, flush=True)
+    # the first groups are searched on the untouched bf16 weights: every decision must agree
+    assert met["first_group_agreement"] == 1.0
+    assert (g.codes.cpu().numpy()[:, 0] == o.codes[:, 0]).all()
+    _assert_parity(met, bgd=False)
+
+
 def test_layer_ragged_shapes(rq, ctx):
     L = synth.make_module("single_512", m=70, n=300, T=1000)
     _banner("layer ragged m=70 n=300 T=1000")
@@ -172,7 +205,7 @@ def test_five_calls_compose_to_the_layer_call(rq, ctx):
     dead = torch.empty((n,), dtype=torch.uint8, device="cuda")
     rq.chol_inverse(ctx, Hacc, T, 0.01, U, None, dead)
     st = rq.BgdState(ctx, W0, X, Xh, s, params=rq.bgd_params(steps=steps, lr=lr))
-    W = W0.clone()
+    W = W0.double()
     codes = torch.empty((m, n), dtype=torch.uint8, device="cuda")
     scales = torch.empty((m, n // 128), dtype=torch.float32, device="cuda")
     zeros = torch.empty((m, n // 128), dtype=torch.uint8, device="cuda")
@@ -184,7 +217,9 @@ def test_five_calls_compose_to_the_layer_call(rq, ctx):
                 rq.bgd_step(ctx, st, W, c0 + 128, 1.0)
     torch.cuda.synchronize()
     assert (codes.cpu() == ref.codes.cpu()).all()
-    assert (W.cpu() == ref.W_hat.cpu()).all()
+    assert (W.float().cpu() == ref.W_hat.cpu()).all()
+    with pytest.raises(ValueError):
+        rq.bgd_step(ctx, st, W.float(), n, 1.0)     # the working weights must be float64
     st.close()
 
 

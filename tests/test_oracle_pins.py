@@ -7,12 +7,13 @@ differences, or constants printed in the paper.  None of these tests uses the GP
 import json
 import math
 import os
+from fractions import Fraction
 
 import numpy as np
 import pytest
 
 import oracle
-from oracle.realq_oracle import (QParams, adam_update, damp_hessian, group_search, hessian, inverse_factor,
+from oracle.realq_oracle import (TIE_ATOL, TIE_RTOL, QParams, adam_update, damp_hessian, group_search, hessian, inverse_factor,
                                  pullback_metric, quantize_layer, residual, surrogate_grad, surrogate_loss,
                                  window_alpha)
 import synth
@@ -93,39 +94,69 @@ def test_inverse_factor_rows_are_sequentially_eliminated_inverse():
 
 # ============================================================================ quantizer: exhaustive search
 
+def _rint_exact(q: Fraction) -> int:
+    """Round-half-to-even of an exact rational."""
+    f = math.floor(q)
+    d = q - f
+    if d != Fraction(1, 2):
+        return f + (1 if d > Fraction(1, 2) else 0)
+    return f + (f % 2)
+
+
 def brute_force_search(x, bits=4, grid=80):
-    """Every (k, z) candidate scored with plain Python loops; lexicographic (err, k, |z-z_nat|, z) winner."""
+    """Every (k, z) candidate scored in exact rational arithmetic with plain Python loops.
+
+    The candidate scales are the float64 values s_k = fl(p_k (hi - lo) / maxq); everything
+    after that (x / s_k, the codes, the squared error) is exact, so an exact tie stays a
+    tie.  Winner: lexicographic (err, k, |z - z_nat|, z), z_nat = rint(-lo maxq / (hi - lo)).
+    Returns (scale, zero, exact error of the winner, {(k, z): exact error}).
+    """
     maxq = 2 ** bits - 1
-    lo = min(0.0, min(x))
-    hi = max(0.0, max(x))
+    xs = [Fraction(float(v)) for v in x]
+    lo = min(Fraction(0), min(xs))
+    hi = max(Fraction(0), max(xs))
     if lo == hi:
-        lo, hi = -1.0, 1.0
-    best = None
+        lo, hi = Fraction(-1), Fraction(1)
+    znat = min(max(_rint_exact(-lo * maxq / (hi - lo)), 0), maxq)
+    best, table = None, {}
     for k in range(grid):
         p = 1.0 - k / 100.0
-        s = (p * (hi - lo)) / maxq
-        znat = min(max(float(np.rint(-(p * lo) / s)), 0.0), maxq)
+        sf = (p * float(hi - lo)) / maxq
+        S = Fraction(sf)
+        r = [_rint_exact(xv / S) for xv in xs]
         for z in range(maxq + 1):
-            err = 0.0
-            for xv in x:
-                q = min(max(float(np.rint(xv / s)) + z, 0.0), maxq)
-                d = xv - s * (q - z)
+            err = Fraction(0)
+            for xv, rv in zip(xs, r):
+                c = min(max(rv + z, 0), maxq) - z
+                d = xv - S * c
                 err += d * d
+            table[(k, z)] = err
             key = (err, k, abs(z - znat), z)
             if best is None or key < best[0]:
-                best = (key, s)
-    return best[1], best[0][3], best[0][0]
+                best = (key, sf)
+    return best[1], best[0][3], best[0][0], table
 
 
 def _check_search(x, bits=4):
+    """The oracle's pick against the exact table: its error evaluated to float64 accuracy and,
+    where it differs from the exact winner, a member of the tie set that wins on (k, dist, z)."""
     qp = QParams(bits=bits)
-    s, z, e = group_search(np.asarray(x)[None, :], qp)
-    bs, bz, be = brute_force_search(list(np.asarray(x, dtype=float)), bits)
+    xs = np.asarray(x, dtype=float)
+    s, z, e = group_search(xs[None, :], qp)
+    bs, bz, be, table = brute_force_search(list(xs), bits)
+    lo, hi = min(0.0, xs.min()), max(0.0, xs.max())
+    if lo == hi:
+        lo, hi = -1.0, 1.0
+    ks = [k for k in range(qp.grid) if ((1.0 - k / 100.0) * (hi - lo)) / qp.maxq == s[0]]
+    assert ks, s[0]
+    pick = (ks[0], int(z[0]))
+    ss = sum(Fraction(float(v)) ** 2 for v in xs)
+    assert abs(Fraction(float(e[0])) - table[pick]) <= Fraction(1e-12) * table[pick] + Fraction(2.0 ** -100) * ss
     if (s[0], z[0]) != (bs, bz):
-        # only a floating-point near tie of the two summation orders may differ
-        assert abs(e[0] - be) <= 1e-12 * max(be, 1e-300), (s[0], z[0], bs, bz, e[0], be)
-    else:
-        assert abs(e[0] - be) <= 1e-12 * max(be, 1e-30)
+        assert table[pick] <= be * (1 + Fraction(TIE_RTOL)) + Fraction(TIE_ATOL) * ss, (pick, bs, bz)
+        znat = min(max(_rint_exact(-Fraction(lo) * qp.maxq / Fraction(hi - lo)), 0), qp.maxq)
+        kb = [k for k in range(qp.grid) if ((1.0 - k / 100.0) * (hi - lo)) / qp.maxq == bs][0]
+        assert (pick[0], abs(pick[1] - znat), pick[1]) < (kb, abs(bz - znat), bz)
     return s[0], z[0], e[0]
 
 
@@ -160,6 +191,40 @@ def test_search_exact_grid_group():
 def test_search_constant_group():
     s, z, e = _check_search(np.full(10, 0.3))
     assert e < 1e-28 and z == 0
+
+
+def _symmetric_bf16_rows(seed, rows=256, g=128):
+    """bf16 rows, every other one with its extremes set to -max and +max (lo = -hi)."""
+    r = rng(seed)
+    x = synth.bf16_round((r.standard_normal((rows, g)) * 0.02).astype(np.float32)).astype(np.float64)
+    half = np.arange(0, rows, 2)
+    mx = np.abs(x[half]).max(1)
+    x[half, x[half].argmin(1)] = -mx
+    x[half, x[half].argmax(1)] = mx
+    return x
+
+
+def test_search_symmetric_bf16_tie():
+    """lo = -hi: the zero points 7 and 8 clamp opposite extremes and tie exactly; z_nat is
+    rint(7.5) = 8.  The oracle must take the exact-arithmetic winner of the brute force."""
+    x = _symmetric_bf16_rows(40, rows=8, g=16)[0]
+    s, z, e = _check_search(x)
+    bs, bz, be, table = brute_force_search(list(x))
+    kb = [k for k in range(80) if ((1 - k / 100) * (2 * x.max())) / 15 == bs][0]
+    assert table[(kb, 7)] == table[(kb, 8)] == be     # the case really is an exact tie
+    assert (s, z) == (bs, bz) and z == 8
+
+
+def test_search_independent_of_summation_order():
+    """Permuting a group's values changes the float64 summation order of every candidate's
+    error but not the candidates themselves, so (scale, zero) must not change."""
+    x = _symmetric_bf16_rows(41)
+    qp = QParams()
+    s0, z0, _ = group_search(x, qp)
+    for t in range(4):
+        perm = rng(100 + t).permutation(x.shape[1])
+        s1, z1, _ = group_search(x[:, perm], qp)
+        assert (s0 == s1).all() and (z0 == z1).all()
 
 
 def test_search_finer_grid_gap_is_small():
@@ -418,3 +483,55 @@ def test_workload_learning_rates_are_the_papers():
     assert synth.CONFIGS["qwen3_32b_layer"]["lr"] == lr["Qwen3-32B"]
     assert synth.CONFIGS["llama3.1_70b_layer"]["lr"] == lr["LLaMA-3.1-70B"]
     assert QParams().block == GOLD["column_block"]["B"]
+
+
+# ============================================================================ hand-off to the next module
+
+def test_bf16_rounding_special_values():
+    from oracle.realq_oracle import bf16
+    one = 1.0
+    ulp = 2.0 ** -7
+    vals = np.array([one, one + ulp / 2, one + 3 * ulp / 2, one + ulp / 2 + 1e-6, -2.5, 0.0, 3.0e38])
+    out = bf16(vals)
+    np.testing.assert_array_equal(out[:4], [one, one, one + 2 * ulp, one + ulp])   # ties to even
+    assert out[4] == -2.5 and out[5] == 0.0
+
+
+def test_handoff_matches_its_definition():
+    from oracle.realq_oracle import bf16, handoff, silu
+    r = rng(80)
+    Wa = r.standard_normal((5, 7))
+    Wb = r.standard_normal((5, 7))
+    X = r.standard_normal((4, 7))
+    Y1 = handoff(Wa, X)
+    Y2 = handoff(Wa, X, Wb)
+    for t in range(4):
+        for i in range(5):
+            a = sum(Wa[i, j] * X[t, j] for j in range(7))
+            b = sum(Wb[i, j] * X[t, j] for j in range(7))
+            assert Y1[t, i] == bf16(np.array([a]))[0]
+            assert Y2[t, i] == bf16(np.array([a / (1 + math.exp(-a)) * b]))[0]
+    # silu: 0 at 0, odd part equals the identity, saturation
+    x = np.array([0.0, 1.5, -1.5, 40.0, -40.0])
+    s = silu(x)
+    assert s[0] == 0.0 and abs((s[1] - s[2]) - 1.5) < 1e-15 and abs(s[3] - 40.0) < 1e-12 and abs(s[4]) < 1e-15
+
+
+def test_layer_chain_runs_and_hands_off():
+    from oracle.realq_oracle import handoff, layer_chain
+    r = rng(81)
+    d, f, T = 16, 24, 64
+    W0s = {"q": r.standard_normal((d, d)) * 0.1, "k": r.standard_normal((8, d)) * 0.1,
+           "v": r.standard_normal((8, d)) * 0.1, "o": r.standard_normal((d, d)) * 0.1,
+           "gate": r.standard_normal((f, d)) * 0.1, "up": r.standard_normal((f, d)) * 0.1,
+           "down": r.standard_normal((d, f)) * 0.1}
+    X0 = r.standard_normal((T, d))
+    res = layer_chain(W0s, X0, X0, qp=QParams(group=8, block=8), steps=1, lr=1e-3)
+    assert set(res) == set(W0s)
+    # with Xhat = X and lr = 0 the quantized chain only differs from the original by quantization
+    res0 = layer_chain(W0s, X0, X0, qp=QParams(group=8, block=8), steps=2, lr=0.0, window=False)
+    q0 = quantize_layer(W0s["q"], X0, X0, qp=QParams(group=8, block=8), steps=0)
+    np.testing.assert_array_equal(res0["q"].codes, q0.codes)
+    o_in = handoff(q0.W_hat, X0)
+    o0 = quantize_layer(W0s["o"], handoff(W0s["q"], X0), o_in, qp=QParams(group=8, block=8), steps=0)
+    np.testing.assert_array_equal(res0["o"].codes, o0.codes)
