@@ -38,7 +38,9 @@ Readings where the paper is silent (each is listed in the design notes):
     (k, |z - z_nat|, z) wins, with the
     natural zero z_nat = rint(-lo maxq / (hi - lo)) of the unshrunk range;
     round-half-to-even; parameters fixed from the weights as they stand when the
-    group's first column is reached;
+    group's first column is reached; the chosen scale is carried as float32 (the format
+    of the output), and codes and dequantized values use that stored scale, so Ŵ is
+    exactly what (codes, scales, zeros) describe;
   * damping: dead columns (H_jj == 0) get H_jj = 1 and their weights zeroed, then
     lambda = damp * mean(diag H) is added to the diagonal;
   * BGD uses all T tokens per step, ``steps`` Adam steps after every block except
@@ -318,7 +320,8 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
             if j % qp.group == 0:
                 g = j // qp.group
                 g1 = min(j + qp.group, n)
-                cur_s, zi, _ = group_search(W[:, j:g1], qp)
+                s64, zi, _ = group_search(W[:, j:g1], qp)
+                cur_s = s64.astype(np.float32).astype(np.float64)   # scales are carried as float32
                 cur_z = zi.astype(np.float64)
                 scales[:, g] = cur_s
                 zeros[:, g] = zi

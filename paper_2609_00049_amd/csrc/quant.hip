@@ -10,8 +10,10 @@
 //      errors up to least * (1 + 2^-40) + 2^-60 * sum x^2 form one tie, and a second
 //      reduction picks the least (k, |z - z_nat|, z) among them, with
 //      z_nat = rint(-lo maxq / (hi - lo));
-//   3. columns are quantized in order, q = clamp(rint(w/s) + z, 0, maxq) decided in
-//      float64 against the float64 scale, w_hat = s (q - z), and the error
+//   3. columns are quantized in order with the scale as stored (float32):
+//      q = clamp(rint(w/s) + z, 0, maxq) decided in float64, w_hat = s (q - z) (exact in
+//      float64, so the float32 output is the float32 dequantization of the stored
+//      parameters), and the error
 //      e = (w - w_hat) / U_jj is propagated to the block's later columns with row j of
 //      the inverse factor U (held in LDS);
 //
@@ -232,6 +234,7 @@ __global__ __launch_bounds__(256) void quantize_block_kernel(QuantArgs q) {
                 }
                 int zi;
                 search_finish<MAXQ>(S, scale, zi);
+                scale = (double)(float)scale;  // the stored float32 scale is the one used
                 zf = (double)zi;
                 if (lane == 0) {
                     q.scales[i * q.ngroups + col / group] = (float)scale;

@@ -168,6 +168,14 @@ def test_layer_ragged_shapes(rq, ctx):
     g = _run(rq, ctx, L, 2, 1e-3)
     o = _oracle(L, 2, 1e-3)
     _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
+    # grid membership: every code on the 16-level grid, and every output weight is the float32
+    # dequantization of its stored (code, scale, zero), bitwise
+    codes = g.codes.cpu()
+    assert int(codes.max()) <= 15
+    gi = np.arange(300) // 128
+    sc = g.scales.cpu()[:, gi]
+    zr = g.zeros.cpu()[:, gi].float()
+    assert (g.W_hat.cpu() == sc * (codes.float() - zr)).all()
 
 
 def test_layer_token_chunks_match_single_chunk(rq, ctx):

@@ -259,6 +259,7 @@ def textbook_obs(W0, X, qp):
     for j in range(n):
         if j % qp.group == 0:
             sc, zz, _ = group_search(W[:, j:j + qp.group], qp)
+            sc = sc.astype(np.float32).astype(float)          # the stored (float32) scale
         q = np.clip(np.rint(W[:, j] / sc) + zz, 0, maxq)
         wq = sc * (q - zz)
         Hinv = np.linalg.inv(Hd[j:, j:])
@@ -319,8 +320,12 @@ def test_codes_on_grid_and_locked_columns_dequantize_exactly():
     res = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=2, lr=1e-3)
     assert res.codes.min() >= 0 and res.codes.max() <= 15
     g = np.arange(256) // 128
+    assert (res.scales == res.scales.astype(np.float32)).all()       # scales are float32 values
     deq = res.scales[:, g] * (res.codes.astype(float) - res.zeros[:, g])
     np.testing.assert_array_equal(res.W_hat, deq)
+    # and the float32 dequantization of the stored parameters is the float32 rounding of W_hat
+    deq32 = res.scales[:, g].astype(np.float32) * (res.codes.astype(np.float32) - res.zeros[:, g].astype(np.float32))
+    np.testing.assert_array_equal(res.W_hat.astype(np.float32), deq32)
 
 
 # ============================================================================ BGD: gradient, Adam, window
