@@ -294,40 +294,74 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
 
     // Epilogue.  Element (row, col) of a 32x32 tile held by this lane in acc[e] is
     // row = 8*(e/4) + 4*(lane/32) + e%4, col = lane%32.  Each tile is restaged through
-    // LDS so that a lane then owns 4 consecutive columns of a row (16-byte accesses).
+    // this wave's own LDS scratch so that a lane then owns 4 consecutive columns of a row
+    // (16-byte accesses).  The global operands of the epilogue (residual base, per-token
+    // weights, the accumulated output) are loaded one sub-tile ahead, so their latency
+    // overlaps the restaging and the stores of the current sub-tile.  LDS accesses of one
+    // wave complete in order; the wavefront fences only keep the compiler from moving the
+    // scratch writes and reads across each other.
     float aux = 0.f;
     float* scr = scratch + wave * (32 * EPI_STRIDE);
     const int64_t z = blockIdx.z;
+    if constexpr (!Epi::kTransposed) {
+        constexpr int NSUB = C::SM * C::SN;
+        const int cc = (lane & 7) * 4;
+        typename Epi::Row rcur[4], rnxt[4];
+        typename Epi::Col ccur, cnxt;
+        auto prefetch = [&](int t, typename Epi::Row(&R)[4], typename Epi::Col& Cl) {
+            const int64_t r0 = m0 + wm * C::WTM + (t / C::SN) * 32;
+            const int64_t col = n0 + wn * C::WTN + (t % C::SN) * 32 + cc;
+            const bool colv = col + 3 < N;
+            if (colv) Cl = epi.load_col(col);
 #pragma unroll
-    for (int i = 0; i < C::SM; ++i)
+            for (int q = 0; q < 4; ++q) {
+                const int64_t row = r0 + q * 8 + (lane >> 3);
+                if (colv && row < M) R[q] = epi.load_row(row, col, z);
+                else R[q].ok = false;
+            }
+        };
+        prefetch(0, rcur, ccur);
 #pragma unroll
-        for (int j = 0; j < C::SN; ++j) {
+        for (int t = 0; t < NSUB; ++t) {
+            if (t + 1 < NSUB) prefetch(t + 1, rnxt, cnxt);
+            const int i = t / C::SN, j = t % C::SN;
 #pragma unroll
             for (int e = 0; e < 16; ++e)
                 scr[(8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)) * EPI_STRIDE + (lane & 31)] = acc[i][j][e];
-            __syncthreads();
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
             const int64_t r0 = m0 + wm * C::WTM + i * 32;
-            const int64_t c0 = n0 + wn * C::WTN + j * 32;
-            if constexpr (!Epi::kTransposed) {
-                // lane owns 4 consecutive columns of one row
-                const int cc = (lane & 7) * 4;
-                const int64_t col = c0 + cc;
+            const int64_t col = n0 + wn * C::WTN + j * 32 + cc;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int rr = q * 8 + (lane >> 3);
-                    const int64_t row = r0 + rr;
-                    const f32x4 v = *reinterpret_cast<const f32x4*>(scr + rr * EPI_STRIDE + cc);
-                    if (row < M) {
-                        if (col + 3 < N) {
-                            epi.vec4(row, col, v, z, aux);
-                        } else {
+            for (int q = 0; q < 4; ++q) {
+                const int rr = q * 8 + (lane >> 3);
+                const int64_t row = r0 + rr;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(scr + rr * EPI_STRIDE + cc);
+                if (row < M) {
+                    if (rcur[q].ok) {
+                        epi.vec4(row, col, v, rcur[q], ccur, z, aux);
+                    } else {
 #pragma unroll
-                            for (int u = 0; u < 4; ++u)
-                                if (col + u < N) epi(row, col + u, v[u], z, aux);
-                        }
+                        for (int u = 0; u < 4; ++u)
+                            if (col + u < N) epi(row, col + u, v[u], z, aux);
                     }
                 }
-            } else {
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+            for (int q = 0; q < 4; ++q) rcur[q] = rnxt[q];
+            ccur = cnxt;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::SN; ++j) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    scr[(8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)) * EPI_STRIDE + (lane & 31)] = acc[i][j][e];
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                const int64_t r0 = m0 + wm * C::WTM + i * 32;
+                const int64_t c0 = n0 + wn * C::WTN + j * 32;
                 // lane owns 4 consecutive rows of one column (outputs stored column-major)
                 const int rr = (lane & 7) * 4;
                 const int64_t row = r0 + rr;
@@ -348,9 +382,9 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
                         }
                     }
                 }
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
             }
-            __syncthreads();
-        }
+    }
     if constexpr (Epi::kReduce) {
         // deterministic block reduction of the per-thread partial sums (reuses the LDS stage)
         double* red = reinterpret_cast<double*>(st1);
@@ -365,12 +399,16 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
 }
 
 // ---------------------------------------------------------------- epilogues
-// operator() handles one element; vec4() handles columns j..j+3 of row i (all < N) and
-// falls back to operator() when an address is not suitably aligned.
+// Row-major epilogues: operator() handles one element.  The fast path handles columns
+// j..j+3 of row i in three parts: load_col(j) and load_row(i, j, z) fetch the global
+// operands ahead of time (ok = false sends the lane to operator() instead, e.g. for an
+// unaligned address), vec4() combines them with the accumulators and stores.
 
 __device__ __forceinline__ bool al16(const void* p) { return (((uintptr_t)p) & 15u) == 0; }
 __device__ __forceinline__ bool al8(const void* p) { return (((uintptr_t)p) & 7u) == 0; }
 typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+
+struct NoCol {};
 
 struct EpiStoreF32 {  // C[z][i][j] = alpha * acc
     static constexpr bool kReduce = false;
@@ -378,16 +416,19 @@ struct EpiStoreF32 {  // C[z][i][j] = alpha * acc
     float* C;
     int64_t ldc, split_stride;
     float alpha;
+    struct Row {
+        bool ok;
+    };
+    using Col = NoCol;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t z, float&) const {
         C[z * split_stride + i * ldc + j] = alpha * v;
     }
-    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
-        float* p = C + z * split_stride + i * ldc + j;
-        if (al16(p)) {
-            *reinterpret_cast<f32x4*>(p) = v * alpha;
-        } else {
-            for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
-        }
+    __device__ Col load_col(int64_t) const { return {}; }
+    __device__ Row load_row(int64_t i, int64_t j, int64_t z) const {
+        return {al16(C + z * split_stride + i * ldc + j)};
+    }
+    __device__ void vec4(int64_t i, int64_t j, f32x4 v, const Row&, const Col&, int64_t z, float&) const {
+        *reinterpret_cast<f32x4*>(C + z * split_stride + i * ldc + j) = v * alpha;
     }
     __device__ void partial(int64_t, double) const {}
 };
@@ -402,15 +443,22 @@ struct EpiAccF32 {  // C[i][j] += alpha * acc
     float* C;
     int64_t ldc;
     float alpha;
+    struct Row {
+        f32x4 c;
+        bool ok;
+    };
+    using Col = NoCol;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { C[i * ldc + j] += alpha * v; }
-    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
-        float* p = C + i * ldc + j;
-        if (al16(p)) {
-            f32x4 c = *reinterpret_cast<const f32x4*>(p);
-            *reinterpret_cast<f32x4*>(p) = c + v * alpha;
-        } else {
-            for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
-        }
+    __device__ Col load_col(int64_t) const { return {}; }
+    __device__ Row load_row(int64_t i, int64_t j, int64_t) const {
+        Row r;
+        const float* p = C + i * ldc + j;
+        r.ok = al16(p);
+        if (r.ok) r.c = *reinterpret_cast<const f32x4*>(p);
+        return r;
+    }
+    __device__ void vec4(int64_t i, int64_t j, f32x4 v, const Row& r, const Col&, int64_t, float&) const {
+        *reinterpret_cast<f32x4*>(C + i * ldc + j) = r.c + v * alpha;
     }
     __device__ void partial(int64_t, double) const {}
 };
@@ -420,12 +468,32 @@ struct EpiAccF64 {  // C[i][j] += acc   (float64 accumulator across chunks)
     static constexpr bool kTransposed = false;
     double* C;
     int64_t ldc;
+    struct Row {
+        bool ok;
+    };
+    using Col = NoCol;
     __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { C[i * ldc + j] += (double)v; }
-    __device__ void vec4(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
-        for (int u = 0; u < 4; ++u) (*this)(i, j + u, v[u], z, aux);
-    }
+    __device__ Col load_col(int64_t) const { return {}; }
+    __device__ Row load_row(int64_t, int64_t, int64_t) const { return {false}; }
+    __device__ void vec4(int64_t, int64_t, f32x4, const Row&, const Col&, int64_t, float&) const {}
     __device__ void partial(int64_t, double) const {}
 };
+
+// Per-token weights of columns t..t+3 (1 without weights).
+struct TokW {
+    f32x4 w;
+    bool ok;
+};
+__device__ __forceinline__ TokW load_tokw(const float* s, int64_t t) {
+    TokW c;
+    c.w = f32x4{1.f, 1.f, 1.f, 1.f};
+    c.ok = true;
+    if (s) {
+        c.ok = al16(s + t);
+        if (c.ok) c.w = *reinterpret_cast<const f32x4*>(s + t);
+    }
+    return c;
+}
 
 // Residual: R = B0[i][t] + acc; writes split(R * s_t) and accumulates s_t R^2.
 struct EpiResid {
@@ -438,6 +506,11 @@ struct EpiResid {
     uint16_t* Rlo;
     int64_t ldr;
     double* partials;
+    struct Row {
+        f32x4 b;
+        bool ok;
+    };
+    using Col = TokW;
     __device__ void operator()(int64_t i, int64_t t, float v, int64_t, float& aux) const {
         float r = B0[i * ldb0 + t] + v;
         float w = s ? s[t] : 1.f;
@@ -448,29 +521,32 @@ struct EpiResid {
         Rlo[i * ldr + t] = lo;
         aux += rs * r;
     }
-    __device__ void vec4(int64_t i, int64_t t, f32x4 v, int64_t z, float& aux) const {
+    __device__ Col load_col(int64_t t) const { return load_tokw(s, t); }
+    __device__ Row load_row(int64_t i, int64_t t, int64_t) const {
+        Row r;
         const float* b = B0 + i * ldb0 + t;
-        uint16_t* ph = Rhi + i * ldr + t;
-        uint16_t* pl = Rlo + i * ldr + t;
-        if (!al16(b) || !al8(ph) || !al8(pl) || (s && !al16(s + t))) {
+        r.ok = al16(b) && al8(Rhi + i * ldr + t) && al8(Rlo + i * ldr + t);
+        if (r.ok) r.b = *reinterpret_cast<const f32x4*>(b);
+        return r;
+    }
+    __device__ void vec4(int64_t i, int64_t t, f32x4 v, const Row& row, const Col& col, int64_t z, float& aux) const {
+        if (!col.ok) {
             for (int u = 0; u < 4; ++u) (*this)(i, t + u, v[u], z, aux);
             return;
         }
-        const f32x4 r = *reinterpret_cast<const f32x4*>(b) + v;
-        f32x4 w = {1.f, 1.f, 1.f, 1.f};
-        if (s) w = *reinterpret_cast<const f32x4*>(s + t);
+        const f32x4 r = row.b + v;
         u16x4 h, l;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const float rs = r[u] * w[u];
+            const float rs = r[u] * col.w[u];
             uint16_t hh, ll;
             split_bf16(rs, hh, ll);
             h[u] = hh;
             l[u] = ll;
             aux += rs * r[u];
         }
-        *reinterpret_cast<u16x4*>(ph) = h;
-        *reinterpret_cast<u16x4*>(pl) = l;
+        *reinterpret_cast<u16x4*>(Rhi + i * ldr + t) = h;
+        *reinterpret_cast<u16x4*>(Rlo + i * ldr + t) = l;
     }
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
@@ -483,13 +559,32 @@ struct EpiLoss {
     int64_t ldb0;
     const float* s;
     double* partials;
+    struct Row {
+        f32x4 b;
+        bool ok;
+    };
+    using Col = TokW;
     __device__ void operator()(int64_t i, int64_t t, float v, int64_t, float& aux) const {
         float r = B0[i * ldb0 + t] + v;
         float w = s ? s[t] : 1.f;
         aux += w * r * r;
     }
-    __device__ void vec4(int64_t i, int64_t t, f32x4 v, int64_t z, float& aux) const {
-        for (int u = 0; u < 4; ++u) (*this)(i, t + u, v[u], z, aux);
+    __device__ Col load_col(int64_t t) const { return load_tokw(s, t); }
+    __device__ Row load_row(int64_t i, int64_t t, int64_t) const {
+        Row r;
+        const float* b = B0 + i * ldb0 + t;
+        r.ok = al16(b);
+        if (r.ok) r.b = *reinterpret_cast<const f32x4*>(b);
+        return r;
+    }
+    __device__ void vec4(int64_t i, int64_t t, f32x4 v, const Row& row, const Col& col, int64_t z, float& aux) const {
+        if (!col.ok) {
+            for (int u = 0; u < 4; ++u) (*this)(i, t + u, v[u], z, aux);
+            return;
+        }
+        const f32x4 r = row.b + v;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) aux += col.w[u] * r[u] * r[u];
     }
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
