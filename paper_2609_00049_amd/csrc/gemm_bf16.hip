@@ -90,20 +90,20 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int row, int k) {
                               *reinterpret_cast<const u16x8*>(lds + row * LDS_STRIDE + swz(row, k >> 3) * 8));
 }
 
-// 16-byte direct-to-LDS load of this lane's global chunk into LDS byte address
-// lds_base + 16 * lane (lds_base is wave-uniform).  Issued as inline assembly so the
-// compiler does not insert conservative waits for it; every consumer is ordered by the
-// explicit vmcnt waits and barriers of the K loop.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory", "m0");
+// 16-byte direct-to-LDS load: lane i reads sbase + voff (its own 32-bit byte offset) and
+// fills LDS bytes [lds + 16i, lds + 16i + 16) (lds is wave-uniform).  Issued as inline
+// assembly so the compiler does not insert conservative waits for it; every consumer is
+// ordered by the explicit vmcnt waits and barriers of the K loop.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+                 : "memory", "m0");
 }
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
+// LDS byte address of a __shared__ object: the low 32 bits of its generic address.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
 // Tile coordinates of this block: XCD-contiguous renumbering, then grouped row-tile order.
 __device__ __forceinline__ void tile_of(int64_t tiles_m, int64_t tiles_n, int64_t group_m, int64_t& tm, int64_t& tn) {
@@ -171,91 +171,92 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
     constexpr int A_RUNS = C::BM / 16 / NW, B_RUNS = C::BN / 16 / NW;  // 1 KB runs per wave per slice
     constexpr int DMA_PER_SLICE = A_RUNS * (HAS_LO ? 2 : 1) + B_RUNS;
     static_assert(C::BM % (16 * NW) == 0 && C::BN % (16 * NW) == 0, "tile rows must split into wave runs");
-    const uint16_t* pA[A_RUNS];
-    const uint16_t* pAl[HAS_LO ? A_RUNS : 1];
-    const uint16_t* pB[B_RUNS];
+    // Per-lane byte offsets (fixed for the whole K loop) from wave-uniform operand bases
+    // that advance by one slice per step.  Rows past the end are clamped to the last row;
+    // their products only reach accumulators the epilogue masks.
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    uint32_t offA[A_RUNS], offB[B_RUNS];
     {
         const int lr = lane >> 2, pc = lane & 3;
 #pragma unroll
         for (int q = 0; q < A_RUNS; ++q) {
             const int r = 16 * (wave + NW * q) + lr;
             const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
-            const int64_t gr = min(m0 + r, M - 1);
-            pA[q] = Ahi + gr * lda + kbeg + c * 8;
-            if constexpr (HAS_LO) pAl[q] = Alo + gr * lda + kbeg + c * 8;
+            const int64_t gr = min(m0 + r, M - 1) - m0;
+            offA[q] = (uint32_t)((gr * lda + c * 8) * 2);
         }
 #pragma unroll
         for (int q = 0; q < B_RUNS; ++q) {
             const int r = 16 * (wave + NW * q) + lr;
             const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
-            const int64_t gr = min(n0 + r, N - 1);
-            pB[q] = B + gr * ldb + kbeg + c * 8;
+            const int64_t gr = min(n0 + r, N - 1) - n0;
+            offB[q] = (uint32_t)((gr * ldb + c * 8) * 2);
         }
     }
-    auto issue = [&](int64_t s, uint16_t* stage) {
-        const int64_t off = s * BK;
+    const char* const baseA = reinterpret_cast<const char*>(Ahi + m0 * lda + kbeg);
+    const char* const baseAl = HAS_LO ? reinterpret_cast<const char*>(Alo + m0 * lda + kbeg) : baseA;
+    const char* const baseB = reinterpret_cast<const char*>(B + n0 * ldb + kbeg);
+    const uint32_t lds_st[3] = {lds_addr(st0), lds_addr(st1), lds_addr(st2)};
+    auto issue = [&](int64_t s, uint32_t stage) {
+        const int64_t off = s * BK * 2;
 #pragma unroll
         for (int q = 0; q < A_RUNS; ++q) {
-            const uint32_t d = __builtin_amdgcn_readfirstlane(lds_addr(stage + (wave + NW * q) * 16 * LDS_STRIDE));
-            dma16(pA[q] + off, d);
-            if constexpr (HAS_LO) dma16(pAl[q] + off, d + C::BM * LDS_STRIDE * 2);
+            const uint32_t d = stage + (uint32_t)((wv + NW * q) * 16 * LDS_STRIDE * 2);
+            dma16(baseA + off, offA[q], d);
+            if constexpr (HAS_LO) dma16(baseAl + off, offA[q], d + C::BM * LDS_STRIDE * 2);
         }
 #pragma unroll
-        for (int q = 0; q < B_RUNS; ++q) {
-            const uint32_t d =
-                __builtin_amdgcn_readfirstlane(lds_addr(stage + (A_ROWS + (wave + NW * q) * 16) * LDS_STRIDE));
-            dma16(pB[q] + off, d);
-        }
+        for (int q = 0; q < B_RUNS; ++q)
+            dma16(baseB + off, offB[q], stage + (uint32_t)((A_ROWS + (wv + NW * q) * 16) * LDS_STRIDE * 2));
     };
     // wait until at most n direct-to-LDS loads of this wave are outstanding
     auto wait_vm = [](int n) {
         if (n >= DMA_PER_SLICE) wait_vmcnt<DMA_PER_SLICE>();
         else wait_vmcnt<0>();
     };
-    auto compute = [&](const uint16_t* sA) {
+    struct Frags {
+        bf16x8 a[C::SM], al[HAS_LO ? C::SM : 1], b[C::SN];
+    };
+    auto load_frags = [&](const uint16_t* sA, int kk, Frags& f) {
         const uint16_t* sAl = sA + C::BM * LDS_STRIDE;
         const uint16_t* sB = sA + A_ROWS * LDS_STRIDE;
+        const int kofs = kk + 8 * (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i) {
+            f.a[i] = frag(sA, wm * C::WTM + i * 32 + (lane & 31), kofs);
+            if constexpr (HAS_LO) f.al[i] = frag(sAl, wm * C::WTM + i * 32 + (lane & 31), kofs);
+        }
+#pragma unroll
+        for (int j = 0; j < C::SN; ++j) f.b[j] = frag(sB, wn * C::WTN + j * 32 + (lane & 31), kofs);
+    };
+    auto mfmas = [&](const Frags& f) {
+#pragma unroll
+        for (int i = 0; i < C::SM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::SN; ++j) {
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+                if constexpr (HAS_LO)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.al[i], f.b[j], acc[i][j], 0, 0, 0);
+            }
+    };
+    auto compute = [&](const uint16_t* sA) {
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 16) {
-            const int kofs = kk + 8 * (lane >> 5);
-            bf16x8 a[C::SM], al[HAS_LO ? C::SM : 1], b[C::SN];
-#pragma unroll
-            for (int i = 0; i < C::SM; ++i) {
-                a[i] = frag(sA, wm * C::WTM + i * 32 + (lane & 31), kofs);
-                if constexpr (HAS_LO) al[i] = frag(sAl, wm * C::WTM + i * 32 + (lane & 31), kofs);
-            }
-#pragma unroll
-            for (int j = 0; j < C::SN; ++j) b[j] = frag(sB, wn * C::WTN + j * 32 + (lane & 31), kofs);
-#pragma unroll
-            for (int i = 0; i < C::SM; ++i)
-#pragma unroll
-                for (int j = 0; j < C::SN; ++j) {
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-                    if constexpr (HAS_LO)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], b[j], acc[i][j], 0, 0, 0);
-                }
+            Frags f;
+            load_frags(sA, kk, f);
+            mfmas(f);
         }
     };
-    // Refill one stage and multiply out of another.  The two stage pointers are restrict
-    // parameters so that, once inlined, the compiler knows the direct-to-LDS writes cannot
-    // touch the stage being read and does not wait for them before the LDS reads.
-    auto step = [&](int64_t s, bool refill, uint16_t* fill, const uint16_t* read) {
-        if (refill) {
-            const int64_t off = s * BK;
-#pragma unroll
-            for (int q = 0; q < A_RUNS; ++q) {
-                const uint32_t d = __builtin_amdgcn_readfirstlane(lds_addr(fill + (wave + NW * q) * 16 * LDS_STRIDE));
-                dma16(pA[q] + off, d);
-                if constexpr (HAS_LO) dma16(pAl[q] + off, d + C::BM * LDS_STRIDE * 2);
-            }
-#pragma unroll
-            for (int q = 0; q < B_RUNS; ++q) {
-                const uint32_t d =
-                    __builtin_amdgcn_readfirstlane(lds_addr(fill + (A_ROWS + (wave + NW * q) * 16) * LDS_STRIDE));
-                dma16(pB[q] + off, d);
-            }
-        }
-        compute(read);
+    // Multiply one stage; the first fragments are read before the refill of another stage
+    // is issued, so their LDS latency overlaps the issue of the direct-to-LDS loads.
+    static_assert(BK == 32, "the slice step reads two 16-wide fragment sets");
+    auto step = [&](int64_t s, bool refill, uint32_t fill, const uint16_t* read) {
+        Frags f0, f1;
+        load_frags(read, 0, f0);
+        if (refill) issue(s, fill);
+        load_frags(read, 16, f1);
+        mfmas(f0);
+        mfmas(f1);
     };
     const int64_t nfull = vec ? (kend - kbeg) / BK : 0;
     // one slice: wait until this slice has landed (the next may stay in flight), barrier (all
@@ -264,16 +265,16 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
     do {                                                           \
         wait_vm((S) + 1 < nfull ? DMA_PER_SLICE : 0);              \
         __builtin_amdgcn_s_barrier();                              \
-        step((S) + 2, (S) + 2 < nfull, NXT2, CUR);                 \
+        step((S) + 2, (S) + 2 < nfull, lds_st[NXT2], CUR);         \
     } while (0)
-    if (nfull > 0) issue(0, st0);
-    if (nfull > 1) issue(1, st1);
+    if (nfull > 0) issue(0, lds_st[0]);
+    if (nfull > 1) issue(1, lds_st[1]);
     for (int64_t s = 0; s < nfull; s += 3) {
-        RQ_STEP(s, st0, st2);
+        RQ_STEP(s, st0, 2);
         if (s + 1 >= nfull) break;
-        RQ_STEP(s + 1, st1, st0);
+        RQ_STEP(s + 1, st1, 0);
         if (s + 2 >= nfull) break;
-        RQ_STEP(s + 2, st2, st1);
+        RQ_STEP(s + 2, st2, 1);
     }
 #undef RQ_STEP
     wait_vmcnt<0>();
@@ -692,8 +693,11 @@ static hipError_t launch_cfg(const GemmArgs& g, const Epi& epi, hipStream_t stre
     if (kps <= 0) kps = BK;
     splits = (g.K + kps - 1) / kps;
     if (splits < 1) splits = 1;
+    // The direct-to-LDS path addresses a tile's rows with 32-bit byte offsets from the tile's
+    // first row; larger strides take the checked register path.
+    const bool offsets32 = (int64_t)C::BM * g.lda * 2 < (int64_t(1) << 32) && (int64_t)C::BN * g.ldb * 2 < (int64_t(1) << 32);
     const bool vec = aligned16(g.Ahi) && (!g.Alo || aligned16(g.Alo)) && aligned16(g.B) && (g.lda % 8 == 0) &&
-                     (g.ldb % 8 == 0);
+                     (g.ldb % 8 == 0) && offsets32;
     // row-tile group: enough row tiles per group that ~32 concurrent blocks of an XCD share operands
     int64_t group_m = tiles_n >= 32 ? 8 : (tiles_n >= 8 ? 2 : 1);
     if (g.group_m > 0) group_m = g.group_m;
