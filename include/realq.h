@@ -212,12 +212,15 @@ typedef struct realq_layer_out {
     uint8_t* codes;           /* [m,n]                     required             */
     float* scales;            /* [m,ceil(n/group)]         required             */
     uint8_t* zeros;           /* [m,ceil(n/group)]         required             */
-    float* W_hat;             /* [m,n] final dequantized weights, required; also the working buffer */
+    float* W_hat;             /* [m,n] final dequantized weights, required      */
     float* H;                 /* [n,n] float32 Hessian before damping | NULL    */
     float* U;                 /* [n,n] inverse factor | NULL (workspace used)   */
     uint8_t* dead;            /* [n] | NULL                                     */
-    double* loss_trace;       /* [nblocks*steps] device float64 | NULL          */
-    double loss_final;        /* host: final loss (M = identity), NaN otherwise */
+    double* loss_trace;       /* [nblocks*steps] device float64 | NULL; entries of
+                                 steps with a dense metric M_a are NaN          */
+    double loss_final;        /* host: final loss with the module's own metric M
+                                 (alpha = 1); with a dense M it is evaluated
+                                 through the calibration Gram matrices         */
     double ms_total;          /* host: wall time of the call between events on the stream */
 } realq_layer_out;
 

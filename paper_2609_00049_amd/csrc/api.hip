@@ -759,6 +759,76 @@ int realq_handoff(realq_ctx* ctx, const float* Wa, const float* Wb, const uint16
     return REALQ_OK;
 }
 
+// ============================================================================ a11 with a dense metric
+// L = (1/2T) sum_t s_t R_t^T M R_t with R = W0 Delta^T + D Xhat^T (Delta = Xhat - X, D = W - W0)
+// expands through the calibration Gram matrices G_dd = Delta^T S Delta, G_dh = Delta^T S Xhat
+// and G_hh = Xhat^T S Xhat (the Hessian accumulator) into
+//   2T L = <W0 G_dd, M W0> + 2 <W0 G_dh, M D> + <D G_hh, M D>,
+// n x n token contractions plus m x n x n and m x m x n float64 products instead of an
+// m x m x T contraction.  Every term is built from the small quantities Delta and D.
+static int dense_final_loss(realq_ctx* ctx, const realq_layer_desc* d, const double* W, const double* Ghh,
+                            double* loss_dev) {
+    const int64_t m = d->m, n = d->n, T = d->T;
+    hipStream_t s = ctx->stream;
+    int rc;
+    void *gdh, *gdd, *sdh, *sdl, *dh, *dl, *xt, *A, *D, *E, *MX, *M64, *parts;
+    int64_t tc = (int64_t)(128ll << 20) / n;
+    tc = tc < 256 ? 256 : (tc / 256) * 256;
+    if (tc > T) tc = ((T + 7) / 8) * 8;
+    if ((rc = get_ws(ctx, "g_dh", (size_t)n * n * 8, &gdh))) return rc;
+    if ((rc = get_ws(ctx, "g_dd", (size_t)n * n * 8, &gdd))) return rc;
+    if ((rc = get_ws(ctx, "g_sdh", (size_t)n * tc * 2, &sdh))) return rc;
+    if ((rc = get_ws(ctx, "g_sdl", (size_t)n * tc * 2, &sdl))) return rc;
+    if ((rc = get_ws(ctx, "g_dh16", (size_t)n * tc * 2, &dh))) return rc;
+    if ((rc = get_ws(ctx, "g_dl16", (size_t)n * tc * 2, &dl))) return rc;
+    if ((rc = get_ws(ctx, "g_xt", (size_t)n * tc * 2, &xt))) return rc;
+    Timed tm(ctx, "dense_loss");
+    RQ_HIP(ctx, realq::fill_f64((double*)gdh, 0.0, n * n, s));
+    RQ_HIP(ctx, realq::fill_f64((double*)gdd, 0.0, n * n, s));
+    for (int64_t t0 = 0; t0 < T; t0 += tc) {
+        const int64_t cur = std::min(tc, T - t0);
+        RQ_HIP(ctx, realq::transpose_delta_split(d->Xhat + t0 * n, d->X + t0 * n, n, d->s ? d->s + t0 : nullptr,
+                                                 (uint16_t*)sdh, (uint16_t*)sdl, (uint16_t*)dh, (uint16_t*)dl, tc, cur,
+                                                 n, s));
+        RQ_HIP(ctx, realq::transpose_u16(d->Xhat + t0 * n, n, (uint16_t*)xt, tc, cur, n, s));
+        realq::GemmArgs g{(const uint16_t*)sdh, (const uint16_t*)sdl, tc, (const uint16_t*)xt, tc, n, n, cur, 1};
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, (double*)gdh, n, s));
+        g.B = (const uint16_t*)dh;
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, (double*)gdd, n, s));
+        g.B = (const uint16_t*)dl;
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, (double*)gdd, n, s));
+    }
+    const int64_t np = realq::dot_f64_partials();
+    if ((rc = get_ws(ctx, "g_A", (size_t)m * n * 8, &A))) return rc;
+    if ((rc = get_ws(ctx, "g_D", (size_t)m * n * 8, &D))) return rc;
+    if ((rc = get_ws(ctx, "g_E", (size_t)m * n * 8, &E))) return rc;
+    if ((rc = get_ws(ctx, "g_MX", (size_t)m * n * 8, &MX))) return rc;
+    if ((rc = get_ws(ctx, "g_M", (size_t)m * m * 8, &M64))) return rc;
+    if ((rc = get_ws(ctx, "g_parts", (size_t)4 * np * 8, &parts))) return rc;
+    double* Ad = (double*)A;
+    double* Dd = (double*)D;
+    double* Ed = (double*)E;
+    double* MXd = (double*)MX;
+    double* pp = (double*)parts;
+    RQ_HIP(ctx, realq::widen_f32(d->W0, Ad, m * n, s));
+    RQ_HIP(ctx, realq::sub_f64_f32(W, d->W0, Dd, m * n, s));
+    RQ_HIP(ctx, realq::widen_f32(d->M, (double*)M64, m * m, s));
+    // <W0 G_dd, M W0>
+    RQ_HIP(ctx, realq::dgemm(Ad, n, (const double*)gdd, n, Ed, n, m, n, n, false, s));
+    RQ_HIP(ctx, realq::dgemm((const double*)M64, m, Ad, n, MXd, n, m, n, m, false, s));
+    RQ_HIP(ctx, realq::dot_f64(Ed, MXd, m * n, pp, s));
+    // 2 <W0 G_dh, M D>
+    RQ_HIP(ctx, realq::dgemm(Ad, n, (const double*)gdh, n, Ed, n, m, n, n, false, s));
+    RQ_HIP(ctx, realq::dgemm((const double*)M64, m, Dd, n, MXd, n, m, n, m, false, s));
+    RQ_HIP(ctx, realq::dot_f64(Ed, MXd, m * n, pp + np, s));
+    RQ_HIP(ctx, realq::dot_f64(Ed, MXd, m * n, pp + 2 * np, s));
+    // <D G_hh, M D>
+    RQ_HIP(ctx, realq::dgemm(Dd, n, Ghh, n, Ed, n, m, n, n, false, s));
+    RQ_HIP(ctx, realq::dot_f64(Ed, MXd, m * n, pp + 3 * np, s));
+    RQ_HIP(ctx, realq::reduce_partials(pp, 4 * np, 0.5 / (double)T, loss_dev, s));
+    return REALQ_OK;
+}
+
 // ============================================================================ a1-a11: whole module
 
 int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_out* out) {
@@ -839,10 +909,12 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
             if ((rc = state_init(&st))) return rc;
         }
         if ((rc = realq_bgd_loss(ctx, &st, W, (double*)lf))) return rc;
+    } else {
+        if ((rc = dense_final_loss(ctx, d, W, (const double*)Hacc, (double*)lf))) return rc;
     }
     RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat, m * n, s));
     RQ_HIP(ctx, hipEventRecord(ev1, s));
-    if (!d->M) RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lf, 8, hipMemcpyDeviceToHost, s));
+    RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lf, 8, hipMemcpyDeviceToHost, s));
     RQ_HIP(ctx, hipStreamSynchronize(s));
     float ms = 0.f;
     RQ_HIP(ctx, hipEventElapsedTime(&ms, ev0, ev1));

@@ -94,6 +94,91 @@ hipError_t transpose_scale_split(const uint16_t* in, int64_t ldi, const float* s
     return hipGetLastError();
 }
 
+// Input perturbation of one token chunk, transposed: delta = Xhat - X (rows = tokens), and
+// the hi/lo bf16 pairs of s[r] * delta and of delta, written as [cols][rows].
+__global__ __launch_bounds__(256) void transpose_delta_kernel(const uint16_t* __restrict__ Xh,
+                                                              const uint16_t* __restrict__ X, int64_t ldi,
+                                                              const float* __restrict__ s, uint16_t* __restrict__ sdh,
+                                                              uint16_t* __restrict__ sdl, uint16_t* __restrict__ dh,
+                                                              uint16_t* __restrict__ dl, int64_t ldo, int64_t rows,
+                                                              int64_t cols, int64_t tiles_c) {
+    __shared__ float td[64][65];
+    __shared__ float ts[64];
+    const int64_t tr = blockIdx.x / tiles_c, tc = blockIdx.x % tiles_c;
+    const int64_t r0 = tr * 64, c0 = tc * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int rr = ty; rr < 64; rr += 4) {
+        const int64_t r = r0 + rr, c = c0 + tx;
+        float v = 0.f;
+        if (r < rows && c < cols) v = bf2f(Xh[r * ldi + c]) - bf2f(X[r * ldi + c]);
+        td[rr][tx] = v;
+    }
+    if (threadIdx.x < 64) {
+        const int64_t r = r0 + threadIdx.x;
+        ts[threadIdx.x] = (s && r < rows) ? s[r] : 1.f;
+    }
+    __syncthreads();
+    for (int cc = ty; cc < 64; cc += 4) {
+        const int64_t c = c0 + cc, r = r0 + tx;
+        if (r < rows && c < cols) {
+            const float d = td[tx][cc];
+            uint16_t hi, lo;
+            split_bf16(d * ts[tx], hi, lo);
+            sdh[c * ldo + r] = hi;
+            sdl[c * ldo + r] = lo;
+            split_bf16(d, hi, lo);
+            dh[c * ldo + r] = hi;
+            dl[c * ldo + r] = lo;
+        }
+    }
+}
+
+hipError_t transpose_delta_split(const uint16_t* Xh, const uint16_t* X, int64_t ldi, const float* s, uint16_t* sdh,
+                                 uint16_t* sdl, uint16_t* dh, uint16_t* dl, int64_t ldo, int64_t rows, int64_t cols,
+                                 hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    const int64_t tr = (rows + 63) / 64, tc = (cols + 63) / 64;
+    hipLaunchKernelGGL(transpose_delta_kernel, dim3((unsigned)(tr * tc)), dim3(256), 0, st, Xh, X, ldi, s, sdh, sdl,
+                       dh, dl, ldo, rows, cols, tc);
+    return hipGetLastError();
+}
+
+// out = A - double(B) (float64 minus float32, elementwise)
+__global__ void sub_f64_f32_kernel(const double* __restrict__ A, const float* __restrict__ B, double* __restrict__ out,
+                                   int64_t count) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x)
+        out[e] = A[e] - (double)B[e];
+}
+
+hipError_t sub_f64_f32(const double* A, const float* B, double* out, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(sub_f64_f32_kernel, dim3(grid_for(count, 4)), dim3(TB), 0, st, A, B, out, count);
+    return hipGetLastError();
+}
+
+// Deterministic dot product of two float64 arrays: each of DOT_BLOCKS blocks sums a fixed
+// strided subset in a fixed order and reduces it in a fixed tree; partials[b] receives it.
+constexpr int DOT_BLOCKS = 1024;
+__global__ __launch_bounds__(256) void dot_f64_kernel(const double* __restrict__ X, const double* __restrict__ Y,
+                                                      int64_t count, double* __restrict__ partials) {
+    __shared__ double red[256];
+    double acc = 0.0;
+    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < count; e += (int64_t)DOT_BLOCKS * 256) acc += X[e] * Y[e];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+        if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partials[blockIdx.x] = red[0];
+}
+
+hipError_t dot_f64(const double* X, const double* Y, int64_t count, double* partials, hipStream_t st) {
+    hipLaunchKernelGGL(dot_f64_kernel, dim3(DOT_BLOCKS), dim3(256), 0, st, X, Y, count, partials);
+    return hipGetLastError();
+}
+int64_t dot_f64_partials() { return DOT_BLOCKS; }
+
 __global__ __launch_bounds__(256) void transpose_f32_kernel(const float* __restrict__ in, int64_t ldi,
                                                             float* __restrict__ out, int64_t ldo, int64_t rows,
                                                             int64_t cols, int64_t tiles_c) {

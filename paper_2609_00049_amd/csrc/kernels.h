@@ -56,6 +56,16 @@ hipError_t split_diff_f32(const float* A, int64_t lda, const float* Bm, int64_t 
 // hi/lo[i*ld + j] = split(float(A[i*lda + j] - Bm[i*ldb + j])) for j < cols (float64 A, float32 Bm)
 hipError_t split_diff_f64(const double* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
                           int64_t ld, int64_t rows, int64_t cols, hipStream_t st);
+// Transposed input perturbation of a token chunk: delta = bf16(Xh) - bf16(X) ([rows = tokens,
+// cols]); sdh/sdl = split(s[r] * delta), dh/dl = split(delta), all written as [cols][ldo].
+hipError_t transpose_delta_split(const uint16_t* Xh, const uint16_t* X, int64_t ldi, const float* s, uint16_t* sdh,
+                                 uint16_t* sdl, uint16_t* dh, uint16_t* dl, int64_t ldo, int64_t rows, int64_t cols,
+                                 hipStream_t st);
+// out = A - double(B)
+hipError_t sub_f64_f32(const double* A, const float* B, double* out, int64_t count, hipStream_t st);
+// partials[0 .. dot_f64_partials()) = fixed-order partial sums of X . Y
+hipError_t dot_f64(const double* X, const double* Y, int64_t count, double* partials, hipStream_t st);
+int64_t dot_f64_partials();
 // out[i] = double(in[i]) / float(in[i])
 hipError_t widen_f32(const float* in, double* out, int64_t count, hipStream_t st);
 hipError_t narrow_f64(const double* in, float* out, int64_t count, hipStream_t st);
@@ -85,8 +95,7 @@ hipError_t reduce_splits(const float* Gp, int64_t splits, int64_t m, int64_t w, 
 hipError_t adam_update_dense(const AdamArgs& a, const float* G, hipStream_t st);
 
 // ---------------------------------------------------------------- fp32 GEMM (VALU): C = beta*C + alpha*A*B
-// A [M,K] lda, B [K,N] ldb, C [M,N] ldc, all float32 row-major.  Optional split of the
-// result: when Dhi != NULL, also Dhi/Dlo[i*ldd + j] = split(C[i][j] - W0[i*ldw + j]).
+// A [M,K] lda, B [K,N] ldb, C [M,N] ldc, all float32 row-major.
 struct SgemmArgs {
     const float* A;
     int64_t lda;
@@ -96,13 +105,12 @@ struct SgemmArgs {
     int64_t ldc;
     int64_t M, N, K;
     float alpha, beta;
-    const float* W0;
-    int64_t ldw;
-    uint16_t* Dhi;
-    uint16_t* Dlo;
-    int64_t ldd;
 };
 hipError_t sgemm(const SgemmArgs& a, hipStream_t st);
+// float64 VALU GEMM: C = A B (accumulate = false) or C += A B; A [M,K] lda, B [K,N] ldb,
+// C [M,N] ldc, all float64 row-major.
+hipError_t dgemm(const double* A, int64_t lda, const double* B, int64_t ldb, double* C, int64_t ldc, int64_t M,
+                 int64_t N, int64_t K, bool accumulate, hipStream_t st);
 
 // ---------------------------------------------------------------- quantize one column block
 struct QuantArgs {

@@ -48,3 +48,13 @@ def compare(gpu, ora, rows=None, group=128):
 
 def rel_fro(a, b):
     return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+
+def row_loss(W, W0, X, Xhat, s=None, M=None):
+    """Surrogate loss of given weights, written out in numpy float64 in the test itself (used on
+    GPU outputs, so it does not go through the oracle): (1/2T) sum_t s_t R_t^T M R_t."""
+    W, W0, X, Xhat = (np.asarray(a, dtype=np.float64) for a in (W, W0, X, Xhat))
+    R = W @ Xhat.T - W0 @ X.T
+    MR = R if M is None else np.asarray(M, dtype=np.float64) @ R
+    w = 1.0 if s is None else np.asarray(s, dtype=np.float64)[None, :]
+    return 0.5 / X.shape[0] * float(np.sum(R * MR * w))
