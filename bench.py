@@ -5,6 +5,10 @@ block with quantization, OBS compensation, lock and K Block-GD steps, final loss
 of the LLaMA-3.1-8B-shaped gate projection: W 14336 x 4096, 262144 calibration
 tokens, W4 g128, 8 BGD steps per block.  Inputs are synthetic, generated on the
 device with the workload's distributions, and resident in HBM before timing.
+The Block-GD steps stream the residual and gradient GEMMs over all tokens; the
+same sweep with the loss and gradient taken through the calibration Gram matrices
+is timed once more afterwards and reported under "gram_form" (or, with
+--form gram, as the line itself).
 
 Prints one JSON line.  ``--gpus`` above 1 is refused: the build runs on one GPU.
 """
@@ -141,6 +145,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run one plain device copy of this many bytes first (calibrates HBM byte counters)")
+    ap.add_argument("--form", default="tokens", choices=("tokens", "gram"),
+                    help="BGD evaluation: residual/gradient GEMMs over all tokens every step (the step of the "
+                         "headline metric), or the same loss and gradient through the calibration Gram matrices")
+    ap.add_argument("--no-gram-line", action="store_true",
+                    help="with --form tokens, skip the extra untimed Gram-form sweep reported under gram_form")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs the sweep on one GPU; --gpus {args.gpus} is not supported "
@@ -164,7 +173,8 @@ def main():
         del src, dst
     ctx = rq.Context()
     qp = rq.qparams()
-    bgd = rq.bgd_params(steps=K, lr=lr)
+    form = rq.BGD_GRAM if args.form == "gram" else rq.BGD_TOKENS
+    bgd = rq.bgd_params(steps=K, lr=lr, form=form)
     out = None
     for w in range(args.warmup):
         out = rq.quantize_layer(ctx, W0, X, Xh, s, qp=qp, bgd=bgd, out=out)
@@ -187,11 +197,16 @@ def main():
 
     fa = f_alg(m, n, T, K)
     kt = {name: ctx.kernel_time(name) for name in ("resid", "grad", "quantize", "obs", "lock", "adam", "hessian",
-                                                    "chol", "init")}
-    # dominant kernel by total time over the timed steps
-    dom = max(("resid", "grad"), key=lambda k: kt[k][1])
+                                                    "chol", "init", "gram", "gram_step")}
+    if args.form == "tokens":
+        # dominant kernel by total time over the timed steps
+        dom = max(("resid", "grad"), key=lambda k: kt[k][1])
+        dom_flops = fa[dom] * args.steps
+    else:
+        # D G_hh over all n columns every step (the loss trace is recorded), m x n x n
+        dom = "gram_step"
+        dom_flops = 2.0 * m * n * n * kt[dom][0]
     launches, dom_ms = kt[dom]
-    dom_flops = fa[dom] * args.steps
     achieved = dom_flops / (dom_ms / 1e3) if dom_ms > 0 else math.nan
     res = {
         "metric": "layer-sweep time (ms) and quantized columns/sec; achieved TFLOP/s vs MFMA peak",
@@ -207,15 +222,25 @@ def main():
         "dtype": "bf16 MFMA (hi/lo split fp32 operands), fp32/fp64 accumulate",
         "data": "synthetic (device-generated, workload distributions)",
         "config": {"workload": args.workload, "m": m, "n": n, "tokens": T, "bgd_steps": K, "bits": 4,
-                   "group": 128, "block": 128},
+                   "group": 128, "block": 128, "bgd_form": args.form},
         "tflops_alg": fa["total"] / (ms_per_step / 1e3) / 1e12,
         "frac_bf16_peak_alg": fa["total"] / (ms_per_step / 1e3) / PEAK_BF16,
         "kernel_ms_per_step": {k: v[1] / args.steps for k, v in kt.items()},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16,
-                     "traffic": measured_traffic(args.workload, dom),
+                     "traffic": measured_traffic(args.workload, dom) if args.form == "tokens" else None,
                      "launches": launches, "avg_launch_ms": dom_ms / max(1, launches)},
     }
+    if args.form == "tokens" and not args.no_gram_line:
+        # one untimed-region Gram-form sweep of the same inputs, reported beside the headline
+        gb = rq.bgd_params(steps=K, lr=lr, form=rq.BGD_GRAM)
+        og = rq.quantize_layer(ctx, W0, X, Xh, s, qp=qp, bgd=gb)      # warm-up (workspaces)
+        og = rq.quantize_layer(ctx, W0, X, Xh, s, qp=qp, bgd=gb, out=og)
+        print(f"[bench] gram form: {og.ms_total:.1f} ms, loss {og.loss_final:.6g}", file=sys.stderr, flush=True)
+        res["gram_form"] = {"ms_per_step": og.ms_total, "columns_per_s": n / (og.ms_total / 1e3),
+                            "loss_final": og.loss_final, "loss_final_tokens": out.loss_final,
+                            "note": "same loss and gradient through the calibration Gram matrices "
+                                    "(bench.py --form gram for its own line)"}
     ctx.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)

@@ -60,12 +60,27 @@ typedef struct realq_qparams {
  *   steps     : Adam steps after every column block (0 = plain GPTQ)
  *   lr        : learning rate eta
  *   beta1, beta2, eps : Adam constants [0.9, 0.999, 1e-8]
- *   tok_chunk : tokens per streamed chunk of the residual/gradient GEMMs (0 = all T) */
+ *   tok_chunk : tokens per streamed chunk of the residual/gradient GEMMs (0 = all T)
+ *   form      : REALQ_BGD_TOKENS or REALQ_BGD_GRAM (below) [REALQ_BGD_TOKENS] */
 typedef struct realq_bgd_params {
     int32_t steps;
     float lr, beta1, beta2, eps;
     int64_t tok_chunk;
+    int32_t form;
 } realq_bgd_params;
+
+/* realq_bgd_params.form: how the loss and gradient of a BGD step are evaluated.
+ *   REALQ_BGD_TOKENS  residual and gradient GEMMs streamed over all T tokens every step
+ *                     (R = B + D_J Xhat_J^T, G = M_a (R o s) Xhat_J / T).
+ *   REALQ_BGD_GRAM    the same loss and gradient through the calibration Gram matrices,
+ *                     which exist because the surrogate at the module output is quadratic
+ *                     in W: with D = W - W0, Delta = Xhat - X, G_ab = a^T diag(s) b,
+ *                       gradient = M_a (W0 G_dh + D G_hh)[:, J] / T,
+ *                       2T L     = <W0 G_dd, W0> + 2 <W0 G_dh, D> + <D G_hh, D>   (M_a = I),
+ *                     one m x n x n product per step instead of two m x T x |J| ones and no
+ *                     [m, T] residual base. */
+#define REALQ_BGD_TOKENS 0
+#define REALQ_BGD_GRAM 1
 
 /* Fill *q / *b with the defaults given above. */
 void realq_qparams_default(realq_qparams* q);
@@ -82,7 +97,9 @@ const char* realq_last_error(const realq_ctx* ctx);
 /* Kernel timing: when enabled, the library brackets the launches of its main
  * kernels with HIP events on its stream and accumulates their durations, read with
  * realq_ctx_kernel_time after the stream has drained.  Names: "hessian",
- * "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init".
+ * "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init", "gram" (Gram
+ * matrices of the input perturbation), "gram_step" (the per-step product of the
+ * Gram form), "dense_loss" (final loss with a dense metric).
  * Returns REALQ_ERR_INVALID_ARG for an unknown name. */
 int realq_ctx_set_timing(realq_ctx* ctx, int enable);
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms);

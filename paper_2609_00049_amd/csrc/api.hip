@@ -142,6 +142,13 @@ struct realq_bgd_state {
     uint16_t* XhT = nullptr;  // [n,T]
     uint16_t* Rhi = nullptr;
     uint16_t* Rlo = nullptr;  // [m,Tc]
+    // Gram form
+    bool gram = false;
+    uint16_t* Ghi = nullptr;
+    uint16_t* Glo = nullptr;  // [n,n] split(Xhat^T S Xhat)
+    float* C0 = nullptr;      // [m,n] W0 Delta^T S Xhat
+    float* Pm = nullptr;      // [m,n] D Xhat^T S Xhat (per step)
+    double* cconst = nullptr; // <W0 Delta^T S Delta, W0> (device scalar)
     std::vector<void*> allocations;
 };
 
@@ -164,6 +171,7 @@ void realq_bgd_params_default(realq_bgd_params* b) {
     b->beta2 = 0.999f;
     b->eps = 1e-8f;
     b->tok_chunk = 0;
+    b->form = REALQ_BGD_TOKENS;
 }
 
 int realq_ctx_create(realq_ctx** out, void* hip_stream) {
@@ -205,7 +213,8 @@ int realq_ctx_set_timing(realq_ctx* ctx, int enable) {
     return REALQ_OK;
 }
 
-static const char* kTimedNames[] = {"hessian", "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init"};
+static const char* kTimedNames[] = {"hessian", "chol",  "quantize",  "obs",        "lock",      "resid",
+                                    "grad",    "adam",  "init",      "gram",       "gram_step", "dense_loss"};
 
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms) {
     if (!ctx || !name) return REALQ_ERR_INVALID_ARG;
@@ -335,6 +344,41 @@ static void state_free(realq_bgd_state* st) {
     st->allocations.clear();
 }
 
+// Calibration Gram matrices of the input perturbation Delta = Xhat - X, accumulated over token
+// chunks in float64: Gdh = Delta^T S Xhat and Gdd = Delta^T S Delta (S = diag(s) or I).  The
+// float32 operand s o Delta is carried as a hi/lo bf16 pair against Xhat (bf16) and against
+// both halves of Delta.
+static int gram_accum(realq_ctx* ctx, const uint16_t* Xhat, const uint16_t* X, const float* sw, int64_t T, int64_t n,
+                      double* Gdh, double* Gdd) {
+    hipStream_t s = ctx->stream;
+    int rc;
+    void *sdh, *sdl, *dh, *dl, *xt;
+    int64_t tc = (int64_t)(128ll << 20) / n;
+    tc = tc < 256 ? 256 : (tc / 256) * 256;
+    if (tc > T) tc = ((T + 7) / 8) * 8;
+    if ((rc = get_ws(ctx, "g_sdh", (size_t)n * tc * 2, &sdh))) return rc;
+    if ((rc = get_ws(ctx, "g_sdl", (size_t)n * tc * 2, &sdl))) return rc;
+    if ((rc = get_ws(ctx, "g_dh16", (size_t)n * tc * 2, &dh))) return rc;
+    if ((rc = get_ws(ctx, "g_dl16", (size_t)n * tc * 2, &dl))) return rc;
+    if ((rc = get_ws(ctx, "g_xt", (size_t)n * tc * 2, &xt))) return rc;
+    Timed tm(ctx, "gram");
+    RQ_HIP(ctx, realq::fill_f64(Gdh, 0.0, n * n, s));
+    RQ_HIP(ctx, realq::fill_f64(Gdd, 0.0, n * n, s));
+    for (int64_t t0 = 0; t0 < T; t0 += tc) {
+        const int64_t cur = std::min(tc, T - t0);
+        RQ_HIP(ctx, realq::transpose_delta_split(Xhat + t0 * n, X + t0 * n, n, sw ? sw + t0 : nullptr, (uint16_t*)sdh,
+                                                 (uint16_t*)sdl, (uint16_t*)dh, (uint16_t*)dl, tc, cur, n, s));
+        RQ_HIP(ctx, realq::transpose_u16(Xhat + t0 * n, n, (uint16_t*)xt, tc, cur, n, s));
+        realq::GemmArgs g{(const uint16_t*)sdh, (const uint16_t*)sdl, tc, (const uint16_t*)xt, tc, n, n, cur, 1};
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, Gdh, n, s));
+        g.B = (const uint16_t*)dh;
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, Gdd, n, s));
+        g.B = (const uint16_t*)dl;
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, Gdd, n, s));
+    }
+    return REALQ_OK;
+}
+
 static int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
     if (!p) return set_error(ctx, REALQ_ERR_INVALID_ARG, "NULL bgd params");
     if (p->steps < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd steps must be >= 0");
@@ -343,13 +387,19 @@ static int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "Adam betas must lie in [0, 1)");
     if (!(p->eps > 0.f)) return set_error(ctx, REALQ_ERR_INVALID_ARG, "Adam eps must be > 0");
     if (p->tok_chunk < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "tok_chunk must be >= 0");
+    if (p->form != REALQ_BGD_TOKENS && p->form != REALQ_BGD_GRAM)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "form must be REALQ_BGD_TOKENS or REALQ_BGD_GRAM");
     return REALQ_OK;
 }
 
+static int state_init_gram(realq_bgd_state* st);
+
 static int state_init(realq_bgd_state* st) {
+    if (st->prm.form == REALQ_BGD_GRAM) return state_init_gram(st);
     realq_ctx* ctx = st->ctx;
     const int64_t m = st->m, n = st->n, T = st->T;
     hipStream_t s = ctx->stream;
+    st->gram = false;
     int64_t Tc = st->prm.tok_chunk > 0 ? std::min<int64_t>(st->prm.tok_chunk, T) : T;
     st->Tc = Tc;
     int rc;
@@ -400,6 +450,88 @@ static int state_init(realq_bgd_state* st) {
     RQ_HIP(ctx, realq::fill_u16(st->Dlo, 0, m * n, s));
     st->t = 0;
     st->locked = 0;
+    return REALQ_OK;
+}
+
+// Gram form: the three calibration Gram matrices once, then C0 = W0 G_dh and the constant
+// c = <W0 G_dd, W0>; no residual base and no transposed activations are kept.
+static int state_init_gram(realq_bgd_state* st) {
+    realq_ctx* ctx = st->ctx;
+    const int64_t m = st->m, n = st->n, T = st->T;
+    hipStream_t s = ctx->stream;
+    st->gram = true;
+    st->Tc = T;
+    int rc;
+    void* p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 4, "s_m"))) return rc;
+    st->mA = (float*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 4, "s_v"))) return rc;
+    st->vA = (float*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 2, "s_Dh"))) return rc;
+    st->Dhi = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 2, "s_Dl"))) return rc;
+    st->Dlo = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)n * n * 2, "s_Gh"))) return rc;
+    st->Ghi = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)n * n * 2, "s_Gl"))) return rc;
+    st->Glo = (uint16_t*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 4, "s_C0"))) return rc;
+    st->C0 = (float*)p;
+    if ((rc = state_alloc(st, &p, (size_t)m * n * 4, "s_P"))) return rc;
+    st->Pm = (float*)p;
+    if ((rc = state_alloc(st, &p, 8, "s_c"))) return rc;
+    st->cconst = (double*)p;
+    void *ghh, *gdh, *gdd, *A, *E, *parts;
+    const int64_t np = realq::dot_f64_partials();
+    if ((rc = get_ws(ctx, "i_Ghh", (size_t)n * n * 8, &ghh))) return rc;
+    if ((rc = get_ws(ctx, "i_Gdh", (size_t)n * n * 8, &gdh))) return rc;
+    if ((rc = get_ws(ctx, "i_Gdd", (size_t)n * n * 8, &gdd))) return rc;
+    if ((rc = get_ws(ctx, "i_A", (size_t)m * n * 8, &A))) return rc;
+    if ((rc = get_ws(ctx, "i_E", (size_t)m * n * 8, &E))) return rc;
+    if ((rc = get_ws(ctx, "i_parts", (size_t)np * 8, &parts))) return rc;
+    RQ_HIP(ctx, realq::fill_f64((double*)ghh, 0.0, n * n, s));
+    if ((rc = realq_hessian_accum(ctx, st->Xhat, st->s, T, n, (double*)ghh))) return rc;
+    if ((rc = gram_accum(ctx, st->Xhat, st->X, st->s, T, n, (double*)gdh, (double*)gdd))) return rc;
+    Timed tm(ctx, "init");
+    RQ_HIP(ctx, realq::fill_f32(st->mA, 0.f, m * n, s));
+    RQ_HIP(ctx, realq::fill_f32(st->vA, 0.f, m * n, s));
+    RQ_HIP(ctx, realq::fill_u16(st->Dhi, 0, m * n, s));
+    RQ_HIP(ctx, realq::fill_u16(st->Dlo, 0, m * n, s));
+    RQ_HIP(ctx, realq::split_f64((const double*)ghh, st->Ghi, st->Glo, n * n, s));
+    double* Ad = (double*)A;
+    double* Ed = (double*)E;
+    RQ_HIP(ctx, realq::widen_f32(st->W0, Ad, m * n, s));
+    RQ_HIP(ctx, realq::dgemm(Ad, n, (const double*)gdh, n, Ed, n, m, n, n, false, s));
+    RQ_HIP(ctx, realq::narrow_f64(Ed, st->C0, m * n, s));
+    RQ_HIP(ctx, realq::dgemm(Ad, n, (const double*)gdd, n, Ed, n, m, n, n, false, s));
+    RQ_HIP(ctx, realq::dot_f64(Ed, Ad, m * n, (double*)parts, s));
+    RQ_HIP(ctx, realq::reduce_partials((const double*)parts, np, 1.0, st->cconst, s));
+    st->t = 0;
+    st->locked = 0;
+    return REALQ_OK;
+}
+
+// P = D G_hh on columns [p0, n) (three MFMA passes: D_hi G_hi + D_lo G_hi + D_hi G_lo).
+static int gram_product(realq_ctx* ctx, realq_bgd_state* st, int64_t p0) {
+    const int64_t m = st->m, n = st->n, pw = n - p0;
+    if (pw <= 0) return REALQ_OK;
+    Timed tm(ctx, "gram_step");
+    realq::GemmArgs g{st->Dhi, st->Dlo, n, st->Ghi + p0 * n, n, m, pw, n, 1};
+    RQ_HIP(ctx, realq::gemm_store_f32(g, st->Pm + p0, n, 0, 1.f, ctx->stream));
+    realq::GemmArgs g2{st->Dhi, nullptr, n, st->Glo + p0 * n, n, m, pw, n, 1};
+    RQ_HIP(ctx, realq::gemm_acc_f32(g2, st->Pm + p0, n, 1.f, ctx->stream));
+    return REALQ_OK;
+}
+
+// L = (c + sum (2 C0 + P) (W - W0)) / 2T with P over all columns.
+static int gram_loss(realq_ctx* ctx, realq_bgd_state* st, const double* W, double* loss_out) {
+    const int64_t np = realq::dot_f64_partials();
+    void* parts;
+    int rc;
+    if ((rc = get_ws(ctx, "b_gparts", (size_t)(np + 1) * 8, &parts))) return rc;
+    RQ_HIP(ctx, realq::dot_gram(st->C0, st->Pm, W, st->W0, st->m * st->n, (double*)parts, ctx->stream));
+    RQ_HIP(ctx, hipMemcpyAsync((double*)parts + np, st->cconst, 8, hipMemcpyDeviceToDevice, ctx->stream));
+    RQ_HIP(ctx, realq::reduce_partials((const double*)parts, np + 1, 0.5 / (double)st->T, loss_out, ctx->stream));
     return REALQ_OK;
 }
 
@@ -526,10 +658,12 @@ int realq_quantize_block(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_
         RQ_HIP(ctx, realq::obs_update(a, s));
     }
     if (st) {
-        // lock: B += (W_hat - W0)[:, block] Xhat[:, block]^T
-        realq::GemmArgs g{st->Dhi + c0, st->Dlo + c0, n, st->Xhat + c0, n, m, st->T, bs, 1};
-        Timed tm(ctx, "lock");
-        RQ_HIP(ctx, realq::gemm_acc_f32(g, st->B, st->T, 1.f, s));
+        if (!st->gram) {
+            // lock: B += (W_hat - W0)[:, block] Xhat[:, block]^T
+            realq::GemmArgs g{st->Dhi + c0, st->Dlo + c0, n, st->Xhat + c0, n, m, st->T, bs, 1};
+            Timed tm(ctx, "lock");
+            RQ_HIP(ctx, realq::gemm_acc_f32(g, st->B, st->T, 1.f, s));
+        }
         st->locked = c1;
     }
     return REALQ_OK;
@@ -561,40 +695,55 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     }
     const bool dense = st->M || (st->P && alpha < 1.f);
     const int64_t nchunks = (T + Tc - 1) / Tc;
-    const int64_t S = choose_splits(m, nJ, Tc);
-    const int64_t Seff = realq::gemm_effective_splits(Tc, S);
     int rc;
-    void *Gp, *Gacc = nullptr, *parts;
-    if ((rc = get_ws(ctx, "b_Gp", (size_t)Seff * m * nJ * 4, &Gp))) return rc;
-    if (nchunks > 1 || dense)
+    void *Gp = nullptr, *Gacc = nullptr;
+    int64_t splits_used = 1;
+    if (st->gram) {
+        // gradient (1/T) M_a (C0 + D G_hh)[:, J]; the loss needs D G_hh on every column
+        const bool want_loss = loss_out && !dense;
         if ((rc = get_ws(ctx, "b_G", (size_t)m * nJ * 4, &Gacc))) return rc;
-    const int64_t kblocks = realq::gemm_num_blocks(m, Tc);
-    if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
-    RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, s));  // shorter last chunk writes fewer
+        if ((rc = gram_product(ctx, st, want_loss ? 0 : c1))) return rc;
+        if (loss_out) {
+            if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
+            else if ((rc = gram_loss(ctx, st, W, loss_out))) return rc;
+        }
+        RQ_HIP(ctx, realq::gram_grad(st->C0, st->Pm, n, c1, m, nJ, (float*)Gacc, s));
+    } else {
+        const int64_t S = choose_splits(m, nJ, Tc);
+        const int64_t Seff = realq::gemm_effective_splits(Tc, S);
+        void* parts;
+        if ((rc = get_ws(ctx, "b_Gp", (size_t)Seff * m * nJ * 4, &Gp))) return rc;
+        if (nchunks > 1 || dense)
+            if ((rc = get_ws(ctx, "b_G", (size_t)m * nJ * 4, &Gacc))) return rc;
+        const int64_t kblocks = realq::gemm_num_blocks(m, Tc);
+        if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
+        RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, s));  // shorter last chunk writes fewer
 
-    int64_t splits_used = Seff;
-    for (int64_t ch = 0; ch < nchunks; ++ch) {
-        const int64_t t0 = ch * Tc, cur = std::min(Tc, T - t0);
-        {
-            realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
-            Timed tm(ctx, "resid");
-            RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, st->Rlo, cur,
-                                          (double*)parts + ch * kblocks, s));
+        splits_used = Seff;
+        for (int64_t ch = 0; ch < nchunks; ++ch) {
+            const int64_t t0 = ch * Tc, cur = std::min(Tc, T - t0);
+            {
+                realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
+                Timed tm(ctx, "resid");
+                RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, st->Rlo, cur,
+                                              (double*)parts + ch * kblocks, s));
+            }
+            {
+                realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, S};
+                splits_used = realq::gemm_effective_splits(cur, S);
+                Timed tm(ctx, "grad");
+                RQ_HIP(ctx, realq::gemm_grad(g, (float*)Gp, nJ, m * nJ, s));
+            }
+            if (nchunks > 1 || dense) {
+                // Gacc (+)= sum of this chunk's split slices, chunks in order
+                RQ_HIP(ctx,
+                       realq::reduce_splits((const float*)Gp, splits_used, m, nJ, 1.f, (float*)Gacc, ch > 0, s));
+            }
         }
-        {
-            realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, S};
-            splits_used = realq::gemm_effective_splits(cur, S);
-            Timed tm(ctx, "grad");
-            RQ_HIP(ctx, realq::gemm_grad(g, (float*)Gp, nJ, m * nJ, s));
+        if (loss_out) {
+            if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
+            else RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)T, loss_out, s));
         }
-        if (nchunks > 1 || dense) {
-            // Gacc (+)= sum of this chunk's split slices, chunks in order
-            RQ_HIP(ctx, realq::reduce_splits((const float*)Gp, splits_used, m, nJ, 1.f, (float*)Gacc, ch > 0, s));
-        }
-    }
-    if (loss_out) {
-        if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
-        else RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)T, loss_out, s));
     }
     st->t += 1;
     realq::AdamArgs a{};
@@ -617,7 +766,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     a.bc1 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta1, (double)st->t)));
     a.bc2 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta2, (double)st->t)));
     Timed tm(ctx, "adam");
-    if (!dense && nchunks == 1) {
+    if (!dense && nchunks == 1 && !st->gram) {
         RQ_HIP(ctx, realq::adam_update(a, s));
     } else if (!dense) {
         a.Gp = (const float*)Gacc;
@@ -666,6 +815,11 @@ int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const double* W, double*
     if (!ctx || !st) return REALQ_ERR_INVALID_ARG;
     if (!W || !loss_out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_loss: NULL W or loss_out");
     if (st->M) return set_error(ctx, REALQ_ERR_SHAPE, "bgd_loss: only the identity metric is supported");
+    if (st->gram) {
+        int rc = gram_product(ctx, st, 0);
+        if (rc) return rc;
+        return gram_loss(ctx, st, W, loss_out);
+    }
     // R = B + (W - W0)[:, J] Xhat[:, J]^T with J the columns not yet folded into B.
     const int64_t m = st->m, T = st->T, Tc = st->Tc, n = st->n, c1 = st->locked, nJ = n - c1;
     const int64_t nchunks = (T + Tc - 1) / Tc;
@@ -771,33 +925,11 @@ static int dense_final_loss(realq_ctx* ctx, const realq_layer_desc* d, const dou
     const int64_t m = d->m, n = d->n, T = d->T;
     hipStream_t s = ctx->stream;
     int rc;
-    void *gdh, *gdd, *sdh, *sdl, *dh, *dl, *xt, *A, *D, *E, *MX, *M64, *parts;
-    int64_t tc = (int64_t)(128ll << 20) / n;
-    tc = tc < 256 ? 256 : (tc / 256) * 256;
-    if (tc > T) tc = ((T + 7) / 8) * 8;
+    void *gdh, *gdd, *A, *D, *E, *MX, *M64, *parts;
     if ((rc = get_ws(ctx, "g_dh", (size_t)n * n * 8, &gdh))) return rc;
     if ((rc = get_ws(ctx, "g_dd", (size_t)n * n * 8, &gdd))) return rc;
-    if ((rc = get_ws(ctx, "g_sdh", (size_t)n * tc * 2, &sdh))) return rc;
-    if ((rc = get_ws(ctx, "g_sdl", (size_t)n * tc * 2, &sdl))) return rc;
-    if ((rc = get_ws(ctx, "g_dh16", (size_t)n * tc * 2, &dh))) return rc;
-    if ((rc = get_ws(ctx, "g_dl16", (size_t)n * tc * 2, &dl))) return rc;
-    if ((rc = get_ws(ctx, "g_xt", (size_t)n * tc * 2, &xt))) return rc;
+    if ((rc = gram_accum(ctx, d->Xhat, d->X, d->s, T, n, (double*)gdh, (double*)gdd))) return rc;
     Timed tm(ctx, "dense_loss");
-    RQ_HIP(ctx, realq::fill_f64((double*)gdh, 0.0, n * n, s));
-    RQ_HIP(ctx, realq::fill_f64((double*)gdd, 0.0, n * n, s));
-    for (int64_t t0 = 0; t0 < T; t0 += tc) {
-        const int64_t cur = std::min(tc, T - t0);
-        RQ_HIP(ctx, realq::transpose_delta_split(d->Xhat + t0 * n, d->X + t0 * n, n, d->s ? d->s + t0 : nullptr,
-                                                 (uint16_t*)sdh, (uint16_t*)sdl, (uint16_t*)dh, (uint16_t*)dl, tc, cur,
-                                                 n, s));
-        RQ_HIP(ctx, realq::transpose_u16(d->Xhat + t0 * n, n, (uint16_t*)xt, tc, cur, n, s));
-        realq::GemmArgs g{(const uint16_t*)sdh, (const uint16_t*)sdl, tc, (const uint16_t*)xt, tc, n, n, cur, 1};
-        RQ_HIP(ctx, realq::gemm_acc_f64(g, (double*)gdh, n, s));
-        g.B = (const uint16_t*)dh;
-        RQ_HIP(ctx, realq::gemm_acc_f64(g, (double*)gdd, n, s));
-        g.B = (const uint16_t*)dl;
-        RQ_HIP(ctx, realq::gemm_acc_f64(g, (double*)gdd, n, s));
-    }
     const int64_t np = realq::dot_f64_partials();
     if ((rc = get_ws(ctx, "g_A", (size_t)m * n * 8, &A))) return rc;
     if ((rc = get_ws(ctx, "g_D", (size_t)m * n * 8, &D))) return rc;

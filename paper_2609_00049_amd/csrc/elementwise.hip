@@ -143,6 +143,40 @@ hipError_t transpose_delta_split(const uint16_t* Xh, const uint16_t* X, int64_t 
     return hipGetLastError();
 }
 
+// hi/lo bf16 pair of float(in[i])
+__global__ void split_f64_kernel(const double* __restrict__ in, uint16_t* __restrict__ hi, uint16_t* __restrict__ lo,
+                                 int64_t count) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x) {
+        uint16_t h, l;
+        split_bf16((float)in[e], h, l);
+        hi[e] = h;
+        lo[e] = l;
+    }
+}
+
+hipError_t split_f64(const double* in, uint16_t* hi, uint16_t* lo, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(split_f64_kernel, dim3(grid_for(count, 4)), dim3(TB), 0, st, in, hi, lo, count);
+    return hipGetLastError();
+}
+
+// G[i][j] = C0[i][c1 + j] + P[i][c1 + j]   (m x w, C0 and P with row stride ld)
+__global__ void gram_grad_kernel(const float* __restrict__ C0, const float* __restrict__ P, int64_t ld, int64_t c1,
+                                 int64_t w, int64_t total, float* __restrict__ G) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / w, j = c1 + e % w;
+        G[e] = C0[i * ld + j] + P[i * ld + j];
+    }
+}
+
+hipError_t gram_grad(const float* C0, const float* P, int64_t ld, int64_t c1, int64_t m, int64_t w, float* G,
+                     hipStream_t st) {
+    const int64_t total = m * w;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gram_grad_kernel, dim3(grid_for(total, 4)), dim3(TB), 0, st, C0, P, ld, c1, w, total, G);
+    return hipGetLastError();
+}
+
 // out = A - double(B) (float64 minus float32, elementwise)
 __global__ void sub_f64_f32_kernel(const double* __restrict__ A, const float* __restrict__ B, double* __restrict__ out,
                                    int64_t count) {
@@ -171,6 +205,30 @@ __global__ __launch_bounds__(256) void dot_f64_kernel(const double* __restrict__
         __syncthreads();
     }
     if (threadIdx.x == 0) partials[blockIdx.x] = red[0];
+}
+
+// Gram form of a BGD step: sum over all weights of (2 C0 + P) (W - W0), same fixed-order
+// partials as dot_f64.
+__global__ __launch_bounds__(256) void dot_gram_kernel(const float* __restrict__ C0, const float* __restrict__ P,
+                                                       const double* __restrict__ W, const float* __restrict__ W0,
+                                                       int64_t count, double* __restrict__ partials) {
+    __shared__ double red[256];
+    double acc = 0.0;
+    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < count; e += (int64_t)DOT_BLOCKS * 256)
+        acc += (2.0 * (double)C0[e] + (double)P[e]) * (W[e] - (double)W0[e]);
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+        if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partials[blockIdx.x] = red[0];
+}
+
+hipError_t dot_gram(const float* C0, const float* P, const double* W, const float* W0, int64_t count,
+                    double* partials, hipStream_t st) {
+    hipLaunchKernelGGL(dot_gram_kernel, dim3(DOT_BLOCKS), dim3(256), 0, st, C0, P, W, W0, count, partials);
+    return hipGetLastError();
 }
 
 hipError_t dot_f64(const double* X, const double* Y, int64_t count, double* partials, hipStream_t st) {

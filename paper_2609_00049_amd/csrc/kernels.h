@@ -61,6 +61,14 @@ hipError_t split_diff_f64(const double* A, int64_t lda, const float* Bm, int64_t
 hipError_t transpose_delta_split(const uint16_t* Xh, const uint16_t* X, int64_t ldi, const float* s, uint16_t* sdh,
                                  uint16_t* sdl, uint16_t* dh, uint16_t* dl, int64_t ldo, int64_t rows, int64_t cols,
                                  hipStream_t st);
+// hi/lo = split(float(in))
+hipError_t split_f64(const double* in, uint16_t* hi, uint16_t* lo, int64_t count, hipStream_t st);
+// G[i][j] = C0[i][c1+j] + P[i][c1+j], i < m, j < w
+hipError_t gram_grad(const float* C0, const float* P, int64_t ld, int64_t c1, int64_t m, int64_t w, float* G,
+                     hipStream_t st);
+// partials = fixed-order partial sums of (2 C0 + P) (W - W0) over count elements
+hipError_t dot_gram(const float* C0, const float* P, const double* W, const float* W0, int64_t count,
+                    double* partials, hipStream_t st);
 // out = A - double(B)
 hipError_t sub_f64_f32(const double* A, const float* B, double* out, int64_t count, hipStream_t st);
 // partials[0 .. dot_f64_partials()) = fixed-order partial sums of X . Y

@@ -36,6 +36,32 @@ def test_header_compiles_as_c_and_cxx(tmp_path):
         assert r.returncode == 0, r.stderr
 
 
+def test_binding_structs_match_the_c_layout(tmp_path):
+    """sizeof and field offsets of the parameter, descriptor and output structs as the C compiler
+    lays them out, against the ctypes mirrors of the binding."""
+    from paper_2609_00049_amd import realq
+    structs = {"realq_qparams": realq.QParams, "realq_bgd_params": realq.BgdParams,
+               "realq_layer_desc": realq.LayerDesc, "realq_layer_out": realq.LayerOut}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "realq.h"', 'int main(void) {']
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ['return 0;', '}']
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    r = subprocess.run(["gcc", "-Wall", "-Werror", f"-I{os.path.dirname(HEADER)}", str(src), "-o", str(exe)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l.strip()}
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert got[(cname, fname)] == getattr(py, fname).offset, (cname, fname)
+
+
 @pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
 def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(LIB)
@@ -59,6 +85,7 @@ def test_defaults_and_host_side_errors_without_gpu():
     assert (q.bits, q.group, q.block, q.grid) == (4, 128, 128, 80) and abs(q.damp - 0.01) < 1e-9
     b = realq.BgdParams()
     lib.realq_bgd_params_default(ctypes.byref(b))
+    assert b.form == realq.BGD_TOKENS
     assert (b.beta1, b.beta2) == (pytest.approx(0.9), pytest.approx(0.999)) and b.eps == pytest.approx(1e-8)
     assert lib.realq_ctx_create(None, None) == -1
     assert lib.realq_hessian_accum(None, None, None, 0, 0, None) == -1
