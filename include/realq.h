@@ -61,12 +61,24 @@ typedef struct realq_qparams {
  *   lr        : learning rate eta
  *   beta1, beta2, eps : Adam constants [0.9, 0.999, 1e-8]
  *   tok_chunk : tokens per streamed chunk of the residual/gradient GEMMs (0 = all T)
- *   form      : REALQ_BGD_TOKENS or REALQ_BGD_GRAM (below) [REALQ_BGD_TOKENS] */
+ *   form      : REALQ_BGD_TOKENS or REALQ_BGD_GRAM (below) [REALQ_BGD_TOKENS]
+ *   loss_clip : output-perturbation clip quantile q in (0, 1], 0 = off [0] (Appendix D.1,
+ *               a_loss_clip): each step scales every token's channels whose |R| exceeds
+ *               the token's nearest-rank q-quantile over the m channels down to it, the
+ *               factor c = tau_t / |R| held fixed (loss sum s (cR)^2, gradient through
+ *               c^2 R).  Needs the identity metric (no M, no window partner P).
+ *   batch     : tokens per BGD step, 0 = all T [0] (Sec. 4.3, calibration mini-batch):
+ *               Adam step t of the module (1-based) uses the consecutive token batch
+ *               (t - 1) mod ceil(T / batch); loss and gradient are normalised by its
+ *               size.  The final loss is always over all T tokens and unclipped.
+ *   The Gram form takes neither a clip nor a batch smaller than T. */
 typedef struct realq_bgd_params {
     int32_t steps;
     float lr, beta1, beta2, eps;
     int64_t tok_chunk;
     int32_t form;
+    float loss_clip;
+    int64_t batch;
 } realq_bgd_params;
 
 /* realq_bgd_params.form: how the loss and gradient of a BGD step are evaluated.

@@ -43,13 +43,18 @@ Readings where the paper is silent (each is listed in the design notes):
     exactly what (codes, scales, zeros) describe;
   * damping: dead columns (H_jj == 0) get H_jj = 1 and their weights zeroed, then
     lambda = damp * mean(diag H) is added to the diagonal;
-  * BGD uses all T tokens per step, ``steps`` Adam steps after every block except
-    the last, one Adam step counter per module;
+  * BGD uses all T tokens per step unless a mini-batch size is given (then consecutive
+    token batches in cyclic order, one per Adam step), ``steps`` Adam steps after every
+    block except the last, one Adam step counter per module;
+  * the optional output-perturbation clip (a_loss_clip) scales each token's channels above
+    that token's nearest-rank q-quantile of |R| down to it, with the factor held fixed;
   * the surrogate is evaluated at the module output:
         R = W Xhat^T - W0 X^T,   L = (1/2T) sum_t s_t R_t^T M R_t,
         grad_W L = (1/T) M R diag(s) Xhat.
 """
 from __future__ import annotations
+
+import math
 
 from dataclasses import dataclass, field
 from typing import List, Optional, Tuple
@@ -243,6 +248,44 @@ def adam_update(W_J, G, mA, vA, t, lr, b1=ADAM_BETA1, b2=ADAM_BETA2, eps=ADAM_EP
     return W_J - lr * mhat / (np.sqrt(vhat) + eps), mA, vA
 
 
+def minibatch(t: int, T: int, batch: Optional[int]) -> slice:
+    """Tokens of Adam step t (1-based, counted over the module) when each step uses a
+    mini-batch (Sec. 4.3: the surrogate is evaluated on a calibration mini-batch): the
+    calibration tokens are cut into consecutive batches of ``batch`` tokens (the last one
+    shorter when batch does not divide T) and the steps cycle through them in order.
+    ``batch = None`` (or >= T) means all tokens every step."""
+    if batch is None or batch >= T:
+        return slice(0, T)
+    nb = -(-T // batch)
+    i = (t - 1) % nb
+    return slice(i * batch, min(T, (i + 1) * batch))
+
+
+def clip_factor(R: np.ndarray, q: float) -> np.ndarray:
+    """Detached per-entry scale of the output-perturbation clip (Appendix D.1, a_loss_clip):
+    for every token (column of R) the channels whose |R| exceeds that token's q-quantile
+    over channels are scaled down to it, c = min(1, tau_t / |R|).  The quantile is the
+    nearest-rank order statistic: the ceil(q m)-th smallest |R[:, t]|."""
+    A = np.abs(R)
+    m = A.shape[0]
+    k = max(1, int(math.ceil(q * m)))
+    tau = np.sort(A, axis=0)[k - 1][None, :]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        c = np.where(A > tau, tau / A, 1.0)
+    return c
+
+
+def clipped_grad(R, c, s, Ma, Xhat_J, T):
+    """Gradient of (1/2T) sum_t s_t (c R)_t^T Ma (c R)_t with c held fixed:
+    (1/T) (c o Ma (c o R)) diag(s) Xhat_J."""
+    Rc = c * R
+    MRc = Rc if Ma is None else Ma @ Rc
+    Y = c * MRc
+    if s is not None:
+        Y = Y * s[None, :]
+    return Y @ Xhat_J / T
+
+
 def window_alpha(b_global: int, B_total: int) -> float:
     """alpha of Eq. slide_window with a 1-based column-block step b_global of B_total.
 
@@ -273,13 +316,17 @@ class LayerResult:
 
 def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams] = None,
                    steps: int = 0, lr: float = 1e-3, window: Optional[Tuple[int, int]] = None,
-                   keep_E: bool = False) -> LayerResult:
+                   keep_E: bool = False, batch: Optional[int] = None,
+                   loss_clip: Optional[float] = None) -> LayerResult:
     """The per-module REAL-Q sweep (Alg. 1, one linear module), in float64.
 
     W0 [m, n]; X, Xhat [T, n]; s [T] or None; M [m, m] or None (identity);
     P [m, m] or None: the consumer's pulled-back metric used by the sliding window;
     ``window = (b_offset, B_total)`` turns the window on: column block b of this
     module is window step b_global = b_offset + b + 1 of B_total.
+    ``batch``: tokens per Adam step (see ``minibatch``; None = all T).  ``loss_clip``: the
+    output-perturbation clip quantile q of ``clip_factor`` applied to the residual of every
+    BGD step (None = off).  The final loss is always over all tokens, unclipped.
     """
     qp = qp or QParams()
     W0 = np.asarray(W0, dtype=np.float64)
@@ -343,9 +390,17 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
             J = slice(c1, n)
             for k in range(steps):
                 t += 1
-                R = residual(W, W0, X, Xhat)
-                trace.append((b, k, surrogate_loss(R, s, Ma, T)))
-                G = surrogate_grad(R, s, Ma, Xhat[:, J], T)
+                sl = minibatch(t, T, batch)
+                Tb = sl.stop - sl.start
+                sb = None if s is None else s[sl]
+                R = residual(W, W0, X[sl], Xhat[sl])
+                if loss_clip is None:
+                    trace.append((b, k, surrogate_loss(R, sb, Ma, Tb)))
+                    G = surrogate_grad(R, sb, Ma, Xhat[sl, J], Tb)
+                else:
+                    c = clip_factor(R, loss_clip)
+                    trace.append((b, k, surrogate_loss(c * R, sb, Ma, Tb)))
+                    G = clipped_grad(R, c, sb, Ma, Xhat[sl, J], Tb)
                 W[:, J], mA[:, J], vA[:, J] = adam_update(W[:, J], G, mA[:, J], vA[:, J], t, lr)
 
     R = residual(W, W0, X, Xhat)

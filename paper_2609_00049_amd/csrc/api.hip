@@ -142,6 +142,9 @@ struct realq_bgd_state {
     uint16_t* XhT = nullptr;  // [n,T]
     uint16_t* Rhi = nullptr;
     uint16_t* Rlo = nullptr;  // [m,Tc]
+    int64_t Tb = 0, nbatch = 1;  // tokens per step and number of batches (mini-batch BGD)
+    float* Rf = nullptr;         // [m,Tc] residual kept whole for the clip
+    float* tau = nullptr;        // [Tc] per-token clip thresholds
     // Gram form
     bool gram = false;
     uint16_t* Ghi = nullptr;
@@ -172,6 +175,8 @@ void realq_bgd_params_default(realq_bgd_params* b) {
     b->eps = 1e-8f;
     b->tok_chunk = 0;
     b->form = REALQ_BGD_TOKENS;
+    b->loss_clip = 0.f;
+    b->batch = 0;
 }
 
 int realq_ctx_create(realq_ctx** out, void* hip_stream) {
@@ -389,6 +394,9 @@ static int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
     if (p->tok_chunk < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "tok_chunk must be >= 0");
     if (p->form != REALQ_BGD_TOKENS && p->form != REALQ_BGD_GRAM)
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "form must be REALQ_BGD_TOKENS or REALQ_BGD_GRAM");
+    if (!std::isfinite(p->loss_clip) || p->loss_clip < 0.f || p->loss_clip > 1.f)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "loss_clip must lie in [0, 1] (0 = off)");
+    if (p->batch < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "batch must be >= 0");
     return REALQ_OK;
 }
 
@@ -400,7 +408,9 @@ static int state_init(realq_bgd_state* st) {
     const int64_t m = st->m, n = st->n, T = st->T;
     hipStream_t s = ctx->stream;
     st->gram = false;
-    int64_t Tc = st->prm.tok_chunk > 0 ? std::min<int64_t>(st->prm.tok_chunk, T) : T;
+    st->Tb = (st->prm.batch > 0 && st->prm.batch < T) ? st->prm.batch : T;
+    st->nbatch = (T + st->Tb - 1) / st->Tb;
+    int64_t Tc = st->prm.tok_chunk > 0 ? std::min<int64_t>(st->prm.tok_chunk, st->Tb) : st->Tb;
     st->Tc = Tc;
     int rc;
     void* p;
@@ -420,6 +430,12 @@ static int state_init(realq_bgd_state* st) {
     st->Rhi = (uint16_t*)p;
     if ((rc = state_alloc(st, &p, (size_t)m * Tc * 2, "s_Rl"))) return rc;
     st->Rlo = (uint16_t*)p;
+    if (st->prm.loss_clip > 0.f) {
+        if ((rc = state_alloc(st, &p, (size_t)m * Tc * 4, "s_Rf"))) return rc;
+        st->Rf = (float*)p;
+        if ((rc = state_alloc(st, &p, (size_t)Tc * 4, "s_tau"))) return rc;
+        st->tau = (float*)p;
+    }
 
     Timed tm(ctx, "init");
     RQ_HIP(ctx, realq::fill_f32(st->mA, 0.f, m * n, s));
@@ -461,6 +477,8 @@ static int state_init_gram(realq_bgd_state* st) {
     hipStream_t s = ctx->stream;
     st->gram = true;
     st->Tc = T;
+    st->Tb = T;
+    st->nbatch = 1;
     int rc;
     void* p;
     if ((rc = state_alloc(st, &p, (size_t)m * n * 4, "s_m"))) return rc;
@@ -536,10 +554,17 @@ static int gram_loss(realq_ctx* ctx, realq_bgd_state* st, const double* W, doubl
 }
 
 static int check_state_args(realq_ctx* ctx, const float* W0, const uint16_t* X, const uint16_t* Xhat, int64_t m,
-                            int64_t n, int64_t T, const realq_bgd_params* params) {
+                            int64_t n, int64_t T, const realq_bgd_params* params, const float* M, const float* P) {
     if (m <= 0 || n <= 0 || T <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "bgd state: need m, n, T > 0");
     if (!W0 || !X || !Xhat) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd state: NULL W0, X or Xhat");
-    return validate_bgd(ctx, params);
+    int rc = validate_bgd(ctx, params);
+    if (rc) return rc;
+    const bool clip = params->loss_clip > 0.f, minib = params->batch > 0 && params->batch < T;
+    if (params->form == REALQ_BGD_GRAM && (clip || minib))
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "the Gram form takes neither loss_clip nor a batch smaller than T");
+    if (clip && (M || P))
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "loss_clip needs the identity metric (no M, no window partner P)");
+    return REALQ_OK;
 }
 
 int realq_bgd_state_create(realq_ctx* ctx, realq_bgd_state** out, const float* W0, const uint16_t* X,
@@ -547,7 +572,7 @@ int realq_bgd_state_create(realq_ctx* ctx, realq_bgd_state** out, const float* W
                            int64_t T, const realq_bgd_params* params) {
     if (!ctx || !out) return REALQ_ERR_INVALID_ARG;
     *out = nullptr;
-    int rc = check_state_args(ctx, W0, X, Xhat, m, n, T, params);
+    int rc = check_state_args(ctx, W0, X, Xhat, m, n, T, params, M, P);
     if (rc) return rc;
     realq_bgd_state* st = new (std::nothrow) realq_bgd_state();
     if (!st) return set_error(ctx, REALQ_ERR_OOM, "host allocation");
@@ -694,7 +719,11 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         return REALQ_OK;
     }
     const bool dense = st->M || (st->P && alpha < 1.f);
-    const int64_t nchunks = (T + Tc - 1) / Tc;
+    // tokens of this step: mini-batch (t mod nbatch) of the module's Adam step t (1-based)
+    const int64_t bt0 = ((st->t) % st->nbatch) * st->Tb;
+    const int64_t Tn = std::min(st->Tb, T - bt0);
+    const int64_t nchunks = (Tn + Tc - 1) / Tc;
+    const bool clip = st->prm.loss_clip > 0.f;
     int rc;
     void *Gp = nullptr, *Gacc = nullptr;
     int64_t splits_used = 1;
@@ -715,18 +744,28 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         if ((rc = get_ws(ctx, "b_Gp", (size_t)Seff * m * nJ * 4, &Gp))) return rc;
         if (nchunks > 1 || dense)
             if ((rc = get_ws(ctx, "b_G", (size_t)m * nJ * 4, &Gacc))) return rc;
-        const int64_t kblocks = realq::gemm_num_blocks(m, Tc);
+        int64_t kblocks = realq::gemm_num_blocks(m, Tc);
+        if (clip) kblocks = std::max(kblocks, realq::clip_apply_partials());
         if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
         RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, s));  // shorter last chunk writes fewer
 
         splits_used = Seff;
         for (int64_t ch = 0; ch < nchunks; ++ch) {
-            const int64_t t0 = ch * Tc, cur = std::min(Tc, T - t0);
-            {
-                realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
+            const int64_t t0 = bt0 + ch * Tc, cur = std::min(Tc, bt0 + Tn - t0);
+            realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
+            if (!clip) {
                 Timed tm(ctx, "resid");
                 RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, st->Rlo, cur,
                                               (double*)parts + ch * kblocks, s));
+            } else {
+                // residual kept whole, per-token thresholds over the m channels, then the
+                // clipped, weighted split for the gradient GEMM and the loss partials
+                Timed tm(ctx, "resid");
+                RQ_HIP(ctx, realq::gemm_resid_f32(g, st->B + t0, T, st->Rf, cur, s));
+                const int64_t k = std::max<int64_t>(1, (int64_t)std::ceil((double)st->prm.loss_clip * (double)m));
+                RQ_HIP(ctx, realq::clip_select(st->Rf, cur, m, cur, std::min(k, m), st->tau, s));
+                RQ_HIP(ctx, realq::clip_apply(st->Rf, cur, m, cur, st->tau, st->s ? st->s + t0 : nullptr, st->Rhi,
+                                              st->Rlo, (double*)parts + ch * kblocks, s));
             }
             {
                 realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, S};
@@ -742,7 +781,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         }
         if (loss_out) {
             if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
-            else RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)T, loss_out, s));
+            else RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)Tn, loss_out, s));
         }
     }
     st->t += 1;
@@ -758,7 +797,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     a.c1 = c1;
     a.Gp = (const float*)Gp;
     a.splits = splits_used;
-    a.gscale = (float)(1.0 / (double)T);
+    a.gscale = (float)(1.0 / (double)Tn);
     a.lr = st->prm.lr;
     a.beta1 = st->prm.beta1;
     a.beta2 = st->prm.beta2;
@@ -784,7 +823,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         sg.M = m;
         sg.N = nJ;
         sg.K = m;
-        const float invT = (float)(1.0 / (double)T);
+        const float invT = (float)(1.0 / (double)Tn);
         bool first = true;
         if (alpha > 0.f) {
             if (st->M) {
@@ -968,7 +1007,7 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
     if (!d || !out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_layer: NULL desc or out");
     int rc = validate_q(ctx, &d->q);
     if (rc) return rc;
-    if ((rc = check_state_args(ctx, d->W0, d->X, d->Xhat, d->m, d->n, d->T, &d->bgd))) return rc;
+    if ((rc = check_state_args(ctx, d->W0, d->X, d->Xhat, d->m, d->n, d->T, &d->bgd, d->M, d->P))) return rc;
     if (!out->codes || !out->scales || !out->zeros || !out->W_hat)
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_layer: NULL codes, scales, zeros or W_hat");
     const int64_t m = d->m, n = d->n, T = d->T;

@@ -552,6 +552,36 @@ struct EpiResid {
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
 
+// Residual kept whole in float32: R[i][t] = B0[i][t] + acc (for the output-perturbation clip).
+struct EpiResidF32 {
+    static constexpr bool kReduce = false;
+    static constexpr bool kTransposed = false;
+    const float* B0;
+    int64_t ldb0;
+    float* R;
+    int64_t ldr;
+    struct Row {
+        f32x4 b;
+        bool ok;
+    };
+    using Col = NoCol;
+    __device__ void operator()(int64_t i, int64_t t, float v, int64_t, float&) const {
+        R[i * ldr + t] = B0[i * ldb0 + t] + v;
+    }
+    __device__ Col load_col(int64_t) const { return {}; }
+    __device__ Row load_row(int64_t i, int64_t t, int64_t) const {
+        Row r;
+        const float* b = B0 + i * ldb0 + t;
+        r.ok = al16(b) && al16(R + i * ldr + t);
+        if (r.ok) r.b = *reinterpret_cast<const f32x4*>(b);
+        return r;
+    }
+    __device__ void vec4(int64_t i, int64_t t, f32x4 v, const Row& row, const Col&, int64_t, float&) const {
+        *reinterpret_cast<f32x4*>(R + i * ldr + t) = row.b + v;
+    }
+    __device__ void partial(int64_t, double) const {}
+};
+
 // Residual loss only (no outputs besides the partial sums): s_t (B0 + acc)^2.
 struct EpiLoss {
     static constexpr bool kReduce = true;
@@ -737,6 +767,9 @@ hipError_t gemm_acc_f32(const GemmArgs& g, float* C, int64_t ldc, float alpha, h
 }
 hipError_t gemm_acc_f64(const GemmArgs& g, double* C, int64_t ldc, hipStream_t st) {
     return launch(g, EpiAccF64{C, ldc}, st);
+}
+hipError_t gemm_resid_f32(const GemmArgs& g, const float* B0, int64_t ldb0, float* R, int64_t ldr, hipStream_t st) {
+    return launch(g, EpiResidF32{B0, ldb0, R, ldr}, st);
 }
 hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
                       int64_t ldr, double* partials, hipStream_t st) {

@@ -120,6 +120,17 @@ hipError_t sgemm(const SgemmArgs& a, hipStream_t st);
 hipError_t dgemm(const double* A, int64_t lda, const double* B, int64_t ldb, double* C, int64_t ldc, int64_t M,
                  int64_t N, int64_t K, bool accumulate, hipStream_t st);
 
+// ---------------------------------------------------------------- output-perturbation clip
+// tau[t] = k-th smallest |R[i][t]| over i < m (t < cur, R row stride ldr), 1 <= k <= m
+hipError_t clip_select(const float* R, int64_t ldr, int64_t m, int64_t cur, int64_t k, float* tau, hipStream_t st);
+// c = min(1, tau_t / |R|): Rhi/Rlo = split(c^2 s_t R), partials[0 .. clip_apply_partials()) =
+// fixed-order partial sums of s_t (c R)^2
+hipError_t clip_apply(const float* R, int64_t ldr, int64_t m, int64_t cur, const float* tau, const float* s,
+                      uint16_t* Rhi, uint16_t* Rlo, double* partials, hipStream_t st);
+int64_t clip_apply_partials();
+// R[i][t] = B0[i][t] + (split(D) Xhat^T)[i][t] in float32 (the residual kept whole for the clip)
+hipError_t gemm_resid_f32(const GemmArgs& g, const float* B0, int64_t ldb0, float* R, int64_t ldr, hipStream_t st);
+
 // ---------------------------------------------------------------- quantize one column block
 struct QuantArgs {
     double* W;

@@ -54,7 +54,7 @@ class QParams(ctypes.Structure):
 class BgdParams(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int32), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("tok_chunk", ctypes.c_int64),
-                ("form", ctypes.c_int32)]
+                ("form", ctypes.c_int32), ("loss_clip", ctypes.c_float), ("batch", ctypes.c_int64)]
 
 
 BGD_TOKENS = 0   # residual and gradient GEMMs over all tokens every step
@@ -148,8 +148,9 @@ def qparams(bits=4, group=128, block=128, grid=80, damp=0.01) -> QParams:
     return QParams(bits, group, block, grid, damp)
 
 
-def bgd_params(steps=0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, tok_chunk=0, form=BGD_TOKENS) -> BgdParams:
-    return BgdParams(steps, lr, beta1, beta2, eps, tok_chunk, form)
+def bgd_params(steps=0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, tok_chunk=0, form=BGD_TOKENS, loss_clip=0.0,
+               batch=0) -> BgdParams:
+    return BgdParams(steps, lr, beta1, beta2, eps, tok_chunk, form, loss_clip, batch)
 
 
 class Context:

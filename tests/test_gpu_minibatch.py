@@ -1,0 +1,88 @@
+"""GPU parity of mini-batch BGD (Sec. 4.3: the surrogate on a calibration mini-batch per step) and
+of the output-perturbation clip (Appendix D.1, a_loss_clip) against the float64 oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _banner(msg):
+    print(f"\n[gpu-case] {msg}", flush=True)
+
+
+def _run(rq, ctx, L, steps, lr, batch=0, clip=0.0):
+    torch = _torch()
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    res = rq.quantize_layer(ctx, W0, X, Xh, s, qp=rq.qparams(),
+                            bgd=rq.bgd_params(steps=steps, lr=lr, batch=batch, loss_clip=clip))
+    torch.cuda.synchronize()
+    return res
+
+
+# With the clip, the per-token threshold couples every channel of a token, so a different Adam
+# step on one near-zero gradient moves other rows' clipped terms too: in the oracle itself,
+# reversing the first Adam step of the three smallest-gradient weights of the 256x512 clip case
+# leaves 99.86% of the codes and 88% of the group parameters unchanged (99.9% without the clip).
+# Clipped runs keep the code and loss bars and hold scale/zero agreement to that envelope.
+CLIP_GROUP_AGREEMENT = 0.85
+
+
+def _check(g, o, steps, clip=False):
+    met = P.compare(g, o)
+    print(met, "loss", g.loss_final, o.loss_final, flush=True)
+    assert met["code_identity"] >= P.CODE_IDENTITY
+    assert met["first_group_agreement"] >= P.CODE_IDENTITY
+    assert met["group_param_agreement"] >= (CLIP_GROUP_AGREEMENT if clip else P.GROUP_AGREEMENT_AFTER_BGD)
+    assert abs(g.loss_final - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+    # the first block's step losses come before any divergence is possible
+    tr = g.loss_trace.cpu().numpy().reshape(-1, steps)[0]
+    ref = np.array([v for (b, _, v) in o.loss_trace if b == 0])
+    np.testing.assert_allclose(tr, ref, rtol=1e-3)
+
+
+def test_minibatch_with_a_ragged_last_batch(rq, ctx):
+    L = synth.make_module("single_512", m=128, n=384, T=2000)
+    _banner("mini-batch 512 of 2000 tokens")
+    g = _run(rq, ctx, L, 3, 1e-3, batch=512)
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3, batch=512)
+    _check(g, o, 3)
+
+
+def test_loss_clip(rq, ctx):
+    L = synth.make_module("qwen3_0.6b_mlp", "gate", m=256, n=384, T=2048)
+    _banner("loss clip 0.95, m=256")
+    g = _run(rq, ctx, L, 3, L.lr, clip=0.95)
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=L.lr, loss_clip=0.95)
+    _check(g, o, 3, clip=True)
+
+
+def test_minibatch_and_loss_clip(rq, ctx):
+    L = synth.make_module("qwen3_0.6b_mlp", "gate", m=320, n=256, T=4096)
+    _banner("mini-batch 1024 + loss clip 0.95")
+    g = _run(rq, ctx, L, 4, L.lr, batch=1024, clip=0.95)
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=4, lr=L.lr, batch=1024, loss_clip=0.95)
+    _check(g, o, 4, clip=True)
+
+
+def test_rejected_combinations(rq, ctx):
+    torch = _torch()
+    L = synth.make_module("single_512", m=16, n=128, T=256)
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    eye = torch.eye(16, dtype=torch.float32, device="cuda")
+    bad = [dict(bgd=rq.bgd_params(steps=1, loss_clip=0.9), M=eye),               # clip with a dense metric
+           dict(bgd=rq.bgd_params(steps=1, batch=64, form=rq.BGD_GRAM)),         # Gram form with a batch
+           dict(bgd=rq.bgd_params(steps=1, loss_clip=1.5)),                      # quantile outside (0, 1]
+           dict(bgd=rq.bgd_params(steps=1, batch=-3))]
+    for kw in bad:
+        with pytest.raises(rq.RealqError) as ei:
+            rq.quantize_layer(ctx, W0, X, Xh, s, kw.get("M"), qp=rq.qparams(), bgd=kw["bgd"])
+        assert ei.value.code == -1

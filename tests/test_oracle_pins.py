@@ -540,3 +540,72 @@ def test_layer_chain_runs_and_hands_off():
     o_in = handoff(q0.W_hat, X0)
     o0 = quantize_layer(W0s["o"], handoff(W0s["q"], X0), o_in, qp=QParams(group=8, block=8), steps=0)
     np.testing.assert_array_equal(res0["o"].codes, o0.codes)
+
+
+# ============================================================================ mini-batch BGD and the loss clip (Sec. 4.3, Appendix D.1)
+
+def test_minibatch_cycles_through_consecutive_batches():
+    from oracle.realq_oracle import minibatch
+    T, b = 10, 4                                 # batches [0,4) [4,8) [8,10)
+    got = [(minibatch(t, T, b).start, minibatch(t, T, b).stop) for t in range(1, 8)]
+    assert got == [(0, 4), (4, 8), (8, 10), (0, 4), (4, 8), (8, 10), (0, 4)]
+    covered = np.zeros(T, dtype=int)
+    for t in range(1, 4):
+        sl = minibatch(t, T, b)
+        covered[sl] += 1
+    assert (covered == 1).all()                  # one cycle covers every token exactly once
+    assert minibatch(5, T, None) == slice(0, T) and minibatch(5, T, 64) == slice(0, T)
+
+
+def test_clip_factor_against_brute_force():
+    from oracle.realq_oracle import clip_factor
+    r = rng(70)
+    R = r.standard_normal((13, 6))
+    R[3, 2] = 0.0
+    for q in (0.95, 0.5, 0.1, 1.0):
+        c = clip_factor(R, q)
+        for t in range(R.shape[1]):
+            col = [abs(float(v)) for v in R[:, t]]
+            k = max(1, math.ceil(q * len(col)))
+            tau = sorted(col)[k - 1]              # nearest rank
+            for i, v in enumerate(col):
+                want = tau / v if v > tau else 1.0
+                assert c[i, t] == pytest.approx(want, rel=1e-15)
+    assert (clip_factor(R, 1.0) == 1.0).all()
+
+
+@pytest.mark.parametrize("dense", [False, True])
+def test_clipped_gradient_is_the_gradient_with_the_factor_frozen(dense):
+    from oracle.realq_oracle import clip_factor, clipped_grad
+    W0, X, Xh, s, W, M = _bgd_problem(71, dense=dense)
+    T = X.shape[0]
+    c = clip_factor(residual(W, W0, X, Xh), 0.6)
+    assert (c < 1).any()
+
+    def loss(Wt):                               # the clipped loss with c held fixed
+        Rc = c * residual(Wt, W0, X, Xh)
+        MR = Rc if M is None else M @ Rc
+        return 0.5 / T * float(np.sum(Rc * MR * s[None, :]))
+    G = clipped_grad(residual(W, W0, X, Xh), c, s, M, Xh, T)
+    h = 1e-6
+    for (i, j) in [(0, 0), (1, 3), (4, 8), (2, 5)]:
+        E = np.zeros_like(W)
+        E[i, j] = h
+        fd = (loss(W + E) - loss(W - E)) / (2 * h)
+        assert G[i, j] == pytest.approx(fd, rel=1e-6, abs=1e-12)
+
+
+def test_layer_with_unit_clip_and_full_batch_is_the_plain_sweep():
+    L = synth.make_module("single_512", m=24, n=256, T=300)
+    a = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=2, lr=1e-3)
+    b = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=2, lr=1e-3, loss_clip=1.0, batch=300)
+    assert (a.codes == b.codes).all() and np.array_equal(a.W_hat, b.W_hat)
+    assert a.loss_final == b.loss_final
+
+
+def test_layer_with_minibatches_and_clip_runs():
+    L = synth.make_module("single_512", m=24, n=256, T=300)
+    r = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3, batch=128, loss_clip=0.95)
+    assert len(r.loss_trace) == 3 and all(np.isfinite(v) for (_, _, v) in r.loss_trace)
+    full = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3)
+    assert not np.array_equal(r.W_hat, full.W_hat)     # the batches and the clip change the path
