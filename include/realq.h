@@ -45,15 +45,20 @@ typedef struct realq_ctx realq_ctx;             /* stream (borrowed), workspaces
 typedef struct realq_bgd_state realq_bgd_state; /* per-module BGD state, see realq_bgd_state_create */
 
 /* Quantizer and GPTQ parameters.
- *   bits  : code width, 2..8 (codes are 0 .. 2^bits-1)                     [4]
- *   group : columns sharing one (scale, zero) per row, >= 1               [128]
+ *   bits  : code width, 2..4 (codes are 0 .. 2^bits-1)                     [4]
+ *   group : columns sharing one (scale, zero) per row, >= 1; 0 = one group
+ *           per row (per-row quantization, the paper's W4A16 setting)      [128]
  *   block : GPTQ column block B (Sec. 3.2), 1..128; BGD runs after each    [128]
  *   grid  : number of shrink factors p_k = 1 - k/100, k = 0..grid-1, 1..100 [80]
  *   damp  : relative damping, lambda = damp * mean(diag H), > 0            [0.01]
- * Either block % group == 0 or group % block == 0 must hold. */
+ *   sym   : 0 = asymmetric (range [min(0, x), max(0, x)], zero searched);
+ *           1 = symmetric (Sec. 6.1: range [-max|x|, max|x|], zero fixed at
+ *           2^(bits-1), only the shrink factor searched)                  [0]
+ * With group > 0 either block % group == 0 or group % block == 0 must hold. */
 typedef struct realq_qparams {
     int32_t bits, group, block, grid;
     float damp;
+    int32_t sym;
 } realq_qparams;
 
 /* Block-GD parameters (Sec. 4.3, Eq. block_gd_update; Adam constants of Appendix D.1).
@@ -172,7 +177,7 @@ void realq_bgd_state_destroy(realq_bgd_state* st);
  * quantized and its error compensated on the block's remaining columns
  * (Eq. gptq_update), then all columns >= c0+bs get the batch update W -= E_b U_{b,:}
  * (Sec. 3.2).  Writes codes (uint8, 0..2^bits-1), scales ([m, ceil(n/group)] float32)
- * and zeros ([m, ceil(n/group)] uint8) for the groups touched.  Group parameters of a
+ * and zeros ([m, ceil(n/group)] uint8, one column when group = 0) for the groups touched.  Group parameters of a
  * group that started in an earlier block are read back from scales/zeros.
  * U and dead come from realq_chol_inverse.  When st != NULL the residual base of
  * the state is also advanced by the locked block (Sec. 4.3: quantized weights stay

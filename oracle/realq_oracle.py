@@ -30,7 +30,10 @@ with the per-layer surrogate of the readings below):
      the pulled-back metric of its consumer.
 
 Readings where the paper is silent (each is listed in the design notes):
-  * quantizer: asymmetric, per (row, group of ``group`` columns), joint search
+  * quantizer: asymmetric by default (the symmetric variant of the paper's main tables
+    takes the range [-max|x|, max|x|] and the fixed zero point (maxq + 1) / 2, searching the
+    shrink factor only; ``group = 0`` is one group per row), per (row, group of ``group``
+    columns), joint search
     over ``grid`` shrink factors p_k = 1 - k/100 and all 2^bits zero points,
     minimising squared error; errors within 2^-40 (relative) of the minimum, plus
     2^-60 of the group's sum of squares, count as equal (an exact tie can come out either
@@ -121,14 +124,22 @@ def inverse_factor(Hd: np.ndarray) -> np.ndarray:
 @dataclass
 class QParams:
     bits: int = 4
-    group: int = 128
+    group: int = 128        # 0 = one group per row (per-row quantization)
     block: int = 128
     grid: int = 80          # shrink factors p_k = 1 - k/100, k = 0 .. grid-1
     damp: float = 0.01
+    sym: bool = False       # symmetric: range [-max|x|, max|x|], zero fixed at (maxq + 1) / 2
 
     @property
     def maxq(self) -> int:
         return (1 << self.bits) - 1
+
+    @property
+    def zsym(self) -> int:
+        return (self.maxq + 1) // 2
+
+    def group_of(self, n: int) -> int:
+        return self.group if self.group > 0 else n
 
 
 TIE_RTOL = 2.0 ** -40   # search errors within TIE_RTOL * least + TIE_ATOL * sum x^2 are one tie
@@ -167,6 +178,9 @@ def search_table(x: np.ndarray, qp: QParams):
     maxq = qp.maxq
     lo = np.minimum(0.0, x.min(axis=1))
     hi = np.maximum(0.0, x.max(axis=1))
+    if qp.sym:
+        amax = np.maximum(-lo, hi)
+        lo, hi = -amax, amax
     flat = lo == hi
     lo = np.where(flat, -1.0, lo)
     hi = np.where(flat, 1.0, hi)
@@ -190,6 +204,8 @@ def _group_search_rows(x, qp):
     dist = np.abs(zz - znat[:, None, None])
     # near-least error first, then the lexicographic minimum of (k, dist, z), one key at a time
     ss = np.sum(x * x, axis=1)[:, None, None]
+    if qp.sym:
+        err = np.where(zz == qp.zsym, err, np.inf)    # the symmetric zero point only
     cand = err <= err.min(axis=(1, 2), keepdims=True) * (1.0 + TIE_RTOL) + TIE_ATOL * ss
     for key in (kk, dist, zz):
         big = np.where(cand, key, np.inf)
@@ -338,7 +354,8 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     m, n = W0.shape
     T = X.shape[0]
     maxq = qp.maxq
-    ng = -(-n // qp.group)
+    grp = qp.group_of(n)
+    ng = -(-n // grp)
 
     H = hessian(Xhat, s)
     Hd, dead = damp_hessian(H, qp.damp)
@@ -364,9 +381,9 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
         c1 = min(c0 + qp.block, n)
         E = np.zeros((m, c1 - c0))
         for j in range(c0, c1):
-            if j % qp.group == 0:
-                g = j // qp.group
-                g1 = min(j + qp.group, n)
+            if j % grp == 0:
+                g = j // grp
+                g1 = min(j + grp, n)
                 s64, zi, _ = group_search(W[:, j:g1], qp)
                 cur_s = s64.astype(np.float32).astype(np.float64)   # scales are carried as float32
                 cur_z = zi.astype(np.float64)

@@ -609,11 +609,12 @@ void realq_bgd_state_destroy(realq_bgd_state* st) {
 static int validate_q(realq_ctx* ctx, const realq_qparams* qp) {
     if (!qp) return set_error(ctx, REALQ_ERR_INVALID_ARG, "NULL qparams");
     if (qp->bits < 2 || qp->bits > 4) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bits must be 2, 3 or 4");
-    if (qp->group < 1) return set_error(ctx, REALQ_ERR_INVALID_ARG, "group must be >= 1");
+    if (qp->group < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "group must be >= 1, or 0 for one group per row");
     if (qp->block < 1 || qp->block > 128) return set_error(ctx, REALQ_ERR_INVALID_ARG, "block must be in 1..128");
     if (qp->grid < 1 || qp->grid > 100) return set_error(ctx, REALQ_ERR_INVALID_ARG, "grid must be in 1..100");
-    if (qp->block % qp->group != 0 && qp->group % qp->block != 0)
+    if (qp->group > 0 && qp->block % qp->group != 0 && qp->group % qp->block != 0)
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "block and group must divide one another");
+    if (qp->sym != 0 && qp->sym != 1) return set_error(ctx, REALQ_ERR_INVALID_ARG, "sym must be 0 or 1");
     if (!(qp->damp > 0.f) || !std::isfinite(qp->damp))
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "damp must be finite and > 0");
     return REALQ_OK;
@@ -646,12 +647,13 @@ int realq_quantize_block(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_
     q.U = U;
     q.dead = dead;
     q.bits = qp->bits;
-    q.group = qp->group;
+    q.group = qp->group > 0 ? qp->group : n;  // 0: one group per row
     q.grid = qp->grid;
+    q.sym = qp->sym;
     q.codes = codes;
     q.scales = scales;
     q.zeros = zeros;
-    q.ngroups = (n + qp->group - 1) / qp->group;
+    q.ngroups = (n + q.group - 1) / q.group;
     q.E = (double*)E;
     q.W0 = st ? st->W0 : nullptr;
     q.Dhi = st ? st->Dhi : nullptr;

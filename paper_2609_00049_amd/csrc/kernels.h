@@ -138,6 +138,7 @@ struct QuantArgs {
     const float* U;
     const uint8_t* dead;
     int bits, group, grid;
+    int sym;  // symmetric range, zero fixed at (maxq + 1) / 2
     uint8_t* codes;
     float* scales;
     uint8_t* zeros;

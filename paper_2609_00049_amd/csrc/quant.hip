@@ -3,13 +3,15 @@
 // One wave64 owns one weight row at a time; lane l holds block columns l and l+64
 // in registers.  Per row:
 //   1. dead columns of the block are zeroed;
-//   2. when a quantization group starts, its (scale, zero) pair is searched in
+//   2. when a quantization group starts (a group may span the whole row), its
+//      (scale, zero) pair is searched in
 //      float64: lanes split the shrink factors p_k = 1 - k/100 (lane l takes k = l and
 //      k = l + 64), every lane scores all zero points of its k over the group's
 //      values (broadcast with readlane); one wave reduction finds the least error,
 //      errors up to least * (1 + 2^-40) + 2^-60 * sum x^2 form one tie, and a second
 //      reduction picks the least (k, |z - z_nat|, z) among them, with
-//      z_nat = rint(-lo maxq / (hi - lo));
+//      z_nat = rint(-lo maxq / (hi - lo)); the symmetric quantizer takes the range
+//      [-max|x|, max|x|] and only the zero point (maxq + 1) / 2;
 //   3. columns are quantized in order with the scale as stored (float32):
 //      q = clamp(rint(w/s) + z, 0, maxq) decided in float64, w_hat = s (q - z) (exact in
 //      float64, so the float32 output is the float32 dequantization of the stored
@@ -87,10 +89,16 @@ __device__ __forceinline__ void search_accumulate(Search& S, double x) {
 }
 
 template <int MAXQ>
-__device__ __forceinline__ void search_begin(Search& S, double lo, double hi, double ss, int grid, int lane) {
+__device__ __forceinline__ void search_begin(Search& S, double lo, double hi, double ss, int grid, int lane,
+                                             bool sym) {
 #pragma clang fp contract(off)
     lo = fmin(0.0, lo);
     hi = fmax(0.0, hi);
+    if (sym) {
+        const double amax = fmax(-lo, hi);
+        lo = -amax;
+        hi = amax;
+    }
     if (lo == hi) {
         lo = -1.0;
         hi = 1.0;
@@ -112,14 +120,16 @@ __device__ __forceinline__ void search_begin(Search& S, double lo, double hi, do
 
 // Reduce the per-lane candidates to the winner; returns (scale, zero) in all lanes.
 template <int MAXQ>
-__device__ __forceinline__ void search_finish(const Search& S, double& scale, int& zero) {
+__device__ __forceinline__ void search_finish(const Search& S, double& scale, int& zero, bool sym) {
 #pragma clang fp contract(off)
+    constexpr int ZSYM = (MAXQ + 1) / 2;
     double emin = INFINITY;
 #pragma unroll
     for (int a = 0; a < 2; ++a) {
         if (!S.valid[a]) continue;
 #pragma unroll
-        for (int z = 0; z <= MAXQ; ++z) emin = fmin(emin, S.err[a][z]);
+        for (int z = 0; z <= MAXQ; ++z)
+            if (!sym || z == ZSYM) emin = fmin(emin, S.err[a][z]);
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) emin = fmin(emin, __shfl_xor(emin, off));
@@ -132,6 +142,7 @@ __device__ __forceinline__ void search_finish(const Search& S, double& scale, in
         if (!S.valid[a]) continue;
 #pragma unroll
         for (int z = 0; z <= MAXQ; ++z) {
+            if (sym && z != ZSYM) continue;
             const Best c{S.kk[a], abs(z - znat), z};
             if (S.err[a][z] <= thr && better(c, best)) best = c;
         }
@@ -198,7 +209,7 @@ __global__ __launch_bounds__(256) void quantize_block_kernel(QuantArgs q) {
                         hi = fmax(hi, x);
                         ss = fma(x, x, ss);
                     }
-                    search_begin<MAXQ>(S, lo, hi, ss, q.grid, lane);
+                    search_begin<MAXQ>(S, lo, hi, ss, q.grid, lane, q.sym != 0);
                     for (int64_t e = 0; e < glen; ++e) {
                         const int64_t jj = j + e;
                         search_accumulate<MAXQ>(S, bcast(jj < 64 ? w0 : w1, (int)(jj & 63)));
@@ -220,7 +231,7 @@ __global__ __launch_bounds__(256) void quantize_block_kernel(QuantArgs q) {
                             ss = fma(x, x, ss);
                         }
                     }
-                    search_begin<MAXQ>(S, lo, hi, ss, q.grid, lane);
+                    search_begin<MAXQ>(S, lo, hi, ss, q.grid, lane, q.sym != 0);
                     for (int64_t e0c = 0; e0c < glen; e0c += 64) {
                         const int64_t cc = col + e0c + lane;
                         double v = 0.0;
@@ -233,7 +244,7 @@ __global__ __launch_bounds__(256) void quantize_block_kernel(QuantArgs q) {
                     }
                 }
                 int zi;
-                search_finish<MAXQ>(S, scale, zi);
+                search_finish<MAXQ>(S, scale, zi, q.sym != 0);
                 scale = (double)(float)scale;  // the stored float32 scale is the one used
                 zf = (double)zi;
                 if (lane == 0) {

@@ -48,7 +48,7 @@ class RealqError(RuntimeError):
 
 class QParams(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("group", ctypes.c_int32), ("block", ctypes.c_int32),
-                ("grid", ctypes.c_int32), ("damp", ctypes.c_float)]
+                ("grid", ctypes.c_int32), ("damp", ctypes.c_float), ("sym", ctypes.c_int32)]
 
 
 class BgdParams(ctypes.Structure):
@@ -144,8 +144,9 @@ def _bits(t: torch.Tensor) -> torch.Tensor:
     return t
 
 
-def qparams(bits=4, group=128, block=128, grid=80, damp=0.01) -> QParams:
-    return QParams(bits, group, block, grid, damp)
+def qparams(bits=4, group=128, block=128, grid=80, damp=0.01, sym=False) -> QParams:
+    """group = 0: one group per row; sym: symmetric range with the zero fixed at 2^(bits-1)."""
+    return QParams(bits, group, block, grid, damp, int(bool(sym)))
 
 
 def bgd_params(steps=0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, tok_chunk=0, form=BGD_TOKENS, loss_clip=0.0,
@@ -283,7 +284,7 @@ def quantize_layer(ctx: Context, W0, X, Xhat, s=None, M=None, P=None, *, qp: Opt
     T = X.shape[0]
     dev = W0.device
     if out is None:
-        ng = -(-n // qp.group)
+        ng = -(-n // (qp.group or n))
         nb = -(-n // qp.block)
         out = LayerResult(
             codes=torch.empty((m, n), dtype=torch.uint8, device=dev),

@@ -162,6 +162,46 @@ def test_search_ties_decided_like_the_oracle(rq, ctx, bits):
     _assert_parity(met, bgd=False)
 
 
+# ============================================================================ the paper's quantizer settings (Sec. 6.1)
+
+def test_symmetric_per_row_w4(rq, ctx):
+    """Symmetric per-row W4 (the main W4A16 tables): one (scale, zero = 8) per row, searched on the
+    whole row at the first block and reused by every later block."""
+    L = synth.make_module("single_512")
+    _banner("symmetric per-row w4")
+    qp = QParams(group=0, sym=True)
+    g = _run(rq, ctx, L, L.steps, L.lr, qp=rq.qparams(group=0, sym=True))
+    o = _oracle(L, L.steps, L.lr, qp=qp)
+    assert g.scales.shape[1] == 1 and (g.zeros.cpu() == 8).all()
+    _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
+
+
+@pytest.mark.parametrize("bits", [3, 2])
+def test_symmetric_low_bit_g128(rq, ctx, bits):
+    """W3 / W2 with group 128 (the low-bit tables), symmetric."""
+    L = synth.make_module("single_512", m=128, n=384, T=1024)
+    _banner(f"symmetric w{bits} g128")
+    qp = QParams(bits=bits, sym=True)
+    g = _run(rq, ctx, L, 2, 1e-3, qp=rq.qparams(bits=bits, sym=True))
+    o = _oracle(L, 2, 1e-3, qp=qp)
+    assert (g.zeros.cpu() == (1 << (bits - 1))).all()
+    _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
+
+
+def test_symmetric_per_row_llama_gate_shape_sampled_rows(rq, ctx):
+    """Per-row symmetric W4 at the full 14336x4096 gate shape (the whole 4096-column row searched
+    once), 8192 tokens, oracle on sampled rows."""
+    L = synth.make_module("llama3.1_8b_layer", "gate", T=8192)
+    _banner("symmetric per-row llama3.1-8b gate 14336x4096 T=8192")
+    qp = QParams(group=0, sym=True)
+    g = _run(rq, ctx, L, L.steps, L.lr, qp=rq.qparams(group=0, sym=True))
+    rows = np.random.default_rng(9).choice(L.W0.shape[0], 6, replace=False)
+    o = _oracle(L, L.steps, L.lr, rows=rows, qp=qp)
+    _assert_parity(P.compare(g, o, rows=rows))
+    lg = P.row_loss(g.W_hat.cpu().numpy()[rows], L.W0[rows], L.X, L.Xhat)
+    assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+
+
 def test_layer_ragged_shapes(rq, ctx):
     L = synth.make_module("single_512", m=70, n=300, T=1000)
     _banner("layer ragged m=70 n=300 T=1000")

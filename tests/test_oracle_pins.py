@@ -256,9 +256,10 @@ def textbook_obs(W0, X, qp):
     m, n = W.shape
     codes = np.zeros((m, n), dtype=int)
     maxq = qp.maxq
+    grp = qp.group if qp.group > 0 else n
     for j in range(n):
-        if j % qp.group == 0:
-            sc, zz, _ = group_search(W[:, j:j + qp.group], qp)
+        if j % grp == 0:
+            sc, zz, _ = group_search(W[:, j:j + grp], qp)
             sc = sc.astype(np.float32).astype(float)          # the stored (float32) scale
         q = np.clip(np.rint(W[:, j] / sc) + zz, 0, maxq)
         wq = sc * (q - zz)
@@ -286,6 +287,20 @@ def test_gptq_matches_textbook_obs(block):
     res = quantize_layer(W0, X, X, qp=qp, steps=0)
     np.testing.assert_array_equal(res.codes, ref_codes)
     np.testing.assert_allclose(res.W_hat, ref_W, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("bits", [4, 3])
+def test_gptq_matches_textbook_obs_symmetric_per_row(bits):
+    """The paper's main quantizer (symmetric, one group per row) through the same reduction."""
+    W0, X = _tiny(43)
+    qp = QParams(bits=bits, group=0, block=8, sym=True)
+    ref_codes, ref_W = textbook_obs(W0, X, qp)
+    res = quantize_layer(W0, X, X, qp=qp, steps=0)
+    np.testing.assert_array_equal(res.codes, ref_codes)
+    np.testing.assert_allclose(res.W_hat, ref_W, rtol=0, atol=1e-12)
+    assert res.scales.shape == (W0.shape[0], 1) and (res.zeros == qp.zsym).all()
+    deq = res.scales[:, :1] * (res.codes.astype(float) - qp.zsym)
+    np.testing.assert_array_equal(res.W_hat, deq)
 
 
 def test_gptq_error_theorem():
@@ -609,3 +624,49 @@ def test_layer_with_minibatches_and_clip_runs():
     assert len(r.loss_trace) == 3 and all(np.isfinite(v) for (_, _, v) in r.loss_trace)
     full = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3)
     assert not np.array_equal(r.W_hat, full.W_hat)     # the batches and the clip change the path
+
+
+# ============================================================================ symmetric quantizer (Sec. 6.1 setup)
+
+def brute_force_search_sym(x, bits=4, grid=80):
+    """Symmetric candidates in exact rational arithmetic: range [-max|x|, max|x|], zero fixed at
+    2^(bits-1); the winner is the least (err, k).  Returns (scale, exact error)."""
+    maxq = 2 ** bits - 1
+    z = (maxq + 1) // 2
+    xs = [Fraction(float(v)) for v in x]
+    amax = max(abs(v) for v in xs)
+    lo, hi = (-amax, amax) if amax > 0 else (Fraction(-1), Fraction(1))
+    best = None
+    for k in range(grid):
+        sf = ((1.0 - k / 100.0) * float(hi - lo)) / maxq
+        S = Fraction(sf)
+        err = Fraction(0)
+        for xv in xs:
+            c = min(max(_rint_exact(xv / S) + z, 0), maxq) - z
+            d = xv - S * c
+            err += d * d
+        if best is None or (err, k) < best[0]:
+            best = ((err, k), sf)
+    return best[1], best[0][0]
+
+
+@pytest.mark.parametrize("bits,seed", [(4, 60), (4, 61), (3, 62), (2, 63)])
+def test_symmetric_search_matches_exhaustive(bits, seed):
+    r = rng(seed)
+    x = r.standard_normal(20) * 0.02
+    if seed == 61:
+        x[3] = 0.15                      # one outlier
+    qp = QParams(bits=bits, sym=True)
+    s, z, e = group_search(x[None, :], qp)
+    bs, be = brute_force_search_sym(list(x), bits)
+    assert z[0] == qp.zsym
+    ss = sum(Fraction(float(v)) ** 2 for v in x)
+    if s[0] != bs:   # only a tie within the tolerance may pick another shrink factor
+        assert Fraction(float(e[0])) <= be * (1 + Fraction(TIE_RTOL)) + Fraction(TIE_ATOL) * ss + Fraction(2.0 ** -90) * ss
+    assert abs(Fraction(float(e[0])) - be) <= Fraction(1e-12) * be + Fraction(2.0 ** -90) * ss
+
+
+def test_symmetric_all_zero_group():
+    qp = QParams(sym=True)
+    s, z, e = group_search(np.zeros((1, 16)), qp)
+    assert e[0] == 0.0 and z[0] == 8 and s[0] == pytest.approx(2.0 / 15.0, rel=1e-15)
