@@ -85,6 +85,33 @@ def hessian(Xhat: np.ndarray, s: Optional[np.ndarray] = None) -> np.ndarray:
     return (2.0 / T) * (A.T @ Xh)
 
 
+def row_groups(m: int, n_groups: int) -> List[slice]:
+    """The N_g row groups of Eq. saliency_hessian: contiguous ranges of ceil(m / N_g) output
+    channels (the last one shorter)."""
+    size = -(-m // n_groups)
+    return [slice(g * size, min(m, (g + 1) * size)) for g in range(n_groups) if g * size < m]
+
+
+def fisher(G: np.ndarray) -> np.ndarray:
+    """Aggregated Fisher F = (1/T) sum_t g_t g_t^T of the per-token output gradients (Eq. fisher_full)."""
+    G = np.asarray(G, dtype=np.float64)
+    return G.T @ G / G.shape[0]
+
+
+def saliency(G: np.ndarray, n_groups: int, clip_q: Optional[float] = None) -> np.ndarray:
+    """Per-token saliency of each row group, s[g, t] = ||g_t restricted to group g||^2 (Sec. 3.3),
+    optionally clipped per group at the nearest-rank clip_q quantile over tokens (Appendix D.1,
+    Hessian-side saliency clipping).  Returns [n_groups, T]."""
+    G = np.asarray(G, dtype=np.float64)
+    T, m = G.shape
+    s = np.stack([np.sum(G[:, sl] ** 2, axis=1) for sl in row_groups(m, n_groups)])
+    if clip_q is not None:
+        k = max(1, int(math.ceil(clip_q * T)))
+        tau = np.sort(s, axis=1)[:, k - 1][:, None]
+        s = np.minimum(s, tau)
+    return s
+
+
 # ============================================================================ step 2: damping + inverse factor
 
 def damp_hessian(H: np.ndarray, damp: float) -> Tuple[np.ndarray, np.ndarray]:
@@ -333,7 +360,7 @@ class LayerResult:
 def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams] = None,
                    steps: int = 0, lr: float = 1e-3, window: Optional[Tuple[int, int]] = None,
                    keep_E: bool = False, batch: Optional[int] = None,
-                   loss_clip: Optional[float] = None) -> LayerResult:
+                   loss_clip: Optional[float] = None, s_groups: Optional[np.ndarray] = None) -> LayerResult:
     """The per-module REAL-Q sweep (Alg. 1, one linear module), in float64.
 
     W0 [m, n]; X, Xhat [T, n]; s [T] or None; M [m, m] or None (identity);
@@ -343,6 +370,11 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     ``batch``: tokens per Adam step (see ``minibatch``; None = all T).  ``loss_clip``: the
     output-perturbation clip quantile q of ``clip_factor`` applied to the residual of every
     BGD step (None = off).  The final loss is always over all tokens, unclipped.
+    ``s_groups`` [N_g, T]: saliency per row group (Eq. saliency_hessian); row group g (see
+    ``row_groups``) is then quantized with its own Hessian H_g = (2/T) sum_t s[g, t] x_t x_t^T
+    (and its own damping, dead columns and inverse factor) instead of the one built from ``s``;
+    ``s`` keeps weighting the tokens of the BGD surrogate.  H, U and dead of the result are
+    then lists over the groups.
     """
     qp = qp or QParams()
     W0 = np.asarray(W0, dtype=np.float64)
@@ -357,12 +389,22 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     grp = qp.group_of(n)
     ng = -(-n // grp)
 
-    H = hessian(Xhat, s)
-    Hd, dead = damp_hessian(H, qp.damp)
-    U = inverse_factor(Hd)
+    if s_groups is None:
+        groups = [slice(0, m)]
+        Hs = [hessian(Xhat, s)]
+    else:
+        sg = np.asarray(s_groups, dtype=np.float64)
+        groups = row_groups(m, sg.shape[0])
+        Hs = [hessian(Xhat, sg[g]) for g in range(len(groups))]
+    deads, Us = [], []
+    for Hg in Hs:
+        Hd, dead_g = damp_hessian(Hg, qp.damp)
+        deads.append(dead_g)
+        Us.append(inverse_factor(Hd))
 
     W = W0.copy()
-    W[:, dead] = 0.0
+    for sl, dead_g in zip(groups, deads):
+        W[sl, dead_g] = 0.0
     mA = np.zeros_like(W)
     vA = np.zeros_like(W)
     t = 0
@@ -380,24 +422,25 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
         c0 = b * qp.block
         c1 = min(c0 + qp.block, n)
         E = np.zeros((m, c1 - c0))
-        for j in range(c0, c1):
-            if j % grp == 0:
-                g = j // grp
-                g1 = min(j + grp, n)
-                s64, zi, _ = group_search(W[:, j:g1], qp)
-                cur_s = s64.astype(np.float32).astype(np.float64)   # scales are carried as float32
-                cur_z = zi.astype(np.float64)
-                scales[:, g] = cur_s
-                zeros[:, g] = zi
-            w = W[:, j].copy()
-            pre[:, j] = w / cur_s + cur_z
-            q, wq = quantize_column(w, cur_s, cur_z, maxq)
-            codes[:, j] = q.astype(np.uint8)
-            e = (w - wq) / U[j, j]
-            W[:, j] = wq
-            W[:, j + 1:c1] -= np.outer(e, U[j, j + 1:c1])
-            E[:, j - c0] = e
-        W[:, c1:] -= E @ U[c0:c1, c1:]
+        for rs, U in zip(groups, Us):           # each row group with its own inverse factor
+            for j in range(c0, c1):
+                if j % grp == 0:
+                    g = j // grp
+                    g1 = min(j + grp, n)
+                    s64, zi, _ = group_search(W[rs, j:g1], qp)
+                    cur_s[rs] = s64.astype(np.float32).astype(np.float64)   # scales are carried as float32
+                    cur_z[rs] = zi.astype(np.float64)
+                    scales[rs, g] = cur_s[rs]
+                    zeros[rs, g] = zi
+                w = W[rs, j].copy()
+                pre[rs, j] = w / cur_s[rs] + cur_z[rs]
+                q, wq = quantize_column(w, cur_s[rs], cur_z[rs], maxq)
+                codes[rs, j] = q.astype(np.uint8)
+                e = (w - wq) / U[j, j]
+                W[rs, j] = wq
+                W[rs, j + 1:c1] -= np.outer(e, U[j, j + 1:c1])
+                E[rs, j - c0] = e
+            W[rs, c1:] -= E[rs] @ U[c0:c1, c1:]
         if keep_E:
             Es.append(E)
 
@@ -422,7 +465,9 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
 
     R = residual(W, W0, X, Xhat)
     loss = surrogate_loss(R, s, M, T)
-    return LayerResult(codes=codes, scales=scales, zeros=zeros, W_hat=W, H=H, U=U, dead=dead,
+    one = s_groups is None
+    return LayerResult(codes=codes, scales=scales, zeros=zeros, W_hat=W, H=Hs[0] if one else Hs,
+                       U=Us[0] if one else Us, dead=deads[0] if one else deads,
                        loss_final=loss, loss_trace=trace, prerounding=pre, E_blocks=Es)
 
 

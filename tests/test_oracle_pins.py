@@ -670,3 +670,58 @@ def test_symmetric_all_zero_group():
     qp = QParams(sym=True)
     s, z, e = group_search(np.zeros((1, 16)), qp)
     assert e[0] == 0.0 and z[0] == 8 and s[0] == pytest.approx(2.0 / 15.0, rel=1e-15)
+
+
+# ============================================================================ Stage-0 accumulators (Sec. 3.3, Eq. fisher_full, Appendix D.1)
+
+def test_fisher_is_the_mean_outer_product_of_gradients():
+    from oracle.realq_oracle import fisher
+    r = rng(90)
+    G = r.standard_normal((9, 5))
+    F = np.zeros((5, 5))
+    for t in range(9):
+        for i in range(5):
+            for j in range(5):
+                F[i, j] += G[t, i] * G[t, j] / 9
+    np.testing.assert_allclose(fisher(G), F, rtol=1e-13, atol=1e-15)
+    assert np.linalg.eigvalsh(fisher(G)).min() > -1e-12
+
+
+def test_row_groups_and_saliency_against_loops():
+    from oracle.realq_oracle import row_groups, saliency
+    assert row_groups(10, 4) == [slice(0, 3), slice(3, 6), slice(6, 9), slice(9, 10)]
+    assert row_groups(8, 4) == [slice(0, 2), slice(2, 4), slice(4, 6), slice(6, 8)]
+    r = rng(91)
+    G = r.standard_normal((50, 10))
+    G[7] *= 40                                   # one outlier token
+    S = saliency(G, 4)
+    for g, sl in enumerate(row_groups(10, 4)):
+        for t in range(50):
+            assert S[g, t] == pytest.approx(sum(G[t, i] ** 2 for i in range(sl.start, sl.stop)), rel=1e-13)
+    Sc = saliency(G, 4, clip_q=0.9)
+    for g in range(4):
+        tau = sorted(S[g])[math.ceil(0.9 * 50) - 1]       # nearest rank over tokens
+        np.testing.assert_array_equal(Sc[g], np.minimum(S[g], tau))
+    assert Sc[:, 7].max() < S[:, 7].max()
+
+
+def test_one_saliency_group_is_the_weighted_hessian_path():
+    L = synth.make_module("single_512", m=12, n=256, T=200)
+    a = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=2, lr=1e-3)
+    b = quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=2, lr=1e-3, s_groups=L.s[None, :])
+    assert (a.codes == b.codes).all() and np.array_equal(a.W_hat, b.W_hat)
+
+
+@pytest.mark.parametrize("steps", [0, 2])
+def test_row_groups_quantize_like_separate_modules(steps):
+    """With M = I rows are independent, so group g's rows match a sweep of those rows alone whose
+    Hessian uses s[g] (the BGD surrogate weights stay None in both)."""
+    from oracle.realq_oracle import row_groups
+    L = synth.make_module("single_512", m=10, n=256, T=200)
+    r = rng(92)
+    S = np.abs(r.standard_normal((3, 200))) ** 2
+    full = quantize_layer(L.W0, L.X, L.Xhat, None, steps=steps, lr=1e-3, s_groups=S)
+    for g, sl in enumerate(row_groups(10, 3)):
+        part = quantize_layer(L.W0[sl], L.X, L.Xhat, None, steps=steps, lr=1e-3, s_groups=S[g][None, :])
+        np.testing.assert_array_equal(full.codes[sl], part.codes)
+        np.testing.assert_allclose(full.W_hat[sl], part.W_hat, rtol=0, atol=1e-15)
