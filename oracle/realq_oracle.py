@@ -44,8 +44,10 @@ Readings where the paper is silent (each is listed in the design notes):
     group's first column is reached; the chosen scale is carried as float32 (the format
     of the output), and codes and dequantized values use that stored scale, so Ŵ is
     exactly what (codes, scales, zeros) describe;
-  * damping: dead columns (H_jj == 0) get H_jj = 1 and their weights zeroed, then
-    lambda = damp * mean(diag H) is added to the diagonal;
+  * damping: dead columns (H_jj == 0) get H_jj = 1, then lambda = damp * mean(diag H)
+    is added to the diagonal; a dead column's weights count as zero from the moment the
+    sweep reaches them (the search of the group holding it, and its block), so they are
+    quantized to exactly zero whatever Block-GD did to them before;
   * BGD uses all T tokens per step unless a mini-batch size is given (then consecutive
     token batches in cyclic order, one per Adam step), ``steps`` Adam steps after every
     block except the last, one Adam step counter per module;
@@ -403,8 +405,6 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
         Us.append(inverse_factor(Hd))
 
     W = W0.copy()
-    for sl, dead_g in zip(groups, deads):
-        W[sl, dead_g] = 0.0
     mA = np.zeros_like(W)
     vA = np.zeros_like(W)
     t = 0
@@ -422,12 +422,13 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
         c0 = b * qp.block
         c1 = min(c0 + qp.block, n)
         E = np.zeros((m, c1 - c0))
-        for rs, U in zip(groups, Us):           # each row group with its own inverse factor
+        for rs, U, dead_g in zip(groups, Us, deads):   # each row group with its own inverse factor
+            W[rs, c0:c1] = np.where(dead_g[c0:c1], 0.0, W[rs, c0:c1])
             for j in range(c0, c1):
                 if j % grp == 0:
                     g = j // grp
                     g1 = min(j + grp, n)
-                    s64, zi, _ = group_search(W[rs, j:g1], qp)
+                    s64, zi, _ = group_search(np.where(dead_g[j:g1], 0.0, W[rs, j:g1]), qp)
                     cur_s[rs] = s64.astype(np.float32).astype(np.float64)   # scales are carried as float32
                     cur_z[rs] = zi.astype(np.float64)
                     scales[rs, g] = cur_s[rs]

@@ -725,3 +725,20 @@ def test_row_groups_quantize_like_separate_modules(steps):
         part = quantize_layer(L.W0[sl], L.X, L.Xhat, None, steps=steps, lr=1e-3, s_groups=S[g][None, :])
         np.testing.assert_array_equal(full.codes[sl], part.codes)
         np.testing.assert_allclose(full.W_hat[sl], part.W_hat, rtol=0, atol=1e-15)
+
+
+def test_dead_column_of_one_row_group_quantizes_to_zero_after_bgd():
+    """Column 200 lives only on tokens whose saliency is zero for row group 0: it is dead for that
+    group (H_jj = 0) but not for group 1, and Block-GD (s = None) moves it before block 1.  The
+    sweep still takes group 0's weights there as zero, so they dequantize to exactly 0."""
+    L = synth.make_module("single_512", m=8, n=256, T=200)
+    X = L.X.copy()
+    X[:, 200] = 0.0
+    X[:20, 200] = 1.5
+    S = np.ones((2, 200))
+    S[0, :20] = 0.0
+    res = quantize_layer(L.W0, X, X, None, steps=2, lr=1e-2, s_groups=S)
+    assert res.dead[0][200] and not res.dead[1][200]
+    assert (res.W_hat[:4, 200] == 0.0).all()
+    assert (res.codes[:4, 200] == res.zeros[:4, 1]).all()
+    assert (res.W_hat[4:, 200] != 0.0).all()
