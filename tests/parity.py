@@ -11,7 +11,11 @@ CODE_IDENTITY = 0.999      # fraction of identical int4 codes
 SCALE_RTOL = 1e-4          # scales and zeros
 LOSS_RTOL = 1e-3           # final surrogate loss
 HESS_RTOL = 1e-3           # relative Frobenius error of H
-GROUP_AGREEMENT_AFTER_BGD = 0.99  # groups searched after Block-GD steps (see the test module)
+# Groups searched after Block-GD steps: Adam's first step is close to lr * sign(g), so near-zero
+# gradients step opposite ways under different rounding.  The oracle against itself, with its
+# gradient perturbed by a bf16 hi/lo split's remainder (2^-17 of each token product), keeps
+# 99.1-99.4% of the 512x512 layer's groups; the bar is twice that mean envelope.
+GROUP_AGREEMENT_AFTER_BGD = 0.985
 
 
 def to_device(L, torch):
