@@ -116,18 +116,46 @@ const char* realq_last_error(const realq_ctx* ctx);
  * realq_ctx_kernel_time after the stream has drained.  Names: "hessian",
  * "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init", "gram" (Gram
  * matrices of the input perturbation), "gram_step" (the per-step product of the
- * Gram form), "dense_loss" (final loss with a dense metric).
+ * Gram form), "dense_loss" (final loss with a dense metric), "saliency".
  * Returns REALQ_ERR_INVALID_ARG for an unknown name. */
 int realq_ctx_set_timing(realq_ctx* ctx, int enable);
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms);
 int realq_ctx_reset_timing(realq_ctx* ctx);
+
+/* ------------------------------------------------------------------ a0: Stage-0 accumulators
+ * Stage 0 of Alg. 1 derives two per-module quantities from the per-token gradients
+ * g_t = dL/dy_t of the module's output, G: [T, m] bf16, token-major (G[t*m + i]).
+ *
+ * Aggregated Fisher (Eq. fisher_full): F = (1/T) sum_t g_t g_t^T.  realq_fisher_accum adds
+ * sum_t g_t g_t^T over the T tokens given to F_acc ([m,m] float64, caller-initialised,
+ * typically zeroed), one call per token chunk (the same MFMA contraction as the Hessian, bf16
+ * products accumulated in float32 per tile and in float64 across tiles).  realq_fisher_finish
+ * writes F = F_acc / T_total as the float32 [m,m] metric that realq_bgd_state_create and
+ * realq_layer_desc take as M.  T == 0 is a no-op; T_total must be > 0. */
+int realq_fisher_accum(realq_ctx* ctx, const uint16_t* G /*[T,m]*/, int64_t T, int64_t m, double* F_acc /*[m,m]*/);
+int realq_fisher_finish(realq_ctx* ctx, const double* F_acc, int64_t m, int64_t T_total, float* F /*[m,m]*/);
+
+/* Saliency per row group (Sec. 3.3, Eq. saliency_hessian).  The m output channels are cut into
+ * n_groups contiguous row groups of r = ceil(m / n_groups) channels (the last one shorter; a
+ * group that would start at or past m is empty), and
+ *   s_out[g*T + t] = sum over the channels i of group g of G[t, i]^2
+ * (squares and sums in float64, stored as float32).  clip_q in (0, 1] then clips every group's
+ * row at its nearest-rank clip_q quantile over the T tokens, the k-th smallest value with
+ * k = ceil(clip_q * T) evaluated in double from the float32 clip_q (Appendix D.1's Hessian-side
+ * saliency clipping uses 0.99); clip_q = 0 disables the clip.  s_out is [n_groups, T] float32;
+ * rows of empty groups are written as zeros.  G must be finite.  1 <= n_groups <= m.  All T
+ * tokens are passed in one call, since the clip is a quantile over them.  T == 0 is a no-op. */
+int realq_saliency(realq_ctx* ctx, const uint16_t* G /*[T,m]*/, int64_t T, int64_t m, int32_t n_groups, float clip_q,
+                   float* s_out /*[n_groups,T]*/);
 
 /* ------------------------------------------------------------------ a1: Hessian
  * Sec. 3.2 (H = (2/T) sum_t x_t x_t^T) and Eq. saliency_hessian (per-token weights).
  * H_acc[n*n] (float64, caller-initialised, typically zeroed) += sum_t s_t xhat_t xhat_t^T
  * over the T tokens given.  Call once per token chunk; the 2/T scale is applied by
  * realq_chol_inverse with the total token count.  s may be NULL (all ones).
- * T == 0 is a no-op.  The full symmetric matrix is written. */
+ * T == 0 is a no-op.  The full symmetric matrix is written.  Precision: the bf16 products
+ * are exact; s_t xhat_t is formed in float32 and carried as three bf16 terms (all of its
+ * 24 bits); tiles accumulate in float32 over a token chunk and in float64 across chunks. */
 int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat /*[T,n]*/, const float* s /*[T]|NULL*/,
                         int64_t T, int64_t n, double* H_acc /*[n,n]*/);
 
@@ -188,6 +216,20 @@ int realq_quantize_block(realq_ctx* ctx, double* W /*[m,n]*/, int64_t m, int64_t
                          const float* U /*[n,n]*/, const uint8_t* dead /*[n]|NULL*/, const realq_qparams* qp,
                          uint8_t* codes /*[m,n]*/, float* scales, uint8_t* zeros, realq_bgd_state* st);
 
+/* Row groups (Eq. saliency_hessian): each group of output rows is quantized with its own inverse
+ * factor.  realq_quantize_block_rows does what realq_quantize_block does for rows [r0, r1) only
+ * (W, codes, scales and zeros are the full [m, ...] arrays; U and dead are the group's), and
+ * with st != NULL refreshes the state's copy of W - W0 on those rows, but does not advance the
+ * residual base.  After every row group of a block has been quantized, realq_bgd_lock_block
+ * folds the block [c0, c0 + bs) into the state (the lock realq_quantize_block performs itself).
+ * Requirements as for realq_quantize_block, plus 0 <= r0 < r1 <= m; the lock takes the blocks in
+ * column order (c0 equal to the columns already locked), else REALQ_ERR_SHAPE. */
+int realq_quantize_block_rows(realq_ctx* ctx, double* W /*[m,n]*/, int64_t m, int64_t n, int64_t r0, int64_t r1,
+                              int64_t c0, int64_t bs, const float* U /*[n,n]*/, const uint8_t* dead /*[n]|NULL*/,
+                              const realq_qparams* qp, uint8_t* codes /*[m,n]*/, float* scales, uint8_t* zeros,
+                              realq_bgd_state* st);
+int realq_bgd_lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_t bs);
+
 /* ------------------------------------------------------------------ a7-a9: one BGD step
  * One Adam step (Eq. block_gd_update) on the trailing columns W[:, c1:n] against
  *   L = (1/2T) sum_t s_t R_t^T M_a R_t,  R = W Xhat^T - W0 X^T,  M_a = alpha M + (1-alpha) P
@@ -228,7 +270,13 @@ int realq_handoff(realq_ctx* ctx, const float* Wa, const float* Wb, const uint16
  * remain) by `steps` realq_bgd_step calls, and the final loss.
  * Window: when window_total > 0, column block b of this module is step
  * b_global = window_offset + b + 1 of window_total and alpha follows Eq. slide_window;
- * otherwise alpha = 1. */
+ * otherwise alpha = 1.
+ * Row groups: with s_groups != NULL ([n_groups, T] float32, e.g. from realq_saliency) row group g
+ * (as in realq_saliency) is quantized with its own Hessian (2/T) sum_t s_groups[g, t] xhat_t xhat_t^T,
+ * damping, dead columns and inverse factor (Eq. saliency_hessian, Alg. 1 Stage 1), while s keeps
+ * weighting the tokens of the Block-GD surrogate; then H, U and dead of the output are
+ * [n_groups, n, n] / [n_groups, n] (entries of empty groups untouched).  s_groups == NULL needs
+ * n_groups == 0 (one Hessian built from s); otherwise 1 <= n_groups <= m. */
 typedef struct realq_layer_desc {
     int64_t m, n, T;
     const float* W0;          /* [m,n] float32                                 */
@@ -240,6 +288,8 @@ typedef struct realq_layer_desc {
     int32_t window_offset, window_total;
     realq_qparams q;
     realq_bgd_params bgd;
+    const float* s_groups;    /* [n_groups,T] | NULL (one Hessian from s)       */
+    int32_t n_groups;         /* 0 with s_groups == NULL, else 1..m             */
 } realq_layer_desc;
 
 typedef struct realq_layer_out {
@@ -247,9 +297,11 @@ typedef struct realq_layer_out {
     float* scales;            /* [m,ceil(n/group)]         required             */
     uint8_t* zeros;           /* [m,ceil(n/group)]         required             */
     float* W_hat;             /* [m,n] final dequantized weights, required      */
-    float* H;                 /* [n,n] float32 Hessian before damping | NULL    */
-    float* U;                 /* [n,n] inverse factor | NULL (workspace used)   */
-    uint8_t* dead;            /* [n] | NULL                                     */
+    float* H;                 /* [n,n] float32 Hessian before damping | NULL
+                                 ([n_groups,n,n] with row groups)               */
+    float* U;                 /* [n,n] inverse factor | NULL (workspace used)
+                                 ([n_groups,n,n] with row groups)               */
+    uint8_t* dead;            /* [n] | NULL ([n_groups,n] with row groups)      */
     double* loss_trace;       /* [nblocks*steps] device float64 | NULL; entries of
                                  steps with a dense metric M_a are NaN          */
     double loss_final;        /* host: final loss with the module's own metric M

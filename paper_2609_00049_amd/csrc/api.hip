@@ -219,7 +219,8 @@ int realq_ctx_set_timing(realq_ctx* ctx, int enable) {
 }
 
 static const char* kTimedNames[] = {"hessian", "chol",  "quantize",  "obs",        "lock",      "resid",
-                                    "grad",    "adam",  "init",      "gram",       "gram_step", "dense_loss"};
+                                    "grad",    "adam",  "init",      "gram",       "gram_step", "dense_loss",
+                                    "saliency"};
 
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms) {
     if (!ctx || !name) return REALQ_ERR_INVALID_ARG;
@@ -252,12 +253,13 @@ int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat, const float* s, in
     int64_t tc = (int64_t)(128ll << 20) / n;
     tc = tc < 256 ? 256 : (tc / 256) * 256;
     if (tc > T) tc = ((T + 7) / 8) * 8;
-    void *xt = nullptr, *hi = nullptr, *lo = nullptr;
+    void *xt = nullptr, *hi = nullptr, *lo = nullptr, *lo2 = nullptr;
     int rc = get_ws(ctx, "h_xt", (size_t)n * tc * 2, &xt);
     if (rc) return rc;
     if (s) {
         if ((rc = get_ws(ctx, "h_hi", (size_t)n * tc * 2, &hi))) return rc;
         if ((rc = get_ws(ctx, "h_lo", (size_t)n * tc * 2, &lo))) return rc;
+        if ((rc = get_ws(ctx, "h_lo2", (size_t)n * tc * 2, &lo2))) return rc;
     }
     Timed tm(ctx, "hessian");
     for (int64_t t0 = 0; t0 < T; t0 += tc) {
@@ -272,8 +274,10 @@ int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat, const float* s, in
         g.lda = tc;
         g.splits = 1;
         if (s) {
-            RQ_HIP(ctx, realq::transpose_scale_split(Xhat + t0 * n, n, s + t0, (uint16_t*)hi, (uint16_t*)lo, tc, cur,
-                                                     n, ctx->stream));
+            // s_t xhat_t in three bf16 terms: with a heavy-tailed s a few tokens carry H, and the
+            // 2^-17 remainder of a hi/lo pair would not average out over the tokens
+            RQ_HIP(ctx, realq::transpose_scale_split(Xhat + t0 * n, n, s + t0, (uint16_t*)hi, (uint16_t*)lo,
+                                                     (uint16_t*)lo2, tc, cur, n, ctx->stream));
             g.Ahi = (const uint16_t*)hi;
             g.Alo = (const uint16_t*)lo;
         } else {
@@ -281,7 +285,50 @@ int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat, const float* s, in
             g.Alo = nullptr;
         }
         RQ_HIP(ctx, realq::gemm_acc_f64(g, H_acc, n, ctx->stream));
+        if (s) {
+            g.Ahi = (const uint16_t*)lo2;
+            g.Alo = nullptr;
+            RQ_HIP(ctx, realq::gemm_acc_f64(g, H_acc, n, ctx->stream));
+        }
     }
+    return REALQ_OK;
+}
+
+// ============================================================================ a0: Stage-0 accumulators
+
+int realq_fisher_accum(realq_ctx* ctx, const uint16_t* G, int64_t T, int64_t m, double* F_acc) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (T < 0 || m <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "fisher_accum: need T >= 0, m > 0");
+    if (T == 0) return REALQ_OK;
+    if (!G || !F_acc) return set_error(ctx, REALQ_ERR_INVALID_ARG, "fisher_accum: NULL G or F_acc");
+    // sum_t g_t g_t^T is the unweighted Hessian contraction with the gradients in place of the inputs
+    return realq_hessian_accum(ctx, G, nullptr, T, m, F_acc);
+}
+
+int realq_fisher_finish(realq_ctx* ctx, const double* F_acc, int64_t m, int64_t T_total, float* F) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (m <= 0 || T_total <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "fisher_finish: need m > 0, T_total > 0");
+    if (!F_acc || !F) return set_error(ctx, REALQ_ERR_INVALID_ARG, "fisher_finish: NULL F_acc or F");
+    RQ_HIP(ctx, realq::div_narrow(F_acc, (double)T_total, F, m * m, ctx->stream));
+    return REALQ_OK;
+}
+
+int realq_saliency(realq_ctx* ctx, const uint16_t* G, int64_t T, int64_t m, int32_t n_groups, float clip_q,
+                   float* s_out) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (T < 0 || m <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "saliency: need T >= 0, m > 0");
+    if (n_groups < 1 || n_groups > m) return set_error(ctx, REALQ_ERR_INVALID_ARG, "saliency: need 1 <= n_groups <= m");
+    if (!std::isfinite(clip_q) || clip_q < 0.f || clip_q > 1.f)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "saliency: clip_q must lie in [0, 1] (0 = off)");
+    if (T == 0) return REALQ_OK;
+    if (!G || !s_out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "saliency: NULL G or s_out");
+    const int64_t k = clip_q > 0.f ? std::max<int64_t>(1, (int64_t)std::ceil((double)clip_q * (double)T)) : 0;
+    void *s64, *tau;
+    int rc;
+    if ((rc = get_ws(ctx, "sal_s", (size_t)n_groups * T * 8, &s64))) return rc;
+    if ((rc = get_ws(ctx, "sal_tau", (size_t)n_groups * 8, &tau))) return rc;
+    Timed tm(ctx, "saliency");
+    RQ_HIP(ctx, realq::saliency(G, T, m, n_groups, k, (double*)s64, (double*)tau, s_out, ctx->stream));
     return REALQ_OK;
 }
 
@@ -620,13 +667,15 @@ static int validate_q(realq_ctx* ctx, const realq_qparams* qp) {
     return REALQ_OK;
 }
 
-int realq_quantize_block(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_t c0, int64_t bs, const float* U,
-                         const uint8_t* dead, const realq_qparams* qp, uint8_t* codes, float* scales, uint8_t* zeros,
-                         realq_bgd_state* st) {
-    if (!ctx) return REALQ_ERR_INVALID_ARG;
+// Rows [r0, r1) of one column block: search, quantize and compensate inside the block, then the
+// trailing update; with a state, its copy of W - W0 follows on those rows.
+static int quantize_rows(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_t r0, int64_t r1, int64_t c0,
+                         int64_t bs, const float* U, const uint8_t* dead, const realq_qparams* qp, uint8_t* codes,
+                         float* scales, uint8_t* zeros, realq_bgd_state* st) {
     int rc = validate_q(ctx, qp);
     if (rc) return rc;
     if (m <= 0 || n <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: need m, n > 0");
+    if (r0 < 0 || r1 <= r0 || r1 > m) return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: need 0 <= r0 < r1 <= m");
     if (c0 < 0 || bs < 1 || bs > 128 || c0 + bs > n)
         return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: need 0 <= c0, 1 <= bs <= 128, c0 + bs <= n");
     if (c0 % qp->block != 0 || (bs != qp->block && c0 + bs != n))
@@ -635,29 +684,34 @@ int realq_quantize_block(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_block: NULL W, U, codes, scales or zeros");
     if (st && (st->m != m || st->n != n))
         return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: state shape differs from W");
+    if (st && st->locked != c0)
+        return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: blocks must be quantized in column order");
+    const int64_t mr = r1 - r0;
+    const int64_t group = qp->group > 0 ? qp->group : n;  // 0: one group per row
+    const int64_t ngroups = (n + group - 1) / group;
     void* E;
-    if ((rc = get_ws(ctx, "q_E", (size_t)m * bs * 8, &E))) return rc;
+    if ((rc = get_ws(ctx, "q_E", (size_t)mr * bs * 8, &E))) return rc;
     hipStream_t s = ctx->stream;
     realq::QuantArgs q{};
-    q.W = W;
-    q.m = m;
+    q.W = W + r0 * n;
+    q.m = mr;
     q.n = n;
     q.c0 = c0;
     q.bs = bs;
     q.U = U;
     q.dead = dead;
     q.bits = qp->bits;
-    q.group = qp->group > 0 ? qp->group : n;  // 0: one group per row
+    q.group = (int)group;
     q.grid = qp->grid;
     q.sym = qp->sym;
-    q.codes = codes;
-    q.scales = scales;
-    q.zeros = zeros;
-    q.ngroups = (n + q.group - 1) / q.group;
+    q.codes = codes + r0 * n;
+    q.scales = scales + r0 * ngroups;
+    q.zeros = zeros + r0 * ngroups;
+    q.ngroups = ngroups;
     q.E = (double*)E;
-    q.W0 = st ? st->W0 : nullptr;
-    q.Dhi = st ? st->Dhi : nullptr;
-    q.Dlo = st ? st->Dlo : nullptr;
+    q.W0 = st ? st->W0 + r0 * n : nullptr;
+    q.Dhi = st ? st->Dhi + r0 * n : nullptr;
+    q.Dlo = st ? st->Dlo + r0 * n : nullptr;
     {
         Timed tm(ctx, "quantize");
         RQ_HIP(ctx, realq::quantize_block(q, s));
@@ -669,31 +723,59 @@ int realq_quantize_block(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_
         a.lde = bs;
         a.U = U + c0 * n + c1;
         a.ldu = n;
-        a.W = W + c1;
+        a.W = W + r0 * n + c1;
         a.ldw = n;
-        a.M = m;
+        a.M = mr;
         a.N = n - c1;
         a.K = bs;
         if (st) {
-            a.W0 = st->W0 + c1;
+            a.W0 = st->W0 + r0 * n + c1;
             a.ldw0 = n;
-            a.Dhi = st->Dhi + c1;
-            a.Dlo = st->Dlo + c1;
+            a.Dhi = st->Dhi + r0 * n + c1;
+            a.Dlo = st->Dlo + r0 * n + c1;
             a.ldd = n;
         }
         Timed tm(ctx, "obs");
         RQ_HIP(ctx, realq::obs_update(a, s));
     }
-    if (st) {
-        if (!st->gram) {
-            // lock: B += (W_hat - W0)[:, block] Xhat[:, block]^T
-            realq::GemmArgs g{st->Dhi + c0, st->Dlo + c0, n, st->Xhat + c0, n, m, st->T, bs, 1};
-            Timed tm(ctx, "lock");
-            RQ_HIP(ctx, realq::gemm_acc_f32(g, st->B, st->T, 1.f, s));
-        }
-        st->locked = c1;
-    }
     return REALQ_OK;
+}
+
+// The block's quantized weights stay locked (Sec. 4.3): B += (W_hat - W0)[:, block] Xhat[:, block]^T
+// (the Gram form keeps no residual base and only moves the boundary).
+static int lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_t bs) {
+    const int64_t n = st->n;
+    if (c0 != st->locked || bs < 1 || c0 + bs > n)
+        return set_error(ctx, REALQ_ERR_SHAPE, "bgd_lock_block: blocks must be locked in column order");
+    if (!st->gram) {
+        realq::GemmArgs g{st->Dhi + c0, st->Dlo + c0, n, st->Xhat + c0, n, st->m, st->T, bs, 1};
+        Timed tm(ctx, "lock");
+        RQ_HIP(ctx, realq::gemm_acc_f32(g, st->B, st->T, 1.f, ctx->stream));
+    }
+    st->locked = c0 + bs;
+    return REALQ_OK;
+}
+
+int realq_quantize_block(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_t c0, int64_t bs, const float* U,
+                         const uint8_t* dead, const realq_qparams* qp, uint8_t* codes, float* scales, uint8_t* zeros,
+                         realq_bgd_state* st) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    int rc = quantize_rows(ctx, W, m, n, 0, m, c0, bs, U, dead, qp, codes, scales, zeros, st);
+    if (rc) return rc;
+    return st ? lock_block(ctx, st, c0, bs) : REALQ_OK;
+}
+
+int realq_quantize_block_rows(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_t r0, int64_t r1, int64_t c0,
+                              int64_t bs, const float* U, const uint8_t* dead, const realq_qparams* qp,
+                              uint8_t* codes, float* scales, uint8_t* zeros, realq_bgd_state* st) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    return quantize_rows(ctx, W, m, n, r0, r1, c0, bs, U, dead, qp, codes, scales, zeros, st);
+}
+
+int realq_bgd_lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_t bs) {
+    if (!ctx) return REALQ_ERR_INVALID_ARG;
+    if (!st) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_lock_block: NULL state");
+    return lock_block(ctx, st, c0, bs);
 }
 
 // ============================================================================ a7-a9: one BGD step
@@ -1013,22 +1095,33 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
     if (!out->codes || !out->scales || !out->zeros || !out->W_hat)
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_layer: NULL codes, scales, zeros or W_hat");
     const int64_t m = d->m, n = d->n, T = d->T;
+    const bool grouped = d->s_groups != nullptr;
+    if (!grouped && d->n_groups != 0)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_layer: n_groups needs s_groups (0 without)");
+    if (grouped && (d->n_groups < 1 || d->n_groups > m))
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "quantize_layer: need 1 <= n_groups <= m");
+    // row groups of rsz rows (one group of all m rows without s_groups); ngr of them hold rows
+    const int64_t rsz = grouped ? (m + d->n_groups - 1) / d->n_groups : m;
+    const int64_t ngr = (m + rsz - 1) / rsz;
     hipStream_t s = ctx->stream;
     hipEvent_t ev0, ev1;
     RQ_HIP(ctx, hipEventCreate(&ev0));
     RQ_HIP(ctx, hipEventCreate(&ev1));
     RQ_HIP(ctx, hipEventRecord(ev0, s));
 
-    // a1: Hessian
+    // a1-a2: Hessian and inverse factor of every row group (each factorisation synchronises once)
     void *Hacc, *Uw = out->U, *deadw = out->dead;
     if ((rc = get_ws(ctx, "l_H", (size_t)n * n * 8, &Hacc))) return rc;
-    if (!Uw && (rc = get_ws(ctx, "l_U", (size_t)n * n * 4, &Uw))) return rc;
-    if (!deadw && (rc = get_ws(ctx, "l_dead", (size_t)n, &deadw))) return rc;
-    RQ_HIP(ctx, realq::fill_f64((double*)Hacc, 0.0, n * n, s));
-    if ((rc = realq_hessian_accum(ctx, d->Xhat, d->s, T, n, (double*)Hacc))) return rc;
-    // a2: inverse factor (synchronises once)
-    if ((rc = realq_chol_inverse(ctx, (const double*)Hacc, n, T, d->q.damp, out->H, (float*)Uw, (uint8_t*)deadw)))
-        return rc;
+    if (!Uw && (rc = get_ws(ctx, "l_U", (size_t)ngr * n * n * 4, &Uw))) return rc;
+    if (!deadw && (rc = get_ws(ctx, "l_dead", (size_t)ngr * n, &deadw))) return rc;
+    for (int64_t g = 0; g < ngr; ++g) {
+        RQ_HIP(ctx, realq::fill_f64((double*)Hacc, 0.0, n * n, s));
+        const float* sg = grouped ? d->s_groups + g * T : d->s;
+        if ((rc = realq_hessian_accum(ctx, d->Xhat, sg, T, n, (double*)Hacc))) return rc;
+        if ((rc = realq_chol_inverse(ctx, (const double*)Hacc, n, T, d->q.damp, out->H ? out->H + g * n * n : nullptr,
+                                     (float*)Uw + g * n * n, (uint8_t*)deadw + g * n)))
+            return rc;
+    }
 
     // state on context workspaces (reused across calls of the same size)
     realq_bgd_state st;
@@ -1056,9 +1149,13 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
     if (out->loss_trace && bgd) RQ_HIP(ctx, realq::fill_f64(out->loss_trace, NAN, nb * d->bgd.steps, s));
     for (int64_t b = 0; b < nb; ++b) {
         const int64_t c0 = b * d->q.block, bs = std::min<int64_t>(d->q.block, n - c0), c1 = c0 + bs;
-        if ((rc = realq_quantize_block(ctx, W, m, n, c0, bs, (const float*)Uw, (const uint8_t*)deadw, &d->q,
-                                       out->codes, out->scales, out->zeros, bgd ? &st : nullptr)))
-            return rc;
+        for (int64_t g = 0; g < ngr; ++g) {
+            if ((rc = quantize_rows(ctx, W, m, n, g * rsz, std::min(m, (g + 1) * rsz), c0, bs,
+                                    (const float*)Uw + g * n * n, (const uint8_t*)deadw + g * n, &d->q, out->codes,
+                                    out->scales, out->zeros, bgd ? &st : nullptr)))
+                return rc;
+        }
+        if (bgd && (rc = lock_block(ctx, &st, c0, bs))) return rc;
         if (!bgd || c1 >= n) continue;
         float alpha = 1.f;
         if (d->window_total > 1) {
@@ -1083,6 +1180,10 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
         }
         if ((rc = realq_bgd_loss(ctx, &st, W, (double*)lf))) return rc;
     } else {
+        if (grouped) {  // the loss weighs tokens by s, not by a row group's saliency
+            RQ_HIP(ctx, realq::fill_f64((double*)Hacc, 0.0, n * n, s));
+            if ((rc = realq_hessian_accum(ctx, d->Xhat, d->s, T, n, (double*)Hacc))) return rc;
+        }
         if ((rc = dense_final_loss(ctx, d, W, (const double*)Hacc, (double*)lf))) return rc;
     }
     RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat, m * n, s));

@@ -40,12 +40,14 @@ hipError_t fill_u16(uint16_t* p, uint16_t v, int64_t count, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------- tiled transposes (64 x 64 tiles via LDS)
-// MODE 0: plain copy of bit patterns; MODE 1: value s[r] * x, written as a hi/lo bf16 pair.
+// MODE 0: plain copy of bit patterns; MODE 1: value s[r] * x, written as a hi/lo bf16 pair and,
+// when o3 != NULL, a third bf16 term of what hi + lo leaves (hi + lo + o3 holds all 24 bits of
+// the float32 product).
 template <int MODE>
 __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restrict__ in, int64_t ldi,
                                                         const float* __restrict__ s, uint16_t* __restrict__ o1,
-                                                        uint16_t* __restrict__ o2, int64_t ldo, int64_t rows,
-                                                        int64_t cols, int64_t tiles_c) {
+                                                        uint16_t* __restrict__ o2, uint16_t* __restrict__ o3,
+                                                        int64_t ldo, int64_t rows, int64_t cols, int64_t tiles_c) {
     __shared__ float tile[64][65];
     const int64_t tr = blockIdx.x / tiles_c, tc = blockIdx.x % tiles_c;
     const int64_t r0 = tr * 64, c0 = tc * 64;
@@ -71,6 +73,8 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restri
                 split_bf16(v, hi, lo);
                 o1[c * ldo + r] = hi;
                 o2[c * ldo + r] = lo;
+                // v - hi and then - lo are exact in float32 (each term keeps v's leading bits)
+                if (o3) o3[c * ldo + r] = f2bf((v - bf2f(hi)) - bf2f(lo));
             }
         }
     }
@@ -81,16 +85,16 @@ hipError_t transpose_u16(const uint16_t* in, int64_t ldi, uint16_t* out, int64_t
     if (rows <= 0 || cols <= 0) return hipSuccess;
     int64_t tr = (rows + 63) / 64, tc = (cols + 63) / 64;
     hipLaunchKernelGGL(transpose_kernel<0>, dim3((unsigned)(tr * tc)), dim3(256), 0, st, in, ldi, nullptr, out,
-                       nullptr, ldo, rows, cols, tc);
+                       nullptr, nullptr, ldo, rows, cols, tc);
     return hipGetLastError();
 }
 
 hipError_t transpose_scale_split(const uint16_t* in, int64_t ldi, const float* s, uint16_t* hi, uint16_t* lo,
-                                 int64_t ldo, int64_t rows, int64_t cols, hipStream_t st) {
+                                 uint16_t* lo2, int64_t ldo, int64_t rows, int64_t cols, hipStream_t st) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
     int64_t tr = (rows + 63) / 64, tc = (cols + 63) / 64;
-    hipLaunchKernelGGL(transpose_kernel<1>, dim3((unsigned)(tr * tc)), dim3(256), 0, st, in, ldi, s, hi, lo, ldo,
-                       rows, cols, tc);
+    hipLaunchKernelGGL(transpose_kernel<1>, dim3((unsigned)(tr * tc)), dim3(256), 0, st, in, ldi, s, hi, lo, lo2,
+                       ldo, rows, cols, tc);
     return hipGetLastError();
 }
 

@@ -47,9 +47,10 @@ hipError_t fill_u16(uint16_t* p, uint16_t v, int64_t count, hipStream_t st);
 // out[c*ldo + r] = in[r*ldi + c] for r < rows, c < cols (bf16 bit patterns)
 hipError_t transpose_u16(const uint16_t* in, int64_t ldi, uint16_t* out, int64_t ldo, int64_t rows, int64_t cols,
                          hipStream_t st);
-// Transposed, weighted split: hi/lo[c*ldo + r] = split(s[r] * bf16(in[r*ldi + c]))   (s may be NULL)
+// Transposed, weighted split: hi/lo[c*ldo + r] = split(s[r] * bf16(in[r*ldi + c]))   (s may be NULL);
+// lo2 (may be NULL) receives the bf16 of the float32 remainder, so hi + lo + lo2 is the product.
 hipError_t transpose_scale_split(const uint16_t* in, int64_t ldi, const float* s, uint16_t* hi, uint16_t* lo,
-                                 int64_t ldo, int64_t rows, int64_t cols, hipStream_t st);
+                                 uint16_t* lo2, int64_t ldo, int64_t rows, int64_t cols, hipStream_t st);
 // hi/lo[i*ld + j] = split(A[i*lda + j] - (Bm ? Bm[i*ldb + j] : 0)) for j < cols (float32 inputs)
 hipError_t split_diff_f32(const float* A, int64_t lda, const float* Bm, int64_t ldb, uint16_t* hi, uint16_t* lo,
                           int64_t ld, int64_t rows, int64_t cols, hipStream_t st);
@@ -130,6 +131,16 @@ hipError_t clip_apply(const float* R, int64_t ldr, int64_t m, int64_t cur, const
 int64_t clip_apply_partials();
 // R[i][t] = B0[i][t] + (split(D) Xhat^T)[i][t] in float32 (the residual kept whole for the clip)
 hipError_t gemm_resid_f32(const GemmArgs& g, const float* B0, int64_t ldb0, float* R, int64_t ldr, hipStream_t st);
+
+// ---------------------------------------------------------------- Stage-0 accumulators
+// Row group g = channels [g r, min(m, (g+1) r)), r = ceil(m / n_groups).  s64 [n_groups][T]
+// (work) = float64 sums of G[t][i]^2 over the group's channels; k > 0: tau[g] = k-th smallest
+// of group g's row (nearest rank, 1 <= k <= T) and out = float(min(s64, tau)); k == 0: out =
+// float(s64).  Rows of empty groups (g r >= m) are written as zeros.
+hipError_t saliency(const uint16_t* G, int64_t T, int64_t m, int64_t n_groups, int64_t k, double* s64, double* tau,
+                    float* out, hipStream_t st);
+// out[e] = float(a[e] / d)
+hipError_t div_narrow(const double* a, double d, float* out, int64_t count, hipStream_t st);
 
 // ---------------------------------------------------------------- quantize one column block
 struct QuantArgs {

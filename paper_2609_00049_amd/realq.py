@@ -31,9 +31,11 @@ EXPORTS = [
     "realq_qparams_default", "realq_bgd_params_default",
     "realq_ctx_create", "realq_ctx_destroy", "realq_last_error",
     "realq_ctx_set_timing", "realq_ctx_kernel_time", "realq_ctx_reset_timing",
+    "realq_fisher_accum", "realq_fisher_finish", "realq_saliency",
     "realq_hessian_accum", "realq_chol_inverse",
     "realq_bgd_state_create", "realq_bgd_state_destroy",
-    "realq_quantize_block", "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
+    "realq_quantize_block", "realq_quantize_block_rows", "realq_bgd_lock_block",
+    "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
     "realq_pullback_metric", "realq_handoff",
 ]
 
@@ -66,7 +68,8 @@ class LayerDesc(ctypes.Structure):
                 ("W0", ctypes.c_void_p), ("X", ctypes.c_void_p), ("Xhat", ctypes.c_void_p),
                 ("s", ctypes.c_void_p), ("M", ctypes.c_void_p), ("P", ctypes.c_void_p),
                 ("window_offset", ctypes.c_int32), ("window_total", ctypes.c_int32),
-                ("q", QParams), ("bgd", BgdParams)]
+                ("q", QParams), ("bgd", BgdParams),
+                ("s_groups", ctypes.c_void_p), ("n_groups", ctypes.c_int32)]
 
 
 class LayerOut(ctypes.Structure):
@@ -91,6 +94,9 @@ def _load():
         "realq_ctx_kernel_time": (ctypes.c_int, [vp, ctypes.c_char_p, ctypes.POINTER(i64),
                                                  ctypes.POINTER(ctypes.c_double)]),
         "realq_ctx_reset_timing": (ctypes.c_int, [vp]),
+        "realq_fisher_accum": (ctypes.c_int, [vp, vp, i64, i64, vp]),
+        "realq_fisher_finish": (ctypes.c_int, [vp, vp, i64, i64, vp]),
+        "realq_saliency": (ctypes.c_int, [vp, vp, i64, i64, i32, f32, vp]),
         "realq_hessian_accum": (ctypes.c_int, [vp, vp, vp, i64, i64, vp]),
         "realq_chol_inverse": (ctypes.c_int, [vp, vp, i64, i64, f32, vp, vp, vp]),
         "realq_bgd_state_create": (ctypes.c_int, [vp, ctypes.POINTER(vp), vp, vp, vp, vp, vp, vp, i64, i64, i64,
@@ -98,6 +104,9 @@ def _load():
         "realq_bgd_state_destroy": (None, [vp]),
         "realq_quantize_block": (ctypes.c_int, [vp, vp, i64, i64, i64, i64, vp, vp, ctypes.POINTER(QParams),
                                                 vp, vp, vp, vp]),
+        "realq_quantize_block_rows": (ctypes.c_int, [vp, vp, i64, i64, i64, i64, i64, i64, vp, vp,
+                                                     ctypes.POINTER(QParams), vp, vp, vp, vp]),
+        "realq_bgd_lock_block": (ctypes.c_int, [vp, vp, i64, i64]),
         "realq_bgd_step": (ctypes.c_int, [vp, vp, vp, i64, f32, vp]),
         "realq_bgd_loss": (ctypes.c_int, [vp, vp, vp, vp]),
         "realq_quantize_layer": (ctypes.c_int, [vp, ctypes.POINTER(LayerDesc), ctypes.POINTER(LayerOut)]),
@@ -194,7 +203,35 @@ class Context:
         return n.value, ms.value
 
 
-# ----------------------------------------------------------------------------- the five calls
+# ----------------------------------------------------------------------------- the calls
+
+def row_groups(m: int, n_groups: int):
+    """(r0, r1) of the row groups that hold rows: contiguous ranges of ceil(m / n_groups) rows."""
+    r = -(-m // n_groups)
+    return [(g * r, min(m, (g + 1) * r)) for g in range(n_groups) if g * r < m]
+
+
+def fisher_accum(ctx: Context, G: torch.Tensor, F_acc: torch.Tensor):
+    """F_acc += sum_t g_t g_t^T (float64 [m,m]); G [T,m] bf16 output gradients."""
+    T, m = G.shape
+    ctx.check(_lib.realq_fisher_accum(ctx.h, _ptr(_bits(G)), T, m, _ptr(F_acc)))
+
+
+def fisher_finish(ctx: Context, F_acc: torch.Tensor, T_total: int, F: torch.Tensor):
+    """F = float32(F_acc / T_total)."""
+    m = F_acc.shape[0]
+    ctx.check(_lib.realq_fisher_finish(ctx.h, _ptr(F_acc), m, T_total, _ptr(F)))
+
+
+def saliency(ctx: Context, G: torch.Tensor, n_groups: int, clip_q: float = 0.0, out: Optional[torch.Tensor] = None):
+    """[n_groups, T] float32 per-token squared gradient norms of each row group, clipped per group
+    at the nearest-rank clip_q quantile over tokens (0 = no clip)."""
+    T, m = G.shape
+    if out is None:
+        out = torch.empty((n_groups, T), dtype=torch.float32, device=G.device)
+    ctx.check(_lib.realq_saliency(ctx.h, _ptr(_bits(G)), T, m, n_groups, clip_q, _ptr(out)))
+    return out
+
 
 def hessian_accum(ctx: Context, Xhat: torch.Tensor, s: Optional[torch.Tensor], H_acc: torch.Tensor):
     """H_acc += sum_t s_t xhat_t xhat_t^T (float64 [n,n])."""
@@ -239,6 +276,18 @@ def quantize_block(ctx: Context, W, c0: int, bs: int, U, dead, qp: QParams, code
                                         _ptr(codes), _ptr(scales), _ptr(zeros), state.h if state else None))
 
 
+def quantize_block_rows(ctx: Context, W, r0: int, r1: int, c0: int, bs: int, U, dead, qp: QParams, codes, scales,
+                        zeros, state: Optional[BgdState] = None):
+    m, n = W.shape
+    ctx.check(_lib.realq_quantize_block_rows(ctx.h, _ptr(_f64(W)), m, n, r0, r1, c0, bs, _ptr(U), _ptr(dead),
+                                             ctypes.byref(qp), _ptr(codes), _ptr(scales), _ptr(zeros),
+                                             state.h if state else None))
+
+
+def bgd_lock_block(ctx: Context, state: BgdState, c0: int, bs: int):
+    ctx.check(_lib.realq_bgd_lock_block(ctx.h, state.h, c0, bs))
+
+
 def bgd_step(ctx: Context, state: BgdState, W, c1: int, alpha: float = 1.0, loss_out=None):
     ctx.check(_lib.realq_bgd_step(ctx.h, state.h, _ptr(_f64(W)), c1, alpha, _ptr(loss_out)))
 
@@ -276,13 +325,16 @@ class LayerResult:
 
 def quantize_layer(ctx: Context, W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams] = None,
                    bgd: Optional[BgdParams] = None, window=None, want_H=False, want_U=False,
-                   want_trace=True, out: Optional[LayerResult] = None) -> LayerResult:
-    """Whole-module sweep; allocates the outputs unless ``out`` supplies them."""
+                   want_trace=True, s_groups=None, out: Optional[LayerResult] = None) -> LayerResult:
+    """Whole-module sweep; allocates the outputs unless ``out`` supplies them.  ``s_groups``
+    [N_g, T] float32: one Hessian per row group (H, U and dead then carry a leading N_g axis)."""
     qp = qp or qparams()
     bgd = bgd or bgd_params()
     m, n = W0.shape
     T = X.shape[0]
     dev = W0.device
+    n_groups = 0 if s_groups is None else s_groups.shape[0]
+    lead = () if s_groups is None else (n_groups,)
     if out is None:
         ng = -(-n // (qp.group or n))
         nb = -(-n // qp.block)
@@ -291,15 +343,15 @@ def quantize_layer(ctx: Context, W0, X, Xhat, s=None, M=None, P=None, *, qp: Opt
             scales=torch.empty((m, ng), dtype=torch.float32, device=dev),
             zeros=torch.empty((m, ng), dtype=torch.uint8, device=dev),
             W_hat=torch.empty((m, n), dtype=torch.float32, device=dev),
-            H=torch.empty((n, n), dtype=torch.float32, device=dev) if want_H else None,
-            U=torch.empty((n, n), dtype=torch.float32, device=dev) if want_U else None,
-            dead=torch.empty((n,), dtype=torch.uint8, device=dev),
+            H=torch.empty(lead + (n, n), dtype=torch.float32, device=dev) if want_H else None,
+            U=torch.empty(lead + (n, n), dtype=torch.float32, device=dev) if want_U else None,
+            dead=torch.empty(lead + (n,), dtype=torch.uint8, device=dev),
             loss_trace=torch.empty((max(1, nb * bgd.steps),), dtype=torch.float64, device=dev)
             if want_trace else None,
             loss_final=math.nan, ms_total=math.nan)
     woff, wtot = (0, 0) if window is None else window
     desc = LayerDesc(m, n, T, _ptr(W0), _ptr(_bits(X)), _ptr(_bits(Xhat)), _ptr(s), _ptr(M), _ptr(P),
-                     woff, wtot, qp, bgd)
+                     woff, wtot, qp, bgd, _ptr(s_groups), n_groups)
     lo = LayerOut(_ptr(out.codes), _ptr(out.scales), _ptr(out.zeros), _ptr(out.W_hat), _ptr(out.H), _ptr(out.U),
                   _ptr(out.dead), _ptr(out.loss_trace), math.nan, math.nan)
     ctx.check(_lib.realq_quantize_layer(ctx.h, ctypes.byref(desc), ctypes.byref(lo)))

@@ -10,6 +10,8 @@ from .gen import (  # noqa: F401
     bf16_bits,
     bf16_round,
     bf16_from_bits,
+    make_group_weights,
     make_module,
+    make_output_grads,
     module_names,
 )

@@ -163,3 +163,33 @@ def make_module(cfg: str, module: Optional[str] = None, seed: int = 0, *,
         M = (A @ A.T) / np.float32(2 * d)
     return LayerInputs(cfg=cfg, module=module, W0=W, X=X, Xhat=Xhat, s=s, M=M,
                        steps=c["steps"], lr=c["lr"])
+
+
+# ----------------------------------------------------------------------------- Stage-0 inputs
+
+def make_output_grads(T: int, m: int, seed: int = 0, outlier_tokens: int = 4,
+                      outlier_scale: float = 1e5) -> np.ndarray:
+    """Per-token gradients of a module's output, [T, m] bf16-exact float32.
+
+    Token magnitudes are log-normal (about one decade of spread), channel magnitudes
+    log-normal (half a decade), and ``outlier_tokens`` tokens are scaled up by
+    ``outlier_scale``: end-to-end gradients in deep layers reach many orders of magnitude
+    above the median (Appendix D.1), which the saliency clip exists for.
+    """
+    rng = np.random.default_rng(seed * 1000 + 900)
+    g = rng.standard_normal((T, m), dtype=np.float32)
+    g *= rng.lognormal(0.0, 2.3, size=(T, 1)).astype(np.float32)
+    g *= rng.lognormal(0.0, 1.15, size=(1, m)).astype(np.float32)
+    if outlier_tokens > 0 and T > 0:
+        idx = rng.choice(T, size=min(outlier_tokens, T), replace=False)
+        g[idx] *= np.float32(outlier_scale)
+    return bf16_round(g * np.float32(1e-3))
+
+
+def make_group_weights(n_groups: int, T: int, seed: int = 0) -> np.ndarray:
+    """Positive per-token weights of ``n_groups`` row groups, [n_groups, T] float32, log-normal
+    with a shared per-token factor (groups of one module see correlated saliency)."""
+    rng = np.random.default_rng(seed * 1000 + 901)
+    common = rng.lognormal(0.0, 1.0, size=(1, T))
+    own = rng.lognormal(0.0, 0.5, size=(n_groups, T))
+    return (common * own).astype(np.float32)
