@@ -109,6 +109,61 @@ def cpu_baseline(wl, rows=64, tokens=16384):
                       f"scaled to the full workload by algorithmic FLOPs ({t_full:.0f} s per sweep)"}
 
 
+def output_grads(torch, T, m, seed=1, chunk=16384):
+    """Device-side stand-in for per-token output gradients [T, m] bf16 with the distribution the
+    synthetic Stage-0 inputs use: Gaussian x LogNormal(0, 2.3) token scale x LogNormal(0, 1.15)
+    channel scale, four tokens x 1e5, scaled by 1e-3."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    chan = torch.exp(1.15 * torch.randn((1, m), generator=g, device="cuda"))
+    G = torch.empty((T, m), dtype=torch.bfloat16, device="cuda")
+    for t0 in range(0, T, chunk):
+        t1 = min(T, t0 + chunk)
+        tok = torch.exp(2.3 * torch.randn((t1 - t0, 1), generator=g, device="cuda"))
+        G[t0:t1] = (torch.randn((t1 - t0, m), generator=g, device="cuda") * tok * chan * 1e-3).to(torch.bfloat16)
+    idx = torch.randperm(T, generator=g, device="cuda")[:4]
+    G[idx] = (G[idx].float() * 1e5).to(torch.bfloat16)
+    torch.cuda.synchronize()
+    return G
+
+
+def stage0(torch, rq, ctx, W0, X, Xh, s, qp, bgd, m, n, T, n_groups=4, fisher_tokens=65536, d_model=4096):
+    """Stage-0 accumulators and the row-group sweep on the bench inputs:
+    saliency of the module's output gradients over all T tokens (HBM-bound: 2 B read per gradient),
+    the aggregated Fisher at the 4096-wide block output on a 65536-token batch (MFMA: 2 T d^2), and
+    the sweep with N_g = 4 saliency Hessians."""
+    out = {}
+    G = output_grads(torch, T, m)
+    S = rq.saliency(ctx, G, n_groups, 0.99)        # warm-up (workspaces)
+    ctx.reset_timing()
+    S = rq.saliency(ctx, G, n_groups, 0.99, out=S)
+    torch.cuda.synchronize()
+    _, ms = ctx.kernel_time("saliency")
+    by = 2.0 * T * m
+    out["saliency"] = {"tokens": T, "m": m, "groups": n_groups, "clip": 0.99, "ms": ms,
+                       "GB_per_s": by / (ms / 1e3) / 1e9, "frac_hbm": by / (ms / 1e3) / PEAK_HBM}
+    del G
+    Gb = output_grads(torch, fisher_tokens, d_model, seed=2)
+    F_acc = torch.zeros((d_model, d_model), dtype=torch.float64, device="cuda")
+    rq.fisher_accum(ctx, Gb, F_acc)                 # warm-up
+    F_acc.zero_()
+    ctx.reset_timing()
+    rq.fisher_accum(ctx, Gb, F_acc)
+    torch.cuda.synchronize()
+    _, ms = ctx.kernel_time("hessian")
+    fl = 2.0 * fisher_tokens * d_model * d_model
+    out["fisher"] = {"tokens": fisher_tokens, "d": d_model, "ms": ms, "TFLOP_per_s": fl / (ms / 1e3) / 1e12,
+                     "frac_bf16_peak": fl / (ms / 1e3) / PEAK_BF16}
+    del Gb, F_acc
+    o = rq.quantize_layer(ctx, W0, X, Xh, s, qp=qp, bgd=bgd, s_groups=S)         # warm-up (workspaces)
+    o = rq.quantize_layer(ctx, W0, X, Xh, s, qp=qp, bgd=bgd, s_groups=S, out=o)
+    print(f"[bench] row-group sweep (N_g = {n_groups}): {o.ms_total:.1f} ms, loss {o.loss_final:.6g}",
+          file=sys.stderr, flush=True)
+    out["row_group_sweep"] = {"groups": n_groups, "ms_per_step": o.ms_total, "columns_per_s": n / (o.ms_total / 1e3),
+                              "loss_final": o.loss_final}
+    return out
+
+
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_00049_amd", "csrc", "gemm_bf16.hip")
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_llama8b_gate_traffic.txt")
 
@@ -150,6 +205,8 @@ def main():
                          "headline metric), or the same loss and gradient through the calibration Gram matrices")
     ap.add_argument("--no-gram-line", action="store_true",
                     help="with --form tokens, skip the extra untimed Gram-form sweep reported under gram_form")
+    ap.add_argument("--no-stage0", action="store_true",
+                    help="skip the Stage-0 accumulator timings and the N_g = 4 row-group sweep (stage0)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs the sweep on one GPU; --gpus {args.gpus} is not supported "
@@ -241,6 +298,8 @@ def main():
                             "loss_final": og.loss_final, "loss_final_tokens": out.loss_final,
                             "note": "same loss and gradient through the calibration Gram matrices "
                                     "(bench.py --form gram for its own line)"}
+    if not args.no_stage0:
+        res["stage0"] = stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n, T)
     ctx.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
