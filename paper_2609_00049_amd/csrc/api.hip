@@ -323,12 +323,13 @@ int realq_saliency(realq_ctx* ctx, const uint16_t* G, int64_t T, int64_t m, int3
     if (T == 0) return REALQ_OK;
     if (!G || !s_out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "saliency: NULL G or s_out");
     const int64_t k = clip_q > 0.f ? std::max<int64_t>(1, (int64_t)std::ceil((double)clip_q * (double)T)) : 0;
-    void *s64, *tau;
+    void *s64, *tau, *sel;
     int rc;
     if ((rc = get_ws(ctx, "sal_s", (size_t)n_groups * T * 8, &s64))) return rc;
     if ((rc = get_ws(ctx, "sal_tau", (size_t)n_groups * 8, &tau))) return rc;
+    if ((rc = get_ws(ctx, "sal_sel", (size_t)realq::saliency_select_bytes(n_groups), &sel))) return rc;
     Timed tm(ctx, "saliency");
-    RQ_HIP(ctx, realq::saliency(G, T, m, n_groups, k, (double*)s64, (double*)tau, s_out, ctx->stream));
+    RQ_HIP(ctx, realq::saliency(G, T, m, n_groups, k, (double*)s64, (double*)tau, sel, s_out, ctx->stream));
     return REALQ_OK;
 }
 

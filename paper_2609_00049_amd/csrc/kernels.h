@@ -136,9 +136,11 @@ hipError_t gemm_resid_f32(const GemmArgs& g, const float* B0, int64_t ldb0, floa
 // Row group g = channels [g r, min(m, (g+1) r)), r = ceil(m / n_groups).  s64 [n_groups][T]
 // (work) = float64 sums of G[t][i]^2 over the group's channels; k > 0: tau[g] = k-th smallest
 // of group g's row (nearest rank, 1 <= k <= T) and out = float(min(s64, tau)); k == 0: out =
-// float(s64).  Rows of empty groups (g r >= m) are written as zeros.
+// float(s64).  Rows of empty groups (g r >= m) are written as zeros.  sel: work of
+// saliency_select_bytes(n_groups) bytes (8-byte aligned).
 hipError_t saliency(const uint16_t* G, int64_t T, int64_t m, int64_t n_groups, int64_t k, double* s64, double* tau,
-                    float* out, hipStream_t st);
+                    void* sel, float* out, hipStream_t st);
+int64_t saliency_select_bytes(int64_t n_groups);
 // out[e] = float(a[e] / d)
 hipError_t div_narrow(const double* a, double d, float* out, int64_t count, hipStream_t st);
 

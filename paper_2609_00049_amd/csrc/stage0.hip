@@ -9,31 +9,46 @@
 namespace realq {
 
 // s[g*T + t] = sum over the channels i of group g of G[t*m + i]^2, squares and sum in float64.
-// One wave per (group, token) item, grid-stride over the items in group-major order; the lanes
-// read consecutive channels of the group's contiguous segment (128 bytes per wave load) and the
-// wave reduces in a fixed butterfly order, so the result does not depend on the launch.
+// One wave per (group, token) item, grid-stride over the items in group-major order.  Lanes read
+// 16-byte runs of 8 channels from the 16-byte-aligned middle of the group's segment and single
+// channels at its ragged ends; the wave reduces in a fixed butterfly order, so the result does
+// not depend on the launch.
 constexpr int SAL_BLOCKS = 2048;
 __global__ __launch_bounds__(256) void saliency_sums_kernel(const uint16_t* __restrict__ G, int64_t T, int64_t m,
                                                             int64_t r, int64_t ng, double* __restrict__ s) {
     const int lane = threadIdx.x & 63;
     const int64_t nw = (int64_t)gridDim.x * 4;
     const int64_t items = T * ng;
+    const bool rows16 = (m & 7) == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0;
     for (int64_t it = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); it < items; it += nw) {
         const int64_t g = it / T, t = it - g * T;
         const int64_t i0 = g * r, i1 = i0 + r < m ? i0 + r : m;
         const uint16_t* row = G + t * m;
-        double a0 = 0.0, a1 = 0.0;
-        int64_t i = i0 + lane;
-        for (; i + 64 < i1; i += 128) {
-            const double v0 = (double)bf2f(row[i]), v1 = (double)bf2f(row[i + 64]);
-            a0 += v0 * v0;
-            a1 += v1 * v1;
+        // aligned middle [a0, a1) in runs of 8; the ends element by element
+        int64_t a0 = i0, a1 = i0;
+        if (rows16) {
+            a0 = (i0 + 7) & ~(int64_t)7;
+            a1 = i1 & ~(int64_t)7;
+            if (a1 < a0) a1 = a0 = i0;
         }
-        if (i < i1) {
-            const double v0 = (double)bf2f(row[i]);
-            a0 += v0 * v0;
+        double acc = 0.0;
+        for (int64_t c = a0 + 8 * lane; c < a1; c += 512) {
+            const u16x8 v = *reinterpret_cast<const u16x8*>(row + c);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const double x = (double)bf2f(v[e]);
+                acc += x * x;
+            }
         }
-        double acc = a0 + a1;
+        for (int64_t i = i0 + lane; i < a0; i += 64) {
+            const double x = (double)bf2f(row[i]);
+            acc += x * x;
+        }
+        const int64_t tail0 = a1 > a0 ? a1 : a0;
+        for (int64_t i = tail0 + lane; i < i1; i += 64) {
+            const double x = (double)bf2f(row[i]);
+            acc += x * x;
+        }
         for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
         if (lane == 0) s[it] = acc;
     }
@@ -41,45 +56,64 @@ __global__ __launch_bounds__(256) void saliency_sums_kernel(const uint16_t* __re
 
 // tau[g] = the k-th smallest of s[g*T .. g*T + T) (nearest rank), found exactly: non-negative
 // doubles order like their uint64 bit patterns, so a radix select over eight 8-bit digits from
-// the top, one block per group.
-__global__ __launch_bounds__(1024) void saliency_select_kernel(const double* __restrict__ s, int64_t T, int64_t k,
-                                                               double* __restrict__ tau) {
-    __shared__ uint32_t hist[256];
-    __shared__ unsigned long long prefix;
-    __shared__ long long krem;
-    const double* v = s + (int64_t)blockIdx.x * T;
+// the top.  Each digit takes two launches: SEL_SPLIT blocks per group count the values that
+// match the prefix found so far into a global histogram (LDS histogram per block, then one
+// global add per nonzero bin), and one block per group picks the digit where the running
+// count reaches the remaining rank and clears the histogram for the next digit.
+constexpr int SEL_SPLIT = 64;
+struct SelState {
+    unsigned long long prefix;
+    long long krem;
+};
+__global__ __launch_bounds__(256) void select_init_kernel(SelState* st, uint32_t* hist, int64_t ng, int64_t k) {
+    const int64_t g = blockIdx.x;
     if (threadIdx.x == 0) {
-        prefix = 0ull;
-        krem = k;
+        st[g].prefix = 0ull;
+        st[g].krem = k;
     }
-    for (int pass = 0; pass < 8; ++pass) {
-        const int shift = 56 - 8 * pass;
-        if (threadIdx.x < 256) hist[threadIdx.x] = 0u;
-        __syncthreads();
-        const unsigned long long pre = prefix;
-        for (int64_t t = threadIdx.x; t < T; t += 1024) {
-            const unsigned long long u = (unsigned long long)__double_as_longlong(v[t]);
-            // digits above this pass must match the prefix found so far
-            if (pass == 0 || (u >> (shift + 8)) == pre) atomicAdd(&hist[(u >> shift) & 255ull], 1u);
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            long long need = krem, acc = 0;
-            unsigned bin = 255u;
-            for (unsigned b = 0; b < 256u; ++b) {
-                const long long h = hist[b];
-                if (acc + h >= need) {
-                    bin = b;
-                    break;
-                }
-                acc += h;
+    hist[g * 256 + threadIdx.x] = 0u;
+    (void)ng;
+}
+__global__ __launch_bounds__(256) void select_count_kernel(const double* __restrict__ s, int64_t T, int pass,
+                                                           const SelState* __restrict__ st, uint32_t* hist) {
+    __shared__ uint32_t h[256];
+    const int64_t g = blockIdx.x / SEL_SPLIT, part = blockIdx.x % SEL_SPLIT;
+    const int64_t per = (T + SEL_SPLIT - 1) / SEL_SPLIT;
+    const int64_t t0 = part * per, t1 = t0 + per < T ? t0 + per : T;
+    const int shift = 56 - 8 * pass;
+    const unsigned long long pre = st[g].prefix;
+    h[threadIdx.x] = 0u;
+    __syncthreads();
+    const double* v = s + g * T;
+    for (int64_t t = t0 + threadIdx.x; t < t1; t += 256) {
+        const unsigned long long u = (unsigned long long)__double_as_longlong(v[t]);
+        if (pass == 0 || (u >> (shift + 8)) == pre) atomicAdd(&h[(u >> shift) & 255ull], 1u);
+    }
+    __syncthreads();
+    const uint32_t c = h[threadIdx.x];
+    if (c) atomicAdd(&hist[g * 256 + threadIdx.x], c);
+}
+__global__ __launch_bounds__(256) void select_pick_kernel(SelState* st, uint32_t* hist, double* tau, int last) {
+    __shared__ uint32_t h[256];
+    const int64_t g = blockIdx.x;
+    h[threadIdx.x] = hist[g * 256 + threadIdx.x];
+    hist[g * 256 + threadIdx.x] = 0u;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const long long need = st[g].krem;
+        long long acc = 0;
+        unsigned bin = 255u;
+        for (unsigned b = 0; b < 256u; ++b) {
+            if (acc + (long long)h[b] >= need) {
+                bin = b;
+                break;
             }
-            krem = need - acc;
-            prefix = (prefix << 8) | bin;
+            acc += h[b];
         }
-        __syncthreads();
+        st[g].krem = need - acc;
+        st[g].prefix = (st[g].prefix << 8) | bin;
+        if (last) tau[g] = __longlong_as_double((long long)st[g].prefix);
     }
-    if (threadIdx.x == 0) tau[blockIdx.x] = __longlong_as_double((long long)prefix);
 }
 
 // out[e] = float(min(s[e], tau[e / T])) for e < live (tau NULL: no clip); out[e] = 0 for the rows
@@ -99,7 +133,7 @@ __global__ __launch_bounds__(256) void saliency_apply_kernel(const double* __res
 }
 
 hipError_t saliency(const uint16_t* G, int64_t T, int64_t m, int64_t n_groups, int64_t k, double* s64, double* tau,
-                    float* out, hipStream_t st) {
+                    void* sel, float* out, hipStream_t st) {
     if (T <= 0 || m <= 0 || n_groups <= 0) return hipSuccess;
     const int64_t r = (m + n_groups - 1) / n_groups;
     const int64_t ng = (m + r - 1) / r;  // groups that hold at least one row
@@ -110,7 +144,15 @@ hipError_t saliency(const uint16_t* G, int64_t T, int64_t m, int64_t n_groups, i
     if (e != hipSuccess) return e;
     if (k > 0) {
         if (k > T) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(saliency_select_kernel, dim3((unsigned)ng), dim3(1024), 0, st, s64, T, k, tau);
+        SelState* ss = reinterpret_cast<SelState*>(sel);
+        uint32_t* hist = reinterpret_cast<uint32_t*>(ss + ng);
+        hipLaunchKernelGGL(select_init_kernel, dim3((unsigned)ng), dim3(256), 0, st, ss, hist, ng, k);
+        for (int pass = 0; pass < 8; ++pass) {
+            hipLaunchKernelGGL(select_count_kernel, dim3((unsigned)(ng * SEL_SPLIT)), dim3(256), 0, st, s64, T, pass,
+                               ss, hist);
+            hipLaunchKernelGGL(select_pick_kernel, dim3((unsigned)ng), dim3(256), 0, st, ss, hist, tau,
+                               pass == 7 ? 1 : 0);
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(saliency_apply_kernel, dim3(APPLY_SAL_BLOCKS), dim3(256), 0, st, s64, T, items, T * n_groups,
@@ -132,5 +174,7 @@ hipError_t div_narrow(const double* a, double d, float* out, int64_t count, hipS
                        count);
     return hipGetLastError();
 }
+
+int64_t saliency_select_bytes(int64_t n_groups) { return n_groups * (int64_t)(sizeof(SelState) + 256 * 4); }
 
 }  // namespace realq
