@@ -362,7 +362,8 @@ class LayerResult:
 def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams] = None,
                    steps: int = 0, lr: float = 1e-3, window: Optional[Tuple[int, int]] = None,
                    keep_E: bool = False, batch: Optional[int] = None,
-                   loss_clip: Optional[float] = None, s_groups: Optional[np.ndarray] = None) -> LayerResult:
+                   loss_clip: Optional[float] = None, s_groups: Optional[np.ndarray] = None,
+                   grad_fn=None, loss_fn=None) -> LayerResult:
     """The per-module REAL-Q sweep (Alg. 1, one linear module), in float64.
 
     W0 [m, n]; X, Xhat [T, n]; s [T] or None; M [m, m] or None (identity);
@@ -377,6 +378,10 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     (and its own damping, dead columns and inverse factor) instead of the one built from ``s``;
     ``s`` keeps weighting the tokens of the BGD surrogate.  H, U and dead of the result are
     then lists over the groups.
+    ``grad_fn(W, J, alpha) -> (loss, grad of W[:, J])`` replaces the module-output surrogate
+    of every BGD step (a surrogate evaluated further downstream, e.g. at a transformer block's
+    output), and ``loss_fn(W)`` the final loss; X and the surrogate arguments are then unused
+    and the Hessian still comes from Xhat.
     """
     qp = qp or QParams()
     W0 = np.asarray(W0, dtype=np.float64)
@@ -451,6 +456,11 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
             J = slice(c1, n)
             for k in range(steps):
                 t += 1
+                if grad_fn is not None:
+                    lv, G = grad_fn(W, J, alpha)
+                    trace.append((b, k, lv))
+                    W[:, J], mA[:, J], vA[:, J] = adam_update(W[:, J], G, mA[:, J], vA[:, J], t, lr)
+                    continue
                 sl = minibatch(t, T, batch)
                 Tb = sl.stop - sl.start
                 sb = None if s is None else s[sl]
@@ -464,8 +474,10 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
                     G = clipped_grad(R, c, sb, Ma, Xhat[sl, J], Tb)
                 W[:, J], mA[:, J], vA[:, J] = adam_update(W[:, J], G, mA[:, J], vA[:, J], t, lr)
 
-    R = residual(W, W0, X, Xhat)
-    loss = surrogate_loss(R, s, M, T)
+    if loss_fn is not None:
+        loss = loss_fn(W)
+    else:
+        loss = surrogate_loss(residual(W, W0, X, Xhat), s, M, T)
     one = s_groups is None
     return LayerResult(codes=codes, scales=scales, zeros=zeros, W_hat=W, H=Hs[0] if one else Hs,
                        U=Us[0] if one else Us, dead=deads[0] if one else deads,
