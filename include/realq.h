@@ -116,7 +116,8 @@ const char* realq_last_error(const realq_ctx* ctx);
  * realq_ctx_kernel_time after the stream has drained.  Names: "hessian",
  * "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init", "gram" (Gram
  * matrices of the input perturbation), "gram_step" (the per-step product of the
- * Gram form), "dense_loss" (final loss with a dense metric), "saliency".
+ * Gram form), "dense_loss" (final loss with a dense metric), "saliency", "block_init" and
+ * "block_step" (realq_mlp_block_sweep: the fixed forwards, one Block-GD step).
  * Returns REALQ_ERR_INVALID_ARG for an unknown name. */
 int realq_ctx_set_timing(realq_ctx* ctx, int enable);
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms);
@@ -313,6 +314,68 @@ typedef struct realq_layer_out {
 /* Synchronises the stream (after the inverse factor, and at the end to read the
  * final loss).  Returns the first error of any stage. */
 int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* desc, realq_layer_out* out);
+
+/* ------------------------------------------------------------------ NEXT: block-output surrogate
+ * Sec. 4.2-4.4 put the Block-GD surrogate at the transformer block's output (Eq. fisher_loss),
+ * take its gradient through a forward and backward pass of the block, and blend in the next
+ * block over the column blocks of all modules of the block (Eq. slide_window).  For the MLP
+ * half of a pre-norm decoder block
+ *     u = bf16(rmsnorm(h) * gamma),  z = bf16(silu(u Wg^T) * (u Wu^T)),  y = h + bf16(z Wd^T)
+ * (rmsnorm(h) = h / sqrt(mean h^2 + eps); products accumulated in float32 from bf16 hi/lo
+ * weights; normalisation and SwiGLU in float64 before the bf16 rounding; y float32),
+ * realq_mlp_block_sweep quantizes gate, up and down in that order (Alg. 1).  Each module gets
+ * GPTQ on its own input in the quantized path (u for gate and up; z with the quantized gate
+ * and up for down) and, after every column block but its last, `bgd.steps` Adam steps
+ * (Eq. block_gd_update) on its trailing columns against
+ *     L = (1/2T) sum_t (y_t - y*_t)^T F (y_t - y*_t),
+ * y* the full-precision block on X, y the partially quantized block on Xhat, the gradient
+ * taken through the block with the bf16 roundings as the identity.  With window != 0 and a
+ * next block, column block b_global (gate's blocks, then up's, then down's; B_total in all)
+ * descends alpha L + (1 - alpha) L_next with alpha of Eq. slide_window and L_next the next
+ * block's loss on y against the next block applied to y*.  Attention is not part of the block.
+ *   X, Xhat   : [T, d] bf16 block inputs of the full-precision and the quantized model
+ *   gamma     : [d] float32;  Wg, Wu: [f, d] float32;  Wd: [d, f] float32 (original weights)
+ *   F         : [d, d] float32 symmetric Fisher at the block output, or NULL (identity)
+ *   next      : the next block, same shapes; next.Wg == NULL when there is none
+ *   q         : quantizer as for realq_quantize_layer (group = 0: one group per row)
+ *   bgd       : steps, lr and the Adam constants; form, loss_clip and batch must be 0
+ * Outputs per module (0 gate, 1 up, 2 down): codes [rows, cols] (gate, up: [f, d]; down:
+ * [d, f]), scales and zeros [rows, ceil(cols/group)], W_hat [rows, cols] float32 (all
+ * required); loss_trace [B_total * steps] device float64, entry (b_global - 1) * steps + k,
+ * NaN for the last column block of each module, or NULL; loss_final (host) = L at the
+ * quantized weights; ms_total (host).  Needs d, f >= 1, T >= 1, d and f multiples of 8.
+ * Synchronises the stream (after each inverse factor and at the end). */
+typedef struct realq_mlp_block {
+    const float* gamma;
+    const float* Wg;
+    const float* Wu;
+    const float* Wd;
+    const float* F;
+} realq_mlp_block;
+
+typedef struct realq_mlp_desc {
+    int64_t T, d, f;
+    const uint16_t* X;
+    const uint16_t* Xhat;
+    realq_mlp_block blk;
+    realq_mlp_block next;
+    float eps;
+    int32_t window;
+    realq_qparams q;
+    realq_bgd_params bgd;
+} realq_mlp_desc;
+
+typedef struct realq_mlp_out {
+    uint8_t* codes[3];
+    float* scales[3];
+    uint8_t* zeros[3];
+    float* W_hat[3];
+    double* loss_trace;
+    double loss_final;
+    double ms_total;
+} realq_mlp_out;
+
+int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* desc, realq_mlp_out* out);
 
 #ifdef __cplusplus
 }

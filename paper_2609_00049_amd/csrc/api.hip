@@ -11,35 +11,9 @@
 #include <vector>
 
 #include "common.h"
+#include "ctx.h"
 #include "kernels.h"
 #include "../../include/realq.h"
-
-// ============================================================================ context
-
-struct realq_ctx {
-    hipStream_t stream = nullptr;
-    int device = 0;
-    std::string err;
-    // grow-only workspaces, by slot name
-    struct Buf {
-        void* p = nullptr;
-        size_t bytes = 0;
-    };
-    std::map<std::string, Buf> ws;
-    // kernel timing
-    bool timing = false;
-    struct Stat {
-        int64_t launches = 0;
-        double ms = 0.0;
-    };
-    std::map<std::string, Stat> stats;
-    struct Pending {
-        std::string name;
-        hipEvent_t a, b;
-    };
-    std::vector<Pending> pending;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> free_events;
-};
 
 namespace realq {
 
@@ -48,7 +22,7 @@ int set_error(realq_ctx* ctx, int code, const std::string& msg) {
     return code;
 }
 
-static int get_ws(realq_ctx* ctx, const char* slot, size_t bytes, void** out) {
+int get_ws(realq_ctx* ctx, const char* slot, size_t bytes, void** out) {
     auto& b = ctx->ws[slot];
     if (bytes == 0) bytes = 16;
     if (b.bytes < bytes) {
@@ -72,33 +46,7 @@ static int get_ws(realq_ctx* ctx, const char* slot, size_t bytes, void** out) {
     return REALQ_OK;
 }
 
-// RAII-free timing helper: begin/end bracket a launch on the context stream.
-struct Timed {
-    realq_ctx* ctx;
-    const char* name;
-    hipEvent_t a = nullptr, b = nullptr;
-    Timed(realq_ctx* c, const char* n) : ctx(c), name(n) {
-        if (!ctx->timing) return;
-        if (!ctx->free_events.empty()) {
-            a = ctx->free_events.back().first;
-            b = ctx->free_events.back().second;
-            ctx->free_events.pop_back();
-        } else {
-            if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
-                a = b = nullptr;
-                return;
-            }
-        }
-        (void)hipEventRecord(a, ctx->stream);
-    }
-    ~Timed() {
-        if (!a) return;
-        (void)hipEventRecord(b, ctx->stream);
-        ctx->pending.push_back({name, a, b});
-    }
-};
-
-static int harvest(realq_ctx* ctx) {
+int harvest(realq_ctx* ctx) {
     if (ctx->pending.empty()) return REALQ_OK;
     RQ_HIP(ctx, hipEventSynchronize(ctx->pending.back().b));
     for (auto& p : ctx->pending) {
@@ -116,6 +64,8 @@ static int harvest(realq_ctx* ctx) {
 }  // namespace realq
 
 using realq::get_ws;
+using realq::validate_bgd;
+using realq::validate_q;
 using realq::set_error;
 using realq::Timed;
 
@@ -220,7 +170,7 @@ int realq_ctx_set_timing(realq_ctx* ctx, int enable) {
 
 static const char* kTimedNames[] = {"hessian", "chol",  "quantize",  "obs",        "lock",      "resid",
                                     "grad",    "adam",  "init",      "gram",       "gram_step", "dense_loss",
-                                    "saliency"};
+                                    "saliency", "block_init", "block_step"};
 
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms) {
     if (!ctx || !name) return REALQ_ERR_INVALID_ARG;
@@ -432,7 +382,8 @@ static int gram_accum(realq_ctx* ctx, const uint16_t* Xhat, const uint16_t* X, c
     return REALQ_OK;
 }
 
-static int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
+extern "C++" {
+int realq::validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
     if (!p) return set_error(ctx, REALQ_ERR_INVALID_ARG, "NULL bgd params");
     if (p->steps < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd steps must be >= 0");
     if (!std::isfinite(p->lr) || p->lr < 0.f) return set_error(ctx, REALQ_ERR_INVALID_ARG, "lr must be finite, >= 0");
@@ -447,6 +398,7 @@ static int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
     if (p->batch < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "batch must be >= 0");
     return REALQ_OK;
 }
+}  // extern "C++"
 
 static int state_init_gram(realq_bgd_state* st);
 
@@ -654,7 +606,8 @@ void realq_bgd_state_destroy(realq_bgd_state* st) {
 
 // ============================================================================ a3-a6: one column block
 
-static int validate_q(realq_ctx* ctx, const realq_qparams* qp) {
+extern "C++" {
+int realq::validate_q(realq_ctx* ctx, const realq_qparams* qp) {
     if (!qp) return set_error(ctx, REALQ_ERR_INVALID_ARG, "NULL qparams");
     if (qp->bits < 2 || qp->bits > 4) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bits must be 2, 3 or 4");
     if (qp->group < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "group must be >= 1, or 0 for one group per row");
@@ -667,6 +620,7 @@ static int validate_q(realq_ctx* ctx, const realq_qparams* qp) {
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "damp must be finite and > 0");
     return REALQ_OK;
 }
+}  // extern "C++"
 
 // Rows [r0, r1) of one column block: search, quantize and compensate inside the block, then the
 // trailing update; with a state, its copy of W - W0 follows on those rows.

@@ -1,0 +1,78 @@
+// Internal context of the REAL-Q library (not part of the C ABI): the stream, grow-only
+// workspaces by slot name, and the optional per-kernel timing that realq_ctx_kernel_time reads.
+#pragma once
+#include <map>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+struct realq_ctx {
+    hipStream_t stream = nullptr;
+    int device = 0;
+    std::string err;
+    // grow-only workspaces, by slot name
+    struct Buf {
+        void* p = nullptr;
+        size_t bytes = 0;
+    };
+    std::map<std::string, Buf> ws;
+    // kernel timing
+    bool timing = false;
+    struct Stat {
+        int64_t launches = 0;
+        double ms = 0.0;
+    };
+    std::map<std::string, Stat> stats;
+    struct Pending {
+        std::string name;
+        hipEvent_t a, b;
+    };
+    std::vector<Pending> pending;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> free_events;
+};
+
+namespace realq {
+
+// Device buffer of at least `bytes` for `slot` (grown by synchronising the stream and
+// reallocating; contents are not kept across growth).
+int get_ws(realq_ctx* ctx, const char* slot, size_t bytes, void** out);
+// Folds finished timing events into ctx->stats (synchronises on the last one).
+int harvest(realq_ctx* ctx);
+}  // namespace realq
+
+struct realq_qparams;
+struct realq_bgd_params;
+
+namespace realq {
+// Argument checks shared by the entry points (REALQ_OK or an error set on ctx).
+int validate_q(realq_ctx* ctx, const realq_qparams* qp);
+int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p);
+
+// Brackets the launches of its scope with events on the context stream when timing is on.
+struct Timed {
+    realq_ctx* ctx;
+    const char* name;
+    hipEvent_t a = nullptr, b = nullptr;
+    Timed(realq_ctx* c, const char* n) : ctx(c), name(n) {
+        if (!ctx->timing) return;
+        if (!ctx->free_events.empty()) {
+            a = ctx->free_events.back().first;
+            b = ctx->free_events.back().second;
+            ctx->free_events.pop_back();
+        } else {
+            if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+                a = b = nullptr;
+                return;
+            }
+        }
+        (void)hipEventRecord(a, ctx->stream);
+    }
+    ~Timed() {
+        if (!a) return;
+        (void)hipEventRecord(b, ctx->stream);
+        ctx->pending.push_back({name, a, b});
+    }
+};
+
+}  // namespace realq

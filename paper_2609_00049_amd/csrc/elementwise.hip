@@ -389,6 +389,7 @@ __device__ __forceinline__ void adam_elem(const AdamArgs& a, int64_t i, int64_t 
     float vh = vv * a.bc2;
     const double w = a.W[idx] - (double)(a.lr * mh / (sqrtf(vh) + a.eps));
     a.W[idx] = w;
+    if (!a.Dhi) return;
     uint16_t h, l;
     split_bf16((float)(w - (double)a.W0[idx]), h, l);
     a.Dhi[idx] = h;

@@ -83,7 +83,8 @@ hipError_t split_diff_bf16(const uint16_t* a, const uint16_t* b, uint16_t* hi, u
                            hipStream_t st);
 // out = sum of partials (fixed order) * scale, written to *out (device)
 hipError_t reduce_partials(const double* partials, int64_t count, double scale, double* out, hipStream_t st);
-// Adam on W[:, c1:n] with G = gscale * sum_z Gp[z][i][j - c1]; refreshes Dhi/Dlo = split(W - W0) there.
+// Adam on W[:, c1:n] with G = gscale * sum_z Gp[z][i][j - c1]; refreshes Dhi/Dlo = split(W - W0) there
+// (skipped when Dhi is NULL).
 struct AdamArgs {
     double* W;
     const float* W0;
@@ -143,6 +144,36 @@ hipError_t saliency(const uint16_t* G, int64_t T, int64_t m, int64_t n_groups, i
 int64_t saliency_select_bytes(int64_t n_groups);
 // out[e] = float(a[e] / d)
 hipError_t div_narrow(const double* a, double d, float* out, int64_t count, hipStream_t st);
+
+// ---------------------------------------------------------------- block-output surrogate (MLP block)
+// u[t, :] = bf16(h[t, :] gamma / sqrt(mean h[t, :]^2 + eps)) (statistics in float64)
+hipError_t rmsnorm_bf16(const uint16_t* h, int64_t T, int64_t d, const float* gamma, double eps, uint16_t* u,
+                        hipStream_t st);
+hipError_t rmsnorm_f32(const float* h, int64_t T, int64_t d, const float* gamma, double eps, uint16_t* u,
+                       hipStream_t st);
+// z = bf16(silu(a) b) elementwise
+hipError_t swiglu_fwd(const float* a, const float* b, uint16_t* z, int64_t count, hipStream_t st);
+// y = h + out, dy = y - ystar (y, dy may be NULL)
+hipError_t residual_out_bf16(const uint16_t* h, const uint16_t* out, const float* ystar, float* y, float* dy,
+                             int64_t count, hipStream_t st);
+hipError_t residual_out_f32(const float* h, const uint16_t* out, const float* ystar, float* y, float* dy,
+                            int64_t count, hipStream_t st);
+// out = s x (out may be NULL), hi/lo = split(s x) (may be NULL)
+hipError_t scale_split(const float* x, float s, float* out, uint16_t* hi, uint16_t* lo, int64_t count,
+                       hipStream_t st);
+// partials[0 .. dot_f32_partials()) = scale * fixed-order partial sums of x . y
+hipError_t dot_f32(const float* x, const float* y, int64_t count, double scale, double* partials, hipStream_t st);
+int64_t dot_f32_partials();
+// SwiGLU backward to the gate (which 0) or up (which 1) input from dz [T, f], split to hi/lo,
+// transposed ([f][ldo]) or row-major ([T][ldo])
+hipError_t swiglu_bwd(const float* dz, const float* a, const float* b, int which, int64_t T, int64_t f,
+                      int transposed, uint16_t* hi, uint16_t* lo, int64_t ldo, hipStream_t st);
+// hi/lo[c * ldo + r] = split(in[r * ldi + c])
+hipError_t transpose_split_f32(const float* in, int64_t ldi, uint16_t* hi, uint16_t* lo, int64_t ldo, int64_t rows,
+                               int64_t cols, hipStream_t st);
+// g = alpha g + (1 - alpha) (g2 + RMSNorm backward of du at h)
+hipError_t rmsnorm_bwd_blend(const float* h, const float* g2, const float* du, const float* gamma, double eps,
+                             double alpha, int64_t T, int64_t d, float* g, hipStream_t st);
 
 // ---------------------------------------------------------------- quantize one column block
 struct QuantArgs {

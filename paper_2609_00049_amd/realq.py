@@ -36,7 +36,7 @@ EXPORTS = [
     "realq_bgd_state_create", "realq_bgd_state_destroy",
     "realq_quantize_block", "realq_quantize_block_rows", "realq_bgd_lock_block",
     "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
-    "realq_pullback_metric", "realq_handoff",
+    "realq_pullback_metric", "realq_handoff", "realq_mlp_block_sweep",
 ]
 
 
@@ -79,6 +79,23 @@ class LayerOut(ctypes.Structure):
                 ("loss_final", ctypes.c_double), ("ms_total", ctypes.c_double)]
 
 
+class MLPBlock(ctypes.Structure):
+    _fields_ = [("gamma", ctypes.c_void_p), ("Wg", ctypes.c_void_p), ("Wu", ctypes.c_void_p),
+                ("Wd", ctypes.c_void_p), ("F", ctypes.c_void_p)]
+
+
+class MLPDesc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int64), ("d", ctypes.c_int64), ("f", ctypes.c_int64),
+                ("X", ctypes.c_void_p), ("Xhat", ctypes.c_void_p), ("blk", MLPBlock), ("next", MLPBlock),
+                ("eps", ctypes.c_float), ("window", ctypes.c_int32), ("q", QParams), ("bgd", BgdParams)]
+
+
+class MLPOut(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p * 3), ("scales", ctypes.c_void_p * 3), ("zeros", ctypes.c_void_p * 3),
+                ("W_hat", ctypes.c_void_p * 3), ("loss_trace", ctypes.c_void_p),
+                ("loss_final", ctypes.c_double), ("ms_total", ctypes.c_double)]
+
+
 def _load():
     if not _LIB_PATH.exists():
         raise ImportError(f"{_LIB_PATH} is not built; run paper_2609_00049_amd.build.build() first")
@@ -112,6 +129,7 @@ def _load():
         "realq_quantize_layer": (ctypes.c_int, [vp, ctypes.POINTER(LayerDesc), ctypes.POINTER(LayerOut)]),
         "realq_pullback_metric": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int, vp]),
         "realq_handoff": (ctypes.c_int, [vp, vp, vp, vp, i64, i64, i64, vp]),
+        "realq_mlp_block_sweep": (ctypes.c_int, [vp, ctypes.POINTER(MLPDesc), ctypes.POINTER(MLPOut)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -358,3 +376,54 @@ def quantize_layer(ctx: Context, W0, X, Xhat, s=None, M=None, P=None, *, qp: Opt
     out.loss_final = lo.loss_final
     out.ms_total = lo.ms_total
     return out
+
+
+# ----------------------------------------------------------------------------- block-output surrogate
+
+MLP_MODULES = ("gate", "up", "down")
+
+
+@dataclass
+class BlockResult:
+    modules: dict            # name -> LayerResult (codes, scales, zeros, W_hat; the rest None)
+    loss_trace: Optional[torch.Tensor]
+    loss_final: float
+    ms_total: float
+
+
+def _mlp_block(gamma, Wg, Wu, Wd, F=None) -> MLPBlock:
+    return MLPBlock(_ptr(gamma), _ptr(Wg), _ptr(Wu), _ptr(Wd), _ptr(F))
+
+
+def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, *, eps=1e-6, window=False,
+                    qp: Optional[QParams] = None, bgd: Optional[BgdParams] = None, want_trace=True) -> BlockResult:
+    """Quantize gate, up and down of one pre-norm SwiGLU MLP block with Block-GD on the block-output
+    surrogate.  X, Xhat [T, d] bf16; gamma [d]; Wg, Wu [f, d]; Wd [d, f]; F [d, d] or None;
+    nxt = (gamma, Wg, Wu, Wd, F) of the next block or None."""
+    qp = qp or qparams()
+    bgd = bgd or bgd_params()
+    T, d = X.shape
+    f = Wg.shape[0]
+    dev = X.device
+    nb = [-(-d // qp.block), -(-d // qp.block), -(-f // qp.block)]
+    mods = {}
+    for name, (rows, cols) in zip(MLP_MODULES, ((f, d), (f, d), (d, f))):
+        ng = -(-cols // (qp.group or cols))
+        mods[name] = LayerResult(codes=torch.empty((rows, cols), dtype=torch.uint8, device=dev),
+                                 scales=torch.empty((rows, ng), dtype=torch.float32, device=dev),
+                                 zeros=torch.empty((rows, ng), dtype=torch.uint8, device=dev),
+                                 W_hat=torch.empty((rows, cols), dtype=torch.float32, device=dev),
+                                 H=None, U=None, dead=None, loss_trace=None, loss_final=math.nan, ms_total=math.nan)
+    trace = torch.empty((max(1, sum(nb) * bgd.steps),), dtype=torch.float64, device=dev) if want_trace else None
+    nx = _mlp_block(*nxt) if nxt is not None else MLPBlock()
+    desc = MLPDesc(T, d, f, _ptr(_bits(X)), _ptr(_bits(Xhat)), _mlp_block(gamma, Wg, Wu, Wd, F), nx, eps,
+                   int(bool(window)), qp, bgd)
+    o = MLPOut()
+    for k, name in enumerate(MLP_MODULES):
+        o.codes[k] = _ptr(mods[name].codes)
+        o.scales[k] = _ptr(mods[name].scales)
+        o.zeros[k] = _ptr(mods[name].zeros)
+        o.W_hat[k] = _ptr(mods[name].W_hat)
+    o.loss_trace = _ptr(trace)
+    ctx.check(_lib.realq_mlp_block_sweep(ctx.h, ctypes.byref(desc), ctypes.byref(o)))
+    return BlockResult(modules=mods, loss_trace=trace, loss_final=o.loss_final, ms_total=o.ms_total)

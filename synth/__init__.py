@@ -7,10 +7,12 @@ arithmetic: no Hessian, no quantizer, no compensation, no gradient.
 from .gen import (  # noqa: F401
     CONFIGS,
     LayerInputs,
+    MLPBlockInputs,
     bf16_bits,
     bf16_round,
     bf16_from_bits,
     make_group_weights,
+    make_mlp_block,
     make_module,
     make_output_grads,
     module_names,

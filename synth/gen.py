@@ -193,3 +193,37 @@ def make_group_weights(n_groups: int, T: int, seed: int = 0) -> np.ndarray:
     common = rng.lognormal(0.0, 1.0, size=(1, T))
     own = rng.lognormal(0.0, 0.5, size=(n_groups, T))
     return (common * own).astype(np.float32)
+
+
+# ----------------------------------------------------------------------------- MLP block inputs
+
+@dataclass
+class MLPBlockInputs:
+    X: np.ndarray        # [T, d] bf16-exact float32, block input of the full-precision model
+    Xhat: np.ndarray     # [T, d] bf16-exact float32, block input of the quantized model
+    gamma: np.ndarray    # [d] float32 RMSNorm weight
+    Wg: np.ndarray       # [f, d] bf16-exact float32
+    Wu: np.ndarray       # [f, d]
+    Wd: np.ndarray       # [d, f]
+    F: Optional[np.ndarray]   # [d, d] float32 Wishart metric at the block output, or None
+
+
+def make_mlp_block(T: int, d: int, f: int, seed: int = 0, dense_F: bool = True, wstd: float = 0.02,
+                   xhat_rel: float = 0.01) -> MLPBlockInputs:
+    """One pre-norm SwiGLU MLP block with its calibration inputs: Student-t (nu = 4) block inputs
+    with four outlier channels x 10, Xhat = X (1 + xhat_rel xi), gamma = 1 + 0.1 N(0, 1), bf16
+    N(0, wstd^2) weights, and a Wishart (2d degrees of freedom) metric at the block output."""
+    rng = np.random.default_rng(seed * 1000 + 950)
+    X32 = rng.standard_t(4.0, size=(T, d)).astype(np.float32)
+    idx = rng.choice(d, size=min(4, d), replace=False)
+    X32[:, idx] *= np.float32(10.0)
+    Xh32 = X32 * (np.float32(1.0) + np.float32(xhat_rel) * rng.standard_normal((T, d), dtype=np.float32))
+    gamma = (1.0 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+    Wg = bf16_round(rng.standard_normal((f, d), dtype=np.float32) * np.float32(wstd))
+    Wu = bf16_round(rng.standard_normal((f, d), dtype=np.float32) * np.float32(wstd))
+    Wd = bf16_round(rng.standard_normal((d, f), dtype=np.float32) * np.float32(wstd))
+    F = None
+    if dense_F:
+        A = rng.standard_normal((d, 2 * d), dtype=np.float32)
+        F = (A @ A.T) / np.float32(2 * d)
+    return MLPBlockInputs(X=bf16_round(X32), Xhat=bf16_round(Xh32), gamma=gamma, Wg=Wg, Wu=Wu, Wd=Wd, F=F)

@@ -41,7 +41,8 @@ def test_binding_structs_match_the_c_layout(tmp_path):
     lays them out, against the ctypes mirrors of the binding."""
     from paper_2609_00049_amd import realq
     structs = {"realq_qparams": realq.QParams, "realq_bgd_params": realq.BgdParams,
-               "realq_layer_desc": realq.LayerDesc, "realq_layer_out": realq.LayerOut}
+               "realq_layer_desc": realq.LayerDesc, "realq_layer_out": realq.LayerOut,
+               "realq_mlp_block": realq.MLPBlock, "realq_mlp_desc": realq.MLPDesc, "realq_mlp_out": realq.MLPOut}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "realq.h"', 'int main(void) {']
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
