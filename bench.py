@@ -164,6 +164,56 @@ def stage0(torch, rq, ctx, W0, X, Xh, s, qp, bgd, m, n, T, n_groups=4, fisher_to
     return out
 
 
+def block_f_alg(T, d, f, block, steps, window, dense):
+    """Algorithmic FLOPs of the Block-GD steps of realq_mlp_block_sweep (the block forward, the
+    surrogate and the backward to one module's trailing columns; the next block's forward and
+    backward when the window blends it in)."""
+    tdf, tdd = 2.0 * T * d * f, 2.0 * T * d * d
+    total = 0.0
+    for mod, (rows, cols) in enumerate(((f, d), (f, d), (d, f))):
+        nb = -(-cols // block)
+        for b in range(nb - 1):
+            nJ = cols - (b + 1) * block
+            per = (tdf if mod < 2 else 0.0) + tdf + (tdd if dense else 0.0)   # a or b; out; F dy
+            per += (tdf if mod < 2 else 0.0) + 2.0 * rows * nJ * T             # dz = g Wd; gradient
+            if window:
+                per += 3 * tdf + (tdd if dense else 0.0) + tdf + 2 * tdf        # next block fwd, F, dz2, du2
+            total += steps * per
+    return total
+
+
+def mlp_block(torch, rq, ctx, qp, T=8192, d=4096, f=14336, steps=8, lr=1e-5):
+    """The block-output surrogate sweep of a LLaMA-3.1-8B-shaped MLP block (d 4096, f 14336) on
+    8192 tokens with a dense 4096 x 4096 block-output metric and the next block blended in."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(77)
+
+    def w(shape, std=0.02):
+        return (torch.randn(shape, generator=g, device="cuda") * std).to(torch.bfloat16).float().contiguous()
+
+    def metric():
+        A = torch.randn((d, 2 * d), generator=g, device="cuda")
+        return (A @ A.T / (2 * d)).contiguous()
+
+    X = (torch.randn((T, d), generator=g, device="cuda")).to(torch.bfloat16).contiguous()
+    Xh = (X.float() * (1 + 0.01 * torch.randn((T, d), generator=g, device="cuda"))).to(torch.bfloat16).contiguous()
+    gamma = (1 + 0.1 * torch.randn((d,), generator=g, device="cuda")).contiguous()
+    blk = (gamma, w((f, d)), w((f, d)), w((d, f)), metric())
+    nxt = ((1 + 0.1 * torch.randn((d,), generator=g, device="cuda")).contiguous(), w((f, d)), w((f, d)),
+           w((d, f)), metric())
+    bgd = rq.bgd_params(steps=steps, lr=lr)
+    ctx.reset_timing()
+    r = rq.mlp_block_sweep(ctx, X, Xh, *blk, nxt, window=True, qp=qp, bgd=bgd)
+    nst, st_ms = ctx.kernel_time("block_step")
+    fl = block_f_alg(T, d, f, qp.block, steps, True, True)
+    print(f"[bench] mlp block sweep: {r.ms_total:.1f} ms, loss {r.loss_final:.6g}", file=sys.stderr, flush=True)
+    return {"tokens": T, "d": d, "f": f, "bgd_steps": steps, "window": True, "dense_metric": True,
+            "ms_total": r.ms_total, "loss_final": r.loss_final, "block_steps": nst,
+            "block_step_ms_total": st_ms, "block_step_tflops_alg": fl / (st_ms / 1e3) / 1e12 if st_ms > 0 else None,
+            "frac_bf16_peak_alg": fl / (st_ms / 1e3) / PEAK_BF16 if st_ms > 0 else None,
+            "columns_per_s": (2 * d + f) / (r.ms_total / 1e3)}
+
+
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_00049_amd", "csrc", "gemm_bf16.hip")
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_llama8b_gate_traffic.txt")
 
@@ -207,6 +257,8 @@ def main():
                     help="with --form tokens, skip the extra untimed Gram-form sweep reported under gram_form")
     ap.add_argument("--no-stage0", action="store_true",
                     help="skip the Stage-0 accumulator timings and the N_g = 4 row-group sweep (stage0)")
+    ap.add_argument("--no-block", action="store_true",
+                    help="skip the block-output surrogate sweep of a LLaMA-3.1-8B-shaped MLP block (mlp_block)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs the sweep on one GPU; --gpus {args.gpus} is not supported "
@@ -300,6 +352,10 @@ def main():
                                     "(bench.py --form gram for its own line)"}
     if not args.no_stage0:
         res["stage0"] = stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n, T)
+    if not args.no_block:
+        del W0, X, Xh, s
+        torch.cuda.empty_cache()
+        res["mlp_block"] = mlp_block(torch, rq, ctx, qp)
     ctx.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
