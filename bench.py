@@ -259,6 +259,8 @@ def main():
                     help="skip the Stage-0 accumulator timings and the N_g = 4 row-group sweep (stage0)")
     ap.add_argument("--no-block", action="store_true",
                     help="skip the block-output surrogate sweep of a LLaMA-3.1-8B-shaped MLP block (mlp_block)")
+    ap.add_argument("--only", choices=("stage0", "block"),
+                    help="run only that part (for per-part kernel profiles) and print its object")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs the sweep on one GPU; --gpus {args.gpus} is not supported "
@@ -270,6 +272,11 @@ def main():
 
     torch.cuda.set_device(0)
     cfg, module, m, n, T, K, lr = WORKLOADS[args.workload]
+    if args.only == "block":
+        ctx = rq.Context()
+        ctx.set_timing(True)
+        print(json.dumps({"mlp_block": mlp_block(torch, rq, ctx, rq.qparams())}), flush=True)
+        return
     print(f"[bench] generating {args.workload}: m={m} n={n} T={T} K={K}", file=sys.stderr, flush=True)
     W0, X, Xh, s = make_inputs(torch, args.workload)
     if args.copy_bytes > 0:
@@ -284,6 +291,11 @@ def main():
     qp = rq.qparams()
     form = rq.BGD_GRAM if args.form == "gram" else rq.BGD_TOKENS
     bgd = rq.bgd_params(steps=K, lr=lr, form=form)
+    if args.only == "stage0":
+        ctx.set_timing(True)
+        print(json.dumps({"stage0": stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n,
+                                           T)}), flush=True)
+        return
     out = None
     for w in range(args.warmup):
         out = rq.quantize_layer(ctx, W0, X, Xh, s, qp=qp, bgd=bgd, out=out)
