@@ -24,12 +24,16 @@ above writes bf16; the backward treats those roundings as the identity (a cast's
 the residual stream y stays unrounded; the sliding window's partner is the same MLP block
 structure with its own weights and Fisher applied to y (and y*), so that
 L_slide = alpha L + (1 - alpha) L_next with alpha over b_global = the column blocks of gate,
-then up, then down (Eq. slide_window, B_total = all three modules' column blocks).  Attention
-is not part of this block.
+then up, then down (Eq. slide_window, B_total = all three modules' column blocks).
+
+The full decoder block (decoder_* below) puts the attention half in front: RMSNorm, the q, k, v
+projections, rotary position embedding, causal softmax attention with grouped key/value heads,
+the o projection and the residual add, then the MLP half; its seven modules are quantized in
+the order q, k, v, o, gate, up, down with b_global running over all of them.
 
 Pins: every backward here is checked against central finite differences of the unrounded
 forward (rnd=False), and the down projection's gradient reduces to the module-level surrogate
-gradient with M = F (tests/test_oracle_pins.py).
+gradient with M = F (tests/test_block_oracle_pins.py).
 """
 from __future__ import annotations
 
@@ -206,3 +210,223 @@ def module_surrogate_grad_of_down(z, zstar, Wd, Wd0, F, J):
     the block surrogate meets when the block input is unperturbed and roundings are dropped)."""
     R = _f64(Wd) @ _f64(z).T - _f64(Wd0) @ _f64(zstar).T
     return surrogate_grad(R, None, F, _f64(z)[:, J], _f64(z).shape[0])
+
+
+# ============================================================================ full decoder block
+# The attention half: h1 = bf16(rmsnorm(x) gamma1), q/k/v = bf16(h1 W^T), rotary position
+# embedding on q and k (rotate-half form, positions counted within each sequence of L tokens,
+# rounded to bf16), causal softmax attention per sequence and head with grouped key/value heads
+# (scores and softmax unrounded), O = bf16(P V), x2 = x + bf16(O Wo^T); then the MLP half on x2.
+# Modules in Alg. 1 order: q, k, v, o, gate, up, down.
+
+DECODER_MODULES = ("q", "k", "v", "o", "gate", "up", "down")
+
+
+@dataclass
+class DecoderBlock:
+    gamma1: np.ndarray
+    Wq: np.ndarray          # [H hd, d]
+    Wk: np.ndarray          # [Hkv hd, d]
+    Wv: np.ndarray          # [Hkv hd, d]
+    Wo: np.ndarray          # [d, H hd]
+    gamma2: np.ndarray
+    Wg: np.ndarray
+    Wu: np.ndarray
+    Wd: np.ndarray
+    n_heads: int
+    n_kv: int
+    head_dim: int
+    seq_len: int
+    F: Optional[np.ndarray] = None
+    rope_base: float = 10000.0
+
+    def weights(self):
+        return {"q": self.Wq, "k": self.Wk, "v": self.Wv, "o": self.Wo, "gate": self.Wg, "up": self.Wu,
+                "down": self.Wd}
+
+
+def rope(x, n, hd, L, base=10000.0, inverse=False):
+    """Rotary embedding of x [T, n hd] (n heads of hd), position t mod L; inverse=True applies
+    the transposed rotation (the backward of the forward one)."""
+    x = _f64(x)
+    T = x.shape[0]
+    pos = (np.arange(T) % L).astype(np.float64)
+    inv = base ** (-2.0 * np.arange(hd // 2) / hd)
+    ang = pos[:, None] * inv[None, :]
+    c, s = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+    xr = x.reshape(T, n, hd)
+    x1, x2 = xr[..., :hd // 2], xr[..., hd // 2:]
+    if inverse:
+        s = -s
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1).reshape(T, n * hd)
+
+
+def attention_forward(qr, kr, v, H, Hkv, hd, L):
+    """Causal softmax attention per sequence of L tokens and head; head h reads key/value head
+    h // (H / Hkv).  Returns (O [T, H hd] unrounded, P [T / L, H, L, L])."""
+    T = qr.shape[0]
+    S = T // L
+    rep = H // Hkv
+    O = np.zeros((T, H * hd))
+    P = np.zeros((S, H, L, L))
+    mask = np.triu(np.ones((L, L), dtype=bool), 1)
+    for s in range(S):
+        rows = slice(s * L, (s + 1) * L)
+        for h in range(H):
+            g = h // rep
+            q = qr[rows, h * hd:(h + 1) * hd]
+            k = kr[rows, g * hd:(g + 1) * hd]
+            sc = q @ k.T / np.sqrt(hd)
+            sc[mask] = -np.inf
+            sc = sc - sc.max(axis=1, keepdims=True)
+            e = np.exp(sc)
+            p = e / e.sum(axis=1, keepdims=True)
+            P[s, h] = p
+            O[rows, h * hd:(h + 1) * hd] = p @ v[rows, g * hd:(g + 1) * hd]
+    return O, P
+
+
+def attention_backward(dO, P, qr, kr, v, H, Hkv, hd, L):
+    """(dqr, dkr, dv) from dO [T, H hd]; key/value gradients summed over the heads that share them."""
+    T = qr.shape[0]
+    S = T // L
+    rep = H // Hkv
+    dq = np.zeros_like(qr)
+    dk = np.zeros_like(kr)
+    dv = np.zeros_like(v)
+    for s in range(S):
+        rows = slice(s * L, (s + 1) * L)
+        for h in range(H):
+            g = h // rep
+            p = P[s, h]
+            do = dO[rows, h * hd:(h + 1) * hd]
+            vv = v[rows, g * hd:(g + 1) * hd]
+            dp = do @ vv.T
+            ds = p * (dp - np.sum(p * dp, axis=1, keepdims=True))
+            dq[rows, h * hd:(h + 1) * hd] = ds @ kr[rows, g * hd:(g + 1) * hd] / np.sqrt(hd)
+            dk[rows, g * hd:(g + 1) * hd] += ds.T @ qr[rows, h * hd:(h + 1) * hd] / np.sqrt(hd)
+            dv[rows, g * hd:(g + 1) * hd] += p.T @ do
+    return dq, dk, dv
+
+
+@dataclass
+class DecoderForward:
+    x: np.ndarray
+    h1: np.ndarray
+    q: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+    qr: np.ndarray
+    kr: np.ndarray
+    P: np.ndarray
+    O: np.ndarray       # bf16-rounded attention output [T, H hd] (the o module's input)
+    x2: np.ndarray      # residual stream after attention
+    mlp: MLPForward     # the MLP half on x2 (its y is the block output)
+
+    @property
+    def y(self):
+        return self.mlp.y
+
+
+def decoder_forward(x, blk: DecoderBlock, W=None, eps=RMS_EPS, rnd=True) -> DecoderForward:
+    """Forward of the decoder block; W overrides the module weights (dict by module name)."""
+    r = bf16 if rnd else (lambda a: a)
+    Wm = blk.weights() if W is None else W
+    H, Hkv, hd, L = blk.n_heads, blk.n_kv, blk.head_dim, blk.seq_len
+    x = _f64(x)
+    h1 = r(rmsnorm(x, blk.gamma1, eps))
+    q = r(h1 @ _f64(Wm["q"]).T)
+    k = r(h1 @ _f64(Wm["k"]).T)
+    v = r(h1 @ _f64(Wm["v"]).T)
+    qr = r(rope(q, H, hd, L, blk.rope_base))
+    kr = r(rope(k, Hkv, hd, L, blk.rope_base))
+    Oa, P = attention_forward(qr, kr, v, H, Hkv, hd, L)
+    O = r(Oa)
+    x2 = x + r(O @ _f64(Wm["o"]).T)
+    mlp = mlp_forward(x2, blk.gamma2, Wm["gate"], Wm["up"], Wm["down"], eps, rnd)
+    return DecoderForward(x=x, h1=h1, q=q, k=k, v=v, qr=qr, kr=kr, P=P, O=O, x2=x2, mlp=mlp)
+
+
+def decoder_backward(fw: DecoderForward, gy, blk: DecoderBlock, W=None, eps=RMS_EPS):
+    """Gradients of the surrogate from gy = dL/dy at every module output and at the block input:
+    a dict with 'gate', 'up' (dL/da, dL/db), 'down' (gy), 'o' (dL/dx2), 'q', 'k', 'v' (before the
+    rotary embedding for q and k) and 'x' (dL/dx).  bf16 casts are taken as the identity."""
+    Wm = blk.weights() if W is None else W
+    H, Hkv, hd, L = blk.n_heads, blk.n_kv, blk.head_dim, blk.seq_len
+    gy = _f64(gy)
+    da, db, dx2 = mlp_backward(fw.mlp, gy, blk.gamma2, Wm["gate"], Wm["up"], Wm["down"], eps)
+    dO = dx2 @ _f64(Wm["o"])
+    dqr, dkr, dv = attention_backward(dO, fw.P, fw.qr, fw.kr, fw.v, H, Hkv, hd, L)
+    dq = rope(dqr, H, hd, L, blk.rope_base, inverse=True)
+    dk = rope(dkr, Hkv, hd, L, blk.rope_base, inverse=True)
+    dh1 = dq @ _f64(Wm["q"]) + dk @ _f64(Wm["k"]) + dv @ _f64(Wm["v"])
+    dx = dx2 + rmsnorm_backward(fw.x, blk.gamma1, dh1, eps)
+    return {"gate": da, "up": db, "down": gy, "o": dx2, "q": dq, "k": dk, "v": dv, "x": dx}
+
+
+def decoder_module_grad(which, fw: DecoderForward, bw, J):
+    """Gradient of the surrogate with respect to columns J of one module's weights."""
+    inp = {"q": fw.h1, "k": fw.h1, "v": fw.h1, "o": fw.O, "gate": fw.mlp.u, "up": fw.mlp.u, "down": fw.mlp.z}[which]
+    return bw[which].T @ inp[:, J]
+
+
+def decoder_surrogate(fw: DecoderForward, ystar, blk: DecoderBlock, T, W=None, nxt: Optional[DecoderBlock] = None,
+                      y2star=None, alpha=1.0, eps=RMS_EPS, rnd=True):
+    """(L_slide, backward dict) at the block output; with alpha < 1 the next block's loss on y
+    is blended in and its input gradient enters dL/dy."""
+    dy = fw.y - _f64(ystar)
+    L = fisher_loss(dy, blk.F, T)
+    gy = (dy if blk.F is None else dy @ _f64(blk.F)) / T
+    if nxt is not None and alpha < 1.0:
+        f2 = decoder_forward(fw.y, nxt, None, eps, rnd)
+        dy2 = f2.y - _f64(y2star)
+        L2 = fisher_loss(dy2, nxt.F, T)
+        g2 = (dy2 if nxt.F is None else dy2 @ _f64(nxt.F)) / T
+        dx_next = decoder_backward(f2, g2, nxt, None, eps)["x"]
+        L = alpha * L + (1.0 - alpha) * L2
+        gy = alpha * gy + (1.0 - alpha) * dx_next
+    return L, decoder_backward(fw, gy, blk, W, eps)
+
+
+def decoder_block_sweep(X, Xhat, blk: DecoderBlock, *, qp: Optional[QParams] = None, steps=0, lr=1e-3,
+                        nxt: Optional[DecoderBlock] = None, window=False, eps=RMS_EPS):
+    """Quantize q, k, v, o, gate, up and down of one decoder block in order (Alg. 1): GPTQ on each
+    module's input in the quantized path and Block-GD on the block-output surrogate after every
+    column block; window=True blends in ``nxt`` over b_global across the seven modules."""
+    qp = qp or QParams()
+    X, Xhat = _f64(X), _f64(Xhat)
+    T = X.shape[0]
+    W = {k: _f64(v).copy() for k, v in blk.weights().items()}
+    ystar = decoder_forward(X, blk, W, eps).y
+    y2star = decoder_forward(ystar, nxt, None, eps).y if nxt is not None else None
+    nb = {k: -(-W[k].shape[1] // qp.block) for k in DECODER_MODULES}
+    offset, B_total = {}, 0
+    for k in DECODER_MODULES:
+        offset[k] = B_total
+        B_total += nb[k]
+    inputs = {"q": "h1", "k": "h1", "v": "h1", "o": "O"}
+    res = {}
+    for name in DECODER_MODULES:
+        fw = decoder_forward(Xhat, blk, W, eps)
+        inp = getattr(fw, inputs[name]) if name in inputs else (fw.mlp.u if name != "down" else fw.mlp.z)
+
+        def grad_fn(Wm, J, alpha, name=name):
+            Wc = dict(W)
+            Wc[name] = Wm
+            f = decoder_forward(Xhat, blk, Wc, eps)
+            Lv, bw = decoder_surrogate(f, ystar, blk, T, Wc, nxt, y2star, alpha, eps)
+            return Lv, decoder_module_grad(name, f, bw, J)
+
+        def loss_fn(Wm, name=name):
+            Wc = dict(W)
+            Wc[name] = Wm
+            f = decoder_forward(Xhat, blk, Wc, eps)
+            return fisher_loss(f.y - ystar, blk.F, T)
+
+        r = quantize_layer(W[name], inp, inp, qp=qp, steps=steps, lr=lr,
+                           window=(offset[name], B_total) if (window and nxt is not None) else None,
+                           grad_fn=grad_fn, loss_fn=loss_fn)
+        W[name] = r.W_hat
+        res[name] = r
+    loss = fisher_loss(decoder_forward(Xhat, blk, W, eps).y - ystar, blk.F, T)
+    return BlockResult(modules=res, loss_final=loss, ystar=ystar)

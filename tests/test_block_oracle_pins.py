@@ -137,3 +137,117 @@ def test_sweep_with_bgd_lowers_the_block_surrogate_and_window_off_ignores_the_pa
     # first step of the sweep is b_global = 1: alpha = 1, so the first trace value is unchanged
     assert w.modules["gate"].loss_trace[0][2] == b.modules["gate"].loss_trace[0][2]
     assert w.loss_final != b.loss_final
+
+
+# ============================================================================ full decoder block
+
+def _dec(seed, d=8, f=12, H=2, Hkv=1, hd=4, L=4, dense=True):
+    r = np.random.default_rng(seed)
+    A = r.standard_normal((d, 2 * d))
+    return B.DecoderBlock(gamma1=1 + 0.1 * r.standard_normal(d), Wq=0.4 * r.standard_normal((H * hd, d)),
+                          Wk=0.4 * r.standard_normal((Hkv * hd, d)), Wv=0.4 * r.standard_normal((Hkv * hd, d)),
+                          Wo=0.4 * r.standard_normal((d, H * hd)), gamma2=1 + 0.1 * r.standard_normal(d),
+                          Wg=0.3 * r.standard_normal((f, d)), Wu=0.3 * r.standard_normal((f, d)),
+                          Wd=0.3 * r.standard_normal((d, f)), n_heads=H, n_kv=Hkv, head_dim=hd, seq_len=L,
+                          F=(A @ A.T / (2 * d)) if dense else None)
+
+
+def test_rope_is_a_rotation_and_its_inverse_undoes_it():
+    r = np.random.default_rng(20)
+    x = r.standard_normal((12, 3 * 8))
+    y = B.rope(x, 3, 8, 5)
+    np.testing.assert_allclose(B.rope(y, 3, 8, 5, inverse=True), x, rtol=0, atol=1e-13)
+    # each (i, i + hd/2) pair keeps its length; position 0 is the identity
+    xr, yr = x.reshape(12, 3, 8), y.reshape(12, 3, 8)
+    np.testing.assert_allclose(xr[..., :4] ** 2 + xr[..., 4:] ** 2, yr[..., :4] ** 2 + yr[..., 4:] ** 2, rtol=1e-12)
+    np.testing.assert_allclose(y[0], x[0], rtol=0, atol=0)
+    np.testing.assert_allclose(y[5], x[5], rtol=0, atol=0)        # position 5 mod 5 = 0
+
+
+def test_single_token_sequences_make_attention_the_identity_on_values():
+    r = np.random.default_rng(21)
+    qr, kr, v = r.standard_normal((6, 8)), r.standard_normal((6, 4)), r.standard_normal((6, 4))
+    O, P = B.attention_forward(qr, kr, v, 2, 1, 4, 1)
+    np.testing.assert_allclose(O, np.concatenate([v, v], axis=1), rtol=0, atol=1e-15)
+    assert (P == 1.0).all()
+
+
+def test_attention_backward_matches_finite_differences():
+    r = np.random.default_rng(22)
+    H, Hkv, hd, L = 4, 2, 3, 5
+    T = 2 * L
+    qr, kr, v = r.standard_normal((T, H * hd)), r.standard_normal((T, Hkv * hd)), r.standard_normal((T, Hkv * hd))
+    c = r.standard_normal((T, H * hd))
+    O, P = B.attention_forward(qr, kr, v, H, Hkv, hd, L)
+    dq, dk, dv = B.attention_backward(c, P, qr, kr, v, H, Hkv, hd, L)
+    L_of = lambda a, b, w: float(np.sum(c * B.attention_forward(a, b, w, H, Hkv, hd, L)[0]))
+    for idx in [(0, 0), (3, 5), (9, 11), (7, 2)]:
+        assert dq[idx] == pytest.approx(_fd(lambda x: L_of(x, kr, v), qr, idx), rel=1e-6, abs=1e-10)
+    for idx in [(0, 0), (4, 5), (9, 3), (6, 1)]:
+        assert dk[idx] == pytest.approx(_fd(lambda x: L_of(qr, x, v), kr, idx), rel=1e-6, abs=1e-10)
+        assert dv[idx] == pytest.approx(_fd(lambda x: L_of(qr, kr, x), v, idx), rel=1e-6, abs=1e-10)
+
+
+@pytest.mark.parametrize("which", list(B.DECODER_MODULES))
+@pytest.mark.parametrize("alpha", [1.0, 0.4])
+def test_decoder_module_gradients_match_finite_differences(which, alpha):
+    blk, nxt = _dec(23), _dec(24)
+    r = np.random.default_rng(25)
+    T = 8
+    X = r.standard_normal((T, 8))
+    Xh = X + 0.05 * r.standard_normal((T, 8))
+    ystar = B.decoder_forward(X, blk, rnd=False).y
+    y2star = B.decoder_forward(ystar, nxt, rnd=False).y
+    W = {k: v + 0.02 * r.standard_normal(v.shape) for k, v in blk.weights().items()}
+    J = slice(2, W[which].shape[1])
+
+    def Lf(Wm):
+        Wc = dict(W)
+        Wc[which] = Wm
+        f = B.decoder_forward(Xh, blk, Wc, rnd=False)
+        return B.decoder_surrogate(f, ystar, blk, T, Wc, nxt, y2star, alpha, rnd=False)[0]
+
+    f = B.decoder_forward(Xh, blk, W, rnd=False)
+    _, bw = B.decoder_surrogate(f, ystar, blk, T, W, nxt, y2star, alpha, rnd=False)
+    G = B.decoder_module_grad(which, f, bw, J)
+    rows, cols = W[which].shape
+    for (i, j) in [(0, 2), (rows - 1, cols - 1), (rows // 2, 3), (1, cols - 2)]:
+        num = _fd(Lf, W[which], (i, j))
+        assert G[i, j - 2] == pytest.approx(num, rel=1e-6, abs=1e-11), (which, i, j)
+
+
+def test_decoder_input_gradient_matches_finite_differences():
+    blk = _dec(26)
+    r = np.random.default_rng(27)
+    T = 8
+    X = r.standard_normal((T, 8))
+    ystar = r.standard_normal((T, 8))
+    Lf = lambda x: B.fisher_loss(B.decoder_forward(x, blk, rnd=False).y - ystar, blk.F, T)
+    f = B.decoder_forward(X, blk, rnd=False)
+    gy = (f.y - ystar) @ blk.F / T
+    dx = B.decoder_backward(f, gy, blk)["x"]
+    for idx in [(0, 0), (3, 5), (7, 7), (5, 2)]:
+        assert dx[idx] == pytest.approx(_fd(Lf, X, idx), rel=1e-6, abs=1e-11)
+
+
+def _dec_inputs(seed=30):
+    inp = synth.make_mlp_block(256, 256, 384, seed=seed)
+    r = np.random.default_rng(seed)
+    d, H, Hkv, hd = 256, 4, 2, 64
+    blk = B.DecoderBlock(gamma1=1 + 0.1 * r.standard_normal(d), Wq=0.02 * r.standard_normal((H * hd, d)),
+                         Wk=0.02 * r.standard_normal((Hkv * hd, d)), Wv=0.02 * r.standard_normal((Hkv * hd, d)),
+                         Wo=0.02 * r.standard_normal((d, H * hd)), gamma2=inp.gamma, Wg=inp.Wg, Wu=inp.Wu,
+                         Wd=inp.Wd, n_heads=H, n_kv=Hkv, head_dim=hd, seq_len=64, F=None)
+    return inp.X, inp.Xhat, blk
+
+
+def test_decoder_sweep_without_bgd_is_gptq_on_each_modules_input():
+    X, Xh, blk = _dec_inputs()
+    res = B.decoder_block_sweep(X, Xh, blk, steps=0)
+    W = {k: np.asarray(v, np.float64) for k, v in blk.weights().items()}
+    for name in B.DECODER_MODULES:
+        f = B.decoder_forward(Xh, blk, W)
+        inp = {"q": f.h1, "k": f.h1, "v": f.h1, "o": f.O, "gate": f.mlp.u, "up": f.mlp.u, "down": f.mlp.z}[name]
+        ref = quantize_layer(W[name], inp, inp)
+        assert (res.modules[name].codes == ref.codes).all(), name
+        W[name] = ref.W_hat
