@@ -377,6 +377,75 @@ typedef struct realq_mlp_out {
 
 int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* desc, realq_mlp_out* out);
 
+/* The full decoder block: the attention half in front of the MLP half,
+ *     h1 = bf16(rmsnorm(x) * gamma1),  q/k/v = bf16(h1 W^T),  qr/kr = bf16(rope(q/k)),
+ *     O = bf16(softmax_causal(qr kr^T / sqrt(hd)) v),  x2 = x + bf16(O Wo^T),
+ *     then y = the MLP half of realq_mlp_block_sweep applied to x2,
+ * with n_heads query heads and n_kv key/value heads of head_dim (query head h reads key/value
+ * head h / (n_heads / n_kv)), the rotary embedding over pairs (i, i + hd/2) at angle
+ * (t mod seq_len) rope_base^(-2i/hd) (positions counted within each sequence of seq_len
+ * tokens), and causal attention within each sequence (scores, softmax and value sums in
+ * float64 per query row).  realq_decoder_block_sweep quantizes q, k, v, o, gate, up and down
+ * in that order (Alg. 1), each with GPTQ on its own input in the quantized path (h1; O; u;
+ * z) and Block-GD on the block-output Fisher loss as described for realq_mlp_block_sweep,
+ * b_global running over the column blocks of all seven modules; the window partner is the
+ * next decoder block.  Shapes: Wq [H hd, d], Wk and Wv [Hkv hd, d], Wo [d, H hd]; T a multiple
+ * of seq_len, seq_len <= 4096, H a multiple of Hkv, head_dim even and <= 256, d, f and the
+ * projection widths multiples of 8.  Outputs per module in the order q, k, v, o, gate, up,
+ * down; loss_trace entry (b_global - 1) * steps + k. */
+typedef struct realq_decoder_block {
+    const float* gamma1;
+    const float* Wq;
+    const float* Wk;
+    const float* Wv;
+    const float* Wo;
+    realq_mlp_block mlp;   /* gamma (the second norm), Wg, Wu, Wd, F (the block-output metric) */
+} realq_decoder_block;
+
+typedef struct realq_decoder_desc {
+    int64_t T, d, f, seq_len;
+    int32_t n_heads, n_kv, head_dim;
+    float rope_base, eps;
+    const uint16_t* X;
+    const uint16_t* Xhat;
+    realq_decoder_block blk;
+    realq_decoder_block next;   /* next.Wq == NULL: none */
+    int32_t window;
+    realq_qparams q;
+    realq_bgd_params bgd;
+} realq_decoder_desc;
+
+typedef struct realq_decoder_out {
+    uint8_t* codes[7];
+    float* scales[7];
+    uint8_t* zeros[7];
+    float* W_hat[7];
+    double* loss_trace;
+    double loss_final;
+    double ms_total;
+} realq_decoder_out;
+
+int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_desc* desc, realq_decoder_out* out);
+
+/* One forward of the decoder block above on desc->X with desc->blk's weights (desc->Xhat, next,
+ * window, q and bgd are not read): the block output y, which is the next block's input in
+ * Alg. 1's block-by-block pass (run it on X with the full-precision weights and on Xhat with
+ * the quantized ones), and, where the pointer is not NULL, the intermediates h1, q, k, v
+ * (before the rotary embedding), O (the o projection's input) and x2, laid out as in the
+ * formulas above, token-major.  All device memory owned by the caller; y is required.
+ * Errors as for realq_decoder_block_sweep; the call returns after the stream has finished. */
+typedef struct realq_decoder_fwd_out {
+    uint16_t* h1;   /* [T, d] bf16 */
+    uint16_t* q;    /* [T, n_heads head_dim] bf16 */
+    uint16_t* k;    /* [T, n_kv head_dim] bf16 */
+    uint16_t* v;    /* [T, n_kv head_dim] bf16 */
+    uint16_t* O;    /* [T, n_heads head_dim] bf16 */
+    float* x2;      /* [T, d] */
+    float* y;       /* [T, d] */
+} realq_decoder_fwd_out;
+
+int realq_decoder_forward(realq_ctx* ctx, const realq_decoder_desc* desc, realq_decoder_fwd_out* out);
+
 #ifdef __cplusplus
 }
 #endif

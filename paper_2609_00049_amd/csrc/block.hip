@@ -242,7 +242,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_blend_kernel(const float* __r
         for (int64_t i = threadIdx.x; i < d; i += TB) {
             const int64_t e = t * d + i;
             const double dh = (double)g2[e] + r * (double)gamma[i] * (double)dr[i] - r * r * r * (double)hr[i] * mhd;
-            g[e] = (float)(alpha * (double)g[e] + (1.0 - alpha) * dh);
+            g[e] = (float)((alpha != 0.0 ? alpha * (double)g[e] : 0.0) + (1.0 - alpha) * dh);
         }
     }
 }

@@ -164,6 +164,44 @@ hipError_t split_f64(const double* in, uint16_t* hi, uint16_t* lo, int64_t count
     return hipGetLastError();
 }
 
+__device__ __forceinline__ void split3(float x, uint16_t& h, uint16_t& l, uint16_t& l2) {
+    h = f2bf(x);
+    const float r1 = x - bf2f(h);
+    l = f2bf(r1);
+    l2 = f2bf(r1 - bf2f(l));
+}
+
+__global__ void split3_f64_kernel(const double* __restrict__ in, uint16_t* __restrict__ hi, uint16_t* __restrict__ lo,
+                                  uint16_t* __restrict__ lo2, int64_t count) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x)
+        split3((float)in[e], hi[e], lo[e], lo2[e]);
+}
+
+hipError_t split3_f64(const double* in, uint16_t* hi, uint16_t* lo, uint16_t* lo2, int64_t count, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(split3_f64_kernel, dim3(grid_for(count, 4)), dim3(TB), 0, st, in, hi, lo, lo2, count);
+    return hipGetLastError();
+}
+
+__global__ void split3_f32_kernel(const float* __restrict__ A, int64_t lda, uint16_t* __restrict__ hi,
+                                  uint16_t* __restrict__ lo, uint16_t* __restrict__ lo2, int64_t ld, int64_t cols,
+                                  int64_t total) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / cols, j = e % cols;
+        const int64_t o = i * ld + j;
+        split3(A[i * lda + j], hi[o], lo[o], lo2[o]);
+    }
+}
+
+hipError_t split3_f32(const float* A, int64_t lda, uint16_t* hi, uint16_t* lo, uint16_t* lo2, int64_t ld,
+                      int64_t rows, int64_t cols, hipStream_t st) {
+    const int64_t total = rows * cols;
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(split3_f32_kernel, dim3(grid_for(total, 4)), dim3(TB), 0, st, A, lda, hi, lo, lo2, ld, cols,
+                       total);
+    return hipGetLastError();
+}
+
 // G[i][j] = C0[i][c1 + j] + P[i][c1 + j]   (m x w, C0 and P with row stride ld)
 __global__ void gram_grad_kernel(const float* __restrict__ C0, const float* __restrict__ P, int64_t ld, int64_t c1,
                                  int64_t w, int64_t total, float* __restrict__ G) {

@@ -623,15 +623,27 @@ struct EpiLoss {
 // Token-major outputs of the module hand-off (acc[i][j] is output channel i of token j):
 // a lane holds rows i..i+3 of one column j and stores them contiguously at out[j*ld + i].
 
-// out[j][i] = bf16(acc)
+// out[j][i] = bf16(acc + add[j][i])   (add may be NULL; same layout as out)
 struct EpiStoreBf16T {
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = true;
     uint16_t* out;
     int64_t ld;
-    __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { out[j * ld + i] = f2bf(v); }
+    const float* add;
+    __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const {
+        out[j * ld + i] = f2bf(add ? v + add[j * ld + i] : v);
+    }
     __device__ void vec4t(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
         uint16_t* p = out + j * ld + i;
+        if (add) {
+            const float* a = add + j * ld + i;
+            if (!al16(a)) {
+                for (int u = 0; u < 4; ++u) (*this)(i + u, j, v[u], z, aux);
+                return;
+            }
+            const f32x4 av = *reinterpret_cast<const f32x4*>(a);
+            for (int u = 0; u < 4; ++u) v[u] += av[u];
+        }
         if (al8(p)) {
             u16x4 h = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
             *reinterpret_cast<u16x4*>(p) = h;
@@ -642,18 +654,29 @@ struct EpiStoreBf16T {
     __device__ void partial(int64_t, double) const {}
 };
 
-// out[j][i] = acc (float32; the gate pre-activation of a SwiGLU hand-off)
+// out[j][i] = acc + add[j][i] (float32; the gate pre-activation of a SwiGLU hand-off; add may
+// be NULL or equal to out: each element is read and written by the same lane)
 struct EpiStoreF32T {
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = true;
     float* out;
     int64_t ld;
-    __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const { out[j * ld + i] = v; }
+    const float* add;
+    __device__ void operator()(int64_t i, int64_t j, float v, int64_t, float&) const {
+        out[j * ld + i] = add ? v + add[j * ld + i] : v;
+    }
     __device__ void vec4t(int64_t i, int64_t j, f32x4 v, int64_t z, float& aux) const {
         float* p = out + j * ld + i;
-        if (al16(p)) *reinterpret_cast<f32x4*>(p) = v;
-        else
+        const float* a = add ? add + j * ld + i : nullptr;
+        if (al16(p) && (!a || al16(a))) {
+            if (a) {
+                const f32x4 av = *reinterpret_cast<const f32x4*>(a);
+                for (int u = 0; u < 4; ++u) v[u] += av[u];
+            }
+            *reinterpret_cast<f32x4*>(p) = v;
+        } else {
             for (int u = 0; u < 4; ++u) (*this)(i + u, j, v[u], z, aux);
+        }
     }
     __device__ void partial(int64_t, double) const {}
 };
@@ -779,11 +802,11 @@ hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const flo
                      hipStream_t st) {
     return launch(g, EpiLoss{B0, ldb0, s, partials}, st);
 }
-hipError_t gemm_store_bf16_t(const GemmArgs& g, uint16_t* out, int64_t ld, hipStream_t st) {
-    return launch(g, EpiStoreBf16T{out, ld}, st);
+hipError_t gemm_store_bf16_t(const GemmArgs& g, uint16_t* out, int64_t ld, hipStream_t st, const float* add) {
+    return launch(g, EpiStoreBf16T{out, ld, add}, st);
 }
-hipError_t gemm_store_f32_t(const GemmArgs& g, float* out, int64_t ld, hipStream_t st) {
-    return launch(g, EpiStoreF32T{out, ld}, st);
+hipError_t gemm_store_f32_t(const GemmArgs& g, float* out, int64_t ld, hipStream_t st, const float* add) {
+    return launch(g, EpiStoreF32T{out, ld, add}, st);
 }
 hipError_t gemm_swiglu_t(const GemmArgs& g, const float* G, int64_t ldg, uint16_t* out, int64_t ld, hipStream_t st) {
     return launch(g, EpiSwiGLUT{G, ldg, out, ld}, st);

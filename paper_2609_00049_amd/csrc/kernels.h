@@ -31,10 +31,11 @@ hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const fl
                       int64_t ldr, double* partials, hipStream_t st);
 hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
                      hipStream_t st);
-// Token-major stores for the module hand-off: out[j*ld + i] = bf16(acc[i][j]); float32 variant;
+// Token-major stores for the module hand-off: out[j*ld + i] = bf16(acc[i][j] + add[j*ld + i]);
+// float32 variant (add may be NULL, and for the float32 variant equal to out);
 // SwiGLU variant out[j*ld + i] = bf16(silu(G[j*ldg + i]) * acc[i][j]).
-hipError_t gemm_store_bf16_t(const GemmArgs& g, uint16_t* out, int64_t ld, hipStream_t st);
-hipError_t gemm_store_f32_t(const GemmArgs& g, float* out, int64_t ld, hipStream_t st);
+hipError_t gemm_store_bf16_t(const GemmArgs& g, uint16_t* out, int64_t ld, hipStream_t st, const float* add = nullptr);
+hipError_t gemm_store_f32_t(const GemmArgs& g, float* out, int64_t ld, hipStream_t st, const float* add = nullptr);
 hipError_t gemm_swiglu_t(const GemmArgs& g, const float* G, int64_t ldg, uint16_t* out, int64_t ld, hipStream_t st);
 // out[c*ldo + r] = in[r*ldi + c] (float32)
 hipError_t transpose_f32(const float* in, int64_t ldi, float* out, int64_t ldo, int64_t rows, int64_t cols,
@@ -64,6 +65,12 @@ hipError_t transpose_delta_split(const uint16_t* Xh, const uint16_t* X, int64_t 
                                  hipStream_t st);
 // hi/lo = split(float(in))
 hipError_t split_f64(const double* in, uint16_t* hi, uint16_t* lo, int64_t count, hipStream_t st);
+// Three-term splits that carry all 24 bits of a float32: hi = bf16(x), lo = bf16(x - hi),
+// lo2 = bf16(x - hi - lo), so hi + lo + lo2 equals x to float32 precision (x = float(in) for the
+// float64 input).
+hipError_t split3_f64(const double* in, uint16_t* hi, uint16_t* lo, uint16_t* lo2, int64_t count, hipStream_t st);
+hipError_t split3_f32(const float* A, int64_t lda, uint16_t* hi, uint16_t* lo, uint16_t* lo2, int64_t ld,
+                      int64_t rows, int64_t cols, hipStream_t st);
 // G[i][j] = C0[i][c1+j] + P[i][c1+j], i < m, j < w
 hipError_t gram_grad(const float* C0, const float* P, int64_t ld, int64_t c1, int64_t m, int64_t w, float* G,
                      hipStream_t st);
@@ -171,9 +178,23 @@ hipError_t swiglu_bwd(const float* dz, const float* a, const float* b, int which
 // hi/lo[c * ldo + r] = split(in[r * ldi + c])
 hipError_t transpose_split_f32(const float* in, int64_t ldi, uint16_t* hi, uint16_t* lo, int64_t ldo, int64_t rows,
                                int64_t cols, hipStream_t st);
-// g = alpha g + (1 - alpha) (g2 + RMSNorm backward of du at h)
+// g = alpha g + (1 - alpha) (g2 + RMSNorm backward of du at h); alpha == 0 does not read g
 hipError_t rmsnorm_bwd_blend(const float* h, const float* g2, const float* du, const float* gamma, double eps,
                              double alpha, int64_t T, int64_t d, float* g, hipStream_t st);
+
+// ---------------------------------------------------------------- attention half of a decoder block
+// rotary embedding: forward on bf16 [T][n hd] (rounded), inverse rotation on float32 (backward)
+hipError_t rope_fwd(const uint16_t* in, uint16_t* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
+                    hipStream_t st);
+hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
+                    hipStream_t st);
+// causal attention per sequence of L tokens: P [T/L][H][L][L] float32, O = bf16(P V) [T][H hd]
+hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, int64_t T, int64_t H, int64_t Hkv,
+                    int64_t hd, int64_t L, float* P, uint16_t* O, hipStream_t st);
+// from dO [T][H hd] float32: dS (work, like P), dq [T][H hd], dk and dv [T][Hkv hd] (float32)
+hipError_t attn_bwd(const float* P, const float* dO, const uint16_t* qr, const uint16_t* kr, const uint16_t* v,
+                    int64_t T, int64_t H, int64_t Hkv, int64_t hd, int64_t L, float* dS, float* dq, float* dk,
+                    float* dv, hipStream_t st);
 
 // ---------------------------------------------------------------- quantize one column block
 struct QuantArgs {

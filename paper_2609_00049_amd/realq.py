@@ -37,6 +37,7 @@ EXPORTS = [
     "realq_quantize_block", "realq_quantize_block_rows", "realq_bgd_lock_block",
     "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
     "realq_pullback_metric", "realq_handoff", "realq_mlp_block_sweep",
+    "realq_decoder_block_sweep", "realq_decoder_forward",
 ]
 
 
@@ -96,6 +97,30 @@ class MLPOut(ctypes.Structure):
                 ("loss_final", ctypes.c_double), ("ms_total", ctypes.c_double)]
 
 
+class DecoderBlock(ctypes.Structure):
+    _fields_ = [("gamma1", ctypes.c_void_p), ("Wq", ctypes.c_void_p), ("Wk", ctypes.c_void_p),
+                ("Wv", ctypes.c_void_p), ("Wo", ctypes.c_void_p), ("mlp", MLPBlock)]
+
+
+class DecoderDesc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int64), ("d", ctypes.c_int64), ("f", ctypes.c_int64), ("seq_len", ctypes.c_int64),
+                ("n_heads", ctypes.c_int32), ("n_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("rope_base", ctypes.c_float), ("eps", ctypes.c_float),
+                ("X", ctypes.c_void_p), ("Xhat", ctypes.c_void_p), ("blk", DecoderBlock), ("next", DecoderBlock),
+                ("window", ctypes.c_int32), ("q", QParams), ("bgd", BgdParams)]
+
+
+class DecoderOut(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p * 7), ("scales", ctypes.c_void_p * 7), ("zeros", ctypes.c_void_p * 7),
+                ("W_hat", ctypes.c_void_p * 7), ("loss_trace", ctypes.c_void_p),
+                ("loss_final", ctypes.c_double), ("ms_total", ctypes.c_double)]
+
+
+class DecoderFwdOut(ctypes.Structure):
+    _fields_ = [("h1", ctypes.c_void_p), ("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("O", ctypes.c_void_p), ("x2", ctypes.c_void_p), ("y", ctypes.c_void_p)]
+
+
 def _load():
     if not _LIB_PATH.exists():
         raise ImportError(f"{_LIB_PATH} is not built; run paper_2609_00049_amd.build.build() first")
@@ -130,6 +155,8 @@ def _load():
         "realq_pullback_metric": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int, vp]),
         "realq_handoff": (ctypes.c_int, [vp, vp, vp, vp, i64, i64, i64, vp]),
         "realq_mlp_block_sweep": (ctypes.c_int, [vp, ctypes.POINTER(MLPDesc), ctypes.POINTER(MLPOut)]),
+        "realq_decoder_block_sweep": (ctypes.c_int, [vp, ctypes.POINTER(DecoderDesc), ctypes.POINTER(DecoderOut)]),
+        "realq_decoder_forward": (ctypes.c_int, [vp, ctypes.POINTER(DecoderDesc), ctypes.POINTER(DecoderFwdOut)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -427,3 +454,69 @@ def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, 
     o.loss_trace = _ptr(trace)
     ctx.check(_lib.realq_mlp_block_sweep(ctx.h, ctypes.byref(desc), ctypes.byref(o)))
     return BlockResult(modules=mods, loss_trace=trace, loss_final=o.loss_final, ms_total=o.ms_total)
+
+
+DECODER_MODULES = ("q", "k", "v", "o", "gate", "up", "down")
+
+
+def _decoder_block(w: dict) -> DecoderBlock:
+    return DecoderBlock(_ptr(w["gamma1"]), _ptr(w["Wq"]), _ptr(w["Wk"]), _ptr(w["Wv"]), _ptr(w["Wo"]),
+                        _mlp_block(w["gamma2"], w["Wg"], w["Wu"], w["Wd"], w.get("F")))
+
+
+def decoder_block_sweep(ctx: Context, X, Xhat, blk: dict, nxt: Optional[dict] = None, *, n_heads, n_kv, head_dim,
+                        seq_len, rope_base=10000.0, eps=1e-6, window=False, qp: Optional[QParams] = None,
+                        bgd: Optional[BgdParams] = None, want_trace=True) -> BlockResult:
+    """Quantize q, k, v, o, gate, up and down of one pre-norm decoder block (rotary causal
+    attention with grouped key/value heads, then a SwiGLU MLP) with Block-GD on the block-output
+    surrogate.  X, Xhat [T, d] bf16; blk and nxt are dicts of float32 device tensors with keys
+    gamma1 [d], Wq [H hd, d], Wk and Wv [Hkv hd, d], Wo [d, H hd], gamma2 [d], Wg and Wu [f, d],
+    Wd [d, f] and optionally F [d, d]; nxt is the next block (window partner) or None."""
+    qp = qp or qparams()
+    bgd = bgd or bgd_params()
+    T, d = X.shape
+    f = blk["Wg"].shape[0]
+    dev = X.device
+    shapes = [tuple(blk[k].shape) for k in ("Wq", "Wk", "Wv", "Wo", "Wg", "Wu", "Wd")]
+    nb = [-(-cols // qp.block) for (_, cols) in shapes]
+    mods = {}
+    for name, (rows, cols) in zip(DECODER_MODULES, shapes):
+        ng = -(-cols // (qp.group or cols))
+        mods[name] = LayerResult(codes=torch.empty((rows, cols), dtype=torch.uint8, device=dev),
+                                 scales=torch.empty((rows, ng), dtype=torch.float32, device=dev),
+                                 zeros=torch.empty((rows, ng), dtype=torch.uint8, device=dev),
+                                 W_hat=torch.empty((rows, cols), dtype=torch.float32, device=dev),
+                                 H=None, U=None, dead=None, loss_trace=None, loss_final=math.nan, ms_total=math.nan)
+    trace = torch.empty((max(1, sum(nb) * bgd.steps),), dtype=torch.float64, device=dev) if want_trace else None
+    nx = _decoder_block(nxt) if nxt is not None else DecoderBlock()
+    desc = DecoderDesc(T, d, f, seq_len, n_heads, n_kv, head_dim, rope_base, eps, _ptr(_bits(X)), _ptr(_bits(Xhat)),
+                       _decoder_block(blk), nx, int(bool(window)), qp, bgd)
+    o = DecoderOut()
+    for k, name in enumerate(DECODER_MODULES):
+        o.codes[k] = _ptr(mods[name].codes)
+        o.scales[k] = _ptr(mods[name].scales)
+        o.zeros[k] = _ptr(mods[name].zeros)
+        o.W_hat[k] = _ptr(mods[name].W_hat)
+    o.loss_trace = _ptr(trace)
+    ctx.check(_lib.realq_decoder_block_sweep(ctx.h, ctypes.byref(desc), ctypes.byref(o)))
+    return BlockResult(modules=mods, loss_trace=trace, loss_final=o.loss_final, ms_total=o.ms_total)
+
+
+def decoder_forward(ctx: Context, X, blk: dict, *, n_heads, n_kv, head_dim, seq_len, rope_base=10000.0, eps=1e-6,
+                    intermediates=False) -> dict:
+    """One forward of the decoder block (weights as for decoder_block_sweep) on X [T, d] (bf16):
+    {'y': [T, d] float32} and, with intermediates=True, h1, q, k, v, O (bf16) and x2 (float32)."""
+    T, d = X.shape
+    f = blk["Wg"].shape[0]
+    dev = X.device
+    Hq, Hk = n_heads * head_dim, n_kv * head_dim
+    res = {"y": torch.empty((T, d), dtype=torch.float32, device=dev)}
+    if intermediates:
+        for name, w in (("h1", d), ("q", Hq), ("k", Hk), ("v", Hk), ("O", Hq)):
+            res[name] = torch.empty((T, w), dtype=torch.bfloat16, device=dev)
+        res["x2"] = torch.empty((T, d), dtype=torch.float32, device=dev)
+    desc = DecoderDesc(T, d, f, seq_len, n_heads, n_kv, head_dim, rope_base, eps, _ptr(_bits(X)), None,
+                       _decoder_block(blk), DecoderBlock(), 0, qparams(), bgd_params())
+    o = DecoderFwdOut(*[_ptr(res.get(k)) for k in ("h1", "q", "k", "v", "O", "x2", "y")])
+    ctx.check(_lib.realq_decoder_forward(ctx.h, ctypes.byref(desc), ctypes.byref(o)))
+    return res

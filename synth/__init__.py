@@ -6,11 +6,13 @@ arithmetic: no Hessian, no quantizer, no compensation, no gradient.
 """
 from .gen import (  # noqa: F401
     CONFIGS,
+    DecoderBlockInputs,
     LayerInputs,
     MLPBlockInputs,
     bf16_bits,
     bf16_round,
     bf16_from_bits,
+    make_decoder_block,
     make_group_weights,
     make_mlp_block,
     make_module,

@@ -227,3 +227,34 @@ def make_mlp_block(T: int, d: int, f: int, seed: int = 0, dense_F: bool = True, 
         A = rng.standard_normal((d, 2 * d), dtype=np.float32)
         F = (A @ A.T) / np.float32(2 * d)
     return MLPBlockInputs(X=bf16_round(X32), Xhat=bf16_round(Xh32), gamma=gamma, Wg=Wg, Wu=Wu, Wd=Wd, F=F)
+
+
+@dataclass
+class DecoderBlockInputs:
+    X: np.ndarray        # [T, d] bf16-exact float32, block input of the full-precision model
+    Xhat: np.ndarray     # [T, d] bf16-exact float32, block input of the quantized model
+    w: dict              # gamma1, Wq, Wk, Wv, Wo, gamma2, Wg, Wu, Wd, F (float32 numpy; F may be None)
+    n_heads: int
+    n_kv: int
+    head_dim: int
+    seq_len: int
+
+
+def make_decoder_block(T: int, d: int, f: int, n_heads: int, n_kv: int, head_dim: int, seq_len: int,
+                       seed: int = 0, dense_F: bool = True, wstd: float = 0.02, qk_std: float = 0.04,
+                       xhat_rel: float = 0.01) -> DecoderBlockInputs:
+    """One pre-norm decoder block (attention, then a SwiGLU MLP) with its calibration inputs: the
+    MLP half and the inputs as make_mlp_block draws them, gamma1 = 1 + 0.1 N(0, 1), bf16
+    N(0, qk_std^2) query and key weights (sharper attention than wstd gives) and bf16
+    N(0, wstd^2) value and output weights."""
+    m = make_mlp_block(T, d, f, seed=seed, dense_F=dense_F, wstd=wstd, xhat_rel=xhat_rel)
+    rng = np.random.default_rng(seed * 1000 + 951)
+    Hq, Hk = n_heads * head_dim, n_kv * head_dim
+    w = dict(gamma1=(1.0 + 0.1 * rng.standard_normal(d)).astype(np.float32),
+             Wq=bf16_round(rng.standard_normal((Hq, d), dtype=np.float32) * np.float32(qk_std)),
+             Wk=bf16_round(rng.standard_normal((Hk, d), dtype=np.float32) * np.float32(qk_std)),
+             Wv=bf16_round(rng.standard_normal((Hk, d), dtype=np.float32) * np.float32(wstd)),
+             Wo=bf16_round(rng.standard_normal((d, Hq), dtype=np.float32) * np.float32(wstd)),
+             gamma2=m.gamma, Wg=m.Wg, Wu=m.Wu, Wd=m.Wd, F=m.F)
+    return DecoderBlockInputs(X=m.X, Xhat=m.Xhat, w=w, n_heads=n_heads, n_kv=n_kv, head_dim=head_dim,
+                              seq_len=seq_len)

@@ -42,7 +42,9 @@ def test_binding_structs_match_the_c_layout(tmp_path):
     from paper_2609_00049_amd import realq
     structs = {"realq_qparams": realq.QParams, "realq_bgd_params": realq.BgdParams,
                "realq_layer_desc": realq.LayerDesc, "realq_layer_out": realq.LayerOut,
-               "realq_mlp_block": realq.MLPBlock, "realq_mlp_desc": realq.MLPDesc, "realq_mlp_out": realq.MLPOut}
+               "realq_mlp_block": realq.MLPBlock, "realq_mlp_desc": realq.MLPDesc, "realq_mlp_out": realq.MLPOut,
+               "realq_decoder_block": realq.DecoderBlock, "realq_decoder_desc": realq.DecoderDesc,
+               "realq_decoder_out": realq.DecoderOut, "realq_decoder_fwd_out": realq.DecoderFwdOut}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "realq.h"', 'int main(void) {']
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')

@@ -55,14 +55,14 @@ DOWN_GROUP_AGREEMENT = 0.995
 # remainder (2^-17 of each token product), keeps at lr = 1e-3 only 85-86% of down's codes and
 # 98.4-98.7% of up's (99.96-100% at lr = 1e-5, the paper's rate for 8B-class models), so the
 # full code bars are held at lr = 1e-5 and at lr = 1e-3 the loss and the first steps are compared.
-# Even at lr = 1e-5 the down projection stays chaotic at the code level: every Adam step moves a
-# weight by about lr, a weight within that distance of a rounding boundary flips, and GPTQ carries
-# the flip along the rest of its 512-column row.  The oracle with the ~25 z entries that the GPU
-# rounds the other way (fixed, in every forward) keeps 98.4-99.9% of down's codes and 86-99.6% of
-# its groups with the identity metric (99.93-99.99% and 99.7-99.8% with a dense one); the GPU adds
-# up's few flipped codes, which change whole rows of z.  Down is therefore held to its first
-# groups (searched before any of its Block-GD steps), to 95% of its codes, and to the loss bar.
-DOWN_CODE_IDENTITY_AFTER_BGD = 0.95
+# Even at lr = 1e-5 the down projection is the sensitive one: every Adam step moves a weight by
+# about lr, a weight within that distance of a rounding boundary flips, and GPTQ carries the flip
+# along the rest of its 512-column row.  The oracle with the ~25 z entries that the GPU rounds the
+# other way (fixed, in every forward) keeps 98.4-99.9% of down's codes and 86-99.6% of its groups
+# with the identity metric (99.93-99.99% and 99.7-99.8% with a dense one).  Down is therefore held
+# to its first groups (searched before any of its Block-GD steps), to 98% of its codes, and to the
+# loss bar.
+DOWN_CODE_IDENTITY_AFTER_BGD = 0.98
 
 
 def _check(g, o, bgd):
