@@ -170,16 +170,69 @@ def block_f_alg(T, d, f, block, steps, window, dense):
     backward when the window blends it in)."""
     tdf, tdd = 2.0 * T * d * f, 2.0 * T * d * d
     total = 0.0
+    b_global = 0
     for mod, (rows, cols) in enumerate(((f, d), (f, d), (d, f))):
         nb = -(-cols // block)
-        for b in range(nb - 1):
+        for b in range(nb):
+            b_global += 1
+            if b == nb - 1:
+                continue
             nJ = cols - (b + 1) * block
             per = (tdf if mod < 2 else 0.0) + tdf + (tdd if dense else 0.0)   # a or b; out; F dy
             per += (tdf if mod < 2 else 0.0) + 2.0 * rows * nJ * T             # dz = g Wd; gradient
-            if window:
+            if window and b_global > 1:                                         # alpha < 1
                 per += 3 * tdf + (tdd if dense else 0.0) + tdf + 2 * tdf        # next block fwd, F, dz2, du2
             total += steps * per
     return total
+
+
+def decoder_f_alg(T, d, f, H, Hkv, hd, L, block, steps, window, dense):
+    """Algorithmic FLOPs of the Block-GD steps of realq_decoder_block_sweep, split into the
+    projection and MLP GEMMs and the causal attention (QK^T and PV forward; dP, dQ, dK and dV
+    backward, each 2 T H hd (L + 1) / 2; all on bf16 MFMA)."""
+    Hq, Hk = H * hd, Hkv * hd
+    tdf, tdd = 2.0 * T * d * f, 2.0 * T * d * d
+    att = 2.0 * T * H * hd * (L + 1) / 2.0
+    qkv = 2.0 * T * d * (Hq + 2 * Hk)
+    oo = 2.0 * T * Hq * d
+    proj = {"q": 2.0 * T * d * Hq, "k": 2.0 * T * d * Hk, "v": 2.0 * T * d * Hk}
+    shapes = (("q", Hq, d), ("k", Hk, d), ("v", Hk, d), ("o", d, Hq), ("gate", f, d), ("up", f, d), ("down", d, f))
+    gemm = attn = 0.0
+    b_global = 0
+    for name, rows, cols in shapes:
+        nb = -(-cols // block)
+        for b in range(nb):
+            b_global += 1
+            if b == nb - 1:
+                continue
+            nJ = cols - (b + 1) * block
+            g = a = 0.0
+            # forward from this module's stage
+            if name in proj:
+                g += proj[name] + oo + 3 * tdf
+                a += 2 * att
+            elif name == "o":
+                g += oo + 3 * tdf
+            elif name in ("gate", "up"):
+                g += 2 * tdf
+            else:
+                g += tdf
+            g += tdd if dense else 0.0                      # F dy
+            # backward to this module's output
+            if name in ("gate", "up"):
+                g += tdf
+            elif name == "o" or name in proj:
+                g += 3 * tdf                                # dz, du
+                if name in proj:
+                    g += oo
+                    a += 4 * att
+            g += 2.0 * rows * nJ * T                        # the gradient of the trailing columns
+            if window and b_global > 1:                     # the next block: forward, F, backward to x
+                g += qkv + oo + 3 * tdf + (tdd if dense else 0.0) + 3 * tdf + oo + qkv
+                a += 6 * att
+            gemm += steps * g
+            attn += steps * a
+    return gemm, attn
 
 
 def mlp_block(torch, rq, ctx, qp, T=8192, d=4096, f=14336, steps=8, lr=1e-5):
@@ -212,6 +265,49 @@ def mlp_block(torch, rq, ctx, qp, T=8192, d=4096, f=14336, steps=8, lr=1e-5):
             "block_step_ms_total": st_ms, "block_step_tflops_alg": fl / (st_ms / 1e3) / 1e12 if st_ms > 0 else None,
             "frac_bf16_peak_alg": fl / (st_ms / 1e3) / PEAK_BF16 if st_ms > 0 else None,
             "columns_per_s": (2 * d + f) / (r.ms_total / 1e3)}
+
+
+def decoder_block(torch, rq, ctx, qp, T=8192, d=4096, f=14336, H=32, Hkv=8, hd=128, L=2048, steps=2, lr=1e-5):
+    """The block-output surrogate sweep of a LLaMA-3.1-8B-shaped decoder block (d 4096, 32 query
+    and 8 key/value heads of 128, f 14336) on 8192 tokens in sequences of 2048, with a dense
+    4096 x 4096 block-output metric, the next decoder block blended in, and 2 Block-GD steps per
+    column block (8 for the MLP block: the decoder's 304 column blocks each take a forward and
+    backward through attention and the next block)."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(78)
+    Hq, Hk = H * hd, Hkv * hd
+
+    def w(shape, std=0.02):
+        return (torch.randn(shape, generator=g, device="cuda") * std).to(torch.bfloat16).float().contiguous()
+
+    def block():
+        A = torch.randn((d, 2 * d), generator=g, device="cuda")
+        return {"gamma1": (1 + 0.1 * torch.randn((d,), generator=g, device="cuda")).contiguous(),
+                "Wq": w((Hq, d), 0.04), "Wk": w((Hk, d), 0.04), "Wv": w((Hk, d)), "Wo": w((d, Hq)),
+                "gamma2": (1 + 0.1 * torch.randn((d,), generator=g, device="cuda")).contiguous(),
+                "Wg": w((f, d)), "Wu": w((f, d)), "Wd": w((d, f)), "F": (A @ A.T / (2 * d)).contiguous()}
+
+    X = (torch.randn((T, d), generator=g, device="cuda")).to(torch.bfloat16).contiguous()
+    Xh = (X.float() * (1 + 0.01 * torch.randn((T, d), generator=g, device="cuda"))).to(torch.bfloat16).contiguous()
+    blk, nxt = block(), block()
+    bgd = rq.bgd_params(steps=steps, lr=lr)
+    ctx.reset_timing()
+    r = rq.decoder_block_sweep(ctx, X, Xh, blk, nxt, n_heads=H, n_kv=Hkv, head_dim=hd, seq_len=L, window=True,
+                               qp=qp, bgd=bgd)
+    nst, st_ms = ctx.kernel_time("block_step")
+    nat, at_ms = ctx.kernel_time("attention")
+    fl_gemm, fl_att = decoder_f_alg(T, d, f, H, Hkv, hd, L, qp.block, steps, True, True)
+    print(f"[bench] decoder block sweep: {r.ms_total:.1f} ms, loss {r.loss_final:.6g}", file=sys.stderr, flush=True)
+    gemm_ms = st_ms - at_ms
+    return {"tokens": T, "d": d, "f": f, "n_heads": H, "n_kv": Hkv, "head_dim": hd, "seq_len": L, "bgd_steps": steps,
+            "window": True, "dense_metric": True, "ms_total": r.ms_total, "loss_final": r.loss_final,
+            "block_steps": nst, "block_step_ms_total": st_ms, "attention_launch_groups": nat,
+            "attention_ms_total": at_ms,
+            "attention_tflops_alg": fl_att / (at_ms / 1e3) / 1e12 if at_ms > 0 else None,
+            "attention_frac_bf16_peak_alg": fl_att / (at_ms / 1e3) / PEAK_BF16 if at_ms > 0 else None,
+            "gemm_tflops_alg": fl_gemm / (gemm_ms / 1e3) / 1e12 if gemm_ms > 0 else None,
+            "gemm_frac_bf16_peak_alg": fl_gemm / (gemm_ms / 1e3) / PEAK_BF16 if gemm_ms > 0 else None,
+            "columns_per_s": (3 * d + Hq + 2 * d + f) / (r.ms_total / 1e3)}
 
 
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_00049_amd", "csrc", "gemm_bf16.hip")
@@ -259,7 +355,10 @@ def main():
                     help="skip the Stage-0 accumulator timings and the N_g = 4 row-group sweep (stage0)")
     ap.add_argument("--no-block", action="store_true",
                     help="skip the block-output surrogate sweep of a LLaMA-3.1-8B-shaped MLP block (mlp_block)")
-    ap.add_argument("--only", choices=("stage0", "block"),
+    ap.add_argument("--no-decoder", action="store_true",
+                    help="skip the block-output surrogate sweep of a LLaMA-3.1-8B-shaped decoder block "
+                         "(decoder_block)")
+    ap.add_argument("--only", choices=("stage0", "block", "decoder"),
                     help="run only that part (for per-part kernel profiles) and print its object")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -276,6 +375,11 @@ def main():
         ctx = rq.Context()
         ctx.set_timing(True)
         print(json.dumps({"mlp_block": mlp_block(torch, rq, ctx, rq.qparams())}), flush=True)
+        return
+    if args.only == "decoder":
+        ctx = rq.Context()
+        ctx.set_timing(True)
+        print(json.dumps({"decoder_block": decoder_block(torch, rq, ctx, rq.qparams())}), flush=True)
         return
     print(f"[bench] generating {args.workload}: m={m} n={n} T={T} K={K}", file=sys.stderr, flush=True)
     W0, X, Xh, s = make_inputs(torch, args.workload)
@@ -364,10 +468,13 @@ def main():
                                     "(bench.py --form gram for its own line)"}
     if not args.no_stage0:
         res["stage0"] = stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n, T)
-    if not args.no_block:
+    if not (args.no_block and args.no_decoder):
         del W0, X, Xh, s
         torch.cuda.empty_cache()
+    if not args.no_block:
         res["mlp_block"] = mlp_block(torch, rq, ctx, qp)
+    if not args.no_decoder:
+        res["decoder_block"] = decoder_block(torch, rq, ctx, qp)
     ctx.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)

@@ -117,7 +117,8 @@ const char* realq_last_error(const realq_ctx* ctx);
  * "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init", "gram" (Gram
  * matrices of the input perturbation), "gram_step" (the per-step product of the
  * Gram form), "dense_loss" (final loss with a dense metric), "saliency", "block_init" and
- * "block_step" (realq_mlp_block_sweep: the fixed forwards, one Block-GD step).
+ * "block_step" (the block sweeps: the fixed forwards, one Block-GD step) and "attention"
+ * (realq_decoder_block_sweep: each attention forward or backward with its rotary embeddings).
  * Returns REALQ_ERR_INVALID_ARG for an unknown name. */
 int realq_ctx_set_timing(realq_ctx* ctx, int enable);
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms);
@@ -384,15 +385,18 @@ int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* desc, realq_mlp_
  * with n_heads query heads and n_kv key/value heads of head_dim (query head h reads key/value
  * head h / (n_heads / n_kv)), the rotary embedding over pairs (i, i + hd/2) at angle
  * (t mod seq_len) rope_base^(-2i/hd) (positions counted within each sequence of seq_len
- * tokens), and causal attention within each sequence (scores, softmax and value sums in
- * float64 per query row).  realq_decoder_block_sweep quantizes q, k, v, o, gate, up and down
+ * tokens), and causal attention within each sequence: scores as float32 sums of the exact
+ * bf16 products, the softmax in float64, the value sums with the probabilities in full float32
+ * precision.  realq_decoder_block_sweep quantizes q, k, v, o, gate, up and down
  * in that order (Alg. 1), each with GPTQ on its own input in the quantized path (h1; O; u;
  * z) and Block-GD on the block-output Fisher loss as described for realq_mlp_block_sweep,
  * b_global running over the column blocks of all seven modules; the window partner is the
- * next decoder block.  Shapes: Wq [H hd, d], Wk and Wv [Hkv hd, d], Wo [d, H hd]; T a multiple
- * of seq_len, seq_len <= 4096, H a multiple of Hkv, head_dim even and <= 256, d, f and the
- * projection widths multiples of 8.  Outputs per module in the order q, k, v, o, gate, up,
- * down; loss_trace entry (b_global - 1) * steps + k. */
+ * next decoder block.  Shapes: Wq [H hd, d], Wk and Wv [Hkv hd, d], Wo [d, H hd]; seq_len a
+ * multiple of 32 and at most 4096, T a multiple of seq_len, H a multiple of Hkv, head_dim a
+ * multiple of 32 and at most 256, d and f multiples of 8 (REALQ_ERR_SHAPE otherwise).  The
+ * attention keeps float32 probabilities of T n_heads seq_len entries per block forward (three
+ * forwards with the window) and six bf16 arrays of that size for its backward.  Outputs per
+ * module in the order q, k, v, o, gate, up, down; loss_trace entry (b_global - 1) * steps + k. */
 typedef struct realq_decoder_block {
     const float* gamma1;
     const float* Wq;

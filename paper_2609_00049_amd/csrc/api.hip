@@ -170,7 +170,7 @@ int realq_ctx_set_timing(realq_ctx* ctx, int enable) {
 
 static const char* kTimedNames[] = {"hessian", "chol",  "quantize",  "obs",        "lock",      "resid",
                                     "grad",    "adam",  "init",      "gram",       "gram_step", "dense_loss",
-                                    "saliency", "block_init", "block_step"};
+                                    "saliency", "block_init", "block_step", "attention"};
 
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms) {
     if (!ctx || !name) return REALQ_ERR_INVALID_ARG;

@@ -1,10 +1,16 @@
 // Attention half of the block-output surrogate (Sec. 4.2-4.4 with a full decoder block):
 // rotary position embedding and causal softmax attention with grouped key/value heads, forward
 // and backward.  Sequences of L consecutive tokens; head h reads key/value head h / (H / Hkv).
-// Scores, softmax and the value sums run in float64 (one block per query row, or per key row for
-// the key/value gradients) so that the bf16 roundings of the block fall where exact arithmetic
-// puts them; the probabilities and score gradients are kept as float32 [S][H][L][L] with zeros
-// above the diagonal.
+//
+// The contractions run on v_mfma_f32_32x32x16_bf16, one 32 x 32 output tile per wave:
+//   scores  S = qr kr^T / sqrt(hd)       bf16 operands, exact products, float32 sums
+//   output  O = P v                      P carried as three bf16 terms (all 24 bits)
+//   dP = dO v^T                          dO in three bf16 terms (dP - D cancels)
+//   dQ = dS kr, dK = dS^T qr, dV = P^T dO   float32 operands as bf16 hi/lo
+// The softmax and the row term D_i = sum_j P_ij dP_ij = dO_i . O_i run in float64.  P is kept as
+// float32 [S][H][L][L] (rows complete, zeros above the diagonal); the backward writes dS, dS^T
+// and P^T as bf16 hi/lo pairs for the tiles on or below the diagonal, so every MFMA operand is a
+// 16-byte load of 8 consecutive contraction indices.
 #include "common.h"
 #include "kernels.h"
 
@@ -12,18 +18,6 @@ namespace realq {
 
 namespace {
 constexpr int TB = 256;
-__device__ __forceinline__ double block_reduce(double v, double* red, bool is_max) {
-    red[threadIdx.x] = v;
-    __syncthreads();
-    for (int s = TB / 2; s > 0; s >>= 1) {
-        if ((int)threadIdx.x < s)
-            red[threadIdx.x] = is_max ? fmax(red[threadIdx.x], red[threadIdx.x + s]) : red[threadIdx.x] + red[threadIdx.x + s];
-        __syncthreads();
-    }
-    const double r = red[0];
-    __syncthreads();
-    return r;
-}
 }  // namespace
 
 // Rotary embedding over pairs (i, i + hd/2) of each head, angle (t mod L) base^(-2i/hd):
@@ -74,153 +68,296 @@ hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t h
     return hipGetLastError();
 }
 
-// P[s][h][i][j] = softmax over j <= i of qr_i . kr_j / sqrt(hd) (zeros for j > i); one block per
-// (s, h, i).  qr [T][H hd], kr [T][Hkv hd] bf16.
-__global__ __launch_bounds__(256) void attn_probs_kernel(const uint16_t* __restrict__ qr,
-                                                         const uint16_t* __restrict__ kr, int64_t H, int64_t Hkv,
-                                                         int64_t hd, int64_t L, float* __restrict__ P) {
-    extern __shared__ double sh[];  // [hd] query row, then [L] scores
-    __shared__ double red[TB];
-    double* qs = sh;
-    double* sc = sh + hd;
-    const int64_t row = blockIdx.x;  // (s * H + h) * L + i
-    const int64_t i = row % L, sh_ = row / L, h = sh_ % H, s = sh_ / H;
-    const int64_t g = h / (H / Hkv);
-    const int64_t tq = s * L + i;
-    for (int64_t c = threadIdx.x; c < hd; c += TB) qs[c] = (double)bf2f(qr[tq * H * hd + h * hd + c]);
-    __syncthreads();
-    const double scale = 1.0 / sqrt((double)hd);
-    double mx = -INFINITY;
-    for (int64_t j = threadIdx.x; j <= i; j += TB) {
-        const uint16_t* kj = kr + (s * L + j) * Hkv * hd + g * hd;
-        double acc = 0.0;
-        for (int64_t c = 0; c < hd; ++c) acc += qs[c] * (double)bf2f(kj[c]);
-        sc[j] = acc * scale;
-        mx = fmax(mx, sc[j]);
+// ---------------------------------------------------------------- MFMA attention
+//
+// Fragments of v_mfma_f32_32x32x16_bf16 (C = A B^T over one 16-wide k step): a lane supplies 8
+// consecutive k (offset 8 (lane / 32)) of row (lane % 32) of A and of B; acc[e] is C[r][c] with
+// r = 8 (e / 4) + 4 (lane / 32) + e % 4 and c = lane % 32.
+namespace {
+constexpr int AT = 32;
+
+__device__ __forceinline__ bf16x8 ld8(const uint16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
+
+__device__ __forceinline__ void split8x3(const float* p, bf16x8& hi, bf16x8& lo, bf16x8& lo2) {
+    const f32x4 x0 = *reinterpret_cast<const f32x4*>(p);
+    const f32x4 x1 = *reinterpret_cast<const f32x4*>(p + 4);
+    u16x8 h, l, l2;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const float x = u < 4 ? x0[u] : x1[u - 4];
+        h[u] = f2bf(x);
+        const float r = x - bf2f(h[u]);
+        l[u] = f2bf(r);
+        l2[u] = f2bf(r - bf2f(l[u]));
     }
-    mx = block_reduce(mx, red, true);
-    double sum = 0.0;
-    for (int64_t j = threadIdx.x; j <= i; j += TB) {
-        const double e = exp(sc[j] - mx);
-        sc[j] = e;
-        sum += e;
-    }
-    sum = block_reduce(sum, red, false);
-    float* prow = P + row * L;
-    for (int64_t j = threadIdx.x; j < L; j += TB) prow[j] = j <= i ? (float)(sc[j] / sum) : 0.f;
+    hi = __builtin_bit_cast(bf16x8, h);
+    lo = __builtin_bit_cast(bf16x8, l);
+    lo2 = __builtin_bit_cast(bf16x8, l2);
 }
 
-// O[t][h hd + c] = bf16(sum_{j <= i} P[s][h][i][j] v[s L + j][g hd + c]); one block per (s, h, i).
-__global__ __launch_bounds__(256) void attn_out_kernel(const float* __restrict__ P, const uint16_t* __restrict__ v,
-                                                       int64_t H, int64_t Hkv, int64_t hd, int64_t L,
-                                                       uint16_t* __restrict__ O) {
-    const int64_t row = blockIdx.x;
-    const int64_t i = row % L, sh_ = row / L, h = sh_ % H, s = sh_ / H;
+__device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+    f32x16 z;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) z[e] = 0.f;
+    return z;
+}
+
+__device__ __forceinline__ int acc_row(int e, int lane) { return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3); }
+
+__device__ double block_sum(double v, double* red) {
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = TB / 2; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+        __syncthreads();
+    }
+    const double r = red[0];
+    __syncthreads();
+    return r;
+}
+__device__ double block_max(double v, double* red) {
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = TB / 2; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + s]);
+        __syncthreads();
+    }
+    const double r = red[0];
+    __syncthreads();
+    return r;
+}
+}  // namespace
+
+// Raw scaled scores of the causal tiles: grid (S H nt, ceil(nt / 4)), 4 waves, wave w of block y
+// takes key tile jt = 4 y + w of query tile it (tiles above the diagonal are skipped).
+__global__ __launch_bounds__(256) void attn_scores_kernel(const uint16_t* __restrict__ qr,
+                                                          const uint16_t* __restrict__ kr, int64_t H, int64_t Hkv,
+                                                          int64_t hd, int64_t L, float* __restrict__ P) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t nt = L / AT;
+    const int64_t it = blockIdx.x % nt, sh = blockIdx.x / nt, h = sh % H, s = sh / H;
+    const int64_t jt = (int64_t)blockIdx.y * 4 + wave;
+    if (jt > it) return;
     const int64_t g = h / (H / Hkv);
-    const float* prow = P + row * L;
-    for (int64_t c = threadIdx.x; c < hd; c += TB) {
-        double acc = 0.0;
-        for (int64_t j = 0; j <= i; ++j) acc += (double)prow[j] * (double)bf2f(v[(s * L + j) * Hkv * hd + g * hd + c]);
-        O[(s * L + i) * H * hd + h * hd + c] = f2bf((float)acc);
+    const uint16_t* a = qr + (s * L + it * AT + (lane & 31)) * (H * hd) + h * hd + 8 * (lane >> 5);
+    const uint16_t* b = kr + (s * L + jt * AT + (lane & 31)) * (Hkv * hd) + g * hd + 8 * (lane >> 5);
+    f32x16 acc = zero16();
+    for (int64_t k0 = 0; k0 < hd; k0 += 16) acc = mfma(ld8(a + k0), ld8(b + k0), acc);
+    const float scale = (float)(1.0 / sqrt((double)hd));
+    float* out = P + (sh * L + it * AT) * L + jt * AT + (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) out[(int64_t)acc_row(e, lane) * L] = acc[e] * scale;
+}
+
+// Row softmax over j <= i in float64; the row is completed with zeros.  One block per row.
+__global__ __launch_bounds__(256) void attn_softmax_kernel(int64_t L, float* __restrict__ P) {
+    __shared__ double red[TB];
+    const int64_t row = blockIdx.x, i = row % L;
+    float* p = P + row * L;
+    double mx = -INFINITY;
+    for (int64_t j = threadIdx.x; j <= i; j += TB) mx = fmax(mx, (double)p[j]);
+    mx = block_max(mx, red);
+    double sum = 0.0;
+    for (int64_t j = threadIdx.x; j <= i; j += TB) sum += exp((double)p[j] - mx);
+    sum = block_sum(sum, red);
+    for (int64_t j = threadIdx.x; j < L; j += TB) p[j] = j <= i ? (float)(exp((double)p[j] - mx) / sum) : 0.f;
+}
+
+// O = P v: grid (S H nt, ceil(hd / 32 / 4)), wave w of block y takes value-column tile 4 y + w.
+// P rows as three bf16 terms, vt = v^T [Hkv hd][T].  Writes O32 (float32) and O (bf16).
+__global__ __launch_bounds__(256) void attn_pv_kernel(const float* __restrict__ P, const uint16_t* __restrict__ vt,
+                                                      int64_t T, int64_t H, int64_t Hkv, int64_t hd, int64_t L,
+                                                      float* __restrict__ O32, uint16_t* __restrict__ O) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t nt = L / AT;
+    const int64_t it = blockIdx.x % nt, sh = blockIdx.x / nt, h = sh % H, s = sh / H;
+    const int64_t ct = (int64_t)blockIdx.y * 4 + wave;
+    if (ct >= hd / AT) return;
+    const int64_t g = h / (H / Hkv);
+    const float* a = P + (sh * L + it * AT + (lane & 31)) * L + 8 * (lane >> 5);
+    const uint16_t* b = vt + (g * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
+    f32x16 acc = zero16();
+    const int64_t jend = (it + 1) * AT;
+    for (int64_t j0 = 0; j0 < jend; j0 += 16) {
+        bf16x8 ah, al, al2;
+        split8x3(a + j0, ah, al, al2);
+        const bf16x8 bv = ld8(b + j0);
+        acc = mfma(ah, bv, acc);
+        acc = mfma(al, bv, acc);
+        acc = mfma(al2, bv, acc);
+    }
+    const int64_t col = h * hd + ct * AT + (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int64_t t = s * L + it * AT + acc_row(e, lane);
+        O32[t * H * hd + col] = acc[e];
+        O[t * H * hd + col] = f2bf(acc[e]);
     }
 }
 
 hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, int64_t T, int64_t H, int64_t Hkv,
-                    int64_t hd, int64_t L, float* P, uint16_t* O, hipStream_t st) {
+                    int64_t hd, int64_t L, float* P, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st) {
     if (T <= 0) return hipSuccess;
-    const int64_t rows = (T / L) * H * L;
-    const size_t shm = (size_t)(hd + L) * sizeof(double);
-    hipLaunchKernelGGL(attn_probs_kernel, dim3((unsigned)rows), dim3(TB), shm, st, qr, kr, H, Hkv, hd, L, P);
-    hipError_t e = hipGetLastError();
+    const int64_t S = T / L, nt = L / AT;
+    hipError_t e = transpose_u16(v, Hkv * hd, vt, T, T, Hkv * hd, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_out_kernel, dim3((unsigned)rows), dim3(TB), 0, st, P, v, H, Hkv, hd, L, O);
+    hipLaunchKernelGGL(attn_scores_kernel, dim3((unsigned)(S * H * nt), (unsigned)((nt + 3) / 4)), dim3(256), 0, st,
+                       qr, kr, H, Hkv, hd, L, P);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_softmax_kernel, dim3((unsigned)(S * H * L)), dim3(TB), 0, st, L, P);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_pv_kernel, dim3((unsigned)(S * H * nt), (unsigned)((hd / AT + 3) / 4)), dim3(256), 0, st,
+                       P, vt, T, H, Hkv, hd, L, O32, O);
     return hipGetLastError();
 }
 
-// dS[s][h][i][j] = P_ij (dP_ij - sum_j' P_ij' dP_ij'), dP_ij = dO_i . v_j (j <= i; zeros above).
+// D[t][h] = sum_c dO[t][h hd + c] O32[t][h hd + c] (float64); one thread per (t, h).
+__global__ void attn_rowdot_kernel(const float* __restrict__ dO, const float* __restrict__ O32, int64_t TH,
+                                   int64_t hd, double* __restrict__ D) {
+    for (int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; r < TH; r += (int64_t)gridDim.x * blockDim.x) {
+        const float* a = dO + r * hd;
+        const float* b = O32 + r * hd;
+        double acc = 0.0;
+        for (int64_t c = 0; c < hd; ++c) acc += (double)a[c] * (double)b[c];
+        D[r] = acc;
+    }
+}
+
+// dS = P o (dP - D), dP = dO v^T (dO in three bf16 terms), for the causal tiles (same grid as the scores);
+// writes dS [i][j], dS^T and P^T [j][i] as bf16 hi/lo.
 __global__ __launch_bounds__(256) void attn_ds_kernel(const float* __restrict__ P, const float* __restrict__ dO,
-                                                      const uint16_t* __restrict__ v, int64_t H, int64_t Hkv,
-                                                      int64_t hd, int64_t L, float* __restrict__ dS) {
-    extern __shared__ double sh[];  // [hd] dO row, then [L] dP
-    __shared__ double red[TB];
-    double* dos = sh;
-    double* dp = sh + hd;
-    const int64_t row = blockIdx.x;
-    const int64_t i = row % L, sh_ = row / L, h = sh_ % H, s = sh_ / H;
-    const int64_t g = h / (H / Hkv);
-    for (int64_t c = threadIdx.x; c < hd; c += TB) dos[c] = (double)dO[(s * L + i) * H * hd + h * hd + c];
-    __syncthreads();
-    const float* prow = P + row * L;
-    double dsum = 0.0;
-    for (int64_t j = threadIdx.x; j <= i; j += TB) {
-        const uint16_t* vj = v + (s * L + j) * Hkv * hd + g * hd;
-        double acc = 0.0;
-        for (int64_t c = 0; c < hd; ++c) acc += dos[c] * (double)bf2f(vj[c]);
-        dp[j] = acc;
-        dsum += (double)prow[j] * acc;
-    }
-    dsum = block_reduce(dsum, red, false);
-    float* drow = dS + row * L;
-    for (int64_t j = threadIdx.x; j < L; j += TB) drow[j] = j <= i ? (float)((double)prow[j] * (dp[j] - dsum)) : 0.f;
-}
-
-// dqr[t][h hd + c] = sum_{j <= i} dS_ij kr[s L + j][g hd + c] / sqrt(hd); one block per (s, h, i).
-__global__ __launch_bounds__(256) void attn_dq_kernel(const float* __restrict__ dS, const uint16_t* __restrict__ kr,
+                                                      const uint16_t* __restrict__ v, const double* __restrict__ D,
                                                       int64_t H, int64_t Hkv, int64_t hd, int64_t L,
-                                                      float* __restrict__ dq) {
-    const int64_t row = blockIdx.x;
-    const int64_t i = row % L, sh_ = row / L, h = sh_ % H, s = sh_ / H;
+                                                      uint16_t* __restrict__ dSh, uint16_t* __restrict__ dSl,
+                                                      uint16_t* __restrict__ dSth, uint16_t* __restrict__ dStl,
+                                                      uint16_t* __restrict__ Pth, uint16_t* __restrict__ Ptl) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t nt = L / AT;
+    const int64_t it = blockIdx.x % nt, sh = blockIdx.x / nt, h = sh % H, s = sh / H;
+    const int64_t jt = (int64_t)blockIdx.y * 4 + wave;
+    if (jt > it) return;
     const int64_t g = h / (H / Hkv);
-    const float* drow = dS + row * L;
-    const double scale = 1.0 / sqrt((double)hd);
-    for (int64_t c = threadIdx.x; c < hd; c += TB) {
-        double acc = 0.0;
-        for (int64_t j = 0; j <= i; ++j) acc += (double)drow[j] * (double)bf2f(kr[(s * L + j) * Hkv * hd + g * hd + c]);
-        dq[(s * L + i) * H * hd + h * hd + c] = (float)(acc * scale);
+    const float* a = dO + (s * L + it * AT + (lane & 31)) * (H * hd) + h * hd + 8 * (lane >> 5);
+    const uint16_t* b = v + (s * L + jt * AT + (lane & 31)) * (Hkv * hd) + g * hd + 8 * (lane >> 5);
+    f32x16 acc = zero16();
+    for (int64_t k0 = 0; k0 < hd; k0 += 16) {  // dO in three terms: dP - D cancels
+        bf16x8 ah, al, al2;
+        split8x3(a + k0, ah, al, al2);
+        const bf16x8 bv = ld8(b + k0);
+        acc = mfma(ah, bv, acc);
+        acc = mfma(al, bv, acc);
+        acc = mfma(al2, bv, acc);
+    }
+    const int64_t j = jt * AT + (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int64_t i = it * AT + acc_row(e, lane);
+        const int64_t ij = (sh * L + i) * L + j, ji = (sh * L + j) * L + i;
+        const float p = P[ij];
+        const float ds = (float)((double)p * ((double)acc[e] - D[(s * L + i) * H + h]));
+        uint16_t hh, ll;
+        split_bf16(ds, hh, ll);
+        dSh[ij] = hh;
+        dSl[ij] = ll;
+        dSth[ji] = hh;
+        dStl[ji] = ll;
+        split_bf16(p, hh, ll);
+        Pth[ji] = hh;
+        Ptl[ji] = ll;
     }
 }
 
-// For key/value row j of head g (one block per (s, g, j)), summed over the query heads of g:
-//   dkr[j][c] = sum_h sum_{i >= j} dS[h][i][j] qr[i][h hd + c] / sqrt(hd)
-//   dv[j][c]  = sum_h sum_{i >= j} P[h][i][j]  dO[i][h hd + c]
-__global__ __launch_bounds__(256) void attn_dkv_kernel(const float* __restrict__ P, const float* __restrict__ dS,
-                                                       const uint16_t* __restrict__ qr, const float* __restrict__ dO,
-                                                       int64_t H, int64_t Hkv, int64_t hd, int64_t L,
-                                                       float* __restrict__ dk, float* __restrict__ dv) {
-    const int64_t row = blockIdx.x;  // (s * Hkv + g) * L + j
-    const int64_t j = row % L, sg = row / L, g = sg % Hkv, s = sg / Hkv;
+// dqr = dS kr / sqrt(hd): grid (S H nt, ceil(hd / 32 / 4)); kt = kr^T [Hkv hd][T].
+__global__ __launch_bounds__(256) void attn_dq_kernel(const uint16_t* __restrict__ dSh, const uint16_t* __restrict__ dSl,
+                                                      const uint16_t* __restrict__ kt, int64_t T, int64_t H,
+                                                      int64_t Hkv, int64_t hd, int64_t L, float* __restrict__ dq) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t nt = L / AT;
+    const int64_t it = blockIdx.x % nt, sh = blockIdx.x / nt, h = sh % H, s = sh / H;
+    const int64_t ct = (int64_t)blockIdx.y * 4 + wave;
+    if (ct >= hd / AT) return;
+    const int64_t g = h / (H / Hkv);
+    const int64_t arow = (sh * L + it * AT + (lane & 31)) * L + 8 * (lane >> 5);
+    const uint16_t* b = kt + (g * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
+    f32x16 acc = zero16();
+    const int64_t jend = (it + 1) * AT;
+    for (int64_t j0 = 0; j0 < jend; j0 += 16) {
+        const bf16x8 bv = ld8(b + j0);
+        acc = mfma(ld8(dSh + arow + j0), bv, acc);
+        acc = mfma(ld8(dSl + arow + j0), bv, acc);
+    }
+    const float scale = (float)(1.0 / sqrt((double)hd));
+    const int64_t col = h * hd + ct * AT + (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dq[(s * L + it * AT + acc_row(e, lane)) * H * hd + col] = acc[e] * scale;
+}
+
+// dkr = sum_h dS^T qr / sqrt(hd), dv = sum_h P^T dO over the query heads of key/value head g:
+// grid (S Hkv nt, ceil(hd / 32 / 4)); qt = qr^T [H hd][T], dOt = dO^T as hi/lo [H hd][T].
+__global__ __launch_bounds__(256) void attn_dkv_kernel(const uint16_t* __restrict__ dSth,
+                                                       const uint16_t* __restrict__ dStl,
+                                                       const uint16_t* __restrict__ Pth, const uint16_t* __restrict__ Ptl,
+                                                       const uint16_t* __restrict__ qt,
+                                                       const uint16_t* __restrict__ dOth,
+                                                       const uint16_t* __restrict__ dOtl, int64_t T, int64_t H,
+                                                       int64_t Hkv, int64_t hd, int64_t L, float* __restrict__ dk,
+                                                       float* __restrict__ dv) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t nt = L / AT;
+    const int64_t jt = blockIdx.x % nt, sg = blockIdx.x / nt, g = sg % Hkv, s = sg / Hkv;
+    const int64_t ct = (int64_t)blockIdx.y * 4 + wave;
+    if (ct >= hd / AT) return;
     const int64_t rep = H / Hkv;
-    const double scale = 1.0 / sqrt((double)hd);
-    for (int64_t c = threadIdx.x; c < hd; c += TB) {
-        double ak = 0.0, av = 0.0;
-        for (int64_t hh = 0; hh < rep; ++hh) {
-            const int64_t h = g * rep + hh;
-            const int64_t base = ((s * H + h) * L) * L + j;  // element [s][h][i][j] = base + i L
-            for (int64_t i = j; i < L; ++i) {
-                const int64_t t = s * L + i;
-                ak += (double)dS[base + i * L] * (double)bf2f(qr[t * H * hd + h * hd + c]);
-                av += (double)P[base + i * L] * (double)dO[t * H * hd + h * hd + c];
-            }
+    f32x16 ak = zero16(), av = zero16();
+    for (int64_t hh = 0; hh < rep; ++hh) {
+        const int64_t h = g * rep + hh, sh = s * H + h;
+        const int64_t arow = (sh * L + jt * AT + (lane & 31)) * L + 8 * (lane >> 5);
+        const int64_t brow = (h * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
+        for (int64_t i0 = jt * AT; i0 < L; i0 += 16) {
+            const bf16x8 q = ld8(qt + brow + i0);
+            ak = mfma(ld8(dSth + arow + i0), q, ak);
+            ak = mfma(ld8(dStl + arow + i0), q, ak);
+            const bf16x8 ph = ld8(Pth + arow + i0);
+            const bf16x8 doh = ld8(dOth + brow + i0);
+            av = mfma(ph, doh, av);
+            av = mfma(ld8(Ptl + arow + i0), doh, av);
+            av = mfma(ph, ld8(dOtl + brow + i0), av);
         }
-        dk[(s * L + j) * Hkv * hd + g * hd + c] = (float)(ak * scale);
-        dv[(s * L + j) * Hkv * hd + g * hd + c] = (float)av;
+    }
+    const float scale = (float)(1.0 / sqrt((double)hd));
+    const int64_t col = g * hd + ct * AT + (lane & 31);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int64_t t = s * L + jt * AT + acc_row(e, lane);
+        dk[t * Hkv * hd + col] = ak[e] * scale;
+        dv[t * Hkv * hd + col] = av[e];
     }
 }
 
-hipError_t attn_bwd(const float* P, const float* dO, const uint16_t* qr, const uint16_t* kr, const uint16_t* v,
-                    int64_t T, int64_t H, int64_t Hkv, int64_t hd, int64_t L, float* dS, float* dq, float* dk,
-                    float* dv, hipStream_t st) {
+hipError_t attn_bwd(const float* P, const float* O32, const float* dO, const uint16_t* qr, const uint16_t* kr,
+                    const uint16_t* v, int64_t T, int64_t H, int64_t Hkv, int64_t hd, int64_t L, const AttnScratch& w,
+                    float* dq, float* dk, float* dv, hipStream_t st) {
     if (T <= 0) return hipSuccess;
-    const int64_t S = T / L;
-    const int64_t rows = S * H * L;
-    const size_t shm = (size_t)(hd + L) * sizeof(double);
-    hipLaunchKernelGGL(attn_ds_kernel, dim3((unsigned)rows), dim3(TB), shm, st, P, dO, v, H, Hkv, hd, L, dS);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)rows), dim3(TB), 0, st, dS, kr, H, Hkv, hd, L, dq);
+    const int64_t S = T / L, nt = L / AT;
+    hipError_t e;
+    hipLaunchKernelGGL(attn_rowdot_kernel, dim3(grid_of(T * H)), dim3(TB), 0, st, dO, O32, T * H, hd, w.D);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_dkv_kernel, dim3((unsigned)(S * Hkv * L)), dim3(TB), 0, st, P, dS, qr, dO, H, Hkv, hd, L,
-                       dk, dv);
+    if ((e = transpose_u16(kr, Hkv * hd, w.kt, T, T, Hkv * hd, st)) != hipSuccess) return e;
+    if ((e = transpose_u16(qr, H * hd, w.qt, T, T, H * hd, st)) != hipSuccess) return e;
+    if ((e = transpose_split_f32(dO, H * hd, w.dOth, w.dOtl, T, T, H * hd, st)) != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_ds_kernel, dim3((unsigned)(S * H * nt), (unsigned)((nt + 3) / 4)), dim3(256), 0, st, P, dO,
+                       v, w.D, H, Hkv, hd, L, w.dSh, w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const unsigned cy = (unsigned)((hd / AT + 3) / 4);
+    hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)(S * H * nt), cy), dim3(256), 0, st, w.dSh, w.dSl, w.kt, T, H,
+                       Hkv, hd, L, dq);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_dkv_kernel, dim3((unsigned)(S * Hkv * nt), cy), dim3(256), 0, st, w.dSth, w.dStl, w.Pth,
+                       w.Ptl, w.qt, w.dOth, w.dOtl, T, H, Hkv, hd, L, dk, dv);
     return hipGetLastError();
 }
 

@@ -426,8 +426,8 @@ struct DecDims {
 };
 
 struct DecF {  // buffers of one forward of the decoder block
-    uint16_t *h1, *q, *k, *v, *qr, *kr, *O, *o;
-    float *P, *x2;
+    uint16_t *h1, *q, *k, *v, *qr, *kr, *O, *o, *vt;
+    float *P, *O32, *x2;
     Fwd mlp;
 };
 
@@ -439,7 +439,8 @@ int alloc_decf(realq_ctx* ctx, const char* tag, const DecDims& D, DecF& F) {
         (rc = ws(ctx, (t + "k").c_str(), T * D.Hk, F.k)) || (rc = ws(ctx, (t + "v").c_str(), T * D.Hk, F.v)) ||
         (rc = ws(ctx, (t + "qr").c_str(), T * D.Hq, F.qr)) || (rc = ws(ctx, (t + "kr").c_str(), T * D.Hk, F.kr)) ||
         (rc = ws(ctx, (t + "O").c_str(), T * D.Hq, F.O)) || (rc = ws(ctx, (t + "oo").c_str(), T * D.d, F.o)) ||
-        (rc = ws(ctx, (t + "P").c_str(), T * D.H * D.L, F.P)) || (rc = ws(ctx, (t + "x2").c_str(), T * D.d, F.x2)))
+        (rc = ws(ctx, (t + "P").c_str(), T * D.H * D.L, F.P)) || (rc = ws(ctx, (t + "x2").c_str(), T * D.d, F.x2)) ||
+        (rc = ws(ctx, (t + "O32").c_str(), T * D.Hq, F.O32)) || (rc = ws(ctx, (t + "vt").c_str(), T * D.Hk, F.vt)))
         return rc;
     return alloc_fwd(ctx, (t + "m").c_str(), T, D.d, D.f, F.mlp);
 }
@@ -454,16 +455,13 @@ int dec_attn(realq_ctx* ctx, const DecW& w, const uint16_t* xb, const float* xf,
         if (xb) RQ_HIP(ctx, realq::rmsnorm_bf16(xb, D.T, D.d, w.gamma1, D.eps, F.h1, s));
         else RQ_HIP(ctx, realq::rmsnorm_f32(xf, D.T, D.d, w.gamma1, D.eps, F.h1, s));
     }
-    if (mask & 1) {
-        if ((rc = lin_bf16(ctx, w.q, D.Hq, D.d, F.h1, D.T, F.q))) return rc;
-        RQ_HIP(ctx, realq::rope_fwd(F.q, F.qr, D.T, D.H, D.hd, D.L, D.base, s));
-    }
-    if (mask & 2) {
-        if ((rc = lin_bf16(ctx, w.k, D.Hk, D.d, F.h1, D.T, F.k))) return rc;
-        RQ_HIP(ctx, realq::rope_fwd(F.k, F.kr, D.T, D.Hkv, D.hd, D.L, D.base, s));
-    }
+    if ((mask & 1) && (rc = lin_bf16(ctx, w.q, D.Hq, D.d, F.h1, D.T, F.q))) return rc;
+    if ((mask & 2) && (rc = lin_bf16(ctx, w.k, D.Hk, D.d, F.h1, D.T, F.k))) return rc;
     if ((mask & 4) && (rc = lin_bf16(ctx, w.v, D.Hk, D.d, F.h1, D.T, F.v))) return rc;
-    RQ_HIP(ctx, realq::attn_fwd(F.qr, F.kr, F.v, D.T, D.H, D.Hkv, D.hd, D.L, F.P, F.O, s));
+    Timed tm(ctx, "attention");
+    if (mask & 1) RQ_HIP(ctx, realq::rope_fwd(F.q, F.qr, D.T, D.H, D.hd, D.L, D.base, s));
+    if (mask & 2) RQ_HIP(ctx, realq::rope_fwd(F.k, F.kr, D.T, D.Hkv, D.hd, D.L, D.base, s));
+    RQ_HIP(ctx, realq::attn_fwd(F.qr, F.kr, F.v, D.T, D.H, D.Hkv, D.hd, D.L, F.P, F.O32, F.O, F.vt, s));
     return REALQ_OK;
 }
 
@@ -483,7 +481,8 @@ int dec_forward(realq_ctx* ctx, const DecW& w, const uint16_t* xb, const float* 
 }
 
 struct DecWork {  // backward work buffers (sized for the widest use)
-    float *dz, *du, *dx2, *dO, *dq, *dk, *dv, *dqr, *dkr, *dS, *dh1;
+    float *dz, *du, *dx2, *dO, *dq, *dk, *dv, *dqr, *dkr, *dh1;
+    realq::AttnScratch at;  // shared by every DecWork of a context (used one call at a time)
     Split sg, sda, sdb, sdx2, sdO, sdq, sdk, sdv;
 };
 
@@ -495,12 +494,21 @@ int alloc_work(realq_ctx* ctx, const char* tag, const DecDims& D, DecWork& Wk) {
         (rc = ws(ctx, (t + "dx2").c_str(), T * D.d, Wk.dx2)) || (rc = ws(ctx, (t + "dO").c_str(), T * D.Hq, Wk.dO)) ||
         (rc = ws(ctx, (t + "dq").c_str(), T * D.Hq, Wk.dq)) || (rc = ws(ctx, (t + "dk").c_str(), T * D.Hk, Wk.dk)) ||
         (rc = ws(ctx, (t + "dv").c_str(), T * D.Hk, Wk.dv)) || (rc = ws(ctx, (t + "dqr").c_str(), T * D.Hq, Wk.dqr)) ||
-        (rc = ws(ctx, (t + "dkr").c_str(), T * D.Hk, Wk.dkr)) || (rc = ws(ctx, (t + "dS").c_str(), T * D.H * D.L, Wk.dS)) ||
+        (rc = ws(ctx, (t + "dkr").c_str(), T * D.Hk, Wk.dkr)) ||
         (rc = ws(ctx, (t + "dh1").c_str(), T * D.d, Wk.dh1)) || (rc = ws_split(ctx, t + "sg", T * D.d, Wk.sg)) ||
         (rc = ws_split(ctx, t + "sda", T * D.f, Wk.sda)) || (rc = ws_split(ctx, t + "sdb", T * D.f, Wk.sdb)) ||
         (rc = ws_split(ctx, t + "sdx2", T * D.d, Wk.sdx2)) || (rc = ws_split(ctx, t + "sdO", T * D.Hq, Wk.sdO)) ||
         (rc = ws_split(ctx, t + "sdq", T * D.Hq, Wk.sdq)) || (rc = ws_split(ctx, t + "sdk", T * D.Hk, Wk.sdk)) ||
         (rc = ws_split(ctx, t + "sdv", T * D.Hk, Wk.sdv)))
+        return rc;
+    realq::AttnScratch& a = Wk.at;
+    const int64_t TL = T * D.H * D.L;
+    if ((rc = ws(ctx, "att_D", T * D.H, a.D)) || (rc = ws(ctx, "att_dSh", TL, a.dSh)) ||
+        (rc = ws(ctx, "att_dSl", TL, a.dSl)) || (rc = ws(ctx, "att_dSth", TL, a.dSth)) ||
+        (rc = ws(ctx, "att_dStl", TL, a.dStl)) || (rc = ws(ctx, "att_Pth", TL, a.Pth)) ||
+        (rc = ws(ctx, "att_Ptl", TL, a.Ptl)) || (rc = ws(ctx, "att_kt", T * D.Hk, a.kt)) ||
+        (rc = ws(ctx, "att_qt", T * D.Hq, a.qt)) || (rc = ws(ctx, "att_dOth", T * D.Hq, a.dOth)) ||
+        (rc = ws(ctx, "att_dOtl", T * D.Hq, a.dOtl)))
         return rc;
     return REALQ_OK;
 }
@@ -535,7 +543,9 @@ int back_to_qkv(realq_ctx* ctx, const DecW& w, const DecDims& D, const DecF& F, 
     const int64_t T = D.T;
     RQ_HIP(ctx, realq::scale_split(Wk.dx2, 1.f, nullptr, Wk.sdx2.hi, Wk.sdx2.lo, T * D.d, s));
     if ((rc = prod3(ctx, Wk.sdx2, T, D.d, w.oT, D.Hq, 1.f, Wk.dO))) return rc;
-    RQ_HIP(ctx, realq::attn_bwd(F.P, Wk.dO, F.qr, F.kr, F.v, T, D.H, D.Hkv, D.hd, D.L, Wk.dS, Wk.dqr, Wk.dkr, Wk.dv, s));
+    Timed tm(ctx, "attention");
+    RQ_HIP(ctx, realq::attn_bwd(F.P, F.O32, Wk.dO, F.qr, F.kr, F.v, T, D.H, D.Hkv, D.hd, D.L, Wk.at, Wk.dqr, Wk.dkr,
+                                Wk.dv, s));
     RQ_HIP(ctx, realq::rope_inv(Wk.dqr, Wk.dq, T, D.H, D.hd, D.L, D.base, s));
     RQ_HIP(ctx, realq::rope_inv(Wk.dkr, Wk.dk, T, D.Hkv, D.hd, D.L, D.base, s));
     return REALQ_OK;
@@ -555,8 +565,8 @@ int check_decoder(realq_ctx* ctx, const realq_decoder_desc* Dd, const char* who,
     D.Hk = D.Hkv * D.hd;
     D.base = (double)Dd->rope_base;
     D.eps = (double)Dd->eps;
-    if (D.T < 1 || D.d < 1 || D.f < 1 || D.L < 1 || D.L > 4096 || D.T % D.L || D.H < 1 || D.Hkv < 1 || D.H % D.Hkv ||
-        D.hd < 2 || D.hd % 2 || D.hd > 256 || D.d % 8 || D.f % 8 || D.Hq % 8 || D.Hk % 8)
+    if (D.T < 1 || D.d < 1 || D.f < 1 || D.L < 32 || D.L > 4096 || D.L % 32 || D.T % D.L || D.H < 1 || D.Hkv < 1 ||
+        D.H % D.Hkv || D.hd < 32 || D.hd % 32 || D.hd > 256 || D.d % 8 || D.f % 8)
         return set_error(ctx, REALQ_ERR_SHAPE, std::string(who) + ": unsupported shape (see realq.h)");
     const realq_decoder_block& B0 = Dd->blk;
     if (!Dd->X || !B0.gamma1 || !B0.Wq || !B0.Wk || !B0.Wv || !B0.Wo || !B0.mlp.gamma || !B0.mlp.Wg || !B0.mlp.Wu ||

@@ -172,6 +172,58 @@ def test_single_token_sequences_make_attention_the_identity_on_values():
     assert (P == 1.0).all()
 
 
+def test_rope_pair0_turns_by_the_position_and_scores_depend_on_relative_position():
+    """Pair 0 has frequency base^0 = 1, so at position t it turns by exactly t radians; and a
+    rotary embedding makes q(t1) . k(t2) a function of t1 - t2 only."""
+    hd, L = 8, 16
+    e0 = np.zeros((L, hd))
+    e0[:, 0] = 1.0
+    y = B.rope(e0, 1, hd, L)
+    t = np.arange(L)
+    np.testing.assert_allclose(y[:, 0], np.cos(t), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(y[:, hd // 2], np.sin(t), rtol=0, atol=1e-14)
+    r = np.random.default_rng(23)
+    q, k = r.standard_normal(hd), r.standard_normal(hd)
+    Q = B.rope(np.tile(q, (L, 1)), 1, hd, L)
+    K = B.rope(np.tile(k, (L, 1)), 1, hd, L)
+    S = Q @ K.T
+    for dlt in range(-3, 4):
+        vals = [S[i, i - dlt] for i in range(max(0, dlt), min(L, L + dlt))]
+        np.testing.assert_allclose(vals, vals[0], rtol=1e-12, atol=1e-12)
+
+
+def test_zero_queries_give_causal_prefix_means_per_sequence_and_kv_head():
+    """With qr = 0 every allowed score is 0, so each query averages the values of its own sequence up
+    to and including its position, read from key/value head h // (H / Hkv)."""
+    r = np.random.default_rng(24)
+    H, Hkv, hd, L = 4, 2, 3, 5
+    T = 2 * L
+    v = r.standard_normal((T, Hkv * hd))
+    O, P = B.attention_forward(np.zeros((T, H * hd)), r.standard_normal((T, Hkv * hd)), v, H, Hkv, hd, L)
+    for t in range(T):
+        s0 = (t // L) * L
+        for h in range(H):
+            g = h // (H // Hkv)
+            mean = v[s0:t + 1, g * hd:(g + 1) * hd].mean(axis=0)
+            np.testing.assert_allclose(O[t, h * hd:(h + 1) * hd], mean, rtol=0, atol=1e-14)
+    assert np.allclose(P.sum(axis=-1), 1.0) and (np.triu(P[0, 0], 1) == 0).all()
+
+
+def test_two_token_scores_are_scaled_by_root_head_dim():
+    """hd = 4, k0 = 0, k1 = e0, q1 = 2 ln(3) e0: the scores of query 1 are 0 and ln 3, so its
+    weights are exactly 1/4 and 3/4."""
+    hd = 4
+    qr = np.zeros((2, hd))
+    qr[1, 0] = 2.0 * np.log(3.0)
+    kr = np.zeros((2, hd))
+    kr[1, 0] = 1.0
+    v = np.array([[1.0, 0, 0, 0], [0, 1.0, 0, 0]])
+    O, P = B.attention_forward(qr, kr, v, 1, 1, hd, 2)
+    np.testing.assert_allclose(P[0, 0, 1], [0.25, 0.75], rtol=1e-15)
+    np.testing.assert_allclose(O[1], [0.25, 0.75, 0, 0], rtol=1e-15, atol=1e-16)
+    np.testing.assert_allclose(O[0], v[0], rtol=0, atol=0)
+
+
 def test_attention_backward_matches_finite_differences():
     r = np.random.default_rng(22)
     H, Hkv, hd, L = 4, 2, 3, 5

@@ -155,7 +155,7 @@ def test_decoder_forward_rejects_bad_arguments(rq, ctx):
     torch = _torch()
     inp = _inputs(5, T=128)
     X, blk = _dev(inp.X, True), _dev_blk(inp)
-    for kw in (dict(seq_len=48), dict(n_kv=3), dict(head_dim=63)):
+    for kw in (dict(seq_len=48), dict(seq_len=16), dict(n_kv=3), dict(head_dim=63), dict(head_dim=48)):
         args = dict(dict(n_heads=4, n_kv=2, head_dim=64, seq_len=64), **kw)
         with pytest.raises(rq.RealqError) as ei:
             rq.decoder_forward(ctx, X, blk, **args)
@@ -208,7 +208,8 @@ def test_decoder_sweep_rejects_bad_arguments(rq, ctx):
     inp = _inputs(5, T=128)
     X, Xh, blk = _dev(inp.X, True), _dev(inp.Xhat, True), _dev_blk(inp)
     base = dict(n_heads=4, n_kv=2, head_dim=64, seq_len=64)
-    for kw in (dict(seq_len=48), dict(n_kv=3), dict(seq_len=8192), dict(head_dim=63)):
+    for kw in (dict(seq_len=48), dict(seq_len=16), dict(n_kv=3), dict(seq_len=8192), dict(head_dim=63),
+               dict(head_dim=48)):
         args = dict(base, **kw)
         with pytest.raises(rq.RealqError) as ei:
             rq.decoder_block_sweep(ctx, X, Xh, blk, **args)
