@@ -274,6 +274,42 @@ def surrogate_grad(R, s, Ma, Xhat_J, T):
     return G / T
 
 
+def gram_surrogate(W0, X, Xhat, s=None):
+    """The module-output surrogate of Eq. fisher_loss (per-token weights s, identity metric) and its
+    gradient, written through the calibration Gram matrices Hs = Xhat^T S Xhat / T and
+    Ks = X^T S Xhat / T instead of the [m, T] residual R = W Xhat^T - W0 X^T:
+
+        (1/T) R S Xhat_J = (W Hs - W0 Ks)[:, J]
+        (1/2T) sum_t s_t |R_t|^2 = 1/2 sum_i (w_i Hs w_i^T - 2 w_i Ks^T w0_i^T) + c_i,
+        c_i = (1/2T) sum_t s_t (w0_i . x_t)^2.
+
+    Equal to surrogate_grad / surrogate_loss of the token form in exact arithmetic.  It lets the
+    oracle follow a sweep over hundreds of thousands of tokens on a few rows W0 [k, n]: the Gram
+    matrices are formed once, every Block-GD step then costs k n |J|.  Returns (grad_fn, loss_fn)
+    for quantize_layer (identity metric, no sliding-window partner)."""
+    W0 = np.asarray(W0, dtype=np.float64)
+    X = np.asarray(X, dtype=np.float64)
+    Xhat = np.asarray(Xhat, dtype=np.float64)
+    T = X.shape[0]
+    sw = np.ones(T) if s is None else np.asarray(s, dtype=np.float64)
+    SXh = Xhat if s is None else Xhat * sw[:, None]
+    Hs = Xhat.T @ SXh / T
+    Ks = X.T @ SXh / T
+    X0 = X @ W0.T                                  # [T, k]
+    c = 0.5 / T * np.sum(X0 * X0 * sw[:, None], axis=0)
+
+    def loss_fn(W):
+        quad = np.sum((W @ Hs) * W, axis=1) - 2.0 * np.sum((W @ Ks.T) * W0, axis=1)
+        return float(np.sum(0.5 * quad + c))
+
+    def grad_fn(W, J, alpha):
+        if alpha != 1.0:
+            raise ValueError("gram_surrogate has no sliding-window partner")
+        return loss_fn(W), (W @ Hs[:, J] - W0 @ Ks[:, J])
+
+    return grad_fn, loss_fn
+
+
 @dataclass
 class AdamState:
     m: np.ndarray

@@ -349,6 +349,38 @@ def test_layer_sliding_window(rq, ctx, window):
     _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
 
 
+def test_layer_llama_gate_full_size_sampled_rows(rq, ctx):
+    """The benchmark's own workload and launch configuration: the 14336x4096 gate projection with
+    262144 tokens, 8 Block-GD steps per block at lr 1e-5.  The oracle follows 4 sampled rows
+    through the whole sweep with the surrogate written through the calibration Gram matrices
+    (oracle.gram_surrogate, pinned equal to the token form).  About a minute on an MI355X host
+    (inputs ~20 s, float64 Gram matrices ~25 s, GPU sweep 15 s), ~40 GB of host memory."""
+    import time
+    torch = _torch()
+    t0 = time.time()
+    L = synth.make_module("llama3.1_8b_layer", "gate", T=262144)
+    _banner(f"layer llama3.1-8b gate 14336x4096 T=262144: inputs drawn in {time.time() - t0:.0f} s")
+    g = _run(rq, ctx, L, L.steps, L.lr)
+    _banner(f"GPU sweep {g.ms_total:.0f} ms")
+    rows = np.random.default_rng(9).choice(L.W0.shape[0], 4, replace=False)
+    X, Xh = L.X.astype(np.float64), L.Xhat.astype(np.float64)
+    grad_fn, loss_fn = oracle.gram_surrogate(L.W0[rows], X, Xh, L.s)
+    _banner(f"Gram matrices formed at {time.time() - t0:.0f} s")
+    o = oracle.quantize_layer(L.W0[rows], X, Xh, L.s, steps=L.steps, lr=L.lr, grad_fn=grad_fn, loss_fn=loss_fn)
+    _banner(f"oracle rows done at {time.time() - t0:.0f} s")
+    _assert_parity(P.compare(g, o, rows=rows))
+    lg = loss_fn(g.W_hat.cpu().numpy()[rows].astype(np.float64))
+    print("row loss", lg, o.loss_final, flush=True)
+    assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+    # the Hessian at the full token count, on sampled entries against their definition
+    H = g.H.cpu().numpy()
+    for (i, j) in [(0, 0), (17, 4000), (2048, 2049), (4095, 1)]:
+        ref = 2.0 / Xh.shape[0] * float(Xh[:, i] @ Xh[:, j])
+        scale = (2.0 / Xh.shape[0]) * math.sqrt(float(Xh[:, i] @ Xh[:, i]) * float(Xh[:, j] @ Xh[:, j]))
+        assert abs(H[i, j] - ref) <= 1e-6 * scale, (i, j)
+    torch.cuda.synchronize()
+
+
 def test_layer_llama_gate_shape_sampled_rows(rq, ctx):
     """14336x4096 gate projection at 8192 tokens (full m and n), oracle on sampled rows."""
     L = synth.make_module("llama3.1_8b_layer", "gate", T=8192)

@@ -395,6 +395,32 @@ def test_gradient_token_form_equals_gram_form():
     assert _loss_at(W, W0, X, Xh, s, M) == pytest.approx(gram_loss, rel=1e-11)
 
 
+def test_gram_surrogate_equals_the_token_form():
+    """gram_surrogate (the calibration Gram matrices) against surrogate_loss / surrogate_grad of the
+    [m, T] residual, with per-token weights."""
+    W0, X, Xh, s, W, _ = _bgd_problem(53, dense=False)
+    T = X.shape[0]
+    grad_fn, loss_fn = oracle.gram_surrogate(W0, X, Xh, s)
+    R = residual(W, W0, X, Xh)
+    for c1 in (0, 3, W.shape[1] - 1):
+        J = slice(c1, W.shape[1])
+        lv, G = grad_fn(W, J, 1.0)
+        np.testing.assert_allclose(G, surrogate_grad(R, s, None, Xh[:, J], T), rtol=1e-10, atol=1e-14)
+        assert lv == pytest.approx(surrogate_loss(R, s, None, T), rel=1e-11)
+    assert loss_fn(W) == pytest.approx(surrogate_loss(R, s, None, T), rel=1e-11)
+    with pytest.raises(ValueError):
+        grad_fn(W, slice(1, 4), 0.5)
+
+
+def test_sweep_driven_by_the_gram_surrogate_is_the_token_sweep():
+    L = synth.make_module("single_512", m=48, n=256, T=1024, seed=7)
+    grad_fn, loss_fn = oracle.gram_surrogate(L.W0, L.X, L.Xhat, L.s)
+    a = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3)
+    b = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3, grad_fn=grad_fn, loss_fn=loss_fn)
+    assert (a.codes == b.codes).all()
+    assert b.loss_final == pytest.approx(a.loss_final, rel=1e-10)
+
+
 def test_adam_constants_are_the_papers():
     a = GOLD["adam"]
     assert (oracle.ADAM_BETA1, oracle.ADAM_BETA2, oracle.ADAM_EPS) == (a["beta1"], a["beta2"], a["eps"])
