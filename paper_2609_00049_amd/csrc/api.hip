@@ -1059,10 +1059,9 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
     const int64_t rsz = grouped ? (m + d->n_groups - 1) / d->n_groups : m;
     const int64_t ngr = (m + rsz - 1) / rsz;
     hipStream_t s = ctx->stream;
-    hipEvent_t ev0, ev1;
-    RQ_HIP(ctx, hipEventCreate(&ev0));
-    RQ_HIP(ctx, hipEventCreate(&ev1));
-    RQ_HIP(ctx, hipEventRecord(ev0, s));
+    realq::EventPair ev;
+    RQ_HIP(ctx, ev.create());
+    RQ_HIP(ctx, hipEventRecord(ev.a, s));
 
     // a1-a2: Hessian and inverse factor of every row group (each factorisation synchronises once)
     void *Hacc, *Uw = out->U, *deadw = out->dead;
@@ -1142,14 +1141,12 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
         if ((rc = dense_final_loss(ctx, d, W, (const double*)Hacc, (double*)lf))) return rc;
     }
     RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat, m * n, s));
-    RQ_HIP(ctx, hipEventRecord(ev1, s));
+    RQ_HIP(ctx, hipEventRecord(ev.b, s));
     RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lf, 8, hipMemcpyDeviceToHost, s));
     RQ_HIP(ctx, hipStreamSynchronize(s));
     float ms = 0.f;
-    RQ_HIP(ctx, hipEventElapsedTime(&ms, ev0, ev1));
+    RQ_HIP(ctx, hipEventElapsedTime(&ms, ev.a, ev.b));
     out->ms_total = ms;
-    (void)hipEventDestroy(ev0);
-    (void)hipEventDestroy(ev1);
     return realq::harvest(ctx);
 }
 

@@ -181,10 +181,9 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
     const bool window = D->window != 0 && has_next;
     const double eps = (double)D->eps;
     hipStream_t s = ctx->stream;
-    hipEvent_t ev0, ev1;
-    RQ_HIP(ctx, hipEventCreate(&ev0));
-    RQ_HIP(ctx, hipEventCreate(&ev1));
-    RQ_HIP(ctx, hipEventRecord(ev0, s));
+    realq::EventPair ev;
+    RQ_HIP(ctx, ev.create());
+    RQ_HIP(ctx, hipEventRecord(ev.a, s));
 
     // module shapes: rows x cols (cols = input channels), its original weights
     const int64_t rows[3] = {f, f, d}, cols[3] = {d, d, f};
@@ -371,14 +370,12 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
     }
     // own-block loss at the quantized weights (fq holds the final forward)
     if ((rc = surrogate(1.0))) return rc;
-    RQ_HIP(ctx, hipEventRecord(ev1, s));
+    RQ_HIP(ctx, hipEventRecord(ev.b, s));
     RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lossd, 8, hipMemcpyDeviceToHost, s));
     RQ_HIP(ctx, hipStreamSynchronize(s));
     float ms = 0.f;
-    RQ_HIP(ctx, hipEventElapsedTime(&ms, ev0, ev1));
+    RQ_HIP(ctx, hipEventElapsedTime(&ms, ev.a, ev.b));
     out->ms_total = ms;
-    (void)hipEventDestroy(ev0);
-    (void)hipEventDestroy(ev1);
     return realq::harvest(ctx);
 }
 
@@ -627,10 +624,9 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
     const bool window = Dd->window != 0 && has_next;
     const int64_t T = D.T, d = D.d, f = D.f;
     hipStream_t s = ctx->stream;
-    hipEvent_t ev0, ev1;
-    RQ_HIP(ctx, hipEventCreate(&ev0));
-    RQ_HIP(ctx, hipEventCreate(&ev1));
-    RQ_HIP(ctx, hipEventRecord(ev0, s));
+    realq::EventPair ev;
+    RQ_HIP(ctx, ev.create());
+    RQ_HIP(ctx, hipEventRecord(ev.a, s));
 
     // modules q, k, v, o, gate, up, down: rows x cols and original weights
     const int64_t rows[7] = {D.Hq, D.Hk, D.Hk, d, f, f, d}, cols[7] = {d, d, d, D.Hq, d, d, f};
@@ -832,13 +828,11 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
         if ((rc = refresh(mod))) return rc;
     }
     if ((rc = surrogate(1.0))) return rc;
-    RQ_HIP(ctx, hipEventRecord(ev1, s));
+    RQ_HIP(ctx, hipEventRecord(ev.b, s));
     RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lossd, 8, hipMemcpyDeviceToHost, s));
     RQ_HIP(ctx, hipStreamSynchronize(s));
     float ms = 0.f;
-    RQ_HIP(ctx, hipEventElapsedTime(&ms, ev0, ev1));
+    RQ_HIP(ctx, hipEventElapsedTime(&ms, ev.a, ev.b));
     out->ms_total = ms;
-    (void)hipEventDestroy(ev0);
-    (void)hipEventDestroy(ev1);
     return realq::harvest(ctx);
 }

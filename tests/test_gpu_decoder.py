@@ -219,3 +219,68 @@ def test_decoder_sweep_rejects_bad_arguments(rq, ctx):
             rq.decoder_block_sweep(ctx, X, Xh, blk, **base, bgd=bgd)
         assert ei.value.code == -1
     torch.cuda.synchronize()
+
+
+def test_decoder_forward_llama8b_shape_one_sequence(rq, ctx):
+    """realq_decoder_forward at the LLaMA-3.1-8B block shape the benchmark times (d 4096, 32 query
+    heads over 8 key/value heads of 128, f 14336) on one 2048-token sequence: 64 attention tiles
+    per side and every value-column tile of the MFMA kernels.  At this shape the bf16 roundings
+    cascade further: a flipped key moves a causal column of up to 2048 queries, and flips of O,
+    x2 and u feed each other through the MLP.  The oracle with every product in float32 (scores
+    included) against itself flips 2.0e-4 of q, k, v and 0.43% of O, with x2 and y normwise
+    4.2e-4 and 2.0e-3 off; the GPU's MFMA sums flip about a third more of q, k, v and about twice
+    as much of O.  Bars: q, k, v as in test_decoder_forward_matches_oracle; O flips under 2%; x2 and
+    y normwise within 2e-3 and 6e-3.  A wrong head, mask or scale moves most entries instead."""
+    torch = _torch()
+    inp = synth.make_decoder_block(2048, 4096, 14336, 32, 8, 128, 2048, seed=11)
+    _banner("decoder forward at the 8B block shape, one 2048-token sequence")
+    r = rq.decoder_forward(ctx, _dev(inp.Xhat, True), _dev_blk(inp), n_heads=32, n_kv=8, head_dim=128,
+                           seq_len=2048, intermediates=True)
+    torch.cuda.synchronize()
+    g = {k: v.float().cpu().numpy().astype(np.float64) for k, v in r.items()}
+    blk = _oracle_blk(inp)
+    o = B.decoder_forward(inp.Xhat, blk)
+    d = 4096
+    frac, within = {}, {}
+    for name, W in (("q", blk.Wq), ("k", blk.Wk), ("v", blk.Wv)):
+        ref = getattr(o, name)
+        bound = _bf16_ulp(ref) + 2 * d * 2.0 ** -24 * (np.abs(o.h1) @ np.abs(np.asarray(W, np.float64)).T)
+        diff = np.abs(g[name] - ref)
+        frac[name] = float((diff > 0).mean())
+        within[name] = bool((diff <= bound).all())
+    frac_O = float((g["O"] != o.O).mean())
+    rel = {name: float(np.linalg.norm(g[name] - ref) / np.linalg.norm(ref)) for name, ref in (("x2", o.x2), ("y", o.y))}
+    print("flipped", frac, "within bound", within, "O flipped", frac_O, "normwise", rel, flush=True)
+    assert (g["h1"] == o.h1).all()
+    for name in ("q", "k", "v"):
+        assert frac[name] <= 5e-4 and within[name], name
+    assert frac_O <= 2e-2
+    assert rel["x2"] <= 2e-3 and rel["y"] <= 6e-3
+
+
+def test_decoder_first_steps_with_wide_heads(rq, ctx):
+    """Block-GD through attention with head_dim 128, 8 query heads over 2 key/value heads (4 per
+    group) and 8 tiles per 256-token sequence, at lr 1e-4.  The first Adam step of each module's
+    first column block lowers the loss by about lr sum |g| (a step far smaller than the weights),
+    so that decrease checks the magnitude and sign of the gradient through the attention backward:
+    within 1% of the oracle's for q (both sides at the same weights; the loss itself agrees to about
+    1e-5 of its value) and within 5% for k, v and o, whose states carry the small differences of
+    the modules before them.  The final loss is held to the module-level tolerance."""
+    inp = synth.make_decoder_block(512, 512, 768, 8, 2, 128, 256, seed=12, dense_F=False)
+    _banner("decoder block, head_dim 128, 8 over 2 heads, 256-token sequences, lr 1e-4")
+    steps, lr = 2, 1e-4
+    g = _run(rq, ctx, inp, steps, lr)
+    o = B.decoder_block_sweep(inp.X, inp.Xhat, _oracle_blk(inp), steps=steps, lr=lr)
+    tr = g.loss_trace.cpu().numpy()
+    off = 0
+    for name in B.DECODER_MODULES:
+        ref = o.modules[name].loss_trace
+        d_g, d_o = tr[off + 1] - tr[off], ref[1][2] - ref[0][2]
+        print(name, "first-step decrease", d_g, d_o, flush=True)
+        if name in ("q", "k", "v", "o"):
+            tol = (0.01 if name == "q" else 0.05) * abs(d_o) + 2e-5 * abs(ref[0][2])
+            assert abs(d_g - d_o) <= tol, name
+        off += steps * -(-o.modules[name].codes.shape[1] // 128)
+    assert tr[0] == pytest.approx(o.modules["q"].loss_trace[0][2], rel=1e-4)
+    print("loss", g.loss_final, o.loss_final, flush=True)
+    assert abs(g.loss_final - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
