@@ -8,7 +8,8 @@
 //   dP = dO v^T                          dO in three bf16 terms (dP - D cancels)
 //   dQ = dS kr, dK = dS^T qr, dV = P^T dO   float32 operands as bf16 hi/lo
 // The softmax and the row term D_i = sum_j P_ij dP_ij = dO_i . O_i run in float64.  P is kept as
-// float32 [S][H][L][L] (rows complete, zeros above the diagonal); the backward writes dS, dS^T
+// float32 [S][H][L][L] (zeros above the diagonal within the diagonal tile; tiles above it are not
+// written); the backward writes dS, dS^T
 // and P^T as bf16 hi/lo pairs for the tiles on or below the diagonal, so every MFMA operand is a
 // 16-byte load of 8 consecutive contraction indices.
 #include "common.h"
@@ -75,6 +76,7 @@ hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t h
 // r = 8 (e / 4) + 4 (lane / 32) + e % 4 and c = lane % 32.
 namespace {
 constexpr int AT = 32;
+constexpr int TSTR = AT + 8;  // bf16 per row of a staged 32 x 32 tile (80 bytes: 16-byte aligned rows)
 
 __device__ __forceinline__ bf16x8 ld8(const uint16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
@@ -153,10 +155,12 @@ __global__ __launch_bounds__(256) void attn_scores_kernel(const uint16_t* __rest
     for (int e = 0; e < 16; ++e) out[(int64_t)acc_row(e, lane) * L] = acc[e] * scale;
 }
 
-// Row softmax over j <= i in float64; the row is completed with zeros.  One block per row.
+// Row softmax over j <= i in float64, zeros after i up to the end of the diagonal tile (entries
+// of tiles above the diagonal are never read).  One block per row.
 __global__ __launch_bounds__(256) void attn_softmax_kernel(int64_t L, float* __restrict__ P) {
     __shared__ double red[TB];
     const int64_t row = blockIdx.x, i = row % L;
+    const int64_t jend = (i / AT + 1) * AT;
     float* p = P + row * L;
     double mx = -INFINITY;
     for (int64_t j = threadIdx.x; j <= i; j += TB) mx = fmax(mx, (double)p[j]);
@@ -164,7 +168,7 @@ __global__ __launch_bounds__(256) void attn_softmax_kernel(int64_t L, float* __r
     double sum = 0.0;
     for (int64_t j = threadIdx.x; j <= i; j += TB) sum += exp((double)p[j] - mx);
     sum = block_sum(sum, red);
-    for (int64_t j = threadIdx.x; j < L; j += TB) p[j] = j <= i ? (float)(exp((double)p[j] - mx) / sum) : 0.f;
+    for (int64_t j = threadIdx.x; j < jend; j += TB) p[j] = j <= i ? (float)(exp((double)p[j] - mx) / sum) : 0.f;
 }
 
 // O = P v: grid (S H nt, ceil(hd / 32 / 4)), wave w of block y takes value-column tile 4 y + w.
@@ -182,13 +186,17 @@ __global__ __launch_bounds__(256) void attn_pv_kernel(const float* __restrict__ 
     const uint16_t* b = vt + (g * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
     f32x16 acc = zero16();
     const int64_t jend = (it + 1) * AT;
-    for (int64_t j0 = 0; j0 < jend; j0 += 16) {
-        bf16x8 ah, al, al2;
+    for (int64_t j0 = 0; j0 < jend; j0 += 32) {  // jend is a multiple of 32: two steps per trip
+        bf16x8 ah, al, al2, bh, bl, bl2;
         split8x3(a + j0, ah, al, al2);
-        const bf16x8 bv = ld8(b + j0);
-        acc = mfma(ah, bv, acc);
-        acc = mfma(al, bv, acc);
-        acc = mfma(al2, bv, acc);
+        split8x3(a + j0 + 16, bh, bl, bl2);
+        const bf16x8 v0 = ld8(b + j0), v1 = ld8(b + j0 + 16);
+        acc = mfma(ah, v0, acc);
+        acc = mfma(al, v0, acc);
+        acc = mfma(al2, v0, acc);
+        acc = mfma(bh, v1, acc);
+        acc = mfma(bl, v1, acc);
+        acc = mfma(bl2, v1, acc);
     }
     const int64_t col = h * hd + ct * AT + (lane & 31);
 #pragma unroll
@@ -252,23 +260,43 @@ __global__ __launch_bounds__(256) void attn_ds_kernel(const float* __restrict__ 
         acc = mfma(al, bv, acc);
         acc = mfma(al2, bv, acc);
     }
-    const int64_t j = jt * AT + (lane & 31);
+    // The six bf16 tiles go out through a per-wave LDS tile (transposed there for dS^T and P^T), so
+    // every row segment is written as 16-byte stores: lane l then owns 8 consecutive entries of
+    // row l / 4 (and of row 16 + l / 4).
+    __shared__ __attribute__((aligned(16))) uint16_t stage[4][AT][TSTR];
+    uint16_t(*tb)[TSTR] = stage[wave];
+    uint16_t vh[16], vl[16], qh[16], ql[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
         const int64_t i = it * AT + acc_row(e, lane);
-        const int64_t ij = (sh * L + i) * L + j, ji = (sh * L + j) * L + i;
-        const float p = P[ij];
+        const float p = P[(sh * L + i) * L + jt * AT + (lane & 31)];
         const float ds = (float)((double)p * ((double)acc[e] - D[(s * L + i) * H + h]));
-        uint16_t hh, ll;
-        split_bf16(ds, hh, ll);
-        dSh[ij] = hh;
-        dSl[ij] = ll;
-        dSth[ji] = hh;
-        dStl[ji] = ll;
-        split_bf16(p, hh, ll);
-        Pth[ji] = hh;
-        Ptl[ji] = ll;
+        split_bf16(ds, vh[e], vl[e]);
+        split_bf16(p, qh[e], ql[e]);
     }
+    const int r = lane >> 2, c8 = (lane & 3) * 8;
+    auto flush = [&](const uint16_t (&v)[16], bool transposed, uint16_t* dst, int64_t row0, int64_t col0) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int a = acc_row(e, lane), b = lane & 31;
+            if (transposed) tb[b][a] = v[e];
+            else tb[a][b] = v[e];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int rr = r + 16 * half;
+            *reinterpret_cast<u16x8*>(dst + (sh * L + row0 + rr) * L + col0 + c8) =
+                *reinterpret_cast<const u16x8*>(&tb[rr][c8]);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    };
+    flush(vh, false, dSh, it * AT, jt * AT);
+    flush(vl, false, dSl, it * AT, jt * AT);
+    flush(vh, true, dSth, jt * AT, it * AT);
+    flush(vl, true, dStl, jt * AT, it * AT);
+    flush(qh, true, Pth, jt * AT, it * AT);
+    flush(ql, true, Ptl, jt * AT, it * AT);
 }
 
 // dqr = dS kr / sqrt(hd): grid (S H nt, ceil(hd / 32 / 4)); kt = kr^T [Hkv hd][T].
@@ -285,10 +313,14 @@ __global__ __launch_bounds__(256) void attn_dq_kernel(const uint16_t* __restrict
     const uint16_t* b = kt + (g * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
     f32x16 acc = zero16();
     const int64_t jend = (it + 1) * AT;
-    for (int64_t j0 = 0; j0 < jend; j0 += 16) {
-        const bf16x8 bv = ld8(b + j0);
-        acc = mfma(ld8(dSh + arow + j0), bv, acc);
-        acc = mfma(ld8(dSl + arow + j0), bv, acc);
+    for (int64_t j0 = 0; j0 < jend; j0 += 32) {  // two steps per trip
+        const bf16x8 b0 = ld8(b + j0), b1 = ld8(b + j0 + 16);
+        const bf16x8 h0 = ld8(dSh + arow + j0), l0 = ld8(dSl + arow + j0);
+        const bf16x8 h1 = ld8(dSh + arow + j0 + 16), l1 = ld8(dSl + arow + j0 + 16);
+        acc = mfma(h0, b0, acc);
+        acc = mfma(l0, b0, acc);
+        acc = mfma(h1, b1, acc);
+        acc = mfma(l1, b1, acc);
     }
     const float scale = (float)(1.0 / sqrt((double)hd));
     const int64_t col = h * hd + ct * AT + (lane & 31);
@@ -317,15 +349,27 @@ __global__ __launch_bounds__(256) void attn_dkv_kernel(const uint16_t* __restric
         const int64_t h = g * rep + hh, sh = s * H + h;
         const int64_t arow = (sh * L + jt * AT + (lane & 31)) * L + 8 * (lane >> 5);
         const int64_t brow = (h * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
-        for (int64_t i0 = jt * AT; i0 < L; i0 += 16) {
-            const bf16x8 q = ld8(qt + brow + i0);
-            ak = mfma(ld8(dSth + arow + i0), q, ak);
-            ak = mfma(ld8(dStl + arow + i0), q, ak);
-            const bf16x8 ph = ld8(Pth + arow + i0);
-            const bf16x8 doh = ld8(dOth + brow + i0);
-            av = mfma(ph, doh, av);
-            av = mfma(ld8(Ptl + arow + i0), doh, av);
-            av = mfma(ph, ld8(dOtl + brow + i0), av);
+        for (int64_t i0 = jt * AT; i0 < L; i0 += 32) {  // L - jt 32 is a multiple of 32: two steps per trip
+            bf16x8 q[2], sh_[2], sl[2], ph[2], pl[2], doh[2], dol[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int64_t k = i0 + 16 * u;
+                q[u] = ld8(qt + brow + k);
+                sh_[u] = ld8(dSth + arow + k);
+                sl[u] = ld8(dStl + arow + k);
+                ph[u] = ld8(Pth + arow + k);
+                pl[u] = ld8(Ptl + arow + k);
+                doh[u] = ld8(dOth + brow + k);
+                dol[u] = ld8(dOtl + brow + k);
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                ak = mfma(sh_[u], q[u], ak);
+                ak = mfma(sl[u], q[u], ak);
+                av = mfma(ph[u], doh[u], av);
+                av = mfma(pl[u], doh[u], av);
+                av = mfma(ph[u], dol[u], av);
+            }
         }
     }
     const float scale = (float)(1.0 / sqrt((double)hd));

@@ -189,7 +189,8 @@ hipError_t rope_fwd(const uint16_t* in, uint16_t* out, int64_t T, int64_t n, int
 hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
                     hipStream_t st);
 // Causal attention per sequence of L tokens (L and hd multiples of 32): P [T/L][H][L][L] float32
-// (rows complete, zeros above the diagonal), O32 = P V [T][H hd] float32 and O = bf16(O32);
+// (zeros above the diagonal inside each diagonal 32 x 32 tile; tiles above the diagonal are not
+// written), O32 = P V [T][H hd] float32 and O = bf16(O32);
 // vt receives v^T [Hkv hd][T].
 hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, int64_t T, int64_t H, int64_t Hkv,
                     int64_t hd, int64_t L, float* P, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st);
