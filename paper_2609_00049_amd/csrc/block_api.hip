@@ -21,6 +21,9 @@ struct Split {  // a float32 matrix as bf16 hi + lo (+ lo2 for all 24 bits: forw
     uint16_t* hi = nullptr;
     uint16_t* lo = nullptr;
     uint16_t* lo2 = nullptr;
+    bool lo_zero = false;  // lo (and lo2) are all zero: a bf16-exact matrix needs only the hi pass
+    const uint16_t* lo_or_null() const { return lo_zero ? nullptr : lo; }
+    const uint16_t* lo2_or_null() const { return lo_zero ? nullptr : lo2; }
 };
 
 int ws_split(realq_ctx* ctx, const std::string& name, int64_t count, Split& s) {
@@ -54,8 +57,8 @@ int ws(realq_ctx* ctx, const char* name, int64_t count, T*& p) {
 // [T][rows].  With lo2 the lo2 product is stored first and the hi/lo pass adds it, so a float32
 // weight (a quantized or Block-GD-updated one) enters with all of its 24 bits.
 int lin_f32(realq_ctx* ctx, const Split& W, int64_t rows, int64_t K, const uint16_t* act, int64_t T, float* out) {
-    realq::GemmArgs g{W.hi, W.lo, K, act, K, rows, T, K, 1};
-    if (W.lo2) {
+    realq::GemmArgs g{W.hi, W.lo_or_null(), K, act, K, rows, T, K, 1};
+    if (W.lo2_or_null()) {
         realq::GemmArgs g2{W.lo2, nullptr, K, act, K, rows, T, K, 1};
         RQ_HIP(ctx, realq::gemm_store_f32_t(g2, out, rows, ctx->stream));
         RQ_HIP(ctx, realq::gemm_store_f32_t(g, out, rows, ctx->stream, out));
@@ -66,8 +69,8 @@ int lin_f32(realq_ctx* ctx, const Split& W, int64_t rows, int64_t K, const uint1
 }
 // same, rounded to bf16 (the lo2 product goes through the float32 slot "lin_tmp")
 int lin_bf16(realq_ctx* ctx, const Split& W, int64_t rows, int64_t K, const uint16_t* act, int64_t T, uint16_t* out) {
-    realq::GemmArgs g{W.hi, W.lo, K, act, K, rows, T, K, 1};
-    if (W.lo2) {
+    realq::GemmArgs g{W.hi, W.lo_or_null(), K, act, K, rows, T, K, 1};
+    if (W.lo2_or_null()) {
         void* tmp;
         int rc;
         if ((rc = get_ws(ctx, "lin_tmp", (size_t)T * rows * 4, &tmp))) return rc;
@@ -83,10 +86,29 @@ int lin_bf16(realq_ctx* ctx, const Split& W, int64_t rows, int64_t K, const uint
 // (Xhi + Xlo) Yhi + Xhi Ylo, float32 [rows][cols]
 int prod3(realq_ctx* ctx, const Split& X, int64_t rows, int64_t K, const Split& Y, int64_t cols, float alpha,
           float* C) {
-    realq::GemmArgs g{X.hi, X.lo, K, Y.hi, K, rows, cols, K, 1};
+    realq::GemmArgs g{X.hi, X.lo_or_null(), K, Y.hi, K, rows, cols, K, 1};
     RQ_HIP(ctx, realq::gemm_store_f32(g, C, cols, 0, alpha, ctx->stream));
-    realq::GemmArgs g2{X.hi, nullptr, K, Y.lo, K, rows, cols, K, 1};
-    RQ_HIP(ctx, realq::gemm_acc_f32(g2, C, cols, alpha, ctx->stream));
+    if (Y.lo_or_null()) {
+        realq::GemmArgs g2{X.hi, nullptr, K, Y.lo, K, rows, cols, K, 1};
+        RQ_HIP(ctx, realq::gemm_acc_f32(g2, C, cols, alpha, ctx->stream));
+    }
+    return REALQ_OK;
+}
+
+// Sets w.lo_zero when the lower terms of a split are all zero (a bf16-exact matrix, such as a
+// weight of a bf16 checkpoint): its products then skip the passes of those terms, which would add
+// exact zeros.  One stream synchronisation; for the fixed operands set up once per call.
+int mark_exact(realq_ctx* ctx, Split& w, int64_t count) {
+    int* flag;
+    int rc;
+    if ((rc = ws(ctx, "nz_flag", 1, flag))) return rc;
+    RQ_HIP(ctx, realq::fill_f32(reinterpret_cast<float*>(flag), 0.f, 1, ctx->stream));
+    RQ_HIP(ctx, realq::any_nonzero_u16(w.lo, count, flag, ctx->stream));
+    if (w.lo2) RQ_HIP(ctx, realq::any_nonzero_u16(w.lo2, count, flag, ctx->stream));
+    int host = 1;
+    RQ_HIP(ctx, hipMemcpyAsync(&host, flag, sizeof(int), hipMemcpyDeviceToHost, ctx->stream));
+    RQ_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    w.lo_zero = host == 0;
     return REALQ_OK;
 }
 
@@ -119,7 +141,12 @@ int split_block(realq_ctx* ctx, const char* tag, const realq_mlp_block& b, int64
     if (b.F) {
         if ((rc = ws_split(ctx, t + "F", d * d, w.F))) return rc;
         RQ_HIP(ctx, realq::split_diff_f32(b.F, d, nullptr, 0, w.F.hi, w.F.lo, d, d, d, s));
+        if ((rc = mark_exact(ctx, w.F, d * d))) return rc;
     }
+    if ((rc = mark_exact(ctx, w.g, f * d)) || (rc = mark_exact(ctx, w.u, f * d)) || (rc = mark_exact(ctx, w.d, d * f)) ||
+        (rc = mark_exact(ctx, w.dT, f * d)))
+        return rc;
+    if (backward && ((rc = mark_exact(ctx, w.gT, d * f)) || (rc = mark_exact(ctx, w.uT, d * f)))) return rc;
     return REALQ_OK;
 }
 
@@ -277,8 +304,10 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
             if ((rc = prod3(ctx, sda2, T, f, w2.gT, d, 1.f, du2))) return rc;  // du2 = da2 Wg2 + db2 Wu2
             realq::GemmArgs a1{sdb2.hi, sdb2.lo, f, w2.uT.hi, f, T, d, f, 1};
             RQ_HIP(ctx, realq::gemm_acc_f32(a1, du2, d, 1.f, s));
-            realq::GemmArgs a2{sdb2.hi, nullptr, f, w2.uT.lo, f, T, d, f, 1};
-            RQ_HIP(ctx, realq::gemm_acc_f32(a2, du2, d, 1.f, s));
+            if (w2.uT.lo_or_null()) {
+                realq::GemmArgs a2{sdb2.hi, nullptr, f, w2.uT.lo, f, T, d, f, 1};
+                RQ_HIP(ctx, realq::gemm_acc_f32(a2, du2, d, 1.f, s));
+            }
             RQ_HIP(ctx, realq::rmsnorm_bwd_blend(fq.y, g2, du2, D->next.gamma, eps, alpha, T, d, g, s));
             RQ_HIP(ctx, realq::reduce_partials(parts, 2 * npart, 1.0, lossd, s));
         } else {
@@ -413,7 +442,13 @@ int split_dec(realq_ctx* ctx, const char* tag, const realq_decoder_block& b, int
         RQ_HIP(ctx, realq::transpose_split_f32(b.Wq, d, w.qT.hi, w.qT.lo, Hq, Hq, d, s));
         RQ_HIP(ctx, realq::transpose_split_f32(b.Wk, d, w.kT.hi, w.kT.lo, Hk, Hk, d, s));
         RQ_HIP(ctx, realq::transpose_split_f32(b.Wv, d, w.vT.hi, w.vT.lo, Hk, Hk, d, s));
+        if ((rc = mark_exact(ctx, w.qT, d * Hq)) || (rc = mark_exact(ctx, w.kT, d * Hk)) ||
+            (rc = mark_exact(ctx, w.vT, d * Hk)))
+            return rc;
     }
+    if ((rc = mark_exact(ctx, w.q, Hq * d)) || (rc = mark_exact(ctx, w.k, Hk * d)) || (rc = mark_exact(ctx, w.v, Hk * d)) ||
+        (rc = mark_exact(ctx, w.o, d * Hq)) || (rc = mark_exact(ctx, w.oT, Hq * d)))
+        return rc;
     return split_block(ctx, (t + "m").c_str(), b.mlp, d, f, true, w.mlp);
 }
 
@@ -511,10 +546,12 @@ int alloc_work(realq_ctx* ctx, const char* tag, const DecDims& D, DecWork& Wk) {
 }
 
 int prod3_acc(realq_ctx* ctx, const Split& X, int64_t rows, int64_t K, const Split& Y, int64_t cols, float* C) {
-    realq::GemmArgs g{X.hi, X.lo, K, Y.hi, K, rows, cols, K, 1};
+    realq::GemmArgs g{X.hi, X.lo_or_null(), K, Y.hi, K, rows, cols, K, 1};
     RQ_HIP(ctx, realq::gemm_acc_f32(g, C, cols, 1.f, ctx->stream));
-    realq::GemmArgs g2{X.hi, nullptr, K, Y.lo, K, rows, cols, K, 1};
-    RQ_HIP(ctx, realq::gemm_acc_f32(g2, C, cols, 1.f, ctx->stream));
+    if (Y.lo_or_null()) {
+        realq::GemmArgs g2{X.hi, nullptr, K, Y.lo, K, rows, cols, K, 1};
+        RQ_HIP(ctx, realq::gemm_acc_f32(g2, C, cols, 1.f, ctx->stream));
+    }
     return REALQ_OK;
 }
 
@@ -771,6 +808,7 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
             const int64_t nJ = n - c1;
             for (int k = 0; k < steps; ++k) {
                 Timed tm(ctx, "block_step");
+                fwd_slot[mod]->lo_zero = false;
                 RQ_HIP(ctx, realq::split3_f64(W, fwd_slot[mod]->hi, fwd_slot[mod]->lo, fwd_slot[mod]->lo2, m * n, s));
                 if ((rc = refresh(mod)) || (rc = surrogate(alpha))) return rc;
                 if (out->loss_trace)
@@ -823,6 +861,7 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
             }
         }
         RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat[mod], m * n, s));
+        fwd_slot[mod]->lo_zero = false;
         RQ_HIP(ctx, realq::split3_f32(out->W_hat[mod], n, fwd_slot[mod]->hi, fwd_slot[mod]->lo, fwd_slot[mod]->lo2, n,
                                       m, n, s));
         if ((rc = refresh(mod))) return rc;

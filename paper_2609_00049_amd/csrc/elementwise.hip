@@ -202,6 +202,20 @@ hipError_t split3_f32(const float* A, int64_t lda, uint16_t* hi, uint16_t* lo, u
     return hipGetLastError();
 }
 
+// flag |= 1 when any of the count bf16 values is nonzero (either sign of zero counts as zero)
+__global__ void any_nonzero_u16_kernel(const uint16_t* __restrict__ p, int64_t count, int* __restrict__ flag) {
+    uint32_t any = 0;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x)
+        any |= p[e] & 0x7FFFu;
+    if (any) atomicOr(flag, 1);
+}
+
+hipError_t any_nonzero_u16(const uint16_t* p, int64_t count, int* flag, hipStream_t st) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(any_nonzero_u16_kernel, dim3(grid_for(count, 8)), dim3(TB), 0, st, p, count, flag);
+    return hipGetLastError();
+}
+
 // G[i][j] = C0[i][c1 + j] + P[i][c1 + j]   (m x w, C0 and P with row stride ld)
 __global__ void gram_grad_kernel(const float* __restrict__ C0, const float* __restrict__ P, int64_t ld, int64_t c1,
                                  int64_t w, int64_t total, float* __restrict__ G) {

@@ -71,6 +71,8 @@ hipError_t split_f64(const double* in, uint16_t* hi, uint16_t* lo, int64_t count
 hipError_t split3_f64(const double* in, uint16_t* hi, uint16_t* lo, uint16_t* lo2, int64_t count, hipStream_t st);
 hipError_t split3_f32(const float* A, int64_t lda, uint16_t* hi, uint16_t* lo, uint16_t* lo2, int64_t ld,
                       int64_t rows, int64_t cols, hipStream_t st);
+// *flag |= 1 when any of p[0 .. count) is a nonzero bf16 value (the caller clears *flag)
+hipError_t any_nonzero_u16(const uint16_t* p, int64_t count, int* flag, hipStream_t st);
 // G[i][j] = C0[i][c1+j] + P[i][c1+j], i < m, j < w
 hipError_t gram_grad(const float* C0, const float* P, int64_t ld, int64_t c1, int64_t m, int64_t w, float* G,
                      hipStream_t st);
