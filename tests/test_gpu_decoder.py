@@ -284,3 +284,26 @@ def test_decoder_first_steps_with_wide_heads(rq, ctx):
     assert tr[0] == pytest.approx(o.modules["q"].loss_trace[0][2], rel=1e-4)
     print("loss", g.loss_final, o.loss_final, flush=True)
     assert abs(g.loss_final - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+
+
+def test_decoder_ragged_and_degenerate_shapes(rq, ctx):
+    """Edge shapes in one block: plain multi-head attention (n_kv = n_heads), head_dim 32 (one
+    value-column tile), 32-token sequences (one attention tile each), d = 264 and f = 392 (column
+    blocks of 128, 128 and 8; 128, 128, 128 and 8) and an o projection of 64 columns (one partial
+    block, so o takes no Block-GD step).  Without Block-GD every module is GPTQ on its own input
+    (module-level bars, down at its no-BGD bar of the decoder tests); with Block-GD the first step
+    and the final loss are compared."""
+    inp = synth.make_decoder_block(96, 264, 392, 2, 2, 32, 32, seed=13)
+    _banner("decoder block, ragged widths, MHA, head_dim 32, 32-token sequences")
+    g = _run(rq, ctx, inp, 0, 1e-5)
+    o = B.decoder_block_sweep(inp.X, inp.Xhat, _oracle_blk(inp), steps=0)
+    _check(g, o, False)
+    g = _run(rq, ctx, inp, 2, 1e-5)
+    o = B.decoder_block_sweep(inp.X, inp.Xhat, _oracle_blk(inp), steps=2, lr=1e-5)
+    tr = g.loss_trace.cpu().numpy()
+    print("trace0", tr[0], o.modules["q"].loss_trace[0][2], "loss", g.loss_final, o.loss_final, flush=True)
+    assert tr[0] == pytest.approx(o.modules["q"].loss_trace[0][2], rel=1e-4)
+    assert abs(g.loss_final - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+    # o (one partial block) and the last block of every module take no Block-GD step
+    off = 3 * 2 * 3
+    assert np.isnan(tr[off:off + 2]).all()
