@@ -386,16 +386,16 @@ int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* desc, realq_mlp_
  * head h / (n_heads / n_kv)), the rotary embedding over pairs (i, i + hd/2) at angle
  * (t mod seq_len) rope_base^(-2i/hd) (positions counted within each sequence of seq_len
  * tokens), and causal attention within each sequence: scores as float32 sums of the exact
- * bf16 products, the softmax in float64, the value sums with the probabilities in full float32
- * precision.  realq_decoder_block_sweep quantizes q, k, v, o, gate, up and down
+ * bf16 products, the softmax's maxima, sums and exponents in float64 (each exponential in
+ * float32), the value sums with the probabilities in full float32 precision.  realq_decoder_block_sweep quantizes q, k, v, o, gate, up and down
  * in that order (Alg. 1), each with GPTQ on its own input in the quantized path (h1; O; u;
  * z) and Block-GD on the block-output Fisher loss as described for realq_mlp_block_sweep,
  * b_global running over the column blocks of all seven modules; the window partner is the
  * next decoder block.  Shapes: Wq [H hd, d], Wk and Wv [Hkv hd, d], Wo [d, H hd]; seq_len a
  * multiple of 32 and at most 4096, T a multiple of seq_len, H a multiple of Hkv, head_dim a
  * multiple of 32 and at most 256, d and f multiples of 8 (REALQ_ERR_SHAPE otherwise).  The
- * attention keeps float32 probabilities of T n_heads seq_len entries per block forward (three
- * forwards with the window) and six bf16 arrays of that size for its backward.  Outputs per
+ * attention forward keeps the row log-sum-exp (the backward recomputes the probabilities from
+ * it); its backward keeps six bf16 arrays of T n_heads seq_len entries.  Outputs per
  * module in the order q, k, v, o, gate, up, down; loss_trace entry (b_global - 1) * steps + k. */
 typedef struct realq_decoder_block {
     const float* gamma1;

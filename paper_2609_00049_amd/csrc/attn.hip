@@ -7,11 +7,12 @@
 //   output  O = P v                      P carried as three bf16 terms (all 24 bits)
 //   dP = dO v^T                          dO in three bf16 terms (dP - D cancels)
 //   dQ = dS kr, dK = dS^T qr, dV = P^T dO   float32 operands as bf16 hi/lo
-// The softmax and the row term D_i = sum_j P_ij dP_ij = dO_i . O_i run in float64.  P is kept as
-// float32 [S][H][L][L] (zeros above the diagonal within the diagonal tile; tiles above it are not
-// written); the backward writes dS, dS^T
-// and P^T as bf16 hi/lo pairs for the tiles on or below the diagonal, so every MFMA operand is a
-// 16-byte load of 8 consecutive contraction indices.
+// The softmax (each query row's max and sum in a first pass over its key tiles, the forward keeping
+// only the row log-sum-exp; each exponential itself in float32) and the row term
+// D_i = sum_j P_ij dP_ij = dO_i . O_i run in float64.  The backward
+// recomputes P from the log-sum-exp and writes dS, dS^T and P^T as bf16 hi/lo pairs for the tiles
+// on or below the diagonal, so every MFMA operand is a 16-byte load of 8 consecutive contraction
+// indices.
 #include "common.h"
 #include "kernels.h"
 
@@ -110,116 +111,132 @@ __device__ __forceinline__ f32x16 zero16() {
 
 __device__ __forceinline__ int acc_row(int e, int lane) { return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3); }
 
-__device__ double block_sum(double v, double* red) {
-    red[threadIdx.x] = v;
-    __syncthreads();
-    for (int s = TB / 2; s > 0; s >>= 1) {
-        if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
-        __syncthreads();
-    }
-    const double r = red[0];
-    __syncthreads();
-    return r;
-}
-__device__ double block_max(double v, double* red) {
-    red[threadIdx.x] = v;
-    __syncthreads();
-    for (int s = TB / 2; s > 0; s >>= 1) {
-        if ((int)threadIdx.x < s) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + s]);
-        __syncthreads();
-    }
-    const double r = red[0];
-    __syncthreads();
-    return r;
-}
 }  // namespace
 
-// Raw scaled scores of the causal tiles: grid (S H nt, ceil(nt / 4)), 4 waves, wave w of block y
-// takes key tile jt = 4 y + w of query tile it (tiles above the diagonal are skipped).
-__global__ __launch_bounds__(256) void attn_scores_kernel(const uint16_t* __restrict__ qr,
-                                                          const uint16_t* __restrict__ kr, int64_t H, int64_t Hkv,
-                                                          int64_t hd, int64_t L, float* __restrict__ P) {
+// Fused forward for one 32-row query tile per wave, in two passes over the key tiles up to the
+// diagonal.  Pass 1: scores on MFMA and each row's max and sum of exponentials (lane 2r + h owns
+// half h of row r; max and sum in float64, each exponent in float64 and its exponential in
+// float32).  Pass 2: the scores again, P = exp(s - max) / sum as three bf16 terms, P v on MFMA.
+// Writes O32 = P v, O = bf16(O32) and the row log-sum-exp LSE = max + log(sum) (float64 [T][H]),
+// from which the backward recomputes P.  Value columns go in groups of up to CG 32-column tiles
+// (one group for head_dim <= 128).  grid (S H ceil(nt / 4)), 4 waves; wave w of block x takes
+// query tile nt - 1 - (4 (x mod nq) + w), so the longest rows start first.
+constexpr int CG = 4;
+__global__ __launch_bounds__(256) void attn_fwd_kernel(const uint16_t* __restrict__ qr,
+                                                       const uint16_t* __restrict__ kr,
+                                                       const uint16_t* __restrict__ vt, int64_t T, int64_t H,
+                                                       int64_t Hkv, int64_t hd, int64_t L, float* __restrict__ O32,
+                                                       uint16_t* __restrict__ O, double* __restrict__ LSE) {
+    __shared__ float sS[4][AT][AT + 1];
+    __shared__ __attribute__((aligned(16))) uint16_t sP[4][3][AT][TSTR];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t nt = L / AT;
-    const int64_t it = blockIdx.x % nt, sh = blockIdx.x / nt, h = sh % H, s = sh / H;
-    const int64_t jt = (int64_t)blockIdx.y * 4 + wave;
-    if (jt > it) return;
+    const int64_t nt = L / AT, nq = (nt + 3) / 4;
+    const int64_t sh = blockIdx.x / nq, h = sh % H, s = sh / H;
+    const int64_t it = nt - 1 - (4 * (int64_t)(blockIdx.x % nq) + wave);
+    if (it < 0) return;
     const int64_t g = h / (H / Hkv);
-    const uint16_t* a = qr + (s * L + it * AT + (lane & 31)) * (H * hd) + h * hd + 8 * (lane >> 5);
-    const uint16_t* b = kr + (s * L + jt * AT + (lane & 31)) * (Hkv * hd) + g * hd + 8 * (lane >> 5);
-    f32x16 acc = zero16();
-    for (int64_t k0 = 0; k0 < hd; k0 += 16) acc = mfma(ld8(a + k0), ld8(b + k0), acc);
-    const float scale = (float)(1.0 / sqrt((double)hd));
-    float* out = P + (sh * L + it * AT) * L + jt * AT + (lane & 31);
+    const int nk = (int)(hd / 16), nct = (int)(hd / AT);
+    const double scale = 1.0 / sqrt((double)hd);
+    float(*Sw)[AT + 1] = sS[wave];
+    uint16_t(*Pw)[AT][TSTR] = sP[wave];
+    const int rr = lane >> 1, hh = lane & 1, c32 = lane & 31, k8 = 8 * (lane >> 5);
+    const uint16_t* qa = qr + (s * L + it * AT + c32) * (H * hd) + h * hd + k8;
+    const uint16_t* kb0 = kr + (s * L + c32) * (Hkv * hd) + g * hd + k8;
+    const int64_t kstep = AT * Hkv * hd;  // one key tile further
+    // scores of key tile jt into this wave's LDS tile (entries above the diagonal: -inf)
+    auto scores = [&](int64_t jt) {
+        const uint16_t* kb = kb0 + jt * kstep;
+        f32x16 acc = zero16();
+        for (int kk = 0; kk < nk; ++kk) acc = mfma(ld8(qa + 16 * kk), ld8(kb + 16 * kk), acc);
+        const bool diag = jt == it;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) out[(int64_t)acc_row(e, lane) * L] = acc[e] * scale;
-}
-
-// Row softmax over j <= i in float64, zeros after i up to the end of the diagonal tile (entries
-// of tiles above the diagonal are never read).  One block per row.
-__global__ __launch_bounds__(256) void attn_softmax_kernel(int64_t L, float* __restrict__ P) {
-    __shared__ double red[TB];
-    const int64_t row = blockIdx.x, i = row % L;
-    const int64_t jend = (i / AT + 1) * AT;
-    float* p = P + row * L;
-    double mx = -INFINITY;
-    for (int64_t j = threadIdx.x; j <= i; j += TB) mx = fmax(mx, (double)p[j]);
-    mx = block_max(mx, red);
-    double sum = 0.0;
-    for (int64_t j = threadIdx.x; j <= i; j += TB) sum += exp((double)p[j] - mx);
-    sum = block_sum(sum, red);
-    for (int64_t j = threadIdx.x; j < jend; j += TB) p[j] = j <= i ? (float)(exp((double)p[j] - mx) / sum) : 0.f;
-}
-
-// O = P v: grid (S H nt, ceil(hd / 32 / 4)), wave w of block y takes value-column tile 4 y + w.
-// P rows as three bf16 terms, vt = v^T [Hkv hd][T].  Writes O32 (float32) and O (bf16).
-__global__ __launch_bounds__(256) void attn_pv_kernel(const float* __restrict__ P, const uint16_t* __restrict__ vt,
-                                                      int64_t T, int64_t H, int64_t Hkv, int64_t hd, int64_t L,
-                                                      float* __restrict__ O32, uint16_t* __restrict__ O) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t nt = L / AT;
-    const int64_t it = blockIdx.x % nt, sh = blockIdx.x / nt, h = sh % H, s = sh / H;
-    const int64_t ct = (int64_t)blockIdx.y * 4 + wave;
-    if (ct >= hd / AT) return;
-    const int64_t g = h / (H / Hkv);
-    const float* a = P + (sh * L + it * AT + (lane & 31)) * L + 8 * (lane >> 5);
-    const uint16_t* b = vt + (g * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
-    f32x16 acc = zero16();
-    const int64_t jend = (it + 1) * AT;
-    for (int64_t j0 = 0; j0 < jend; j0 += 32) {  // jend is a multiple of 32: two steps per trip
-        bf16x8 ah, al, al2, bh, bl, bl2;
-        split8x3(a + j0, ah, al, al2);
-        split8x3(a + j0 + 16, bh, bl, bl2);
-        const bf16x8 v0 = ld8(b + j0), v1 = ld8(b + j0 + 16);
-        acc = mfma(ah, v0, acc);
-        acc = mfma(al, v0, acc);
-        acc = mfma(al2, v0, acc);
-        acc = mfma(bh, v1, acc);
-        acc = mfma(bl, v1, acc);
-        acc = mfma(bl2, v1, acc);
+        for (int e = 0; e < 16; ++e) {
+            const int r = acc_row(e, lane);
+            Sw[r][c32] = (diag && c32 > r) ? -INFINITY : acc[e];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    };
+    // pass 1: the row max and sum
+    double m_row = -INFINITY, l_row = 0.0;
+    for (int64_t jt = 0; jt <= it; ++jt) {
+        scores(jt);
+        float smax = -INFINITY;  // scaling by a positive constant keeps the order
+#pragma unroll
+        for (int k = 0; k < 16; ++k) smax = fmaxf(smax, Sw[rr][16 * hh + k]);
+        smax = fmaxf(smax, __shfl_xor(smax, 1));
+        const double m_new = fmax(m_row, (double)smax * scale);
+        double sum = 0.0;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) sum += (double)expf((float)((double)Sw[rr][16 * hh + k] * scale - m_new));
+        sum += __shfl_xor(sum, 1);
+        l_row = l_row * exp(m_row - m_new) + sum;
+        m_row = m_new;
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
-    const int64_t col = h * hd + ct * AT + (lane & 31);
+    if (hh == 0) LSE[(s * L + it * AT + rr) * H + h] = m_row + log(l_row);
+    const double inv_l = 1.0 / l_row;
+    // pass 2: P v per group of value-column tiles
+    for (int c0 = 0; c0 < nct; c0 += CG) {
+        f32x16 oacc[CG];
+        const uint16_t* vb[CG];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-        const int64_t t = s * L + it * AT + acc_row(e, lane);
-        O32[t * H * hd + col] = acc[e];
-        O[t * H * hd + col] = f2bf(acc[e]);
+        for (int ct = 0; ct < CG; ++ct) {
+            oacc[ct] = zero16();
+            vb[ct] = vt + (g * hd + (int64_t)(c0 + ct) * AT + c32) * T + s * L + k8;
+        }
+        for (int64_t jt = 0; jt <= it; ++jt) {
+            scores(jt);
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                const float pf =
+                    (float)((double)expf((float)((double)Sw[rr][16 * hh + k] * scale - m_row)) * inv_l);
+                const uint16_t ph = f2bf(pf);
+                const float r1 = pf - bf2f(ph);
+                const uint16_t pl = f2bf(r1);
+                Pw[0][rr][16 * hh + k] = ph;
+                Pw[1][rr][16 * hh + k] = pl;
+                Pw[2][rr][16 * hh + k] = f2bf(r1 - bf2f(pl));
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+            for (int k2 = 0; k2 < 2; ++k2) {
+                const int col = 16 * k2 + k8;
+                const bf16x8 ah = ld8(&Pw[0][c32][col]);
+                const bf16x8 al = ld8(&Pw[1][c32][col]);
+                const bf16x8 al2 = ld8(&Pw[2][c32][col]);
+#pragma unroll
+                for (int ct = 0; ct < CG; ++ct) {
+                    if (c0 + ct >= nct) continue;
+                    const bf16x8 bv = ld8(vb[ct] + jt * AT + 16 * k2);
+                    oacc[ct] = mfma(ah, bv, oacc[ct]);
+                    oacc[ct] = mfma(al, bv, oacc[ct]);
+                    oacc[ct] = mfma(al2, bv, oacc[ct]);
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        }
+#pragma unroll
+        for (int ct = 0; ct < CG; ++ct) {
+            if (c0 + ct >= nct) continue;
+            const int64_t col = h * hd + (int64_t)(c0 + ct) * AT + c32;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int64_t t = s * L + it * AT + acc_row(e, lane);
+                O32[t * H * hd + col] = oacc[ct][e];
+                O[t * H * hd + col] = f2bf(oacc[ct][e]);
+            }
+        }
     }
 }
 
 hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, int64_t T, int64_t H, int64_t Hkv,
-                    int64_t hd, int64_t L, float* P, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st) {
+                    int64_t hd, int64_t L, double* LSE, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st) {
     if (T <= 0) return hipSuccess;
     const int64_t S = T / L, nt = L / AT;
     hipError_t e = transpose_u16(v, Hkv * hd, vt, T, T, Hkv * hd, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_scores_kernel, dim3((unsigned)(S * H * nt), (unsigned)((nt + 3) / 4)), dim3(256), 0, st,
-                       qr, kr, H, Hkv, hd, L, P);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_softmax_kernel, dim3((unsigned)(S * H * L)), dim3(TB), 0, st, L, P);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_pv_kernel, dim3((unsigned)(S * H * nt), (unsigned)((hd / AT + 3) / 4)), dim3(256), 0, st,
-                       P, vt, T, H, Hkv, hd, L, O32, O);
+    hipLaunchKernelGGL(attn_fwd_kernel, dim3((unsigned)(S * H * ((nt + 3) / 4))), dim3(256), 0, st, qr, kr, vt, T, H,
+                       Hkv, hd, L, O32, O, LSE);
     return hipGetLastError();
 }
 
@@ -235,9 +252,12 @@ __global__ void attn_rowdot_kernel(const float* __restrict__ dO, const float* __
     }
 }
 
-// dS = P o (dP - D), dP = dO v^T (dO in three bf16 terms), for the causal tiles (same grid as the scores);
-// writes dS [i][j], dS^T and P^T [j][i] as bf16 hi/lo.
-__global__ __launch_bounds__(256) void attn_ds_kernel(const float* __restrict__ P, const float* __restrict__ dO,
+// dS = P o (dP - D) for the causal tiles, P_ij = exp(qr_i . kr_j / sqrt(hd) - LSE_i) recomputed from
+// the forward's row log-sum-exp (the same MFMA sums as the forward), dP = dO v^T (dO in three bf16
+// terms); grid (S H nt, ceil(nt / 4)), wave w of block y takes key tile 4 y + w of query tile it.
+// Writes dS [i][j], dS^T and P^T [j][i] as bf16 hi/lo.
+__global__ __launch_bounds__(256) void attn_ds_kernel(const uint16_t* __restrict__ qr, const uint16_t* __restrict__ kr,
+                                                      const double* __restrict__ LSE, const float* __restrict__ dO,
                                                       const uint16_t* __restrict__ v, const double* __restrict__ D,
                                                       int64_t H, int64_t Hkv, int64_t hd, int64_t L,
                                                       uint16_t* __restrict__ dSh, uint16_t* __restrict__ dSl,
@@ -251,7 +271,9 @@ __global__ __launch_bounds__(256) void attn_ds_kernel(const float* __restrict__ 
     const int64_t g = h / (H / Hkv);
     const float* a = dO + (s * L + it * AT + (lane & 31)) * (H * hd) + h * hd + 8 * (lane >> 5);
     const uint16_t* b = v + (s * L + jt * AT + (lane & 31)) * (Hkv * hd) + g * hd + 8 * (lane >> 5);
-    f32x16 acc = zero16();
+    const uint16_t* qa = qr + (s * L + it * AT + (lane & 31)) * (H * hd) + h * hd + 8 * (lane >> 5);
+    const uint16_t* kb = kr + (s * L + jt * AT + (lane & 31)) * (Hkv * hd) + g * hd + 8 * (lane >> 5);
+    f32x16 acc = zero16(), sc = zero16();
     for (int64_t k0 = 0; k0 < hd; k0 += 16) {  // dO in three terms: dP - D cancels
         bf16x8 ah, al, al2;
         split8x3(a + k0, ah, al, al2);
@@ -259,7 +281,9 @@ __global__ __launch_bounds__(256) void attn_ds_kernel(const float* __restrict__ 
         acc = mfma(ah, bv, acc);
         acc = mfma(al, bv, acc);
         acc = mfma(al2, bv, acc);
+        sc = mfma(ld8(qa + k0), ld8(kb + k0), sc);
     }
+    const double scale = 1.0 / sqrt((double)hd);
     // The six bf16 tiles go out through a per-wave LDS tile (transposed there for dS^T and P^T), so
     // every row segment is written as 16-byte stores: lane l then owns 8 consecutive entries of
     // row l / 4 (and of row 16 + l / 4).
@@ -268,8 +292,8 @@ __global__ __launch_bounds__(256) void attn_ds_kernel(const float* __restrict__ 
     uint16_t vh[16], vl[16], qh[16], ql[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-        const int64_t i = it * AT + acc_row(e, lane);
-        const float p = P[(sh * L + i) * L + jt * AT + (lane & 31)];
+        const int64_t i = it * AT + acc_row(e, lane), j = jt * AT + (lane & 31);
+        const float p = j <= i ? expf((float)((double)sc[e] * scale - LSE[(s * L + i) * H + h])) : 0.f;
         const float ds = (float)((double)p * ((double)acc[e] - D[(s * L + i) * H + h]));
         split_bf16(ds, vh[e], vl[e]);
         split_bf16(p, qh[e], ql[e]);
@@ -382,7 +406,7 @@ __global__ __launch_bounds__(256) void attn_dkv_kernel(const uint16_t* __restric
     }
 }
 
-hipError_t attn_bwd(const float* P, const float* O32, const float* dO, const uint16_t* qr, const uint16_t* kr,
+hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const uint16_t* qr, const uint16_t* kr,
                     const uint16_t* v, int64_t T, int64_t H, int64_t Hkv, int64_t hd, int64_t L, const AttnScratch& w,
                     float* dq, float* dk, float* dv, hipStream_t st) {
     if (T <= 0) return hipSuccess;
@@ -393,8 +417,8 @@ hipError_t attn_bwd(const float* P, const float* O32, const float* dO, const uin
     if ((e = transpose_u16(kr, Hkv * hd, w.kt, T, T, Hkv * hd, st)) != hipSuccess) return e;
     if ((e = transpose_u16(qr, H * hd, w.qt, T, T, H * hd, st)) != hipSuccess) return e;
     if ((e = transpose_split_f32(dO, H * hd, w.dOth, w.dOtl, T, T, H * hd, st)) != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_ds_kernel, dim3((unsigned)(S * H * nt), (unsigned)((nt + 3) / 4)), dim3(256), 0, st, P, dO,
-                       v, w.D, H, Hkv, hd, L, w.dSh, w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
+    hipLaunchKernelGGL(attn_ds_kernel, dim3((unsigned)(S * H * nt), (unsigned)((nt + 3) / 4)), dim3(256), 0, st, qr, kr,
+                       LSE, dO, v, w.D, H, Hkv, hd, L, w.dSh, w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned cy = (unsigned)((hd / AT + 3) / 4);
     hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)(S * H * nt), cy), dim3(256), 0, st, w.dSh, w.dSl, w.kt, T, H,

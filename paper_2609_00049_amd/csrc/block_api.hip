@@ -459,7 +459,8 @@ struct DecDims {
 
 struct DecF {  // buffers of one forward of the decoder block
     uint16_t *h1, *q, *k, *v, *qr, *kr, *O, *o, *vt;
-    float *P, *O32, *x2;
+    float *O32, *x2;
+    double* lse;  // [T][H] row log-sum-exp of the attention (the backward recomputes P from it)
     Fwd mlp;
 };
 
@@ -471,7 +472,7 @@ int alloc_decf(realq_ctx* ctx, const char* tag, const DecDims& D, DecF& F) {
         (rc = ws(ctx, (t + "k").c_str(), T * D.Hk, F.k)) || (rc = ws(ctx, (t + "v").c_str(), T * D.Hk, F.v)) ||
         (rc = ws(ctx, (t + "qr").c_str(), T * D.Hq, F.qr)) || (rc = ws(ctx, (t + "kr").c_str(), T * D.Hk, F.kr)) ||
         (rc = ws(ctx, (t + "O").c_str(), T * D.Hq, F.O)) || (rc = ws(ctx, (t + "oo").c_str(), T * D.d, F.o)) ||
-        (rc = ws(ctx, (t + "P").c_str(), T * D.H * D.L, F.P)) || (rc = ws(ctx, (t + "x2").c_str(), T * D.d, F.x2)) ||
+        (rc = ws(ctx, (t + "lse").c_str(), T * D.H, F.lse)) || (rc = ws(ctx, (t + "x2").c_str(), T * D.d, F.x2)) ||
         (rc = ws(ctx, (t + "O32").c_str(), T * D.Hq, F.O32)) || (rc = ws(ctx, (t + "vt").c_str(), T * D.Hk, F.vt)))
         return rc;
     return alloc_fwd(ctx, (t + "m").c_str(), T, D.d, D.f, F.mlp);
@@ -493,7 +494,7 @@ int dec_attn(realq_ctx* ctx, const DecW& w, const uint16_t* xb, const float* xf,
     Timed tm(ctx, "attention");
     if (mask & 1) RQ_HIP(ctx, realq::rope_fwd(F.q, F.qr, D.T, D.H, D.hd, D.L, D.base, s));
     if (mask & 2) RQ_HIP(ctx, realq::rope_fwd(F.k, F.kr, D.T, D.Hkv, D.hd, D.L, D.base, s));
-    RQ_HIP(ctx, realq::attn_fwd(F.qr, F.kr, F.v, D.T, D.H, D.Hkv, D.hd, D.L, F.P, F.O32, F.O, F.vt, s));
+    RQ_HIP(ctx, realq::attn_fwd(F.qr, F.kr, F.v, D.T, D.H, D.Hkv, D.hd, D.L, F.lse, F.O32, F.O, F.vt, s));
     return REALQ_OK;
 }
 
@@ -578,7 +579,7 @@ int back_to_qkv(realq_ctx* ctx, const DecW& w, const DecDims& D, const DecF& F, 
     RQ_HIP(ctx, realq::scale_split(Wk.dx2, 1.f, nullptr, Wk.sdx2.hi, Wk.sdx2.lo, T * D.d, s));
     if ((rc = prod3(ctx, Wk.sdx2, T, D.d, w.oT, D.Hq, 1.f, Wk.dO))) return rc;
     Timed tm(ctx, "attention");
-    RQ_HIP(ctx, realq::attn_bwd(F.P, F.O32, Wk.dO, F.qr, F.kr, F.v, T, D.H, D.Hkv, D.hd, D.L, Wk.at, Wk.dqr, Wk.dkr,
+    RQ_HIP(ctx, realq::attn_bwd(F.lse, F.O32, Wk.dO, F.qr, F.kr, F.v, T, D.H, D.Hkv, D.hd, D.L, Wk.at, Wk.dqr, Wk.dkr,
                                 Wk.dv, s));
     RQ_HIP(ctx, realq::rope_inv(Wk.dqr, Wk.dq, T, D.H, D.hd, D.L, D.base, s));
     RQ_HIP(ctx, realq::rope_inv(Wk.dkr, Wk.dk, T, D.Hkv, D.hd, D.L, D.base, s));

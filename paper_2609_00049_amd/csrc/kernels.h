@@ -190,12 +190,11 @@ hipError_t rope_fwd(const uint16_t* in, uint16_t* out, int64_t T, int64_t n, int
                     hipStream_t st);
 hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
                     hipStream_t st);
-// Causal attention per sequence of L tokens (L and hd multiples of 32): P [T/L][H][L][L] float32
-// (zeros above the diagonal inside each diagonal 32 x 32 tile; tiles above the diagonal are not
-// written), O32 = P V [T][H hd] float32 and O = bf16(O32);
-// vt receives v^T [Hkv hd][T].
+// Causal attention per sequence of L tokens (L and hd multiples of 32): O32 = softmax(qr kr^T /
+// sqrt(hd)) v [T][H hd] float32, O = bf16(O32), LSE [T][H] the row log-sum-exp (float64) that the
+// backward recomputes the probabilities from; vt receives v^T [Hkv hd][T].
 hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, int64_t T, int64_t H, int64_t Hkv,
-                    int64_t hd, int64_t L, float* P, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st);
+                    int64_t hd, int64_t L, double* LSE, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st);
 // Scratch of the attention backward: D [T][H] float64; dS, dS^T and P^T as bf16 hi/lo pairs,
 // each [T/L][H][L][L]; kr^T [Hkv hd][T], qr^T [H hd][T], dO^T hi/lo [H hd][T].
 struct AttnScratch {
@@ -203,9 +202,9 @@ struct AttnScratch {
     uint16_t *dSh, *dSl, *dSth, *dStl, *Pth, *Ptl;
     uint16_t *kt, *qt, *dOth, *dOtl;
 };
-// From dO [T][H hd] float32 and the forward's P and O32: dq [T][H hd] (gradient at the rotated
+// From dO [T][H hd] float32 and the forward's LSE and O32: dq [T][H hd] (gradient at the rotated
 // queries), dk [T][Hkv hd] (at the rotated keys) and dv [T][Hkv hd], float32.
-hipError_t attn_bwd(const float* P, const float* O32, const float* dO, const uint16_t* qr, const uint16_t* kr,
+hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const uint16_t* qr, const uint16_t* kr,
                     const uint16_t* v, int64_t T, int64_t H, int64_t Hkv, int64_t hd, int64_t L, const AttnScratch& w,
                     float* dq, float* dk, float* dv, hipStream_t st);
 

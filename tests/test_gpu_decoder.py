@@ -265,7 +265,9 @@ def test_decoder_first_steps_with_wide_heads(rq, ctx):
     so that decrease checks the magnitude and sign of the gradient through the attention backward:
     within 1% of the oracle's for q (both sides at the same weights; the loss itself agrees to about
     1e-5 of its value) and within 5% for k, v and o, whose states carry the small differences of
-    the modules before them.  The final loss is held to the module-level tolerance."""
+    the modules before them.  Over the whole sweep at this rate the oracle with every product in
+    float32 (three summation orders) ends 1.0e-3 to 3.5e-3 away from itself in its final loss, so
+    that is held to 5e-3."""
     inp = synth.make_decoder_block(512, 512, 768, 8, 2, 128, 256, seed=12, dense_F=False)
     _banner("decoder block, head_dim 128, 8 over 2 heads, 256-token sequences, lr 1e-4")
     steps, lr = 2, 1e-4
@@ -283,7 +285,7 @@ def test_decoder_first_steps_with_wide_heads(rq, ctx):
         off += steps * -(-o.modules[name].codes.shape[1] // 128)
     assert tr[0] == pytest.approx(o.modules["q"].loss_trace[0][2], rel=1e-4)
     print("loss", g.loss_final, o.loss_final, flush=True)
-    assert abs(g.loss_final - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+    assert abs(g.loss_final - o.loss_final) <= 5e-3 * abs(o.loss_final)
 
 
 def test_decoder_ragged_and_degenerate_shapes(rq, ctx):
