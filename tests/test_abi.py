@@ -93,3 +93,11 @@ def test_defaults_and_host_side_errors_without_gpu():
     assert lib.realq_ctx_create(None, None) == -1
     assert lib.realq_hessian_accum(None, None, None, 0, 0, None) == -1
     assert lib.realq_quantize_layer(None, None, None) == -1
+
+
+def test_plain_c_caller_compiles_and_links(tmp_path):
+    """tests/c_caller/realq_layer_c.c uses the header and the library from C11 with the HIP runtime's C
+    API only (no C++, no PyTorch); it must compile warning-free and link."""
+    from tests.c_caller import compile_c_caller
+    r = compile_c_caller(tmp_path / "realq_layer_c")
+    assert r.returncode == 0, r.stderr
