@@ -352,28 +352,37 @@ __global__ __launch_bounds__(256) void attn_dq_kernel(const uint16_t* __restrict
     for (int e = 0; e < 16; ++e) dq[(s * L + it * AT + acc_row(e, lane)) * H * hd + col] = acc[e] * scale;
 }
 
-// dkr = sum_h dS^T qr / sqrt(hd), dv = sum_h P^T dO over the query heads of key/value head g:
-// grid (S Hkv nt, ceil(hd / 32 / 4)); qt = qr^T [H hd][T], dOt = dO^T as hi/lo [H hd][T].
+// Query tiles per chunk of the dK/dV sums: each (key tile, chunk) pair is one wave, so no wave
+// walks more than CH query tiles per head.
+constexpr int CH = 8;
+int64_t attn_dkv_chunks(int64_t L) { return (L / AT + CH - 1) / CH; }
+
+// Partial dkr = sum_h dS^T qr / sqrt(hd) and dv = sum_h P^T dO over the query heads of key/value
+// head g and the query tiles of chunk z (tiles [z CH, z CH + CH) on or past the key tile):
+// grid (S Hkv nt, ceil(hd / 32 / 4), nch); qt = qr^T [H hd][T], dOt = dO^T as hi/lo [H hd][T].
+// Writes part[z][0][T][Hkv hd] (dk) and part[z][1][T][Hkv hd] (dv); chunks wholly before the key
+// tile write nothing (the reduction skips them).
 __global__ __launch_bounds__(256) void attn_dkv_kernel(const uint16_t* __restrict__ dSth,
                                                        const uint16_t* __restrict__ dStl,
                                                        const uint16_t* __restrict__ Pth, const uint16_t* __restrict__ Ptl,
                                                        const uint16_t* __restrict__ qt,
                                                        const uint16_t* __restrict__ dOth,
                                                        const uint16_t* __restrict__ dOtl, int64_t T, int64_t H,
-                                                       int64_t Hkv, int64_t hd, int64_t L, float* __restrict__ dk,
-                                                       float* __restrict__ dv) {
+                                                       int64_t Hkv, int64_t hd, int64_t L, float* __restrict__ part) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t nt = L / AT;
     const int64_t jt = blockIdx.x % nt, sg = blockIdx.x / nt, g = sg % Hkv, s = sg / Hkv;
     const int64_t ct = (int64_t)blockIdx.y * 4 + wave;
-    if (ct >= hd / AT) return;
+    const int64_t z = blockIdx.z;
+    if (ct >= hd / AT || (z + 1) * CH <= jt) return;
+    const int64_t ibeg = (jt > z * CH ? jt : z * CH) * AT, iend = ((z + 1) * CH < nt ? (z + 1) * CH : nt) * AT;
     const int64_t rep = H / Hkv;
     f32x16 ak = zero16(), av = zero16();
     for (int64_t hh = 0; hh < rep; ++hh) {
         const int64_t h = g * rep + hh, sh = s * H + h;
         const int64_t arow = (sh * L + jt * AT + (lane & 31)) * L + 8 * (lane >> 5);
         const int64_t brow = (h * hd + ct * AT + (lane & 31)) * T + s * L + 8 * (lane >> 5);
-        for (int64_t i0 = jt * AT; i0 < L; i0 += 32) {  // L - jt 32 is a multiple of 32: two steps per trip
+        for (int64_t i0 = ibeg; i0 < iend; i0 += 32) {  // whole tiles: two steps per trip
             bf16x8 q[2], sh_[2], sl[2], ph[2], pl[2], doh[2], dol[2];
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -397,12 +406,30 @@ __global__ __launch_bounds__(256) void attn_dkv_kernel(const uint16_t* __restric
         }
     }
     const float scale = (float)(1.0 / sqrt((double)hd));
-    const int64_t col = g * hd + ct * AT + (lane & 31);
+    const int64_t col = g * hd + ct * AT + (lane & 31), TK = T * Hkv * hd;
+    float* pk = part + 2 * z * TK;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
         const int64_t t = s * L + jt * AT + acc_row(e, lane);
-        dk[t * Hkv * hd + col] = ak[e] * scale;
-        dv[t * Hkv * hd + col] = av[e];
+        pk[t * Hkv * hd + col] = ak[e] * scale;
+        pk[TK + t * Hkv * hd + col] = av[e];
+    }
+}
+
+// dk, dv [T][Hkv hd] = sum over the chunks z of token t's key tile and after (z ascending: a fixed
+// order) of the partial sums.
+__global__ void attn_dkv_reduce_kernel(const float* __restrict__ part, int64_t T, int64_t K, int64_t L,
+                                       int64_t nch, float* __restrict__ dk, float* __restrict__ dv) {
+    const int64_t TK = T * K;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < TK; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t jt = ((e / K) % L) / AT;
+        float a = 0.f, b = 0.f;
+        for (int64_t z = jt / CH; z < nch; ++z) {
+            a += part[2 * z * TK + e];
+            b += part[(2 * z + 1) * TK + e];
+        }
+        dk[e] = a;
+        dv[e] = b;
     }
 }
 
@@ -424,8 +451,12 @@ hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const 
     hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)(S * H * nt), cy), dim3(256), 0, st, w.dSh, w.dSl, w.kt, T, H,
                        Hkv, hd, L, dq);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_dkv_kernel, dim3((unsigned)(S * Hkv * nt), cy), dim3(256), 0, st, w.dSth, w.dStl, w.Pth,
-                       w.Ptl, w.qt, w.dOth, w.dOtl, T, H, Hkv, hd, L, dk, dv);
+    const int64_t nch = attn_dkv_chunks(L);
+    hipLaunchKernelGGL(attn_dkv_kernel, dim3((unsigned)(S * Hkv * nt), cy, (unsigned)nch), dim3(256), 0, st, w.dSth,
+                       w.dStl, w.Pth, w.Ptl, w.qt, w.dOth, w.dOtl, T, H, Hkv, hd, L, w.part);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_dkv_reduce_kernel, dim3(grid_of(T * Hkv * hd)), dim3(TB), 0, st, w.part, T, Hkv * hd, L, nch,
+                       dk, dv);
     return hipGetLastError();
 }
 

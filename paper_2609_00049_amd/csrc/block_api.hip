@@ -541,7 +541,8 @@ int alloc_work(realq_ctx* ctx, const char* tag, const DecDims& D, DecWork& Wk) {
         (rc = ws(ctx, "att_dStl", TL, a.dStl)) || (rc = ws(ctx, "att_Pth", TL, a.Pth)) ||
         (rc = ws(ctx, "att_Ptl", TL, a.Ptl)) || (rc = ws(ctx, "att_kt", T * D.Hk, a.kt)) ||
         (rc = ws(ctx, "att_qt", T * D.Hq, a.qt)) || (rc = ws(ctx, "att_dOth", T * D.Hq, a.dOth)) ||
-        (rc = ws(ctx, "att_dOtl", T * D.Hq, a.dOtl)))
+        (rc = ws(ctx, "att_dOtl", T * D.Hq, a.dOtl)) ||
+        (rc = ws(ctx, "att_part", realq::attn_dkv_chunks(D.L) * 2 * T * D.Hk, a.part)))
         return rc;
     return REALQ_OK;
 }

@@ -196,12 +196,15 @@ hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t h
 hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, int64_t T, int64_t H, int64_t Hkv,
                     int64_t hd, int64_t L, double* LSE, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st);
 // Scratch of the attention backward: D [T][H] float64; dS, dS^T and P^T as bf16 hi/lo pairs,
-// each [T/L][H][L][L]; kr^T [Hkv hd][T], qr^T [H hd][T], dO^T hi/lo [H hd][T].
+// each [T/L][H][L][L]; kr^T [Hkv hd][T], qr^T [H hd][T], dO^T hi/lo [H hd][T]; partial dK/dV.
 struct AttnScratch {
     double* D;
     uint16_t *dSh, *dSl, *dSth, *dStl, *Pth, *Ptl;
     uint16_t *kt, *qt, *dOth, *dOtl;
+    float* part;  // [attn_dkv_chunks(L)][2][T][Hkv hd] partial dK/dV sums
 };
+// number of query-tile chunks whose partial dK/dV sums the backward keeps
+int64_t attn_dkv_chunks(int64_t L);
 // From dO [T][H hd] float32 and the forward's LSE and O32: dq [T][H hd] (gradient at the rotated
 // queries), dk [T][Hkv hd] (at the rotated keys) and dv [T][Hkv hd], float32.
 hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const uint16_t* qr, const uint16_t* kr,
