@@ -218,6 +218,28 @@ def test_layer_ragged_shapes(rq, ctx):
     assert (g.W_hat.cpu() == sc * (codes.float() - zr)).all()
 
 
+@pytest.mark.parametrize("case", ["one_row", "eight_columns", "one_token", "dead_column"])
+def test_layer_degenerate_shapes(rq, ctx, case):
+    """Whole sweeps at the method's degenerate points: a single output row (m = 1); eight input
+    columns (one partial block and group); a single calibration token (a rank-1 Hessian, carried
+    by the damping); and an input channel that is zero in both X and X_hat (a dead column: its
+    weights are zeroed at its block and Block-GD, whose gradient there is zero, leaves them at
+    zero)."""
+    sizes = {"one_row": (1, 136, 64), "eight_columns": (9, 8, 16), "one_token": (33, 200, 1),
+             "dead_column": (24, 256, 300)}[case]
+    m, n, T = sizes
+    L = synth.make_module("single_512", m=m, n=n, T=T, seed=5)
+    if case == "dead_column":
+        L.X[:, 140] = 0.0
+        L.Xhat[:, 140] = 0.0
+    _banner(f"layer degenerate {case} m={m} n={n} T={T}")
+    g = _run(rq, ctx, L, 2, 1e-3)
+    o = _oracle(L, 2, 1e-3)
+    _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
+    if case == "dead_column":
+        assert (g.W_hat.cpu()[:, 140] == 0).all() and (o.W_hat[:, 140] == 0).all()
+
+
 def test_layer_token_chunks_match_single_chunk(rq, ctx):
     L = synth.make_module("single_512", m=64, n=256, T=2000)
     _banner("layer token chunks")
