@@ -158,10 +158,12 @@ class BlockResult:
 
 def mlp_block_sweep(X, Xhat, blk: MLPBlock, *, qp: Optional[QParams] = None, steps=0, lr=1e-3,
                     nxt: Optional[MLPBlock] = None, window=False, eps=RMS_EPS,
-                    modules=MODULES) -> BlockResult:
+                    modules=MODULES, batch: Optional[int] = None) -> BlockResult:
     """Quantize gate, up and down of one MLP block in order (Alg. 1), each with GPTQ on its own
     input in the quantized path (u for gate and up, z for down) and Block-GD on the block-output
-    surrogate after every column block.  window=True blends in ``nxt`` over b_global."""
+    surrogate after every column block.  window=True blends in ``nxt`` over b_global.
+    ``batch``: tokens per Adam step (Sec. 4.3 mini-batch, scheduled by realq_oracle.minibatch);
+    a step's surrogate is the block's on those tokens alone, normalised by their count."""
     qp = qp or QParams()
     X, Xhat = _f64(X), _f64(Xhat)
     T = X.shape[0]
@@ -176,19 +178,21 @@ def mlp_block_sweep(X, Xhat, blk: MLPBlock, *, qp: Optional[QParams] = None, ste
         offset[k] = B_total
         B_total += nb[k]
 
-    def forward(Wcur):
-        return mlp_forward(Xhat, blk.gamma, Wcur["gate"], Wcur["up"], Wcur["down"], eps)
+    def forward(Wcur, tokens=slice(0, T)):
+        return mlp_forward(Xhat[tokens], blk.gamma, Wcur["gate"], Wcur["up"], Wcur["down"], eps)
 
     res = {}
     for name in modules:
         fw = forward(W)
         inp = fw.u if name != "down" else fw.z
 
-        def grad_fn(Wm, J, alpha, name=name):
+        def grad_fn(Wm, J, alpha, tokens, name=name):
             Wc = dict(W)
             Wc[name] = Wm
-            f = forward(Wc)
-            L, gy = surrogate(f, ystar, blk.F, T, nxt, y2star, alpha, eps)
+            f = forward(Wc, tokens)
+            Tb = f.y.shape[0]
+            L, gy = surrogate(f, ystar[tokens], blk.F, Tb, nxt, None if y2star is None else y2star[tokens],
+                              alpha, eps)
             return L, module_grad(name, f, gy, Wc["gate"], Wc["up"], Wc["down"], J, eps)
 
         def loss_fn(Wm, name=name):
@@ -198,7 +202,7 @@ def mlp_block_sweep(X, Xhat, blk: MLPBlock, *, qp: Optional[QParams] = None, ste
 
         r = quantize_layer(W[name], inp, inp, qp=qp, steps=steps, lr=lr,
                            window=(offset[name], B_total) if (window and nxt is not None) else None,
-                           grad_fn=grad_fn, loss_fn=loss_fn)
+                           batch=batch, grad_fn=grad_fn, loss_fn=loss_fn)
         W[name] = r.W_hat
         res[name] = r
     loss = surrogate(forward(W), ystar, blk.F, T)[0]
@@ -389,13 +393,18 @@ def decoder_surrogate(fw: DecoderForward, ystar, blk: DecoderBlock, T, W=None, n
 
 
 def decoder_block_sweep(X, Xhat, blk: DecoderBlock, *, qp: Optional[QParams] = None, steps=0, lr=1e-3,
-                        nxt: Optional[DecoderBlock] = None, window=False, eps=RMS_EPS):
+                        nxt: Optional[DecoderBlock] = None, window=False, eps=RMS_EPS,
+                        batch: Optional[int] = None):
     """Quantize q, k, v, o, gate, up and down of one decoder block in order (Alg. 1): GPTQ on each
     module's input in the quantized path and Block-GD on the block-output surrogate after every
-    column block; window=True blends in ``nxt`` over b_global across the seven modules."""
+    column block; window=True blends in ``nxt`` over b_global across the seven modules.
+    ``batch``: tokens per Adam step (Sec. 4.3 mini-batch), a multiple of seq_len so that every
+    batch holds whole calibration sequences (attention mixes the tokens of a sequence)."""
     qp = qp or QParams()
     X, Xhat = _f64(X), _f64(Xhat)
     T = X.shape[0]
+    if batch is not None and batch % blk.seq_len:
+        raise ValueError("decoder_block_sweep: batch must be a multiple of seq_len")
     W = {k: _f64(v).copy() for k, v in blk.weights().items()}
     ystar = decoder_forward(X, blk, W, eps).y
     y2star = decoder_forward(ystar, nxt, None, eps).y if nxt is not None else None
@@ -410,11 +419,13 @@ def decoder_block_sweep(X, Xhat, blk: DecoderBlock, *, qp: Optional[QParams] = N
         fw = decoder_forward(Xhat, blk, W, eps)
         inp = getattr(fw, inputs[name]) if name in inputs else (fw.mlp.u if name != "down" else fw.mlp.z)
 
-        def grad_fn(Wm, J, alpha, name=name):
+        def grad_fn(Wm, J, alpha, tokens, name=name):
             Wc = dict(W)
             Wc[name] = Wm
-            f = decoder_forward(Xhat, blk, Wc, eps)
-            Lv, bw = decoder_surrogate(f, ystar, blk, T, Wc, nxt, y2star, alpha, eps)
+            f = decoder_forward(Xhat[tokens], blk, Wc, eps)
+            Tb = f.y.shape[0]
+            Lv, bw = decoder_surrogate(f, ystar[tokens], blk, Tb, Wc, nxt,
+                                       None if y2star is None else y2star[tokens], alpha, eps)
             return Lv, decoder_module_grad(name, f, bw, J)
 
         def loss_fn(Wm, name=name):
@@ -425,7 +436,7 @@ def decoder_block_sweep(X, Xhat, blk: DecoderBlock, *, qp: Optional[QParams] = N
 
         r = quantize_layer(W[name], inp, inp, qp=qp, steps=steps, lr=lr,
                            window=(offset[name], B_total) if (window and nxt is not None) else None,
-                           grad_fn=grad_fn, loss_fn=loss_fn)
+                           batch=batch, grad_fn=grad_fn, loss_fn=loss_fn)
         W[name] = r.W_hat
         res[name] = r
     loss = fisher_loss(decoder_forward(Xhat, blk, W, eps).y - ystar, blk.F, T)

@@ -302,9 +302,11 @@ def gram_surrogate(W0, X, Xhat, s=None):
         quad = np.sum((W @ Hs) * W, axis=1) - 2.0 * np.sum((W @ Ks.T) * W0, axis=1)
         return float(np.sum(0.5 * quad + c))
 
-    def grad_fn(W, J, alpha):
+    def grad_fn(W, J, alpha, tokens=slice(0, T)):
         if alpha != 1.0:
             raise ValueError("gram_surrogate has no sliding-window partner")
+        if range(T)[tokens] != range(T):
+            raise ValueError("gram_surrogate is formed over all tokens: no mini-batch")
         return loss_fn(W), (W @ Hs[:, J] - W0 @ Ks[:, J])
 
     return grad_fn, loss_fn
@@ -414,9 +416,10 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     (and its own damping, dead columns and inverse factor) instead of the one built from ``s``;
     ``s`` keeps weighting the tokens of the BGD surrogate.  H, U and dead of the result are
     then lists over the groups.
-    ``grad_fn(W, J, alpha) -> (loss, grad of W[:, J])`` replaces the module-output surrogate
-    of every BGD step (a surrogate evaluated further downstream, e.g. at a transformer block's
-    output), and ``loss_fn(W)`` the final loss; X and the surrogate arguments are then unused
+    ``grad_fn(W, J, alpha, tokens) -> (loss, grad of W[:, J])`` replaces the module-output
+    surrogate of every BGD step (a surrogate evaluated further downstream, e.g. at a transformer
+    block's output) on the calibration tokens ``tokens = minibatch(t, T, batch)`` of step t, and
+    ``loss_fn(W)`` the final loss over all tokens; X and the surrogate arguments are then unused
     and the Hessian still comes from Xhat.
     """
     qp = qp or QParams()
@@ -492,12 +495,12 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
             J = slice(c1, n)
             for k in range(steps):
                 t += 1
+                sl = minibatch(t, T, batch)
                 if grad_fn is not None:
-                    lv, G = grad_fn(W, J, alpha)
+                    lv, G = grad_fn(W, J, alpha, sl)
                     trace.append((b, k, lv))
                     W[:, J], mA[:, J], vA[:, J] = adam_update(W[:, J], G, mA[:, J], vA[:, J], t, lr)
                     continue
-                sl = minibatch(t, T, batch)
                 Tb = sl.stop - sl.start
                 sb = None if s is None else s[sl]
                 R = residual(W, W0, X[sl], Xhat[sl])

@@ -303,3 +303,54 @@ def test_decoder_sweep_without_bgd_is_gptq_on_each_modules_input():
         ref = quantize_layer(W[name], inp, inp)
         assert (res.modules[name].codes == ref.codes).all(), name
         W[name] = ref.W_hat
+
+
+# ============================================================================ mini-batch Block-GD
+
+def _batch_sizes(T, batch):
+    return [min(T, (i + 1) * batch) - i * batch for i in range(-(-T // batch))]
+
+
+def _check_token_average(full, mb, sizes, T):
+    """With lr = 0 the weights never move, so step k of a column block sees the weights of the
+    full-batch run at the same step; each surrogate is a token average, hence the count-weighted
+    mean of the batch losses over one cycle of batches is the full-batch loss."""
+    nb = len(sizes)
+    for name, r in full.modules.items():
+        tr_f, tr_b = r.loss_trace, mb.modules[name].loss_trace
+        assert len(tr_f) == len(tr_b) and len(tr_f) % nb == 0
+        for i in range(0, len(tr_f), nb):
+            # a module's steps count from t = 1, so every cycle starts at batch 0
+            mean = sum(sizes[j] * tr_b[i + j][2] for j in range(nb)) / T
+            assert mean == pytest.approx(tr_f[i][2], rel=1e-11), name
+            assert len({tr_b[i + j][2] for j in range(nb)}) == nb   # distinct batches
+        assert np.array_equal(r.W_hat, mb.modules[name].W_hat)
+    assert mb.loss_final == full.loss_final
+
+
+def test_mlp_minibatch_losses_average_to_the_full_batch_loss():
+    X, Xh, blk = _inputs(seed=12)
+    nxt = B.MLPBlock(gamma=blk.gamma[::-1].copy(), Wg=blk.Wu.copy(), Wu=blk.Wg.copy() * 0.5,
+                     Wd=blk.Wd[::-1].copy(), F=None)
+    T, batch = X.shape[0], 96                       # batches of 96, 96 and a ragged 64
+    sizes = _batch_sizes(T, batch)
+    kw = dict(steps=len(sizes), lr=0.0, nxt=nxt, window=True)
+    full = B.mlp_block_sweep(X, Xh, blk, **kw)
+    _check_token_average(full, B.mlp_block_sweep(X, Xh, blk, batch=batch, **kw), sizes, T)
+    # a batch of at least T tokens is the full batch, bit for bit
+    same = B.mlp_block_sweep(X, Xh, blk, steps=2, lr=1e-3, batch=T)
+    ref = B.mlp_block_sweep(X, Xh, blk, steps=2, lr=1e-3)
+    assert all(np.array_equal(same.modules[k].W_hat, ref.modules[k].W_hat) for k in B.MODULES)
+
+
+def test_decoder_minibatch_losses_average_to_the_full_batch_loss():
+    X, Xh, blk = _dec_inputs(seed=31)
+    nxt = B.DecoderBlock(**{**blk.__dict__, "Wq": blk.Wk.repeat(2, axis=0), "Wo": blk.Wo[::-1].copy(),
+                            "gamma1": blk.gamma1[::-1].copy()})
+    T, batch = X.shape[0], 2 * blk.seq_len          # two batches of two sequences
+    sizes = _batch_sizes(T, batch)
+    kw = dict(steps=len(sizes), lr=0.0, nxt=nxt, window=True)
+    full = B.decoder_block_sweep(X, Xh, blk, **kw)
+    _check_token_average(full, B.decoder_block_sweep(X, Xh, blk, batch=batch, **kw), sizes, T)
+    with pytest.raises(ValueError):
+        B.decoder_block_sweep(X, Xh, blk, steps=1, batch=blk.seq_len + 8)

@@ -410,6 +410,9 @@ def test_gram_surrogate_equals_the_token_form():
     assert loss_fn(W) == pytest.approx(surrogate_loss(R, s, None, T), rel=1e-11)
     with pytest.raises(ValueError):
         grad_fn(W, slice(1, 4), 0.5)
+    assert grad_fn(W, slice(1, 4), 1.0, slice(0, T))[0] == lv
+    with pytest.raises(ValueError):
+        grad_fn(W, slice(1, 4), 1.0, slice(0, T - 1))
 
 
 def test_sweep_driven_by_the_gram_surrogate_is_the_token_sweep():
