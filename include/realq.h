@@ -339,7 +339,10 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* desc, realq_lay
  *   F         : [d, d] float32 symmetric Fisher at the block output, or NULL (identity)
  *   next      : the next block, same shapes; next.Wg == NULL when there is none
  *   q         : quantizer as for realq_quantize_layer (group = 0: one group per row)
- *   bgd       : steps, lr and the Adam constants; form, loss_clip and batch must be 0
+ *   bgd       : steps, lr, the Adam constants and batch; form and loss_clip must be 0.
+ *               With 0 < batch < T, Adam step t of a module (1-based) evaluates L (and
+ *               L_next) on token batch (t - 1) mod ceil(T / batch) only, normalised by its
+ *               token count (Sec. 4.3 mini-batch); loss_final is over all T tokens
  * Outputs per module (0 gate, 1 up, 2 down): codes [rows, cols] (gate, up: [f, d]; down:
  * [d, f]), scales and zeros [rows, ceil(cols/group)], W_hat [rows, cols] float32 (all
  * required); loss_trace [B_total * steps] device float64, entry (b_global - 1) * steps + k,
@@ -393,7 +396,8 @@ int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* desc, realq_mlp_
  * b_global running over the column blocks of all seven modules; the window partner is the
  * next decoder block.  Shapes: Wq [H hd, d], Wk and Wv [Hkv hd, d], Wo [d, H hd]; seq_len a
  * multiple of 32 and at most 4096, T a multiple of seq_len, H a multiple of Hkv, head_dim a
- * multiple of 32 and at most 256, d and f multiples of 8 (REALQ_ERR_SHAPE otherwise).  The
+ * multiple of 32 and at most 256, d and f multiples of 8, bgd.batch a multiple of seq_len, so
+ * that a mini-batch holds whole sequences (REALQ_ERR_SHAPE otherwise).  The
  * attention forward keeps the row log-sum-exp (the backward recomputes the probabilities from
  * it); its backward keeps six bf16 arrays of T n_heads seq_len entries.  Outputs per
  * module in the order q, k, v, o, gate, up, down; loss_trace entry (b_global - 1) * steps + k. */

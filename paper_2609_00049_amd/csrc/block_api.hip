@@ -167,6 +167,23 @@ int alloc_fwd(realq_ctx* ctx, const char* tag, int64_t T, int64_t d, int64_t f, 
     return REALQ_OK;
 }
 
+// tokens [t0, ...) of a forward: every buffer is token-major, so a row offset is a pointer offset
+Fwd rows_of(const Fwd& F, int64_t t0, int64_t d, int64_t f) {
+    return Fwd{F.u + t0 * d, F.a + t0 * f, F.b + t0 * f, F.z + t0 * f, F.out + t0 * d, F.y + t0 * d};
+}
+
+// The tokens of Block-GD step t (1-based, counted over a module): consecutive batches of
+// `batch` tokens (the last one shorter when batch does not divide T), cycled in order; batch 0
+// or >= T means all tokens.
+struct TokenBatch {
+    int64_t t0, n;
+};
+TokenBatch step_tokens(int64_t t, int64_t T, int64_t batch) {
+    if (batch <= 0 || batch >= T) return {0, T};
+    const int64_t nbatch = (T + batch - 1) / batch, t0 = ((t - 1) % nbatch) * batch;
+    return {t0, std::min(T, t0 + batch) - t0};
+}
+
 // full forward of a block on h (bf16 or float32 input), y written; dy = y - ystar when dy != NULL
 int forward(realq_ctx* ctx, const BlockW& w, const uint16_t* hb, const float* hf, int64_t T, int64_t d, int64_t f,
             double eps, Fwd& F, const float* ystar, float* dy) {
@@ -192,8 +209,8 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
     const int64_t T = D->T, d = D->d, f = D->f;
     if (T < 1 || d < 1 || f < 1 || d % 8 || f % 8)
         return set_error(ctx, REALQ_ERR_SHAPE, "mlp_block_sweep: need T, d, f >= 1 and d, f multiples of 8");
-    if (D->bgd.form != REALQ_BGD_TOKENS || D->bgd.loss_clip != 0.f || D->bgd.batch != 0)
-        return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: form, loss_clip and batch must be 0");
+    if (D->bgd.form != REALQ_BGD_TOKENS || D->bgd.loss_clip != 0.f)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: form and loss_clip must be 0");
     const realq_mlp_block& B0 = D->blk;
     if (!D->X || !D->Xhat || !B0.gamma || !B0.Wg || !B0.Wu || !B0.Wd)
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: NULL input or weight");
@@ -275,40 +292,43 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
         RQ_HIP(ctx, realq::transpose_u16(fq.u, d, uT, T, T, d, s));
     }
 
-    // L (and L_next) at the quantized path's current forward fq; g = dL_slide/dy.  Returns
-    // the loss on the device in *lossd (scaled partial sums reduced in a fixed order).
-    auto surrogate = [&](double alpha) -> int {
-        RQ_HIP(ctx, realq::residual_out_bf16(D->Xhat, fq.out, ystar, nullptr, dy, T * d, s));
+    // L (and L_next) at the quantized path's current forward fq over tokens [t0, t0 + Tb);
+    // g = dL_slide/dy of those tokens (rows 0..Tb-1).  Returns the loss on the device in *lossd
+    // (scaled partial sums reduced in a fixed order).
+    auto surrogate = [&](double alpha, int64_t t0, int64_t Tb) -> int {
+        const Fwd q = rows_of(fq, t0, d, f);
+        const uint16_t* xh = D->Xhat + t0 * d;
+        RQ_HIP(ctx, realq::residual_out_bf16(xh, q.out, ystar + t0 * d, nullptr, dy, Tb * d, s));
         if (B0.F) {
-            RQ_HIP(ctx, realq::scale_split(dy, 1.f, nullptr, sdy.hi, sdy.lo, T * d, s));
-            if ((rc = prod3(ctx, sdy, T, d, w0.F, d, (float)(1.0 / (double)T), g))) return rc;
+            RQ_HIP(ctx, realq::scale_split(dy, 1.f, nullptr, sdy.hi, sdy.lo, Tb * d, s));
+            if ((rc = prod3(ctx, sdy, Tb, d, w0.F, d, (float)(1.0 / (double)Tb), g))) return rc;
         } else {
-            RQ_HIP(ctx, realq::scale_split(dy, (float)(1.0 / (double)T), g, nullptr, nullptr, T * d, s));
+            RQ_HIP(ctx, realq::scale_split(dy, (float)(1.0 / (double)Tb), g, nullptr, nullptr, Tb * d, s));
         }
-        RQ_HIP(ctx, realq::dot_f32(dy, g, T * d, 0.5 * alpha, parts, s));
+        RQ_HIP(ctx, realq::dot_f32(dy, g, Tb * d, 0.5 * alpha, parts, s));
         if (window && alpha < 1.0) {
             // next block on y = Xhat + out, its loss, and its input gradient blended into g
-            RQ_HIP(ctx, realq::residual_out_bf16(D->Xhat, fq.out, nullptr, fq.y, nullptr, T * d, s));
-            if ((rc = forward(ctx, w2, nullptr, fq.y, T, d, f, eps, fn, y2star, dy2))) return rc;
+            RQ_HIP(ctx, realq::residual_out_bf16(xh, q.out, nullptr, q.y, nullptr, Tb * d, s));
+            if ((rc = forward(ctx, w2, nullptr, q.y, Tb, d, f, eps, fn, y2star + t0 * d, dy2))) return rc;
             if (D->next.F) {
-                RQ_HIP(ctx, realq::scale_split(dy2, 1.f, nullptr, sdy2.hi, sdy2.lo, T * d, s));
-                if ((rc = prod3(ctx, sdy2, T, d, w2.F, d, (float)(1.0 / (double)T), g2))) return rc;
+                RQ_HIP(ctx, realq::scale_split(dy2, 1.f, nullptr, sdy2.hi, sdy2.lo, Tb * d, s));
+                if ((rc = prod3(ctx, sdy2, Tb, d, w2.F, d, (float)(1.0 / (double)Tb), g2))) return rc;
             } else {
-                RQ_HIP(ctx, realq::scale_split(dy2, (float)(1.0 / (double)T), g2, nullptr, nullptr, T * d, s));
+                RQ_HIP(ctx, realq::scale_split(dy2, (float)(1.0 / (double)Tb), g2, nullptr, nullptr, Tb * d, s));
             }
-            RQ_HIP(ctx, realq::dot_f32(dy2, g2, T * d, 0.5 * (1.0 - alpha), parts + npart, s));
-            RQ_HIP(ctx, realq::scale_split(g2, 1.f, nullptr, sg2.hi, sg2.lo, T * d, s));
-            if ((rc = prod3(ctx, sg2, T, d, w2.dT, f, 1.f, dz2))) return rc;  // dz2 = g2 Wd2
-            RQ_HIP(ctx, realq::swiglu_bwd(dz2, fn.a, fn.b, 0, T, f, 0, sda2.hi, sda2.lo, f, s));
-            RQ_HIP(ctx, realq::swiglu_bwd(dz2, fn.a, fn.b, 1, T, f, 0, sdb2.hi, sdb2.lo, f, s));
-            if ((rc = prod3(ctx, sda2, T, f, w2.gT, d, 1.f, du2))) return rc;  // du2 = da2 Wg2 + db2 Wu2
-            realq::GemmArgs a1{sdb2.hi, sdb2.lo, f, w2.uT.hi, f, T, d, f, 1};
+            RQ_HIP(ctx, realq::dot_f32(dy2, g2, Tb * d, 0.5 * (1.0 - alpha), parts + npart, s));
+            RQ_HIP(ctx, realq::scale_split(g2, 1.f, nullptr, sg2.hi, sg2.lo, Tb * d, s));
+            if ((rc = prod3(ctx, sg2, Tb, d, w2.dT, f, 1.f, dz2))) return rc;  // dz2 = g2 Wd2
+            RQ_HIP(ctx, realq::swiglu_bwd(dz2, fn.a, fn.b, 0, Tb, f, 0, sda2.hi, sda2.lo, f, s));
+            RQ_HIP(ctx, realq::swiglu_bwd(dz2, fn.a, fn.b, 1, Tb, f, 0, sdb2.hi, sdb2.lo, f, s));
+            if ((rc = prod3(ctx, sda2, Tb, f, w2.gT, d, 1.f, du2))) return rc;  // du2 = da2 Wg2 + db2 Wu2
+            realq::GemmArgs a1{sdb2.hi, sdb2.lo, f, w2.uT.hi, f, Tb, d, f, 1};
             RQ_HIP(ctx, realq::gemm_acc_f32(a1, du2, d, 1.f, s));
             if (w2.uT.lo_or_null()) {
-                realq::GemmArgs a2{sdb2.hi, nullptr, f, w2.uT.lo, f, T, d, f, 1};
+                realq::GemmArgs a2{sdb2.hi, nullptr, f, w2.uT.lo, f, Tb, d, f, 1};
                 RQ_HIP(ctx, realq::gemm_acc_f32(a2, du2, d, 1.f, s));
             }
-            RQ_HIP(ctx, realq::rmsnorm_bwd_blend(fq.y, g2, du2, D->next.gamma, eps, alpha, T, d, g, s));
+            RQ_HIP(ctx, realq::rmsnorm_bwd_blend(q.y, g2, du2, D->next.gamma, eps, alpha, Tb, d, g, s));
             RQ_HIP(ctx, realq::reduce_partials(parts, 2 * npart, 1.0, lossd, s));
         } else {
             RQ_HIP(ctx, realq::reduce_partials(parts, npart, 1.0, lossd, s));
@@ -343,29 +363,33 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
             const int64_t nJ = n - c1;
             for (int k = 0; k < steps; ++k) {
                 Timed tm(ctx, "block_step");
+                const TokenBatch tb = step_tokens(t_adam + 1, T, D->bgd.batch);
+                const int64_t Tb = tb.n;
+                const Fwd q = rows_of(fq, tb.t0, d, f);
                 // forward of the partially quantized block with this module's current weights
                 RQ_HIP(ctx, realq::split3_f64(W, sW.hi, sW.lo, sW.lo2, m * n, s));
                 if (mod == 0) {
-                    if ((rc = lin_f32(ctx, sW, f, d, fq.u, T, fq.a))) return rc;
+                    if ((rc = lin_f32(ctx, sW, f, d, q.u, Tb, q.a))) return rc;
                 } else if (mod == 1) {
-                    if ((rc = lin_f32(ctx, sW, f, d, fq.u, T, fq.b))) return rc;
+                    if ((rc = lin_f32(ctx, sW, f, d, q.u, Tb, q.b))) return rc;
                 }
-                if (mod < 2) RQ_HIP(ctx, realq::swiglu_fwd(fq.a, fq.b, fq.z, T * f, s));
-                if ((rc = lin_bf16(ctx, mod == 2 ? sW : w0.d, d, f, fq.z, T, fq.out))) return rc;
-                if ((rc = surrogate(alpha))) return rc;
+                if (mod < 2) RQ_HIP(ctx, realq::swiglu_fwd(q.a, q.b, q.z, Tb * f, s));
+                if ((rc = lin_bf16(ctx, mod == 2 ? sW : w0.d, d, f, q.z, Tb, q.out))) return rc;
+                if ((rc = surrogate(alpha, tb.t0, Tb))) return rc;
                 if (out->loss_trace)
                     RQ_HIP(ctx, hipMemcpyAsync(out->loss_trace + (off[mod] + b) * steps + k, lossd, 8,
                                                hipMemcpyDeviceToDevice, s));
-                // gradient of this module's trailing columns
+                // gradient of this module's trailing columns over the step's tokens (the
+                // transposed inputs keep their stride T, the transposed output gradient has Tb)
                 if (mod < 2) {
-                    RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, sg.hi, sg.lo, T * d, s));
-                    if ((rc = prod3(ctx, sg, T, d, w0.dT, f, 1.f, dz))) return rc;  // dz = g Wd
-                    RQ_HIP(ctx, realq::swiglu_bwd(dz, fq.a, fq.b, mod, T, f, 1, svT.hi, svT.lo, T, s));
-                    realq::GemmArgs gg{svT.hi, svT.lo, T, uT + c1 * T, T, f, nJ, T, 1};
+                    RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, sg.hi, sg.lo, Tb * d, s));
+                    if ((rc = prod3(ctx, sg, Tb, d, w0.dT, f, 1.f, dz))) return rc;  // dz = g Wd
+                    RQ_HIP(ctx, realq::swiglu_bwd(dz, q.a, q.b, mod, Tb, f, 1, svT.hi, svT.lo, Tb, s));
+                    realq::GemmArgs gg{svT.hi, svT.lo, Tb, uT + c1 * T + tb.t0, T, f, nJ, Tb, 1};
                     RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
                 } else {
-                    RQ_HIP(ctx, realq::transpose_split_f32(g, d, sgT.hi, sgT.lo, T, T, d, s));
-                    realq::GemmArgs gg{sgT.hi, sgT.lo, T, zT + c1 * T, T, d, nJ, T, 1};
+                    RQ_HIP(ctx, realq::transpose_split_f32(g, d, sgT.hi, sgT.lo, Tb, Tb, d, s));
+                    realq::GemmArgs gg{sgT.hi, sgT.lo, Tb, zT + c1 * T + tb.t0, T, d, nJ, Tb, 1};
                     RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
                 }
                 ++t_adam;
@@ -397,8 +421,8 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
         if (mod < 2) RQ_HIP(ctx, realq::swiglu_fwd(fq.a, fq.b, fq.z, T * f, s));
         if ((rc = lin_bf16(ctx, mod == 2 ? q : w0.d, d, f, fq.z, T, fq.out))) return rc;
     }
-    // own-block loss at the quantized weights (fq holds the final forward)
-    if ((rc = surrogate(1.0))) return rc;
+    // own-block loss at the quantized weights over all tokens (fq holds the final forward)
+    if ((rc = surrogate(1.0, 0, T))) return rc;
     RQ_HIP(ctx, hipEventRecord(ev.b, s));
     RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lossd, 8, hipMemcpyDeviceToHost, s));
     RQ_HIP(ctx, hipStreamSynchronize(s));
@@ -463,6 +487,26 @@ struct DecF {  // buffers of one forward of the decoder block
     double* lse;  // [T][H] row log-sum-exp of the attention (the backward recomputes P from it)
     Fwd mlp;
 };
+
+// tokens [t0, ...) of a decoder forward (t0 a multiple of the sequence length).  vt is the
+// attention's own transposed copy of v, written and read with the stride of the token count it
+// is given, so it is shared rather than offset.
+DecF rows_of(const DecF& F, const DecDims& D, int64_t t0) {
+    DecF v = F;
+    v.h1 += t0 * D.d;
+    v.q += t0 * D.Hq;
+    v.k += t0 * D.Hk;
+    v.v += t0 * D.Hk;
+    v.qr += t0 * D.Hq;
+    v.kr += t0 * D.Hk;
+    v.O += t0 * D.Hq;
+    v.o += t0 * D.d;
+    v.O32 += t0 * D.Hq;
+    v.x2 += t0 * D.d;
+    v.lse += t0 * D.H;
+    v.mlp = rows_of(F.mlp, t0, D.d, D.f);
+    return v;
+}
 
 int alloc_decf(realq_ctx* ctx, const char* tag, const DecDims& D, DecF& F) {
     const std::string t(tag);
@@ -646,10 +690,12 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
     if (!Dd || !out) return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: NULL desc or out");
     int rc;
     if ((rc = realq::validate_q(ctx, &Dd->q)) || (rc = realq::validate_bgd(ctx, &Dd->bgd))) return rc;
-    if (Dd->bgd.form != REALQ_BGD_TOKENS || Dd->bgd.loss_clip != 0.f || Dd->bgd.batch != 0)
-        return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: form, loss_clip and batch must be 0");
+    if (Dd->bgd.form != REALQ_BGD_TOKENS || Dd->bgd.loss_clip != 0.f)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: form and loss_clip must be 0");
     DecDims D;
     if ((rc = check_decoder(ctx, Dd, "decoder_block_sweep", D))) return rc;
+    if (Dd->bgd.batch % D.L)
+        return set_error(ctx, REALQ_ERR_SHAPE, "decoder_block_sweep: batch must be a multiple of seq_len");
     if (!Dd->Xhat) return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: NULL Xhat");
     const realq_decoder_block& B0 = Dd->blk;
     const realq_decoder_block& N0 = Dd->next;
@@ -723,37 +769,41 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
         RQ_HIP(ctx, realq::transpose_u16(Fq.h1, d, h1T, T, T, d, s));
     }
 
-    // L_slide and g = dL_slide/dy at the quantized path's current forward Fq
-    auto surrogate = [&](double alpha) -> int {
-        RQ_HIP(ctx, realq::residual_out_f32(Fq.x2, Fq.mlp.out, ystar, nullptr, dy, T * d, s));
+    // L_slide and g = dL_slide/dy at the quantized path's current forward Fq over the whole
+    // sequences of tokens [t0, t0 + Tb); g holds those tokens' rows from row 0
+    auto surrogate = [&](double alpha, int64_t t0, int64_t Tb) -> int {
+        const DecF q = rows_of(Fq, D, t0);
+        DecDims Db = D;
+        Db.T = Tb;
+        RQ_HIP(ctx, realq::residual_out_f32(q.x2, q.mlp.out, ystar + t0 * d, nullptr, dy, Tb * d, s));
         if (B0.mlp.F) {
-            RQ_HIP(ctx, realq::scale_split(dy, 1.f, nullptr, sdy.hi, sdy.lo, T * d, s));
-            if ((rc = prod3(ctx, sdy, T, d, wq.mlp.F, d, (float)(1.0 / (double)T), g))) return rc;
+            RQ_HIP(ctx, realq::scale_split(dy, 1.f, nullptr, sdy.hi, sdy.lo, Tb * d, s));
+            if ((rc = prod3(ctx, sdy, Tb, d, wq.mlp.F, d, (float)(1.0 / (double)Tb), g))) return rc;
         } else {
-            RQ_HIP(ctx, realq::scale_split(dy, (float)(1.0 / (double)T), g, nullptr, nullptr, T * d, s));
+            RQ_HIP(ctx, realq::scale_split(dy, (float)(1.0 / (double)Tb), g, nullptr, nullptr, Tb * d, s));
         }
-        RQ_HIP(ctx, realq::dot_f32(dy, g, T * d, 0.5 * alpha, parts, s));
+        RQ_HIP(ctx, realq::dot_f32(dy, g, Tb * d, 0.5 * alpha, parts, s));
         if (window && alpha < 1.0) {
-            RQ_HIP(ctx, realq::residual_out_f32(Fq.x2, Fq.mlp.out, nullptr, Fq.mlp.y, nullptr, T * d, s));
-            if ((rc = dec_forward(ctx, wn, nullptr, Fq.mlp.y, D, Fn))) return rc;
-            RQ_HIP(ctx, realq::residual_out_f32(Fn.x2, Fn.mlp.out, y2star, nullptr, dy2, T * d, s));
+            RQ_HIP(ctx, realq::residual_out_f32(q.x2, q.mlp.out, nullptr, q.mlp.y, nullptr, Tb * d, s));
+            if ((rc = dec_forward(ctx, wn, nullptr, q.mlp.y, Db, Fn))) return rc;
+            RQ_HIP(ctx, realq::residual_out_f32(Fn.x2, Fn.mlp.out, y2star + t0 * d, nullptr, dy2, Tb * d, s));
             if (N0.mlp.F) {
-                RQ_HIP(ctx, realq::scale_split(dy2, 1.f, nullptr, sdy2.hi, sdy2.lo, T * d, s));
-                if ((rc = prod3(ctx, sdy2, T, d, wn.mlp.F, d, (float)(1.0 / (double)T), g2))) return rc;
+                RQ_HIP(ctx, realq::scale_split(dy2, 1.f, nullptr, sdy2.hi, sdy2.lo, Tb * d, s));
+                if ((rc = prod3(ctx, sdy2, Tb, d, wn.mlp.F, d, (float)(1.0 / (double)Tb), g2))) return rc;
             } else {
-                RQ_HIP(ctx, realq::scale_split(dy2, (float)(1.0 / (double)T), g2, nullptr, nullptr, T * d, s));
+                RQ_HIP(ctx, realq::scale_split(dy2, (float)(1.0 / (double)Tb), g2, nullptr, nullptr, Tb * d, s));
             }
-            RQ_HIP(ctx, realq::dot_f32(dy2, g2, T * d, 0.5 * (1.0 - alpha), parts + npart, s));
+            RQ_HIP(ctx, realq::dot_f32(dy2, g2, Tb * d, 0.5 * (1.0 - alpha), parts + npart, s));
             // the next block's input gradient: through its MLP half, attention and first norm
-            if ((rc = back_to_x2(ctx, wn, D, Fn, g2, Wn)) || (rc = back_to_qkv(ctx, wn, D, Fn, Wn))) return rc;
-            RQ_HIP(ctx, realq::scale_split(Wn.dq, 1.f, nullptr, Wn.sdq.hi, Wn.sdq.lo, T * D.Hq, s));
-            RQ_HIP(ctx, realq::scale_split(Wn.dk, 1.f, nullptr, Wn.sdk.hi, Wn.sdk.lo, T * D.Hk, s));
-            RQ_HIP(ctx, realq::scale_split(Wn.dv, 1.f, nullptr, Wn.sdv.hi, Wn.sdv.lo, T * D.Hk, s));
-            if ((rc = prod3(ctx, Wn.sdq, T, D.Hq, wn.qT, d, 1.f, Wn.dh1)) ||
-                (rc = prod3_acc(ctx, Wn.sdk, T, D.Hk, wn.kT, d, Wn.dh1)) ||
-                (rc = prod3_acc(ctx, Wn.sdv, T, D.Hk, wn.vT, d, Wn.dh1)))
+            if ((rc = back_to_x2(ctx, wn, Db, Fn, g2, Wn)) || (rc = back_to_qkv(ctx, wn, Db, Fn, Wn))) return rc;
+            RQ_HIP(ctx, realq::scale_split(Wn.dq, 1.f, nullptr, Wn.sdq.hi, Wn.sdq.lo, Tb * D.Hq, s));
+            RQ_HIP(ctx, realq::scale_split(Wn.dk, 1.f, nullptr, Wn.sdk.hi, Wn.sdk.lo, Tb * D.Hk, s));
+            RQ_HIP(ctx, realq::scale_split(Wn.dv, 1.f, nullptr, Wn.sdv.hi, Wn.sdv.lo, Tb * D.Hk, s));
+            if ((rc = prod3(ctx, Wn.sdq, Tb, D.Hq, wn.qT, d, 1.f, Wn.dh1)) ||
+                (rc = prod3_acc(ctx, Wn.sdk, Tb, D.Hk, wn.kT, d, Wn.dh1)) ||
+                (rc = prod3_acc(ctx, Wn.sdv, Tb, D.Hk, wn.vT, d, Wn.dh1)))
                 return rc;
-            RQ_HIP(ctx, realq::rmsnorm_bwd_blend(Fq.mlp.y, Wn.dx2, Wn.dh1, wn.gamma1, D.eps, alpha, T, d, g, s));
+            RQ_HIP(ctx, realq::rmsnorm_bwd_blend(q.mlp.y, Wn.dx2, Wn.dh1, wn.gamma1, D.eps, alpha, Tb, d, g, s));
             RQ_HIP(ctx, realq::reduce_partials(parts, 2 * npart, 1.0, lossd, s));
         } else {
             RQ_HIP(ctx, realq::reduce_partials(parts, npart, 1.0, lossd, s));
@@ -762,17 +812,22 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
     };
 
     Split* fwd_slot[7] = {&wq.q, &wq.k, &wq.v, &wq.o, &wq.mlp.g, &wq.mlp.u, &wq.mlp.d};
-    // forward of the quantized path from module mod's stage (its weights changed)
-    auto refresh = [&](int mod) -> int {
+    // forward of the quantized path over tokens [t0, t0 + Tb) from module mod's stage (its
+    // weights changed); the earlier stages of those tokens are current in Fq
+    auto refresh = [&](int mod, int64_t t0, int64_t Tb) -> int {
+        DecF q = rows_of(Fq, D, t0);
+        DecDims Db = D;
+        Db.T = Tb;
+        const uint16_t* xh = Dd->Xhat + t0 * d;
         if (mod <= 2) {
-            if ((rc = dec_attn(ctx, wq, Dd->Xhat, nullptr, D, Fq, 1 << mod, false))) return rc;
+            if ((rc = dec_attn(ctx, wq, xh, nullptr, Db, q, 1 << mod, false))) return rc;
         }
-        if (mod <= 3 && (rc = dec_o(ctx, wq, Dd->Xhat, nullptr, D, Fq))) return rc;
-        if (mod <= 3) return forward(ctx, wq.mlp, nullptr, Fq.x2, T, d, f, D.eps, Fq.mlp, nullptr, nullptr);
-        if (mod == 4 && (rc = lin_f32(ctx, wq.mlp.g, f, d, Fq.mlp.u, T, Fq.mlp.a))) return rc;
-        if (mod == 5 && (rc = lin_f32(ctx, wq.mlp.u, f, d, Fq.mlp.u, T, Fq.mlp.b))) return rc;
-        if (mod <= 5) RQ_HIP(ctx, realq::swiglu_fwd(Fq.mlp.a, Fq.mlp.b, Fq.mlp.z, T * f, s));
-        return lin_bf16(ctx, wq.mlp.d, d, f, Fq.mlp.z, T, Fq.mlp.out);
+        if (mod <= 3 && (rc = dec_o(ctx, wq, xh, nullptr, Db, q))) return rc;
+        if (mod <= 3) return forward(ctx, wq.mlp, nullptr, q.x2, Tb, d, f, D.eps, q.mlp, nullptr, nullptr);
+        if (mod == 4 && (rc = lin_f32(ctx, wq.mlp.g, f, d, q.mlp.u, Tb, q.mlp.a))) return rc;
+        if (mod == 5 && (rc = lin_f32(ctx, wq.mlp.u, f, d, q.mlp.u, Tb, q.mlp.b))) return rc;
+        if (mod <= 5) RQ_HIP(ctx, realq::swiglu_fwd(q.mlp.a, q.mlp.b, q.mlp.z, Tb * f, s));
+        return lin_bf16(ctx, wq.mlp.d, d, f, q.mlp.z, Tb, q.mlp.out);
     };
 
     for (int mod = 0; mod < 7; ++mod) {
@@ -810,39 +865,45 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
             const int64_t nJ = n - c1;
             for (int k = 0; k < steps; ++k) {
                 Timed tm(ctx, "block_step");
+                const TokenBatch tb = step_tokens(t_adam + 1, T, Dd->bgd.batch);
+                const int64_t Tb = tb.n;
+                const DecF q = rows_of(Fq, D, tb.t0);
+                DecDims Db = D;
+                Db.T = Tb;
                 fwd_slot[mod]->lo_zero = false;
                 RQ_HIP(ctx, realq::split3_f64(W, fwd_slot[mod]->hi, fwd_slot[mod]->lo, fwd_slot[mod]->lo2, m * n, s));
-                if ((rc = refresh(mod)) || (rc = surrogate(alpha))) return rc;
+                if ((rc = refresh(mod, tb.t0, Tb)) || (rc = surrogate(alpha, tb.t0, Tb))) return rc;
                 if (out->loss_trace)
                     RQ_HIP(ctx, hipMemcpyAsync(out->loss_trace + (off[mod] + b) * steps + k, lossd, 8,
                                                hipMemcpyDeviceToDevice, s));
-                // gradient of this module's trailing columns: (dL/d output)^T input[:, J]
+                // gradient of this module's trailing columns over the step's tokens:
+                // (dL/d output)^T input[:, J] (the transposed input keeps its stride T)
                 const float* gout = nullptr;
                 int64_t gw = 0;
                 if (mod == 6) {
                     gout = g;
                     gw = d;
                 } else if (mod >= 4) {
-                    RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, Wk.sg.hi, Wk.sg.lo, T * d, s));
-                    if ((rc = prod3(ctx, Wk.sg, T, d, wq.mlp.dT, f, 1.f, Wk.dz))) return rc;
-                    RQ_HIP(ctx, realq::swiglu_bwd(Wk.dz, Fq.mlp.a, Fq.mlp.b, mod - 4, T, f, 1, svT.hi, svT.lo, T, s));
+                    RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, Wk.sg.hi, Wk.sg.lo, Tb * d, s));
+                    if ((rc = prod3(ctx, Wk.sg, Tb, d, wq.mlp.dT, f, 1.f, Wk.dz))) return rc;
+                    RQ_HIP(ctx, realq::swiglu_bwd(Wk.dz, q.mlp.a, q.mlp.b, mod - 4, Tb, f, 1, svT.hi, svT.lo, Tb, s));
                 } else {
-                    if ((rc = back_to_x2(ctx, wq, D, Fq, g, Wk))) return rc;
+                    if ((rc = back_to_x2(ctx, wq, Db, q, g, Wk))) return rc;
                     if (mod == 3) {
                         gout = Wk.dx2;
                         gw = d;
                     } else {
-                        if ((rc = back_to_qkv(ctx, wq, D, Fq, Wk))) return rc;
+                        if ((rc = back_to_qkv(ctx, wq, Db, q, Wk))) return rc;
                         gout = mod == 0 ? Wk.dq : (mod == 1 ? Wk.dk : Wk.dv);
                         gw = mod == 0 ? D.Hq : D.Hk;
                     }
                 }
                 const Split* A = &svT;
                 if (gout) {
-                    RQ_HIP(ctx, realq::transpose_split_f32(gout, gw, sgT.hi, sgT.lo, T, T, gw, s));
+                    RQ_HIP(ctx, realq::transpose_split_f32(gout, gw, sgT.hi, sgT.lo, Tb, Tb, gw, s));
                     A = &sgT;
                 }
-                realq::GemmArgs gg{A->hi, A->lo, T, inT + c1 * T, T, m, nJ, T, 1};
+                realq::GemmArgs gg{A->hi, A->lo, Tb, inT + c1 * T + tb.t0, T, m, nJ, Tb, 1};
                 RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
                 ++t_adam;
                 realq::AdamArgs a{};
@@ -866,9 +927,9 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
         fwd_slot[mod]->lo_zero = false;
         RQ_HIP(ctx, realq::split3_f32(out->W_hat[mod], n, fwd_slot[mod]->hi, fwd_slot[mod]->lo, fwd_slot[mod]->lo2, n,
                                       m, n, s));
-        if ((rc = refresh(mod))) return rc;
+        if ((rc = refresh(mod, 0, T))) return rc;
     }
-    if ((rc = surrogate(1.0))) return rc;
+    if ((rc = surrogate(1.0, 0, T))) return rc;
     RQ_HIP(ctx, hipEventRecord(ev.b, s));
     RQ_HIP(ctx, hipMemcpyAsync(&out->loss_final, lossd, 8, hipMemcpyDeviceToHost, s));
     RQ_HIP(ctx, hipStreamSynchronize(s));

@@ -31,14 +31,14 @@ def _blk(inp):
     return B.MLPBlock(gamma=inp.gamma, Wg=inp.Wg, Wu=inp.Wu, Wd=inp.Wd, F=inp.F)
 
 
-def _run(rq, ctx, inp, steps, lr, nxt=None, window=False):
+def _run(rq, ctx, inp, steps, lr, nxt=None, window=False, batch=0):
     torch = _torch()
     nx = None
     if nxt is not None:
         nx = (_dev(nxt.gamma), _dev(nxt.Wg), _dev(nxt.Wu), _dev(nxt.Wd), None if nxt.F is None else _dev(nxt.F))
     res = rq.mlp_block_sweep(ctx, _dev(inp.X, True), _dev(inp.Xhat, True), _dev(inp.gamma), _dev(inp.Wg),
                              _dev(inp.Wu), _dev(inp.Wd), None if inp.F is None else _dev(inp.F), nx,
-                             window=window, qp=rq.qparams(), bgd=rq.bgd_params(steps=steps, lr=lr))
+                             window=window, qp=rq.qparams(), bgd=rq.bgd_params(steps=steps, lr=lr, batch=batch))
     torch.cuda.synchronize()
     return res
 
@@ -129,10 +129,27 @@ def test_block_sweep_sliding_window(rq, ctx):
     assert np.isnan(tr[steps * 1]) and np.isnan(tr[steps * 3])     # last blocks of gate and up
 
 
+def test_block_sweep_minibatch_with_window(rq, ctx):
+    inp = synth.make_mlp_block(1024, 256, 384, seed=7)
+    nx = synth.make_mlp_block(8, 256, 384, seed=8)
+    batch, steps, lr = 384, 3, 1e-5                 # batches of 384, 384 and a ragged 256
+    _banner(f"mlp block mini-batch Block-GD, batch {batch}, with the next block over b_global")
+    g = _run(rq, ctx, inp, steps, lr, nxt=nx, window=True, batch=batch)
+    o = B.mlp_block_sweep(inp.X, inp.Xhat, _blk(inp), steps=steps, lr=lr, nxt=_blk(nx), window=True,
+                          batch=batch)
+    _check(g, o, True)
+    # the gate's first column block takes one step on each batch; steps of lr 1e-5 keep the
+    # two sides together, so each batch's own loss is compared
+    tr = g.loss_trace.cpu().numpy()
+    ref = [v for (_, _, v) in o.modules["gate"].loss_trace]
+    np.testing.assert_allclose(tr[:steps], ref[:steps], rtol=1e-4)
+    assert len({round(v, 6) for v in ref[:steps]}) == steps
+
+
 def test_block_sweep_rejects_bad_arguments(rq, ctx):
     torch = _torch()
     inp = synth.make_mlp_block(64, 128, 256, seed=5)
-    for bgd in (rq.bgd_params(steps=1, batch=16), rq.bgd_params(steps=1, loss_clip=0.9),
+    for bgd in (rq.bgd_params(steps=1, loss_clip=0.9),
                 rq.bgd_params(steps=1, form=rq.BGD_GRAM)):
         with pytest.raises(rq.RealqError) as ei:
             rq.mlp_block_sweep(ctx, _dev(inp.X, True), _dev(inp.Xhat, True), _dev(inp.gamma), _dev(inp.Wg),

@@ -49,12 +49,12 @@ def _dev_blk(inp):
     return {k: (None if v is None else _dev(v)) for k, v in inp.w.items()}
 
 
-def _run(rq, ctx, inp, steps, lr, nxt=None, window=False):
+def _run(rq, ctx, inp, steps, lr, nxt=None, window=False, batch=0):
     torch = _torch()
     res = rq.decoder_block_sweep(ctx, _dev(inp.X, True), _dev(inp.Xhat, True), _dev_blk(inp),
                                  None if nxt is None else _dev_blk(nxt), n_heads=inp.n_heads, n_kv=inp.n_kv,
                                  head_dim=inp.head_dim, seq_len=inp.seq_len, window=window, qp=rq.qparams(),
-                                 bgd=rq.bgd_params(steps=steps, lr=lr))
+                                 bgd=rq.bgd_params(steps=steps, lr=lr, batch=batch))
     torch.cuda.synchronize()
     return res
 
@@ -214,11 +214,29 @@ def test_decoder_sweep_rejects_bad_arguments(rq, ctx):
         with pytest.raises(rq.RealqError) as ei:
             rq.decoder_block_sweep(ctx, X, Xh, blk, **args)
         assert ei.value.code == -2, kw
-    for bgd in (rq.bgd_params(steps=1, batch=16), rq.bgd_params(steps=1, form=rq.BGD_GRAM)):
+    for bgd in (rq.bgd_params(steps=1, loss_clip=0.9), rq.bgd_params(steps=1, form=rq.BGD_GRAM)):
         with pytest.raises(rq.RealqError) as ei:
             rq.decoder_block_sweep(ctx, X, Xh, blk, **base, bgd=bgd)
         assert ei.value.code == -1
+    # a mini-batch must hold whole sequences
+    with pytest.raises(rq.RealqError) as ei:
+        rq.decoder_block_sweep(ctx, X, Xh, blk, **base, bgd=rq.bgd_params(steps=1, batch=96))
+    assert ei.value.code == -2
     torch.cuda.synchronize()
+
+
+def test_decoder_sweep_minibatch(rq, ctx):
+    inp = _inputs(6)
+    batch, steps, lr = 384, 3, 1e-5                 # six sequences, six, and a ragged four
+    _banner(f"decoder block mini-batch Block-GD, batch {batch}")
+    g = _run(rq, ctx, inp, steps, lr, batch=batch)
+    o = B.decoder_block_sweep(inp.X, inp.Xhat, _oracle_blk(inp), steps=steps, lr=lr, batch=batch)
+    tr = g.loss_trace.cpu().numpy()
+    ref = [v for (_, _, v) in o.modules["q"].loss_trace]
+    print("trace", tr[:steps], ref[:steps], flush=True)
+    _check(g, o, True)
+    # q's first column block takes one step on each batch
+    np.testing.assert_allclose(tr[:steps], ref[:steps], rtol=1e-4)
 
 
 def test_decoder_forward_llama8b_shape_one_sequence(rq, ctx):
