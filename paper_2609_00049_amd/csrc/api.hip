@@ -135,11 +135,13 @@ int realq_ctx_create(realq_ctx** out, void* hip_stream) {
     realq_ctx* c = new (std::nothrow) realq_ctx();
     if (!c) return REALQ_ERR_OOM;
     c->stream = (hipStream_t)hip_stream;
-    if (hipGetDevice(&c->device) != hipSuccess) {
+    if (hipGetDevice(&c->device) != hipSuccess ||
+        hipDeviceGetAttribute(&c->cus, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess) {
         (void)hipGetLastError();
         delete c;
         return REALQ_ERR_HIP;
     }
+    if (c->cus < 1) c->cus = 1;
     *out = c;
     return REALQ_OK;
 }
@@ -735,14 +737,28 @@ int realq_bgd_lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_
 
 // ============================================================================ a7-a9: one BGD step
 
-// Split-K factor of the gradient GEMM: enough blocks for two rounds over the 256 CUs.
-static int64_t choose_splits(int64_t M, int64_t N, int64_t K) {
+// Split-K factor of the gradient GEMM.  One 256x256 block fills a CU and every block of a
+// launch does the same work, so a launch takes ceil(blocks * S / cus) rounds and a partly
+// filled last round idles the rest of the chip (896 tiles on 256 CUs: half a round idle).
+// S is the smallest factor up to 16 whose rounds are at least 97% full, else the fullest one;
+// every split keeps at least 256 tokens.
+static int64_t choose_splits(int64_t M, int64_t N, int64_t K, int cus) {
     const int64_t blocks = realq::gemm_grad_blocks(M, N);
-    int64_t s = (512 + blocks - 1) / blocks;
-    int64_t kmax = K / 256;  // keep at least 256 tokens per split
-    if (s > kmax) s = kmax;
-    if (s > 64) s = 64;
-    return s < 1 ? 1 : s;
+    int64_t smax = std::min<int64_t>(16, K / 256);
+    if (smax < 1) smax = 1;
+    int64_t best = 1;
+    double best_fill = -1.0;
+    for (int64_t q = 1; q <= smax; ++q) {
+        const int64_t bq = blocks * q;
+        const int64_t rounds = (bq + cus - 1) / cus;
+        const double fill = (double)bq / (double)(rounds * cus);
+        if (fill >= 0.97) return q;
+        if (fill > best_fill + 1e-9) {
+            best_fill = fill;
+            best = q;
+        }
+    }
+    return best;
 }
 
 int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, float alpha, double* loss_out) {
@@ -777,7 +793,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         }
         RQ_HIP(ctx, realq::gram_grad(st->C0, st->Pm, n, c1, m, nJ, (float*)Gacc, s));
     } else {
-        const int64_t S = choose_splits(m, nJ, Tc);
+        const int64_t S = choose_splits(m, nJ, Tc, ctx->cus);
         const int64_t Seff = realq::gemm_effective_splits(Tc, S);
         void* parts;
         if ((rc = get_ws(ctx, "b_Gp", (size_t)Seff * m * nJ * 4, &Gp))) return rc;

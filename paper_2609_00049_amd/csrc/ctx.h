@@ -10,6 +10,7 @@
 struct realq_ctx {
     hipStream_t stream = nullptr;
     int device = 0;
+    int cus = 256;  // compute units of the device (blocks of the 256x256 GEMM tile resident at once)
     std::string err;
     // grow-only workspaces, by slot name
     struct Buf {
