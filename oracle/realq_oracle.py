@@ -274,7 +274,7 @@ def surrogate_grad(R, s, Ma, Xhat_J, T):
     return G / T
 
 
-def gram_surrogate(W0, X, Xhat, s=None):
+def gram_surrogate(W0, X, Xhat, s=None, trace_loss=True):
     """The module-output surrogate of Eq. fisher_loss (per-token weights s, identity metric) and its
     gradient, written through the calibration Gram matrices Hs = Xhat^T S Xhat / T and
     Ks = X^T S Xhat / T instead of the [m, T] residual R = W Xhat^T - W0 X^T:
@@ -286,7 +286,9 @@ def gram_surrogate(W0, X, Xhat, s=None):
     Equal to surrogate_grad / surrogate_loss of the token form in exact arithmetic.  It lets the
     oracle follow a sweep over hundreds of thousands of tokens on a few rows W0 [k, n]: the Gram
     matrices are formed once, every Block-GD step then costs k n |J|.  Returns (grad_fn, loss_fn)
-    for quantize_layer (identity metric, no sliding-window partner)."""
+    for quantize_layer (identity metric, no sliding-window partner).  With trace_loss False the
+    per-step loss in the trace is NaN (only the final loss is evaluated), which saves one pass over
+    Hs and Ks per step when only the final weights are checked."""
     W0 = np.asarray(W0, dtype=np.float64)
     X = np.asarray(X, dtype=np.float64)
     Xhat = np.asarray(Xhat, dtype=np.float64)
@@ -307,7 +309,7 @@ def gram_surrogate(W0, X, Xhat, s=None):
             raise ValueError("gram_surrogate has no sliding-window partner")
         if range(T)[tokens] != range(T):
             raise ValueError("gram_surrogate is formed over all tokens: no mini-batch")
-        return loss_fn(W), (W @ Hs[:, J] - W0 @ Ks[:, J])
+        return (loss_fn(W) if trace_loss else float("nan")), (W @ Hs[:, J] - W0 @ Ks[:, J])
 
     return grad_fn, loss_fn
 
