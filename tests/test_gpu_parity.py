@@ -407,9 +407,10 @@ def test_layer_llama_gate_full_size_sampled_rows(rq, ctx):
     ("qwen3_32b_layer", "gate", 0),          # 25600 x 5120, Student-t nu = 3 activations
     pytest.param("llama3.1_70b_layer", "gate", 2048,   # 28672 x 8192, calibration tokens streamed in chunks
                  marks=pytest.mark.xfail(strict=False, reason=(
-                     "codes agree in 99.0% of 32 sampled rows (bar 99.9%); the trailing D = W - W0 of the "
-                     "residual GEMM is carried as a bf16 hi/lo pair whose rounding is large next to the "
-                     "residual it cancels into at this width"))),
+                     "codes agree in 99.0% of 32 sampled rows (bar 99.9%) at lr 3e-6 with 8 steps per "
+                     "block (100% without Block-GD, 100% at lr 1e-5): many small Adam steps leave weights "
+                     "near a zero gradient, where float rounding flips the step; the source on the GPU "
+                     "side is not yet isolated"))),
 ])
 def test_layer_large_module_shape_sampled_rows(rq, ctx, cfg, module, chunk):
     """The largest projections of the Qwen3-32B- and LLaMA-3.1-70B-shaped layers at their full
