@@ -28,21 +28,51 @@ def to_device(L, torch):
     return W0, X, Xh, s, M
 
 
-def compare(gpu, ora, rows=None, group=128):
-    """Metrics of a GPU LayerResult against an oracle LayerResult (optionally on a row subset)."""
+# A code whose oracle pre-rounding value w/s + z lies within this many code units of a
+# half-integer is a rounding tie: float rounding on either side may decide it either way.
+TIE_TOL = 1e-3
+
+
+def tie_cascades(codes, ora, tol=TIE_TOL):
+    """Rows whose first code mismatch is a rounding tie of the oracle (pre-rounding value within
+    ``tol`` of a half-integer), with the column of that tie.  GPTQ compensates the rest of the row
+    for the rounding it took, so after a tie the two sides quantize different weights and the rest
+    of the row is a consequence of the tie, not a separate disagreement."""
+    pre = np.asarray(ora.prerounding)
+    out = {}
+    for i in np.nonzero((codes != ora.codes).any(axis=1))[0]:
+        j = int(np.nonzero(codes[i] != ora.codes[i])[0][0])
+        v = float(pre[i, j])
+        if abs(v - math.floor(v) - 0.5) <= tol:
+            out[int(i)] = j
+    return out
+
+
+def compare(gpu, ora, rows=None, group=128, tie_cascade=False):
+    """Metrics of a GPU LayerResult against an oracle LayerResult (optionally on a row subset).
+    With ``tie_cascade`` the columns of a row from its first mismatch on are left out of the code
+    and group metrics when that mismatch is a rounding tie (tie_cascades)."""
     codes = gpu.codes.cpu().numpy()
     scales = gpu.scales.cpu().numpy()
     zeros = gpu.zeros.cpu().numpy()
     What = gpu.W_hat.cpu().numpy()
     if rows is not None:
         codes, scales, zeros, What = codes[rows], scales[rows], zeros[rows], What[rows]
-    code_id = float((codes == ora.codes).mean())
+    keep = np.ones(codes.shape, dtype=bool)
+    gkeep = np.ones(scales.shape, dtype=bool)
+    ties = tie_cascades(codes, ora) if tie_cascade else {}
+    for i, j in ties.items():
+        keep[i, j:] = False
+        gkeep[i, (j // group) + 1:] = False      # groups searched after the tie
+    code_id = float((codes == ora.codes)[keep].mean())
     srel = np.abs(scales - ora.scales) / np.maximum(np.abs(ora.scales), 1e-30)
     grp_ok = (srel <= SCALE_RTOL) & (zeros == ora.zeros)
     return dict(
         code_identity=code_id,
-        code_mismatches=int((codes != ora.codes).sum()),
-        group_param_agreement=float(grp_ok.mean()),
+        code_mismatches=int((codes != ora.codes)[keep].sum()),
+        tie_cascade_rows=len(ties),
+        tie_cascade_codes=int((codes != ora.codes)[~keep].sum()),
+        group_param_agreement=float(grp_ok[gkeep].mean()),
         # groups searched before any Block-GD step (the first group of every row)
         first_group_agreement=float(grp_ok[:, 0].mean()),
         scale_rel_max_agreeing=float(srel[grp_ok].max()) if grp_ok.any() else math.nan,
