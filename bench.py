@@ -32,7 +32,11 @@ WORKLOADS = {
     "llama3.1_8b_gate": ("llama3.1_8b_layer", "gate", 14336, 4096, 262144, 8, 1e-5),
     "qwen3_0.6b_gate": ("qwen3_0.6b_mlp", "gate", 3072, 1024, 131072, 8, 3e-4),
     "single_512": ("single_512", "linear", 512, 512, 4096, 4, 1e-3),
+    "qwen3_32b_gate": ("qwen3_32b_layer", "gate", 25600, 5120, 262144, 8, 2e-6),
+    "llama3.1_70b_gate": ("llama3.1_70b_layer", "gate", 28672, 8192, 262144, 8, 3e-6),
 }
+# residual and gradient GEMMs streamed over the tokens in chunks of this size (0: all at once)
+TOKEN_CHUNK = {"llama3.1_70b_gate": 32768}
 
 
 def f_alg(m, n, T, K, block=128, xhat_differs=True):
@@ -394,7 +398,7 @@ def main():
     ctx = rq.Context()
     qp = rq.qparams()
     form = rq.BGD_GRAM if args.form == "gram" else rq.BGD_TOKENS
-    bgd = rq.bgd_params(steps=K, lr=lr, form=form)
+    bgd = rq.bgd_params(steps=K, lr=lr, form=form, tok_chunk=TOKEN_CHUNK.get(args.workload, 0))
     if args.only == "stage0":
         ctx.set_timing(True)
         print(json.dumps({"stage0": stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n,
@@ -447,7 +451,8 @@ def main():
         "dtype": "bf16 MFMA (hi/lo split fp32 operands), fp32/fp64 accumulate",
         "data": "synthetic (device-generated, workload distributions)",
         "config": {"workload": args.workload, "m": m, "n": n, "tokens": T, "bgd_steps": K, "bits": 4,
-                   "group": 128, "block": 128, "bgd_form": args.form},
+                   "group": 128, "block": 128, "bgd_form": args.form,
+                   "token_chunk": TOKEN_CHUNK.get(args.workload, 0)},
         "tflops_alg": fa["total"] / (ms_per_step / 1e3) / 1e12,
         "frac_bf16_peak_alg": fa["total"] / (ms_per_step / 1e3) / PEAK_BF16,
         "kernel_ms_per_step": {k: v[1] / args.steps for k, v in kt.items()},
