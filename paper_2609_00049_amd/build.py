@@ -21,11 +21,11 @@ HIPCC_FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     # packed fp32 instructions are kept out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-result",
 ]
+OBJ = PKG / "_build"
 
 
 def hipcc() -> str:
@@ -36,20 +36,39 @@ def hipcc() -> str:
 
 
 def sources():
-    return sorted(str(p) for p in CSRC.glob("*.hip"))
+    """HIP sources plus the host-only C++ units (launch planning)."""
+    return sorted(str(p) for p in CSRC.glob("*.hip")) + sorted(str(p) for p in CSRC.glob("*.cpp"))
 
 
-def build(verbose: bool = False) -> Path:
-    """Compile every HIP source into librealq.so (always recompiles)."""
-    tmp = LIB.with_suffix(".so.tmp")
-    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{ROOT / 'include'}", *sources(), "-o", str(tmp)]
+def _compile(src: str, verbose: bool) -> Path:
+    obj = OBJ / (Path(src).name + ".o")
+    cmd = [hipcc(), *HIPCC_FLAGS, f"-I{ROOT / 'include'}", "-c", src, "-o", str(obj)]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass warns that it does not know the packed-fp32 feature; only errors matter
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
+        raise RuntimeError(f"hipcc failed on {src} with exit code {res.returncode}")
+    return obj
+
+
+def build(verbose: bool = False) -> Path:
+    """Compile every source into librealq.so (always recompiles; one hipcc per source, in parallel)."""
+    from concurrent.futures import ThreadPoolExecutor
+    OBJ.mkdir(exist_ok=True)
+    srcs = sources()
+    workers = max(1, min(len(srcs), os.cpu_count() or 1, 16))
+    with ThreadPoolExecutor(workers) as ex:
+        objs = list(ex.map(lambda p: _compile(p, verbose), srcs))
+    tmp = LIB.with_suffix(".so.tmp")
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *[str(o) for o in objs], "-o", str(tmp)]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"link failed with exit code {res.returncode}")
     os.replace(tmp, LIB)
     return LIB
 

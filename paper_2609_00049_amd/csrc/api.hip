@@ -13,6 +13,7 @@
 #include "common.h"
 #include "ctx.h"
 #include "kernels.h"
+#include "plan.h"
 #include "../../include/realq.h"
 
 namespace realq {
@@ -737,30 +738,6 @@ int realq_bgd_lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_
 
 // ============================================================================ a7-a9: one BGD step
 
-// Split-K factor of the gradient GEMM.  One 256x256 block fills a CU and every block of a
-// launch does the same work, so a launch takes ceil(blocks * S / cus) rounds and a partly
-// filled last round idles the rest of the chip (896 tiles on 256 CUs: half a round idle).
-// S is the smallest factor up to 16 whose rounds are at least 97% full, else the fullest one;
-// every split keeps at least 256 tokens.
-static int64_t choose_splits(int64_t M, int64_t N, int64_t K, int cus) {
-    const int64_t blocks = realq::gemm_grad_blocks(M, N);
-    int64_t smax = std::min<int64_t>(16, K / 256);
-    if (smax < 1) smax = 1;
-    int64_t best = 1;
-    double best_fill = -1.0;
-    for (int64_t q = 1; q <= smax; ++q) {
-        const int64_t bq = blocks * q;
-        const int64_t rounds = (bq + cus - 1) / cus;
-        const double fill = (double)bq / (double)(rounds * cus);
-        if (fill >= 0.97) return q;
-        if (fill > best_fill + 1e-9) {
-            best_fill = fill;
-            best = q;
-        }
-    }
-    return best;
-}
-
 int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, float alpha, double* loss_out) {
     if (!ctx || !st) return REALQ_ERR_INVALID_ARG;
     if (!W) return set_error(ctx, REALQ_ERR_INVALID_ARG, "bgd_step: NULL W");
@@ -774,14 +751,16 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         return REALQ_OK;
     }
     const bool dense = st->M || (st->P && alpha < 1.f);
-    // tokens of this step: mini-batch (t mod nbatch) of the module's Adam step t (1-based)
-    const int64_t bt0 = ((st->t) % st->nbatch) * st->Tb;
-    const int64_t Tn = std::min(st->Tb, T - bt0);
-    const int64_t nchunks = (Tn + Tc - 1) / Tc;
     const bool clip = st->prm.loss_clip > 0.f;
     int rc;
     void *Gp = nullptr, *Gacc = nullptr;
     int64_t splits_used = 1;
+    // tokens of this step: mini-batch (t mod nbatch) of the module's Adam step t (1-based), cut
+    // into chunks; the plan sizes the split-K and loss-partial workspaces for every chunk
+    const realq::plan::StepPlan pl = realq::plan::plan_step(m, nJ, T, st->Tb, Tc, st->t, ctx->cus,
+                                                            clip ? realq::clip_apply_partials() : 0);
+    const int64_t Tn = pl.Tn;
+    const int64_t nchunks = (int64_t)pl.chunks.size();
     if (st->gram) {
         // gradient (1/T) M_a (C0 + D G_hh)[:, J]; the loss needs D G_hh on every column
         const bool want_loss = loss_out && !dense;
@@ -793,25 +772,21 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         }
         RQ_HIP(ctx, realq::gram_grad(st->C0, st->Pm, n, c1, m, nJ, (float*)Gacc, s));
     } else {
-        const int64_t S = choose_splits(m, nJ, Tc, ctx->cus);
-        const int64_t Seff = realq::gemm_effective_splits(Tc, S);
         void* parts;
-        if ((rc = get_ws(ctx, "b_Gp", (size_t)Seff * m * nJ * 4, &Gp))) return rc;
+        if ((rc = get_ws(ctx, "b_Gp", (size_t)pl.gp_slices * m * nJ * 4, &Gp))) return rc;
         if (nchunks > 1 || dense)
             if ((rc = get_ws(ctx, "b_G", (size_t)m * nJ * 4, &Gacc))) return rc;
-        int64_t kblocks = realq::gemm_num_blocks(m, Tc);
-        if (clip) kblocks = std::max(kblocks, realq::clip_apply_partials());
-        if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
-        RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, s));  // shorter last chunk writes fewer
+        if ((rc = get_ws(ctx, "b_parts", (size_t)pl.parts_total * 8, &parts))) return rc;
+        double* const pbase = (double*)parts;
 
-        splits_used = Seff;
         for (int64_t ch = 0; ch < nchunks; ++ch) {
-            const int64_t t0 = bt0 + ch * Tc, cur = std::min(Tc, bt0 + Tn - t0);
+            const int64_t t0 = pl.chunks[ch].t0, cur = pl.chunks[ch].len;
+            double* const pch = pbase + pl.chunks[ch].parts_off;
             realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
             if (!clip) {
                 Timed tm(ctx, "resid");
                 RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, st->Rlo, cur,
-                                              (double*)parts + ch * kblocks, s));
+                                              pch, s));
             } else {
                 // residual kept whole, per-token thresholds over the m channels, then the
                 // clipped, weighted split for the gradient GEMM and the loss partials
@@ -820,11 +795,11 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
                 const int64_t k = std::max<int64_t>(1, (int64_t)std::ceil((double)st->prm.loss_clip * (double)m));
                 RQ_HIP(ctx, realq::clip_select(st->Rf, cur, m, cur, std::min(k, m), st->tau, s));
                 RQ_HIP(ctx, realq::clip_apply(st->Rf, cur, m, cur, st->tau, st->s ? st->s + t0 : nullptr, st->Rhi,
-                                              st->Rlo, (double*)parts + ch * kblocks, s));
+                                              st->Rlo, pch, s));
             }
             {
-                realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, S};
-                splits_used = realq::gemm_effective_splits(cur, S);
+                realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, pl.splits};
+                splits_used = realq::gemm_effective_splits(cur, pl.splits);
                 Timed tm(ctx, "grad");
                 RQ_HIP(ctx, realq::gemm_grad(g, (float*)Gp, nJ, m * nJ, s));
             }
@@ -836,7 +811,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         }
         if (loss_out) {
             if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
-            else RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)Tn, loss_out, s));
+            else RQ_HIP(ctx, realq::reduce_partials(pbase, pl.parts_total, 0.5 / (double)Tn, loss_out, s));
         }
     }
     st->t += 1;
@@ -916,21 +891,19 @@ int realq_bgd_loss(realq_ctx* ctx, realq_bgd_state* st, const double* W, double*
     }
     // R = B + (W - W0)[:, J] Xhat[:, J]^T with J the columns not yet folded into B.
     const int64_t m = st->m, T = st->T, Tc = st->Tc, n = st->n, c1 = st->locked, nJ = n - c1;
-    const int64_t nchunks = (T + Tc - 1) / Tc;
-    const int64_t kblocks = realq::gemm_num_blocks(m, Tc);
+    int64_t nparts = 0;
+    const std::vector<realq::plan::Chunk> chunks = realq::plan::plan_loss(m, T, Tc, &nparts);
     void* parts;
     int rc;
-    if ((rc = get_ws(ctx, "b_parts", (size_t)kblocks * nchunks * 8, &parts))) return rc;
-    RQ_HIP(ctx, realq::fill_f64((double*)parts, 0.0, kblocks * nchunks, ctx->stream));
+    if ((rc = get_ws(ctx, "b_parts", (size_t)nparts * 8, &parts))) return rc;
     if (nJ > 0) RQ_HIP(ctx, realq::split_diff_f64(W + c1, n, st->W0 + c1, n, st->Dhi + c1, st->Dlo + c1, n, m, nJ,
                                                   ctx->stream));
-    for (int64_t ch = 0; ch < nchunks; ++ch) {
-        const int64_t t0 = ch * Tc, cur = std::min(Tc, T - t0);
-        realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
-        RQ_HIP(ctx, realq::gemm_loss(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, (double*)parts + ch * kblocks,
+    for (const auto& c : chunks) {
+        realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + c.t0 * n + c1, n, m, c.len, nJ, 1};
+        RQ_HIP(ctx, realq::gemm_loss(g, st->B + c.t0, T, st->s ? st->s + c.t0 : nullptr, (double*)parts + c.parts_off,
                                      ctx->stream));
     }
-    RQ_HIP(ctx, realq::reduce_partials((const double*)parts, kblocks * nchunks, 0.5 / (double)T, loss_out, ctx->stream));
+    RQ_HIP(ctx, realq::reduce_partials((const double*)parts, nparts, 0.5 / (double)T, loss_out, ctx->stream));
     return REALQ_OK;
 }
 

@@ -24,6 +24,7 @@
 // gridDim.z with a fixed K range per split (deterministic).
 #include "common.h"
 #include "kernels.h"
+#include "plan.h"
 
 namespace realq {
 
@@ -712,40 +713,21 @@ struct EpiSwiGLUT {
 
 static inline bool aligned16(const void* p) { return (((uintptr_t)p) & 15u) == 0; }
 
-// The large tile is used once the problem has at least this many large tiles.
-static constexpr int64_t kLargeMinTiles = 256;
+// Tile choice and split-K arithmetic are the host-side plan's (plan.h), so that the
+// workspace sizes the entry points derive from it describe exactly these launches.
+static_assert(CfgLarge::BM == plan::kLargeBM && CfgLarge::BN == plan::kLargeBN, "large tile differs from the plan");
+static_assert(CfgSmall::BM == plan::kSmallBM && CfgSmall::BN == plan::kSmallBN, "small tile differs from the plan");
+static_assert(BK == plan::kBK, "K slice differs from the plan");
 
-template <class C>
-static int64_t tiles_of(int64_t M, int64_t N) {
-    return ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
-}
+int64_t gemm_num_blocks(int64_t M, int64_t N, int tile) { return plan::num_blocks(M, N, tile); }
 
-static bool use_large(int64_t M, int64_t N) { return tiles_of<CfgLarge>(M, N) >= kLargeMinTiles; }
-
-static bool pick_large(int64_t M, int64_t N, int tile) { return tile == 1 || (tile == 0 && use_large(M, N)); }
-
-int64_t gemm_num_blocks(int64_t M, int64_t N, int tile) {
-    return pick_large(M, N, tile) ? tiles_of<CfgLarge>(M, N) : tiles_of<CfgSmall>(M, N);
-}
-
-int64_t gemm_effective_splits(int64_t K, int64_t splits) {
-    if (splits < 1) splits = 1;
-    int64_t kps = (K + splits - 1) / splits;
-    kps = ((kps + BK - 1) / BK) * BK;
-    if (kps <= 0) kps = BK;
-    int64_t s = (K + kps - 1) / kps;
-    return s < 1 ? 1 : s;
-}
+int64_t gemm_effective_splits(int64_t K, int64_t splits) { return plan::effective_splits(K, splits); }
 
 template <class C, class Epi>
 static hipError_t launch_cfg(const GemmArgs& g, const Epi& epi, hipStream_t stream) {
     const int64_t tiles_m = (g.M + C::BM - 1) / C::BM, tiles_n = (g.N + C::BN - 1) / C::BN;
-    int64_t splits = g.splits < 1 ? 1 : g.splits;
-    int64_t kps = (g.K + splits - 1) / splits;
-    kps = ((kps + BK - 1) / BK) * BK;
-    if (kps <= 0) kps = BK;
-    splits = (g.K + kps - 1) / kps;
-    if (splits < 1) splits = 1;
+    const int64_t kps = plan::k_per_split(g.K, g.splits);
+    const int64_t splits = plan::effective_splits(g.K, g.splits);
     // The direct-to-LDS path addresses a tile's rows with 32-bit byte offsets from the tile's
     // first row; larger strides take the checked register path.
     const bool offsets32 = (int64_t)C::BM * g.lda * 2 < (int64_t(1) << 32) && (int64_t)C::BN * g.ldb * 2 < (int64_t(1) << 32);
@@ -767,7 +749,7 @@ static hipError_t launch_cfg(const GemmArgs& g, const Epi& epi, hipStream_t stre
 template <class Epi>
 static hipError_t launch(const GemmArgs& g, const Epi& epi, hipStream_t stream) {
     if (g.M <= 0 || g.N <= 0) return hipSuccess;
-    if (pick_large(g.M, g.N, g.tile)) return launch_cfg<CfgLarge>(g, epi, stream);
+    if (plan::pick_large(g.M, g.N, g.tile)) return launch_cfg<CfgLarge>(g, epi, stream);
     return launch_cfg<CfgSmall>(g, epi, stream);
 }
 
@@ -775,7 +757,7 @@ hipError_t gemm_store_f32(const GemmArgs& g, float* C, int64_t ldc, int64_t spli
                           hipStream_t st) {
     return launch(g, EpiStoreF32{C, ldc, split_stride, alpha}, st);
 }
-int64_t gemm_grad_blocks(int64_t M, int64_t N) { return tiles_of<CfgLarge>(M, N); }
+int64_t gemm_grad_blocks(int64_t M, int64_t N) { return plan::tiles(M, N, true); }
 hipError_t gemm_grad(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, hipStream_t st) {
     if (g.M <= 0 || g.N <= 0) return hipSuccess;
     EpiGrad e;

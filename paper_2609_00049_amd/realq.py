@@ -184,18 +184,29 @@ def _ptr(t: Optional[torch.Tensor]):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def _f64(t: torch.Tensor) -> torch.Tensor:
-    """The sweep's working weights are float64."""
-    if t.dtype != torch.float64:
-        raise ValueError("working weights W must be float64")
-    return t
+def _t(t: Optional[torch.Tensor], name: str, dtype, shape, optional: bool = False):
+    """Device pointer of ``t`` after checking its dtype and exact shape (the C ABI reads the
+    buffer with the layout the shape implies, so a mismatch would read past the allocation)."""
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(int(x) for x in shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return _ptr(t)
 
 
-def _bits(t: torch.Tensor) -> torch.Tensor:
-    """bf16 tensor -> same storage viewed as int16 bit patterns."""
-    if t.dtype != torch.bfloat16:
-        raise ValueError("calibration inputs must be bfloat16")
-    return t
+def _dims(t: torch.Tensor, name: str, ndim: int):
+    if not isinstance(t, torch.Tensor) or t.dim() != ndim:
+        raise ValueError(f"{name} must be a {ndim}-d tensor")
+    return tuple(t.shape)
+
+
+F32, F64, BF16, U8 = torch.float32, torch.float64, torch.bfloat16, torch.uint8
 
 
 def qparams(bits=4, group=128, block=128, grid=80, damp=0.01, sym=False) -> QParams:
@@ -258,49 +269,56 @@ def row_groups(m: int, n_groups: int):
 
 def fisher_accum(ctx: Context, G: torch.Tensor, F_acc: torch.Tensor):
     """F_acc += sum_t g_t g_t^T (float64 [m,m]); G [T,m] bf16 output gradients."""
-    T, m = G.shape
-    ctx.check(_lib.realq_fisher_accum(ctx.h, _ptr(_bits(G)), T, m, _ptr(F_acc)))
+    T, m = _dims(G, "G", 2)
+    ctx.check(_lib.realq_fisher_accum(ctx.h, _t(G, "G", BF16, (T, m)), T, m, _t(F_acc, "F_acc", F64, (m, m))))
 
 
 def fisher_finish(ctx: Context, F_acc: torch.Tensor, T_total: int, F: torch.Tensor):
     """F = float32(F_acc / T_total)."""
-    m = F_acc.shape[0]
-    ctx.check(_lib.realq_fisher_finish(ctx.h, _ptr(F_acc), m, T_total, _ptr(F)))
+    m = _dims(F_acc, "F_acc", 2)[0]
+    ctx.check(_lib.realq_fisher_finish(ctx.h, _t(F_acc, "F_acc", F64, (m, m)), m, T_total, _t(F, "F", F32, (m, m))))
 
 
 def saliency(ctx: Context, G: torch.Tensor, n_groups: int, clip_q: float = 0.0, out: Optional[torch.Tensor] = None):
     """[n_groups, T] float32 per-token squared gradient norms of each row group, clipped per group
     at the nearest-rank clip_q quantile over tokens (0 = no clip)."""
-    T, m = G.shape
+    T, m = _dims(G, "G", 2)
     if out is None:
         out = torch.empty((n_groups, T), dtype=torch.float32, device=G.device)
-    ctx.check(_lib.realq_saliency(ctx.h, _ptr(_bits(G)), T, m, n_groups, clip_q, _ptr(out)))
+    ctx.check(_lib.realq_saliency(ctx.h, _t(G, "G", BF16, (T, m)), T, m, n_groups, clip_q,
+                                  _t(out, "out", F32, (n_groups, T))))
     return out
 
 
 def hessian_accum(ctx: Context, Xhat: torch.Tensor, s: Optional[torch.Tensor], H_acc: torch.Tensor):
     """H_acc += sum_t s_t xhat_t xhat_t^T (float64 [n,n])."""
-    T, n = Xhat.shape
-    ctx.check(_lib.realq_hessian_accum(ctx.h, _ptr(_bits(Xhat)), _ptr(s), T, n, _ptr(H_acc)))
+    T, n = _dims(Xhat, "Xhat", 2)
+    ctx.check(_lib.realq_hessian_accum(ctx.h, _t(Xhat, "Xhat", BF16, (T, n)), _t(s, "s", F32, (T,), True), T, n,
+                                       _t(H_acc, "H_acc", F64, (n, n))))
 
 
 def chol_inverse(ctx: Context, H_acc: torch.Tensor, T_total: int, damp: float, U: torch.Tensor,
                  H_out: Optional[torch.Tensor] = None, dead: Optional[torch.Tensor] = None):
-    n = H_acc.shape[0]
-    ctx.check(_lib.realq_chol_inverse(ctx.h, _ptr(H_acc), n, T_total, damp, _ptr(H_out), _ptr(U), _ptr(dead)))
+    n = _dims(H_acc, "H_acc", 2)[0]
+    ctx.check(_lib.realq_chol_inverse(ctx.h, _t(H_acc, "H_acc", F64, (n, n)), n, T_total, damp,
+                                      _t(H_out, "H_out", F32, (n, n), True), _t(U, "U", F32, (n, n)),
+                                      _t(dead, "dead", U8, (n,), True)))
 
 
 class BgdState:
     def __init__(self, ctx: Context, W0, X, Xhat, s=None, M=None, P=None, params: Optional[BgdParams] = None):
         self.ctx = ctx
         self._keep = (W0, X, Xhat, s, M, P)
-        m, n = W0.shape
-        T = X.shape[0]
+        m, n = _dims(W0, "W0", 2)
+        T = _dims(X, "X", 2)[0]
         params = params or bgd_params()
         h = ctypes.c_void_p()
-        ctx.check(_lib.realq_bgd_state_create(ctx.h, ctypes.byref(h), _ptr(W0), _ptr(_bits(X)), _ptr(_bits(Xhat)),
-                                              _ptr(s), _ptr(M), _ptr(P), m, n, T, ctypes.byref(params)))
+        ctx.check(_lib.realq_bgd_state_create(
+            ctx.h, ctypes.byref(h), _t(W0, "W0", F32, (m, n)), _t(X, "X", BF16, (T, n)),
+            _t(Xhat, "Xhat", BF16, (T, n)), _t(s, "s", F32, (T,), True), _t(M, "M", F32, (m, m), True),
+            _t(P, "P", F32, (m, m), True), m, n, T, ctypes.byref(params)))
         self.h = h
+        self.m, self.n, self.T = m, n, T
 
     def close(self):
         if getattr(self, "h", None):
@@ -314,19 +332,34 @@ class BgdState:
             pass
 
 
+def _block_outputs(W, qp: QParams, U, dead, codes, scales, zeros):
+    m, n = _dims(W, "W", 2)
+    ng = -(-n // (qp.group or n))
+    return (m, n, _t(W, "W (float64 working weights)", F64, (m, n)), _t(U, "U", F32, (n, n)),
+            _t(dead, "dead", U8, (n,), True), _t(codes, "codes", U8, (m, n)), _t(scales, "scales", F32, (m, ng)),
+            _t(zeros, "zeros", U8, (m, ng)))
+
+
+def _state_h(state: Optional[BgdState], m: int, n: int):
+    if state is None:
+        return None
+    if (state.m, state.n) != (m, n):
+        raise ValueError(f"state is {state.m}x{state.n}, W is {m}x{n}")
+    return state.h
+
+
 def quantize_block(ctx: Context, W, c0: int, bs: int, U, dead, qp: QParams, codes, scales, zeros,
                    state: Optional[BgdState] = None):
-    m, n = W.shape
-    ctx.check(_lib.realq_quantize_block(ctx.h, _ptr(_f64(W)), m, n, c0, bs, _ptr(U), _ptr(dead), ctypes.byref(qp),
-                                        _ptr(codes), _ptr(scales), _ptr(zeros), state.h if state else None))
+    m, n, pW, pU, pd, pc, ps, pz = _block_outputs(W, qp, U, dead, codes, scales, zeros)
+    ctx.check(_lib.realq_quantize_block(ctx.h, pW, m, n, c0, bs, pU, pd, ctypes.byref(qp), pc, ps, pz,
+                                        _state_h(state, m, n)))
 
 
 def quantize_block_rows(ctx: Context, W, r0: int, r1: int, c0: int, bs: int, U, dead, qp: QParams, codes, scales,
                         zeros, state: Optional[BgdState] = None):
-    m, n = W.shape
-    ctx.check(_lib.realq_quantize_block_rows(ctx.h, _ptr(_f64(W)), m, n, r0, r1, c0, bs, _ptr(U), _ptr(dead),
-                                             ctypes.byref(qp), _ptr(codes), _ptr(scales), _ptr(zeros),
-                                             state.h if state else None))
+    m, n, pW, pU, pd, pc, ps, pz = _block_outputs(W, qp, U, dead, codes, scales, zeros)
+    ctx.check(_lib.realq_quantize_block_rows(ctx.h, pW, m, n, r0, r1, c0, bs, pU, pd, ctypes.byref(qp), pc, ps, pz,
+                                             _state_h(state, m, n)))
 
 
 def bgd_lock_block(ctx: Context, state: BgdState, c0: int, bs: int):
@@ -334,24 +367,29 @@ def bgd_lock_block(ctx: Context, state: BgdState, c0: int, bs: int):
 
 
 def bgd_step(ctx: Context, state: BgdState, W, c1: int, alpha: float = 1.0, loss_out=None):
-    ctx.check(_lib.realq_bgd_step(ctx.h, state.h, _ptr(_f64(W)), c1, alpha, _ptr(loss_out)))
+    pW = _t(W, "W (float64 working weights)", F64, (state.m, state.n))
+    ctx.check(_lib.realq_bgd_step(ctx.h, state.h, pW, c1, alpha, _t(loss_out, "loss_out", F64, (1,), True)))
 
 
 def bgd_loss(ctx: Context, state: BgdState, W, loss_out):
-    ctx.check(_lib.realq_bgd_loss(ctx.h, state.h, _ptr(_f64(W)), _ptr(loss_out)))
+    pW = _t(W, "W (float64 working weights)", F64, (state.m, state.n))
+    ctx.check(_lib.realq_bgd_loss(ctx.h, state.h, pW, _t(loss_out, "loss_out", F64, (1,))))
 
 
 def pullback_metric(ctx: Context, W_next, P, M_next=None, accumulate=False):
     """P (+)= W_next^T M_next W_next."""
-    m_next, m = W_next.shape
-    ctx.check(_lib.realq_pullback_metric(ctx.h, _ptr(W_next), _ptr(M_next), m_next, m, int(accumulate), _ptr(P)))
+    m_next, m = _dims(W_next, "W_next", 2)
+    ctx.check(_lib.realq_pullback_metric(ctx.h, _t(W_next, "W_next", F32, (m_next, m)),
+                                         _t(M_next, "M_next", F32, (m_next, m_next), True), m_next, m,
+                                         int(accumulate), _t(P, "P", F32, (m, m))))
 
 
 def handoff(ctx: Context, Wa, X, Y, Wb=None):
     """Y = bf16(X Wa^T), or bf16(silu(X Wa^T) * (X Wb^T)) when Wb is given."""
-    T, n = X.shape
-    m = Wa.shape[0]
-    ctx.check(_lib.realq_handoff(ctx.h, _ptr(Wa), _ptr(Wb), _ptr(_bits(X)), T, n, m, _ptr(Y)))
+    T, n = _dims(X, "X", 2)
+    m = _dims(Wa, "Wa", 2)[0]
+    ctx.check(_lib.realq_handoff(ctx.h, _t(Wa, "Wa", F32, (m, n)), _t(Wb, "Wb", F32, (m, n), True),
+                                 _t(X, "X", BF16, (T, n)), T, n, m, _t(Y, "Y", BF16, (T, m))))
 
 
 @dataclass
@@ -375,10 +413,10 @@ def quantize_layer(ctx: Context, W0, X, Xhat, s=None, M=None, P=None, *, qp: Opt
     [N_g, T] float32: one Hessian per row group (H, U and dead then carry a leading N_g axis)."""
     qp = qp or qparams()
     bgd = bgd or bgd_params()
-    m, n = W0.shape
-    T = X.shape[0]
+    m, n = _dims(W0, "W0", 2)
+    T = _dims(X, "X", 2)[0]
     dev = W0.device
-    n_groups = 0 if s_groups is None else s_groups.shape[0]
+    n_groups = 0 if s_groups is None else _dims(s_groups, "s_groups", 2)[0]
     lead = () if s_groups is None else (n_groups,)
     if out is None:
         ng = -(-n // (qp.group or n))
@@ -395,10 +433,16 @@ def quantize_layer(ctx: Context, W0, X, Xhat, s=None, M=None, P=None, *, qp: Opt
             if want_trace else None,
             loss_final=math.nan, ms_total=math.nan)
     woff, wtot = (0, 0) if window is None else window
-    desc = LayerDesc(m, n, T, _ptr(W0), _ptr(_bits(X)), _ptr(_bits(Xhat)), _ptr(s), _ptr(M), _ptr(P),
-                     woff, wtot, qp, bgd, _ptr(s_groups), n_groups)
-    lo = LayerOut(_ptr(out.codes), _ptr(out.scales), _ptr(out.zeros), _ptr(out.W_hat), _ptr(out.H), _ptr(out.U),
-                  _ptr(out.dead), _ptr(out.loss_trace), math.nan, math.nan)
+    ng = -(-n // (qp.group or n))
+    nb = -(-n // qp.block)
+    desc = LayerDesc(m, n, T, _t(W0, "W0", F32, (m, n)), _t(X, "X", BF16, (T, n)), _t(Xhat, "Xhat", BF16, (T, n)),
+                     _t(s, "s", F32, (T,), True), _t(M, "M", F32, (m, m), True), _t(P, "P", F32, (m, m), True),
+                     woff, wtot, qp, bgd, _t(s_groups, "s_groups", F32, (n_groups, T), True), n_groups)
+    lo = LayerOut(_t(out.codes, "codes", U8, (m, n)), _t(out.scales, "scales", F32, (m, ng)),
+                  _t(out.zeros, "zeros", U8, (m, ng)), _t(out.W_hat, "W_hat", F32, (m, n)),
+                  _t(out.H, "H", F32, lead + (n, n), True), _t(out.U, "U", F32, lead + (n, n), True),
+                  _t(out.dead, "dead", U8, lead + (n,), True),
+                  _t(out.loss_trace, "loss_trace", F64, (max(1, nb * bgd.steps),), True), math.nan, math.nan)
     ctx.check(_lib.realq_quantize_layer(ctx.h, ctypes.byref(desc), ctypes.byref(lo)))
     out.loss_final = lo.loss_final
     out.ms_total = lo.ms_total
@@ -418,8 +462,14 @@ class BlockResult:
     ms_total: float
 
 
-def _mlp_block(gamma, Wg, Wu, Wd, F=None) -> MLPBlock:
-    return MLPBlock(_ptr(gamma), _ptr(Wg), _ptr(Wu), _ptr(Wd), _ptr(F))
+def _mlp_block(gamma, Wg, Wu, Wd, F=None, *, d=None, f=None) -> MLPBlock:
+    """MLP block weights after shape checks: gamma [d], Wg and Wu [f, d], Wd [d, f], F [d, d] or None."""
+    if d is None:
+        d = _dims(gamma, "gamma", 1)[0]
+    if f is None:
+        f = _dims(Wg, "Wg", 2)[0]
+    return MLPBlock(_t(gamma, "gamma", F32, (d,)), _t(Wg, "Wg", F32, (f, d)), _t(Wu, "Wu", F32, (f, d)),
+                    _t(Wd, "Wd", F32, (d, f)), _t(F, "F", F32, (d, d), True))
 
 
 def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, *, eps=1e-6, window=False,
@@ -429,8 +479,8 @@ def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, 
     nxt = (gamma, Wg, Wu, Wd, F) of the next block or None."""
     qp = qp or qparams()
     bgd = bgd or bgd_params()
-    T, d = X.shape
-    f = Wg.shape[0]
+    T, d = _dims(X, "X", 2)
+    f = _dims(Wg, "Wg", 2)[0]
     dev = X.device
     nb = [-(-d // qp.block), -(-d // qp.block), -(-f // qp.block)]
     mods = {}
@@ -442,9 +492,9 @@ def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, 
                                  W_hat=torch.empty((rows, cols), dtype=torch.float32, device=dev),
                                  H=None, U=None, dead=None, loss_trace=None, loss_final=math.nan, ms_total=math.nan)
     trace = torch.empty((max(1, sum(nb) * bgd.steps),), dtype=torch.float64, device=dev) if want_trace else None
-    nx = _mlp_block(*nxt) if nxt is not None else MLPBlock()
-    desc = MLPDesc(T, d, f, _ptr(_bits(X)), _ptr(_bits(Xhat)), _mlp_block(gamma, Wg, Wu, Wd, F), nx, eps,
-                   int(bool(window)), qp, bgd)
+    nx = _mlp_block(*nxt, d=d) if nxt is not None else MLPBlock()
+    desc = MLPDesc(T, d, f, _t(X, "X", BF16, (T, d)), _t(Xhat, "Xhat", BF16, (T, d)),
+                   _mlp_block(gamma, Wg, Wu, Wd, F, d=d, f=f), nx, eps, int(bool(window)), qp, bgd)
     o = MLPOut()
     for k, name in enumerate(MLP_MODULES):
         o.codes[k] = _ptr(mods[name].codes)
@@ -459,9 +509,12 @@ def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, 
 DECODER_MODULES = ("q", "k", "v", "o", "gate", "up", "down")
 
 
-def _decoder_block(w: dict) -> DecoderBlock:
-    return DecoderBlock(_ptr(w["gamma1"]), _ptr(w["Wq"]), _ptr(w["Wk"]), _ptr(w["Wv"]), _ptr(w["Wo"]),
-                        _mlp_block(w["gamma2"], w["Wg"], w["Wu"], w["Wd"], w.get("F")))
+def _decoder_block(w: dict, d: int, Hq: int, Hk: int) -> DecoderBlock:
+    """Decoder block weights after shape checks (Hq = n_heads head_dim, Hk = n_kv head_dim)."""
+    return DecoderBlock(_t(w["gamma1"], "gamma1", F32, (d,)), _t(w["Wq"], "Wq", F32, (Hq, d)),
+                        _t(w["Wk"], "Wk", F32, (Hk, d)), _t(w["Wv"], "Wv", F32, (Hk, d)),
+                        _t(w["Wo"], "Wo", F32, (d, Hq)),
+                        _mlp_block(w["gamma2"], w["Wg"], w["Wu"], w["Wd"], w.get("F"), d=d))
 
 
 def decoder_block_sweep(ctx: Context, X, Xhat, blk: dict, nxt: Optional[dict] = None, *, n_heads, n_kv, head_dim,
@@ -474,10 +527,11 @@ def decoder_block_sweep(ctx: Context, X, Xhat, blk: dict, nxt: Optional[dict] = 
     Wd [d, f] and optionally F [d, d]; nxt is the next block (window partner) or None."""
     qp = qp or qparams()
     bgd = bgd or bgd_params()
-    T, d = X.shape
-    f = blk["Wg"].shape[0]
+    T, d = _dims(X, "X", 2)
+    f = _dims(blk["Wg"], "Wg", 2)[0]
     dev = X.device
-    shapes = [tuple(blk[k].shape) for k in ("Wq", "Wk", "Wv", "Wo", "Wg", "Wu", "Wd")]
+    Hq, Hk = n_heads * head_dim, n_kv * head_dim
+    shapes = [(Hq, d), (Hk, d), (Hk, d), (d, Hq), (f, d), (f, d), (d, f)]
     nb = [-(-cols // qp.block) for (_, cols) in shapes]
     mods = {}
     for name, (rows, cols) in zip(DECODER_MODULES, shapes):
@@ -488,9 +542,9 @@ def decoder_block_sweep(ctx: Context, X, Xhat, blk: dict, nxt: Optional[dict] = 
                                  W_hat=torch.empty((rows, cols), dtype=torch.float32, device=dev),
                                  H=None, U=None, dead=None, loss_trace=None, loss_final=math.nan, ms_total=math.nan)
     trace = torch.empty((max(1, sum(nb) * bgd.steps),), dtype=torch.float64, device=dev) if want_trace else None
-    nx = _decoder_block(nxt) if nxt is not None else DecoderBlock()
-    desc = DecoderDesc(T, d, f, seq_len, n_heads, n_kv, head_dim, rope_base, eps, _ptr(_bits(X)), _ptr(_bits(Xhat)),
-                       _decoder_block(blk), nx, int(bool(window)), qp, bgd)
+    nx = _decoder_block(nxt, d, Hq, Hk) if nxt is not None else DecoderBlock()
+    desc = DecoderDesc(T, d, f, seq_len, n_heads, n_kv, head_dim, rope_base, eps, _t(X, "X", BF16, (T, d)),
+                       _t(Xhat, "Xhat", BF16, (T, d)), _decoder_block(blk, d, Hq, Hk), nx, int(bool(window)), qp, bgd)
     o = DecoderOut()
     for k, name in enumerate(DECODER_MODULES):
         o.codes[k] = _ptr(mods[name].codes)
@@ -506,8 +560,8 @@ def decoder_forward(ctx: Context, X, blk: dict, *, n_heads, n_kv, head_dim, seq_
                     intermediates=False) -> dict:
     """One forward of the decoder block (weights as for decoder_block_sweep) on X [T, d] (bf16):
     {'y': [T, d] float32} and, with intermediates=True, h1, q, k, v, O (bf16) and x2 (float32)."""
-    T, d = X.shape
-    f = blk["Wg"].shape[0]
+    T, d = _dims(X, "X", 2)
+    f = _dims(blk["Wg"], "Wg", 2)[0]
     dev = X.device
     Hq, Hk = n_heads * head_dim, n_kv * head_dim
     res = {"y": torch.empty((T, d), dtype=torch.float32, device=dev)}
@@ -515,8 +569,8 @@ def decoder_forward(ctx: Context, X, blk: dict, *, n_heads, n_kv, head_dim, seq_
         for name, w in (("h1", d), ("q", Hq), ("k", Hk), ("v", Hk), ("O", Hq)):
             res[name] = torch.empty((T, w), dtype=torch.bfloat16, device=dev)
         res["x2"] = torch.empty((T, d), dtype=torch.float32, device=dev)
-    desc = DecoderDesc(T, d, f, seq_len, n_heads, n_kv, head_dim, rope_base, eps, _ptr(_bits(X)), None,
-                       _decoder_block(blk), DecoderBlock(), 0, qparams(), bgd_params())
+    desc = DecoderDesc(T, d, f, seq_len, n_heads, n_kv, head_dim, rope_base, eps, _t(X, "X", BF16, (T, d)), None,
+                       _decoder_block(blk, d, Hq, Hk), DecoderBlock(), 0, qparams(), bgd_params())
     o = DecoderFwdOut(*[_ptr(res.get(k)) for k in ("h1", "q", "k", "v", "O", "x2", "y")])
     ctx.check(_lib.realq_decoder_forward(ctx.h, ctypes.byref(desc), ctypes.byref(o)))
     return res

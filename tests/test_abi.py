@@ -101,3 +101,43 @@ def test_plain_c_caller_compiles_and_links(tmp_path):
     from tests.c_caller import compile_c_caller
     r = compile_c_caller(tmp_path / "realq_layer_c")
     assert r.returncode == 0, r.stderr
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_binding_rejects_wrong_dtypes_and_shapes_before_the_call():
+    """The binding checks the dtype and exact shape of every tensor it hands to the C ABI (which
+    reads each buffer with the layout the sizes imply) and raises ValueError before any call; the
+    checks come before the device check, so they run here on host tensors."""
+    import torch
+    from paper_2609_00049_amd import realq as rq
+
+    class NoCall:           # stands in for a Context: any call into the library fails the test
+        h = None
+
+        def check(self, rc):
+            raise AssertionError("the C ABI was called")
+
+    ctx = NoCall()
+    m, n, T = 8, 16, 32
+    W0 = torch.zeros((m, n), dtype=torch.float32)
+    X = torch.zeros((T, n), dtype=torch.bfloat16)
+    cases = [
+        dict(W0=W0.to(torch.bfloat16), X=X, Xhat=X),                         # bf16 weights
+        dict(W0=W0, X=X.float(), Xhat=X),                                     # float32 activations
+        dict(W0=W0, X=X, Xhat=X[:, :8].contiguous()),                         # Xhat narrower than X
+        dict(W0=W0, X=X, Xhat=X, s=torch.ones(T - 1)),                        # short s
+        dict(W0=W0, X=X, Xhat=X, M=torch.eye(m + 1)),                         # wrong metric size
+        dict(W0=W0, X=X, Xhat=X, P=torch.eye(m, dtype=torch.float64)),        # float64 partner metric
+    ]
+    for kw in cases:
+        with pytest.raises(ValueError):
+            rq.quantize_layer(ctx, **kw)
+    with pytest.raises(ValueError):
+        rq.hessian_accum(ctx, X, None, torch.zeros((n, n), dtype=torch.float32))
+    with pytest.raises(ValueError):
+        rq.chol_inverse(ctx, torch.zeros((n, n), dtype=torch.float64), T, 0.01, torch.zeros((n, n + 1)))
+    with pytest.raises(ValueError):
+        rq.handoff(ctx, W0, X, torch.zeros((T, m), dtype=torch.float32))
+    with pytest.raises(ValueError):
+        rq.mlp_block_sweep(ctx, X, X, torch.ones(n), torch.zeros((24, n)), torch.zeros((24, n)),
+                           torch.zeros((24, n)))                             # Wd must be [d, f]
