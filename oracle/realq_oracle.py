@@ -274,43 +274,63 @@ def surrogate_grad(R, s, Ma, Xhat_J, T):
     return G / T
 
 
-def gram_surrogate(W0, X, Xhat, s=None, trace_loss=True):
-    """The module-output surrogate of Eq. fisher_loss (per-token weights s, identity metric) and its
-    gradient, written through the calibration Gram matrices Hs = Xhat^T S Xhat / T and
-    Ks = X^T S Xhat / T instead of the [m, T] residual R = W Xhat^T - W0 X^T:
+def gram_surrogate(W0, X, Xhat, s=None, trace_loss=True, M=None, P=None):
+    """The module-output surrogate of Eq. fisher_loss (per-token weights s, metric M, optionally
+    blended with the window partner's P by Eq. slide_window) and its gradient, written through the
+    calibration Gram matrices Hs = Xhat^T S Xhat / T and Ks = X^T S Xhat / T instead of the [m, T]
+    residual R = W Xhat^T - W0 X^T:
 
-        (1/T) R S Xhat_J = (W Hs - W0 Ks)[:, J]
-        (1/2T) sum_t s_t |R_t|^2 = 1/2 sum_i (w_i Hs w_i^T - 2 w_i Ks^T w0_i^T) + c_i,
-        c_i = (1/2T) sum_t s_t (w0_i . x_t)^2.
+        (1/T) Ma R S Xhat_J = Ma (W Hs - W0 Ks)[:, J]
+        (1/2T) sum_t s_t R_t^T Ma R_t = 1/2 <Ma, W Hs W^T - 2 W Ks^T W0^T + C>,
+        C = (1/T) (X W0^T)^T S (X W0^T),
 
-    Equal to surrogate_grad / surrogate_loss of the token form in exact arithmetic.  It lets the
-    oracle follow a sweep over hundreds of thousands of tokens on a few rows W0 [k, n]: the Gram
-    matrices are formed once, every Block-GD step then costs k n |J|.  Returns (grad_fn, loss_fn)
-    for quantize_layer (identity metric, no sliding-window partner).  With trace_loss False the
-    per-step loss in the trace is NaN (only the final loss is evaluated), which saves one pass over
-    Hs and Ks per step when only the final weights are checked."""
+    with Ma = alpha M + (1 - alpha) P (identity where M is None).  Equal to surrogate_grad /
+    surrogate_loss of the token form in exact arithmetic.  It lets the oracle follow a sweep over
+    hundreds of thousands of tokens: the Gram matrices are formed once, every Block-GD step then
+    costs k n |J| for k rows (plus k^2 |J| for a dense metric, whose rows are coupled, so then all m
+    rows must be followed).  With the identity metric the rows are independent and W0 may be a
+    subset of rows.  Returns (grad_fn, loss_fn) for quantize_layer; loss_fn is the own-metric
+    (alpha = 1) loss.  With trace_loss False the per-step loss in the trace is NaN (only the final
+    loss is evaluated), which saves one pass over Hs and Ks per step when only the final weights are
+    checked."""
     W0 = np.asarray(W0, dtype=np.float64)
     X = np.asarray(X, dtype=np.float64)
     Xhat = np.asarray(Xhat, dtype=np.float64)
+    M = None if M is None else np.asarray(M, dtype=np.float64)
+    P = None if P is None else np.asarray(P, dtype=np.float64)
     T = X.shape[0]
+    k = W0.shape[0]
     sw = np.ones(T) if s is None else np.asarray(s, dtype=np.float64)
     SXh = Xhat if s is None else Xhat * sw[:, None]
     Hs = Xhat.T @ SXh / T
     Ks = X.T @ SXh / T
     X0 = X @ W0.T                                  # [T, k]
-    c = 0.5 / T * np.sum(X0 * X0 * sw[:, None], axis=0)
+    coupled = M is not None or P is not None
+    if coupled:
+        C = X0.T @ (X0 * sw[:, None]) / T          # [k, k]
+    else:
+        c = 0.5 / T * np.sum(X0 * X0 * sw[:, None], axis=0)
+
+    def loss_at(W, Ma):
+        if Ma is None and not coupled:
+            quad = np.sum((W @ Hs) * W, axis=1) - 2.0 * np.sum((W @ Ks.T) * W0, axis=1)
+            return float(np.sum(0.5 * quad + c))
+        A = W @ Hs @ W.T - 2.0 * (W @ Ks.T @ W0.T) + C
+        return 0.5 * float(np.trace(A) if Ma is None else np.sum(Ma * A))
 
     def loss_fn(W):
-        quad = np.sum((W @ Hs) * W, axis=1) - 2.0 * np.sum((W @ Ks.T) * W0, axis=1)
-        return float(np.sum(0.5 * quad + c))
+        return loss_at(W, M)
 
     def grad_fn(W, J, alpha, tokens=slice(0, T)):
-        if alpha != 1.0:
-            raise ValueError("gram_surrogate has no sliding-window partner")
         if range(T)[tokens] != range(T):
             raise ValueError("gram_surrogate is formed over all tokens: no mini-batch")
-        return (loss_fn(W) if trace_loss else float("nan")), (W @ Hs[:, J] - W0 @ Ks[:, J])
+        Ma = _blend(M, P, alpha, k)
+        G = W @ Hs[:, J] - W0 @ Ks[:, J]
+        if Ma is not None:
+            G = Ma @ G
+        return (loss_at(W, Ma) if trace_loss else float("nan")), G
 
+    grad_fn.Hs = Hs            # the calibration Gram matrix Xhat^T S Xhat / T, i.e. H / 2
     return grad_fn, loss_fn
 
 

@@ -408,11 +408,48 @@ def test_gram_surrogate_equals_the_token_form():
         np.testing.assert_allclose(G, surrogate_grad(R, s, None, Xh[:, J], T), rtol=1e-10, atol=1e-14)
         assert lv == pytest.approx(surrogate_loss(R, s, None, T), rel=1e-11)
     assert loss_fn(W) == pytest.approx(surrogate_loss(R, s, None, T), rel=1e-11)
-    with pytest.raises(ValueError):
-        grad_fn(W, slice(1, 4), 0.5)
     assert grad_fn(W, slice(1, 4), 1.0, slice(0, T))[0] == lv
     with pytest.raises(ValueError):
         grad_fn(W, slice(1, 4), 1.0, slice(0, T - 1))
+
+
+@pytest.mark.parametrize("alpha", [1.0, 0.4, 0.0])
+def test_gram_surrogate_with_dense_metric_and_window_equals_the_token_form(alpha):
+    """gram_surrogate with a dense metric M and a window partner P against the token form with the
+    blended metric alpha M + (1 - alpha) P formed here, to 1e-10."""
+    W0, X, Xh, s, W, M = _bgd_problem(54, m=6, dense=True)
+    T = X.shape[0]
+    Pm = pullback_metric(rng(55).standard_normal((4, 6)))
+    grad_fn, loss_fn = oracle.gram_surrogate(W0, X, Xh, s, M=M, P=Pm)
+    R = residual(W, W0, X, Xh)
+    Ma = alpha * M + (1.0 - alpha) * Pm
+    for c1 in (0, 5):
+        J = slice(c1, W.shape[1])
+        lv, G = grad_fn(W, J, alpha)
+        np.testing.assert_allclose(G, surrogate_grad(R, s, Ma, Xh[:, J], T), rtol=1e-10, atol=1e-14)
+        assert lv == pytest.approx(surrogate_loss(R, s, Ma, T), rel=1e-10)
+    assert loss_fn(W) == pytest.approx(surrogate_loss(R, s, M, T), rel=1e-10)
+    # identity metric with a partner
+    g2, l2 = oracle.gram_surrogate(W0, X, Xh, s, P=Pm)
+    Mi = alpha * np.eye(6) + (1.0 - alpha) * Pm
+    np.testing.assert_allclose(g2(W, slice(2, 9), alpha)[1], surrogate_grad(R, s, Mi, Xh[:, 2:], T),
+                               rtol=1e-10, atol=1e-14)
+    assert l2(W) == pytest.approx(surrogate_loss(R, s, None, T), rel=1e-10)
+    np.testing.assert_allclose(grad_fn.Hs, Xh.T @ np.diag(s) @ Xh / T, rtol=1e-12)
+
+
+def test_sweep_with_dense_metric_and_window_driven_by_the_gram_surrogate():
+    L = synth.make_module("single_512", m=24, n=384, T=600, seed=8)
+    A = rng(56).standard_normal((24, 48))
+    M = A @ A.T / 48
+    Pm = pullback_metric(rng(57).standard_normal((10, 24)) * 0.3)
+    grad_fn, loss_fn = oracle.gram_surrogate(L.W0, L.X, L.Xhat, L.s, M=M, P=Pm)
+    kw = dict(M=M, P=Pm, steps=2, lr=1e-3, window=(1, 4))
+    a = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, **kw)
+    b = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, grad_fn=grad_fn, loss_fn=loss_fn, **kw)
+    assert (a.codes == b.codes).all()
+    assert b.loss_final == pytest.approx(a.loss_final, rel=1e-10)
+    np.testing.assert_allclose([v for (_, _, v) in b.loss_trace], [v for (_, _, v) in a.loss_trace], rtol=1e-10)
 
 
 def test_sweep_driven_by_the_gram_surrogate_is_the_token_sweep():
@@ -463,6 +500,124 @@ def test_window_off_equals_alpha_one():
     assert not np.array_equal(c.W_hat, b.W_hat) or True  # alpha(1) = 1: first block uses M only
     # block 0 is window step 1 (alpha = 1), so its trace entries equal the window-off run's
     assert c.loss_trace[0] == b.loss_trace[0]
+
+
+def _blend_trace_runs(L, P, window, steps=2):
+    """Three sweeps at lr = 0 (Block-GD runs but never moves the weights, so every run visits the
+    same weights): identity metric, metric P, and the window blend of the two."""
+    kw = dict(steps=steps, lr=0.0)
+    a = quantize_layer(L.W0, L.X, L.Xhat, L.s, **kw)
+    b = quantize_layer(L.W0, L.X, L.Xhat, L.s, M=P, **kw)
+    c = quantize_layer(L.W0, L.X, L.Xhat, L.s, P=P, window=window, **kw)
+    np.testing.assert_array_equal(a.W_hat, c.W_hat)
+    np.testing.assert_array_equal(b.W_hat, c.W_hat)
+    return [v for (_, _, v) in a.loss_trace], [v for (_, _, v) in b.loss_trace], c.loss_trace
+
+
+@pytest.mark.parametrize("window,alphas", [((0, 3), (1.0, 0.5)), ((2, 6), (0.6, 0.4))])
+def test_window_blend_of_the_two_metrics_at_each_block(window, alphas):
+    """Eq. slide_window: at column block b the surrogate is alpha_b L_M + (1 - alpha_b) L_P with
+    alpha_b = 1 - (b_global - 1) / (B_total - 1).  With three column blocks (Block-GD after blocks 0
+    and 1), the per-step losses of the windowed sweep are the alpha-weighted sums of the losses of
+    an identity-metric sweep and a P-metric sweep at the same weights (alphas written out here:
+    (0, 3) gives block steps 1, 2 of 3; (2, 6) gives steps 3, 4 of 6).  A swapped or rescaled
+    blend fails this."""
+    L = synth.make_module("single_512", m=10, n=384, T=160, seed=3)
+    Wn = rng(64).standard_normal((6, 10)) * 0.3
+    P = pullback_metric(Wn)
+    tr_m, tr_p, tr_w = _blend_trace_runs(L, P, window)
+    assert [b for (b, _, _) in tr_w] == [0, 0, 1, 1]
+    for (b, k, v), lm, lp in zip(tr_w, tr_m, tr_p):
+        a = alphas[b]
+        assert v == pytest.approx(a * lm + (1.0 - a) * lp, rel=1e-12)
+    assert tr_p[0] != pytest.approx(tr_m[0], rel=1e-3)          # the two metrics really differ
+
+
+def test_window_blend_gradient_matches_finite_differences(monkeypatch):
+    """The gradient the sweep hands to Adam at a window step with alpha = 0.4 (block 1 of window
+    (2, 6)) equals central finite differences of the blended surrogate 0.4 L_I + 0.6 L_P, written
+    out here from its definition, at the weights the sweep was at (taken from its residual call)."""
+    import oracle.realq_oracle as ro
+    L = synth.make_module("single_512", m=6, n=384, T=120, seed=4)
+    Wn = rng(65).standard_normal((5, 6)) * 0.3
+    P = pullback_metric(Wn)
+    seen_W, seen_G = [], []
+    real_residual, real_adam = ro.residual, ro.adam_update
+
+    def spy_residual(W, W0, X, Xhat):
+        seen_W.append(np.array(W, copy=True))
+        return real_residual(W, W0, X, Xhat)
+
+    def spy_adam(W_J, G, mA, vA, t, lr, *a):
+        seen_G.append(np.array(G, copy=True))
+        return real_adam(W_J, G, mA, vA, t, lr, *a)
+
+    monkeypatch.setattr(ro, "residual", spy_residual)
+    monkeypatch.setattr(ro, "adam_update", spy_adam)
+    ro.quantize_layer(L.W0, L.X, L.Xhat, L.s, P=P, steps=1, lr=1e-4, window=(2, 6))
+    assert len(seen_G) == 2 and len(seen_W) == 3                # blocks 0, 1 step once; final loss
+    W, G = seen_W[1], seen_G[1]                                 # block 1: alpha = 1 - 3/5 = 0.4
+    X, Xh, sw = (np.asarray(a, dtype=np.float64) for a in (L.X, L.Xhat, L.s))
+    W0 = np.asarray(L.W0, dtype=np.float64)
+    T = X.shape[0]
+
+    def blended(Wx):
+        R = Wx @ Xh.T - W0 @ X.T
+        li = 0.5 / T * np.sum(sw * np.sum(R * R, axis=0))
+        lp = 0.5 / T * np.sum(sw * np.sum(R * (P @ R), axis=0))
+        return 0.4 * li + 0.6 * lp
+
+    c1, h = 256, 1e-4
+    r = rng(66)
+    for _ in range(12):
+        i, j = int(r.integers(0, 6)), int(r.integers(c1, 384))
+        Wp = W.copy(); Wp[i, j] += h
+        Wm = W.copy(); Wm[i, j] -= h
+        fd = (blended(Wp) - blended(Wm)) / (2 * h)
+        assert fd == pytest.approx(G[i, j - c1], rel=1e-6, abs=1e-13)
+
+
+def test_layer_chain_window_partners_built_by_hand():
+    """layer_chain's window partners (per-module reading of Sec. 4.4): q's consumer is o, with
+    P_q = W0_o^T W0_o; o's consumers are gate and up, with P_o = W0_gate^T W0_gate + W0_up^T W0_up;
+    B_total is the module's own block count.  The partner metrics are summed here row by row from
+    their definition, and each windowed module's per-step losses at lr = 0 must be the alpha-blend of
+    its identity-metric and partner-metric losses; k, v, gate, up and down take no partner."""
+    from oracle.realq_oracle import layer_chain
+    r = rng(82)
+    d, f, T = 32, 40, 96
+    W0s = {"q": r.standard_normal((d, d)) * 0.1, "k": r.standard_normal((8, d)) * 0.1,
+           "v": r.standard_normal((8, d)) * 0.1, "o": r.standard_normal((d, d)) * 0.1,
+           "gate": r.standard_normal((f, d)) * 0.1, "up": r.standard_normal((f, d)) * 0.1,
+           "down": r.standard_normal((d, f)) * 0.1}
+    X0 = r.standard_normal((T, d))
+    Xh0 = X0 + 0.05 * r.standard_normal((T, d))
+    qp = QParams(group=8, block=8)
+    res, ins = layer_chain(W0s, X0, Xh0, qp=qp, steps=1, lr=0.0, return_inputs=True)
+
+    def outer_sum(*Ws):
+        P = np.zeros((d, d))
+        for Wx in Ws:
+            for row in Wx:
+                for a in range(d):
+                    for b in range(d):
+                        P[a, b] += row[a] * row[b]
+        return P
+
+    partners = {"q": outer_sum(W0s["o"]), "o": outer_sum(W0s["gate"], W0s["up"])}
+    alphas = [1.0, 2.0 / 3.0, 1.0 / 3.0]                         # 4 column blocks: steps 1..3 of 4
+    for name, Pm in partners.items():
+        X, Xh = ins[name]
+        plain = quantize_layer(W0s[name], X, Xh, qp=qp, steps=1, lr=0.0)
+        with_p = quantize_layer(W0s[name], X, Xh, M=Pm, qp=qp, steps=1, lr=0.0)
+        got = res[name].loss_trace
+        assert len(got) == 3
+        for (b, _, v), (_, _, li), (_, _, lp) in zip(got, plain.loss_trace, with_p.loss_trace):
+            assert v == pytest.approx(alphas[b] * li + (1.0 - alphas[b]) * lp, rel=1e-12), (name, b)
+    for name in ("k", "v", "gate", "up", "down"):
+        X, Xh = ins[name]
+        plain = quantize_layer(W0s[name], X, Xh, qp=qp, steps=1, lr=0.0)
+        assert [v for (_, _, v) in res[name].loss_trace] == [v for (_, _, v) in plain.loss_trace], name
 
 
 def test_pullback_gradient_matches_consumer_finite_differences():
