@@ -175,7 +175,7 @@ TIE_RTOL = 2.0 ** -40   # search errors within TIE_RTOL * least + TIE_ATOL * sum
 TIE_ATOL = 2.0 ** -60
 
 
-def group_search(x: np.ndarray, qp: QParams, row_chunk: int = 32) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+def group_search(x: np.ndarray, qp: QParams, row_chunk: int = 32, with_margin: bool = False):
     """Best asymmetric (scale, zero) per row of ``x`` ([rows, g]).
 
     For each row: lo = min(0, min x), hi = max(0, max x) (lo = -1, hi = 1 when both
@@ -189,16 +189,22 @@ def group_search(x: np.ndarray, qp: QParams, row_chunk: int = 32) -> Tuple[np.nd
     z_nat = clamp(rint(-lo maxq / (hi - lo)), 0, maxq) (the shrink factor cancels from
     -p_k lo / s_k, so one natural zero serves every k, and an exact half stays exact).
 
-    Returns (scale [rows], zero [rows] int, err [rows]).
+    Returns (scale [rows], zero [rows] int, err [rows]), and with ``with_margin`` also the relative
+    margin (e2 - e1) / e1 between the least error e1 and the least error e2 of a candidate outside
+    the tie set (inf when every candidate ties): a search whose margin is tiny is a near-tie, which
+    a float reordering on another machine can decide the other way.
     """
     x = np.asarray(x, dtype=np.float64)
     rows = x.shape[0]
     best_s = np.empty(rows)
     best_z = np.empty(rows, dtype=np.int64)
     best_e = np.empty(rows)
+    margin = np.empty(rows)
     for r0 in range(0, rows, row_chunk):
         r1 = min(rows, r0 + row_chunk)
-        best_s[r0:r1], best_z[r0:r1], best_e[r0:r1] = _group_search_rows(x[r0:r1], qp)
+        best_s[r0:r1], best_z[r0:r1], best_e[r0:r1], margin[r0:r1] = _group_search_rows(x[r0:r1], qp)
+    if with_margin:
+        return best_s, best_z, best_e, margin
     return best_s, best_z, best_e
 
 
@@ -235,14 +241,18 @@ def _group_search_rows(x, qp):
     ss = np.sum(x * x, axis=1)[:, None, None]
     if qp.sym:
         err = np.where(zz == qp.zsym, err, np.inf)    # the symmetric zero point only
-    cand = err <= err.min(axis=(1, 2), keepdims=True) * (1.0 + TIE_RTOL) + TIE_ATOL * ss
+    emin = err.min(axis=(1, 2), keepdims=True)
+    cand = err <= emin * (1.0 + TIE_RTOL) + TIE_ATOL * ss
+    e2 = np.where(cand, np.inf, err).min(axis=(1, 2))
+    with np.errstate(divide="ignore", invalid="ignore"):
+        margin = np.where(np.isinf(e2), np.inf, (e2 - emin[:, 0, 0]) / np.maximum(emin[:, 0, 0], 1e-300))
     for key in (kk, dist, zz):
         big = np.where(cand, key, np.inf)
         cand &= key == big.min(axis=(1, 2), keepdims=True)
     flat = cand.reshape(rows, -1).argmax(axis=1)
     kb, zb = np.divmod(flat, Z)
     ridx = np.arange(rows)
-    return s[ridx, kb], zb.astype(np.int64), err[ridx, kb, zb]
+    return s[ridx, kb], zb.astype(np.int64), err[ridx, kb, zb], margin
 
 
 def quantize_column(w: np.ndarray, scale: np.ndarray, zero: np.ndarray, maxq: int):
@@ -417,13 +427,14 @@ class LayerResult:
     loss_trace: List[Tuple[int, int, float]] = field(default_factory=list)  # (block, step, loss)
     prerounding: Optional[np.ndarray] = None   # float64 [m, n]: w/s + z just before rounding
     E_blocks: Optional[List[np.ndarray]] = None
+    search_margin: Optional[np.ndarray] = None  # float64 [m, ngroups]: group_search's margin
 
 
 def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams] = None,
                    steps: int = 0, lr: float = 1e-3, window: Optional[Tuple[int, int]] = None,
                    keep_E: bool = False, batch: Optional[int] = None,
                    loss_clip: Optional[float] = None, s_groups: Optional[np.ndarray] = None,
-                   grad_fn=None, loss_fn=None) -> LayerResult:
+                   grad_fn=None, loss_fn=None, H: Optional[np.ndarray] = None) -> LayerResult:
     """The per-module REAL-Q sweep (Alg. 1, one linear module), in float64.
 
     W0 [m, n]; X, Xhat [T, n]; s [T] or None; M [m, m] or None (identity);
@@ -443,6 +454,8 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     block's output) on the calibration tokens ``tokens = minibatch(t, T, batch)`` of step t, and
     ``loss_fn(W)`` the final loss over all tokens; X and the surrogate arguments are then unused
     and the Hessian still comes from Xhat.
+    ``H``: the Hessian of step 1 when the caller has already formed it from Xhat and s (for
+    instance as 2 Hs of gram_surrogate); it is then used instead of forming it again.
     """
     qp = qp or QParams()
     W0 = np.asarray(W0, dtype=np.float64)
@@ -459,7 +472,7 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
 
     if s_groups is None:
         groups = [slice(0, m)]
-        Hs = [hessian(Xhat, s)]
+        Hs = [hessian(Xhat, s) if H is None else np.asarray(H, dtype=np.float64)]
     else:
         sg = np.asarray(s_groups, dtype=np.float64)
         groups = row_groups(m, sg.shape[0])
@@ -478,6 +491,7 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     scales = np.zeros((m, ng))
     zeros = np.zeros((m, ng), dtype=np.int64)
     pre = np.zeros((m, n))
+    margin = np.full((m, ng), np.inf)
     trace: List[Tuple[int, int, float]] = []
     Es = [] if keep_E else None
 
@@ -494,7 +508,8 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
                 if j % grp == 0:
                     g = j // grp
                     g1 = min(j + grp, n)
-                    s64, zi, _ = group_search(np.where(dead_g[j:g1], 0.0, W[rs, j:g1]), qp)
+                    s64, zi, _, mg = group_search(np.where(dead_g[j:g1], 0.0, W[rs, j:g1]), qp, with_margin=True)
+                    margin[rs, g] = mg
                     cur_s[rs] = s64.astype(np.float32).astype(np.float64)   # scales are carried as float32
                     cur_z[rs] = zi.astype(np.float64)
                     scales[rs, g] = cur_s[rs]
@@ -542,7 +557,7 @@ def quantize_layer(W0, X, Xhat, s=None, M=None, P=None, *, qp: Optional[QParams]
     one = s_groups is None
     return LayerResult(codes=codes, scales=scales, zeros=zeros, W_hat=W, H=Hs[0] if one else Hs,
                        U=Us[0] if one else Us, dead=deads[0] if one else deads,
-                       loss_final=loss, loss_trace=trace, prerounding=pre, E_blocks=Es)
+                       loss_final=loss, loss_trace=trace, prerounding=pre, E_blocks=Es, search_margin=margin)
 
 
 def _blend(M, P, alpha, m):

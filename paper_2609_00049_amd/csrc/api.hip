@@ -197,6 +197,49 @@ int realq_ctx_reset_timing(realq_ctx* ctx) {
 
 // ============================================================================ a1: Hessian
 
+}  // extern "C"
+
+// Token chunks of tc tokens staged in caller-provided bf16 buffers of n * tc elements each (xt, and
+// hi, lo, lo2 when s is given): the chunk transposed (and, with weights, s_t xhat_t split into three
+// bf16 terms), then H_acc += chunk^T chunk on MFMA with a float64 epilogue.  timed = false skips the
+// timing events (the allocation-free entry point creates none).
+int realq::hessian_accum_chunks(realq_ctx* ctx, const uint16_t* Xhat, const float* s, int64_t T, int64_t n,
+                                double* H_acc, int64_t tc, uint16_t* xt, uint16_t* hi, uint16_t* lo, uint16_t* lo2,
+                                bool timed) {
+    Timed tm(ctx, timed ? "hessian" : nullptr);
+    for (int64_t t0 = 0; t0 < T; t0 += tc) {
+        const int64_t cur = std::min(tc, T - t0);
+        RQ_HIP(ctx, realq::transpose_u16(Xhat + t0 * n, n, xt, tc, cur, n, ctx->stream));
+        realq::GemmArgs g{};
+        g.B = xt;
+        g.ldb = tc;
+        g.M = n;
+        g.N = n;
+        g.K = cur;
+        g.lda = tc;
+        g.splits = 1;
+        if (s) {
+            // s_t xhat_t in three bf16 terms: with a heavy-tailed s a few tokens carry H, and the
+            // 2^-17 remainder of a hi/lo pair would not average out over the tokens
+            RQ_HIP(ctx, realq::transpose_scale_split(Xhat + t0 * n, n, s + t0, hi, lo, lo2, tc, cur, n, ctx->stream));
+            g.Ahi = hi;
+            g.Alo = lo;
+        } else {
+            g.Ahi = xt;
+            g.Alo = nullptr;
+        }
+        RQ_HIP(ctx, realq::gemm_acc_f64(g, H_acc, n, ctx->stream));
+        if (s) {
+            g.Ahi = lo2;
+            g.Alo = nullptr;
+            RQ_HIP(ctx, realq::gemm_acc_f64(g, H_acc, n, ctx->stream));
+        }
+    }
+    return REALQ_OK;
+}
+
+extern "C" {
+
 int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat, const float* s, int64_t T, int64_t n, double* H_acc) {
     if (!ctx) return REALQ_ERR_INVALID_ARG;
     if (T < 0 || n <= 0) return set_error(ctx, REALQ_ERR_SHAPE, "hessian_accum: need T >= 0, n > 0");
@@ -214,37 +257,8 @@ int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat, const float* s, in
         if ((rc = get_ws(ctx, "h_lo", (size_t)n * tc * 2, &lo))) return rc;
         if ((rc = get_ws(ctx, "h_lo2", (size_t)n * tc * 2, &lo2))) return rc;
     }
-    Timed tm(ctx, "hessian");
-    for (int64_t t0 = 0; t0 < T; t0 += tc) {
-        const int64_t cur = std::min(tc, T - t0);
-        RQ_HIP(ctx, realq::transpose_u16(Xhat + t0 * n, n, (uint16_t*)xt, tc, cur, n, ctx->stream));
-        realq::GemmArgs g{};
-        g.B = (const uint16_t*)xt;
-        g.ldb = tc;
-        g.M = n;
-        g.N = n;
-        g.K = cur;
-        g.lda = tc;
-        g.splits = 1;
-        if (s) {
-            // s_t xhat_t in three bf16 terms: with a heavy-tailed s a few tokens carry H, and the
-            // 2^-17 remainder of a hi/lo pair would not average out over the tokens
-            RQ_HIP(ctx, realq::transpose_scale_split(Xhat + t0 * n, n, s + t0, (uint16_t*)hi, (uint16_t*)lo,
-                                                     (uint16_t*)lo2, tc, cur, n, ctx->stream));
-            g.Ahi = (const uint16_t*)hi;
-            g.Alo = (const uint16_t*)lo;
-        } else {
-            g.Ahi = (const uint16_t*)xt;
-            g.Alo = nullptr;
-        }
-        RQ_HIP(ctx, realq::gemm_acc_f64(g, H_acc, n, ctx->stream));
-        if (s) {
-            g.Ahi = (const uint16_t*)lo2;
-            g.Alo = nullptr;
-            RQ_HIP(ctx, realq::gemm_acc_f64(g, H_acc, n, ctx->stream));
-        }
-    }
-    return REALQ_OK;
+    return realq::hessian_accum_chunks(ctx, Xhat, s, T, n, H_acc, tc, (uint16_t*)xt, (uint16_t*)hi, (uint16_t*)lo,
+                                       (uint16_t*)lo2, true);
 }
 
 // ============================================================================ a0: Stage-0 accumulators

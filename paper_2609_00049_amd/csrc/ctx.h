@@ -49,6 +49,10 @@ namespace realq {
 // Argument checks shared by the entry points (REALQ_OK or an error set on ctx).
 int validate_q(realq_ctx* ctx, const realq_qparams* qp);
 int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p);
+// Token-chunked Hessian accumulation into H_acc with caller-provided staging buffers (n * tc bf16
+// each; hi, lo, lo2 only used when s is given).
+int hessian_accum_chunks(realq_ctx* ctx, const uint16_t* Xhat, const float* s, int64_t T, int64_t n, double* H_acc,
+                         int64_t tc, uint16_t* xt, uint16_t* hi, uint16_t* lo, uint16_t* lo2, bool timed);
 
 // Brackets the launches of its scope with events on the context stream when timing is on.
 struct Timed {
@@ -56,7 +60,7 @@ struct Timed {
     const char* name;
     hipEvent_t a = nullptr, b = nullptr;
     Timed(realq_ctx* c, const char* n) : ctx(c), name(n) {
-        if (!ctx->timing) return;
+        if (!ctx->timing || !n) return;
         if (!ctx->free_events.empty()) {
             a = ctx->free_events.back().first;
             b = ctx->free_events.back().second;

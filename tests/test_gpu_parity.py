@@ -371,12 +371,19 @@ def test_layer_sliding_window(rq, ctx, window):
     _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
 
 
+def _assert_tie_rows(met, nrows):
+    """At most 1% of the sampled rows (and at least one allowed) may end in a rounding-tie cascade."""
+    assert met["tie_cascade_rows"] <= max(1, nrows // 100), met
+
+
 def test_layer_llama_gate_full_size_sampled_rows(rq, ctx):
     """The benchmark's own workload and launch configuration: the 14336x4096 gate projection with
-    262144 tokens, 8 Block-GD steps per block at lr 1e-5.  The oracle follows 4 sampled rows
-    through the whole sweep with the surrogate written through the calibration Gram matrices
-    (oracle.gram_surrogate, pinned equal to the token form).  About a minute on an MI355X host
-    (inputs ~20 s, float64 Gram matrices ~25 s, GPU sweep 15 s), ~40 GB of host memory."""
+    262144 tokens, 8 Block-GD steps per block at lr 1e-5.  The oracle follows 256 sampled rows (one
+    in every 256-row tile of the GEMMs, 200 more at random) through the whole sweep with the
+    surrogate written through the calibration Gram matrices (oracle.gram_surrogate, pinned equal to
+    the token form); the Hessian is checked whole against the oracle's X^T X / T.  A few minutes on
+    an MI355X host (inputs ~20 s, float64 Gram matrices ~25 s, GPU sweep 15 s, oracle rows ~60 s),
+    ~45 GB of host memory."""
     import time
     torch = _torch()
     t0 = time.time()
@@ -384,22 +391,27 @@ def test_layer_llama_gate_full_size_sampled_rows(rq, ctx):
     _banner(f"layer llama3.1-8b gate 14336x4096 T=262144: inputs drawn in {time.time() - t0:.0f} s")
     g = _run(rq, ctx, L, L.steps, L.lr)
     _banner(f"GPU sweep {g.ms_total:.0f} ms")
-    rows = np.random.default_rng(9).choice(L.W0.shape[0], 4, replace=False)
+    Hg = g.H.cpu().numpy().astype(np.float64)
+    g.H = None
+    rows = P.tile_rows(L.W0.shape[0], per_tile=1, extra=200, seed=9)
     X, Xh = L.X.astype(np.float64), L.Xhat.astype(np.float64)
-    grad_fn, loss_fn = oracle.gram_surrogate(L.W0[rows], X, Xh, L.s)
+    del L.X, L.Xhat
+    grad_fn, loss_fn = oracle.gram_surrogate(L.W0[rows], X, Xh, L.s, trace_loss=False)
     _banner(f"Gram matrices formed at {time.time() - t0:.0f} s")
-    o = oracle.quantize_layer(L.W0[rows], X, Xh, L.s, steps=L.steps, lr=L.lr, grad_fn=grad_fn, loss_fn=loss_fn)
+    herr = P.rel_fro(Hg, 2.0 * grad_fn.Hs)
+    print("Hessian rel Frobenius", herr, flush=True)
+    assert herr <= P.HESS_RTOL
+    o = oracle.quantize_layer(L.W0[rows], X, Xh, L.s, steps=L.steps, lr=L.lr, grad_fn=grad_fn, loss_fn=loss_fn,
+                              H=2.0 * grad_fn.Hs)
+    del X, Xh
     _banner(f"oracle rows done at {time.time() - t0:.0f} s")
-    _assert_parity(P.compare(g, o, rows=rows))
+    met = P.compare(g, o, rows=rows, tie_cascade=True)
+    _assert_parity(met)
+    _assert_tie_rows(met, len(rows))
+    # final loss of the sampled rows at the GPU's own weights, every row
     lg = loss_fn(g.W_hat.cpu().numpy()[rows].astype(np.float64))
     print("row loss", lg, o.loss_final, flush=True)
     assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
-    # the Hessian at the full token count, on sampled entries against their definition
-    H = g.H.cpu().numpy()
-    for (i, j) in [(0, 0), (17, 4000), (2048, 2049), (4095, 1)]:
-        ref = 2.0 / Xh.shape[0] * float(Xh[:, i] @ Xh[:, j])
-        scale = (2.0 / Xh.shape[0]) * math.sqrt(float(Xh[:, i] @ Xh[:, i]) * float(Xh[:, j] @ Xh[:, j]))
-        assert abs(H[i, j] - ref) <= 1e-6 * scale, (i, j)
     torch.cuda.synchronize()
 
 
@@ -412,15 +424,15 @@ def test_layer_large_module_shape_sampled_rows(rq, ctx, cfg, module, chunk):
     m x n with 8192 tokens and 8 Block-GD steps per block at the
     workload's learning rate.  The 70B case streams the tokens through the residual and gradient
     GEMMs in chunks (2048 of 8192 here), as its full-size workload does with 32768-token chunks.
-    The oracle follows 32 sampled rows through the Gram-form surrogate (pinned equal to the token
-    form; rows are independent for the identity metric).  Adam's first step is about
-    lr * sign(g), so a weight whose gradient is near zero can step the other way under float32
-    rounding; once such a difference carries a later weight across a rounding boundary, GPTQ
-    re-routes the rest of that row (about one row in a hundred at this width), so the code bar
-    needs a sample of many rows to mean anything.  A row whose first mismatch is a rounding tie
-    of the oracle (pre-rounding value within 1e-3 code units of a half-integer) is compared up to
-    that tie only: from there on the two sides quantize different weights (at 28672 x 8192 one of
-    the 32 rows meets a tie at 8.4999989 in column 1214)."""
+    The oracle follows 128 sampled rows (one in every 256-row tile of the GEMMs, the rest at random)
+    through the Gram-form surrogate (pinned equal to the token form; rows are independent for the
+    identity metric).  Adam's first step is about lr * sign(g), so a weight whose gradient is near
+    zero can step the other way under float32 rounding; once such a difference carries a later
+    weight across a rounding boundary, GPTQ re-routes the rest of that row.  A row whose first
+    mismatch is a rounding tie of the oracle (pre-rounding value within 1e-5 code units of a
+    half-integer, the float drift bound of tests/parity.py) is compared up to that tie only (at
+    28672 x 8192 one row meets a tie at 8.4999989 in column 1214); the final loss is taken at the
+    GPU's own weights in every row."""
     import time
     t0 = time.time()
     L = synth.make_module(cfg, module, T=8192)
@@ -429,27 +441,21 @@ def test_layer_large_module_shape_sampled_rows(rq, ctx, cfg, module, chunk):
     _banner(f"layer {cfg} {module} {m}x{n} T={T} chunk={chunk}: inputs drawn in {time.time() - t0:.0f} s")
     g = _run(rq, ctx, L, L.steps, L.lr, chunk=chunk)
     _banner(f"GPU sweep {g.ms_total:.0f} ms")
-    rows = np.random.default_rng(10).choice(m, 32, replace=False)
+    rows = P.tile_rows(m, per_tile=1, extra=128 - -(-m // 256), seed=10)
     X, Xh = L.X.astype(np.float64), L.Xhat.astype(np.float64)
     grad_fn, loss_fn = oracle.gram_surrogate(L.W0[rows], X, Xh, L.s, trace_loss=False)
-    o = oracle.quantize_layer(L.W0[rows], X, Xh, L.s, steps=L.steps, lr=L.lr, grad_fn=grad_fn, loss_fn=loss_fn)
+    herr = P.rel_fro(g.H.cpu().numpy().astype(np.float64), 2.0 * grad_fn.Hs)
+    print("Hessian rel Frobenius", herr, flush=True)
+    assert herr <= P.HESS_RTOL
+    o = oracle.quantize_layer(L.W0[rows], X, Xh, L.s, steps=L.steps, lr=L.lr, grad_fn=grad_fn, loss_fn=loss_fn,
+                              H=2.0 * grad_fn.Hs)
     _banner(f"oracle rows done at {time.time() - t0:.0f} s")
     met = P.compare(g, o, rows=rows, tie_cascade=True)
     _assert_parity(met)
-    assert met["tie_cascade_rows"] <= 2
-    # loss at the GPU weights, rows past a rounding tie taken from the oracle
-    Wg = g.W_hat.cpu().numpy()[rows].astype(np.float64)
-    for i in P.tie_cascades(g.codes.cpu().numpy()[rows], o):
-        Wg[i] = o.W_hat[i]
-    lg = loss_fn(Wg)
+    _assert_tie_rows(met, len(rows))
+    lg = loss_fn(g.W_hat.cpu().numpy()[rows].astype(np.float64))
     print("row loss", lg, o.loss_final, flush=True)
     assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
-    # Hessian on sampled entries against its definition
-    H = g.H.cpu().numpy()
-    for (i, j) in [(0, 0), (n - 1, 3), (n // 2, n // 2 + 1)]:
-        ref = 2.0 / T * float(Xh[:, i] @ Xh[:, j])
-        scale = (2.0 / T) * math.sqrt(float(Xh[:, i] @ Xh[:, i]) * float(Xh[:, j] @ Xh[:, j]))
-        assert abs(H[i, j] - ref) <= 1e-6 * scale, (i, j)
 
 
 def test_layer_llama_gate_shape_sampled_rows(rq, ctx):

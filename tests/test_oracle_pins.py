@@ -152,6 +152,12 @@ def _check_search(x, bits=4):
     pick = (ks[0], int(z[0]))
     ss = sum(Fraction(float(v)) ** 2 for v in xs)
     assert abs(Fraction(float(e[0])) - table[pick]) <= Fraction(1e-12) * table[pick] + Fraction(2.0 ** -100) * ss
+    # the reported margin: gap from the least exact error to the least one outside the tie set
+    _, _, _, mg = group_search(xs[None, :], qp, with_margin=True)
+    emin = min(table.values())
+    outside = [v for v in table.values() if v > emin * (1 + Fraction(TIE_RTOL)) + Fraction(TIE_ATOL) * ss]
+    if outside and emin > Fraction(1e-12) * ss:       # a relative margin is only defined away from 0
+        assert float(mg[0]) == pytest.approx(float((min(outside) - emin) / emin), rel=1e-9, abs=1e-12)
     if (s[0], z[0]) != (bs, bz):
         assert table[pick] <= be * (1 + Fraction(TIE_RTOL)) + Fraction(TIE_ATOL) * ss, (pick, bs, bz)
         znat = min(max(_rint_exact(-Fraction(lo) * qp.maxq / Fraction(hi - lo)), 0), qp.maxq)
@@ -459,6 +465,11 @@ def test_sweep_driven_by_the_gram_surrogate_is_the_token_sweep():
     b = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3, grad_fn=grad_fn, loss_fn=loss_fn)
     assert (a.codes == b.codes).all()
     assert b.loss_final == pytest.approx(a.loss_final, rel=1e-10)
+    # the Hessian handed in (2 Hs of the Gram matrices) instead of formed from Xhat: same sweep
+    c = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3, grad_fn=grad_fn, loss_fn=loss_fn,
+                              H=2.0 * grad_fn.Hs)
+    np.testing.assert_allclose(2.0 * grad_fn.Hs, a.H, rtol=1e-12, atol=1e-12 * np.abs(a.H).max())
+    assert (c.codes == a.codes).all()
 
 
 def test_adam_constants_are_the_papers():
