@@ -161,6 +161,20 @@ int realq_saliency(realq_ctx* ctx, const uint16_t* G /*[T,m]*/, int64_t T, int64
 int realq_hessian_accum(realq_ctx* ctx, const uint16_t* Xhat /*[T,n]*/, const float* s /*[T]|NULL*/,
                         int64_t T, int64_t n, double* H_acc /*[n,n]*/);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): the same accumulation as realq_hessian_accum, with the
+ * token chunks staged in a fixed scratch array of REALQ_NOALLOC_SCRATCH_BYTES that the library
+ * holds on each GPU it runs on (from the first call on that GPU until the process ends) instead of
+ * context workspaces; it calls no device allocator.  Chunks are shorter than realq_hessian_accum's,
+ * so float64 sums across chunks may differ from it in the last bits.  n > REALQ_NOALLOC_MAX_N gives
+ * REALQ_ERR_SHAPE.  Every call on one GPU shares that GPU's scratch array: calls that overlap on one
+ * GPU (from several streams or threads) race and must be serialised by the caller.  Nothing in the
+ * array needs clearing between calls. */
+#define REALQ_NOALLOC_SCRATCH_BYTES (64ll << 20)
+#define REALQ_NOALLOC_MAX_N 32768
+int realq_hessian_accum_noalloc(realq_ctx* ctx, const uint16_t* Xhat /*[T,n]*/, const float* s /*[T]|NULL*/,
+                                int64_t T, int64_t n, double* H_acc /*[n,n]*/);
+
 /* ------------------------------------------------------------------ a2: inverse factor
  * H = (2/T_total) H_acc is written to H_out (float32) when H_out != NULL.  Dead
  * columns (H_jj == 0) get H_jj = 1 and are flagged in dead[j] (when non-NULL);

@@ -32,7 +32,7 @@ EXPORTS = [
     "realq_ctx_create", "realq_ctx_destroy", "realq_last_error",
     "realq_ctx_set_timing", "realq_ctx_kernel_time", "realq_ctx_reset_timing",
     "realq_fisher_accum", "realq_fisher_finish", "realq_saliency",
-    "realq_hessian_accum", "realq_chol_inverse",
+    "realq_hessian_accum", "realq_hessian_accum_noalloc", "realq_chol_inverse",
     "realq_bgd_state_create", "realq_bgd_state_destroy",
     "realq_quantize_block", "realq_quantize_block_rows", "realq_bgd_lock_block",
     "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
@@ -140,6 +140,7 @@ def _load():
         "realq_fisher_finish": (ctypes.c_int, [vp, vp, i64, i64, vp]),
         "realq_saliency": (ctypes.c_int, [vp, vp, i64, i64, i32, f32, vp]),
         "realq_hessian_accum": (ctypes.c_int, [vp, vp, vp, i64, i64, vp]),
+        "realq_hessian_accum_noalloc": (ctypes.c_int, [vp, vp, vp, i64, i64, vp]),
         "realq_chol_inverse": (ctypes.c_int, [vp, vp, i64, i64, f32, vp, vp, vp]),
         "realq_bgd_state_create": (ctypes.c_int, [vp, ctypes.POINTER(vp), vp, vp, vp, vp, vp, vp, i64, i64, i64,
                                                   ctypes.POINTER(BgdParams)]),
@@ -295,6 +296,14 @@ def hessian_accum(ctx: Context, Xhat: torch.Tensor, s: Optional[torch.Tensor], H
     T, n = _dims(Xhat, "Xhat", 2)
     ctx.check(_lib.realq_hessian_accum(ctx.h, _t(Xhat, "Xhat", BF16, (T, n)), _t(s, "s", F32, (T,), True), T, n,
                                        _t(H_acc, "H_acc", F64, (n, n))))
+
+
+def hessian_accum_noalloc(ctx: Context, Xhat: torch.Tensor, s: Optional[torch.Tensor], H_acc: torch.Tensor):
+    """hessian_accum with its staging in the library's fixed per-GPU scratch array (no device
+    allocation; calls that overlap on one GPU race)."""
+    T, n = _dims(Xhat, "Xhat", 2)
+    ctx.check(_lib.realq_hessian_accum_noalloc(ctx.h, _t(Xhat, "Xhat", BF16, (T, n)), _t(s, "s", F32, (T,), True),
+                                               T, n, _t(H_acc, "H_acc", F64, (n, n))))
 
 
 def chol_inverse(ctx: Context, H_acc: torch.Tensor, T_total: int, damp: float, U: torch.Tensor,
