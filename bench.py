@@ -89,28 +89,92 @@ def make_inputs(torch, wl, seed=0):
     return W0.contiguous(), X.contiguous(), Xh.contiguous(), s
 
 
-def cpu_baseline(wl, rows=64, tokens=16384):
-    """Oracle timed on a bounded sample of the same workload, scaled by algorithmic FLOPs."""
+def _host_info():
+    """CPU model, usable cores and the BLAS numpy calls (recorded with the CPU baseline)."""
+    import numpy as np
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = "unknown"
+    try:
+        cfg = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{cfg.get('name')} {cfg.get('version')}"
+    except Exception:
+        pass
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
+                      default=None)
+    except Exception:
+        pass
+    return model, len(os.sched_getaffinity(0)), blas, threads
+
+
+def cpu_baseline(wl, hess_tokens=32768, rows=256, tokens=16384):
+    """The oracle on the machine's host cores, timed phase by phase at the workload's shape: the
+    Hessian on a slice of the calibration tokens (full n), damping and the inverse factor at full
+    n, and column block 0 with its K Block-GD steps on a sample of rows and tokens (full n).  The
+    oracle's own floating-point rate over these phases then prices the workload's algorithmic
+    FLOPs: the result is an extrapolation (a full sweep is hours on a host)."""
     import numpy as np
     import synth
     import oracle
     cfg, module, m, n, T, steps, lr = WORKLOADS[wl]
+    model, cores, blas, threads = _host_info()
+    Th = min(hess_tokens, T)
     Ts = min(tokens, T)
-    L = synth.make_module(cfg, module, m=min(rows, m), n=n, T=Ts)
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
+    r = min(rows, m)
+    L = synth.make_module(cfg, module, m=r, n=n, T=max(Th, Ts))
+    X, Xh = L.X.astype(np.float64), L.Xhat.astype(np.float64)
+    qp = oracle.QParams()
+    # 1. Hessian (2 n^2 Th)
     t0 = time.perf_counter()
-    oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=steps, lr=lr)
-    dt = time.perf_counter() - t0
-    f_sample = f_alg(L.W0.shape[0], n, Ts, steps)["total"]
-    f_full = f_alg(m, n, T, steps)["total"]
-    t_full = dt * f_full / f_sample
-    return {"value": n / t_full, "unit": "columns/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{L.W0.shape[0]} of {m} rows, {Ts} of {T} tokens, n={n}, K={steps}: {dt:.1f} s, "
-                      f"scaled to the full workload by algorithmic FLOPs ({t_full:.0f} s per sweep)"}
+    H = oracle.hessian(Xh[:Th], None if L.s is None else L.s[:Th])
+    t_h = time.perf_counter() - t0
+    # 2. damping and the inverse factor (about 2 n^3 for the inverse, n^3 / 3 for the factor)
+    t0 = time.perf_counter()
+    Hd, _ = oracle.damp_hessian(H, qp.damp)
+    oracle.inverse_factor(Hd)
+    t_c = time.perf_counter() - t0
+    # 3. column block 0 (search, GPTQ, trailing update) and its K Block-GD steps
+    t0 = time.perf_counter()
+    oracle.quantize_layer(L.W0, X[:Ts], Xh[:Ts], None if L.s is None else L.s[:Ts],
+                          qp=oracle.QParams(block=n), steps=0)   # one block of n columns: search + GPTQ
+    t_q = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    sw = None if L.s is None else L.s[:Ts]
+    W = L.W0.astype(np.float64)
+    J = slice(qp.block, n)
+    mA = np.zeros((r, n - qp.block))
+    vA = np.zeros_like(mA)
+    for k in range(steps):
+        R = oracle.residual(W, L.W0, X[:Ts], Xh[:Ts])
+        G = oracle.surrogate_grad(R, sw, None, Xh[:Ts, J], Ts)
+        W[:, J], mA, vA = oracle.adam_update(W[:, J], G, mA, vA, k + 1, lr)
+    t_b = time.perf_counter() - t0
+    # floating-point work of the timed phases (the oracle's own: its residual is the full forward)
+    nJ = n - qp.block
+    fl = (2.0 * n * n * Th + 2.0 * n ** 3 + n ** 3 / 3.0
+          + steps * (4.0 * r * n * Ts + 2.0 * r * Ts * nJ))
+    t_timed = t_h + t_c + t_b
+    rate = fl / t_timed
+    # the search and GPTQ are not FLOP-shaped: scaled by rows and column blocks instead
+    t_quant_full = t_q * (m / r)
+    t_full = f_alg(m, n, T, steps)["total"] / rate + t_quant_full
+    return {"value": n / t_full, "unit": "columns/s", "cores": int(cores), "kind": "oracle", "extrapolated": True,
+            "cpu": model, "blas": blas, "blas_threads": threads,
+            "sample": f"oracle phases at n={n}: Hessian on {Th} of {T} tokens {t_h:.1f} s; damping + inverse "
+                      f"factor {t_c:.1f} s; block 0 of {r} of {m} rows: search + GPTQ of all {n} columns "
+                      f"{t_q:.1f} s, {steps} Block-GD steps on {Ts} tokens {t_b:.1f} s; oracle rate "
+                      f"{rate / 1e9:.1f} GFLOP/s fp64 over the FLOP-shaped phases, the algorithmic FLOPs of the "
+                      f"full sweep priced at it plus the search and GPTQ scaled by rows: {t_full:.0f} s per "
+                      f"sweep (extrapolated)"}
 
 
 def output_grads(torch, T, m, seed=1, chunk=16384):
@@ -314,6 +378,63 @@ def decoder_block(torch, rq, ctx, qp, T=8192, d=4096, f=14336, H=32, Hkv=8, hd=1
             "columns_per_s": (3 * d + Hq + 2 * d + f) / (r.ms_total / 1e3)}
 
 
+# Further modules of the layer workloads, one sweep each at full size (name: cfg, module, T, token
+# chunk, window partner module or None): the Qwen3-32B q projection with its dense Wishart metric,
+# the LLaMA-3.1-8B q projection with o as its window partner, the LLaMA-3.1-8B down projection
+# (inverse factor at n = 14336) at 8192 tokens, and the Qwen3-0.6B down projection at its full
+# 131072 tokens.
+CONFIG_LEGS = {
+    "qwen3_32b_q_dense_metric": ("qwen3_32b_layer", "q", 262144, 0, None),
+    "llama3.1_8b_q_window_o": ("llama3.1_8b_layer", "q", 262144, 0, "o"),
+    "llama3.1_8b_down_T8192": ("llama3.1_8b_layer", "down", 8192, 0, None),
+    "qwen3_0.6b_down": ("qwen3_0.6b_mlp", "down", 131072, 0, None),
+}
+
+
+def config_legs(torch, rq, ctx, qp):
+    """One warm-up and one timed sweep of each CONFIG_LEGS module (inputs generated on the device
+    with the workload's distributions); F_alg counts K 2 m^2 SJ per dense metric or partner term."""
+    import synth
+    out = {}
+    for name, (cfg, module, T, chunk, partner) in CONFIG_LEGS.items():
+        c = synth.CONFIGS[cfg]
+        m, n = c["modules"][module]
+        K, lr = c["steps"], c["lr"]
+        WORKLOADS["_leg"] = (cfg, module, m, n, T, K, lr)
+        W0, X, Xh, s = make_inputs(torch, "_leg")
+        M = P = None
+        window = None
+        g = torch.Generator(device="cuda")
+        g.manual_seed(4242)
+        if c["M"] is not None and c["M"][1] == m:
+            A = torch.randn((m, 2 * m), generator=g, device="cuda")
+            M = (A @ A.T / (2 * m)).contiguous()
+            del A
+        if partner is not None:
+            mp, _ = c["modules"][partner]
+            Wn = (torch.randn((mp, m), generator=g, device="cuda") * c["w"][1]).to(torch.bfloat16).float().contiguous()
+            P = torch.empty((m, m), dtype=torch.float32, device="cuda")
+            rq.pullback_metric(ctx, Wn, P)
+            del Wn
+            window = (0, -(-n // qp.block))
+        bgd = rq.bgd_params(steps=K, lr=lr, tok_chunk=chunk)
+        o = rq.quantize_layer(ctx, W0, X, Xh, s, M, P, qp=qp, bgd=bgd, window=window)
+        o = rq.quantize_layer(ctx, W0, X, Xh, s, M, P, qp=qp, bgd=bgd, window=window, out=o)
+        fa = f_alg(m, n, T, K)
+        dense_terms = (1 if M is not None else 0) + (1 if P is not None else 0)
+        fl = fa["total"] + dense_terms * K * 2.0 * m * m * fa["SJ"]
+        print(f"[bench] {name}: {m}x{n} T={T}: {o.ms_total:.1f} ms, loss {o.loss_final:.6g}", file=sys.stderr,
+              flush=True)
+        out[name] = {"m": m, "n": n, "tokens": T, "bgd_steps": K, "dense_metric": M is not None,
+                     "window_partner": partner, "ms": o.ms_total, "columns_per_s": n / (o.ms_total / 1e3),
+                     "tflops_alg": fl / (o.ms_total / 1e3) / 1e12, "frac_bf16_peak_alg": fl / (o.ms_total / 1e3) / PEAK_BF16,
+                     "loss_final": o.loss_final}
+        del W0, X, Xh, s, M, P, o
+        torch.cuda.empty_cache()
+    WORKLOADS.pop("_leg", None)
+    return out
+
+
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_00049_amd", "csrc", "gemm_bf16.hip")
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_llama8b_gate_traffic.txt")
 
@@ -362,7 +483,9 @@ def main():
     ap.add_argument("--no-decoder", action="store_true",
                     help="skip the block-output surrogate sweep of a LLaMA-3.1-8B-shaped decoder block "
                          "(decoder_block)")
-    ap.add_argument("--only", choices=("stage0", "block", "decoder"),
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the sweeps of the further modules (dense metric, window partner, down projections)")
+    ap.add_argument("--only", choices=("stage0", "block", "decoder", "configs"),
                     help="run only that part (for per-part kernel profiles) and print its object")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -384,6 +507,10 @@ def main():
         ctx = rq.Context()
         ctx.set_timing(True)
         print(json.dumps({"decoder_block": decoder_block(torch, rq, ctx, rq.qparams())}), flush=True)
+        return
+    if args.only == "configs":
+        ctx = rq.Context()
+        print(json.dumps({"configs": config_legs(torch, rq, ctx, rq.qparams())}), flush=True)
         return
     print(f"[bench] generating {args.workload}: m={m} n={n} T={T} K={K}", file=sys.stderr, flush=True)
     W0, X, Xh, s = make_inputs(torch, args.workload)
@@ -437,6 +564,10 @@ def main():
         dom_flops = 2.0 * m * n * n * kt[dom][0]
     launches, dom_ms = kt[dom]
     achieved = dom_flops / (dom_ms / 1e3) if dom_ms > 0 else math.nan
+    # the achievable MFMA rate of this GPU (register-resident loop), beside the data-sheet peak;
+    # executed MFMA work counts both halves of every hi/lo split operand (twice the algorithmic)
+    peak_meas = rq.mfma_peak(ctx) * 1e12
+    sweep_rate = fa["total"] / (ms_per_step / 1e3)
     res = {
         "metric": "layer-sweep time (ms) and quantized columns/sec; achieved TFLOP/s vs MFMA peak",
         "value": n / (ms_per_step / 1e3),
@@ -453,13 +584,18 @@ def main():
         "config": {"workload": args.workload, "m": m, "n": n, "tokens": T, "bgd_steps": K, "bits": 4,
                    "group": 128, "block": 128, "bgd_form": args.form,
                    "token_chunk": TOKEN_CHUNK.get(args.workload, 0)},
-        "tflops_alg": fa["total"] / (ms_per_step / 1e3) / 1e12,
-        "frac_bf16_peak_alg": fa["total"] / (ms_per_step / 1e3) / PEAK_BF16,
+        "tflops_alg": sweep_rate / 1e12,
+        "frac_bf16_peak_alg": sweep_rate / PEAK_BF16,
+        "mfma_peak_measured_tflops": peak_meas / 1e12,
+        "frac_measured_peak_alg": sweep_rate / peak_meas,
         "kernel_ms_per_step": {k: v[1] / args.steps for k, v in kt.items()},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16,
                      "traffic": measured_traffic(args.workload, dom) if args.form == "tokens" else None,
-                     "launches": launches, "avg_launch_ms": dom_ms / max(1, launches)},
+                     "launches": launches, "avg_launch_ms": dom_ms / max(1, launches),
+                     "measured_peak": peak_meas / 1e12, "frac_measured_peak": achieved / peak_meas,
+                     "executed_frac": 2.0 * achieved / PEAK_BF16 if args.form == "tokens" else None,
+                     "executed_frac_measured_peak": 2.0 * achieved / peak_meas if args.form == "tokens" else None},
     }
     if args.form == "tokens" and not args.no_gram_line:
         # one untimed-region Gram-form sweep of the same inputs, reported beside the headline
@@ -473,9 +609,11 @@ def main():
                                     "(bench.py --form gram for its own line)"}
     if not args.no_stage0:
         res["stage0"] = stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n, T)
-    if not (args.no_block and args.no_decoder):
+    if not (args.no_block and args.no_decoder and args.no_configs):
         del W0, X, Xh, s
         torch.cuda.empty_cache()
+    if not args.no_configs:
+        res["configs"] = config_legs(torch, rq, ctx, qp)
     if not args.no_block:
         res["mlp_block"] = mlp_block(torch, rq, ctx, qp)
     if not args.no_decoder:

@@ -150,6 +150,14 @@ int realq_fisher_finish(realq_ctx* ctx, const double* F_acc, int64_t m, int64_t 
 int realq_saliency(realq_ctx* ctx, const uint16_t* G /*[T,m]*/, int64_t T, int64_t m, int32_t n_groups, float clip_q,
                    float* s_out /*[n_groups,T]*/);
 
+/* ------------------------------------------------------------------ diagnostics (not part of the method)
+ * The bf16 MFMA rate the GPU sustains on a register-resident loop (v_mfma_f32_32x32x16_bf16,
+ * eight independent accumulator chains per wave, two waves per SIMD, four blocks per CU; no
+ * memory traffic in the loop), in TFLOP/s written to *tflops (host).  The sweep's MFMA fraction is
+ * reported against it beside the data-sheet peak.  iters in 1 .. 2^24 rounds per wave (2^16 takes
+ * about 50 ms).  Synchronises the stream. */
+int realq_mfma_peak(realq_ctx* ctx, int64_t iters, double* tflops);
+
 /* ------------------------------------------------------------------ a1: Hessian
  * Sec. 3.2 (H = (2/T) sum_t x_t x_t^T) and Eq. saliency_hessian (per-token weights).
  * H_acc[n*n] (float64, caller-initialised, typically zeroed) += sum_t s_t xhat_t xhat_t^T
@@ -182,8 +190,9 @@ int realq_hessian_accum_noalloc(realq_ctx* ctx, const uint16_t* Xhat /*[T,n]*/, 
  * float32, lower triangle zero) with H_d^{-1} = U^T U is written.  Row j of U
  * over U_jj is the compensation direction of Eq. gptq_update (Sec. 3.2) with the
  * sequentially eliminated inverse.  Computed in float64.  Synchronises the stream
- * once to read the positive-definiteness flag: REALQ_ERR_NOT_SPD if it fails
- * (retry with a larger damp). */
+ * once to read two flags: REALQ_ERR_NONFINITE if H_acc holds a NaN or an infinity (a
+ * non-finite Xhat or s reached the Hessian), else REALQ_ERR_NOT_SPD if the factorisation
+ * fails (retry with a larger damp). */
 int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T_total, float damp,
                        float* H_out /*[n,n]|NULL*/, float* U /*[n,n]*/, uint8_t* dead /*[n]|NULL*/);
 
@@ -327,7 +336,9 @@ typedef struct realq_layer_out {
 } realq_layer_out;
 
 /* Synchronises the stream (after the inverse factor, and at the end to read the
- * final loss).  Returns the first error of any stage. */
+ * final loss).  Returns the first error of any stage; REALQ_ERR_NONFINITE when the Hessian
+ * (non-finite Xhat or s) or the final loss (non-finite W0, X, s or metric) is not finite, in
+ * which case the outputs are undefined. */
 int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* desc, realq_layer_out* out);
 
 /* ------------------------------------------------------------------ NEXT: block-output surrogate
@@ -357,6 +368,20 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* desc, realq_lay
  *               With 0 < batch < T, Adam step t of a module (1-based) evaluates L (and
  *               L_next) on token batch (t - 1) mod ceil(T / batch) only, normalised by its
  *               token count (Sec. 4.3 mini-batch); loss_final is over all T tokens
+ *   start_module, n_modules, W_fixed : quantize modules start_module .. start_module +
+ *               n_modules - 1 only (n_modules = 0: through the last; [0, 0] is the whole
+ *               block).  The modules before start_module are taken as already quantized, with
+ *               W_fixed[k] their float32 quantized weights (required, copied to W_hat[k]; their
+ *               codes, scales and zeros are not written); the modules after the range keep their
+ *               original weights, also in loss_final.  b_global and the window's alpha count
+ *               every module's column blocks, as in a whole-block sweep, so a module swept alone
+ *               on the upstream modules' quantized weights follows the steps it takes in the
+ *               whole sweep.  loss_trace entries of modules not swept stay NaN.
+ *   X_fixed   : the start module's input in the quantized path ([T, cols] bf16: u for gate
+ *               and up, z for down) taken as given instead of computed by the block from the
+ *               fixed weights, or NULL.  With X_fixed and W_fixed from a reference sweep, the
+ *               start module sees exactly the reference's inputs (a bf16 rounding of an
+ *               activation can fall either way between two correct implementations).
  * Outputs per module (0 gate, 1 up, 2 down): codes [rows, cols] (gate, up: [f, d]; down:
  * [d, f]), scales and zeros [rows, ceil(cols/group)], W_hat [rows, cols] float32 (all
  * required); loss_trace [B_total * steps] device float64, entry (b_global - 1) * steps + k,
@@ -381,6 +406,9 @@ typedef struct realq_mlp_desc {
     int32_t window;
     realq_qparams q;
     realq_bgd_params bgd;
+    int32_t start_module, n_modules;
+    const float* W_fixed[3];
+    const uint16_t* X_fixed;
 } realq_mlp_desc;
 
 typedef struct realq_mlp_out {
@@ -414,7 +442,10 @@ int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* desc, realq_mlp_
  * that a mini-batch holds whole sequences (REALQ_ERR_SHAPE otherwise).  The
  * attention forward keeps the row log-sum-exp (the backward recomputes the probabilities from
  * it); its backward keeps six bf16 arrays of T n_heads seq_len entries.  Outputs per
- * module in the order q, k, v, o, gate, up, down; loss_trace entry (b_global - 1) * steps + k. */
+ * module in the order q, k, v, o, gate, up, down; loss_trace entry (b_global - 1) * steps + k.
+ * start_module, n_modules, W_fixed[7] and X_fixed select the modules swept as for
+ * realq_mlp_desc (module indices in the order above; X_fixed is h1 for q, k and v, O for o, u
+ * for gate and up, z for down). */
 typedef struct realq_decoder_block {
     const float* gamma1;
     const float* Wq;
@@ -435,6 +466,9 @@ typedef struct realq_decoder_desc {
     int32_t window;
     realq_qparams q;
     realq_bgd_params bgd;
+    int32_t start_module, n_modules;
+    const float* W_fixed[7];
+    const uint16_t* X_fixed;
 } realq_decoder_desc;
 
 typedef struct realq_decoder_out {

@@ -317,7 +317,8 @@ int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T
     if ((rc = get_ws(ctx, "c_D", (size_t)np * 64 * 8, &D))) return rc;
     if ((rc = get_ws(ctx, "c_F", 64, &F))) return rc;
     if ((rc = get_ws(ctx, "c_S", 64, &S))) return rc;
-    RQ_HIP(ctx, realq::fill_f64((double*)F, 0.0, 1, ctx->stream));  // flag word (int) cleared via a double fill
+    // two flag words (not positive definite; non-finite accumulator) cleared by one double fill
+    RQ_HIP(ctx, realq::fill_f64((double*)F, 0.0, 1, ctx->stream));
     realq::CholArgs c{};
     c.Hacc = H_acc;
     c.n = n;
@@ -336,10 +337,13 @@ int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T
         Timed tm(ctx, "chol");
         RQ_HIP(ctx, realq::chol_inverse(c, ctx->stream));
     }
-    int flag = 0;
-    RQ_HIP(ctx, hipMemcpyAsync(&flag, F, sizeof(int), hipMemcpyDeviceToHost, ctx->stream));
+    int flag[2] = {0, 0};
+    RQ_HIP(ctx, hipMemcpyAsync(flag, F, sizeof(flag), hipMemcpyDeviceToHost, ctx->stream));
     RQ_HIP(ctx, hipStreamSynchronize(ctx->stream));
-    if (flag) return set_error(ctx, REALQ_ERR_NOT_SPD, "chol_inverse: damped Hessian is not positive definite");
+    if (flag[1])
+        return set_error(ctx, REALQ_ERR_NONFINITE,
+                         "chol_inverse: the Hessian accumulator holds NaN or Inf (non-finite Xhat or s)");
+    if (flag[0]) return set_error(ctx, REALQ_ERR_NOT_SPD, "chol_inverse: damped Hessian is not positive definite");
     return REALQ_OK;
 }
 
@@ -1150,7 +1154,11 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
     float ms = 0.f;
     RQ_HIP(ctx, hipEventElapsedTime(&ms, ev.a, ev.b));
     out->ms_total = ms;
-    return realq::harvest(ctx);
+    if ((rc = realq::harvest(ctx))) return rc;
+    if (!std::isfinite(out->loss_final))
+        return set_error(ctx, REALQ_ERR_NONFINITE,
+                         "quantize_layer: the final loss is not finite (NaN or Inf in W0, X, s or the metric)");
+    return REALQ_OK;
 }
 
 }  // extern "C"

@@ -219,8 +219,15 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: incomplete next block");
     if (!(D->eps > 0.f) || !std::isfinite(D->eps))
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: eps must be finite and > 0");
-    for (int k = 0; k < 3; ++k)
-        if (!out->codes[k] || !out->scales[k] || !out->zeros[k] || !out->W_hat[k])
+    const int start = D->start_module;
+    if (start < 0 || start > 2 || D->n_modules < 0 || start + D->n_modules > 3)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: need 0 <= start_module <= 2, n_modules >= 0 "
+                                                     "and start_module + n_modules <= 3");
+    const int stop = D->n_modules == 0 ? 3 : start + D->n_modules;
+    for (int k = 0; k < start; ++k)
+        if (!D->W_fixed[k]) return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: NULL W_fixed before start_module");
+    for (int k = 0; k < stop; ++k)
+        if (!out->W_hat[k] || (k >= start && (!out->codes[k] || !out->scales[k] || !out->zeros[k])))
             return set_error(ctx, REALQ_ERR_INVALID_ARG, "mlp_block_sweep: NULL output array");
     const bool window = D->window != 0 && has_next;
     const double eps = (double)D->eps;
@@ -289,6 +296,14 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
         }
         // quantized path with the original weights: u (gate and up input), a and b
         if ((rc = forward(ctx, w0, D->Xhat, nullptr, T, d, f, eps, fq, nullptr, nullptr))) return rc;
+        if (D->X_fixed && start <= 1) {
+            // the gate and up input taken as given: the quantized path from u on
+            RQ_HIP(ctx, hipMemcpyAsync(fq.u, D->X_fixed, (size_t)T * d * 2, hipMemcpyDeviceToDevice, s));
+            if ((rc = lin_f32(ctx, w0.g, f, d, fq.u, T, fq.a)) || (rc = lin_f32(ctx, w0.u, f, d, fq.u, T, fq.b)))
+                return rc;
+            RQ_HIP(ctx, realq::swiglu_fwd(fq.a, fq.b, fq.z, T * f, s));
+            if ((rc = lin_bf16(ctx, w0.d, d, f, fq.z, T, fq.out))) return rc;
+        }
         RQ_HIP(ctx, realq::transpose_u16(fq.u, d, uT, T, T, d, s));
     }
 
@@ -337,80 +352,88 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
     };
 
     const float* Wq[3] = {nullptr, nullptr, nullptr};  // quantized weights of finished modules
-    for (int mod = 0; mod < 3; ++mod) {
+    for (int mod = 0; mod < stop; ++mod) {
         const int64_t m = rows[mod], n = cols[mod];
-        const uint16_t* inp = mod < 2 ? fq.u : fq.z;
-        // GPTQ operands from this module's input in the quantized path
-        RQ_HIP(ctx, realq::fill_f64(Hacc, 0.0, n * n, s));
-        if ((rc = realq_hessian_accum(ctx, inp, nullptr, T, n, Hacc))) return rc;
-        if ((rc = realq_chol_inverse(ctx, Hacc, n, T, D->q.damp, nullptr, Uf, dead))) return rc;
-        if (mod == 2) RQ_HIP(ctx, realq::transpose_u16(fq.z, f, zT, T, T, f, s));
-        RQ_HIP(ctx, realq::widen_f32(W0[mod], W, m * n, s));
-        RQ_HIP(ctx, realq::fill_f32(mA, 0.f, m * n, s));
-        RQ_HIP(ctx, realq::fill_f32(vA, 0.f, m * n, s));
-        int64_t t_adam = 0;
-        for (int64_t b = 0; b < nb[mod]; ++b) {
-            const int64_t c0 = b * blk, bs = std::min<int64_t>(blk, n - c0), c1 = c0 + bs;
-            if ((rc = realq_quantize_block(ctx, W, m, n, c0, bs, Uf, dead, &D->q, out->codes[mod], out->scales[mod],
-                                           out->zeros[mod], nullptr)))
-                return rc;
-            if (steps == 0 || c1 >= n) continue;
-            double alpha = 1.0;
-            if (window && B_total > 1) {
-                const double bg = (double)(off[mod] + b + 1);
-                alpha = std::min(1.0, std::max(0.0, 1.0 - (bg - 1.0) / (double)(B_total - 1)));
+        if (mod < start) {  // taken as already quantized
+            RQ_HIP(ctx, hipMemcpyAsync(out->W_hat[mod], D->W_fixed[mod], (size_t)m * n * 4, hipMemcpyDeviceToDevice, s));
+        } else {
+            if (D->X_fixed && mod == 2 && start == 2) {  // the down input taken as given
+                RQ_HIP(ctx, hipMemcpyAsync(fq.z, D->X_fixed, (size_t)T * f * 2, hipMemcpyDeviceToDevice, s));
+                if ((rc = lin_bf16(ctx, w0.d, d, f, fq.z, T, fq.out))) return rc;
             }
-            const int64_t nJ = n - c1;
-            for (int k = 0; k < steps; ++k) {
-                Timed tm(ctx, "block_step");
-                const TokenBatch tb = step_tokens(t_adam + 1, T, D->bgd.batch);
-                const int64_t Tb = tb.n;
-                const Fwd q = rows_of(fq, tb.t0, d, f);
-                // forward of the partially quantized block with this module's current weights
-                RQ_HIP(ctx, realq::split3_f64(W, sW.hi, sW.lo, sW.lo2, m * n, s));
-                if (mod == 0) {
-                    if ((rc = lin_f32(ctx, sW, f, d, q.u, Tb, q.a))) return rc;
-                } else if (mod == 1) {
-                    if ((rc = lin_f32(ctx, sW, f, d, q.u, Tb, q.b))) return rc;
+            const uint16_t* inp = mod < 2 ? fq.u : fq.z;
+            // GPTQ operands from this module's input in the quantized path
+            RQ_HIP(ctx, realq::fill_f64(Hacc, 0.0, n * n, s));
+            if ((rc = realq_hessian_accum(ctx, inp, nullptr, T, n, Hacc))) return rc;
+            if ((rc = realq_chol_inverse(ctx, Hacc, n, T, D->q.damp, nullptr, Uf, dead))) return rc;
+            if (mod == 2) RQ_HIP(ctx, realq::transpose_u16(fq.z, f, zT, T, T, f, s));
+            RQ_HIP(ctx, realq::widen_f32(W0[mod], W, m * n, s));
+            RQ_HIP(ctx, realq::fill_f32(mA, 0.f, m * n, s));
+            RQ_HIP(ctx, realq::fill_f32(vA, 0.f, m * n, s));
+            int64_t t_adam = 0;
+            for (int64_t b = 0; b < nb[mod]; ++b) {
+                const int64_t c0 = b * blk, bs = std::min<int64_t>(blk, n - c0), c1 = c0 + bs;
+                if ((rc = realq_quantize_block(ctx, W, m, n, c0, bs, Uf, dead, &D->q, out->codes[mod], out->scales[mod],
+                                               out->zeros[mod], nullptr)))
+                    return rc;
+                if (steps == 0 || c1 >= n) continue;
+                double alpha = 1.0;
+                if (window && B_total > 1) {
+                    const double bg = (double)(off[mod] + b + 1);
+                    alpha = std::min(1.0, std::max(0.0, 1.0 - (bg - 1.0) / (double)(B_total - 1)));
                 }
-                if (mod < 2) RQ_HIP(ctx, realq::swiglu_fwd(q.a, q.b, q.z, Tb * f, s));
-                if ((rc = lin_bf16(ctx, mod == 2 ? sW : w0.d, d, f, q.z, Tb, q.out))) return rc;
-                if ((rc = surrogate(alpha, tb.t0, Tb))) return rc;
-                if (out->loss_trace)
-                    RQ_HIP(ctx, hipMemcpyAsync(out->loss_trace + (off[mod] + b) * steps + k, lossd, 8,
-                                               hipMemcpyDeviceToDevice, s));
-                // gradient of this module's trailing columns over the step's tokens (the
-                // transposed inputs keep their stride T, the transposed output gradient has Tb)
-                if (mod < 2) {
-                    RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, sg.hi, sg.lo, Tb * d, s));
-                    if ((rc = prod3(ctx, sg, Tb, d, w0.dT, f, 1.f, dz))) return rc;  // dz = g Wd
-                    RQ_HIP(ctx, realq::swiglu_bwd(dz, q.a, q.b, mod, Tb, f, 1, svT.hi, svT.lo, Tb, s));
-                    realq::GemmArgs gg{svT.hi, svT.lo, Tb, uT + c1 * T + tb.t0, T, f, nJ, Tb, 1};
-                    RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
-                } else {
-                    RQ_HIP(ctx, realq::transpose_split_f32(g, d, sgT.hi, sgT.lo, Tb, Tb, d, s));
-                    realq::GemmArgs gg{sgT.hi, sgT.lo, Tb, zT + c1 * T + tb.t0, T, d, nJ, Tb, 1};
-                    RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
+                const int64_t nJ = n - c1;
+                for (int k = 0; k < steps; ++k) {
+                    Timed tm(ctx, "block_step");
+                    const TokenBatch tb = step_tokens(t_adam + 1, T, D->bgd.batch);
+                    const int64_t Tb = tb.n;
+                    const Fwd q = rows_of(fq, tb.t0, d, f);
+                    // forward of the partially quantized block with this module's current weights
+                    RQ_HIP(ctx, realq::split3_f64(W, sW.hi, sW.lo, sW.lo2, m * n, s));
+                    if (mod == 0) {
+                        if ((rc = lin_f32(ctx, sW, f, d, q.u, Tb, q.a))) return rc;
+                    } else if (mod == 1) {
+                        if ((rc = lin_f32(ctx, sW, f, d, q.u, Tb, q.b))) return rc;
+                    }
+                    if (mod < 2) RQ_HIP(ctx, realq::swiglu_fwd(q.a, q.b, q.z, Tb * f, s));
+                    if ((rc = lin_bf16(ctx, mod == 2 ? sW : w0.d, d, f, q.z, Tb, q.out))) return rc;
+                    if ((rc = surrogate(alpha, tb.t0, Tb))) return rc;
+                    if (out->loss_trace)
+                        RQ_HIP(ctx, hipMemcpyAsync(out->loss_trace + (off[mod] + b) * steps + k, lossd, 8,
+                                                   hipMemcpyDeviceToDevice, s));
+                    // gradient of this module's trailing columns over the step's tokens (the
+                    // transposed inputs keep their stride T, the transposed output gradient has Tb)
+                    if (mod < 2) {
+                        RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, sg.hi, sg.lo, Tb * d, s));
+                        if ((rc = prod3(ctx, sg, Tb, d, w0.dT, f, 1.f, dz))) return rc;  // dz = g Wd
+                        RQ_HIP(ctx, realq::swiglu_bwd(dz, q.a, q.b, mod, Tb, f, 1, svT.hi, svT.lo, Tb, s));
+                        realq::GemmArgs gg{svT.hi, svT.lo, Tb, uT + c1 * T + tb.t0, T, f, nJ, Tb, 1};
+                        RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
+                    } else {
+                        RQ_HIP(ctx, realq::transpose_split_f32(g, d, sgT.hi, sgT.lo, Tb, Tb, d, s));
+                        realq::GemmArgs gg{sgT.hi, sgT.lo, Tb, zT + c1 * T + tb.t0, T, d, nJ, Tb, 1};
+                        RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
+                    }
+                    ++t_adam;
+                    realq::AdamArgs a{};
+                    a.W = W;
+                    a.mA = mA;
+                    a.vA = vA;
+                    a.m = m;
+                    a.n = n;
+                    a.c1 = c1;
+                    a.lr = D->bgd.lr;
+                    a.beta1 = D->bgd.beta1;
+                    a.beta2 = D->bgd.beta2;
+                    a.eps = D->bgd.eps;
+                    a.bc1 = (float)(1.0 / (1.0 - std::pow((double)D->bgd.beta1, (double)t_adam)));
+                    a.bc2 = (float)(1.0 / (1.0 - std::pow((double)D->bgd.beta2, (double)t_adam)));
+                    a.gscale = 1.f;
+                    RQ_HIP(ctx, realq::adam_update_dense(a, G, s));
                 }
-                ++t_adam;
-                realq::AdamArgs a{};
-                a.W = W;
-                a.mA = mA;
-                a.vA = vA;
-                a.m = m;
-                a.n = n;
-                a.c1 = c1;
-                a.lr = D->bgd.lr;
-                a.beta1 = D->bgd.beta1;
-                a.beta2 = D->bgd.beta2;
-                a.eps = D->bgd.eps;
-                a.bc1 = (float)(1.0 / (1.0 - std::pow((double)D->bgd.beta1, (double)t_adam)));
-                a.bc2 = (float)(1.0 / (1.0 - std::pow((double)D->bgd.beta2, (double)t_adam)));
-                a.gscale = 1.f;
-                RQ_HIP(ctx, realq::adam_update_dense(a, G, s));
             }
+            RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat[mod], m * n, s));
         }
-        RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat[mod], m * n, s));
         Wq[mod] = out->W_hat[mod];
         // the quantized path with this module's final weights
         Split q;
@@ -703,8 +726,16 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
     if (has_next && (!N0.gamma1 || !N0.Wk || !N0.Wv || !N0.Wo || !N0.mlp.gamma || !N0.mlp.Wg || !N0.mlp.Wu ||
                      !N0.mlp.Wd))
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: incomplete next block");
-    for (int k = 0; k < 7; ++k)
-        if (!out->codes[k] || !out->scales[k] || !out->zeros[k] || !out->W_hat[k])
+    const int start = Dd->start_module;
+    if (start < 0 || start > 6 || Dd->n_modules < 0 || start + Dd->n_modules > 7)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: need 0 <= start_module <= 6, n_modules >= 0 "
+                                                     "and start_module + n_modules <= 7");
+    const int stop = Dd->n_modules == 0 ? 7 : start + Dd->n_modules;
+    for (int k = 0; k < start; ++k)
+        if (!Dd->W_fixed[k])
+            return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: NULL W_fixed before start_module");
+    for (int k = 0; k < stop; ++k)
+        if (!out->W_hat[k] || (k >= start && (!out->codes[k] || !out->scales[k] || !out->zeros[k])))
             return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: NULL output array");
     const bool window = Dd->window != 0 && has_next;
     const int64_t T = D.T, d = D.d, f = D.f;
@@ -830,100 +861,124 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
         return lin_bf16(ctx, wq.mlp.d, d, f, q.mlp.z, Tb, q.mlp.out);
     };
 
-    for (int mod = 0; mod < 7; ++mod) {
+    for (int mod = 0; mod < stop; ++mod) {
         const int64_t m = rows[mod], n = cols[mod];
-        const uint16_t* inp = mod <= 2 ? Fq.h1 : (mod == 3 ? Fq.O : (mod <= 5 ? Fq.mlp.u : Fq.mlp.z));
-        RQ_HIP(ctx, realq::fill_f64(Hacc, 0.0, n * n, s));
-        if ((rc = realq_hessian_accum(ctx, inp, nullptr, T, n, Hacc))) return rc;
-        if ((rc = realq_chol_inverse(ctx, Hacc, n, T, Dd->q.damp, nullptr, Uf, dead))) return rc;
-        const uint16_t* inT = h1T;
-        if (mod == 3) {
-            RQ_HIP(ctx, realq::transpose_u16(Fq.O, D.Hq, OT, T, T, D.Hq, s));
-            inT = OT;
-        } else if (mod == 4 || mod == 5) {
-            if (mod == 4) RQ_HIP(ctx, realq::transpose_u16(Fq.mlp.u, d, uT, T, T, d, s));
-            inT = uT;
-        } else if (mod == 6) {
-            RQ_HIP(ctx, realq::transpose_u16(Fq.mlp.z, f, zT, T, T, f, s));
-            inT = zT;
-        }
-        RQ_HIP(ctx, realq::widen_f32(W0[mod], W, m * n, s));
-        RQ_HIP(ctx, realq::fill_f32(mA, 0.f, m * n, s));
-        RQ_HIP(ctx, realq::fill_f32(vA, 0.f, m * n, s));
-        int64_t t_adam = 0;
-        for (int64_t b = 0; b < nb[mod]; ++b) {
-            const int64_t c0 = b * blk, bs = std::min<int64_t>(blk, n - c0), c1 = c0 + bs;
-            if ((rc = realq_quantize_block(ctx, W, m, n, c0, bs, Uf, dead, &Dd->q, out->codes[mod], out->scales[mod],
-                                           out->zeros[mod], nullptr)))
-                return rc;
-            if (steps == 0 || c1 >= n) continue;
-            double alpha = 1.0;
-            if (window && B_total > 1) {
-                const double bg = (double)(off[mod] + b + 1);
-                alpha = std::min(1.0, std::max(0.0, 1.0 - (bg - 1.0) / (double)(B_total - 1)));
-            }
-            const int64_t nJ = n - c1;
-            for (int k = 0; k < steps; ++k) {
-                Timed tm(ctx, "block_step");
-                const TokenBatch tb = step_tokens(t_adam + 1, T, Dd->bgd.batch);
-                const int64_t Tb = tb.n;
-                const DecF q = rows_of(Fq, D, tb.t0);
-                DecDims Db = D;
-                Db.T = Tb;
-                fwd_slot[mod]->lo_zero = false;
-                RQ_HIP(ctx, realq::split3_f64(W, fwd_slot[mod]->hi, fwd_slot[mod]->lo, fwd_slot[mod]->lo2, m * n, s));
-                if ((rc = refresh(mod, tb.t0, Tb)) || (rc = surrogate(alpha, tb.t0, Tb))) return rc;
-                if (out->loss_trace)
-                    RQ_HIP(ctx, hipMemcpyAsync(out->loss_trace + (off[mod] + b) * steps + k, lossd, 8,
-                                               hipMemcpyDeviceToDevice, s));
-                // gradient of this module's trailing columns over the step's tokens:
-                // (dL/d output)^T input[:, J] (the transposed input keeps its stride T)
-                const float* gout = nullptr;
-                int64_t gw = 0;
-                if (mod == 6) {
-                    gout = g;
-                    gw = d;
-                } else if (mod >= 4) {
-                    RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, Wk.sg.hi, Wk.sg.lo, Tb * d, s));
-                    if ((rc = prod3(ctx, Wk.sg, Tb, d, wq.mlp.dT, f, 1.f, Wk.dz))) return rc;
-                    RQ_HIP(ctx, realq::swiglu_bwd(Wk.dz, q.mlp.a, q.mlp.b, mod - 4, Tb, f, 1, svT.hi, svT.lo, Tb, s));
+        if (mod < start) {  // taken as already quantized
+            RQ_HIP(ctx, hipMemcpyAsync(out->W_hat[mod], Dd->W_fixed[mod], (size_t)m * n * 4, hipMemcpyDeviceToDevice,
+                                       s));
+        } else {
+            if (Dd->X_fixed && mod == start) {
+                // this module's input taken as given; the quantized path recomputed from it on
+                if (mod <= 2) {
+                    RQ_HIP(ctx, hipMemcpyAsync(Fq.h1, Dd->X_fixed, (size_t)T * d * 2, hipMemcpyDeviceToDevice, s));
+                    RQ_HIP(ctx, realq::transpose_u16(Fq.h1, d, h1T, T, T, d, s));
+                    if ((rc = dec_attn(ctx, wq, Dd->Xhat, nullptr, D, Fq, 7, false))) return rc;
+                    if ((rc = refresh(3, 0, T))) return rc;
+                } else if (mod == 3) {
+                    RQ_HIP(ctx, hipMemcpyAsync(Fq.O, Dd->X_fixed, (size_t)T * D.Hq * 2, hipMemcpyDeviceToDevice, s));
+                    if ((rc = refresh(3, 0, T))) return rc;
+                } else if (mod <= 5) {
+                    RQ_HIP(ctx, hipMemcpyAsync(Fq.mlp.u, Dd->X_fixed, (size_t)T * d * 2, hipMemcpyDeviceToDevice, s));
+                    if ((rc = lin_f32(ctx, wq.mlp.u, f, d, Fq.mlp.u, T, Fq.mlp.b))) return rc;
+                    if ((rc = refresh(4, 0, T))) return rc;
                 } else {
-                    if ((rc = back_to_x2(ctx, wq, Db, q, g, Wk))) return rc;
-                    if (mod == 3) {
-                        gout = Wk.dx2;
-                        gw = d;
-                    } else {
-                        if ((rc = back_to_qkv(ctx, wq, Db, q, Wk))) return rc;
-                        gout = mod == 0 ? Wk.dq : (mod == 1 ? Wk.dk : Wk.dv);
-                        gw = mod == 0 ? D.Hq : D.Hk;
-                    }
+                    RQ_HIP(ctx, hipMemcpyAsync(Fq.mlp.z, Dd->X_fixed, (size_t)T * f * 2, hipMemcpyDeviceToDevice, s));
+                    if ((rc = refresh(6, 0, T))) return rc;
                 }
-                const Split* A = &svT;
-                if (gout) {
-                    RQ_HIP(ctx, realq::transpose_split_f32(gout, gw, sgT.hi, sgT.lo, Tb, Tb, gw, s));
-                    A = &sgT;
-                }
-                realq::GemmArgs gg{A->hi, A->lo, Tb, inT + c1 * T + tb.t0, T, m, nJ, Tb, 1};
-                RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
-                ++t_adam;
-                realq::AdamArgs a{};
-                a.W = W;
-                a.mA = mA;
-                a.vA = vA;
-                a.m = m;
-                a.n = n;
-                a.c1 = c1;
-                a.lr = Dd->bgd.lr;
-                a.beta1 = Dd->bgd.beta1;
-                a.beta2 = Dd->bgd.beta2;
-                a.eps = Dd->bgd.eps;
-                a.bc1 = (float)(1.0 / (1.0 - std::pow((double)Dd->bgd.beta1, (double)t_adam)));
-                a.bc2 = (float)(1.0 / (1.0 - std::pow((double)Dd->bgd.beta2, (double)t_adam)));
-                a.gscale = 1.f;
-                RQ_HIP(ctx, realq::adam_update_dense(a, G, s));
             }
+            const uint16_t* inp = mod <= 2 ? Fq.h1 : (mod == 3 ? Fq.O : (mod <= 5 ? Fq.mlp.u : Fq.mlp.z));
+            RQ_HIP(ctx, realq::fill_f64(Hacc, 0.0, n * n, s));
+            if ((rc = realq_hessian_accum(ctx, inp, nullptr, T, n, Hacc))) return rc;
+            if ((rc = realq_chol_inverse(ctx, Hacc, n, T, Dd->q.damp, nullptr, Uf, dead))) return rc;
+            const uint16_t* inT = h1T;
+            if (mod == 3) {
+                RQ_HIP(ctx, realq::transpose_u16(Fq.O, D.Hq, OT, T, T, D.Hq, s));
+                inT = OT;
+            } else if (mod == 4 || mod == 5) {
+                if (mod == 4 || start == 5) RQ_HIP(ctx, realq::transpose_u16(Fq.mlp.u, d, uT, T, T, d, s));
+                inT = uT;
+            } else if (mod == 6) {
+                RQ_HIP(ctx, realq::transpose_u16(Fq.mlp.z, f, zT, T, T, f, s));
+                inT = zT;
+            }
+            RQ_HIP(ctx, realq::widen_f32(W0[mod], W, m * n, s));
+            RQ_HIP(ctx, realq::fill_f32(mA, 0.f, m * n, s));
+            RQ_HIP(ctx, realq::fill_f32(vA, 0.f, m * n, s));
+            int64_t t_adam = 0;
+            for (int64_t b = 0; b < nb[mod]; ++b) {
+                const int64_t c0 = b * blk, bs = std::min<int64_t>(blk, n - c0), c1 = c0 + bs;
+                if ((rc = realq_quantize_block(ctx, W, m, n, c0, bs, Uf, dead, &Dd->q, out->codes[mod], out->scales[mod],
+                                               out->zeros[mod], nullptr)))
+                    return rc;
+                if (steps == 0 || c1 >= n) continue;
+                double alpha = 1.0;
+                if (window && B_total > 1) {
+                    const double bg = (double)(off[mod] + b + 1);
+                    alpha = std::min(1.0, std::max(0.0, 1.0 - (bg - 1.0) / (double)(B_total - 1)));
+                }
+                const int64_t nJ = n - c1;
+                for (int k = 0; k < steps; ++k) {
+                    Timed tm(ctx, "block_step");
+                    const TokenBatch tb = step_tokens(t_adam + 1, T, Dd->bgd.batch);
+                    const int64_t Tb = tb.n;
+                    const DecF q = rows_of(Fq, D, tb.t0);
+                    DecDims Db = D;
+                    Db.T = Tb;
+                    fwd_slot[mod]->lo_zero = false;
+                    RQ_HIP(ctx, realq::split3_f64(W, fwd_slot[mod]->hi, fwd_slot[mod]->lo, fwd_slot[mod]->lo2, m * n, s));
+                    if ((rc = refresh(mod, tb.t0, Tb)) || (rc = surrogate(alpha, tb.t0, Tb))) return rc;
+                    if (out->loss_trace)
+                        RQ_HIP(ctx, hipMemcpyAsync(out->loss_trace + (off[mod] + b) * steps + k, lossd, 8,
+                                                   hipMemcpyDeviceToDevice, s));
+                    // gradient of this module's trailing columns over the step's tokens:
+                    // (dL/d output)^T input[:, J] (the transposed input keeps its stride T)
+                    const float* gout = nullptr;
+                    int64_t gw = 0;
+                    if (mod == 6) {
+                        gout = g;
+                        gw = d;
+                    } else if (mod >= 4) {
+                        RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, Wk.sg.hi, Wk.sg.lo, Tb * d, s));
+                        if ((rc = prod3(ctx, Wk.sg, Tb, d, wq.mlp.dT, f, 1.f, Wk.dz))) return rc;
+                        RQ_HIP(ctx, realq::swiglu_bwd(Wk.dz, q.mlp.a, q.mlp.b, mod - 4, Tb, f, 1, svT.hi, svT.lo, Tb, s));
+                    } else {
+                        if ((rc = back_to_x2(ctx, wq, Db, q, g, Wk))) return rc;
+                        if (mod == 3) {
+                            gout = Wk.dx2;
+                            gw = d;
+                        } else {
+                            if ((rc = back_to_qkv(ctx, wq, Db, q, Wk))) return rc;
+                            gout = mod == 0 ? Wk.dq : (mod == 1 ? Wk.dk : Wk.dv);
+                            gw = mod == 0 ? D.Hq : D.Hk;
+                        }
+                    }
+                    const Split* A = &svT;
+                    if (gout) {
+                        RQ_HIP(ctx, realq::transpose_split_f32(gout, gw, sgT.hi, sgT.lo, Tb, Tb, gw, s));
+                        A = &sgT;
+                    }
+                    realq::GemmArgs gg{A->hi, A->lo, Tb, inT + c1 * T + tb.t0, T, m, nJ, Tb, 1};
+                    RQ_HIP(ctx, realq::gemm_store_f32(gg, G, nJ, 0, 1.f, s));
+                    ++t_adam;
+                    realq::AdamArgs a{};
+                    a.W = W;
+                    a.mA = mA;
+                    a.vA = vA;
+                    a.m = m;
+                    a.n = n;
+                    a.c1 = c1;
+                    a.lr = Dd->bgd.lr;
+                    a.beta1 = Dd->bgd.beta1;
+                    a.beta2 = Dd->bgd.beta2;
+                    a.eps = Dd->bgd.eps;
+                    a.bc1 = (float)(1.0 / (1.0 - std::pow((double)Dd->bgd.beta1, (double)t_adam)));
+                    a.bc2 = (float)(1.0 / (1.0 - std::pow((double)Dd->bgd.beta2, (double)t_adam)));
+                    a.gscale = 1.f;
+                    RQ_HIP(ctx, realq::adam_update_dense(a, G, s));
+                }
+            }
+            RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat[mod], m * n, s));
         }
-        RQ_HIP(ctx, realq::narrow_f64(W, out->W_hat[mod], m * n, s));
         fwd_slot[mod]->lo_zero = false;
         RQ_HIP(ctx, realq::split3_f32(out->W_hat[mod], n, fwd_slot[mod]->hi, fwd_slot[mod]->lo, fwd_slot[mod]->lo2, n,
                                       m, n, s));

@@ -86,8 +86,11 @@ __global__ __launch_bounds__(256) void chol_diag_kernel(const double* __restrict
     if (threadIdx.x == 0) scratch[0] = damp * (red[0] / (double)n);
 }
 
+// A = the index-reversed damped Hessian (padded with the identity); nonfinite[0] = 1 when an entry
+// of the accumulator is NaN or infinite (a non-finite input reached the Hessian).
 __global__ void chol_fill_kernel(const double* __restrict__ Hacc, int64_t n, int64_t np, double scale,
-                                 const double* __restrict__ scratch, double* __restrict__ A, float* Hout) {
+                                 const double* __restrict__ scratch, double* __restrict__ A, float* Hout,
+                                 int* nonfinite) {
     const double lam = scratch[0];
     const int64_t total = np * np;
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
@@ -96,6 +99,7 @@ __global__ void chol_fill_kernel(const double* __restrict__ Hacc, int64_t n, int
         if (r < n && c < n) {
             const int64_t hr = n - 1 - r, hc = n - 1 - c;
             double h = scale * Hacc[hr * n + hc];
+            if (!isfinite(h)) *nonfinite = 1;
             if (Hout) Hout[hr * n + hc] = (float)h;
             if (hr == hc) v = (h == 0.0 ? 1.0 : h) + lam;
             else v = h;
@@ -256,7 +260,7 @@ hipError_t chol_inverse(const CholArgs& c, hipStream_t st) {
     };
     hipLaunchKernelGGL(chol_diag_kernel, dim3(1), dim3(256), 0, st, c.Hacc, n, c.scale, c.damp, c.dead, c.scratch);
     hipLaunchKernelGGL(chol_fill_kernel, dim3(grid_of(np * np)), dim3(256), 0, st, c.Hacc, n, np, c.scale, c.scratch,
-                       c.A, c.Hout);
+                       c.A, c.Hout, c.flag + 1);
     hipLaunchKernelGGL(chol_zero_kernel, dim3(grid_of(np * np)), dim3(256), 0, st, c.Linv, np * np);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

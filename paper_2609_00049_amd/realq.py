@@ -37,7 +37,7 @@ EXPORTS = [
     "realq_quantize_block", "realq_quantize_block_rows", "realq_bgd_lock_block",
     "realq_bgd_step", "realq_bgd_loss", "realq_quantize_layer",
     "realq_pullback_metric", "realq_handoff", "realq_mlp_block_sweep",
-    "realq_decoder_block_sweep", "realq_decoder_forward",
+    "realq_decoder_block_sweep", "realq_decoder_forward", "realq_mfma_peak",
 ]
 
 
@@ -88,7 +88,9 @@ class MLPBlock(ctypes.Structure):
 class MLPDesc(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int64), ("d", ctypes.c_int64), ("f", ctypes.c_int64),
                 ("X", ctypes.c_void_p), ("Xhat", ctypes.c_void_p), ("blk", MLPBlock), ("next", MLPBlock),
-                ("eps", ctypes.c_float), ("window", ctypes.c_int32), ("q", QParams), ("bgd", BgdParams)]
+                ("eps", ctypes.c_float), ("window", ctypes.c_int32), ("q", QParams), ("bgd", BgdParams),
+                ("start_module", ctypes.c_int32), ("n_modules", ctypes.c_int32), ("W_fixed", ctypes.c_void_p * 3),
+                ("X_fixed", ctypes.c_void_p)]
 
 
 class MLPOut(ctypes.Structure):
@@ -107,7 +109,9 @@ class DecoderDesc(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("n_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("rope_base", ctypes.c_float), ("eps", ctypes.c_float),
                 ("X", ctypes.c_void_p), ("Xhat", ctypes.c_void_p), ("blk", DecoderBlock), ("next", DecoderBlock),
-                ("window", ctypes.c_int32), ("q", QParams), ("bgd", BgdParams)]
+                ("window", ctypes.c_int32), ("q", QParams), ("bgd", BgdParams),
+                ("start_module", ctypes.c_int32), ("n_modules", ctypes.c_int32), ("W_fixed", ctypes.c_void_p * 7),
+                ("X_fixed", ctypes.c_void_p)]
 
 
 class DecoderOut(ctypes.Structure):
@@ -158,6 +162,7 @@ def _load():
         "realq_mlp_block_sweep": (ctypes.c_int, [vp, ctypes.POINTER(MLPDesc), ctypes.POINTER(MLPOut)]),
         "realq_decoder_block_sweep": (ctypes.c_int, [vp, ctypes.POINTER(DecoderDesc), ctypes.POINTER(DecoderOut)]),
         "realq_decoder_forward": (ctypes.c_int, [vp, ctypes.POINTER(DecoderDesc), ctypes.POINTER(DecoderFwdOut)]),
+        "realq_mfma_peak": (ctypes.c_int, [vp, i64, ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -261,6 +266,13 @@ class Context:
 
 
 # ----------------------------------------------------------------------------- the calls
+
+def mfma_peak(ctx: Context, iters: int = 1 << 16) -> float:
+    """TFLOP/s of the register-resident bf16 MFMA loop (the achievable MFMA ceiling of this GPU)."""
+    v = ctypes.c_double()
+    ctx.check(_lib.realq_mfma_peak(ctx.h, iters, ctypes.byref(v)))
+    return v.value
+
 
 def row_groups(m: int, n_groups: int):
     """(r0, r1) of the row groups that hold rows: contiguous ranges of ceil(m / n_groups) rows."""
@@ -481,11 +493,32 @@ def _mlp_block(gamma, Wg, Wu, Wd, F=None, *, d=None, f=None) -> MLPBlock:
                     _t(Wd, "Wd", F32, (d, f)), _t(F, "F", F32, (d, d), True))
 
 
+def _fixed(names, shapes, start, n_modules, fixed):
+    """start_module / n_modules / W_fixed of a block sweep: the quantized weights of the modules
+    before ``start`` (dict name -> float32 tensor), shape-checked."""
+    if not 0 <= start < len(names) or n_modules < 0 or start + n_modules > len(names):
+        raise ValueError(f"need 0 <= start < {len(names)}, n_modules >= 0, start + n_modules <= {len(names)}")
+    fixed = fixed or {}
+    ptrs = []
+    for k, name in enumerate(names):
+        if k < start:
+            if name not in fixed:
+                raise ValueError(f"fixed weights of {name} are required (it comes before start)")
+            ptrs.append(_t(fixed[name], f"fixed[{name}]", F32, shapes[k]))
+        else:
+            ptrs.append(None)
+    return (ctypes.c_void_p * len(names))(*ptrs)
+
+
 def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, *, eps=1e-6, window=False,
-                    qp: Optional[QParams] = None, bgd: Optional[BgdParams] = None, want_trace=True) -> BlockResult:
+                    qp: Optional[QParams] = None, bgd: Optional[BgdParams] = None, want_trace=True,
+                    start=0, n_modules=0, fixed=None, x_fixed=None) -> BlockResult:
     """Quantize gate, up and down of one pre-norm SwiGLU MLP block with Block-GD on the block-output
     surrogate.  X, Xhat [T, d] bf16; gamma [d]; Wg, Wu [f, d]; Wd [d, f]; F [d, d] or None;
-    nxt = (gamma, Wg, Wu, Wd, F) of the next block or None."""
+    nxt = (gamma, Wg, Wu, Wd, F) of the next block or None.  ``start`` / ``n_modules``: sweep only
+    modules start .. start + n_modules - 1 (0: through the last), the earlier ones taken as already
+    quantized with weights ``fixed[name]``; ``x_fixed`` [T, cols] bf16: the start module's input
+    (u for gate and up, z for down) taken as given."""
     qp = qp or qparams()
     bgd = bgd or bgd_params()
     T, d = _dims(X, "X", 2)
@@ -502,8 +535,10 @@ def mlp_block_sweep(ctx: Context, X, Xhat, gamma, Wg, Wu, Wd, F=None, nxt=None, 
                                  H=None, U=None, dead=None, loss_trace=None, loss_final=math.nan, ms_total=math.nan)
     trace = torch.empty((max(1, sum(nb) * bgd.steps),), dtype=torch.float64, device=dev) if want_trace else None
     nx = _mlp_block(*nxt, d=d) if nxt is not None else MLPBlock()
+    fx = _fixed(MLP_MODULES, ((f, d), (f, d), (d, f)), start, n_modules, fixed)
     desc = MLPDesc(T, d, f, _t(X, "X", BF16, (T, d)), _t(Xhat, "Xhat", BF16, (T, d)),
-                   _mlp_block(gamma, Wg, Wu, Wd, F, d=d, f=f), nx, eps, int(bool(window)), qp, bgd)
+                   _mlp_block(gamma, Wg, Wu, Wd, F, d=d, f=f), nx, eps, int(bool(window)), qp, bgd,
+                   start, n_modules, fx, _t(x_fixed, "x_fixed", BF16, (T, (d, d, f)[start]), True))
     o = MLPOut()
     for k, name in enumerate(MLP_MODULES):
         o.codes[k] = _ptr(mods[name].codes)
@@ -528,12 +563,16 @@ def _decoder_block(w: dict, d: int, Hq: int, Hk: int) -> DecoderBlock:
 
 def decoder_block_sweep(ctx: Context, X, Xhat, blk: dict, nxt: Optional[dict] = None, *, n_heads, n_kv, head_dim,
                         seq_len, rope_base=10000.0, eps=1e-6, window=False, qp: Optional[QParams] = None,
-                        bgd: Optional[BgdParams] = None, want_trace=True) -> BlockResult:
+                        bgd: Optional[BgdParams] = None, want_trace=True, start=0, n_modules=0,
+                        fixed=None, x_fixed=None) -> BlockResult:
     """Quantize q, k, v, o, gate, up and down of one pre-norm decoder block (rotary causal
     attention with grouped key/value heads, then a SwiGLU MLP) with Block-GD on the block-output
     surrogate.  X, Xhat [T, d] bf16; blk and nxt are dicts of float32 device tensors with keys
     gamma1 [d], Wq [H hd, d], Wk and Wv [Hkv hd, d], Wo [d, H hd], gamma2 [d], Wg and Wu [f, d],
-    Wd [d, f] and optionally F [d, d]; nxt is the next block (window partner) or None."""
+    Wd [d, f] and optionally F [d, d]; nxt is the next block (window partner) or None.
+    ``start`` / ``n_modules`` / ``fixed`` / ``x_fixed`` as for mlp_block_sweep (module order q, k, v,
+    o, gate, up, down; x_fixed is h1 [T, d] for q, k, v, O [T, H hd] for o, u [T, d] for gate and
+    up, z [T, f] for down)."""
     qp = qp or qparams()
     bgd = bgd or bgd_params()
     T, d = _dims(X, "X", 2)
@@ -552,8 +591,10 @@ def decoder_block_sweep(ctx: Context, X, Xhat, blk: dict, nxt: Optional[dict] = 
                                  H=None, U=None, dead=None, loss_trace=None, loss_final=math.nan, ms_total=math.nan)
     trace = torch.empty((max(1, sum(nb) * bgd.steps),), dtype=torch.float64, device=dev) if want_trace else None
     nx = _decoder_block(nxt, d, Hq, Hk) if nxt is not None else DecoderBlock()
+    fx = _fixed(DECODER_MODULES, shapes, start, n_modules, fixed)
     desc = DecoderDesc(T, d, f, seq_len, n_heads, n_kv, head_dim, rope_base, eps, _t(X, "X", BF16, (T, d)),
-                       _t(Xhat, "Xhat", BF16, (T, d)), _decoder_block(blk, d, Hq, Hk), nx, int(bool(window)), qp, bgd)
+                       _t(Xhat, "Xhat", BF16, (T, d)), _decoder_block(blk, d, Hq, Hk), nx, int(bool(window)), qp, bgd,
+                       start, n_modules, fx, _t(x_fixed, "x_fixed", BF16, (T, (d, d, d, Hq, d, d, f)[start]), True))
     o = DecoderOut()
     for k, name in enumerate(DECODER_MODULES):
         o.codes[k] = _ptr(mods[name].codes)

@@ -151,6 +151,19 @@ def test_decoder_forward_matches_oracle(rq, ctx, seed, which):
         assert rel <= 2e-5, name
 
 
+def _blk_for(blk, n_heads, n_kv, head_dim, **_):
+    """The block's tensors with the attention weights re-shaped (zero) to the given head layout, so
+    that the binding's shape checks pass and the library's own checks decide."""
+    torch = _torch()
+    d = blk["Wq"].shape[1]
+    out = dict(blk)
+    out["Wq"] = torch.zeros((n_heads * head_dim, d), device="cuda")
+    out["Wk"] = torch.zeros((n_kv * head_dim, d), device="cuda")
+    out["Wv"] = torch.zeros((n_kv * head_dim, d), device="cuda")
+    out["Wo"] = torch.zeros((d, n_heads * head_dim), device="cuda")
+    return out
+
+
 def test_decoder_forward_rejects_bad_arguments(rq, ctx):
     torch = _torch()
     inp = _inputs(5, T=128)
@@ -158,8 +171,10 @@ def test_decoder_forward_rejects_bad_arguments(rq, ctx):
     for kw in (dict(seq_len=48), dict(seq_len=16), dict(n_kv=3), dict(head_dim=63), dict(head_dim=48)):
         args = dict(dict(n_heads=4, n_kv=2, head_dim=64, seq_len=64), **kw)
         with pytest.raises(rq.RealqError) as ei:
-            rq.decoder_forward(ctx, X, blk, **args)
+            rq.decoder_forward(ctx, X, _blk_for(blk, **args), **args)
         assert ei.value.code == -2, kw
+    with pytest.raises(ValueError):           # weights that do not match the head layout
+        rq.decoder_forward(ctx, X, blk, n_heads=4, n_kv=3, head_dim=64, seq_len=64)
     with pytest.raises(rq.RealqError) as ei:
         rq.decoder_forward(ctx, X, blk, n_heads=4, n_kv=2, head_dim=64, seq_len=64, eps=0.0)
     assert ei.value.code == -1
@@ -212,7 +227,7 @@ def test_decoder_sweep_rejects_bad_arguments(rq, ctx):
                dict(head_dim=48)):
         args = dict(base, **kw)
         with pytest.raises(rq.RealqError) as ei:
-            rq.decoder_block_sweep(ctx, X, Xh, blk, **args)
+            rq.decoder_block_sweep(ctx, X, Xh, _blk_for(blk, **args), **args)
         assert ei.value.code == -2, kw
     for bgd in (rq.bgd_params(steps=1, loss_clip=0.9), rq.bgd_params(steps=1, form=rq.BGD_GRAM)):
         with pytest.raises(rq.RealqError) as ei:

@@ -468,3 +468,28 @@ def test_layer_llama_gate_shape_sampled_rows(rq, ctx):
     _assert_parity(P.compare(g, o, rows=rows))
     lg = P.row_loss(g.W_hat.cpu().numpy()[rows], L.W0[rows], L.X, L.Xhat)
     assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
+
+
+# ============================================================================ failure detection
+
+@pytest.mark.parametrize("where", ["Xhat", "W0"])
+def test_non_finite_input_is_reported(rq, ctx, where):
+    """A NaN in the calibration input reaches the Hessian and is reported by the inverse factor;
+    a NaN in the weights reaches the final loss.  Both return REALQ_ERR_NONFINITE (an error
+    return: NaN values only flow through the arithmetic, no index depends on them)."""
+    torch = _torch()
+    L = synth.make_module("single_512", m=16, n=256, T=128)
+    _banner(f"non-finite {where}")
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    if where == "Xhat":
+        Xh[5, 17] = float("nan")
+    else:
+        W0[3, 200] = float("inf")
+    with pytest.raises(rq.RealqError) as ei:
+        rq.quantize_layer(ctx, W0, X, Xh, s, qp=rq.qparams(), bgd=rq.bgd_params(steps=1, lr=1e-3))
+    assert ei.value.code == -6, str(ei.value)
+    torch.cuda.synchronize()
+    # the context stays usable
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    r = rq.quantize_layer(ctx, W0, X, Xh, s, qp=rq.qparams())
+    assert math.isfinite(r.loss_final)
