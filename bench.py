@@ -64,9 +64,13 @@ def make_inputs(torch, wl, seed=0):
         W0 = W0.to(torch.bfloat16).float()
     spec = c["x"]
     if spec[0] == "student_t":
+        # Student-t with integer nu: z / sqrt(chi2_nu / nu), chi2_nu a sum of nu squared normals, all
+        # drawn from the seeded generator so the inputs do not depend on earlier random draws
+        nu = int(spec[1])
+        assert nu == spec[1], "integer degrees of freedom"
         z = torch.randn((T, n), generator=g, device="cuda")
-        chi = torch.distributions.Chi2(torch.tensor(float(spec[1]), device="cuda")).sample((T, 1))
-        X32 = z * torch.sqrt(spec[1] / chi)
+        chi = (torch.randn((T, nu), generator=g, device="cuda") ** 2).sum(dim=1, keepdim=True)
+        X32 = z * torch.sqrt(nu / chi)
     else:
         X32 = torch.randn((T, n), generator=g, device="cuda")
         k = int(spec[1]) if spec[0] == "outlier_count" else max(1, int(round(spec[1] * n)))

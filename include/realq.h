@@ -118,7 +118,8 @@ const char* realq_last_error(const realq_ctx* ctx);
  * matrices of the input perturbation), "gram_step" (the per-step product of the
  * Gram form), "dense_loss" (final loss with a dense metric), "saliency", "block_init" and
  * "block_step" (the block sweeps: the fixed forwards, one Block-GD step) and "attention"
- * (realq_decoder_block_sweep: each attention forward or backward with its rotary embeddings).
+ * (realq_decoder_block_sweep: each attention forward or backward with its rotary embeddings),
+ * "metric" (the dense-metric product of a Block-GD step).
  * Returns REALQ_ERR_INVALID_ARG for an unknown name. */
 int realq_ctx_set_timing(realq_ctx* ctx, int enable);
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms);

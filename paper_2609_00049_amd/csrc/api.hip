@@ -103,6 +103,10 @@ struct realq_bgd_state {
     float* C0 = nullptr;      // [m,n] W0 Delta^T S Xhat
     float* Pm = nullptr;      // [m,n] D Xhat^T S Xhat (per step)
     double* cconst = nullptr; // <W0 Delta^T S Delta, W0> (device scalar)
+    // blended metric alpha M + (1 - alpha) P as a bf16 pair [m,m], formed once per alpha
+    uint16_t* Mah = nullptr;
+    uint16_t* Mal = nullptr;
+    float Ma_alpha = -1.f;
     std::vector<void*> allocations;
 };
 
@@ -173,7 +177,7 @@ int realq_ctx_set_timing(realq_ctx* ctx, int enable) {
 
 static const char* kTimedNames[] = {"hessian", "chol",  "quantize",  "obs",        "lock",      "resid",
                                     "grad",    "adam",  "init",      "gram",       "gram_step", "dense_loss",
-                                    "saliency", "block_init", "block_step", "attention"};
+                                    "saliency", "block_init", "block_step", "attention", "metric"};
 
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms) {
     if (!ctx || !name) return REALQ_ERR_INVALID_ARG;
@@ -852,47 +856,46 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     a.eps = st->prm.eps;
     a.bc1 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta1, (double)st->t)));
     a.bc2 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta2, (double)st->t)));
-    Timed tm(ctx, "adam");
     if (!dense && nchunks == 1 && !st->gram) {
+        Timed tm(ctx, "adam");
         RQ_HIP(ctx, realq::adam_update(a, s));
     } else if (!dense) {
         a.Gp = (const float*)Gacc;
         a.splits = 1;
+        Timed tm(ctx, "adam");
         RQ_HIP(ctx, realq::adam_update(a, s));
     } else {
-        // G = (1/T) (alpha M + (1 - alpha) P) Gacc
-        void* Gm;
+        // G = (1/T) M_a Gacc with M_a = alpha M + (1 - alpha) P (M = I when absent; Eq. slide_window),
+        // on the matrix cores: M_a as a bf16 pair formed once per alpha (one per column block),
+        // Gacc transposed and split; hi*hi + lo*hi in one launch, hi*lo accumulated in a second
+        // (the lo*lo term is below float32 rounding of the product).
+        if (!st->Mah) {
+            void* p;
+            if ((rc = state_alloc(st, &p, (size_t)m * m * 2, "s_Mah"))) return rc;
+            st->Mah = (uint16_t*)p;
+            if ((rc = state_alloc(st, &p, (size_t)m * m * 2, "s_Mal"))) return rc;
+            st->Mal = (uint16_t*)p;
+            st->Ma_alpha = -1.f;
+        }
+        if (st->Ma_alpha != alpha) {
+            RQ_HIP(ctx, realq::blend_split(st->M, alpha < 1.f ? st->P : nullptr, alpha, m, st->Mah, st->Mal, s));
+            st->Ma_alpha = alpha;
+        }
+        void *Gm, *gth, *gtl;
         if ((rc = get_ws(ctx, "b_Gm", (size_t)m * nJ * 4, &Gm))) return rc;
-        realq::SgemmArgs sg{};
-        sg.B = (const float*)Gacc;
-        sg.ldb = nJ;
-        sg.C = (float*)Gm;
-        sg.ldc = nJ;
-        sg.M = m;
-        sg.N = nJ;
-        sg.K = m;
+        if ((rc = get_ws(ctx, "b_GTh", (size_t)m * nJ * 2, &gth))) return rc;
+        if ((rc = get_ws(ctx, "b_GTl", (size_t)m * nJ * 2, &gtl))) return rc;
         const float invT = (float)(1.0 / (double)Tn);
-        bool first = true;
-        if (alpha > 0.f) {
-            if (st->M) {
-                sg.A = st->M;
-                sg.lda = m;
-                sg.alpha = alpha * invT;
-                sg.beta = 0.f;
-                RQ_HIP(ctx, realq::sgemm(sg, s));
-            } else {
-                // identity metric: Gm = alpha/T * Gacc
-                RQ_HIP(ctx, realq::reduce_splits((const float*)Gacc, 1, m, nJ, alpha * invT, (float*)Gm, false, s));
-            }
-            first = false;
+        {
+            Timed tm(ctx, "metric");
+            RQ_HIP(ctx,
+                   realq::transpose_split_f32((const float*)Gacc, nJ, (uint16_t*)gth, (uint16_t*)gtl, m, m, nJ, s));
+            realq::GemmArgs g1{st->Mah, st->Mal, m, (const uint16_t*)gth, m, m, nJ, m, 1};
+            RQ_HIP(ctx, realq::gemm_store_f32(g1, (float*)Gm, nJ, 0, invT, s));
+            realq::GemmArgs g2{st->Mah, nullptr, m, (const uint16_t*)gtl, m, m, nJ, m, 1};
+            RQ_HIP(ctx, realq::gemm_acc_f32(g2, (float*)Gm, nJ, invT, s));
         }
-        if (st->P && alpha < 1.f) {
-            sg.A = st->P;
-            sg.lda = m;
-            sg.alpha = (1.f - alpha) * invT;
-            sg.beta = first ? 0.f : 1.f;
-            RQ_HIP(ctx, realq::sgemm(sg, s));
-        }
+        Timed tm(ctx, "adam");
         RQ_HIP(ctx, realq::adam_update_dense(a, (const float*)Gm, s));
     }
     return REALQ_OK;

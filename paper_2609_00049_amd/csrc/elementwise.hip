@@ -389,6 +389,29 @@ hipError_t split_diff_f32(const float* A, int64_t lda, const float* Bm, int64_t 
     return hipGetLastError();
 }
 
+// Blended metric of Eq. slide_window as a bf16 pair: x = alpha (M or I)[i][k] + (1 - alpha) P[i][k]
+// (P may be NULL), hi = bf16(x), lo = bf16(x - hi); m x m, row-major.
+__global__ void blend_split_kernel(const float* __restrict__ M, const float* __restrict__ P, float alpha, int64_t m,
+                                   uint16_t* __restrict__ hi, uint16_t* __restrict__ lo) {
+    const int64_t total = m * m;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / m, k = e % m;
+        float v = alpha * (M ? M[e] : (i == k ? 1.f : 0.f));
+        if (P) v += (1.f - alpha) * P[e];
+        uint16_t h, l;
+        split_bf16(v, h, l);
+        hi[e] = h;
+        lo[e] = l;
+    }
+}
+
+hipError_t blend_split(const float* M, const float* P, float alpha, int64_t m, uint16_t* hi, uint16_t* lo,
+                       hipStream_t st) {
+    if (m <= 0) return hipSuccess;
+    hipLaunchKernelGGL(blend_split_kernel, dim3(grid_for(m * m, 4)), dim3(TB), 0, st, M, P, alpha, m, hi, lo);
+    return hipGetLastError();
+}
+
 __global__ void split_diff_bf16_kernel(const uint16_t* __restrict__ a, const uint16_t* __restrict__ b,
                                        uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, int64_t count) {
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += (int64_t)gridDim.x * blockDim.x) {

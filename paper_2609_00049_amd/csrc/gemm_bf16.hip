@@ -15,10 +15,13 @@
 // Tiling (two shapes, picked by problem size):
 //   large: 256 x 256 block tile, 8 wave64s as 4 (M) x 2 (N), 64 x 128 per wave
 //   small: 128 x 128 block tile, 4 wave64s as 2 x 2,        64 x 64 per wave
-// with v_mfma_f32_32x32x16_bf16 (accumulators live in AGPRs).  K advances in
-// slices of 32 through a ring of three LDS stages filled by direct-to-LDS 16-byte
-// loads, so two slices are in flight while the MFMAs consume the third; one barrier
-// per slice, with explicit vmcnt waits.  Blocks are renumbered
+// with v_mfma_f32_32x32x16_bf16.  K advances in slices of 32 through a ring of three
+// LDS stages filled by direct-to-LDS 16-byte loads with explicit vmcnt waits.  The large
+// tile runs its K loop as a ping-pong of its two 4-wave groups (one wave of each per
+// SIMD): between two barriers one group multiplies a slice from registers while the other
+// reads the next fragments out of LDS and issues the next loads, so the matrix pipe of
+// every SIMD stays fed while a wave waits on LDS.  The small tile keeps one barrier per
+// slice with two slices in flight.  Blocks are renumbered
 // so that each XCD (blocks are dealt round-robin over the 8 XCDs) owns a contiguous
 // run of tiles, walked in groups of `group_m` row tiles for L2 reuse.  Split-K over
 // gridDim.z with a fixed K range per split (deterministic).
@@ -50,6 +53,10 @@ struct Cfg {
 };
 using CfgLarge = Cfg<256, 256, 4, 2>;
 using CfgSmall = Cfg<128, 128, 2, 2>;
+// The 8-wave tile runs its K loop as a ping-pong of two 4-wave groups.
+template <class C>
+constexpr bool kPingPong = C::WAVES_M == 4 && C::WAVES_N == 2;
+__device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
 
 template <int CH, int NT>
 __device__ __forceinline__ void load_rows(u16x8 (&v)[CH], const uint16_t* __restrict__ P, int64_t ld, int64_t rows,
@@ -103,6 +110,7 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 // LDS byte address of a __shared__ object: the low 32 bits of its generic address.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
@@ -260,6 +268,56 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
         mfmas(f1);
     };
     const int64_t nfull = vec ? (kend - kbeg) / BK : 0;
+    if constexpr (kPingPong<C>) {
+        // Ping-pong over the two SIMD-sharing wave groups: waves 0-3 and 4-7 sit one per SIMD
+        // each (group 0 owns rows 0..127 of the tile, group 1 rows 128..255).  Every wave runs
+        // the same loop, "read slice s's fragments out of LDS and refill a stage | barrier |
+        // multiply slice s from registers | barrier", but group 1 enters it one barrier later,
+        // so between any two barriers one group multiplies while the other reads: on each SIMD
+        // one wave keeps the matrix pipe busy while the other waits on LDS and memory.
+        //   slice s lives in stage s % 3; each wave issues its share of slice s+2 in its read
+        //   phase of slice s (into the stage of slice s-1, which both groups have read by then)
+        //   and waits there until its share of slice s+1 has landed, which is before either
+        //   group's read phase of slice s+1.
+        const int grp = wv >> 2;
+        auto mem = [&](int64_t s, const uint16_t* cur, uint32_t fill, Frags& f0, Frags& f1) {
+            load_frags(cur, 0, f0);
+            load_frags(cur, 16, f1);
+            if (s + 2 < nfull) issue(s + 2, fill);
+            wait_lgkm0();
+            if (s + 2 < nfull) wait_vmcnt<DMA_PER_SLICE>();
+            else wait_vmcnt<0>();
+        };
+        if (nfull > 0) issue(0, lds_st[0]);
+        if (nfull > 1) issue(1, lds_st[1]);
+        if (nfull > 1) wait_vmcnt<DMA_PER_SLICE>();
+        else wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        if (grp == 1) __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+#define RQ_PP_SLICE(S, CUR, FILL)                       \
+    do {                                                \
+        Frags f0, f1;                                   \
+        mem((S), CUR, lds_st[FILL], f0, f1);            \
+        __builtin_amdgcn_sched_barrier(0);              \
+        __builtin_amdgcn_s_barrier();                   \
+        __builtin_amdgcn_sched_barrier(0);              \
+        mfmas(f0);                                      \
+        mfmas(f1);                                      \
+        __builtin_amdgcn_sched_barrier(0);              \
+        __builtin_amdgcn_s_barrier();                   \
+        __builtin_amdgcn_sched_barrier(0);              \
+    } while (0)
+        for (int64_t s = 0; s < nfull; s += 3) {
+            RQ_PP_SLICE(s, st0, 2);
+            if (s + 1 >= nfull) break;
+            RQ_PP_SLICE(s + 1, st1, 0);
+            if (s + 2 >= nfull) break;
+            RQ_PP_SLICE(s + 2, st2, 1);
+        }
+#undef RQ_PP_SLICE
+        if (grp == 0) __builtin_amdgcn_s_barrier();
+    } else {
     // one slice: wait until this slice has landed (the next may stay in flight), barrier (all
     // waves' loads visible; the stage read two slices ago is free), refill it, multiply.
 #define RQ_STEP(S, CUR, NXT2)                                      \
@@ -278,6 +336,7 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
         RQ_STEP(s + 2, st2, 1);
     }
 #undef RQ_STEP
+    }
     wait_vmcnt<0>();
     __syncthreads();
     for (int64_t s = nfull; s < nk; ++s) {  // checked tail, single-buffered in stage 0

@@ -90,6 +90,9 @@ hipError_t narrow_f64(const double* in, float* out, int64_t count, hipStream_t s
 // hi/lo[i] = split(bf16(a[i]) - bf16(b[i]))
 hipError_t split_diff_bf16(const uint16_t* a, const uint16_t* b, uint16_t* hi, uint16_t* lo, int64_t count,
                            hipStream_t st);
+// hi/lo[i*m + k] = split(alpha (M ? M : I)[i][k] + (1 - alpha) (P ? P[i][k] : 0)), m x m float32 inputs
+hipError_t blend_split(const float* M, const float* P, float alpha, int64_t m, uint16_t* hi, uint16_t* lo,
+                       hipStream_t st);
 // out = sum of partials (fixed order) * scale, written to *out (device)
 hipError_t reduce_partials(const double* partials, int64_t count, double scale, double* out, hipStream_t st);
 // Adam on W[:, c1:n] with G = gscale * sum_z Gp[z][i][j - c1]; refreshes Dhi/Dlo = split(W - W0) there
