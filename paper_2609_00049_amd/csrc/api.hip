@@ -91,8 +91,8 @@ struct realq_bgd_state {
     uint16_t* Dhi = nullptr;
     uint16_t* Dlo = nullptr;  // [m,n] split(W - W0)
     uint16_t* XhT = nullptr;  // [n,T]
-    uint16_t* Rhi = nullptr;
-    uint16_t* Rlo = nullptr;  // [m,Tc]
+    uint16_t* Rhi = nullptr;  // split(R o s): blocked layout [m, r_ld(Tc)], or with the clip
+    uint16_t* Rlo = nullptr;  // two arrays Rhi/Rlo [m, Tc]
     int64_t Tb = 0, nbatch = 1;  // tokens per step and number of batches (mini-batch BGD)
     float* Rf = nullptr;         // [m,Tc] residual kept whole for the clip
     float* tau = nullptr;        // [Tc] per-token clip thresholds
@@ -353,6 +353,10 @@ int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T
 
 // ============================================================================ BGD state
 
+// Row stride (bf16 values) of split(R o s) in the blocked layout for `cur` tokens: hi and lo of
+// every 32 tokens, rounded up to whole blocks.
+static int64_t r_ld(int64_t cur) { return 2 * ((cur + 31) / 32) * 32; }
+
 static int state_alloc(realq_bgd_state* st, void** p, size_t bytes, const char* slot) {
     realq_ctx* ctx = st->ctx;
     if (!st->owns) return get_ws(ctx, slot, bytes, p);
@@ -451,10 +455,18 @@ static int state_init(realq_bgd_state* st) {
     st->Dlo = (uint16_t*)p;
     if ((rc = state_alloc(st, &p, (size_t)n * T * 2, "s_XT"))) return rc;
     st->XhT = (uint16_t*)p;
-    if ((rc = state_alloc(st, &p, (size_t)m * Tc * 2, "s_Rh"))) return rc;
-    st->Rhi = (uint16_t*)p;
-    if ((rc = state_alloc(st, &p, (size_t)m * Tc * 2, "s_Rl"))) return rc;
-    st->Rlo = (uint16_t*)p;
+    if (st->prm.loss_clip > 0.f) {
+        // the clip writes split(R o s) as two arrays
+        if ((rc = state_alloc(st, &p, (size_t)m * Tc * 2, "s_Rh"))) return rc;
+        st->Rhi = (uint16_t*)p;
+        if ((rc = state_alloc(st, &p, (size_t)m * Tc * 2, "s_Rl"))) return rc;
+        st->Rlo = (uint16_t*)p;
+    } else {
+        // one array of 128-byte lines (32 tokens' hi, then their lo): whole-line stores
+        if ((rc = state_alloc(st, &p, (size_t)m * r_ld(Tc) * 2, "s_Rh"))) return rc;
+        st->Rhi = (uint16_t*)p;
+        st->Rlo = nullptr;
+    }
     if (st->prm.loss_clip > 0.f) {
         if ((rc = state_alloc(st, &p, (size_t)m * Tc * 4, "s_Rf"))) return rc;
         st->Rf = (float*)p;
@@ -807,8 +819,8 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
             realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
             if (!clip) {
                 Timed tm(ctx, "resid");
-                RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, st->Rlo, cur,
-                                              pch, s));
+                RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, nullptr,
+                                              r_ld(cur), pch, s, true));
             } else {
                 // residual kept whole, per-token thresholds over the m channels, then the
                 // clipped, weighted split for the gradient GEMM and the loss partials
@@ -820,7 +832,9 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
                                               st->Rlo, pch, s));
             }
             {
-                realq::GemmArgs g{st->Rhi, st->Rlo, cur, st->XhT + c1 * T + t0, T, m, nJ, cur, pl.splits};
+                realq::GemmArgs g{st->Rhi, clip ? st->Rlo : st->Rhi + 32, clip ? cur : r_ld(cur),
+                                  st->XhT + c1 * T + t0, T, m, nJ, cur, pl.splits};
+                g.a_blocked = clip ? 0 : 1;
                 splits_used = realq::gemm_effective_splits(cur, pl.splits);
                 Timed tm(ctx, "grad");
                 RQ_HIP(ctx, realq::gemm_grad(g, (float*)Gp, nJ, m * nJ, s));

@@ -58,9 +58,12 @@ template <class C>
 constexpr bool kPingPong = C::WAVES_M == 4 && C::WAVES_N == 2;
 __device__ __forceinline__ int64_t imin64(int64_t a, int64_t b) { return a < b ? a : b; }
 
+// element offset of column k in a row: plain, or the blocked hi/lo layout (32 values a block)
+__device__ __forceinline__ int64_t kofs_of(int64_t k, bool blk) { return blk ? ((k >> 5) << 6) + (k & 31) : k; }
+
 template <int CH, int NT>
 __device__ __forceinline__ void load_rows(u16x8 (&v)[CH], const uint16_t* __restrict__ P, int64_t ld, int64_t rows,
-                                          int64_t r0, int64_t k0, int64_t kend, bool vec) {
+                                          int64_t r0, int64_t k0, int64_t kend, bool vec, bool blk = false) {
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
         const int chunk = threadIdx.x + c * NT;
@@ -70,7 +73,7 @@ __device__ __forceinline__ void load_rows(u16x8 (&v)[CH], const uint16_t* __rest
         const int64_t gk = k0 + kc;
         u16x8 x = {0, 0, 0, 0, 0, 0, 0, 0};
         if (gr < rows) {
-            const uint16_t* p = P + gr * ld + gk;
+            const uint16_t* p = P + gr * ld + kofs_of(gk, blk);
             if (vec && gk + 8 <= kend) {
                 x = *reinterpret_cast<const u16x8*>(p);
             } else {
@@ -114,10 +117,10 @@ __device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0
 // LDS byte address of a __shared__ object: the low 32 bits of its generic address.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
-// Tile coordinates of this block: XCD-contiguous renumbering, then grouped row-tile order.
-__device__ __forceinline__ void tile_of(int64_t tiles_m, int64_t tiles_n, int64_t group_m, int64_t& tm, int64_t& tn) {
+// Tile coordinates of block b: XCD-contiguous renumbering, then grouped row-tile order.
+__device__ __forceinline__ void tile_of_v(int64_t b, int64_t tiles_m, int64_t tiles_n, int64_t group_m, int64_t& tm,
+                                          int64_t& tn) {
     const int64_t nblk = tiles_m * tiles_n;
-    const int64_t b = blockIdx.x;
     int64_t L = b;
     if ((nblk & 7) == 0) L = (b & 7) * (nblk >> 3) + (b >> 3);
     const int64_t per_group = group_m * tiles_n;
@@ -128,6 +131,9 @@ __device__ __forceinline__ void tile_of(int64_t tiles_m, int64_t tiles_n, int64_
     tm = first + r % gs;
     tn = r / gs;
 }
+__device__ __forceinline__ void tile_of(int64_t tiles_m, int64_t tiles_n, int64_t group_m, int64_t& tm, int64_t& tn) {
+    tile_of_v(blockIdx.x, tiles_m, tiles_n, group_m, tm, tn);
+}
 
 }  // namespace
 
@@ -136,7 +142,8 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
                                                         const uint16_t* __restrict__ Alo, int64_t lda,
                                                         const uint16_t* __restrict__ B, int64_t ldb, int64_t M,
                                                         int64_t N, int64_t K, int64_t k_per_split, int vec_ok,
-                                                        int64_t tiles_m, int64_t tiles_n, int64_t group_m, Epi epi) {
+                                                        int64_t tiles_m, int64_t tiles_n, int64_t group_m, int a_blk,
+                                                        Epi epi) {
     constexpr int A_ROWS = C::BM * (HAS_LO ? 2 : 1);
     constexpr int STAGE = (A_ROWS + C::BN) * LDS_STRIDE;  // bf16 elements per stage
     // Three LDS stages as separate arrays (the compiler can tell a stage being filled by the
@@ -202,17 +209,22 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
             offB[q] = (uint32_t)((gr * ldb + c * 8) * 2);
         }
     }
-    const char* const baseA = reinterpret_cast<const char*>(Ahi + m0 * lda + kbeg);
-    const char* const baseAl = HAS_LO ? reinterpret_cast<const char*>(Alo + m0 * lda + kbeg) : baseA;
+    // A in the blocked hi/lo layout advances 64 values (hi and lo of 32) per slice
+    const bool blk = a_blk != 0;
+    const int a_sh = __builtin_amdgcn_readfirstlane(blk ? 1 : 0);  // kept scalar for the load addresses
+    const int64_t a_step = (int64_t)(BK * 2) << a_sh;               // bytes of A per slice
+    const char* const baseA = reinterpret_cast<const char*>(Ahi + m0 * lda + (kbeg << a_sh));
+    const char* const baseAl = HAS_LO ? reinterpret_cast<const char*>(Alo + m0 * lda + (kbeg << a_sh)) : baseA;
     const char* const baseB = reinterpret_cast<const char*>(B + n0 * ldb + kbeg);
     const uint32_t lds_st[3] = {lds_addr(st0), lds_addr(st1), lds_addr(st2)};
     auto issue = [&](int64_t s, uint32_t stage) {
         const int64_t off = s * BK * 2;
+        const int64_t offa = s * a_step;
 #pragma unroll
         for (int q = 0; q < A_RUNS; ++q) {
             const uint32_t d = stage + (uint32_t)((wv + NW * q) * 16 * LDS_STRIDE * 2);
-            dma16(baseA + off, offA[q], d);
-            if constexpr (HAS_LO) dma16(baseAl + off, offA[q], d + C::BM * LDS_STRIDE * 2);
+            dma16(baseA + offa, offA[q], d);
+            if constexpr (HAS_LO) dma16(baseAl + offa, offA[q], d + C::BM * LDS_STRIDE * 2);
         }
 #pragma unroll
         for (int q = 0; q < B_RUNS; ++q)
@@ -342,8 +354,8 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
     for (int64_t s = nfull; s < nk; ++s) {  // checked tail, single-buffered in stage 0
         const int64_t k0 = kbeg + s * BK;
         u16x8 ra[C::A_CH], ral[HAS_LO ? C::A_CH : 1], rb[C::B_CH];
-        load_rows<C::A_CH, C::NT>(ra, Ahi, lda, M, m0, k0, kend, vec);
-        if constexpr (HAS_LO) load_rows<C::A_CH, C::NT>(ral, Alo, lda, M, m0, k0, kend, vec);
+        load_rows<C::A_CH, C::NT>(ra, Ahi, lda, M, m0, k0, kend, vec, blk);
+        if constexpr (HAS_LO) load_rows<C::A_CH, C::NT>(ral, Alo, lda, M, m0, k0, kend, vec, blk);
         load_rows<C::B_CH, C::NT>(rb, B, ldb, N, n0, k0, kend, vec);
         store_rows<C::A_CH, C::NT>(ra, st0);
         if constexpr (HAS_LO) store_rows<C::A_CH, C::NT>(ral, st0 + C::BM * LDS_STRIDE);
@@ -557,6 +569,7 @@ __device__ __forceinline__ TokW load_tokw(const float* s, int64_t t) {
 }
 
 // Residual: R = B0[i][t] + acc; writes split(R * s_t) and accumulates s_t R^2.
+// With blk, split(R o s) goes to one array of 128-byte lines: 32 tokens' hi, then their lo.
 struct EpiResid {
     static constexpr bool kReduce = true;
     static constexpr bool kTransposed = false;
@@ -567,26 +580,31 @@ struct EpiResid {
     uint16_t* Rlo;
     int64_t ldr;
     double* partials;
+    bool blk;
     struct Row {
         f32x4 b;
         bool ok;
     };
     using Col = TokW;
+    __device__ uint16_t* hi_at(int64_t i, int64_t t) const {
+        return blk ? Rhi + i * ldr + ((t >> 5) << 6) + (t & 31) : Rhi + i * ldr + t;
+    }
+    __device__ uint16_t* lo_at(int64_t i, int64_t t) const { return blk ? hi_at(i, t) + 32 : Rlo + i * ldr + t; }
     __device__ void operator()(int64_t i, int64_t t, float v, int64_t, float& aux) const {
         float r = B0[i * ldb0 + t] + v;
         float w = s ? s[t] : 1.f;
         float rs = r * w;
         uint16_t hi, lo;
         split_bf16(rs, hi, lo);
-        Rhi[i * ldr + t] = hi;
-        Rlo[i * ldr + t] = lo;
+        *hi_at(i, t) = hi;
+        *lo_at(i, t) = lo;
         aux += rs * r;
     }
     __device__ Col load_col(int64_t t) const { return load_tokw(s, t); }
     __device__ Row load_row(int64_t i, int64_t t, int64_t) const {
         Row r;
         const float* b = B0 + i * ldb0 + t;
-        r.ok = al16(b) && al8(Rhi + i * ldr + t) && al8(Rlo + i * ldr + t);
+        r.ok = al16(b) && al8(hi_at(i, t)) && al8(lo_at(i, t));
         if (r.ok) r.b = *reinterpret_cast<const f32x4*>(b);
         return r;
     }
@@ -606,8 +624,8 @@ struct EpiResid {
             l[u] = ll;
             aux += rs * r[u];
         }
-        *reinterpret_cast<u16x4*>(Rhi + i * ldr + t) = h;
-        *reinterpret_cast<u16x4*>(Rlo + i * ldr + t) = l;
+        *reinterpret_cast<u16x4*>(hi_at(i, t)) = h;
+        *reinterpret_cast<u16x4*>(lo_at(i, t)) = l;
     }
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
@@ -798,10 +816,10 @@ static hipError_t launch_cfg(const GemmArgs& g, const Epi& epi, hipStream_t stre
     dim3 grid((unsigned)(tiles_m * tiles_n), 1, (unsigned)splits);
     if (g.Alo)
         hipLaunchKernelGGL((gemm_nt_kernel<C, Epi, true>), grid, dim3(C::NT), 0, stream, g.Ahi, g.Alo, g.lda, g.B,
-                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_m, tiles_n, group_m, epi);
+                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_m, tiles_n, group_m, g.a_blocked, epi);
     else
         hipLaunchKernelGGL((gemm_nt_kernel<C, Epi, false>), grid, dim3(C::NT), 0, stream, g.Ahi, g.Alo, g.lda, g.B,
-                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_m, tiles_n, group_m, epi);
+                           g.ldb, g.M, g.N, g.K, kps, (int)vec, tiles_m, tiles_n, group_m, g.a_blocked, epi);
     return hipGetLastError();
 }
 
@@ -836,8 +854,9 @@ hipError_t gemm_resid_f32(const GemmArgs& g, const float* B0, int64_t ldb0, floa
     return launch(g, EpiResidF32{B0, ldb0, R, ldr}, st);
 }
 hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
-                      int64_t ldr, double* partials, hipStream_t st) {
-    return launch(g, EpiResid{B0, ldb0, s, Rhi, Rlo, ldr, partials}, st);
+                      int64_t ldr, double* partials, hipStream_t st, bool blocked) {
+    if (blocked && (ldr % 64 != 0 || g.N > ldr / 2)) return hipErrorInvalidValue;
+    return launch(g, EpiResid{B0, ldb0, s, Rhi, Rlo, ldr, partials, blocked}, st);
 }
 hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
                      hipStream_t st) {

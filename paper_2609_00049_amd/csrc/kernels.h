@@ -18,6 +18,8 @@ struct GemmArgs {
     int64_t splits;
     int64_t group_m = 0;  // row tiles walked together per XCD (0 = chosen from the shape)
     int tile = 0;         // 0: chosen from the shape, 1: 256x256 tile, 2: 128x128 tile
+    int a_blocked = 0;    // A in the blocked hi/lo layout of gemm_resid (Alo = Ahi + 32): element
+                          // (i, k) at i*lda + (k/32)*64 + k%32
 };
 int64_t gemm_effective_splits(int64_t K, int64_t splits);
 int64_t gemm_num_blocks(int64_t M, int64_t N, int tile = 0);
@@ -27,8 +29,12 @@ int64_t gemm_grad_blocks(int64_t M, int64_t N);
 hipError_t gemm_grad(const GemmArgs& g, float* C, int64_t ldc, int64_t split_stride, hipStream_t st);
 hipError_t gemm_acc_f32(const GemmArgs& g, float* C, int64_t ldc, float alpha, hipStream_t st);
 hipError_t gemm_acc_f64(const GemmArgs& g, double* C, int64_t ldc, hipStream_t st);
+// Residual R = B0 + acc with split(R o s) stored either as two arrays Rhi/Rlo [i*ldr + t]
+// (blocked = false) or in one array of 128-byte lines holding 32 tokens' hi then their lo
+// (blocked = true: hi at Rhi[i*ldr + (t/32)*64 + t%32], lo 32 further, ldr a multiple of 64;
+// Rlo unused), the A layout of a_blocked gradient launches.
 hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
-                      int64_t ldr, double* partials, hipStream_t st);
+                      int64_t ldr, double* partials, hipStream_t st, bool blocked = false);
 hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
                      hipStream_t st);
 // Token-major stores for the module hand-off: out[j*ld + i] = bf16(acc[i][j] + add[j*ld + i]);
