@@ -376,6 +376,92 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
     float aux = 0.f;
     float* scr = scratch + wave * (32 * EPI_STRIDE);
     const int64_t z = blockIdx.z;
+    // Full tiles of the large shape stream a residual-base epilogue's row operand into LDS with
+    // direct-to-LDS loads, three 32x32 sub-tiles ahead per wave (a ring of 3 x 4 KB per wave in
+    // stages 1 and 2, freed by the K loop): the register-held prefetch reaches one sub-tile ahead
+    // only, and a tile's epilogue then waits out one memory latency per sub-tile.
+    constexpr int RING = 3;
+    constexpr bool kDma = Epi::kRowDma && C::NT == 512 && EPI_IN_STAGE && STAGE * 2 >= 4 * RING * 4096;
+    bool dma_path = false;
+    if constexpr (kDma) dma_path = m0 + C::BM <= M && n0 + C::BN <= N && epi.row_dma_ok();
+    if constexpr (kDma) {
+        if (dma_path) {
+            constexpr int NSUB = C::SM * C::SN;
+            const int cc = (lane & 7) * 4;
+            const int wms = wv / C::WAVES_N, wns = wv % C::WAVES_N;  // scalar copies for the load bases
+            // token weights of this wave's columns, consumed before the streamed loads start (the
+            // compiler's own waits for them must not wait for those)
+            typename Epi::Col cw[C::SN];
+#pragma unroll
+            for (int j = 0; j < C::SN; ++j) {
+                cw[j] = epi.load_col(n0 + wn * C::WTN + j * 32 + cc);
+                asm volatile("" ::"v"(cw[j].w[0]), "v"(cw[j].w[1]), "v"(cw[j].w[2]), "v"(cw[j].w[3]));
+            }
+            const float* const b0 = epi.row_base();
+            const int64_t ldb0 = epi.row_ld();
+            uint16_t* const ring16 = (wv < 4 ? st1 : st2) + (wv & 3) * (RING * 2048);
+            const float* const ring = reinterpret_cast<const float*>(ring16);
+            const uint32_t ring_lds = lds_addr(ring16);
+            auto dma_sub = [&](int t) {
+                const int64_t r0 = m0 + wms * C::WTM + (t / C::SN) * 32;
+                const int64_t c0 = n0 + wns * C::WTN + (t % C::SN) * 32;
+                const char* base = reinterpret_cast<const char*>(b0 + r0 * ldb0 + c0);
+                const uint32_t slot = ring_lds + (uint32_t)((t % RING) * 4096);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    dma16(base, (uint32_t)(((int64_t)(q * 8 + (lane >> 3)) * ldb0 + (lane & 7) * 4) * 4),
+                          slot + q * 1024);
+            };
+            // vector-memory operations of this lane issued after sub-tile t's streamed loads, at the
+            // point where t is consumed (4 loads per sub-tile, kRowStores stores per sub-tile)
+            auto after = [](int t) {
+                int c = 0;
+                if (t < RING) {
+                    c += (RING - 1 - t) * 4;
+                    for (int u = 0; u < t; ++u) c += Epi::kRowStores + (u + RING < NSUB ? 4 : 0);
+                } else {
+                    for (int u = t - RING + 1; u < t; ++u) c += Epi::kRowStores + (u + RING < NSUB ? 4 : 0);
+                }
+                return c;
+            };
+            static_assert(RING <= NSUB, "ring deeper than the sub-tiles");
+#pragma unroll
+            for (int t = 0; t < RING; ++t) dma_sub(t);
+#pragma unroll
+            for (int t = 0; t < NSUB; ++t) {
+                switch (after(t)) {  // constant after unrolling
+                    case 8: wait_vmcnt<8>(); break;
+                    case 16: wait_vmcnt<16>(); break;
+                    case 20: wait_vmcnt<20>(); break;
+                    case 24: wait_vmcnt<24>(); break;
+                    default: wait_vmcnt<0>(); break;
+                }
+                const int i = t / C::SN, j = t % C::SN;
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    scr[(8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)) * EPI_STRIDE + (lane & 31)] = acc[i][j][e];
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                const int64_t r0 = m0 + wm * C::WTM + i * 32;
+                const int64_t col = n0 + wn * C::WTN + j * 32 + cc;
+                const float* slot = ring + (t % RING) * 1024;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int rr = q * 8 + (lane >> 3);
+                    const f32x4 v = *reinterpret_cast<const f32x4*>(scr + rr * EPI_STRIDE + cc);
+                    typename Epi::Row rw;
+                    rw.b = *reinterpret_cast<const f32x4*>(slot + rr * 32 + cc);
+                    rw.ok = true;
+                    epi.vec4(r0 + rr, col, v, rw, cw[j], z, aux);
+                }
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                if (t + RING < NSUB) {
+                    wait_lgkm0();  // this slot's reads are done before it is refilled
+                    dma_sub(t + RING);
+                }
+            }
+        }
+    }
+    if (!dma_path) {
     if constexpr (!Epi::kTransposed) {
         constexpr int NSUB = C::SM * C::SN;
         const int cc = (lane & 7) * 4;
@@ -458,9 +544,14 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
                 __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
             }
     }
+    }  // !dma_path
     if constexpr (Epi::kReduce) {
-        // deterministic block reduction of the per-thread partial sums (reuses the LDS stage)
-        double* red = reinterpret_cast<double*>(st1);
+        // deterministic block reduction of the per-thread partial sums, in stage 0 past the
+        // restaging scratch when it fits there (stages 1 and 2 may still feed other waves'
+        // epilogues), else in stage 1
+        constexpr bool RED0 = EPI_IN_STAGE && (C::NT / 64) * 32 * EPI_STRIDE * 4 + C::NT * 8 <= STAGE * 2;
+        double* red = RED0 ? reinterpret_cast<double*>(reinterpret_cast<char*>(st0) + (C::NT / 64) * 32 * EPI_STRIDE * 4)
+                           : reinterpret_cast<double*>(st1);
         red[threadIdx.x] = (double)aux;
         __syncthreads();
         for (int s = C::NT / 2; s > 0; s >>= 1) {
@@ -484,6 +575,7 @@ typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 struct NoCol {};
 
 struct EpiStoreF32 {  // C[z][i][j] = alpha * acc
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = false;
     float* C;
@@ -511,6 +603,7 @@ struct EpiStoreF32 {  // C[z][i][j] = alpha * acc
 struct EpiGrad : EpiStoreF32 {};
 
 struct EpiAccF32 {  // C[i][j] += alpha * acc
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = false;
     float* C;
@@ -537,6 +630,7 @@ struct EpiAccF32 {  // C[i][j] += alpha * acc
 };
 
 struct EpiAccF64 {  // C[i][j] += acc   (float64 accumulator across chunks)
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = false;
     double* C;
@@ -571,6 +665,8 @@ __device__ __forceinline__ TokW load_tokw(const float* s, int64_t t) {
 // Residual: R = B0[i][t] + acc; writes split(R * s_t) and accumulates s_t R^2.
 // With blk, split(R o s) goes to one array of 128-byte lines: 32 tokens' hi, then their lo.
 struct EpiResid {
+    static constexpr bool kRowDma = true;  // residual base streamed into LDS by full tiles
+    static constexpr int kRowStores = 8;   // store instructions per lane and 32x32 sub-tile (4 rows x hi, lo)
     static constexpr bool kReduce = true;
     static constexpr bool kTransposed = false;
     const float* B0;
@@ -590,6 +686,14 @@ struct EpiResid {
         return blk ? Rhi + i * ldr + ((t >> 5) << 6) + (t & 31) : Rhi + i * ldr + t;
     }
     __device__ uint16_t* lo_at(int64_t i, int64_t t) const { return blk ? hi_at(i, t) + 32 : Rlo + i * ldr + t; }
+    __device__ const float* row_base() const { return B0; }
+    __device__ int64_t row_ld() const { return ldb0; }
+    // every row of a full tile may take the streamed path: 16-byte base rows within 32-bit
+    // offsets of a sub-tile's first row, 8-byte output quads
+    __device__ bool row_dma_ok() const {
+        const bool out = blk ? (al8(Rhi) && ldr % 64 == 0) : (al8(Rhi) && al8(Rlo) && ldr % 4 == 0);
+        return al16(B0) && ldb0 % 4 == 0 && ldb0 < (int64_t(1) << 24) && out;
+    }
     __device__ void operator()(int64_t i, int64_t t, float v, int64_t, float& aux) const {
         float r = B0[i * ldb0 + t] + v;
         float w = s ? s[t] : 1.f;
@@ -632,6 +736,7 @@ struct EpiResid {
 
 // Residual kept whole in float32: R[i][t] = B0[i][t] + acc (for the output-perturbation clip).
 struct EpiResidF32 {
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = false;
     const float* B0;
@@ -662,6 +767,7 @@ struct EpiResidF32 {
 
 // Residual loss only (no outputs besides the partial sums): s_t (B0 + acc)^2.
 struct EpiLoss {
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = true;
     static constexpr bool kTransposed = false;
     const float* B0;
@@ -703,6 +809,7 @@ struct EpiLoss {
 
 // out[j][i] = bf16(acc + add[j][i])   (add may be NULL; same layout as out)
 struct EpiStoreBf16T {
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = true;
     uint16_t* out;
@@ -735,6 +842,7 @@ struct EpiStoreBf16T {
 // out[j][i] = acc + add[j][i] (float32; the gate pre-activation of a SwiGLU hand-off; add may
 // be NULL or equal to out: each element is read and written by the same lane)
 struct EpiStoreF32T {
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = true;
     float* out;
@@ -761,6 +869,7 @@ struct EpiStoreF32T {
 
 // SwiGLU hand-off: out[j][i] = bf16(silu(G[j][i]) * acc), silu(g) = g / (1 + e^-g).
 struct EpiSwiGLUT {
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = false;
     static constexpr bool kTransposed = true;
     const float* G;
