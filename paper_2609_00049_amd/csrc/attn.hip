@@ -229,14 +229,205 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const uint16_t* __restric
     }
 }
 
+// The same forward with the key and value tiles staged in LDS and shared by the block's four query
+// tiles (one per wave, the waves of a block take consecutive query tiles of one head): every key
+// tile is loaded once per block with direct-to-LDS 16-byte loads into one of two buffers, the next
+// tile's loads overlapping the current tile's work, and each wave keeps its query fragments in
+// registers.  Per lane the arithmetic (MFMA order, the float64 statistics, the three-term P) is that
+// of attn_fwd_kernel, so the outputs are bitwise the same.  LDS rows are XOR-swizzled by 16-byte
+// chunk so the fragment reads (one chunk of 16 or 32 consecutive rows) are free of bank conflicts:
+//   key tile   [32 keys][HD] bf16, chunk c of key row r at position c ^ (r mod HD/8)
+//   value tile [HD cols][32 keys] bf16 (from v^T), chunk c of row r at c ^ ((r/2 ^ r/8) mod 4)
+namespace {
+__device__ __forceinline__ void attn_dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+                 : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void attn_wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ int vswz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+}  // namespace
+
+template <int HD>
+__global__ __launch_bounds__(256) void attn_fwd_lds_kernel(const uint16_t* __restrict__ qr,
+                                                           const uint16_t* __restrict__ kr,
+                                                           const uint16_t* __restrict__ vt, int64_t T, int64_t H,
+                                                           int64_t Hkv, int64_t L, float* __restrict__ O32,
+                                                           uint16_t* __restrict__ O, double* __restrict__ LSE) {
+    constexpr int NK = HD / 16, NCT = HD / AT;
+    constexpr int KCH = HD / 8;                // 16-byte chunks per key row
+    constexpr int KBYTES = AT * HD * 2, VBYTES = HD * AT * 2;
+    constexpr int KDMA = KBYTES / 1024 / 4, VDMA = VBYTES / 1024 / 4;  // 1 KB loads per wave and tile
+    static_assert(KDMA >= 1 && VDMA >= 1 && NCT <= CG, "head width");
+    __shared__ float sS[4][AT][AT + 1];
+    __shared__ __attribute__((aligned(16))) uint16_t sP[4][3][AT][TSTR];
+    __shared__ __attribute__((aligned(16))) uint16_t sKV[2][(KBYTES + VBYTES) / 2];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int64_t nt = L / AT, nq = (nt + 3) / 4;
+    const int64_t sh = blockIdx.x / nq, h = sh % H, s = sh / H;
+    const int64_t qb = blockIdx.x % nq;
+    const int64_t itmax = nt - 1 - 4 * qb;          // the block's longest row of key tiles
+    const int64_t it = itmax - wave;                 // this wave's query tile (may be < 0)
+    const int64_t g = h / (H / Hkv);
+    const double scale = 1.0 / sqrt((double)HD);
+    float(*Sw)[AT + 1] = sS[wave];
+    uint16_t(*Pw)[AT][TSTR] = sP[wave];
+    const int rr = lane >> 1, hh = lane & 1, c32 = lane & 31, k8 = 8 * (lane >> 5);
+    const int64_t ldk = Hkv * HD;                    // key row stride (elements)
+    const uint16_t* kbase = kr + (s * L) * ldk + g * HD;
+    const uint16_t* vbase = vt + (g * HD) * T + s * L;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)&sKV[0][0];
+    constexpr uint32_t BUFB = KBYTES + VBYTES;
+    // this wave's share of key tile jt (and with V, its value tile) into buffer b
+    auto load_tile = [&](int64_t jt, int b, bool with_v) {
+        const uint32_t kd = lds0 + (uint32_t)b * BUFB;
+        const char* kb = reinterpret_cast<const char*>(kbase + jt * AT * ldk);
+#pragma unroll
+        for (int q = 0; q < KDMA; ++q) {
+            const int qi = wv * KDMA + q;                    // 1 KB piece of the tile
+            const int row = qi * (1024 / (HD * 2)) + lane / KCH, pos = lane % KCH;
+            const int c = pos ^ (row % KCH);
+            attn_dma16(kb, (uint32_t)((row * ldk + c * 8) * 2), kd + (uint32_t)qi * 1024);
+        }
+        if (with_v) {
+            const char* vb = reinterpret_cast<const char*>(vbase + jt * AT);
+#pragma unroll
+            for (int q = 0; q < VDMA; ++q) {
+                const int qi = wv * VDMA + q;
+                const int row = qi * 16 + (lane >> 2), pos = lane & 3;
+                const int c = pos ^ vswz(row);
+                attn_dma16(vb, (uint32_t)((row * T + c * 8) * 2), kd + KBYTES + (uint32_t)qi * 1024);
+            }
+        }
+    };
+    const bool active0 = it >= 0;
+    // query fragments of this wave's tile, kept for both passes
+    bf16x8 qf[NK];
+    if (active0) {
+        const uint16_t* qa = qr + (s * L + it * AT + c32) * (H * HD) + h * HD + k8;
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) qf[kk] = ld8(qa + 16 * kk);
+    }
+    auto scores = [&](int b, int64_t jt) {
+        const uint16_t* kt = &sKV[b][0];
+        f32x16 acc = zero16();
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+            const int c = 2 * kk + (lane >> 5);
+            const bf16x8 bk = ld8(kt + c32 * HD + ((c ^ (c32 % KCH)) * 8));
+            acc = mfma(qf[kk], bk, acc);
+        }
+        const bool diag = jt == it;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int r = acc_row(e, lane);
+            Sw[r][c32] = (diag && c32 > r) ? -INFINITY : acc[e];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    };
+    // pass 1: the row max and sum
+    double m_row = -INFINITY, l_row = 0.0;
+    load_tile(0, 0, false);
+    for (int64_t jt = 0; jt <= itmax; ++jt) {
+        attn_wait_vm<0>();                 // this wave's share of tile jt has landed
+        __syncthreads();                   // every share landed; tile jt-1's buffer is free
+        if (jt + 1 <= itmax) load_tile(jt + 1, (int)((jt + 1) & 1), false);
+        if (jt <= it) {
+            scores((int)(jt & 1), jt);
+            float smax = -INFINITY;  // scaling by a positive constant keeps the order
+#pragma unroll
+            for (int k = 0; k < 16; ++k) smax = fmaxf(smax, Sw[rr][16 * hh + k]);
+            smax = fmaxf(smax, __shfl_xor(smax, 1));
+            const double m_new = fmax(m_row, (double)smax * scale);
+            double sum = 0.0;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) sum += (double)expf((float)((double)Sw[rr][16 * hh + k] * scale - m_new));
+            sum += __shfl_xor(sum, 1);
+            l_row = l_row * exp(m_row - m_new) + sum;
+            m_row = m_new;
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        }
+    }
+    if (active0 && hh == 0) LSE[(s * L + it * AT + rr) * H + h] = m_row + log(l_row);
+    const double inv_l = 1.0 / l_row;
+    // pass 2: P v over the value-column tiles
+    f32x16 oacc[NCT];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) oacc[ct] = zero16();
+    attn_wait_vm<0>();
+    __syncthreads();                       // pass 1's reads of both buffers are done
+    load_tile(0, 0, true);
+    for (int64_t jt = 0; jt <= itmax; ++jt) {
+        attn_wait_vm<0>();
+        __syncthreads();
+        if (jt + 1 <= itmax) load_tile(jt + 1, (int)((jt + 1) & 1), true);
+        if (jt <= it) {
+            const int b = (int)(jt & 1);
+            scores(b, jt);
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                const float pf =
+                    (float)((double)expf((float)((double)Sw[rr][16 * hh + k] * scale - m_row)) * inv_l);
+                const uint16_t ph = f2bf(pf);
+                const float r1 = pf - bf2f(ph);
+                const uint16_t pl = f2bf(r1);
+                Pw[0][rr][16 * hh + k] = ph;
+                Pw[1][rr][16 * hh + k] = pl;
+                Pw[2][rr][16 * hh + k] = f2bf(r1 - bf2f(pl));
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            const uint16_t* vtile = &sKV[b][KBYTES / 2];
+#pragma unroll
+            for (int k2 = 0; k2 < 2; ++k2) {
+                const int col = 16 * k2 + k8;
+                const bf16x8 ah = ld8(&Pw[0][c32][col]);
+                const bf16x8 al = ld8(&Pw[1][c32][col]);
+                const bf16x8 al2 = ld8(&Pw[2][c32][col]);
+                const int c = 2 * k2 + (lane >> 5);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const int row = ct * AT + c32;
+                    const bf16x8 bv = ld8(vtile + row * AT + ((c ^ vswz(row)) * 8));
+                    oacc[ct] = mfma(ah, bv, oacc[ct]);
+                    oacc[ct] = mfma(al, bv, oacc[ct]);
+                    oacc[ct] = mfma(al2, bv, oacc[ct]);
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        }
+    }
+    if (!active0) return;
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int64_t col = h * HD + (int64_t)ct * AT + c32;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int64_t t = s * L + it * AT + acc_row(e, lane);
+            O32[t * H * HD + col] = oacc[ct][e];
+            O[t * H * HD + col] = f2bf(oacc[ct][e]);
+        }
+    }
+}
+
 hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, int64_t T, int64_t H, int64_t Hkv,
                     int64_t hd, int64_t L, double* LSE, float* O32, uint16_t* O, uint16_t* vt, hipStream_t st) {
     if (T <= 0) return hipSuccess;
     const int64_t S = T / L, nt = L / AT;
     hipError_t e = transpose_u16(v, Hkv * hd, vt, T, T, Hkv * hd, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_fwd_kernel, dim3((unsigned)(S * H * ((nt + 3) / 4))), dim3(256), 0, st, qr, kr, vt, T, H,
-                       Hkv, hd, L, O32, O, LSE);
+    const dim3 grid((unsigned)(S * H * ((nt + 3) / 4)));
+    // the LDS-staged kernel where the 32-bit load offsets of a tile fit (rows of v^T are T long)
+    const bool lds_ok = (int64_t)hd * T * 2 < (int64_t(1) << 31) && (((uintptr_t)kr | (uintptr_t)vt) & 15) == 0 &&
+                        (Hkv * hd) % 8 == 0 && T % 8 == 0;
+    if (lds_ok && hd == 128)
+        hipLaunchKernelGGL((attn_fwd_lds_kernel<128>), grid, dim3(256), 0, st, qr, kr, vt, T, H, Hkv, L, O32, O, LSE);
+    else if (lds_ok && hd == 64)
+        hipLaunchKernelGGL((attn_fwd_lds_kernel<64>), grid, dim3(256), 0, st, qr, kr, vt, T, H, Hkv, L, O32, O, LSE);
+    else
+        hipLaunchKernelGGL(attn_fwd_kernel, grid, dim3(256), 0, st, qr, kr, vt, T, H, Hkv, hd, L, O32, O, LSE);
     return hipGetLastError();
 }
 
