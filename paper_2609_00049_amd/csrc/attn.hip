@@ -78,6 +78,7 @@ hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t h
 namespace {
 constexpr int AT = 32;
 constexpr int TSTR = AT + 8;  // bf16 per row of a staged 32 x 32 tile (80 bytes: 16-byte aligned rows)
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8 ld8(const uint16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
@@ -88,6 +89,21 @@ __device__ __forceinline__ void split8x3(const float* p, bf16x8& hi, bf16x8& lo,
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
         const float x = u < 4 ? x0[u] : x1[u - 4];
+        h[u] = f2bf(x);
+        const float r = x - bf2f(h[u]);
+        l[u] = f2bf(r);
+        l2[u] = f2bf(r - bf2f(l[u]));
+    }
+    hi = __builtin_bit_cast(bf16x8, h);
+    lo = __builtin_bit_cast(bf16x8, l);
+    lo2 = __builtin_bit_cast(bf16x8, l2);
+}
+
+__device__ __forceinline__ void split8x3(const float (&x8)[8], bf16x8& hi, bf16x8& lo, bf16x8& lo2) {
+    u16x8 h, l, l2;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const float x = x8[u];
         h[u] = f2bf(x);
         const float r = x - bf2f(h[u]);
         l[u] = f2bf(r);
@@ -514,6 +530,152 @@ __global__ __launch_bounds__(256) void attn_ds_kernel(const uint16_t* __restrict
     flush(ql, true, Ptl, jt * AT, it * AT);
 }
 
+// attn_ds_kernel with the work of a query tile in one wave (used when the grid has at least 512
+// blocks: with 300 registers a wave has its SIMD to itself): the four waves of a block take
+// consecutive query tiles of one head (as the forward's), keep their query fragments, LSE and D in
+// LDS and their dO rows in registers (split into three terms per key tile), and walk the
+// key tiles on or below their diagonal while the block streams each key tile and value tile into
+// two LDS buffers (rows XOR-swizzled as in the forward).  Per element the arithmetic is that of
+// attn_ds_kernel, so the six outputs are bitwise the same.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_ds_lds_kernel(const uint16_t* __restrict__ qr,
+                                                          const uint16_t* __restrict__ kr,
+                                                          const double* __restrict__ LSE,
+                                                          const float* __restrict__ dO,
+                                                          const uint16_t* __restrict__ v,
+                                                          const double* __restrict__ D, int64_t H, int64_t Hkv,
+                                                          int64_t L, uint16_t* __restrict__ dSh,
+                                                          uint16_t* __restrict__ dSl, uint16_t* __restrict__ dSth,
+                                                          uint16_t* __restrict__ dStl, uint16_t* __restrict__ Pth,
+                                                          uint16_t* __restrict__ Ptl) {
+    constexpr int NK = HD / 16;
+    constexpr int KCH = HD / 8;
+    constexpr int TBYTES = AT * HD * 2;                  // one key (or value) tile
+    constexpr int TDMA = TBYTES / 1024 / 4;              // 1 KB loads per wave and tile
+    static_assert(TDMA >= 1, "head width");
+    __shared__ __attribute__((aligned(16))) uint16_t sKV[2][TBYTES];   // [buf][key tile | value tile]
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[4][AT * HD];    // each wave's query rows (swizzled)
+    __shared__ __attribute__((aligned(16))) uint16_t stage[4][AT][TSTR];
+    __shared__ double sLD[4][2][AT];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int64_t nt = L / AT, nq = (nt + 3) / 4;
+    const int64_t sh = blockIdx.x / nq, h = sh % H, s = sh / H;
+    const int64_t qb = blockIdx.x % nq;
+    const int64_t itmax = nt - 1 - 4 * qb;
+    const int64_t it = itmax - wave;
+    const bool active = it >= 0;
+    const int64_t g = h / (H / Hkv);
+    const int64_t ldk = Hkv * HD;
+    const int c32 = lane & 31, k8 = 8 * (lane >> 5);
+    const uint16_t* kbase = kr + (s * L) * ldk + g * HD;
+    const uint16_t* vbase = v + (s * L) * ldk + g * HD;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)&sKV[0][0];
+    auto load_tile = [&](int64_t jt, int b) {
+        const uint32_t dst = lds0 + (uint32_t)b * (2 * TBYTES);
+        const char* kb = reinterpret_cast<const char*>(kbase + jt * AT * ldk);
+        const char* vb = reinterpret_cast<const char*>(vbase + jt * AT * ldk);
+#pragma unroll
+        for (int q = 0; q < TDMA; ++q) {
+            const int qi = wv * TDMA + q;
+            const int row = qi * (1024 / (HD * 2)) + lane / KCH, pos = lane % KCH;
+            const uint32_t off = (uint32_t)((row * ldk + (pos ^ (row % KCH)) * 8) * 2);
+            attn_dma16(kb, off, dst + (uint32_t)qi * 1024);
+            attn_dma16(vb, off, dst + TBYTES + (uint32_t)qi * 1024);
+        }
+    };
+    // this wave's rows: query fragments (LDS), dO (registers, split per key tile), LSE and D (LDS)
+    uint16_t* const qw = sQ[wave];
+    f32x4 dOr[NK][2];
+    if (active) {
+        const uint16_t* qa = qr + (s * L + it * AT + c32) * (H * HD) + h * HD + k8;
+        const float* a = dO + (s * L + it * AT + c32) * (H * HD) + h * HD + k8;
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+            const int c = 2 * kk + (lane >> 5);
+            *reinterpret_cast<u16x8*>(qw + c32 * HD + (c ^ (c32 % KCH)) * 8) =
+                *reinterpret_cast<const u16x8*>(qa + 16 * kk);
+            dOr[kk][0] = *reinterpret_cast<const f32x4*>(a + 16 * kk);
+            dOr[kk][1] = *reinterpret_cast<const f32x4*>(a + 16 * kk + 4);
+        }
+        if (lane < AT) {
+            sLD[wave][0][lane] = LSE[(s * L + it * AT + lane) * H + h];
+            sLD[wave][1][lane] = D[(s * L + it * AT + lane) * H + h];
+        }
+    }
+    const double scale = 1.0 / sqrt((double)HD);
+    uint16_t(*tb)[TSTR] = stage[wave];
+    const int r = lane >> 2, c8 = (lane & 3) * 8;
+    // values packed as hi | lo << 16; `lo` picks the half
+    auto flush = [&](const uint32_t (&val)[16], bool lo, bool transposed, uint16_t* dst, int64_t row0, int64_t col0) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int a = acc_row(e, lane), b = lane & 31;
+            const uint16_t x = (uint16_t)(lo ? (val[e] >> 16) : (val[e] & 0xffffu));
+            if (transposed) tb[b][a] = x;
+            else tb[a][b] = x;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int rr = r + 16 * half;
+            *reinterpret_cast<u16x8*>(dst + (sh * L + row0 + rr) * L + col0 + c8) =
+                *reinterpret_cast<const u16x8*>(&tb[rr][c8]);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    };
+    load_tile(0, 0);
+    for (int64_t jt = 0; jt <= itmax; ++jt) {
+        // this wave's loads of tile jt have landed; the 12 stores of the previous tile, issued after
+        // those loads, may still be in flight
+        if (jt >= 1 && jt - 1 <= it) attn_wait_vm<12>();
+        else attn_wait_vm<0>();
+        __syncthreads();
+        if (jt + 1 <= itmax) load_tile(jt + 1, (int)((jt + 1) & 1));
+        if (jt > it) continue;
+        const uint16_t* kt = &sKV[jt & 1][0];
+        const uint16_t* vt_ = kt + TBYTES / 2;
+        f32x16 acc = zero16(), sc = zero16();
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {  // dO in three terms: dP - D cancels
+            const int c = 2 * kk + (lane >> 5);
+            const int off = c32 * HD + ((c ^ (c32 % KCH)) * 8);
+            float x8[8];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                x8[u] = dOr[kk][0][u];
+                x8[u + 4] = dOr[kk][1][u];
+            }
+            bf16x8 ah, al, al2;
+            split8x3(x8, ah, al, al2);
+            const bf16x8 bv = ld8(vt_ + off);
+            acc = mfma(ah, bv, acc);
+            acc = mfma(al, bv, acc);
+            acc = mfma(al2, bv, acc);
+            sc = mfma(ld8(qw + off), ld8(kt + off), sc);
+        }
+        uint32_t dsv[16], pv2[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int ir = acc_row(e, lane);
+            const int64_t i = it * AT + ir, j = jt * AT + c32;
+            const float pv = j <= i ? expf((float)((double)sc[e] * scale - sLD[wave][0][ir])) : 0.f;
+            const float ds = (float)((double)pv * ((double)acc[e] - sLD[wave][1][ir]));
+            uint16_t a0, a1, b0, b1;
+            split_bf16(ds, a0, a1);
+            split_bf16(pv, b0, b1);
+            dsv[e] = (uint32_t)a0 | ((uint32_t)a1 << 16);
+            pv2[e] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+        }
+        flush(dsv, false, false, dSh, it * AT, jt * AT);
+        flush(dsv, true, false, dSl, it * AT, jt * AT);
+        flush(dsv, false, true, dSth, jt * AT, it * AT);
+        flush(dsv, true, true, dStl, jt * AT, it * AT);
+        flush(pv2, false, true, Pth, jt * AT, it * AT);
+        flush(pv2, true, true, Ptl, jt * AT, it * AT);
+    }
+}
+
 // dqr = dS kr / sqrt(hd): grid (S H nt, ceil(hd / 32 / 4)); kt = kr^T [Hkv hd][T].
 __global__ __launch_bounds__(256) void attn_dq_kernel(const uint16_t* __restrict__ dSh, const uint16_t* __restrict__ dSl,
                                                       const uint16_t* __restrict__ kt, int64_t T, int64_t H,
@@ -635,8 +797,19 @@ hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const 
     if ((e = transpose_u16(kr, Hkv * hd, w.kt, T, T, Hkv * hd, st)) != hipSuccess) return e;
     if ((e = transpose_u16(qr, H * hd, w.qt, T, T, H * hd, st)) != hipSuccess) return e;
     if ((e = transpose_split_f32(dO, H * hd, w.dOth, w.dOtl, T, T, H * hd, st)) != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_ds_kernel, dim3((unsigned)(S * H * nt), (unsigned)((nt + 3) / 4)), dim3(256), 0, st, qr, kr,
-                       LSE, dO, v, w.D, H, Hkv, hd, L, w.dSh, w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
+    // the query-tile-per-wave kernel needs enough blocks to fill the chip (one wave per SIMD)
+    const bool lds_ok = (((uintptr_t)kr | (uintptr_t)v) & 15) == 0 && (Hkv * hd) % 8 == 0 &&
+                        (int64_t)AT * Hkv * hd * 2 < (int64_t(1) << 31) && S * H * ((nt + 3) / 4) >= 512;
+    const dim3 gq((unsigned)(S * H * ((nt + 3) / 4)));
+    if (lds_ok && hd == 128)
+        hipLaunchKernelGGL((attn_ds_lds_kernel<128>), gq, dim3(256), 0, st, qr, kr, LSE, dO, v, w.D, H, Hkv, L, w.dSh,
+                           w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
+    else if (lds_ok && hd == 64)
+        hipLaunchKernelGGL((attn_ds_lds_kernel<64>), gq, dim3(256), 0, st, qr, kr, LSE, dO, v, w.D, H, Hkv, L, w.dSh,
+                           w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
+    else
+        hipLaunchKernelGGL(attn_ds_kernel, dim3((unsigned)(S * H * nt), (unsigned)((nt + 3) / 4)), dim3(256), 0, st, qr,
+                           kr, LSE, dO, v, w.D, H, Hkv, hd, L, w.dSh, w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned cy = (unsigned)((hd / AT + 3) / 4);
     hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)(S * H * nt), cy), dim3(256), 0, st, w.dSh, w.dSl, w.kt, T, H,
