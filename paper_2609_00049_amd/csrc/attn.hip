@@ -769,6 +769,141 @@ __global__ __launch_bounds__(256) void attn_dkv_kernel(const uint16_t* __restric
     }
 }
 
+// attn_dkv_kernel with the four waves of a block on four consecutive key tiles of one key/value
+// head, each computing all HD/32 value-column tiles: the B operands of a step (head h of the
+// group, query tile it: the 32 tokens of q^T and of dO^T hi/lo over the head's HD rows, 24 KB for
+// HD = 128) are loaded once per block, one step ahead into registers, and stored to one of two LDS
+// buffers (rows swizzled as the forward's value tile); each wave's dS^T / P^T fragments of the
+// step are loaded one step ahead into registers, before the block's loads of the following step,
+// so no wait for them waits for those.  Steps run over the group's heads, then the chunk's query
+// tiles, as in attn_dkv_kernel, and every accumulator takes its products in the same order: the
+// partial sums are bitwise the same.  grid (S Hkv ceil(nt / 4), nch).
+template <int HD>
+__global__ __launch_bounds__(256) void attn_dkv_lds_kernel(const uint16_t* __restrict__ dSth,
+                                                           const uint16_t* __restrict__ dStl,
+                                                           const uint16_t* __restrict__ Pth,
+                                                           const uint16_t* __restrict__ Ptl,
+                                                           const uint16_t* __restrict__ qt,
+                                                           const uint16_t* __restrict__ dOth,
+                                                           const uint16_t* __restrict__ dOtl, int64_t T, int64_t H,
+                                                           int64_t Hkv, int64_t L, float* __restrict__ part) {
+    constexpr int NCT = HD / AT;
+    constexpr int BT = HD * AT;                       // bf16 per B tile
+    constexpr int BCH = 3 * HD * 4 / 256;             // 16-byte chunks per thread and step
+    static_assert(3 * HD * 4 % 256 == 0, "head width");
+    __shared__ __attribute__((aligned(16))) uint16_t sB[2][3][BT];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t nt = L / AT, ng = (nt + 3) / 4;
+    const int64_t jg = blockIdx.x % ng, sg = blockIdx.x / ng, g = sg % Hkv, s = sg / Hkv;
+    const int64_t z = blockIdx.y;
+    const int64_t jt = 4 * jg + wave;
+    const int64_t i0 = (4 * jg > z * CH ? 4 * jg : z * CH), i1 = ((z + 1) * CH < nt ? (z + 1) * CH : nt);
+    if (i0 >= i1) return;                             // the whole chunk lies before the group's key tiles
+    const bool wave_on = jt < nt && (z + 1) * CH > jt;  // this wave's key tile has terms in the chunk
+    const int64_t rep = H / Hkv;
+    const int64_t nsteps = rep * (i1 - i0);
+    const int c32 = lane & 31, k8 = 8 * (lane >> 5);
+    const uint16_t* Bsrc[3] = {qt, dOth, dOtl};
+    // step x: head hh = x / (i1 - i0), query tile it = i0 + x % (i1 - i0)
+    auto step_of = [&](int64_t x, int64_t& h, int64_t& it) {
+        h = g * rep + x / (i1 - i0);
+        it = i0 + x % (i1 - i0);
+    };
+    u16x8 breg[BCH];
+    auto load_B = [&](int64_t x) {
+        int64_t h, it;
+        step_of(x, h, it);
+#pragma unroll
+        for (int q = 0; q < BCH; ++q) {
+            const int id = threadIdx.x + 256 * q;
+            const int a = id / (HD * 4), row = (id % (HD * 4)) >> 2, c = id & 3;
+            breg[q] = *reinterpret_cast<const u16x8*>(Bsrc[a] + (h * HD + row) * T + s * L + it * AT + c * 8);
+        }
+    };
+    auto store_B = [&](int b) {
+#pragma unroll
+        for (int q = 0; q < BCH; ++q) {
+            const int id = threadIdx.x + 256 * q;
+            const int a = id / (HD * 4), row = (id % (HD * 4)) >> 2, c = id & 3;
+            *reinterpret_cast<u16x8*>(&sB[b][a][row * AT + ((c ^ vswz(row)) * 8)]) = breg[q];
+        }
+    };
+    struct AF {
+        bf16x8 sh[2], sl[2], ph[2], pl[2];
+    };
+    auto load_A = [&](int64_t x, AF& f) {
+        int64_t h, it;
+        step_of(x, h, it);
+        const int64_t sh = s * H + h;
+        const int64_t arow = (sh * L + jt * AT + c32) * L + it * AT + k8;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            f.sh[u] = ld8(dSth + arow + 16 * u);
+            f.sl[u] = ld8(dStl + arow + 16 * u);
+            f.ph[u] = ld8(Pth + arow + 16 * u);
+            f.pl[u] = ld8(Ptl + arow + 16 * u);
+        }
+    };
+    auto active = [&](int64_t x) {
+        int64_t h, it;
+        step_of(x, h, it);
+        return wave_on && it >= jt;
+    };
+    f32x16 ak[NCT], av[NCT];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        ak[ct] = zero16();
+        av[ct] = zero16();
+    }
+    AF acur, anxt;
+    if (active(0)) load_A(0, acur);
+    load_B(0);
+    store_B(0);
+    __syncthreads();
+    for (int64_t x = 0; x < nsteps; ++x) {
+        const bool more = x + 1 < nsteps;
+        if (more && active(x + 1)) load_A(x + 1, anxt);
+        if (more) load_B(x + 1);
+        if (active(x)) {
+            const uint16_t* bq = sB[x & 1][0];
+            const uint16_t* bh = sB[x & 1][1];
+            const uint16_t* bl = sB[x & 1][2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int c = 2 * u + (lane >> 5);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const int row = ct * AT + c32;
+                    const int off = row * AT + ((c ^ vswz(row)) * 8);
+                    const bf16x8 q = ld8(bq + off), doh = ld8(bh + off), dol = ld8(bl + off);
+                    ak[ct] = mfma(acur.sh[u], q, ak[ct]);
+                    ak[ct] = mfma(acur.sl[u], q, ak[ct]);
+                    av[ct] = mfma(acur.ph[u], doh, av[ct]);
+                    av[ct] = mfma(acur.pl[u], doh, av[ct]);
+                    av[ct] = mfma(acur.ph[u], dol, av[ct]);
+                }
+            }
+        }
+        if (more) store_B((int)((x + 1) & 1));
+        __syncthreads();
+        acur = anxt;
+    }
+    if (!wave_on) return;
+    const float scale = (float)(1.0 / sqrt((double)HD));
+    const int64_t TK = T * Hkv * HD;
+    float* pk = part + 2 * z * TK;
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int64_t col = g * HD + ct * AT + c32;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int64_t t = s * L + jt * AT + acc_row(e, lane);
+            pk[t * Hkv * HD + col] = ak[ct][e] * scale;
+            pk[TK + t * Hkv * HD + col] = av[ct][e];
+        }
+    }
+}
+
 // dk, dv [T][Hkv hd] = sum over the chunks z of token t's key tile and after (z ascending: a fixed
 // order) of the partial sums.
 __global__ void attn_dkv_reduce_kernel(const float* __restrict__ part, int64_t T, int64_t K, int64_t L,
@@ -816,8 +951,16 @@ hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const 
                        Hkv, hd, L, dq);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t nch = attn_dkv_chunks(L);
-    hipLaunchKernelGGL(attn_dkv_kernel, dim3((unsigned)(S * Hkv * nt), cy, (unsigned)nch), dim3(256), 0, st, w.dSth,
-                       w.dStl, w.Pth, w.Ptl, w.qt, w.dOth, w.dOtl, T, H, Hkv, hd, L, w.part);
+    const bool dkv_lds = T % 8 == 0 && (hd == 128 || hd == 64) && S * Hkv * ((nt + 3) / 4) * nch >= 64;
+    if (dkv_lds && hd == 128)
+        hipLaunchKernelGGL((attn_dkv_lds_kernel<128>), dim3((unsigned)(S * Hkv * ((nt + 3) / 4)), (unsigned)nch),
+                           dim3(256), 0, st, w.dSth, w.dStl, w.Pth, w.Ptl, w.qt, w.dOth, w.dOtl, T, H, Hkv, L, w.part);
+    else if (dkv_lds)
+        hipLaunchKernelGGL((attn_dkv_lds_kernel<64>), dim3((unsigned)(S * Hkv * ((nt + 3) / 4)), (unsigned)nch),
+                           dim3(256), 0, st, w.dSth, w.dStl, w.Pth, w.Ptl, w.qt, w.dOth, w.dOtl, T, H, Hkv, L, w.part);
+    else
+        hipLaunchKernelGGL(attn_dkv_kernel, dim3((unsigned)(S * Hkv * nt), cy, (unsigned)nch), dim3(256), 0, st,
+                           w.dSth, w.dStl, w.Pth, w.Ptl, w.qt, w.dOth, w.dOtl, T, H, Hkv, hd, L, w.part);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(attn_dkv_reduce_kernel, dim3(grid_of(T * Hkv * hd)), dim3(TB), 0, st, w.part, T, Hkv * hd, L, nch,
                        dk, dv);
