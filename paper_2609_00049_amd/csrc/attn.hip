@@ -705,6 +705,98 @@ __global__ __launch_bounds__(256) void attn_dq_kernel(const uint16_t* __restrict
     for (int e = 0; e < 16; ++e) dq[(s * L + it * AT + acc_row(e, lane)) * H * hd + col] = acc[e] * scale;
 }
 
+// attn_dq_kernel with the four waves of a block on four consecutive query tiles of one head (the
+// longest first), each computing every value-column tile: the k^T tile of a key tile (the head's
+// HD rows over its 32 tokens) is loaded once per block, one step ahead into registers, and stored
+// to one of two LDS buffers (rows swizzled as the forward's value tile); each wave's dS hi/lo
+// fragments are loaded one step ahead.  Every accumulator takes its products in the old order,
+// so dq is bitwise the same.  grid (S H ceil(nt / 4)).
+template <int HD>
+__global__ __launch_bounds__(256) void attn_dq_lds_kernel(const uint16_t* __restrict__ dSh,
+                                                          const uint16_t* __restrict__ dSl,
+                                                          const uint16_t* __restrict__ kt, int64_t T, int64_t H,
+                                                          int64_t Hkv, int64_t L, float* __restrict__ dq) {
+    constexpr int NCT = HD / AT;
+    constexpr int BT = HD * AT;
+    constexpr int BCH = HD * 4 / 256;                 // 16-byte chunks per thread and step
+    static_assert(HD * 4 % 256 == 0, "head width");
+    __shared__ __attribute__((aligned(16))) uint16_t sB[2][BT];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t nt = L / AT, nq = (nt + 3) / 4;
+    const int64_t sh = blockIdx.x / nq, h = sh % H, s = sh / H;
+    const int64_t qb = blockIdx.x % nq;
+    const int64_t itmax = nt - 1 - 4 * qb;
+    const int64_t it = itmax - wave;
+    const int64_t g = h / (H / Hkv);
+    const int c32 = lane & 31, k8 = 8 * (lane >> 5);
+    u16x8 breg[BCH];
+    auto load_B = [&](int64_t jt) {
+#pragma unroll
+        for (int q = 0; q < BCH; ++q) {
+            const int id = threadIdx.x + 256 * q;
+            const int row = id >> 2, c = id & 3;
+            breg[q] = *reinterpret_cast<const u16x8*>(kt + (g * HD + row) * T + s * L + jt * AT + c * 8);
+        }
+    };
+    auto store_B = [&](int b) {
+#pragma unroll
+        for (int q = 0; q < BCH; ++q) {
+            const int id = threadIdx.x + 256 * q;
+            const int row = id >> 2, c = id & 3;
+            *reinterpret_cast<u16x8*>(&sB[b][row * AT + ((c ^ vswz(row)) * 8)]) = breg[q];
+        }
+    };
+    struct AF {
+        bf16x8 h[2], l[2];
+    };
+    const int64_t arow = (sh * L + it * AT + c32) * L + k8;
+    auto load_A = [&](int64_t jt, AF& f) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            f.h[u] = ld8(dSh + arow + jt * AT + 16 * u);
+            f.l[u] = ld8(dSl + arow + jt * AT + 16 * u);
+        }
+    };
+    f32x16 acc[NCT];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) acc[ct] = zero16();
+    AF acur, anxt;
+    if (it >= 0) load_A(0, acur);
+    load_B(0);
+    store_B(0);
+    __syncthreads();
+    for (int64_t jt = 0; jt <= itmax; ++jt) {
+        const bool more = jt + 1 <= itmax;
+        if (more && jt + 1 <= it) load_A(jt + 1, anxt);
+        if (more) load_B(jt + 1);
+        if (jt <= it) {
+            const uint16_t* bt = sB[jt & 1];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int c = 2 * u + (lane >> 5);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const int row = ct * AT + c32;
+                    const bf16x8 b = ld8(bt + row * AT + ((c ^ vswz(row)) * 8));
+                    acc[ct] = mfma(acur.h[u], b, acc[ct]);
+                    acc[ct] = mfma(acur.l[u], b, acc[ct]);
+                }
+            }
+        }
+        if (more) store_B((int)((jt + 1) & 1));
+        __syncthreads();
+        acur = anxt;
+    }
+    if (it < 0) return;
+    const float scale = (float)(1.0 / sqrt((double)HD));
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int64_t col = h * HD + ct * AT + c32;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) dq[(s * L + it * AT + acc_row(e, lane)) * H * HD + col] = acc[ct][e] * scale;
+    }
+}
+
 // Query tiles per chunk of the dK/dV sums: each (key tile, chunk) pair is one wave, so no wave
 // walks more than CH query tiles per head.
 constexpr int CH = 8;
@@ -947,8 +1039,16 @@ hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const 
                            kr, LSE, dO, v, w.D, H, Hkv, hd, L, w.dSh, w.dSl, w.dSth, w.dStl, w.Pth, w.Ptl);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const unsigned cy = (unsigned)((hd / AT + 3) / 4);
-    hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)(S * H * nt), cy), dim3(256), 0, st, w.dSh, w.dSl, w.kt, T, H,
-                       Hkv, hd, L, dq);
+    const bool dq_lds = T % 8 == 0 && (hd == 128 || hd == 64) && S * H * ((nt + 3) / 4) >= 64;
+    if (dq_lds && hd == 128)
+        hipLaunchKernelGGL((attn_dq_lds_kernel<128>), dim3((unsigned)(S * H * ((nt + 3) / 4))), dim3(256), 0, st, w.dSh,
+                           w.dSl, w.kt, T, H, Hkv, L, dq);
+    else if (dq_lds)
+        hipLaunchKernelGGL((attn_dq_lds_kernel<64>), dim3((unsigned)(S * H * ((nt + 3) / 4))), dim3(256), 0, st, w.dSh,
+                           w.dSl, w.kt, T, H, Hkv, L, dq);
+    else
+        hipLaunchKernelGGL(attn_dq_kernel, dim3((unsigned)(S * H * nt), cy), dim3(256), 0, st, w.dSh, w.dSl, w.kt, T, H,
+                           Hkv, hd, L, dq);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t nch = attn_dkv_chunks(L);
     const bool dkv_lds = T % 8 == 0 && (hd == 128 || hd == 64) && S * Hkv * ((nt + 3) / 4) * nch >= 64;
