@@ -423,7 +423,11 @@ def config_legs(torch, rq, ctx, qp):
             window = (0, -(-n // qp.block))
         bgd = rq.bgd_params(steps=K, lr=lr, tok_chunk=chunk)
         o = rq.quantize_layer(ctx, W0, X, Xh, s, M, P, qp=qp, bgd=bgd, window=window)
+        ctx.set_timing(True)
+        ctx.reset_timing()
         o = rq.quantize_layer(ctx, W0, X, Xh, s, M, P, qp=qp, bgd=bgd, window=window, out=o)
+        kt = {kn: ctx.kernel_time(kn)[1] for kn in ("resid", "grad", "metric", "adam", "lock", "quantize",
+                                                          "chol", "init", "dense_loss")}
         fa = f_alg(m, n, T, K)
         dense_terms = (1 if M is not None else 0) + (1 if P is not None else 0)
         fl = fa["total"] + dense_terms * K * 2.0 * m * m * fa["SJ"]
@@ -432,7 +436,11 @@ def config_legs(torch, rq, ctx, qp):
         out[name] = {"m": m, "n": n, "tokens": T, "bgd_steps": K, "dense_metric": M is not None,
                      "window_partner": partner, "ms": o.ms_total, "columns_per_s": n / (o.ms_total / 1e3),
                      "tflops_alg": fl / (o.ms_total / 1e3) / 1e12, "frac_bf16_peak_alg": fl / (o.ms_total / 1e3) / PEAK_BF16,
-                     "loss_final": o.loss_final}
+                     "loss_final": o.loss_final, "kernel_ms": {k: round(v, 2) for k, v in kt.items() if v > 0}}
+        if kt["metric"] > 0:
+            # the dense-metric products: K 2 m^2 SJ algorithmic FLOPs, three bf16 MFMA passes executed
+            fm = K * 2.0 * m * m * fa["SJ"]
+            out[name]["metric_tflops_alg"] = fm / (kt["metric"] / 1e3) / 1e12
         del W0, X, Xh, s, M, P, o
         torch.cuda.empty_cache()
     WORKLOADS.pop("_leg", None)
