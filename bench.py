@@ -481,6 +481,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="llama3.1_8b_gate", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tok-chunk", type=int, default=None,
+                    help="stream the tokens through the Block-GD GEMMs in chunks of this many (default: the "
+                         "workload's own setting, 0 = all tokens at once)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run one plain device copy of this many bytes first (calibrates HBM byte counters)")
     ap.add_argument("--form", default="tokens", choices=("tokens", "gram"),
@@ -537,7 +540,8 @@ def main():
     ctx = rq.Context()
     qp = rq.qparams()
     form = rq.BGD_GRAM if args.form == "gram" else rq.BGD_TOKENS
-    bgd = rq.bgd_params(steps=K, lr=lr, form=form, tok_chunk=TOKEN_CHUNK.get(args.workload, 0))
+    tok_chunk = TOKEN_CHUNK.get(args.workload, 0) if args.tok_chunk is None else args.tok_chunk
+    bgd = rq.bgd_params(steps=K, lr=lr, form=form, tok_chunk=tok_chunk)
     if args.only == "stage0":
         ctx.set_timing(True)
         print(json.dumps({"stage0": stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n,
@@ -595,7 +599,7 @@ def main():
         "data": "synthetic (device-generated, workload distributions)",
         "config": {"workload": args.workload, "m": m, "n": n, "tokens": T, "bgd_steps": K, "bits": 4,
                    "group": 128, "block": 128, "bgd_form": args.form,
-                   "token_chunk": TOKEN_CHUNK.get(args.workload, 0)},
+                   "token_chunk": tok_chunk},
         "tflops_alg": sweep_rate / 1e12,
         "frac_bf16_peak_alg": sweep_rate / PEAK_BF16,
         "mfma_peak_measured_tflops": peak_meas / 1e12,
@@ -603,7 +607,8 @@ def main():
         "kernel_ms_per_step": {k: v[1] / args.steps for k, v in kt.items()},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16,
-                     "traffic": measured_traffic(args.workload, dom) if args.form == "tokens" else None,
+                     "traffic": (measured_traffic(args.workload, dom) if args.form == "tokens"
+                                 and tok_chunk == TOKEN_CHUNK.get(args.workload, 0) else None),
                      "launches": launches, "avg_launch_ms": dom_ms / max(1, launches),
                      "measured_peak": peak_meas / 1e12, "frac_measured_peak": achieved / peak_meas,
                      "executed_frac": 2.0 * achieved / PEAK_BF16 if args.form == "tokens" else None,

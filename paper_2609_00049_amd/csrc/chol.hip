@@ -11,7 +11,12 @@
 //   Cholesky right-looking, 64-wide panels: factor the diagonal block in one
 //            workgroup (and invert it), triangular-solve the panel below, update the
 //            trailing lower triangle.
-//   inverse  block rows of X = L^{-1}: X_ii = L_ii^{-1}, X_ij = -L_ii^{-1} sum_{j<=k<i} L_ik X_kj.
+//   inverse  X = L^{-1} by recursive doubling: with the aligned diagonal blocks of size s already
+//            inverted (s = 64: the diagonal factor's own inverses), each aligned block of size 2s
+//            [[L_A, 0], [L_CA, L_C]] gets its lower-left block X_CA = -X_C (L_CA X_A), two batched
+//            float64 tile products per level that skip the tiles where a triangular operand is
+//            zero; the intermediate L_CA X_A is parked, transposed, in the unused upper triangle of
+//            the factor's work array.
 //   U        U[i][j] = X[n-1-i][n-1-j] (j >= i), stored as float32.
 #include "common.h"
 #include "kernels.h"
@@ -205,37 +210,115 @@ __global__ __launch_bounds__(256) void chol_syrk_kernel(double* A, int64_t np, i
         for (int j = 0; j < 4; ++j) C[(ty * 4 + i) * np + tx * 4 + j] -= acc[i][j];
 }
 
-// ---------------------------------------------------------------- block row ib of X = L^{-1}
-// X[ib][jb] = -Linv_ib * sum_{kb=jb}^{ib-1} L[ib][kb] X[kb][jb], one block per jb < ib.
-__global__ __launch_bounds__(256) void chol_inv_row_kernel(const double* __restrict__ A, double* X, int64_t np,
-                                                           int64_t ib, const double* __restrict__ diaginv) {
-    __shared__ double sa[NB][NB + 1];
-    __shared__ double sb[NB][NB + 1];
-    const int64_t jb = blockIdx.x;
+// ---------------------------------------------------------------- triangular inverse, one doubling level
+// C (M x N) = alpha * A (M x K) * B (K x N) for every pair p of the level, all dimensions multiples
+// of 64.  Element (i, k) of A sits at A[i * lda + k] (A_KC) or A[i + k * lda]; element (k, j) of B at
+// B[k + j * ldb] (B_KC) or B[k * ldb + j]; element (i, j) of C at C[i * ldc + j] (C_ROW) or
+// C[i + j * ldc].  Pair p offsets every base by p * 2s (1 + ld) and has M_p = min(s, np - p*2s - s)
+// rows.  TRI_B: B is lower triangular, so output column tile jt needs k >= 64 jt; TRI_A: A is lower
+// triangular, so row tile it needs k < 64 (it + 1).  A 64 x 64 output tile per block, 4 x 4 per
+// thread, K in slices of 16 through two LDS buffers.
+namespace {
+constexpr int KS = 16;
+constexpr int SP = 64 + 2;  // padded LDS row: 16-byte aligned, transposed stores spread over banks
+
+// one 64 x 16 operand slice: outer index o (row of A, column of B) and k.  KC: consecutive k adjacent.
+template <bool KC>
+__device__ __forceinline__ void slice_load(double (&r)[4], const double* __restrict__ p, int64_t ld) {
+    const int t = threadIdx.x;
+    if constexpr (KC) {
+        const double2* q = reinterpret_cast<const double2*>(p + (int64_t)(t >> 2) * ld + (t & 3) * 4);
+        const double2 u = q[0], v = q[1];
+        r[0] = u.x; r[1] = u.y; r[2] = v.x; r[3] = v.y;
+    } else {
+        const double2* q = reinterpret_cast<const double2*>(p + (int64_t)(t >> 4) * ld + (t & 15) * 4);
+        const double2 u = q[0], v = q[1];
+        r[0] = u.x; r[1] = u.y; r[2] = v.x; r[3] = v.y;
+    }
+}
+template <bool KC>
+__device__ __forceinline__ void slice_store(double (*sx)[SP], const double (&r)[4]) {
+    const int t = threadIdx.x;
+    if constexpr (KC) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) sx[(t & 3) * 4 + q][t >> 2] = r[q];
+    } else {
+        double2* d = reinterpret_cast<double2*>(&sx[t >> 4][(t & 15) * 4]);
+        d[0] = make_double2(r[0], r[1]);
+        d[1] = make_double2(r[2], r[3]);
+    }
+}
+}  // namespace
+
+template <bool A_KC, bool B_KC, bool C_ROW, bool TRI_A, bool TRI_B>
+__global__ __launch_bounds__(256) void chol_pair_gemm_kernel(const double* __restrict__ A, int64_t lda,
+                                                             const double* __restrict__ B, int64_t ldb,
+                                                             double* __restrict__ C, int64_t ldc, int64_t np,
+                                                             int64_t s, int64_t N, int64_t Kfull, bool k_is_m,
+                                                             double alpha) {
+    __shared__ __attribute__((aligned(16))) double sa[2][KS][SP];
+    __shared__ __attribute__((aligned(16))) double sb[2][KS][SP];
+    const int64_t p = blockIdx.z;
+    const int64_t off = p * 2 * s;
+    const int64_t Mp = np - off - s < s ? np - off - s : s;  // rows of this pair's C block
+    const int64_t it = blockIdx.y, jt = blockIdx.x;
+    if (it * 64 >= Mp || jt * 64 >= N) return;
+    const int64_t K = k_is_m ? Mp : Kfull;
+    int64_t k_lo = 0, k_hi = K;
+    if constexpr (TRI_B) k_lo = jt * 64;
+    if constexpr (TRI_A) k_hi = (it + 1) * 64 < K ? (it + 1) * 64 : K;
+    const double* Ap = A + off * (lda + 1) + (A_KC ? it * 64 * lda : it * 64);
+    const double* Bp = B + off * (ldb + 1) + (B_KC ? jt * 64 * ldb : jt * 64);
+    auto a_at = [&](int64_t k) { return A_KC ? Ap + k : Ap + k * lda; };
+    auto b_at = [&](int64_t k) { return B_KC ? Bp + k : Bp + k * ldb; };
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
     double acc[4][4];
-    zero_acc(acc);
-    for (int64_t kb = jb; kb < ib; ++kb) {
-        __syncthreads();
-        load_tile(sa, A + ib * NB * np + kb * NB, np);
-        load_tile(sb, X + kb * NB * np + jb * NB, np);
-        __syncthreads();
-        tile_mac_nn(acc, sa, sb);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+    double ra[4], rb[4];
+    if (k_lo < k_hi) {
+        slice_load<A_KC>(ra, a_at(k_lo), lda);
+        slice_load<B_KC>(rb, b_at(k_lo), ldb);
+        slice_store<A_KC>(sa[0], ra);
+        slice_store<B_KC>(sb[0], rb);
     }
     __syncthreads();
-    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    int cur = 0;
+    for (int64_t k = k_lo; k < k_hi; k += KS) {
+        const bool more = k + KS < k_hi;
+        if (more) {
+            slice_load<A_KC>(ra, a_at(k + KS), lda);
+            slice_load<B_KC>(rb, b_at(k + KS), ldb);
+        }
+#pragma unroll 4
+        for (int kk = 0; kk < KS; ++kk) {
+            const double2* pa = reinterpret_cast<const double2*>(&sa[cur][kk][ty * 4]);
+            const double2* pb = reinterpret_cast<const double2*>(&sb[cur][kk][tx * 4]);
+            const double2 a01 = pa[0], a23 = pa[1], b01 = pb[0], b23 = pb[1];
+            const double a[4] = {a01.x, a01.y, a23.x, a23.y};
+            const double b[4] = {b01.x, b01.y, b23.x, b23.y};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fma(a[i], b[j], acc[i][j]);
+        }
+        if (more) {
+            slice_store<A_KC>(sa[cur ^ 1], ra);
+            slice_store<B_KC>(sb[cur ^ 1], rb);
+        }
+        __syncthreads();
+        cur ^= 1;
+    }
+    double* Cp = C + off * (ldc + 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sb[ty * 4 + i][tx * 4 + j] = acc[i][j];
-    load_tile(sa, diaginv + ib * NB * NB, NB);
-    __syncthreads();
-    zero_acc(acc);
-    tile_mac_nn(acc, sa, sb);
-    double* C = X + ib * NB * np + jb * NB;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) C[(ty * 4 + i) * np + tx * 4 + j] = -acc[i][j];
+        for (int j = 0; j < 4; ++j) {
+            const int64_t r = it * 64 + ty * 4 + i, c = jt * 64 + tx * 4 + j;
+            Cp[C_ROW ? r * ldc + c : r + c * ldc] = alpha * acc[i][j];
+        }
 }
 
 __global__ void chol_extract_u_kernel(const double* __restrict__ X, int64_t np, int64_t n, float* __restrict__ U) {
@@ -276,9 +359,20 @@ hipError_t chol_inverse(const CholArgs& c, hipStream_t st) {
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    for (int64_t ib = 1; ib < nb; ++ib) {
-        hipLaunchKernelGGL(chol_inv_row_kernel, dim3((unsigned)ib), dim3(256), 0, st, c.A, c.Linv, np, ib,
-                           c.diaginv);
+    // X = L^{-1}: the diagonal 64-blocks came out of the factorisation; level s completes every
+    // aligned 2s block (the last one cut at np) from its two inverted halves
+    for (int64_t sz = NB; sz < np; sz *= 2) {
+        const unsigned t = (unsigned)(sz / NB);
+        const unsigned pairs = (unsigned)((np - sz + 2 * sz - 1) / (2 * sz));
+        // T1 = L_CA X_A, stored transposed above the diagonal of the factor's array
+        hipLaunchKernelGGL((chol_pair_gemm_kernel<true, false, false, false, true>), dim3(t, t, pairs), dim3(256), 0,
+                           st, c.A + sz * np, np, c.Linv, np, c.A + sz, np, np, sz, sz, sz, false, 1.0);
+        // X_CA = -X_C T1
+        hipLaunchKernelGGL((chol_pair_gemm_kernel<true, true, true, true, false>), dim3(t, t, pairs), dim3(256), 0,
+                           st, c.Linv + sz * np + sz, np, c.A + sz, np, c.Linv + sz * np, np, np, sz, sz, 0, true,
+                           -1.0);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(chol_extract_u_kernel, dim3(grid_of(n * n)), dim3(256), 0, st, c.Linv, np, n, c.U);
     return hipGetLastError();
