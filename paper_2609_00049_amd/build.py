@@ -62,7 +62,8 @@ def build(verbose: bool = False) -> Path:
     with ThreadPoolExecutor(workers) as ex:
         objs = list(ex.map(lambda p: _compile(p, verbose), srcs))
     tmp = LIB.with_suffix(".so.tmp")
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *[str(o) for o in objs], "-o", str(tmp)]
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *[str(o) for o in objs],
+           "-lrocprofiler-sdk-roctx", "-o", str(tmp)]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

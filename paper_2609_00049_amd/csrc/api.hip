@@ -1127,6 +1127,10 @@ int realq_quantize_layer(realq_ctx* ctx, const realq_layer_desc* d, realq_layer_
     if (out->loss_trace && bgd) RQ_HIP(ctx, realq::fill_f64(out->loss_trace, NAN, nb * d->bgd.steps, s));
     for (int64_t b = 0; b < nb; ++b) {
         const int64_t c0 = b * d->q.block, bs = std::min<int64_t>(d->q.block, n - c0), c1 = c0 + bs;
+        char rname[48];
+        snprintf(rname, sizeof(rname), "block %lld (columns %lld..%lld)", (long long)b, (long long)c0,
+                 (long long)(c1 - 1));
+        realq::Range block_range(rname);
         for (int64_t g = 0; g < ngr; ++g) {
             if ((rc = quantize_rows(ctx, W, m, n, g * rsz, std::min(m, (g + 1) * rsz), c0, bs,
                                     (const float*)Uw + g * n * n, (const uint8_t*)deadw + g * n, &d->q, out->codes,

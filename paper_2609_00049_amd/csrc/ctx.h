@@ -5,6 +5,8 @@
 #include <string>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "common.h"
 
 struct realq_ctx {
@@ -54,12 +56,23 @@ int validate_bgd(realq_ctx* ctx, const realq_bgd_params* p);
 int hessian_accum_chunks(realq_ctx* ctx, const uint16_t* Xhat, const float* s, int64_t T, int64_t n, double* H_acc,
                          int64_t tc, uint16_t* xt, uint16_t* hi, uint16_t* lo, uint16_t* lo2, bool timed);
 
-// Brackets the launches of its scope with events on the context stream when timing is on.
+// A roctx range over a host scope: the launches it encloses show under its name in a
+// `rocprofv3 --marker-trace` run (the push is a no-op call when no tool is attached).
+struct Range {
+    explicit Range(const char* n) { roctxRangePushA(n); }
+    ~Range() { roctxRangePop(); }
+    Range(const Range&) = delete;
+    Range& operator=(const Range&) = delete;
+};
+
+// Brackets the launches of its scope with events on the context stream when timing is on, and
+// with a roctx range of the same name.
 struct Timed {
     realq_ctx* ctx;
     const char* name;
     hipEvent_t a = nullptr, b = nullptr;
-    Timed(realq_ctx* c, const char* n) : ctx(c), name(n) {
+    Range range;
+    Timed(realq_ctx* c, const char* n) : ctx(c), name(n), range(n ? n : "realq") {
         if (!ctx->timing || !n) return;
         if (!ctx->free_events.empty()) {
             a = ctx->free_events.back().first;
