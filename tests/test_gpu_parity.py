@@ -63,6 +63,58 @@ def test_hessian_and_inverse_factor(rq, ctx, case):
     assert np.abs(Ug - U_ref).max() <= 1e-4 * np.abs(U_ref).max()
 
 
+@pytest.mark.parametrize("n", [20000, 28672])
+def test_inverse_factor_at_model_widths(rq, ctx, n):
+    """The inverse factor at the widths of the largest down projections (28672: LLaMA-3.1-70B;
+    20000: a width that is not a multiple of the 64-wide panels, so the padded last panel and the
+    cut-off last pair of every doubling level are exercised) through the property that defines
+    it: U upper triangular with a positive diagonal and H_d^{-1} = U^T U, i.e. U H_d U^T = I, with
+    H_d the oracle's damping of the accumulated Hessian.  Checked on four random probe vectors
+    (every row and column of U enters) and on a 16 x 16 block of sampled rows, each entry against
+    four times the float32 rounding bound 2 * 2^-24 (|U| |H_d| |U|^T)."""
+    torch = _torch()
+    T = 8192
+    _banner(f"inverse factor n={n} T={T}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(n)
+    Xh = torch.randn((T, n), generator=g, device="cuda")
+    Xh[:, :: max(1, n // 64)] *= 20.0          # outlier channels
+    Xh[:, n // 3] = 0.0                          # a dead channel
+    Xh = Xh.to(torch.bfloat16)
+    Hacc = torch.zeros((n, n), dtype=torch.float64, device="cuda")
+    rq.hessian_accum(ctx, Xh, None, Hacc)
+    del Xh
+    U = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    dead = torch.empty((n,), dtype=torch.uint8, device="cuda")
+    rq.chol_inverse(ctx, Hacc, T, 0.01, U, None, dead)
+    torch.cuda.synchronize()
+    assert int(torch.count_nonzero(torch.tril(U, -1))) == 0
+    assert bool((torch.diagonal(U) > 0).all())
+    Hd, dead_ref = damp_hessian(Hacc.cpu().numpy() * (2.0 / T), 0.01)
+    del Hacc
+    np.testing.assert_array_equal(dead.cpu().numpy().astype(bool), dead_ref)
+    U64 = U.cpu().numpy().astype(np.float64)
+    del U
+    torch.cuda.empty_cache()
+    aU, aH = np.abs(U64), np.abs(Hd)
+    rel = 8.0 * 2.0 ** -24
+    rng = np.random.default_rng(n)
+    worst = 0.0
+    for _ in range(4):
+        x = rng.standard_normal(n)
+        w = U64 @ (Hd @ (U64.T @ x))
+        bound = aU @ (aH @ (aU.T @ np.abs(x)))
+        worst = max(worst, float(np.max(np.abs(w - x) / bound)))
+        assert np.all(np.abs(w - x) <= rel * bound)
+    rows = np.sort(rng.choice(n, size=16, replace=False))
+    Ur = U64[rows]
+    E = Ur @ Hd @ Ur.T - np.eye(16)
+    bound = aU[rows] @ aH @ aU[rows].T
+    worst = max(worst, float(np.max(np.abs(E) / bound)))
+    print("worst |U H U^T - I| / (|U||H||U|^T):", worst, "bar", rel, flush=True)
+    assert np.all(np.abs(E) <= rel * bound)
+
+
 def test_not_positive_definite_is_reported(rq, ctx):
     torch = _torch()
     n = 64
