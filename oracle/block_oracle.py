@@ -394,12 +394,13 @@ def decoder_surrogate(fw: DecoderForward, ystar, blk: DecoderBlock, T, W=None, n
 
 def decoder_block_sweep(X, Xhat, blk: DecoderBlock, *, qp: Optional[QParams] = None, steps=0, lr=1e-3,
                         nxt: Optional[DecoderBlock] = None, window=False, eps=RMS_EPS,
-                        batch: Optional[int] = None):
+                        batch: Optional[int] = None, modules=DECODER_MODULES):
     """Quantize q, k, v, o, gate, up and down of one decoder block in order (Alg. 1): GPTQ on each
     module's input in the quantized path and Block-GD on the block-output surrogate after every
     column block; window=True blends in ``nxt`` over b_global across the seven modules.
     ``batch``: tokens per Adam step (Sec. 4.3 mini-batch), a multiple of seq_len so that every
-    batch holds whole calibration sequences (attention mixes the tokens of a sequence)."""
+    batch holds whole calibration sequences (attention mixes the tokens of a sequence).
+    ``modules``: the leading modules to sweep (q, then k, ...); the rest keep their given weights."""
     qp = qp or QParams()
     X, Xhat = _f64(X), _f64(Xhat)
     T = X.shape[0]
@@ -415,7 +416,9 @@ def decoder_block_sweep(X, Xhat, blk: DecoderBlock, *, qp: Optional[QParams] = N
         B_total += nb[k]
     inputs = {"q": "h1", "k": "h1", "v": "h1", "o": "O"}
     res = {}
-    for name in DECODER_MODULES:
+    if tuple(modules) != DECODER_MODULES[:len(modules)]:
+        raise ValueError("decoder_block_sweep: modules must be a leading run of q, k, v, o, gate, up, down")
+    for name in modules:
         fw = decoder_forward(Xhat, blk, W, eps)
         inp = getattr(fw, inputs[name]) if name in inputs else (fw.mlp.u if name != "down" else fw.mlp.z)
 

@@ -293,6 +293,24 @@ def _dec_inputs(seed=30):
     return inp.X, inp.Xhat, blk
 
 
+def test_decoder_sweep_of_leading_modules_matches_the_full_sweep():
+    """Sweeping only q and k gives their codes and weights of the full sweep (the later modules
+    come after them in Alg. 1), and the final loss is taken with the rest at their given weights."""
+    X, Xh, blk = _dec_inputs(31)
+    full = B.decoder_block_sweep(X, Xh, blk, steps=1, lr=1e-4)
+    part = B.decoder_block_sweep(X, Xh, blk, steps=1, lr=1e-4, modules=("q", "k"))
+    assert sorted(part.modules) == ["k", "q"]
+    for name in ("q", "k"):
+        assert (part.modules[name].codes == full.modules[name].codes).all(), name
+        assert np.array_equal(part.modules[name].W_hat, full.modules[name].W_hat), name
+    W = {k: np.asarray(v, np.float64) for k, v in blk.weights().items()}
+    W["q"], W["k"] = part.modules["q"].W_hat, part.modules["k"].W_hat
+    y = B.decoder_forward(Xh, blk, W).y
+    assert part.loss_final == B.fisher_loss(y - part.ystar, blk.F, X.shape[0])
+    with pytest.raises(ValueError):
+        B.decoder_block_sweep(X, Xh, blk, modules=("k",))
+
+
 def test_decoder_sweep_without_bgd_is_gptq_on_each_modules_input():
     X, Xh, blk = _dec_inputs()
     res = B.decoder_block_sweep(X, Xh, blk, steps=0)

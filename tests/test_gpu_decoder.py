@@ -342,3 +342,37 @@ def test_decoder_ragged_and_degenerate_shapes(rq, ctx):
     # o (one partial block) and the last block of every module take no Block-GD step
     off = 3 * 2 * 3
     assert np.isnan(tr[off:off + 2]).all()
+
+
+def test_decoder_lds_attention_ragged_tile_count(rq, ctx):
+    """The LDS-staged attention kernels (forward, dS, dQ and dK/dV, which take 4 consecutive
+    32-token tiles per block) at a tile count that is not a multiple of 4: 160-token sequences
+    (5 tiles, so every sequence's second block has 3 idle waves), 16 sequences of 16 query heads
+    over 4 key/value heads of 64, enough blocks that every LDS kernel's launch condition holds.
+    q (its gradient through dS and dQ) and then k (through dS and dK), each with one Block-GD step
+    per block; k runs teacher-forced on the oracle's quantized q and its input h1, so that q's
+    own rounding differences do not reach it.  Module-level bars."""
+    inp = synth.make_decoder_block(2560, 1024, 256, 16, 4, 64, 160, seed=17, dense_F=False)
+    S, nt = inp.X.shape[0] // inp.seq_len, inp.seq_len // 32
+    assert S * inp.n_heads * -(-nt // 4) >= 512 and nt % 4 != 0
+    _banner("decoder block, 5-tile sequences on the LDS-staged attention kernels, q and k")
+    torch = _torch()
+    blk = _oracle_blk(inp)
+    o = B.decoder_block_sweep(inp.X, inp.Xhat, blk, steps=1, lr=1e-5, modules=("q", "k"))
+    W = {k: np.asarray(v, np.float64) for k, v in blk.weights().items()}
+    W["q"] = o.modules["q"].W_hat
+    h1 = B.decoder_forward(inp.Xhat, blk, W).h1
+    for k, name in enumerate(("q", "k")):
+        g = rq.decoder_block_sweep(ctx, _dev(inp.X, True), _dev(inp.Xhat, True), _dev_blk(inp), None,
+                                   n_heads=inp.n_heads, n_kv=inp.n_kv, head_dim=inp.head_dim, seq_len=inp.seq_len,
+                                   qp=rq.qparams(), bgd=rq.bgd_params(steps=1, lr=1e-5), start=k, n_modules=1,
+                                   fixed={"q": _dev(o.modules["q"].W_hat)} if k else None,
+                                   x_fixed=_dev(h1, True) if k else None)
+        torch.cuda.synchronize()
+        met = P.compare(g.modules[name], o.modules[name])
+        print(name, met, flush=True)
+        assert met["code_identity"] >= P.CODE_IDENTITY, name
+        assert met["first_group_agreement"] >= P.CODE_IDENTITY, name
+        assert met["group_param_agreement"] >= P.GROUP_AGREEMENT_AFTER_BGD, name
+    print("loss", g.loss_final, o.loss_final, flush=True)
+    assert abs(g.loss_final - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
