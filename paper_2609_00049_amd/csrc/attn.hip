@@ -25,15 +25,28 @@ constexpr int TB = 256;
 // Rotary embedding over pairs (i, i + hd/2) of each head, angle (t mod L) base^(-2i/hd):
 //   forward (bf16 in and out):  (x1 c - x2 s, x2 c + x1 s)
 //   inverse (float32 in and out): (x1 c + x2 s, x2 c - x1 s)
+// cs [L][hd/2][2]: cos and sin of the angle of each position and pair (float64), computed once by
+// rope_table_kernel rather than per element.
+__global__ void rope_table_kernel(double* __restrict__ cs, int64_t L, int64_t hd, double base) {
+    const int64_t half = hd / 2, total = L * half;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t pos = e / half, i = e % half;
+        const double ang = (double)pos * pow(base, -2.0 * (double)i / (double)hd);
+        double s, c;
+        sincos(ang, &s, &c);
+        cs[2 * e] = c;
+        cs[2 * e + 1] = s;
+    }
+}
+
 template <bool FWD, typename TI, typename TO>
-__global__ void rope_kernel(const TI* __restrict__ in, TO* __restrict__ out, int64_t T, int64_t n, int64_t hd,
-                            int64_t L, double base) {
+__global__ void rope_kernel(const TI* __restrict__ in, TO* __restrict__ out, const double* __restrict__ cs, int64_t T,
+                            int64_t n, int64_t hd, int64_t L) {
     const int64_t half = hd / 2, total = T * n * half;
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
         const int64_t t = e / (n * half), r = e % (n * half), h = r / half, i = r % half;
-        const double ang = (double)(t % L) * pow(base, -2.0 * (double)i / (double)hd);
-        double s, c;
-        sincos(ang, &s, &c);
+        const double2 sc = *reinterpret_cast<const double2*>(cs + 2 * ((t % L) * half + i));
+        const double c = sc.x, s = sc.y;
         const int64_t p = t * n * hd + h * hd + i;
         double x1, x2;
         if constexpr (FWD) {
@@ -55,18 +68,22 @@ static unsigned grid_of(int64_t count) {
     return (unsigned)(b < 1 ? 1 : (b > 65536 ? 65536 : b));
 }
 
-hipError_t rope_fwd(const uint16_t* in, uint16_t* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
+hipError_t rope_table(double* cs, int64_t L, int64_t hd, double base, hipStream_t st) {
+    hipLaunchKernelGGL(rope_table_kernel, dim3(grid_of(L * hd / 2)), dim3(TB), 0, st, cs, L, hd, base);
+    return hipGetLastError();
+}
+hipError_t rope_fwd(const uint16_t* in, uint16_t* out, const double* cs, int64_t T, int64_t n, int64_t hd, int64_t L,
                     hipStream_t st) {
     if (T <= 0) return hipSuccess;
     hipLaunchKernelGGL((rope_kernel<true, uint16_t, uint16_t>), dim3(grid_of(T * n * hd / 2)), dim3(TB), 0, st, in,
-                       out, T, n, hd, L, base);
+                       out, cs, T, n, hd, L);
     return hipGetLastError();
 }
-hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
+hipError_t rope_inv(const float* in, float* out, const double* cs, int64_t T, int64_t n, int64_t hd, int64_t L,
                     hipStream_t st) {
     if (T <= 0) return hipSuccess;
     hipLaunchKernelGGL((rope_kernel<false, float, float>), dim3(grid_of(T * n * hd / 2)), dim3(TB), 0, st, in, out,
-                       T, n, hd, L, base);
+                       cs, T, n, hd, L);
     return hipGetLastError();
 }
 
@@ -447,15 +464,34 @@ hipError_t attn_fwd(const uint16_t* qr, const uint16_t* kr, const uint16_t* v, i
     return hipGetLastError();
 }
 
-// D[t][h] = sum_c dO[t][h hd + c] O32[t][h hd + c] (float64); one thread per (t, h).
-__global__ void attn_rowdot_kernel(const float* __restrict__ dO, const float* __restrict__ O32, int64_t TH,
-                                   int64_t hd, double* __restrict__ D) {
-    for (int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; r < TH; r += (int64_t)gridDim.x * blockDim.x) {
-        const float* a = dO + r * hd;
-        const float* b = O32 + r * hd;
+// D[t][h] = sum_c dO[t][h hd + c] O32[t][h hd + c] (float64, summed in order of c); a block takes 32
+// rows: the 256 threads stage both row sets through LDS with coalesced 16-byte loads, then one
+// thread per row sums it.  hd a multiple of 32, at most 256.
+constexpr int RD_ROWS = 32;
+__global__ __launch_bounds__(256) void attn_rowdot_kernel(const float* __restrict__ dO, const float* __restrict__ O32,
+                                                          int64_t TH, int64_t hd, double* __restrict__ D) {
+    __shared__ float sa[RD_ROWS * (256 + 1)];
+    __shared__ float sb[RD_ROWS * (256 + 1)];
+    const int64_t r0 = (int64_t)blockIdx.x * RD_ROWS;
+    const int64_t rows = TH - r0 < RD_ROWS ? TH - r0 : RD_ROWS;
+    const int64_t st = hd + 1;
+    const int64_t n4 = rows * hd / 4;
+    for (int64_t q = threadIdx.x; q < n4; q += 256) {
+        const int64_t rr = (q * 4) / hd, c = (q * 4) % hd;
+        const float4 a = *reinterpret_cast<const float4*>(dO + (r0 + rr) * hd + c);
+        const float4 b = *reinterpret_cast<const float4*>(O32 + (r0 + rr) * hd + c);
+        float* pa = sa + rr * st + c;
+        float* pb = sb + rr * st + c;
+        pa[0] = a.x; pa[1] = a.y; pa[2] = a.z; pa[3] = a.w;
+        pb[0] = b.x; pb[1] = b.y; pb[2] = b.z; pb[3] = b.w;
+    }
+    __syncthreads();
+    if (threadIdx.x < rows) {
+        const float* a = sa + threadIdx.x * st;
+        const float* b = sb + threadIdx.x * st;
         double acc = 0.0;
         for (int64_t c = 0; c < hd; ++c) acc += (double)a[c] * (double)b[c];
-        D[r] = acc;
+        D[r0 + threadIdx.x] = acc;
     }
 }
 
@@ -1019,7 +1055,8 @@ hipError_t attn_bwd(const double* LSE, const float* O32, const float* dO, const 
     if (T <= 0) return hipSuccess;
     const int64_t S = T / L, nt = L / AT;
     hipError_t e;
-    hipLaunchKernelGGL(attn_rowdot_kernel, dim3(grid_of(T * H)), dim3(TB), 0, st, dO, O32, T * H, hd, w.D);
+    hipLaunchKernelGGL(attn_rowdot_kernel, dim3((unsigned)((T * H + RD_ROWS - 1) / RD_ROWS)), dim3(256), 0, st, dO, O32,
+                       T * H, hd, w.D);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = transpose_u16(kr, Hkv * hd, w.kt, T, T, Hkv * hd, st)) != hipSuccess) return e;
     if ((e = transpose_u16(qr, H * hd, w.qt, T, T, H * hd, st)) != hipSuccess) return e;

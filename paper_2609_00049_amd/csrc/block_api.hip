@@ -502,6 +502,7 @@ int split_dec(realq_ctx* ctx, const char* tag, const realq_decoder_block& b, int
 struct DecDims {
     int64_t T, d, f, L, H, Hkv, hd, Hq, Hk;
     double base, eps;
+    double* rope = nullptr;  // device [L][hd/2][2]: the rotary cos/sin table of (L, hd, base)
 };
 
 struct DecF {  // buffers of one forward of the decoder block
@@ -559,8 +560,8 @@ int dec_attn(realq_ctx* ctx, const DecW& w, const uint16_t* xb, const float* xf,
     if ((mask & 2) && (rc = lin_bf16(ctx, w.k, D.Hk, D.d, F.h1, D.T, F.k))) return rc;
     if ((mask & 4) && (rc = lin_bf16(ctx, w.v, D.Hk, D.d, F.h1, D.T, F.v))) return rc;
     Timed tm(ctx, "attention");
-    if (mask & 1) RQ_HIP(ctx, realq::rope_fwd(F.q, F.qr, D.T, D.H, D.hd, D.L, D.base, s));
-    if (mask & 2) RQ_HIP(ctx, realq::rope_fwd(F.k, F.kr, D.T, D.Hkv, D.hd, D.L, D.base, s));
+    if (mask & 1) RQ_HIP(ctx, realq::rope_fwd(F.q, F.qr, D.rope, D.T, D.H, D.hd, D.L, s));
+    if (mask & 2) RQ_HIP(ctx, realq::rope_fwd(F.k, F.kr, D.rope, D.T, D.Hkv, D.hd, D.L, s));
     RQ_HIP(ctx, realq::attn_fwd(F.qr, F.kr, F.v, D.T, D.H, D.Hkv, D.hd, D.L, F.lse, F.O32, F.O, F.vt, s));
     return REALQ_OK;
 }
@@ -649,8 +650,8 @@ int back_to_qkv(realq_ctx* ctx, const DecW& w, const DecDims& D, const DecF& F, 
     Timed tm(ctx, "attention");
     RQ_HIP(ctx, realq::attn_bwd(F.lse, F.O32, Wk.dO, F.qr, F.kr, F.v, T, D.H, D.Hkv, D.hd, D.L, Wk.at, Wk.dqr, Wk.dkr,
                                 Wk.dv, s));
-    RQ_HIP(ctx, realq::rope_inv(Wk.dqr, Wk.dq, T, D.H, D.hd, D.L, D.base, s));
-    RQ_HIP(ctx, realq::rope_inv(Wk.dkr, Wk.dk, T, D.Hkv, D.hd, D.L, D.base, s));
+    RQ_HIP(ctx, realq::rope_inv(Wk.dqr, Wk.dq, D.rope, T, D.H, D.hd, D.L, s));
+    RQ_HIP(ctx, realq::rope_inv(Wk.dkr, Wk.dk, D.rope, T, D.Hkv, D.hd, D.L, s));
     return REALQ_OK;
 }
 
@@ -680,6 +681,14 @@ int check_decoder(realq_ctx* ctx, const realq_decoder_desc* Dd, const char* who,
     return REALQ_OK;
 }
 
+// The rotary cos/sin table of the decoder's (seq_len, head_dim, rope_base), filled on the stream.
+int rope_init(realq_ctx* ctx, DecDims& D) {
+    int rc;
+    if ((rc = ws(ctx, "d_rope", D.L * D.hd, D.rope))) return rc;
+    RQ_HIP(ctx, realq::rope_table(D.rope, D.L, D.hd, D.base, ctx->stream));
+    return REALQ_OK;
+}
+
 }  // namespace
 
 extern "C" int realq_decoder_forward(realq_ctx* ctx, const realq_decoder_desc* Dd, realq_decoder_fwd_out* out) {
@@ -687,7 +696,7 @@ extern "C" int realq_decoder_forward(realq_ctx* ctx, const realq_decoder_desc* D
     if (!Dd || !out || !out->y) return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_forward: NULL desc or y");
     int rc;
     DecDims D;
-    if ((rc = check_decoder(ctx, Dd, "decoder_forward", D))) return rc;
+    if ((rc = check_decoder(ctx, Dd, "decoder_forward", D)) || (rc = rope_init(ctx, D))) return rc;
     hipStream_t s = ctx->stream;
     DecW w;
     DecF F;
@@ -716,7 +725,7 @@ extern "C" int realq_decoder_block_sweep(realq_ctx* ctx, const realq_decoder_des
     if (Dd->bgd.form != REALQ_BGD_TOKENS || Dd->bgd.loss_clip != 0.f)
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: form and loss_clip must be 0");
     DecDims D;
-    if ((rc = check_decoder(ctx, Dd, "decoder_block_sweep", D))) return rc;
+    if ((rc = check_decoder(ctx, Dd, "decoder_block_sweep", D)) || (rc = rope_init(ctx, D))) return rc;
     if (Dd->bgd.batch % D.L)
         return set_error(ctx, REALQ_ERR_SHAPE, "decoder_block_sweep: batch must be a multiple of seq_len");
     if (!Dd->Xhat) return set_error(ctx, REALQ_ERR_INVALID_ARG, "decoder_block_sweep: NULL Xhat");

@@ -194,10 +194,12 @@ hipError_t rmsnorm_bwd_blend(const float* h, const float* g2, const float* du, c
                              double alpha, int64_t T, int64_t d, float* g, hipStream_t st);
 
 // ---------------------------------------------------------------- attention half of a decoder block
-// rotary embedding: forward on bf16 [T][n hd] (rounded), inverse rotation on float32 (backward)
-hipError_t rope_fwd(const uint16_t* in, uint16_t* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
+// rotary embedding: forward on bf16 [T][n hd] (rounded), inverse rotation on float32 (backward),
+// with the cos/sin table cs [L][hd/2][2] (float64) that rope_table fills for (L, hd, base)
+hipError_t rope_table(double* cs, int64_t L, int64_t hd, double base, hipStream_t st);
+hipError_t rope_fwd(const uint16_t* in, uint16_t* out, const double* cs, int64_t T, int64_t n, int64_t hd, int64_t L,
                     hipStream_t st);
-hipError_t rope_inv(const float* in, float* out, int64_t T, int64_t n, int64_t hd, int64_t L, double base,
+hipError_t rope_inv(const float* in, float* out, const double* cs, int64_t T, int64_t n, int64_t hd, int64_t L,
                     hipStream_t st);
 // Causal attention per sequence of L tokens (L and hd multiples of 32): O32 = softmax(qr kr^T /
 // sqrt(hd)) v [T][H hd] float32, O = bf16(O32), LSE [T][H] the row log-sum-exp (float64) that the
