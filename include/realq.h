@@ -120,7 +120,9 @@ const char* realq_last_error(const realq_ctx* ctx);
  * "block_step" (the block sweeps: the fixed forwards, one Block-GD step) and "attention"
  * (realq_decoder_block_sweep: each attention forward or backward with its rotary embeddings),
  * "metric" (the dense-metric product of a Block-GD step).
- * Returns REALQ_ERR_INVALID_ARG for an unknown name. */
+ * Returns REALQ_ERR_INVALID_ARG for an unknown name.  Independently of this switch, each of
+ * these phases (and each column block of realq_quantize_layer) is a roctx range of the same
+ * name around its launches, visible with `rocprofv3 --marker-trace`. */
 int realq_ctx_set_timing(realq_ctx* ctx, int enable);
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms);
 int realq_ctx_reset_timing(realq_ctx* ctx);
