@@ -447,6 +447,85 @@ def config_legs(torch, rq, ctx, qp):
     return out
 
 
+LAYER_ORDER = ("q", "k", "v", "o", "gate", "up", "down")
+LAYER_PARTNERS = {"q": ("o",), "o": ("gate", "up")}
+
+
+def whole_layer(torch, rq, ctx, qp, cfg="llama3.1_8b_layer"):
+    """The seven modules of one synthetic decoder layer at full size, in the order q, k, v, o, gate,
+    up, down, each on the hand-off of the module before it (X_o = X W_q^T, X_gate,up = X_o W_o^T,
+    X_down = SiLU(X W_gate^T) * (X W_up^T), the quantized path with the quantized weights, all in
+    bf16), q and o with their consumers' pull-back metric over the window of their own blocks.
+    One pass; each module's time is the library's own (Hessian, factorisation, the whole sweep,
+    final loss), the hand-offs are timed apart."""
+    import synth
+    c = synth.CONFIGS[cfg]
+    T, K, lr = c["T"], c["steps"], c["lr"]
+    shapes = {k: tuple(v) for k, v in c["modules"].items()}
+    WORKLOADS["_leg"] = (cfg, "q", *shapes["q"], T, K, lr)
+    W0q, X0, Xh0, s = make_inputs(torch, "_leg")
+    WORKLOADS.pop("_leg", None)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(777)
+    W0 = {"q": W0q}
+    for name in LAYER_ORDER[1:]:
+        W = torch.randn(shapes[name], generator=g, device="cuda") * c["w"][1]
+        W0[name] = W.to(torch.bfloat16).float().contiguous()
+    bf = torch.bfloat16
+    inputs = {k: (X0, Xh0) for k in ("q", "k", "v")}
+    out, gate_hat = {}, None
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    handoff_ms = 0.0
+    fl_total = 0.0
+    for name in LAYER_ORDER:
+        m, n = shapes[name]
+        X, Xh = inputs[name]
+        P, window = None, None
+        if name in LAYER_PARTNERS:
+            P = torch.empty((m, m), dtype=torch.float32, device="cuda")
+            for i, partner in enumerate(LAYER_PARTNERS[name]):
+                rq.pullback_metric(ctx, W0[partner], P, accumulate=i > 0)
+            window = (0, -(-n // qp.block))
+        bgd = rq.bgd_params(steps=K, lr=lr, tok_chunk=TOKEN_CHUNK.get(f"{cfg}:{name}", 0))
+        r = rq.quantize_layer(ctx, W0[name], X, Xh, s, None, P, qp=qp, bgd=bgd, window=window)
+        fa = f_alg(m, n, T, K)
+        fl = fa["total"] + (K * 2.0 * m * m * fa["SJ"] if P is not None else 0.0)
+        fl_total += fl
+        out[name] = {"m": m, "n": n, "ms": r.ms_total, "tflops_alg": fl / (r.ms_total / 1e3) / 1e12,
+                     "loss_final": r.loss_final}
+        print(f"[bench] layer {name}: {m}x{n} {r.ms_total:.1f} ms, loss {r.loss_final:.6g}", file=sys.stderr,
+              flush=True)
+        ev0.record()
+        if name in ("q", "o"):
+            Y = torch.empty((T, m), dtype=bf, device="cuda")
+            Yh = torch.empty_like(Y)
+            rq.handoff(ctx, W0[name], X, Y)
+            rq.handoff(ctx, r.W_hat, Xh, Yh)
+            if name == "q":
+                inputs["o"] = (Y, Yh)
+            else:
+                inputs["gate"] = inputs["up"] = (Y, Yh)
+        elif name == "gate":
+            gate_hat = r.W_hat
+        elif name == "up":
+            Xg, Xhg = inputs["gate"]
+            Y = torch.empty((T, m), dtype=bf, device="cuda")
+            Yh = torch.empty_like(Y)
+            rq.handoff(ctx, W0["gate"], Xg, Y, Wb=W0["up"])
+            rq.handoff(ctx, gate_hat, Xhg, Yh, Wb=r.W_hat)
+            inputs["down"] = (Y, Yh)
+            del inputs["gate"], inputs["up"]
+        ev1.record()
+        torch.cuda.synchronize()
+        handoff_ms += ev0.elapsed_time(ev1)
+        del r, P
+        torch.cuda.empty_cache()
+    total = sum(v["ms"] for v in out.values()) + handoff_ms
+    return {"config": cfg, "tokens": T, "bgd_steps": K, "modules": out, "handoff_ms": handoff_ms,
+            "ms_total": total, "flops_alg": fl_total, "tflops_alg": fl_total / (total / 1e3) / 1e12,
+            "frac_bf16_peak_alg": fl_total / (total / 1e3) / PEAK_BF16}
+
+
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_00049_amd", "csrc", "gemm_bf16.hip")
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_llama8b_gate_traffic.txt")
 
@@ -500,7 +579,7 @@ def main():
                          "(decoder_block)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the sweeps of the further modules (dense metric, window partner, down projections)")
-    ap.add_argument("--only", choices=("stage0", "block", "decoder", "configs"),
+    ap.add_argument("--only", choices=("stage0", "block", "decoder", "configs", "layer"),
                     help="run only that part (for per-part kernel profiles) and print its object")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -522,6 +601,10 @@ def main():
         ctx = rq.Context()
         ctx.set_timing(True)
         print(json.dumps({"decoder_block": decoder_block(torch, rq, ctx, rq.qparams())}), flush=True)
+        return
+    if args.only == "layer":
+        ctx = rq.Context()
+        print(json.dumps({"whole_layer": whole_layer(torch, rq, ctx, rq.qparams())}), flush=True)
         return
     if args.only == "configs":
         ctx = rq.Context()
