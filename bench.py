@@ -683,6 +683,7 @@ def main():
         "config": {"workload": args.workload, "m": m, "n": n, "tokens": T, "bgd_steps": K, "bits": 4,
                    "group": 128, "block": 128, "bgd_form": args.form,
                    "token_chunk": tok_chunk},
+        "weights_per_s": m * n / (ms_per_step / 1e3),
         "tflops_alg": sweep_rate / 1e12,
         "frac_bf16_peak_alg": sweep_rate / PEAK_BF16,
         "mfma_peak_measured_tflops": peak_meas / 1e12,
