@@ -686,6 +686,7 @@ def main():
         "weights_per_s": m * n / (ms_per_step / 1e3),
         "sweep_ms_each": [round(x, 1) for x in sweep_ms],
         "sweep_ms_median": float(sorted(sweep_ms)[len(sweep_ms) // 2]),
+        "loss_final": out.loss_final,
         "tflops_alg": sweep_rate / 1e12,
         "frac_bf16_peak_alg": sweep_rate / PEAK_BF16,
         "mfma_peak_measured_tflops": peak_meas / 1e12,
