@@ -284,7 +284,7 @@ def surrogate_grad(R, s, Ma, Xhat_J, T):
     return G / T
 
 
-def gram_surrogate(W0, X, Xhat, s=None, trace_loss=True, M=None, P=None):
+def gram_surrogate(W0, X, Xhat, s=None, trace_loss=True, M=None, P=None, batch=None):
     """The module-output surrogate of Eq. fisher_loss (per-token weights s, metric M, optionally
     blended with the window partner's P by Eq. slide_window) and its gradient, written through the
     calibration Gram matrices Hs = Xhat^T S Xhat / T and Ks = X^T S Xhat / T instead of the [m, T]
@@ -300,9 +300,13 @@ def gram_surrogate(W0, X, Xhat, s=None, trace_loss=True, M=None, P=None):
     costs k n |J| for k rows (plus k^2 |J| for a dense metric, whose rows are coupled, so then all m
     rows must be followed).  With the identity metric the rows are independent and W0 may be a
     subset of rows.  Returns (grad_fn, loss_fn) for quantize_layer; loss_fn is the own-metric
-    (alpha = 1) loss.  With trace_loss False the per-step loss in the trace is NaN (only the final
-    loss is evaluated), which saves one pass over Hs and Ks per step when only the final weights are
-    checked."""
+    (alpha = 1) loss over all tokens.  With trace_loss False the per-step loss in the trace is NaN
+    (only the final loss is evaluated), which saves one pass over Hs and Ks per step when only the
+    final weights are checked.
+
+    ``batch``: the Sec. 4.3 mini-batch of ``minibatch`` -- the same matrices are then formed for
+    every batch of consecutive tokens, each over its own token count Tb (as the token form
+    normalises a batch), and grad_fn answers the step's batch (``tokens`` must be one of them)."""
     W0 = np.asarray(W0, dtype=np.float64)
     X = np.asarray(X, dtype=np.float64)
     Xhat = np.asarray(Xhat, dtype=np.float64)
@@ -311,36 +315,49 @@ def gram_surrogate(W0, X, Xhat, s=None, trace_loss=True, M=None, P=None):
     T = X.shape[0]
     k = W0.shape[0]
     sw = np.ones(T) if s is None else np.asarray(s, dtype=np.float64)
-    SXh = Xhat if s is None else Xhat * sw[:, None]
-    Hs = Xhat.T @ SXh / T
-    Ks = X.T @ SXh / T
-    X0 = X @ W0.T                                  # [T, k]
     coupled = M is not None or P is not None
-    if coupled:
-        C = X0.T @ (X0 * sw[:, None]) / T          # [k, k]
-    else:
-        c = 0.5 / T * np.sum(X0 * X0 * sw[:, None], axis=0)
+    nb = 1 if batch is None or batch >= T else -(-T // batch)
+    slices = [minibatch(i + 1, T, batch if nb > 1 else None) for i in range(nb)]
+    # unnormalised sums over each batch: Xhat_b^T S_b Xhat_b, X_b^T S_b Xhat_b and the constant term
+    parts = []
+    for sl in slices:
+        SXh = Xhat[sl] if s is None else Xhat[sl] * sw[sl, None]
+        X0 = X[sl] @ W0.T                          # [Tb, k]
+        const = X0.T @ (X0 * sw[sl, None]) if coupled else np.sum(X0 * X0 * sw[sl, None], axis=0)
+        parts.append((sl, Xhat[sl].T @ SXh, X[sl].T @ SXh, const))
+    full = (sum(p[1] for p in parts) / T, sum(p[2] for p in parts) / T, sum(p[3] for p in parts) / T)
+    per = {p[0].start: (p[1] / (p[0].stop - p[0].start), p[2] / (p[0].stop - p[0].start),
+                        p[3] / (p[0].stop - p[0].start)) for p in parts}
 
-    def loss_at(W, Ma):
+    def loss_at(W, Ma, g):
+        Hs, Ks, C = g
         if Ma is None and not coupled:
             quad = np.sum((W @ Hs) * W, axis=1) - 2.0 * np.sum((W @ Ks.T) * W0, axis=1)
-            return float(np.sum(0.5 * quad + c))
+            return float(np.sum(0.5 * quad + 0.5 * C))
         A = W @ Hs @ W.T - 2.0 * (W @ Ks.T @ W0.T) + C
         return 0.5 * float(np.trace(A) if Ma is None else np.sum(Ma * A))
 
     def loss_fn(W):
-        return loss_at(W, M)
+        return loss_at(W, M, full)
 
     def grad_fn(W, J, alpha, tokens=slice(0, T)):
-        if range(T)[tokens] != range(T):
-            raise ValueError("gram_surrogate is formed over all tokens: no mini-batch")
+        sl = range(T)[tokens]
+        if nb == 1:
+            g = full if sl == range(T) else None
+        else:
+            g = per.get(sl.start) if len(sl) > 0 and sl.start % batch == 0 else None
+            if g is not None and sl != range(T)[minibatch(1 + sl.start // batch, T, batch)]:
+                g = None
+        if g is None:
+            raise ValueError("gram_surrogate: tokens are not one of the batches it was formed for")
+        Hs, Ks, _ = g
         Ma = _blend(M, P, alpha, k)
         G = W @ Hs[:, J] - W0 @ Ks[:, J]
         if Ma is not None:
             G = Ma @ G
-        return (loss_at(W, Ma) if trace_loss else float("nan")), G
+        return (loss_at(W, Ma, g) if trace_loss else float("nan")), G
 
-    grad_fn.Hs = Hs            # the calibration Gram matrix Xhat^T S Xhat / T, i.e. H / 2
+    grad_fn.Hs = full[0]       # the calibration Gram matrix Xhat^T S Xhat / T over all tokens, i.e. H / 2
     return grad_fn, loss_fn
 
 

@@ -472,6 +472,42 @@ def test_sweep_driven_by_the_gram_surrogate_is_the_token_sweep():
     assert (c.codes == a.codes).all()
 
 
+@pytest.mark.parametrize("dense", [False, True])
+def test_gram_surrogate_per_minibatch_equals_the_token_form(dense):
+    """gram_surrogate formed per mini-batch (a ragged last batch included) against surrogate_loss /
+    surrogate_grad of each batch's own [m, Tb] residual over its Tb tokens; the final loss stays the
+    full-token one, and a slice that is not one of the batches is refused."""
+    W0, X, Xh, s, W, M = _bgd_problem(58, m=5, dense=dense)
+    T = X.shape[0]
+    batch = (T + 2) // 3                          # three batches, the last one shorter
+    grad_fn, loss_fn = oracle.gram_surrogate(W0, X, Xh, s, M=M, batch=batch)
+    J = slice(2, W.shape[1])
+    for t in (1, 2, 3, 4):
+        sl = oracle.minibatch(t, T, batch)
+        Tb = sl.stop - sl.start
+        R = residual(W, W0, X[sl], Xh[sl])
+        lv, G = grad_fn(W, J, 1.0, sl)
+        np.testing.assert_allclose(G, surrogate_grad(R, s[sl], M, Xh[sl, J], Tb), rtol=1e-10, atol=1e-14)
+        assert lv == pytest.approx(surrogate_loss(R, s[sl], M, Tb), rel=1e-10)
+    assert oracle.minibatch(3, T, batch).stop - oracle.minibatch(3, T, batch).start < batch
+    assert loss_fn(W) == pytest.approx(surrogate_loss(residual(W, W0, X, Xh), s, M, T), rel=1e-10)
+    np.testing.assert_allclose(grad_fn.Hs, Xh.T @ np.diag(s) @ Xh / T, rtol=1e-12)
+    for bad in (slice(0, T), slice(1, batch + 1), slice(0, batch - 1)):
+        with pytest.raises(ValueError):
+            grad_fn(W, J, 1.0, bad)
+
+
+def test_minibatch_sweep_driven_by_the_gram_surrogate_is_the_token_sweep():
+    L = synth.make_module("single_512", m=40, n=256, T=1000, seed=9)
+    grad_fn, loss_fn = oracle.gram_surrogate(L.W0, L.X, L.Xhat, L.s, batch=300)
+    a = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3, batch=300)
+    b = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=3, lr=1e-3, batch=300, grad_fn=grad_fn,
+                              loss_fn=loss_fn)
+    assert (a.codes == b.codes).all()
+    assert b.loss_final == pytest.approx(a.loss_final, rel=1e-10)
+    np.testing.assert_allclose([v for (_, _, v) in b.loss_trace], [v for (_, _, v) in a.loss_trace], rtol=1e-9)
+
+
 def test_adam_constants_are_the_papers():
     a = GOLD["adam"]
     assert (oracle.ADAM_BETA1, oracle.ADAM_BETA2, oracle.ADAM_EPS) == (a["beta1"], a["beta2"], a["eps"])
