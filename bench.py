@@ -39,14 +39,15 @@ WORKLOADS = {
 TOKEN_CHUNK = {"llama3.1_70b_gate": 32768}
 
 
-def f_alg(m, n, T, K, block=128, xhat_differs=True):
-    """Algorithmic FLOPs of the token-streamed sweep (hi/lo split passes not counted)."""
+def f_alg(m, n, T, K, block=128, xhat_differs=True, Tb=None):
+    """Algorithmic FLOPs of the token-streamed sweep (hi/lo split passes not counted); Tb: tokens per
+    Block-GD step when each step takes a mini-batch (default all T)."""
     nb = -(-n // block)
     SJ = sum(n - min((b + 1) * block, n) for b in range(nb))
     hess = 2 * n * n * T
     init = 2 * m * n * T if xhat_differs else 0
     lock = 2 * m * (n - min(block, n)) * T
-    bgd = K * 4 * m * T * SJ
+    bgd = K * 4 * m * (T if Tb is None else min(Tb, T)) * SJ
     obs = 2 * m * block * SJ
     return dict(total=hess + init + lock + bgd + obs, resid=K * 2 * m * T * SJ, grad=K * 2 * m * T * SJ, SJ=SJ)
 
@@ -447,6 +448,37 @@ def config_legs(torch, rq, ctx, qp):
     return out
 
 
+def next_legs(torch, rq, ctx, W0, X, Xh, s, m, n, T, K, lr, workload, batch=65536):
+    """One sweep each (after the headline, so the workspaces exist) of the extensions beyond the
+    plain sweep, on the headline's own inputs: Block-GD on mini-batches of 65536 tokens per Adam
+    step (Sec. 4.3; the paper's 32 calibration sequences of 2048 tokens), and the symmetric per-row
+    W4 quantizer of the paper's main tables; then the Qwen3-0.6B gate (3072 x 1024, 131072 tokens)
+    with mini-batches and the output-perturbation clip a_loss_clip = 0.95 (Appendix D.1's setting
+    for the small Qwen3 models).  F_alg counts the Block-GD GEMMs over the tokens each step takes."""
+    out = {}
+
+    def one(name, W0_, X_, Xh_, s_, m_, n_, T_, K_, lr_, qp_, bgd_, Tb):
+        o = rq.quantize_layer(ctx, W0_, X_, Xh_, s_, qp=qp_, bgd=bgd_)
+        fl = f_alg(m_, n_, T_, K_, Tb=Tb)["total"]
+        print(f"[bench] {name}: {o.ms_total:.1f} ms, loss {o.loss_final:.6g}", file=sys.stderr, flush=True)
+        out[name] = {"m": m_, "n": n_, "tokens": T_, "tokens_per_step": min(Tb, T_), "bgd_steps": K_,
+                     "ms": o.ms_total, "columns_per_s": n_ / (o.ms_total / 1e3),
+                     "tflops_alg": fl / (o.ms_total / 1e3) / 1e12, "loss_final": o.loss_final}
+
+    one(f"{workload}_minibatch{batch}", W0, X, Xh, s, m, n, T, K, lr, rq.qparams(),
+        rq.bgd_params(steps=K, lr=lr, batch=batch), batch)
+    one(f"{workload}_sym_per_row_w4", W0, X, Xh, s, m, n, T, K, lr, rq.qparams(sym=True, group=0),
+        rq.bgd_params(steps=K, lr=lr), T)
+    WORKLOADS["_leg"] = ("qwen3_0.6b_mlp", "gate", 3072, 1024, 131072, 8, 3e-4)
+    try:
+        W0q, Xq, Xhq, sq = make_inputs(torch, "_leg")
+    finally:
+        WORKLOADS.pop("_leg", None)
+    one(f"qwen3_0.6b_gate_minibatch{batch}_clip0.95", W0q, Xq, Xhq, sq, 3072, 1024, 131072, 8, 3e-4, rq.qparams(),
+        rq.bgd_params(steps=8, lr=3e-4, batch=batch, loss_clip=0.95), batch)
+    return out
+
+
 LAYER_ORDER = ("q", "k", "v", "o", "gate", "up", "down")
 LAYER_PARTNERS = {"q": ("o",), "o": ("gate", "up")}
 
@@ -577,6 +609,8 @@ def main():
     ap.add_argument("--no-decoder", action="store_true",
                     help="skip the block-output surrogate sweep of a LLaMA-3.1-8B-shaped decoder block "
                          "(decoder_block)")
+    ap.add_argument("--no-next", action="store_true",
+                    help="skip the mini-batch, symmetric-quantizer and clip sweeps (also skipped with --no-configs)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the sweeps of the further modules (dense metric, window partner, down projections)")
     ap.add_argument("--only", choices=("stage0", "block", "decoder", "configs", "layer"),
@@ -713,6 +747,8 @@ def main():
                                     "(bench.py --form gram for its own line)"}
     if not args.no_stage0:
         res["stage0"] = stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n, T)
+    if not (args.no_next or args.no_configs) and args.form == "tokens":
+        res["next"] = next_legs(torch, rq, ctx, W0, X, Xh, s, m, n, T, K, lr, args.workload)
     if not (args.no_block and args.no_decoder and args.no_configs):
         del W0, X, Xh, s
         torch.cuda.empty_cache()

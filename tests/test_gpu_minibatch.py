@@ -86,3 +86,47 @@ def test_rejected_combinations(rq, ctx):
         with pytest.raises(rq.RealqError) as ei:
             rq.quantize_layer(ctx, W0, X, Xh, s, kw.get("M"), qp=rq.qparams(), bgd=kw["bgd"])
         assert ei.value.code == -1
+
+
+def test_minibatch_llama_gate_full_width_sampled_rows(rq, ctx):
+    """Mini-batch Block-GD at the full 14336 x 4096 width of the LLaMA-3.1-8B gate projection: 131072
+    tokens cut into four batches of 32768 (16 calibration sequences of 2048 per Adam step), 8 steps
+    per block at the workload's learning rate, so every block's steps cycle through the batches.
+    The oracle follows 64 sampled rows (one in every 256-row tile, 8 more at random) with the
+    surrogate written through each batch's own Gram matrices (oracle.gram_surrogate with a batch,
+    pinned per batch against the token form); the Hessian over all tokens is checked whole."""
+    import time
+    torch = _torch()
+    t0 = time.time()
+    T, batch = 131072, 32768
+    L = synth.make_module("llama3.1_8b_layer", "gate", T=T)
+    m = L.W0.shape[0]
+    _banner(f"mini-batch llama gate {m}x{L.W0.shape[1]} T={T} batch={batch}: inputs in {time.time() - t0:.0f} s")
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    g = rq.quantize_layer(ctx, W0, X, Xh, s, qp=rq.qparams(), bgd=rq.bgd_params(steps=L.steps, lr=L.lr, batch=batch),
+                          want_H=True)
+    torch.cuda.synchronize()
+    del W0, X, Xh
+    _banner(f"GPU sweep {g.ms_total:.0f} ms")
+    Hg = g.H.cpu().numpy().astype(np.float64)
+    g.H = None
+    rows = P.tile_rows(m, per_tile=1, extra=8, seed=31)
+    Xd, Xhd = L.X.astype(np.float64), L.Xhat.astype(np.float64)
+    grad_fn, loss_fn = oracle.gram_surrogate(L.W0[rows], Xd, Xhd, L.s, trace_loss=False, batch=batch)
+    _banner(f"per-batch Gram matrices formed at {time.time() - t0:.0f} s")
+    herr = P.rel_fro(Hg, 2.0 * grad_fn.Hs)
+    print("Hessian rel Frobenius", herr, flush=True)
+    assert herr <= P.HESS_RTOL
+    o = oracle.quantize_layer(L.W0[rows], Xd, Xhd, L.s, steps=L.steps, lr=L.lr, batch=batch, grad_fn=grad_fn,
+                              loss_fn=loss_fn, H=2.0 * grad_fn.Hs)
+    del Xd, Xhd
+    _banner(f"oracle rows done at {time.time() - t0:.0f} s")
+    met = P.compare(g, o, rows=rows, tie_cascade=True)
+    print(met, flush=True)
+    assert met["code_identity"] >= P.CODE_IDENTITY
+    assert met["first_group_agreement"] >= P.CODE_IDENTITY
+    assert met["group_param_agreement"] >= P.GROUP_AGREEMENT_AFTER_BGD
+    assert met["tie_cascade_rows"] <= 1, met
+    lg = loss_fn(g.W_hat.cpu().numpy()[rows].astype(np.float64))
+    print("row loss", lg, o.loss_final, flush=True)
+    assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
