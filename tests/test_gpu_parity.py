@@ -240,17 +240,31 @@ def test_symmetric_low_bit_g128(rq, ctx, bits):
     _assert_parity(P.compare(g, o), g.loss_final, o.loss_final)
 
 
-def test_symmetric_per_row_llama_gate_shape_sampled_rows(rq, ctx):
-    """Per-row symmetric W4 at the full 14336x4096 gate shape (the whole 4096-column row searched
-    once), 8192 tokens, oracle on sampled rows."""
+@pytest.mark.parametrize("bits,group", [(4, 0), (3, 128), (2, 128)])
+def test_paper_quantizers_llama_gate_full_width_sampled_rows(rq, ctx, bits, group):
+    """The paper's symmetric quantizers at the full 14336x4096 gate width: per-row W4 (the main
+    tables; the whole 4096-column row searched once) and W3 / W2 with groups of 128 (the low-bit
+    tables), 8192 tokens, 8 Block-GD steps per block.  The oracle follows 64 sampled rows (one in
+    every 256-row tile, 8 more at random) through the Gram-form surrogate; the Hessian is checked
+    whole."""
     L = synth.make_module("llama3.1_8b_layer", "gate", T=8192)
-    _banner("symmetric per-row llama3.1-8b gate 14336x4096 T=8192")
-    qp = QParams(group=0, sym=True)
-    g = _run(rq, ctx, L, L.steps, L.lr, qp=rq.qparams(group=0, sym=True))
-    rows = np.random.default_rng(9).choice(L.W0.shape[0], 6, replace=False)
-    o = _oracle(L, L.steps, L.lr, rows=rows, qp=qp)
-    _assert_parity(P.compare(g, o, rows=rows))
-    lg = P.row_loss(g.W_hat.cpu().numpy()[rows], L.W0[rows], L.X, L.Xhat)
+    m = L.W0.shape[0]
+    _banner(f"symmetric w{bits} group {group or 'per-row'} llama3.1-8b gate {m}x{L.W0.shape[1]} T=8192")
+    qp = QParams(bits=bits, group=group, sym=True)
+    g = _run(rq, ctx, L, L.steps, L.lr, qp=rq.qparams(bits=bits, group=group, sym=True))
+    assert (g.zeros.cpu() == (1 << (bits - 1))).all()
+    rows = P.tile_rows(m, per_tile=1, extra=8, seed=40 + bits)
+    X, Xh = L.X.astype(np.float64), L.Xhat.astype(np.float64)
+    grad_fn, loss_fn = oracle.gram_surrogate(L.W0[rows], X, Xh, L.s, trace_loss=False)
+    herr = P.rel_fro(g.H.cpu().numpy().astype(np.float64), 2.0 * grad_fn.Hs)
+    assert herr <= P.HESS_RTOL, herr
+    o = oracle.quantize_layer(L.W0[rows], X, Xh, L.s, steps=L.steps, lr=L.lr, qp=qp, grad_fn=grad_fn,
+                              loss_fn=loss_fn, H=2.0 * grad_fn.Hs)
+    met = P.compare(g, o, rows=rows, tie_cascade=True)
+    _assert_parity(met)
+    _assert_tie_rows(met, len(rows))
+    lg = loss_fn(g.W_hat.cpu().numpy()[rows].astype(np.float64))
+    print("row loss", lg, o.loss_final, flush=True)
     assert abs(lg - o.loss_final) <= P.LOSS_RTOL * abs(o.loss_final)
 
 
