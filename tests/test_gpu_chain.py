@@ -187,3 +187,42 @@ def test_decoder_layer_chain_free_running(rq, ctx, chain_case):
             assert loss_rel <= P.LOSS_RTOL, name
         else:
             assert loss_rel <= FREE_CHAIN_LOSS_RTOL, name
+
+
+@pytest.mark.parametrize("swiglu", [False, True])
+def test_handoff_at_model_width_sampled_tokens(rq, ctx, swiglu):
+    """The hand-off at the LLaMA-3.1-8B widths and all 262144 calibration tokens: q's output
+    (4096 x 4096, the o projection's input) and the SwiGLU input of the down projection from gate
+    and up (14336 x 4096 each; the output, 262144 x 14336, has more elements than a 32-bit index
+    reaches).  Checked against the oracle's definition on 48 sampled tokens (the last ones
+    included), to the bound of the small-shape hand-off test."""
+    torch = _torch()
+    T = 262144
+    m = 14336 if swiglu else 4096
+    L = synth.make_module("llama3.1_8b_layer", "gate" if swiglu else "q", T=T)
+    assert L.W0.shape == (m, 4096)
+    r = np.random.default_rng(93)
+    Wb = (r.standard_normal((m, 4096)) * 0.02).astype(np.float32) if swiglu else None
+    _banner(f"handoff at model width m={m} T={T} swiglu={swiglu}")
+    X = _dev(L.Xhat, torch, torch.bfloat16)
+    Y = torch.empty((T, m), dtype=torch.bfloat16, device="cuda")
+    rq.handoff(ctx, _dev(L.W0, torch), X, Y, Wb=_dev(Wb, torch) if swiglu else None)
+    torch.cuda.synchronize()
+    toks = np.sort(np.concatenate([r.choice(T - 8, 40, replace=False), np.arange(T - 8, T)]))
+    got = Y[torch.from_numpy(toks).cuda()].float().cpu().numpy().astype(np.float64)
+    del X, Y
+    Xd = L.Xhat[toks].astype(np.float64)
+    ref = oracle.handoff(L.W0, Xd, Wb)
+    a = Xd @ L.W0.astype(np.float64).T
+    ea = 2.0 ** -20 * (np.abs(Xd) @ np.abs(L.W0.astype(np.float64)).T)
+    if swiglu:
+        b = Xd @ Wb.astype(np.float64).T
+        eb = 2.0 ** -20 * (np.abs(Xd) @ np.abs(Wb.astype(np.float64)).T)
+        err = 1.1 * np.abs(b) * ea + np.abs(oracle.silu(a)) * eb
+    else:
+        err = ea
+    ulp = np.abs(ref) * 2.0 ** -7
+    same = float((got == ref).mean())
+    print("identical entries", same, flush=True)
+    assert same >= 0.99
+    assert (np.abs(got - ref) <= ulp + 2 * err + 1e-30).all()
