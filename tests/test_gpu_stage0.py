@@ -246,3 +246,76 @@ def test_row_groups_llama_gate_shape_sampled_rows(rq, ctx):
         met = P.compare(g, o, rows=rows)
         lg = P.row_loss(g.W_hat.cpu().numpy()[rows], L.W0[rows], L.X, L.Xhat)
         _assert_parity(met, lg, o.loss_final, True)
+
+
+# ============================================================================ Stage 0 at the full workload sizes
+
+def _device_grads(torch, T, m, seed, chunk=16384):
+    """Seeded per-token output gradients [T, m] bf16 drawn on the device (Gaussian x LogNormal(0, 2.3)
+    token scale x LogNormal(0, 1.15) channel scale x 1e-3, four tokens x 1e5): the distribution of the
+    synthetic Stage-0 inputs at sizes the host would take minutes to draw.  Returns (G, outlier tokens)."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    chan = torch.exp(1.15 * torch.randn((1, m), generator=g, device="cuda"))
+    G = torch.empty((T, m), dtype=torch.bfloat16, device="cuda")
+    for t0 in range(0, T, chunk):
+        t1 = min(T, t0 + chunk)
+        tok = torch.exp(2.3 * torch.randn((t1 - t0, 1), generator=g, device="cuda"))
+        G[t0:t1] = (torch.randn((t1 - t0, m), generator=g, device="cuda") * tok * chan * 1e-3).to(torch.bfloat16)
+    idx = torch.randperm(T, generator=g, device="cuda")[:4]
+    G[idx] = (G[idx].float() * 1e5).to(torch.bfloat16)
+    torch.cuda.synchronize()
+    return G, idx.cpu().numpy()
+
+
+def test_fisher_at_block_output_width_sampled_entries(rq, ctx):
+    """Aggregated Fisher of 65536 tokens at the 4096-wide LLaMA-3.1-8B block output in one call; the
+    oracle computes the principal submatrix on 160 sampled channels (one in each 32-channel stripe of
+    the contraction's tiles, 32 more at random), which spans every pair of output tiles."""
+    torch = _torch()
+    T, m = 65536, 4096
+    _banner(f"fisher full width T={T} m={m}")
+    Gd, _ = _device_grads(torch, T, m, seed=31)
+    Facc = torch.zeros((m, m), dtype=torch.float64, device="cuda")
+    rq.fisher_accum(ctx, Gd, Facc)
+    F = torch.empty((m, m), dtype=torch.float32, device="cuda")
+    rq.fisher_finish(ctx, Facc, T, F)
+    torch.cuda.synchronize()
+    idx = P.tile_rows(m, per_tile=1, extra=32, seed=32, tile=32)
+    Gs = Gd[:, torch.from_numpy(idx).cuda()].float().cpu().numpy().astype(np.float64)
+    del Gd, Facc
+    ref = oracle.fisher(Gs)
+    got = F.cpu().numpy()[np.ix_(idx, idx)].astype(np.float64)
+    d = np.sqrt(np.diag(ref))
+    err = np.abs(got - ref) / np.outer(d, d)
+    print("max scaled error", err.max(), flush=True)
+    # products of bf16 values are exact; each 32768-token chunk (128 Mi elements at 4096 channels)
+    # sums in float32 over 2048 MFMA steps of 16 tokens, and |sum_t g_ti g_tj| <= T sqrt(F_ii F_jj)
+    # (Cauchy-Schwarz), so the scaled error stays within the summation bound 2048 * 2^-24 plus the
+    # final float32 rounding
+    assert err.max() <= (32768 // 16 + 1) * 2.0 ** -24
+
+
+def test_saliency_at_llama_gate_size_sampled_tokens(rq, ctx):
+    """Saliency of the LLaMA-3.1-8B gate's 262144 x 14336 output gradients (3.8e9 bf16 values, past
+    2^31) in 4 row groups.  Unclipped, 256 sampled tokens and the four outliers match the oracle;
+    clipped at 0.99, every token holds min(unclipped, tau) with tau the nearest-rank quantile of the
+    unclipped values over all tokens, so the selection is checked exactly at any size."""
+    torch = _torch()
+    T, m, ng, q = 262144, 14336, 4, 0.99
+    _banner(f"saliency full size T={T} m={m} groups={ng}")
+    Gd, outl = _device_grads(torch, T, m, seed=33)
+    s0 = rq.saliency(ctx, Gd, ng, 0.0).cpu().numpy()
+    sq = rq.saliency(ctx, Gd, ng, q).cpu().numpy()
+    rng = np.random.default_rng(34)
+    toks = np.unique(np.concatenate([rng.choice(T, 256, replace=False), outl, [0, T - 1]]))
+    Gs = Gd[torch.from_numpy(toks).cuda()].float().cpu().numpy().astype(np.float64)
+    del Gd
+    ref = oracle.saliency(Gs, ng).astype(np.float32)
+    np.testing.assert_allclose(s0[:, toks], ref, rtol=2.0 ** -23, atol=0)
+    k = int(np.ceil(np.float64(np.float32(q)) * T))
+    for g in range(ng):
+        tau = np.sort(s0[g])[k - 1]
+        assert sq[g].max() == tau
+        np.testing.assert_array_equal(sq[g], np.minimum(s0[g], tau))
+    assert (sq[:, outl] == sq.max(axis=1, keepdims=True)).all()       # the outliers sit on the clip
