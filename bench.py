@@ -427,8 +427,8 @@ def config_legs(torch, rq, ctx, qp):
         ctx.set_timing(True)
         ctx.reset_timing()
         o = rq.quantize_layer(ctx, W0, X, Xh, s, M, P, qp=qp, bgd=bgd, window=window, out=o)
-        kt = {kn: ctx.kernel_time(kn)[1] for kn in ("resid", "grad", "metric", "adam", "lock", "quantize",
-                                                          "chol", "init", "dense_loss")}
+        kt = {kn: ctx.kernel_time(kn)[1] for kn in ("resid", "grad", "resid_inc", "grad_inc", "metric", "adam",
+                                                          "lock", "quantize", "chol", "init", "dense_loss")}
         fa = f_alg(m, n, T, K)
         dense_terms = (1 if M is not None else 0) + (1 if P is not None else 0)
         fl = fa["total"] + dense_terms * K * 2.0 * m * m * fa["SJ"]
@@ -685,20 +685,27 @@ def main():
     ms_per_step = total_ms / args.steps
 
     fa = f_alg(m, n, T, K)
-    kt = {name: ctx.kernel_time(name) for name in ("resid", "grad", "quantize", "obs", "lock", "adam", "hessian",
-                                                    "chol", "init", "gram", "gram_step")}
+    kt = {name: ctx.kernel_time(name) for name in ("resid", "grad", "resid_inc", "grad_inc", "quantize", "obs",
+                                                    "lock", "adam", "hessian", "chol", "init", "gram", "gram_step")}
+    # the residual (gradient) GEMM: a column block's first step ("resid") and its later steps,
+    # which take the residual as an increment where the library allows it ("resid_inc")
+    both = {k: (kt[k][0] + kt[k + "_inc"][0], kt[k][1] + kt[k + "_inc"][1]) for k in ("resid", "grad")}
+    increments = kt["resid_inc"][0] > 0
     if args.form == "tokens":
         # dominant kernel by total time over the timed steps
-        dom = max(("resid", "grad"), key=lambda k: kt[k][1])
+        dom = max(("resid", "grad"), key=lambda k: both[k][1])
         dom_flops = fa[dom] * args.steps
+        launches, dom_ms = both[dom]
     else:
         # D G_hh over all n columns every step (the loss trace is recorded), m x n x n
         dom = "gram_step"
         dom_flops = 2.0 * m * n * n * kt[dom][0]
-    launches, dom_ms = kt[dom]
+        launches, dom_ms = kt[dom]
     achieved = dom_flops / (dom_ms / 1e3) if dom_ms > 0 else math.nan
     # the achievable MFMA rate of this GPU (register-resident loop), beside the data-sheet peak;
-    # executed MFMA work counts both halves of every hi/lo split operand (twice the algorithmic)
+    # executed MFMA work counts both halves of every hi/lo split operand: twice the algorithmic on
+    # a block's first step, once on the later steps that take increments
+    exec_factor = (2.0 + (K - 1)) / K if increments else 2.0
     peak_meas = rq.mfma_peak(ctx) * 1e12
     sweep_rate = fa["total"] / (ms_per_step / 1e3)
     res = {
@@ -712,7 +719,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 MFMA (hi/lo split fp32 operands), fp32/fp64 accumulate",
+        "dtype": ("bf16 MFMA (hi/lo split fp32 operands on a block's first step, bf16 increments on the later "
+                  "steps), fp32/fp64 accumulate" if increments else
+                  "bf16 MFMA (hi/lo split fp32 operands), fp32/fp64 accumulate"),
         "data": "synthetic (device-generated, workload distributions)",
         "config": {"workload": args.workload, "m": m, "n": n, "tokens": T, "bgd_steps": K, "bits": 4,
                    "group": 128, "block": 128, "bgd_form": args.form,
@@ -732,8 +741,10 @@ def main():
                                  and tok_chunk == TOKEN_CHUNK.get(args.workload, 0) else None),
                      "launches": launches, "avg_launch_ms": dom_ms / max(1, launches),
                      "measured_peak": peak_meas / 1e12, "frac_measured_peak": achieved / peak_meas,
-                     "executed_frac": 2.0 * achieved / PEAK_BF16 if args.form == "tokens" else None,
-                     "executed_frac_measured_peak": 2.0 * achieved / peak_meas if args.form == "tokens" else None},
+                     "executed_frac": exec_factor * achieved / PEAK_BF16 if args.form == "tokens" else None,
+                     "executed_frac_measured_peak": (exec_factor * achieved / peak_meas if args.form == "tokens"
+                                                     else None),
+                     "increment_launches": kt[dom + "_inc"][0] if args.form == "tokens" else 0},
     }
     if args.form == "tokens" and not args.no_gram_line:
         # one untimed-region Gram-form sweep of the same inputs, reported beside the headline

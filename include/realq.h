@@ -76,6 +76,20 @@ typedef struct realq_qparams {
  *               Adam step t of the module (1-based) uses the consecutive token batch
  *               (t - 1) mod ceil(T / batch); loss and gradient are normalised by its
  *               size.  The final loss is always over all T tokens and unclipped.
+ *   resid_increment : 1 = allowed [1], 0 = never.  Residual and gradient are linear in
+ *               the weights, so within one column block step k > 0 can take them as
+ *               R_k = R_0 + Q_k with Q_k = bf16(W_k - W_0)_J Xhat_J^T, and
+ *               G_k = G_0 + M_a bf16(Q_k o s) Xhat_J / T, from the block's first residual R_0
+ *               (kept in float32) and gradient G_0: one bf16 MFMA pass each over the weight
+ *               change instead of two over the float32 D = W - W0 and R o s.  Token form, no
+ *               clip, batch = T, and only where the change is small enough that its bf16
+ *               rounding stays below what the sweep's decisions resolve: the weights cannot
+ *               move by more than rms(W0) / 32 within a block ((steps - 1) lr (1 - beta1) /
+ *               sqrt((1 - beta2)(1 - beta1^2/beta2)) bounds that move: the Adam step's supremum
+ *               over every gradient history; needs beta1^2 < beta2), n <= 8192 (at most 64
+ *               column blocks carry the rounding forward) and T >= 16 n (the gradient's
+ *               rounding averages over at least 16 tokens per input column).  Costs a float32
+ *               [m, T] array and [m, n] arrays (two float32, one bf16).
  *   The Gram form takes neither a clip nor a batch smaller than T. */
 typedef struct realq_bgd_params {
     int32_t steps;
@@ -84,6 +98,7 @@ typedef struct realq_bgd_params {
     int32_t form;
     float loss_clip;
     int64_t batch;
+    int32_t resid_increment;
 } realq_bgd_params;
 
 /* realq_bgd_params.form: how the loss and gradient of a BGD step are evaluated.
@@ -114,7 +129,9 @@ const char* realq_last_error(const realq_ctx* ctx);
 /* Kernel timing: when enabled, the library brackets the launches of its main
  * kernels with HIP events on its stream and accumulates their durations, read with
  * realq_ctx_kernel_time after the stream has drained.  Names: "hessian",
- * "chol", "quantize", "obs", "lock", "resid", "grad", "adam", "init", "gram" (Gram
+ * "chol", "quantize", "obs", "lock", "resid", "grad", "resid_inc" and "grad_inc" (the
+ * residual and gradient GEMMs of the Block-GD steps that take increments, see
+ * resid_increment), "adam", "init", "gram" (Gram
  * matrices of the input perturbation), "gram_step" (the per-step product of the
  * Gram form), "dense_loss" (final loss with a dense metric), "saliency", "block_init" and
  * "block_step" (the block sweeps: the fixed forwards, one Block-GD step) and "attention"

@@ -96,6 +96,17 @@ struct realq_bgd_state {
     int64_t Tb = 0, nbatch = 1;  // tokens per step and number of batches (mini-batch BGD)
     float* Rf = nullptr;         // [m,Tc] residual kept whole for the clip
     float* tau = nullptr;        // [Tc] per-token clip thresholds
+    // increments within a column block: R0 [m,T] the block's first residual, G0 its first
+    // gradient ([m, n - c1], unscaled sum over tokens), Dacc [m,n] the weight change since then
+    // and Dinc = bf16(Dacc); inc_c1 names the block they belong to (-1: none) and inc_ready says
+    // Dinc holds the change of the current weights
+    bool inc = false;
+    float* R0 = nullptr;
+    float* G0 = nullptr;
+    float* Dacc = nullptr;
+    uint16_t* Dinc = nullptr;
+    int64_t inc_c1 = -1;
+    bool inc_ready = false;
     // Gram form
     bool gram = false;
     uint16_t* Ghi = nullptr;
@@ -132,6 +143,7 @@ void realq_bgd_params_default(realq_bgd_params* b) {
     b->form = REALQ_BGD_TOKENS;
     b->loss_clip = 0.f;
     b->batch = 0;
+    b->resid_increment = 1;
 }
 
 int realq_ctx_create(realq_ctx** out, void* hip_stream) {
@@ -175,9 +187,10 @@ int realq_ctx_set_timing(realq_ctx* ctx, int enable) {
     return REALQ_OK;
 }
 
-static const char* kTimedNames[] = {"hessian", "chol",  "quantize",  "obs",        "lock",      "resid",
-                                    "grad",    "adam",  "init",      "gram",       "gram_step", "dense_loss",
-                                    "saliency", "block_init", "block_step", "attention", "metric"};
+static const char* kTimedNames[] = {"hessian",    "chol",      "quantize",   "obs",        "lock",
+                                    "resid",      "grad",      "resid_inc",  "grad_inc",   "adam",
+                                    "init",       "gram",      "gram_step",  "dense_loss", "saliency",
+                                    "block_init", "block_step", "attention", "metric"};
 
 int realq_ctx_kernel_time(realq_ctx* ctx, const char* name, int64_t* launches, double* total_ms) {
     if (!ctx || !name) return REALQ_ERR_INVALID_ARG;
@@ -356,6 +369,8 @@ int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T
 // Row stride (bf16 values) of split(R o s) in the blocked layout for `cur` tokens: hi and lo of
 // every 32 tokens, rounded up to whole blocks.
 static int64_t r_ld(int64_t cur) { return 2 * ((cur + 31) / 32) * 32; }
+// row stride of bf16(acc o s) on a later step of a column block (row-major, in the same buffer)
+static int64_t q_ld(int64_t cur) { return ((cur + 31) / 32) * 32; }
 
 static int state_alloc(realq_bgd_state* st, void** p, size_t bytes, const char* slot) {
     realq_ctx* ctx = st->ctx;
@@ -425,11 +440,59 @@ int realq::validate_bgd(realq_ctx* ctx, const realq_bgd_params* p) {
     if (!std::isfinite(p->loss_clip) || p->loss_clip < 0.f || p->loss_clip > 1.f)
         return set_error(ctx, REALQ_ERR_INVALID_ARG, "loss_clip must lie in [0, 1] (0 = off)");
     if (p->batch < 0) return set_error(ctx, REALQ_ERR_INVALID_ARG, "batch must be >= 0");
+    if (p->resid_increment != 0 && p->resid_increment != 1)
+        return set_error(ctx, REALQ_ERR_INVALID_ARG, "resid_increment must be 0 or 1");
     return REALQ_OK;
 }
 }  // extern "C++"
 
 static int state_init_gram(realq_bgd_state* st);
+
+// Whether steps after a block's first may take residual and gradient as increments
+// (resid_increment in realq.h).  Adam's step is at most lr (1 - b1) / sqrt((1 - b2)(1 - b1^2/b2))
+// for any gradient history (Cauchy-Schwarz on the two moment sums, bias corrections included), so
+// the weight change over the steps - 1 later steps of a block is at most that times steps - 1;
+// the increments are taken when this bound is within rms(W0) / 32, the module has at most
+// kIncMaxColumns input columns (64 column blocks) and at least kIncTokensPerColumn tokens per
+// input column.
+static constexpr int64_t kIncMaxColumns = 8192;
+static constexpr int64_t kIncTokensPerColumn = 16;
+static int inc_init(realq_bgd_state* st) {
+    realq_ctx* ctx = st->ctx;
+    const realq_bgd_params& p = st->prm;
+    st->inc = false;
+    st->inc_c1 = -1;
+    st->inc_ready = false;
+    const double b1 = p.beta1, b2 = p.beta2;
+    const int64_t m = st->m, n = st->n, T = st->T;
+    if (!p.resid_increment || p.steps < 2 || p.loss_clip > 0.f || st->Tb != T || !(b1 * b1 < b2) ||
+        n > kIncMaxColumns || T < kIncTokensPerColumn * n)
+        return REALQ_OK;
+    const double step_max = (1.0 - b1) / std::sqrt((1.0 - b2) * (1.0 - b1 * b1 / b2));
+    const double disp = (double)(p.steps - 1) * step_max * (double)p.lr;
+    void *parts, *ms;
+    int rc;
+    if ((rc = get_ws(ctx, "i_parts", (size_t)realq::dot_f32_partials() * 8, &parts))) return rc;
+    if ((rc = get_ws(ctx, "i_ms", 8, &ms))) return rc;
+    RQ_HIP(ctx, realq::dot_f32(st->W0, st->W0, m * n, 1.0, (double*)parts, ctx->stream));
+    RQ_HIP(ctx, realq::reduce_partials((const double*)parts, realq::dot_f32_partials(), 1.0 / ((double)m * (double)n),
+                                       (double*)ms, ctx->stream));
+    double msq = 0.0;
+    RQ_HIP(ctx, hipMemcpyAsync(&msq, ms, 8, hipMemcpyDeviceToHost, ctx->stream));
+    RQ_HIP(ctx, hipStreamSynchronize(ctx->stream));
+    if (!(disp <= std::sqrt(msq) / 32.0)) return REALQ_OK;
+    void* q;
+    if ((rc = state_alloc(st, &q, (size_t)m * T * 4, "s_R0"))) return rc;
+    st->R0 = (float*)q;
+    if ((rc = state_alloc(st, &q, (size_t)m * n * 4, "s_Dacc"))) return rc;
+    st->Dacc = (float*)q;
+    if ((rc = state_alloc(st, &q, (size_t)m * n * 2, "s_Dinc"))) return rc;
+    st->Dinc = (uint16_t*)q;
+    if ((rc = state_alloc(st, &q, (size_t)m * n * 4, "s_G0"))) return rc;
+    st->G0 = (float*)q;
+    st->inc = true;
+    return REALQ_OK;
+}
 
 static int state_init(realq_bgd_state* st) {
     if (st->prm.form == REALQ_BGD_GRAM) return state_init_gram(st);
@@ -503,7 +566,7 @@ static int state_init(realq_bgd_state* st) {
     RQ_HIP(ctx, realq::fill_u16(st->Dlo, 0, m * n, s));
     st->t = 0;
     st->locked = 0;
-    return REALQ_OK;
+    return inc_init(st);
 }
 
 // Gram form: the three calibration Gram matrices once, then C0 = W0 G_dh and the constant
@@ -678,6 +741,10 @@ static int quantize_rows(realq_ctx* ctx, double* W, int64_t m, int64_t n, int64_
         return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: state shape differs from W");
     if (st && st->locked != c0)
         return set_error(ctx, REALQ_ERR_SHAPE, "quantize_block: blocks must be quantized in column order");
+    if (st) {  // the trailing update changes D: the next step starts a block
+        st->inc_c1 = -1;
+        st->inc_ready = false;
+    }
     const int64_t mr = r1 - r0;
     const int64_t group = qp->group > 0 ? qp->group : n;  // 0: one group per row
     const int64_t ngroups = (n + group - 1) / group;
@@ -739,6 +806,8 @@ static int lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_t b
     const int64_t n = st->n;
     if (c0 != st->locked || bs < 1 || c0 + bs > n)
         return set_error(ctx, REALQ_ERR_SHAPE, "bgd_lock_block: blocks must be locked in column order");
+    st->inc_c1 = -1;  // the residual base moves: the next step starts a block
+    st->inc_ready = false;
     if (!st->gram) {
         realq::GemmArgs g{st->Dhi + c0, st->Dlo + c0, n, st->Xhat + c0, n, st->m, st->T, bs, 1};
         Timed tm(ctx, "lock");
@@ -793,6 +862,11 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     // into chunks; the plan sizes the split-K and loss-partial workspaces for every chunk
     const realq::plan::StepPlan pl = realq::plan::plan_step(m, nJ, T, st->Tb, Tc, st->t, ctx->cus,
                                                             clip ? realq::clip_apply_partials() : 0);
+    // increments (token form): a later step of the block takes the residual as R0 + Q with
+    // Q = bf16(Dacc) Xhat_J^T and the gradient as G0 + bf16(Q o s) Xhat_J; the block's first step
+    // writes R0 and G0 and restarts Dacc
+    const bool inc_step = st->inc && !st->gram && st->inc_c1 == c1 && st->inc_ready;
+    const bool inc_first = st->inc && !st->gram && !inc_step;
     const int64_t Tn = pl.Tn;
     const int64_t nchunks = (int64_t)pl.chunks.size();
     if (st->gram) {
@@ -812,15 +886,25 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
             if ((rc = get_ws(ctx, "b_G", (size_t)m * nJ * 4, &Gacc))) return rc;
         if ((rc = get_ws(ctx, "b_parts", (size_t)pl.parts_total * 8, &parts))) return rc;
         double* const pbase = (double*)parts;
+        const bool via_acc = nchunks > 1 || dense;
+        // a later step's gradient GEMM gives the change since the block's first: that one is
+        // added back (in Adam, or as the start of the accumulated gradient)
+        if (inc_step && via_acc)
+            RQ_HIP(ctx, hipMemcpyAsync(Gacc, st->G0, (size_t)m * nJ * 4, hipMemcpyDeviceToDevice, s));
 
         for (int64_t ch = 0; ch < nchunks; ++ch) {
             const int64_t t0 = pl.chunks[ch].t0, cur = pl.chunks[ch].len;
             double* const pch = pbase + pl.chunks[ch].parts_off;
             realq::GemmArgs g{st->Dhi + c1, st->Dlo + c1, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
-            if (!clip) {
+            if (inc_step) {
+                realq::GemmArgs gi{st->Dinc + c1, nullptr, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
+                Timed tm(ctx, "resid_inc");
+                RQ_HIP(ctx, realq::gemm_resid_inc(gi, st->R0 + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi,
+                                                  q_ld(cur), pch, s));
+            } else if (!clip) {
                 Timed tm(ctx, "resid");
                 RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, nullptr,
-                                              r_ld(cur), pch, s, true));
+                                              r_ld(cur), pch, s, true, inc_first ? st->R0 + t0 : nullptr));
             } else {
                 // residual kept whole, per-token thresholds over the m channels, then the
                 // clipped, weighted split for the gradient GEMM and the loss partials
@@ -835,16 +919,23 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
                 realq::GemmArgs g{st->Rhi, clip ? st->Rlo : st->Rhi + 32, clip ? cur : r_ld(cur),
                                   st->XhT + c1 * T + t0, T, m, nJ, cur, pl.splits};
                 g.a_blocked = clip ? 0 : 1;
+                if (inc_step) {  // bf16(Q o s) alone, row-major
+                    g.Alo = nullptr;
+                    g.lda = q_ld(cur);
+                    g.a_blocked = 0;
+                }
                 splits_used = realq::gemm_effective_splits(cur, pl.splits);
-                Timed tm(ctx, "grad");
+                Timed tm(ctx, inc_step ? "grad_inc" : "grad");
                 RQ_HIP(ctx, realq::gemm_grad(g, (float*)Gp, nJ, m * nJ, s));
             }
-            if (nchunks > 1 || dense) {
+            if (via_acc) {
                 // Gacc (+)= sum of this chunk's split slices, chunks in order
-                RQ_HIP(ctx,
-                       realq::reduce_splits((const float*)Gp, splits_used, m, nJ, 1.f, (float*)Gacc, ch > 0, s));
+                RQ_HIP(ctx, realq::reduce_splits((const float*)Gp, splits_used, m, nJ, 1.f, (float*)Gacc,
+                                                 ch > 0 || inc_step, s));
             }
         }
+        if (inc_first && via_acc)
+            RQ_HIP(ctx, hipMemcpyAsync(st->G0, Gacc, (size_t)m * nJ * 4, hipMemcpyDeviceToDevice, s));
         if (loss_out) {
             if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
             else RQ_HIP(ctx, realq::reduce_partials(pbase, pl.parts_total, 0.5 / (double)Tn, loss_out, s));
@@ -870,6 +961,15 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     a.eps = st->prm.eps;
     a.bc1 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta1, (double)st->t)));
     a.bc2 = (float)(1.0 / (1.0 - std::pow((double)st->prm.beta2, (double)st->t)));
+    if (st->inc && !st->gram) {
+        a.Dacc = st->Dacc;
+        a.Dinc = st->Dinc;
+        a.inc_reset = inc_first ? 1 : 0;
+        a.G0 = st->G0;
+        a.g0_mode = (nchunks > 1 || dense) ? 0 : (inc_first ? 1 : 2);
+        st->inc_c1 = c1;
+        st->inc_ready = true;
+    }
     if (!dense && nchunks == 1 && !st->gram) {
         Timed tm(ctx, "adam");
         RQ_HIP(ctx, realq::adam_update(a, s));

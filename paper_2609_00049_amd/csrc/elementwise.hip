@@ -462,8 +462,14 @@ __device__ __forceinline__ void adam_elem(const AdamArgs& a, int64_t i, int64_t 
     a.vA[idx] = vv;
     float mh = mv * a.bc1;
     float vh = vv * a.bc2;
-    const double w = a.W[idx] - (double)(a.lr * mh / (sqrtf(vh) + a.eps));
+    const float step = a.lr * mh / (sqrtf(vh) + a.eps);
+    const double w = a.W[idx] - (double)step;
     a.W[idx] = w;
+    if (a.Dacc) {
+        const float d = (a.inc_reset ? 0.f : a.Dacc[idx]) - step;
+        a.Dacc[idx] = d;
+        a.Dinc[idx] = f2bf(d);
+    }
     if (!a.Dhi) return;
     uint16_t h, l;
     split_bf16((float)(w - (double)a.W0[idx]), h, l);
@@ -478,6 +484,8 @@ __global__ void adam_kernel(AdamArgs a) {
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
         float g = 0.f;
         for (int64_t z = 0; z < a.splits; ++z) g += a.Gp[z * zstride + e];
+        if (a.g0_mode == 2) g += a.G0[e];
+        else if (a.g0_mode == 1) a.G0[e] = g;
         g *= a.gscale;
         int64_t i = e / w, j = a.c1 + e % w;
         adam_elem(a, i, j, g);

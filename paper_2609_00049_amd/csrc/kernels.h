@@ -33,8 +33,13 @@ hipError_t gemm_acc_f64(const GemmArgs& g, double* C, int64_t ldc, hipStream_t s
 // (blocked = false) or in one array of 128-byte lines holding 32 tokens' hi then their lo
 // (blocked = true: hi at Rhi[i*ldr + (t/32)*64 + t%32], lo 32 further, ldr a multiple of 64;
 // Rlo unused), the A layout of a_blocked gradient launches.
+// With Rout, R is also stored there in float32 (layout of B0, ld ldb0).
 hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
-                      int64_t ldr, double* partials, hipStream_t st, bool blocked = false);
+                      int64_t ldr, double* partials, hipStream_t st, bool blocked = false, float* Rout = nullptr);
+// Later step of a column block (A = the weight change since its first step): loss partials of
+// R = R0 + acc, and Q = bf16(acc * s_t) [i*ldq + t].
+hipError_t gemm_resid_inc(const GemmArgs& g, const float* R0, int64_t ldr0, const float* s, uint16_t* Q, int64_t ldq,
+                          double* partials, hipStream_t st);
 hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
                      hipStream_t st);
 // Token-major stores for the module hand-off: out[j*ld + i] = bf16(acc[i][j] + add[j*ld + i]);
@@ -102,7 +107,8 @@ hipError_t blend_split(const float* M, const float* P, float alpha, int64_t m, u
 // out = sum of partials (fixed order) * scale, written to *out (device)
 hipError_t reduce_partials(const double* partials, int64_t count, double scale, double* out, hipStream_t st);
 // Adam on W[:, c1:n] with G = gscale * sum_z Gp[z][i][j - c1]; refreshes Dhi/Dlo = split(W - W0) there
-// (skipped when Dhi is NULL).
+// (skipped when Dhi is NULL).  With Dacc, the block's weight change since its first step is kept
+// too: Dacc = (reset ? 0 : Dacc) + the step (float32), Dinc = bf16(Dacc).
 struct AdamArgs {
     double* W;
     const float* W0;
@@ -114,6 +120,13 @@ struct AdamArgs {
     const float* Gp;  // [splits][m][n - c1]
     int64_t splits;
     float gscale, lr, beta1, beta2, eps, bc1, bc2;  // bc1 = 1/(1-beta1^t), bc2 = 1/(1-beta2^t)
+    float* Dacc = nullptr;     // [m, n]
+    uint16_t* Dinc = nullptr;  // [m, n]
+    int inc_reset = 0;
+    // the block's first gradient, [m][n - c1], unscaled: g0_mode 1 stores sum_z Gp there,
+    // 2 adds it to sum_z Gp (later steps, whose Gp holds the change only)
+    float* G0 = nullptr;
+    int g0_mode = 0;
 };
 hipError_t adam_update(const AdamArgs& a, hipStream_t st);
 // G[i][j] = (accumulate ? G[i][j] : 0) + gscale * sum_z Gp[z][i][j]  (m x w), z in order

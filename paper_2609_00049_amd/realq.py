@@ -57,7 +57,8 @@ class QParams(ctypes.Structure):
 class BgdParams(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int32), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("eps", ctypes.c_float), ("tok_chunk", ctypes.c_int64),
-                ("form", ctypes.c_int32), ("loss_clip", ctypes.c_float), ("batch", ctypes.c_int64)]
+                ("form", ctypes.c_int32), ("loss_clip", ctypes.c_float), ("batch", ctypes.c_int64),
+                ("resid_increment", ctypes.c_int32)]
 
 
 BGD_TOKENS = 0   # residual and gradient GEMMs over all tokens every step
@@ -221,8 +222,8 @@ def qparams(bits=4, group=128, block=128, grid=80, damp=0.01, sym=False) -> QPar
 
 
 def bgd_params(steps=0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, tok_chunk=0, form=BGD_TOKENS, loss_clip=0.0,
-               batch=0) -> BgdParams:
-    return BgdParams(steps, lr, beta1, beta2, eps, tok_chunk, form, loss_clip, batch)
+               batch=0, resid_increment=1) -> BgdParams:
+    return BgdParams(steps, lr, beta1, beta2, eps, tok_chunk, form, loss_clip, batch, resid_increment)
 
 
 class Context:

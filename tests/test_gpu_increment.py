@@ -1,0 +1,110 @@
+"""GPU parity of the increments (realq_bgd_params.resid_increment): within a column block,
+Block-GD steps after the first take the residual as R_0 + Q with Q = bf16(W_k - W_0) Xhat^T and
+the gradient as G_0 + bf16(Q o s)^T Xhat (Sec. 4.3: both are linear in the weights), where
+Adam's displacement bound keeps the weight change within rms(W0) / 32, n <= 8192 and T >= 16 n.
+The float64 oracle computes every step from scratch; the GPU runs with the increments allowed and
+forbidden on the same inputs.  Bars as in test_gpu_parity.py."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _banner(msg):
+    print(f"\n[gpu-case] {msg}", flush=True)
+
+
+def _run(rq, ctx, L, steps, lr, inc, chunk=0):
+    torch = _torch()
+    W0, X, Xh, s, M = P.to_device(L, torch)
+    res = rq.quantize_layer(ctx, W0, X, Xh, s, M, qp=rq.qparams(),
+                            bgd=rq.bgd_params(steps=steps, lr=lr, tok_chunk=chunk, resid_increment=inc))
+    torch.cuda.synchronize()
+    return res
+
+
+def _assert_parity(met, loss_gpu, loss_ref):
+    print(met, "loss", loss_gpu, loss_ref, flush=True)
+    assert met["code_identity"] >= P.CODE_IDENTITY
+    assert met["first_group_agreement"] >= P.CODE_IDENTITY
+    assert met["group_param_agreement"] >= P.GROUP_AGREEMENT_AFTER_BGD
+    assert abs(loss_gpu - loss_ref) <= P.LOSS_RTOL * abs(loss_ref)
+
+
+@pytest.mark.parametrize("m,n,T,chunk", [(300, 300, 4803, 0), (256, 384, 6144, 2048), (33, 200, 3200, 0)])
+def test_increment_matches_oracle(rq, ctx, m, n, T, chunk):
+    """LLaMA-3.1-8B-shaped inputs (weights N(0, 0.02^2), lr 1e-5, 8 steps per block: the bound holds)
+    at ragged row, column and token counts (T >= 16 n), and with the tokens streamed in chunks."""
+    L = synth.make_module("llama3.1_8b_layer", "gate", m=m, n=n, T=T, seed=11)
+    _banner(f"increment m={m} n={n} T={T} chunk={chunk}")
+    on = _run(rq, ctx, L, L.steps, L.lr, 1, chunk)
+    off = _run(rq, ctx, L, L.steps, L.lr, 0, chunk)
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=L.steps, lr=L.lr)
+    _assert_parity(P.compare(on, o), on.loss_final, o.loss_final)
+    _assert_parity(P.compare(off, o), off.loss_final, o.loss_final)
+    # the increment ran: the scales (searched on the stepped weights) or the loss differ in their
+    # last bits; the codes agree to the parity bar
+    assert on.loss_final != off.loss_final or not (on.W_hat.cpu() == off.W_hat.cpu()).all()
+    assert (on.codes.cpu() == off.codes.cpu()).float().mean().item() >= P.CODE_IDENTITY
+
+
+@pytest.mark.parametrize("case", ["lr", "tokens"])
+def test_increment_not_taken_where_the_gate_fails(rq, ctx, case):
+    """lr 1e-3 on weights of rms 0.02 (the displacement bound exceeds rms(W0) / 32), or the
+    workload's lr with fewer than 16 tokens per input column: the two settings run the same
+    launches and agree bitwise."""
+    if case == "lr":
+        L = synth.make_module("single_512", m=64, n=384, T=6144, seed=12)
+        steps, lr = 4, 1e-3
+    else:
+        L = synth.make_module("llama3.1_8b_layer", "gate", m=64, n=384, T=6143, seed=12)
+        steps, lr = L.steps, L.lr
+    _banner(f"increment gated off ({case})")
+    on = _run(rq, ctx, L, steps, lr, 1)
+    off = _run(rq, ctx, L, steps, lr, 0)
+    assert (on.W_hat.cpu() == off.W_hat.cpu()).all() and on.loss_final == off.loss_final
+
+
+def test_five_calls_compose_to_the_layer_call_with_increment(rq, ctx):
+    """The public calls (quantize_block, bgd_step) reproduce realq_quantize_layer bitwise with the
+    increment taken: quantize_block restarts it at every column block."""
+    torch = _torch()
+    L = synth.make_module("llama3.1_8b_layer", "gate", m=96, n=384, T=6144, seed=13)
+    _banner("five-call composition with the increment")
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    m, n, T = L.shape
+    steps, lr = 4, 1e-5
+    prm = rq.bgd_params(steps=steps, lr=lr)
+    ref = rq.quantize_layer(ctx, W0, X, Xh, s, qp=rq.qparams(), bgd=prm)
+    off = rq.quantize_layer(ctx, W0, X, Xh, s, qp=rq.qparams(), bgd=rq.bgd_params(steps=steps, lr=lr,
+                                                                                   resid_increment=0))
+    Hacc = torch.zeros((n, n), dtype=torch.float64, device="cuda")
+    rq.hessian_accum(ctx, Xh, s, Hacc)
+    U = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    dead = torch.empty((n,), dtype=torch.uint8, device="cuda")
+    rq.chol_inverse(ctx, Hacc, T, 0.01, U, None, dead)
+    st = rq.BgdState(ctx, W0, X, Xh, s, params=prm)
+    W = W0.double()
+    codes = torch.empty((m, n), dtype=torch.uint8, device="cuda")
+    scales = torch.empty((m, n // 128), dtype=torch.float32, device="cuda")
+    zeros = torch.empty((m, n // 128), dtype=torch.uint8, device="cuda")
+    qp = rq.qparams()
+    for c0 in range(0, n, 128):
+        rq.quantize_block(ctx, W, c0, 128, U, dead, qp, codes, scales, zeros, st)
+        if c0 + 128 < n:
+            for _ in range(steps):
+                rq.bgd_step(ctx, st, W, c0 + 128, 1.0)
+    torch.cuda.synchronize()
+    st.close()
+    assert (codes.cpu() == ref.codes.cpu()).all()
+    assert (W.float().cpu() == ref.W_hat.cpu()).all()
+    assert ref.loss_final != off.loss_final or not (ref.W_hat.cpu() == off.W_hat.cpu()).all()
