@@ -108,3 +108,36 @@ def test_five_calls_compose_to_the_layer_call_with_increment(rq, ctx):
     assert (codes.cpu() == ref.codes.cpu()).all()
     assert (W.float().cpu() == ref.W_hat.cpu()).all()
     assert ref.loss_final != off.loss_final or not (ref.W_hat.cpu() == off.W_hat.cpu()).all()
+
+
+@pytest.mark.parametrize("case", ["dense_metric", "window_partner"])
+def test_increment_with_a_metric(rq, ctx, case):
+    """The gradient through a dense metric M (Eq. fisher_loss) or blended with the window partner's
+    pull-back P (Eq. slide_window): the block's first gradient sum is added back before M_a is
+    applied.  256 x 256 at 4096 tokens (16 per column), the workload's lr, 4 steps per block."""
+    torch = _torch()
+    L = synth.make_module("llama3.1_8b_layer", "q", m=256, n=256, T=4096, seed=14)
+    r = np.random.default_rng(15)
+    M = Pm = None
+    window = None
+    if case == "dense_metric":
+        A = r.standard_normal((256, 512))
+        M = (A @ A.T / 512).astype(np.float32)
+    else:
+        Wn = (r.standard_normal((192, 256)) * 0.05).astype(np.float32)
+        Pm = oracle.pullback_metric(Wn).astype(np.float32)
+        window = (1, 3)     # alpha = 1/2 at the one Block-GD block
+    steps, lr = 4, L.lr
+    _banner(f"increment with {case}")
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    Md = None if M is None else torch.from_numpy(M).cuda()
+    Pd = None if Pm is None else torch.from_numpy(Pm).cuda()
+    res = {}
+    for inc in (1, 0):
+        res[inc] = rq.quantize_layer(ctx, W0, X, Xh, s, Md, Pd, qp=rq.qparams(),
+                                     bgd=rq.bgd_params(steps=steps, lr=lr, resid_increment=inc), window=window)
+    torch.cuda.synchronize()
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, M=M, P=Pm, steps=steps, lr=lr, window=window)
+    for inc in (1, 0):
+        _assert_parity(P.compare(res[inc], o), res[inc].loss_final, o.loss_final)
+    assert res[1].loss_final != res[0].loss_final or not (res[1].W_hat.cpu() == res[0].W_hat.cpu()).all()
