@@ -481,15 +481,18 @@ def test_layer_llama_gate_full_size_sampled_rows(rq, ctx):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("cfg,module,chunk", [
-    ("qwen3_32b_layer", "gate", 0),          # 25600 x 5120, Student-t nu = 3 activations
-    ("llama3.1_70b_layer", "gate", 2048),    # 28672 x 8192, calibration tokens streamed in chunks
+@pytest.mark.parametrize("cfg,module,chunk,T", [
+    ("qwen3_32b_layer", "gate", 0, 8192),          # 25600 x 5120, Student-t nu = 3 activations
+    ("llama3.1_70b_layer", "gate", 2048, 8192),    # 28672 x 8192, calibration tokens streamed in chunks
+    ("qwen3_32b_layer", "gate", 0, 131072),        # 25.6 tokens per input column: Block-GD increments on
 ])
-def test_layer_large_module_shape_sampled_rows(rq, ctx, cfg, module, chunk):
+def test_layer_large_module_shape_sampled_rows(rq, ctx, cfg, module, chunk, T):
     """The largest projections of the Qwen3-32B- and LLaMA-3.1-70B-shaped layers at their full
-    m x n with 8192 tokens and 8 Block-GD steps per block at the
-    workload's learning rate.  The 70B case streams the tokens through the residual and gradient
-    GEMMs in chunks (2048 of 8192 here), as its full-size workload does with 32768-token chunks.
+    m x n with 8192 tokens (and the 32B gate with 131072, where the Block-GD steps after a column
+    block's first take their residual and gradient as bf16 increments) and 8 Block-GD steps per
+    block at the workload's learning rate.  The 70B case streams the tokens through the residual
+    and gradient GEMMs in chunks (2048 of 8192 here), as its full-size workload does with
+    32768-token chunks.
     The oracle follows 128 sampled rows (one in every 256-row tile of the GEMMs, the rest at random)
     through the Gram-form surrogate (pinned equal to the token form; rows are independent for the
     identity metric).  Adam's first step is about lr * sign(g), so a weight whose gradient is near
@@ -501,7 +504,7 @@ def test_layer_large_module_shape_sampled_rows(rq, ctx, cfg, module, chunk):
     GPU's own weights in every row."""
     import time
     t0 = time.time()
-    L = synth.make_module(cfg, module, T=8192)
+    L = synth.make_module(cfg, module, T=T)
     m, n, T = L.shape
     assert L.M is None
     _banner(f"layer {cfg} {module} {m}x{n} T={T} chunk={chunk}: inputs drawn in {time.time() - t0:.0f} s")
