@@ -141,3 +141,23 @@ def test_increment_with_a_metric(rq, ctx, case):
     for inc in (1, 0):
         _assert_parity(P.compare(res[inc], o), res[inc].loss_final, o.loss_final)
     assert res[1].loss_final != res[0].loss_final or not (res[1].W_hat.cpu() == res[0].W_hat.cpu()).all()
+
+
+def test_increment_with_row_groups(rq, ctx):
+    """N_g = 3 row groups, each with its own saliency Hessian (Alg. 1, Stage 1): the increments
+    restart at every group's quantization of a block and at the lock."""
+    torch = _torch()
+    L = synth.make_module("llama3.1_8b_layer", "gate", m=200, n=256, T=4096, seed=16)
+    S = synth.make_group_weights(3, 4096, seed=17)
+    _banner("increment with 3 row groups")
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    Sd = torch.from_numpy(S).cuda()
+    res = {}
+    for inc in (1, 0):
+        res[inc] = rq.quantize_layer(ctx, W0, X, Xh, s, qp=rq.qparams(),
+                                     bgd=rq.bgd_params(steps=L.steps, lr=L.lr, resid_increment=inc), s_groups=Sd)
+    torch.cuda.synchronize()
+    o = oracle.quantize_layer(L.W0, L.X, L.Xhat, L.s, steps=L.steps, lr=L.lr, s_groups=S)
+    for inc in (1, 0):
+        _assert_parity(P.compare(res[inc], o), res[inc].loss_final, o.loss_final)
+    assert res[1].loss_final != res[0].loss_final or not (res[1].W_hat.cpu() == res[0].W_hat.cpu()).all()
