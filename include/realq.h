@@ -76,20 +76,22 @@ typedef struct realq_qparams {
  *               Adam step t of the module (1-based) uses the consecutive token batch
  *               (t - 1) mod ceil(T / batch); loss and gradient are normalised by its
  *               size.  The final loss is always over all T tokens and unclipped.
- *   resid_increment : 1 = allowed [1], 0 = never.  Residual and gradient are linear in
- *               the weights, so within one column block step k > 0 can take them as
- *               R_k = R_0 + Q_k with Q_k = bf16(W_k - W_0)_J Xhat_J^T, and
- *               G_k = G_0 + M_a bf16(Q_k o s) Xhat_J / T, from the block's first residual R_0
- *               (kept in float32) and gradient G_0: one bf16 MFMA pass each over the weight
- *               change instead of two over the float32 D = W - W0 and R o s.  Token form, no
+ *   resid_increment : 1 = allowed [1], 0 = never.  Residual, gradient and loss are
+ *               linear or quadratic in the weights, so within one column block step k > 0
+ *               can take them from the block's first step (residual R_0, gradient G_0, loss
+ *               L_0) and the weight change Delta = bf16(W_k - W_0)_J: R_k = R_0 + Q_k with
+ *               Q_k = Delta Xhat_J^T, G_k = G_0 + M_a bf16(Q_k o s) Xhat_J / T and, for
+ *               M_a = I, loss L_0 + <G_0, Delta> + sum s Q_k^2 / 2T.  One bf16 MFMA pass over
+ *               Delta for Q_k and one over Q_k for the gradient, instead of two over the
+ *               float32 D = W - W0 and R o s; R_0 itself is never stored.  Token form, no
  *               clip, batch = T, and only where the change is small enough that its bf16
  *               rounding stays below what the sweep's decisions resolve: the weights cannot
  *               move by more than rms(W0) / 32 within a block ((steps - 1) lr (1 - beta1) /
- *               sqrt((1 - beta2)(1 - beta1^2/beta2)) bounds that move: the Adam step's supremum
- *               over every gradient history; needs beta1^2 < beta2), n <= 8192 (at most 64
- *               column blocks carry the rounding forward) and T >= 16 n (the gradient's
- *               rounding averages over at least 16 tokens per input column).  Costs a float32
- *               [m, T] array and [m, n] arrays (two float32, one bf16).
+ *               sqrt((1 - beta2)(1 - beta1^2/beta2)) bounds that move: the Adam step's
+ *               supremum over every gradient history; needs beta1^2 < beta2), n <= 8192 (at
+ *               most 64 column blocks carry the rounding forward) and T >= 16 n (the
+ *               gradient's rounding averages over at least 16 tokens per input column).
+ *               Costs [m, n] arrays (two float32, one bf16).
  *   The Gram form takes neither a clip nor a batch smaller than T. */
 typedef struct realq_bgd_params {
     int32_t steps;

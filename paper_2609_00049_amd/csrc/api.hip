@@ -96,12 +96,12 @@ struct realq_bgd_state {
     int64_t Tb = 0, nbatch = 1;  // tokens per step and number of batches (mini-batch BGD)
     float* Rf = nullptr;         // [m,Tc] residual kept whole for the clip
     float* tau = nullptr;        // [Tc] per-token clip thresholds
-    // increments within a column block: R0 [m,T] the block's first residual, G0 its first
-    // gradient ([m, n - c1], unscaled sum over tokens), Dacc [m,n] the weight change since then
-    // and Dinc = bf16(Dacc); inc_c1 names the block they belong to (-1: none) and inc_ready says
-    // Dinc holds the change of the current weights
+    // increments within a column block: L0 the loss of the block's first step (device scalar),
+    // G0 its gradient ([m, n - c1], unscaled sum over tokens), Dacc [m,n] the weight change since
+    // then and Dinc = bf16(Dacc); inc_c1 names the block they belong to (-1: none) and inc_ready
+    // says Dinc holds the change of the current weights
     bool inc = false;
-    float* R0 = nullptr;
+    double* L0 = nullptr;
     float* G0 = nullptr;
     float* Dacc = nullptr;
     uint16_t* Dinc = nullptr;
@@ -482,8 +482,8 @@ static int inc_init(realq_bgd_state* st) {
     RQ_HIP(ctx, hipStreamSynchronize(ctx->stream));
     if (!(disp <= std::sqrt(msq) / 32.0)) return REALQ_OK;
     void* q;
-    if ((rc = state_alloc(st, &q, (size_t)m * T * 4, "s_R0"))) return rc;
-    st->R0 = (float*)q;
+    if ((rc = state_alloc(st, &q, 8, "s_L0"))) return rc;
+    st->L0 = (double*)q;
     if ((rc = state_alloc(st, &q, (size_t)m * n * 4, "s_Dacc"))) return rc;
     st->Dacc = (float*)q;
     if ((rc = state_alloc(st, &q, (size_t)m * n * 2, "s_Dinc"))) return rc;
@@ -862,9 +862,10 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     // into chunks; the plan sizes the split-K and loss-partial workspaces for every chunk
     const realq::plan::StepPlan pl = realq::plan::plan_step(m, nJ, T, st->Tb, Tc, st->t, ctx->cus,
                                                             clip ? realq::clip_apply_partials() : 0);
-    // increments (token form): a later step of the block takes the residual as R0 + Q with
-    // Q = bf16(Dacc) Xhat_J^T and the gradient as G0 + bf16(Q o s) Xhat_J; the block's first step
-    // writes R0 and G0 and restarts Dacc
+    // increments (token form): a later step of the block takes the change of its residual as
+    // Q = bf16(Dacc) Xhat_J^T, its gradient as G0 + bf16(Q o s) Xhat_J and its loss as
+    // L0 + <G0, bf16(Dacc)> / T + sum s Q^2 / 2T; the block's first step writes L0 and G0 and
+    // restarts Dacc
     const bool inc_step = st->inc && !st->gram && st->inc_c1 == c1 && st->inc_ready;
     const bool inc_first = st->inc && !st->gram && !inc_step;
     const int64_t Tn = pl.Tn;
@@ -899,12 +900,11 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
             if (inc_step) {
                 realq::GemmArgs gi{st->Dinc + c1, nullptr, n, st->Xhat + t0 * n + c1, n, m, cur, nJ, 1};
                 Timed tm(ctx, "resid_inc");
-                RQ_HIP(ctx, realq::gemm_resid_inc(gi, st->R0 + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi,
-                                                  q_ld(cur), pch, s));
+                RQ_HIP(ctx, realq::gemm_resid_inc(gi, st->s ? st->s + t0 : nullptr, st->Rhi, q_ld(cur), pch, s));
             } else if (!clip) {
                 Timed tm(ctx, "resid");
                 RQ_HIP(ctx, realq::gemm_resid(g, st->B + t0, T, st->s ? st->s + t0 : nullptr, st->Rhi, nullptr,
-                                              r_ld(cur), pch, s, true, inc_first ? st->R0 + t0 : nullptr));
+                                              r_ld(cur), pch, s, true));
             } else {
                 // residual kept whole, per-token thresholds over the m channels, then the
                 // clipped, weighted split for the gradient GEMM and the loss partials
@@ -936,9 +936,19 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         }
         if (inc_first && via_acc)
             RQ_HIP(ctx, hipMemcpyAsync(st->G0, Gacc, (size_t)m * nJ * 4, hipMemcpyDeviceToDevice, s));
+        if (inc_first && !dense)
+            RQ_HIP(ctx, realq::reduce_partials(pbase, pl.parts_total, 0.5 / (double)Tn, st->L0, s));
         if (loss_out) {
-            if (dense) RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
-            else RQ_HIP(ctx, realq::reduce_partials(pbase, pl.parts_total, 0.5 / (double)Tn, loss_out, s));
+            if (dense) {
+                RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));
+            } else if (inc_step) {
+                void* dots;
+                if ((rc = get_ws(ctx, "b_incdots", (size_t)realq::inc_loss_partials() * 8, &dots))) return rc;
+                RQ_HIP(ctx, realq::inc_loss(st->L0, st->G0, st->Dinc + c1, n, m, nJ, pbase, pl.parts_total,
+                                            (double)Tn, (double*)dots, loss_out, s));
+            } else {
+                RQ_HIP(ctx, realq::reduce_partials(pbase, pl.parts_total, 0.5 / (double)Tn, loss_out, s));
+            }
         }
     }
     st->t += 1;

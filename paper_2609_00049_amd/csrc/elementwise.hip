@@ -499,6 +499,56 @@ hipError_t adam_update(const AdamArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// The cross term <G0, Dinc> in fixed-order per-block float64 sums, then one block adds it to L0
+// and the partial sums of s_t acc^2.
+constexpr int INC_DOT_BLOCKS = 512;
+__global__ __launch_bounds__(256) void inc_dot_kernel(const float* __restrict__ G0, const uint16_t* __restrict__ Dinc,
+                                                      int64_t ldd, int64_t m, int64_t w, double* __restrict__ dots) {
+    __shared__ double red[256];
+    double acc = 0.0;
+    const int64_t total = m * w;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)INC_DOT_BLOCKS * 256) {
+        const int64_t i = e / w, j = e - i * w;
+        acc += (double)G0[e] * (double)bf2f(Dinc[i * ldd + j]);
+    }
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int k = 128; k > 0; k >>= 1) {
+        if (threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) dots[blockIdx.x] = red[0];
+}
+
+__global__ __launch_bounds__(256) void inc_loss_kernel(const double* __restrict__ L0, const double* __restrict__ dots,
+                                                       const double* __restrict__ parts, int64_t nparts, double T,
+                                                       double* __restrict__ out) {
+    __shared__ double rd[256], rp[256];
+    double d = 0.0, p = 0.0;
+    for (int64_t k = threadIdx.x; k < INC_DOT_BLOCKS; k += 256) d += dots[k];
+    for (int64_t k = threadIdx.x; k < nparts; k += 256) p += parts[k];
+    rd[threadIdx.x] = d;
+    rp[threadIdx.x] = p;
+    __syncthreads();
+    for (int k = 128; k > 0; k >>= 1) {
+        if (threadIdx.x < k) {
+            rd[threadIdx.x] += rd[threadIdx.x + k];
+            rp[threadIdx.x] += rp[threadIdx.x + k];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *out = *L0 + rd[0] / T + 0.5 / T * rp[0];
+}
+
+int64_t inc_loss_partials() { return INC_DOT_BLOCKS; }
+
+hipError_t inc_loss(const double* L0, const float* G0, const uint16_t* Dinc, int64_t ldd, int64_t m, int64_t w,
+                    const double* parts, int64_t nparts, double T, double* dots, double* out, hipStream_t st) {
+    hipLaunchKernelGGL(inc_dot_kernel, dim3(INC_DOT_BLOCKS), dim3(256), 0, st, G0, Dinc, ldd, m, w, dots);
+    hipLaunchKernelGGL(inc_loss_kernel, dim3(1), dim3(256), 0, st, L0, dots, parts, nparts, T, out);
+    return hipGetLastError();
+}
+
 __global__ void adam_dense_kernel(AdamArgs a, const float* __restrict__ G) {
     const int64_t w = a.n - a.c1;
     const int64_t total = a.m * w;

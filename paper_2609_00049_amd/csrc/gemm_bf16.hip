@@ -430,9 +430,7 @@ __global__ __launch_bounds__(C::NT) void gemm_nt_kernel(const uint16_t* __restri
 #pragma unroll
             for (int t = 0; t < NSUB; ++t) {
                 switch (after(t)) {  // constant after unrolling
-                    case 4: wait_vmcnt<4>(); break;
                     case 8: wait_vmcnt<8>(); break;
-                    case 12: wait_vmcnt<12>(); break;
                     case 16: wait_vmcnt<16>(); break;
                     case 20: wait_vmcnt<20>(); break;
                     case 24: wait_vmcnt<24>(); break;
@@ -666,13 +664,9 @@ __device__ __forceinline__ TokW load_tokw(const float* s, int64_t t) {
 
 // Residual: R = B0[i][t] + acc; writes split(R * s_t) and accumulates s_t R^2.
 // With blk, split(R o s) goes to one array of 128-byte lines: 32 tokens' hi, then their lo.
-// With kOut, R itself is also stored to Rout in float32, in B0's layout.
-template <bool kOut>
-struct EpiResidT {
+struct EpiResid {
     static constexpr bool kRowDma = true;  // residual base streamed into LDS by full tiles
-    // store instructions per lane and 32x32 sub-tile (4 rows x hi, lo); the streamed path waits
-    // on this count, and the 4 more stores of Rout only make those waits stricter
-    static constexpr int kRowStores = 8;
+    static constexpr int kRowStores = 8;   // store instructions per lane and 32x32 sub-tile (4 rows x hi, lo)
     static constexpr bool kReduce = true;
     static constexpr bool kTransposed = false;
     const float* B0;
@@ -683,7 +677,6 @@ struct EpiResidT {
     int64_t ldr;
     double* partials;
     bool blk;
-    float* Rout;
     struct Row {
         f32x4 b;
         bool ok;
@@ -699,11 +692,10 @@ struct EpiResidT {
     // offsets of a sub-tile's first row, 8-byte output quads
     __device__ bool row_dma_ok() const {
         const bool out = blk ? (al8(Rhi) && ldr % 64 == 0) : (al8(Rhi) && al8(Rlo) && ldr % 4 == 0);
-        return al16(B0) && ldb0 % 4 == 0 && ldb0 < (int64_t(1) << 24) && out && (!kOut || al16(Rout));
+        return al16(B0) && ldb0 % 4 == 0 && ldb0 < (int64_t(1) << 24) && out;
     }
     __device__ void operator()(int64_t i, int64_t t, float v, int64_t, float& aux) const {
         float r = B0[i * ldb0 + t] + v;
-        if constexpr (kOut) Rout[i * ldb0 + t] = r;
         float w = s ? s[t] : 1.f;
         float rs = r * w;
         uint16_t hi, lo;
@@ -716,7 +708,7 @@ struct EpiResidT {
     __device__ Row load_row(int64_t i, int64_t t, int64_t) const {
         Row r;
         const float* b = B0 + i * ldb0 + t;
-        r.ok = al16(b) && al8(hi_at(i, t)) && al8(lo_at(i, t)) && (!kOut || al16(Rout + i * ldb0 + t));
+        r.ok = al16(b) && al8(hi_at(i, t)) && al8(lo_at(i, t));
         if (r.ok) r.b = *reinterpret_cast<const f32x4*>(b);
         return r;
     }
@@ -726,7 +718,6 @@ struct EpiResidT {
             return;
         }
         const f32x4 r = row.b + v;
-        if constexpr (kOut) *reinterpret_cast<f32x4*>(Rout + i * ldb0 + t) = r;
         u16x4 h, l;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -743,61 +734,41 @@ struct EpiResidT {
     __device__ void partial(int64_t b, double v) const { partials[b] = v; }
 };
 
-struct EpiResid : EpiResidT<false> {};
-struct EpiResidKeep : EpiResidT<true> {};  // the first step of a column block keeps R
-
-// A later step of a column block: acc = bf16(W_k - W_0) Xhat^T is the change since the block's
-// first residual B0 = R_0.  R = B0 + acc gives the loss partials (s_t R^2); the gradient GEMM
-// takes bf16(acc * s_t) alone, row-major [i * ldq + t] (the caller adds the block's first
-// gradient back).
+// A later step of a column block: acc = bf16(W_k - W_0) Xhat^T is the change of the residual since
+// the block's first step.  Writes bf16(acc * s_t) row-major [i * ldq + t] for the gradient GEMM
+// and accumulates s_t acc^2, the part of the step's loss that the block's first residual and
+// gradient do not give (the caller adds them).
 struct EpiResidInc {
-    static constexpr bool kRowDma = true;
-    static constexpr int kRowStores = 4;  // store instructions per lane and 32x32 sub-tile (4 rows)
+    static constexpr bool kRowDma = false;
     static constexpr bool kReduce = true;
     static constexpr bool kTransposed = false;
-    const float* B0;
-    int64_t ldb0;
     const float* s;
     uint16_t* Q;
     int64_t ldq;
     double* partials;
     struct Row {
-        f32x4 b;
         bool ok;
     };
     using Col = TokW;
-    __device__ const float* row_base() const { return B0; }
-    __device__ int64_t row_ld() const { return ldb0; }
-    __device__ bool row_dma_ok() const {
-        return al16(B0) && ldb0 % 4 == 0 && ldb0 < (int64_t(1) << 24) && al8(Q) && ldq % 4 == 0;
-    }
     __device__ void operator()(int64_t i, int64_t t, float v, int64_t, float& aux) const {
-        const float r = B0[i * ldb0 + t] + v;
         const float w = s ? s[t] : 1.f;
-        Q[i * ldq + t] = f2bf(v * w);
-        const float rs = r * w;
-        aux += rs * r;
+        const float vs = v * w;
+        Q[i * ldq + t] = f2bf(vs);
+        aux += vs * v;
     }
     __device__ Col load_col(int64_t t) const { return load_tokw(s, t); }
-    __device__ Row load_row(int64_t i, int64_t t, int64_t) const {
-        Row r;
-        const float* b = B0 + i * ldb0 + t;
-        r.ok = al16(b) && al8(Q + i * ldq + t);
-        if (r.ok) r.b = *reinterpret_cast<const f32x4*>(b);
-        return r;
-    }
-    __device__ void vec4(int64_t i, int64_t t, f32x4 v, const Row& row, const Col& col, int64_t z, float& aux) const {
+    __device__ Row load_row(int64_t i, int64_t t, int64_t) const { return {al8(Q + i * ldq + t)}; }
+    __device__ void vec4(int64_t i, int64_t t, f32x4 v, const Row&, const Col& col, int64_t z, float& aux) const {
         if (!col.ok) {
             for (int u = 0; u < 4; ++u) (*this)(i, t + u, v[u], z, aux);
             return;
         }
-        const f32x4 r = row.b + v;
         u16x4 q;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            q[u] = f2bf(v[u] * col.w[u]);
-            const float rs = r[u] * col.w[u];
-            aux += rs * r[u];
+            const float vs = v[u] * col.w[u];
+            q[u] = f2bf(vs);
+            aux += vs * v[u];
         }
         *reinterpret_cast<u16x4*>(Q + i * ldq + t) = q;
     }
@@ -1033,14 +1004,13 @@ hipError_t gemm_resid_f32(const GemmArgs& g, const float* B0, int64_t ldb0, floa
     return launch(g, EpiResidF32{B0, ldb0, R, ldr}, st);
 }
 hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
-                      int64_t ldr, double* partials, hipStream_t st, bool blocked, float* Rout) {
+                      int64_t ldr, double* partials, hipStream_t st, bool blocked) {
     if (blocked && (ldr % 64 != 0 || g.N > ldr / 2)) return hipErrorInvalidValue;
-    if (Rout) return launch(g, EpiResidKeep{{B0, ldb0, s, Rhi, Rlo, ldr, partials, blocked, Rout}}, st);
-    return launch(g, EpiResid{{B0, ldb0, s, Rhi, Rlo, ldr, partials, blocked, nullptr}}, st);
+    return launch(g, EpiResid{B0, ldb0, s, Rhi, Rlo, ldr, partials, blocked}, st);
 }
-hipError_t gemm_resid_inc(const GemmArgs& g, const float* R0, int64_t ldr0, const float* s, uint16_t* Q, int64_t ldq,
-                          double* partials, hipStream_t st) {
-    return launch(g, EpiResidInc{R0, ldr0, s, Q, ldq, partials}, st);
+hipError_t gemm_resid_inc(const GemmArgs& g, const float* s, uint16_t* Q, int64_t ldq, double* partials,
+                          hipStream_t st) {
+    return launch(g, EpiResidInc{s, Q, ldq, partials}, st);
 }
 hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
                      hipStream_t st) {

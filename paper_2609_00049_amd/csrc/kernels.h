@@ -33,13 +33,12 @@ hipError_t gemm_acc_f64(const GemmArgs& g, double* C, int64_t ldc, hipStream_t s
 // (blocked = false) or in one array of 128-byte lines holding 32 tokens' hi then their lo
 // (blocked = true: hi at Rhi[i*ldr + (t/32)*64 + t%32], lo 32 further, ldr a multiple of 64;
 // Rlo unused), the A layout of a_blocked gradient launches.
-// With Rout, R is also stored there in float32 (layout of B0, ld ldb0).
 hipError_t gemm_resid(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, uint16_t* Rhi, uint16_t* Rlo,
-                      int64_t ldr, double* partials, hipStream_t st, bool blocked = false, float* Rout = nullptr);
-// Later step of a column block (A = the weight change since its first step): loss partials of
-// R = R0 + acc, and Q = bf16(acc * s_t) [i*ldq + t].
-hipError_t gemm_resid_inc(const GemmArgs& g, const float* R0, int64_t ldr0, const float* s, uint16_t* Q, int64_t ldq,
-                          double* partials, hipStream_t st);
+                      int64_t ldr, double* partials, hipStream_t st, bool blocked = false);
+// Later step of a column block (A = the weight change since its first step): Q = bf16(acc * s_t)
+// [i*ldq + t] and partial sums of s_t acc^2.
+hipError_t gemm_resid_inc(const GemmArgs& g, const float* s, uint16_t* Q, int64_t ldq, double* partials,
+                          hipStream_t st);
 hipError_t gemm_loss(const GemmArgs& g, const float* B0, int64_t ldb0, const float* s, double* partials,
                      hipStream_t st);
 // Token-major stores for the module hand-off: out[j*ld + i] = bf16(acc[i][j] + add[j*ld + i]);
@@ -129,6 +128,13 @@ struct AdamArgs {
     int g0_mode = 0;
 };
 hipError_t adam_update(const AdamArgs& a, hipStream_t st);
+// Loss of a later step of a column block from the block's first loss L0 and first gradient sum
+// G0 [m][w] (unscaled, over the T tokens), the bf16 weight change Dinc [i*ldd + j] and the partial
+// sums of s_t acc^2: *out = *L0 + <G0, Dinc> / T + 0.5 / T * sum(parts).  dots: inc_loss_partials()
+// doubles of workspace.
+hipError_t inc_loss(const double* L0, const float* G0, const uint16_t* Dinc, int64_t ldd, int64_t m, int64_t w,
+                    const double* parts, int64_t nparts, double T, double* dots, double* out, hipStream_t st);
+int64_t inc_loss_partials();
 // G[i][j] = (accumulate ? G[i][j] : 0) + gscale * sum_z Gp[z][i][j]  (m x w), z in order
 hipError_t reduce_splits(const float* Gp, int64_t splits, int64_t m, int64_t w, float gscale, float* G,
                          bool accumulate, hipStream_t st);

@@ -55,6 +55,14 @@ def test_increment_matches_oracle(rq, ctx, m, n, T, chunk):
     # last bits; the codes agree to the parity bar
     assert on.loss_final != off.loss_final or not (on.W_hat.cpu() == off.W_hat.cpu()).all()
     assert (on.codes.cpu() == off.codes.cpu()).float().mean().item() >= P.CODE_IDENTITY
+    # the per-step losses of the later steps come from L0 + <G0, Delta> + sum s Q^2 / 2T: the first
+    # block's match the oracle's trace, every block's the two-pass run's
+    steps = L.steps
+    tr_on = on.loss_trace.cpu().numpy().reshape(-1, steps)[:-1]
+    tr_off = off.loss_trace.cpu().numpy().reshape(-1, steps)[:-1]
+    ref = np.array([v for (_, _, v) in o.loss_trace]).reshape(-1, steps)
+    np.testing.assert_allclose(tr_on[0], ref[0], rtol=1e-4)
+    np.testing.assert_allclose(tr_on, tr_off, rtol=1e-4)
 
 
 @pytest.mark.parametrize("case", ["lr", "tokens"])
