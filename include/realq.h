@@ -283,7 +283,11 @@ int realq_bgd_lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_
  * (Eq. fisher_loss at the module output; Eq. slide_window for alpha).  The gradient
  * (1/T) M_a R diag(s) Xhat[:, c1:] is formed with token-streamed GEMMs.
  * loss_out (device float64 scalar, may be NULL) receives L before the update; it
- * is computed for M_a = identity only and set to NaN otherwise.  c1 == n is a no-op. */
+ * is computed for M_a = identity only and set to NaN otherwise.  c1 == n is a no-op.
+ * With increments (realq_bgd_params.resid_increment and its gate), the state keeps the
+ * loss and gradient of the first step at a given c1 and later steps at the same c1 start
+ * from them; realq_quantize_block(_rows) and realq_bgd_lock_block restart that, as does a
+ * step at another c1. */
 int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W /*[m,n]*/, int64_t c1, float alpha,
                    double* loss_out);
 
