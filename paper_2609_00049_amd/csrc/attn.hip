@@ -620,9 +620,12 @@ __global__ __launch_bounds__(256) void attn_ds_lds_kernel(const uint16_t* __rest
             attn_dma16(vb, off, dst + TBYTES + (uint32_t)qi * 1024);
         }
     };
-    // this wave's rows: query fragments (LDS), dO (registers, split per key tile), LSE and D (LDS)
+    // this wave's rows: query fragments (LDS), dO (registers, split once into its three bf16
+    // terms: the same for every key tile), LSE and D (LDS)
     uint16_t* const qw = sQ[wave];
-    f32x4 dOr[NK][2];
+    bf16x8 dOh[NK], dOl[NK], dOl2[NK];
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) dOh[kk] = dOl[kk] = dOl2[kk] = bf16x8{};
     if (active) {
         const uint16_t* qa = qr + (s * L + it * AT + c32) * (H * HD) + h * HD + k8;
         const float* a = dO + (s * L + it * AT + c32) * (H * HD) + h * HD + k8;
@@ -631,8 +634,7 @@ __global__ __launch_bounds__(256) void attn_ds_lds_kernel(const uint16_t* __rest
             const int c = 2 * kk + (lane >> 5);
             *reinterpret_cast<u16x8*>(qw + c32 * HD + (c ^ (c32 % KCH)) * 8) =
                 *reinterpret_cast<const u16x8*>(qa + 16 * kk);
-            dOr[kk][0] = *reinterpret_cast<const f32x4*>(a + 16 * kk);
-            dOr[kk][1] = *reinterpret_cast<const f32x4*>(a + 16 * kk + 4);
+            split8x3(a + 16 * kk, dOh[kk], dOl[kk], dOl2[kk]);
         }
         if (lane < AT) {
             sLD[wave][0][lane] = LSE[(s * L + it * AT + lane) * H + h];
@@ -676,18 +678,10 @@ __global__ __launch_bounds__(256) void attn_ds_lds_kernel(const uint16_t* __rest
         for (int kk = 0; kk < NK; ++kk) {  // dO in three terms: dP - D cancels
             const int c = 2 * kk + (lane >> 5);
             const int off = c32 * HD + ((c ^ (c32 % KCH)) * 8);
-            float x8[8];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                x8[u] = dOr[kk][0][u];
-                x8[u + 4] = dOr[kk][1][u];
-            }
-            bf16x8 ah, al, al2;
-            split8x3(x8, ah, al, al2);
             const bf16x8 bv = ld8(vt_ + off);
-            acc = mfma(ah, bv, acc);
-            acc = mfma(al, bv, acc);
-            acc = mfma(al2, bv, acc);
+            acc = mfma(dOh[kk], bv, acc);
+            acc = mfma(dOl[kk], bv, acc);
+            acc = mfma(dOl2[kk], bv, acc);
             sc = mfma(ld8(qw + off), ld8(kt + off), sc);
         }
         uint32_t dsv[16], pv2[16];
