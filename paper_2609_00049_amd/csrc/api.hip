@@ -936,8 +936,9 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         }
         if (inc_first && via_acc)
             RQ_HIP(ctx, hipMemcpyAsync(st->G0, Gacc, (size_t)m * nJ * 4, hipMemcpyDeviceToDevice, s));
-        if (inc_first && !dense)
-            RQ_HIP(ctx, realq::reduce_partials(pbase, pl.parts_total, 0.5 / (double)Tn, st->L0, s));
+        // the identity-metric loss of the block's first step (its partials exist for any metric: a
+        // caller may change alpha between the steps of one block)
+        if (inc_first) RQ_HIP(ctx, realq::reduce_partials(pbase, pl.parts_total, 0.5 / (double)Tn, st->L0, s));
         if (loss_out) {
             if (dense) {
                 RQ_HIP(ctx, realq::fill_f64(loss_out, NAN, 1, s));

@@ -169,3 +169,43 @@ def test_increment_with_row_groups(rq, ctx):
     for inc in (1, 0):
         _assert_parity(P.compare(res[inc], o), res[inc].loss_final, o.loss_final)
     assert res[1].loss_final != res[0].loss_final or not (res[1].W_hat.cpu() == res[0].W_hat.cpu()).all()
+
+
+def test_increment_loss_when_alpha_changes_within_a_block(rq, ctx):
+    """Through the public calls a caller may change the window's alpha between the steps of one
+    column block: a first step through the blended metric (its loss is NaN) followed by identity
+    steps, whose losses come from the block's first loss and gradient; they equal the two-pass run's."""
+    import math
+    torch = _torch()
+    L = synth.make_module("llama3.1_8b_layer", "q", m=128, n=256, T=4096, seed=18)
+    r = np.random.default_rng(19)
+    Wn = (r.standard_normal((96, 128)) * 0.05).astype(np.float32)
+    Pd = torch.from_numpy(oracle.pullback_metric(Wn).astype(np.float32)).cuda()
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    m, n, T = L.shape
+    _banner("increment: alpha changes within a block")
+    Hacc = torch.zeros((n, n), dtype=torch.float64, device="cuda")
+    rq.hessian_accum(ctx, Xh, s, Hacc)
+    U = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    dead = torch.empty((n,), dtype=torch.uint8, device="cuda")
+    rq.chol_inverse(ctx, Hacc, T, 0.01, U, None, dead)
+    qp = rq.qparams()
+    out = {}
+    for inc in (1, 0):
+        st = rq.BgdState(ctx, W0, X, Xh, s, None, Pd, params=rq.bgd_params(steps=4, lr=L.lr, resid_increment=inc))
+        W = W0.double()
+        codes = torch.empty((m, n), dtype=torch.uint8, device="cuda")
+        scales = torch.empty((m, n // 128), dtype=torch.float32, device="cuda")
+        zeros = torch.empty((m, n // 128), dtype=torch.uint8, device="cuda")
+        rq.quantize_block(ctx, W, 0, 128, U, dead, qp, codes, scales, zeros, st)
+        losses = []
+        for alpha in (0.5, 1.0, 1.0, 1.0):
+            lo = torch.empty((1,), dtype=torch.float64, device="cuda")
+            rq.bgd_step(ctx, st, W, 128, alpha, lo)
+            losses.append(lo.item())
+        torch.cuda.synchronize()
+        st.close()
+        out[inc] = losses
+    print(out, flush=True)
+    assert math.isnan(out[1][0]) and math.isnan(out[0][0])
+    np.testing.assert_allclose(out[1][1:], out[0][1:], rtol=1e-6)
