@@ -233,7 +233,9 @@ int realq_chol_inverse(realq_ctx* ctx, const double* H_acc, int64_t n, int64_t T
  *   P    : consumer's pulled-back metric [m,m] float32 or NULL, blended with M by
  *          the sliding window (Eq. slide_window).
  * The state assumes the caller's working weights start equal to W0 and are only
- * changed through realq_quantize_block / realq_bgd_step afterwards. */
+ * changed through realq_quantize_block / realq_bgd_step afterwards.  When the other
+ * conditions of resid_increment hold, creation synchronises the stream once to read
+ * rms(W0). */
 int realq_bgd_state_create(realq_ctx* ctx, realq_bgd_state** out, const float* W0 /*[m,n]*/,
                            const uint16_t* X /*[T,n]*/, const uint16_t* Xhat /*[T,n]*/,
                            const float* s /*[T]|NULL*/, const float* M /*[m,m]|NULL*/,
@@ -285,9 +287,9 @@ int realq_bgd_lock_block(realq_ctx* ctx, realq_bgd_state* st, int64_t c0, int64_
  * loss_out (device float64 scalar, may be NULL) receives L before the update; it
  * is computed for M_a = identity only and set to NaN otherwise.  c1 == n is a no-op.
  * With increments (realq_bgd_params.resid_increment and its gate), the state keeps the
- * loss and gradient of the first step at a given c1 and later steps at the same c1 start
- * from them; realq_quantize_block(_rows) and realq_bgd_lock_block restart that, as does a
- * step at another c1. */
+ * loss and gradient of the first step at a given c1 and up to steps - 1 later steps at the
+ * same c1 start from them; realq_quantize_block(_rows) and realq_bgd_lock_block restart
+ * that, as does a step at another c1 or the steps-th step after a first one. */
 int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W /*[m,n]*/, int64_t c1, float alpha,
                    double* loss_out);
 

@@ -107,6 +107,7 @@ struct realq_bgd_state {
     uint16_t* Dinc = nullptr;
     int64_t inc_c1 = -1;
     bool inc_ready = false;
+    int64_t inc_taken = 0;  // later steps taken since the block's first (at most steps - 1)
     // Gram form
     bool gram = false;
     uint16_t* Ghi = nullptr;
@@ -866,7 +867,10 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
     // Q = bf16(Dacc) Xhat_J^T, its gradient as G0 + bf16(Q o s) Xhat_J and its loss as
     // L0 + <G0, bf16(Dacc)> / T + sum s Q^2 / 2T; the block's first step writes L0 and G0 and
     // restarts Dacc
-    const bool inc_step = st->inc && !st->gram && st->inc_c1 == c1 && st->inc_ready;
+    // (a caller taking more than `steps` steps at one c1 gets a fresh first step every `steps`
+    // steps, so the displacement bound of the gate holds)
+    const bool inc_step = st->inc && !st->gram && st->inc_c1 == c1 && st->inc_ready &&
+                          st->inc_taken < (int64_t)st->prm.steps - 1;
     const bool inc_first = st->inc && !st->gram && !inc_step;
     const int64_t Tn = pl.Tn;
     const int64_t nchunks = (int64_t)pl.chunks.size();
@@ -980,6 +984,7 @@ int realq_bgd_step(realq_ctx* ctx, realq_bgd_state* st, double* W, int64_t c1, f
         a.g0_mode = (nchunks > 1 || dense) ? 0 : (inc_first ? 1 : 2);
         st->inc_c1 = c1;
         st->inc_ready = true;
+        st->inc_taken = inc_first ? 0 : st->inc_taken + 1;
     }
     if (!dense && nchunks == 1 && !st->gram) {
         Timed tm(ctx, "adam");

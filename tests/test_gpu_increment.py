@@ -209,3 +209,41 @@ def test_increment_loss_when_alpha_changes_within_a_block(rq, ctx):
     print(out, flush=True)
     assert math.isnan(out[1][0]) and math.isnan(out[0][0])
     np.testing.assert_allclose(out[1][1:], out[0][1:], rtol=1e-6)
+
+
+def test_increment_restarts_after_steps_minus_one_later_steps(rq, ctx):
+    """A caller may take more Block-GD steps at one c1 than the parameters' `steps`: the state takes a
+    fresh first step (two passes) after steps - 1 increments, so the displacement bound holds; the
+    losses of 10 steps with steps = 4 equal the two-pass run's."""
+    torch = _torch()
+    L = synth.make_module("llama3.1_8b_layer", "gate", m=128, n=256, T=4096, seed=20)
+    W0, X, Xh, s, _ = P.to_device(L, torch)
+    m, n, T = L.shape
+    _banner("increment: more steps than `steps` at one c1")
+    Hacc = torch.zeros((n, n), dtype=torch.float64, device="cuda")
+    rq.hessian_accum(ctx, Xh, s, Hacc)
+    U = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    dead = torch.empty((n,), dtype=torch.uint8, device="cuda")
+    rq.chol_inverse(ctx, Hacc, T, 0.01, U, None, dead)
+    out = {}
+    for inc in (1, 0):
+        ctx.set_timing(True)
+        ctx.reset_timing()
+        st = rq.BgdState(ctx, W0, X, Xh, s, params=rq.bgd_params(steps=4, lr=L.lr, resid_increment=inc))
+        W = W0.double()
+        codes = torch.empty((m, n), dtype=torch.uint8, device="cuda")
+        scales = torch.empty((m, n // 128), dtype=torch.float32, device="cuda")
+        zeros = torch.empty((m, n // 128), dtype=torch.uint8, device="cuda")
+        rq.quantize_block(ctx, W, 0, 128, U, dead, rq.qparams(), codes, scales, zeros, st)
+        losses = []
+        for _ in range(10):
+            lo = torch.empty((1,), dtype=torch.float64, device="cuda")
+            rq.bgd_step(ctx, st, W, 128, 1.0, lo)
+            losses.append(lo.item())
+        torch.cuda.synchronize()
+        st.close()
+        out[inc] = (losses, ctx.kernel_time("resid")[0], ctx.kernel_time("resid_inc")[0])
+        ctx.set_timing(False)
+    print(out, flush=True)
+    assert out[1][1:] == (3, 7) and out[0][1:] == (10, 0)     # first steps at 0, 4, 8
+    np.testing.assert_allclose(out[1][0], out[0][0], rtol=1e-6)
