@@ -506,10 +506,10 @@ __global__ __launch_bounds__(256) void inc_dot_kernel(const float* __restrict__ 
                                                       int64_t ldd, int64_t m, int64_t w, double* __restrict__ dots) {
     __shared__ double red[256];
     double acc = 0.0;
-    const int64_t total = m * w;
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)INC_DOT_BLOCKS * 256) {
-        const int64_t i = e / w, j = e - i * w;
-        acc += (double)G0[e] * (double)bf2f(Dinc[i * ldd + j]);
+    for (int64_t i = blockIdx.x; i < m; i += INC_DOT_BLOCKS) {  // rows, coalesced along each
+        const float* g = G0 + i * w;
+        const uint16_t* d = Dinc + i * ldd;
+        for (int64_t j = threadIdx.x; j < w; j += 256) acc += (double)g[j] * (double)bf2f(d[j]);
     }
     red[threadIdx.x] = acc;
     __syncthreads();
