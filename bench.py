@@ -600,6 +600,9 @@ def main():
     ap.add_argument("--form", default="tokens", choices=("tokens", "gram"),
                     help="BGD evaluation: residual/gradient GEMMs over all tokens every step (the step of the "
                          "headline metric), or the same loss and gradient through the calibration Gram matrices")
+    ap.add_argument("--no-increment", action="store_true",
+                    help="run every Block-GD step with both passes (resid_increment = 0): the sweep without "
+                         "the increments of a column block's later steps")
     ap.add_argument("--no-gram-line", action="store_true",
                     help="with --form tokens, skip the extra untimed Gram-form sweep reported under gram_form")
     ap.add_argument("--no-stage0", action="store_true",
@@ -658,7 +661,7 @@ def main():
     qp = rq.qparams()
     form = rq.BGD_GRAM if args.form == "gram" else rq.BGD_TOKENS
     tok_chunk = TOKEN_CHUNK.get(args.workload, 0) if args.tok_chunk is None else args.tok_chunk
-    bgd = rq.bgd_params(steps=K, lr=lr, form=form, tok_chunk=tok_chunk)
+    bgd = rq.bgd_params(steps=K, lr=lr, form=form, tok_chunk=tok_chunk, resid_increment=0 if args.no_increment else 1)
     if args.only == "stage0":
         ctx.set_timing(True)
         print(json.dumps({"stage0": stage0(torch, rq, ctx, W0, X, Xh, s, qp, rq.bgd_params(steps=K, lr=lr), m, n,
