@@ -96,6 +96,8 @@ namespace {
 constexpr int AT = 32;
 constexpr int TSTR = AT + 8;  // bf16 per row of a staged 32 x 32 tile (80 bytes: 16-byte aligned rows)
 typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int TSTR32 = AT + 4;  // uint32 per row of a staged 32 x 32 tile of hi | lo pairs (144 bytes)
 
 __device__ __forceinline__ bf16x8 ld8(const uint16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
@@ -591,7 +593,7 @@ __global__ __launch_bounds__(256) void attn_ds_lds_kernel(const uint16_t* __rest
     static_assert(TDMA >= 1, "head width");
     __shared__ __attribute__((aligned(16))) uint16_t sKV[2][TBYTES];   // [buf][key tile | value tile]
     __shared__ __attribute__((aligned(16))) uint16_t sQ[4][AT * HD];    // each wave's query rows (swizzled)
-    __shared__ __attribute__((aligned(16))) uint16_t stage[4][AT][TSTR];
+    __shared__ __attribute__((aligned(16))) uint32_t stage[4][AT][TSTR32];
     __shared__ double sLD[4][2][AT];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wv = __builtin_amdgcn_readfirstlane(wave);
@@ -642,23 +644,34 @@ __global__ __launch_bounds__(256) void attn_ds_lds_kernel(const uint16_t* __rest
         }
     }
     const double scale = 1.0 / sqrt((double)HD);
-    uint16_t(*tb)[TSTR] = stage[wave];
+    uint32_t(*tb)[TSTR32] = stage[wave];
     const int r = lane >> 2, c8 = (lane & 3) * 8;
-    // values packed as hi | lo << 16; `lo` picks the half
-    auto flush = [&](const uint32_t (&val)[16], bool lo, bool transposed, uint16_t* dst, int64_t row0, int64_t col0) {
+    // values packed as hi | lo << 16, staged whole and split into the hi and lo arrays on the way out
+    auto flush = [&](const uint32_t (&val)[16], bool transposed, uint16_t* dst_hi, uint16_t* dst_lo, int64_t row0,
+                     int64_t col0) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
             const int a = acc_row(e, lane), b = lane & 31;
-            const uint16_t x = (uint16_t)(lo ? (val[e] >> 16) : (val[e] & 0xffffu));
-            if (transposed) tb[b][a] = x;
-            else tb[a][b] = x;
+            if (transposed) tb[b][a] = val[e];
+            else tb[a][b] = val[e];
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int rr = r + 16 * half;
-            *reinterpret_cast<u16x8*>(dst + (sh * L + row0 + rr) * L + col0 + c8) =
-                *reinterpret_cast<const u16x8*>(&tb[rr][c8]);
+            const u32x4 v0 = *reinterpret_cast<const u32x4*>(&tb[rr][c8]);
+            const u32x4 v1 = *reinterpret_cast<const u32x4*>(&tb[rr][c8 + 4]);
+            u16x8 h, l;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                h[u] = (uint16_t)(v0[u] & 0xffffu);
+                l[u] = (uint16_t)(v0[u] >> 16);
+                h[u + 4] = (uint16_t)(v1[u] & 0xffffu);
+                l[u + 4] = (uint16_t)(v1[u] >> 16);
+            }
+            const int64_t o = (sh * L + row0 + rr) * L + col0 + c8;
+            *reinterpret_cast<u16x8*>(dst_hi + o) = h;
+            *reinterpret_cast<u16x8*>(dst_lo + o) = l;
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     };
@@ -697,12 +710,9 @@ __global__ __launch_bounds__(256) void attn_ds_lds_kernel(const uint16_t* __rest
             dsv[e] = (uint32_t)a0 | ((uint32_t)a1 << 16);
             pv2[e] = (uint32_t)b0 | ((uint32_t)b1 << 16);
         }
-        flush(dsv, false, false, dSh, it * AT, jt * AT);
-        flush(dsv, true, false, dSl, it * AT, jt * AT);
-        flush(dsv, false, true, dSth, jt * AT, it * AT);
-        flush(dsv, true, true, dStl, jt * AT, it * AT);
-        flush(pv2, false, true, Pth, jt * AT, it * AT);
-        flush(pv2, true, true, Ptl, jt * AT, it * AT);
+        flush(dsv, false, dSh, dSl, it * AT, jt * AT);
+        flush(dsv, true, dSth, dStl, jt * AT, it * AT);
+        flush(pv2, true, Pth, Ptl, jt * AT, it * AT);
     }
 }
 
