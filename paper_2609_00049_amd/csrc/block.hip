@@ -14,6 +14,7 @@ namespace realq {
 
 namespace {
 constexpr int TB = 256;
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 inline unsigned grid_for(int64_t count) {
     int64_t b = (count + TB * 4 - 1) / (TB * 4);
     if (b < 1) b = 1;
@@ -180,6 +181,64 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const float* __restrict
         if (t < T && i < f) split_bf16(tile[tx][cc], hi[i * ldo + t], lo[i * ldo + t]);
     }
 }
+// Both row-major SwiGLU backward outputs of one dz in one pass (the gate's to hi0/lo0, the up
+// projection's to hi1/lo1), four consecutive columns per thread when rows allow 16-byte loads;
+// per element the arithmetic of swiglu_bwd_kernel, so both outputs are bitwise the same.
+__device__ __forceinline__ void swiglu_bwd_pair_elem(float d, float av, float bv, uint16_t& h0, uint16_t& l0,
+                                                     uint16_t& h1, uint16_t& l1) {
+    const double x = (double)av;
+    const double sg = 1.0 / (1.0 + exp(-x));
+    const double w0 = (double)bv * sg * (1.0 + x * (1.0 - sg));
+    const double w1 = x * sg;
+    split_bf16((float)((double)d * w0), h0, l0);
+    split_bf16((float)((double)d * w1), h1, l1);
+}
+__global__ __launch_bounds__(256) void swiglu_bwd_pair_kernel(const float* __restrict__ dz, const float* __restrict__ a,
+                                                              const float* __restrict__ b, int64_t T, int64_t f,
+                                                              uint16_t* __restrict__ hi0, uint16_t* __restrict__ lo0,
+                                                              uint16_t* __restrict__ hi1, uint16_t* __restrict__ lo1,
+                                                              int64_t ldo, int vec) {
+    const int64_t fq = vec ? f / 4 : f;
+    const int64_t n = T * fq;
+    for (int64_t q = (int64_t)blockIdx.x * TB + threadIdx.x; q < n; q += (int64_t)gridDim.x * TB) {
+        const int64_t t = q / fq, c = q - t * fq;
+        if (vec) {
+            const int64_t e = t * f + 4 * c, o = t * ldo + 4 * c;
+            const f32x4 xd = *reinterpret_cast<const f32x4*>(dz + e);
+            const f32x4 xa = *reinterpret_cast<const f32x4*>(a + e);
+            const f32x4 xb = *reinterpret_cast<const f32x4*>(b + e);
+            u16x4 h0, l0, h1, l1;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                uint16_t a0, a1, b0, b1;
+                swiglu_bwd_pair_elem(xd[u], xa[u], xb[u], a0, a1, b0, b1);
+                h0[u] = a0;
+                l0[u] = a1;
+                h1[u] = b0;
+                l1[u] = b1;
+            }
+            *reinterpret_cast<u16x4*>(hi0 + o) = h0;
+            *reinterpret_cast<u16x4*>(lo0 + o) = l0;
+            *reinterpret_cast<u16x4*>(hi1 + o) = h1;
+            *reinterpret_cast<u16x4*>(lo1 + o) = l1;
+        } else {
+            const int64_t e = t * f + c, o = t * ldo + c;
+            swiglu_bwd_pair_elem(dz[e], a[e], b[e], hi0[o], lo0[o], hi1[o], lo1[o]);
+        }
+    }
+}
+hipError_t swiglu_bwd_pair(const float* dz, const float* a, const float* b, int64_t T, int64_t f, uint16_t* hi0,
+                           uint16_t* lo0, uint16_t* hi1, uint16_t* lo1, int64_t ldo, hipStream_t st) {
+    if (T <= 0 || f <= 0) return hipSuccess;
+    auto a16 = [](const void* p) { return ((uintptr_t)p & 15u) == 0; };
+    auto a8 = [](const void* p) { return ((uintptr_t)p & 7u) == 0; };
+    const int vec = f % 4 == 0 && ldo % 4 == 0 && a16(dz) && a16(a) && a16(b) && a8(hi0) && a8(lo0) && a8(hi1) && a8(lo1);
+    const int64_t n = T * (vec ? f / 4 : f);
+    hipLaunchKernelGGL(swiglu_bwd_pair_kernel, dim3(grid_for(n)), dim3(TB), 0, st, dz, a, b, T, f, hi0, lo0, hi1, lo1,
+                       ldo, vec);
+    return hipGetLastError();
+}
+
 hipError_t swiglu_bwd(const float* dz, const float* a, const float* b, int which, int64_t T, int64_t f,
                       int transposed, uint16_t* hi, uint16_t* lo, int64_t ldo, hipStream_t st) {
     if (T <= 0 || f <= 0) return hipSuccess;

@@ -334,8 +334,7 @@ extern "C" int realq_mlp_block_sweep(realq_ctx* ctx, const realq_mlp_desc* D, re
             RQ_HIP(ctx, realq::dot_f32(dy2, g2, Tb * d, 0.5 * (1.0 - alpha), parts + npart, s));
             RQ_HIP(ctx, realq::scale_split(g2, 1.f, nullptr, sg2.hi, sg2.lo, Tb * d, s));
             if ((rc = prod3(ctx, sg2, Tb, d, w2.dT, f, 1.f, dz2))) return rc;  // dz2 = g2 Wd2
-            RQ_HIP(ctx, realq::swiglu_bwd(dz2, fn.a, fn.b, 0, Tb, f, 0, sda2.hi, sda2.lo, f, s));
-            RQ_HIP(ctx, realq::swiglu_bwd(dz2, fn.a, fn.b, 1, Tb, f, 0, sdb2.hi, sdb2.lo, f, s));
+            RQ_HIP(ctx, realq::swiglu_bwd_pair(dz2, fn.a, fn.b, Tb, f, sda2.hi, sda2.lo, sdb2.hi, sdb2.lo, f, s));
             if ((rc = prod3(ctx, sda2, Tb, f, w2.gT, d, 1.f, du2))) return rc;  // du2 = da2 Wg2 + db2 Wu2
             realq::GemmArgs a1{sdb2.hi, sdb2.lo, f, w2.uT.hi, f, Tb, d, f, 1};
             RQ_HIP(ctx, realq::gemm_acc_f32(a1, du2, d, 1.f, s));
@@ -632,8 +631,7 @@ int back_to_x2(realq_ctx* ctx, const DecW& w, const DecDims& D, const DecF& F, c
     const int64_t T = D.T, d = D.d, f = D.f;
     RQ_HIP(ctx, realq::scale_split(g, 1.f, nullptr, Wk.sg.hi, Wk.sg.lo, T * d, s));
     if ((rc = prod3(ctx, Wk.sg, T, d, w.mlp.dT, f, 1.f, Wk.dz))) return rc;
-    RQ_HIP(ctx, realq::swiglu_bwd(Wk.dz, F.mlp.a, F.mlp.b, 0, T, f, 0, Wk.sda.hi, Wk.sda.lo, f, s));
-    RQ_HIP(ctx, realq::swiglu_bwd(Wk.dz, F.mlp.a, F.mlp.b, 1, T, f, 0, Wk.sdb.hi, Wk.sdb.lo, f, s));
+    RQ_HIP(ctx, realq::swiglu_bwd_pair(Wk.dz, F.mlp.a, F.mlp.b, T, f, Wk.sda.hi, Wk.sda.lo, Wk.sdb.hi, Wk.sdb.lo, f, s));
     if ((rc = prod3(ctx, Wk.sda, T, f, w.mlp.gT, d, 1.f, Wk.du)) || (rc = prod3_acc(ctx, Wk.sdb, T, f, w.mlp.uT, d, Wk.du)))
         return rc;
     RQ_HIP(ctx, realq::rmsnorm_bwd_blend(F.x2, g, Wk.du, w.mlp.gamma, D.eps, 0.0, T, d, Wk.dx2, s));

@@ -205,6 +205,9 @@ int64_t dot_f32_partials();
 // transposed ([f][ldo]) or row-major ([T][ldo])
 hipError_t swiglu_bwd(const float* dz, const float* a, const float* b, int which, int64_t T, int64_t f,
                       int transposed, uint16_t* hi, uint16_t* lo, int64_t ldo, hipStream_t st);
+// Both row-major outputs (gate: hi0/lo0, up: hi1/lo1) of swiglu_bwd in one pass over dz, a, b.
+hipError_t swiglu_bwd_pair(const float* dz, const float* a, const float* b, int64_t T, int64_t f, uint16_t* hi0,
+                           uint16_t* lo0, uint16_t* hi1, uint16_t* lo1, int64_t ldo, hipStream_t st);
 // hi/lo[c * ldo + r] = split(in[r * ldi + c])
 hipError_t transpose_split_f32(const float* in, int64_t ldi, uint16_t* hi, uint16_t* lo, int64_t ldo, int64_t rows,
                                int64_t cols, hipStream_t st);
